@@ -1,0 +1,225 @@
+"""Seeded synthetic workloads for the MTP + Viterbi decode path.
+
+This module only *generates inputs*: model shapes, seeded weights, the
+transition table Q and prompts.  It holds none of the method's arithmetic
+(no forward pass, no scoring, no selection), so both the HIP path and the
+CPU oracle can consume its arrays without sharing any computation.
+
+Shapes follow a VALL-E style AR decoder: a decoder-only Transformer over the
+concatenation [phonemes; acoustic prompt; generated codec tokens] (paper
+Sec. 3.1, Eq. 1) with n parallel next-token heads on the last hidden state
+(Sec. 3.2).  The codec vocabulary is 1024 first-quantizer codes plus EOS.
+
+Seeding: every tensor is drawn from numpy's PCG64 seeded with
+SeedSequence([seed, tensor_index]), N(0, 0.02) in float32.  For bf16 models
+the float32 draw is rounded once to bf16 (round-to-nearest-even); both sides
+use exactly those values.
+"""
+from __future__ import annotations
+
+import dataclasses
+from dataclasses import dataclass, field
+from typing import Dict, List, Optional, Tuple
+
+import numpy as np
+
+VOCAB = 1025          # 1024 first-quantizer codec codes + EOS
+EOS_ID = 1024
+N_PHONE = 512         # phoneme inventory (ids 0..511)
+HEAD_DIM = 64
+MAX_POS = 4096        # learned absolute position table length
+
+DTYPE_F32 = "f32"
+DTYPE_BF16 = "bf16"
+
+
+@dataclass(frozen=True)
+class ModelShape:
+    """Decoder shape.  `k_heads` is the number of prediction heads loaded."""
+    n_layers: int
+    d_model: int
+    n_heads: int
+    d_ff: int
+    k_heads: int
+    dtype: str
+    vocab: int = VOCAB
+    eos_id: int = EOS_ID
+    n_phone: int = N_PHONE
+    max_pos: int = MAX_POS
+
+    @property
+    def head_dim(self) -> int:
+        return self.d_model // self.n_heads
+
+
+@dataclass(frozen=True)
+class Workload:
+    """One benchmark / parity configuration."""
+    name: str
+    model: ModelShape
+    K: int                       # heads used per decode step (n in the paper)
+    top_k: int                   # candidates kept per head
+    batch: int
+    phon_len: Tuple[int, int]    # inclusive range; (a, a) means fixed
+    ac_len: Tuple[int, int]
+    max_new: int                 # generation budget per sequence
+    eos_min: int                 # EOS masked while generated index < eos_min
+    description: str = ""
+
+    @property
+    def max_prompt(self) -> int:
+        return self.phon_len[1] + self.ac_len[1]
+
+    @property
+    def max_seq(self) -> int:
+        return self.max_prompt + self.max_new
+
+
+_TINY = ModelShape(n_layers=2, d_model=256, n_heads=4, d_ff=1024, k_heads=2, dtype=DTYPE_F32)
+_VALLE = ModelShape(n_layers=12, d_model=1024, n_heads=16, d_ff=4096, k_heads=8, dtype=DTYPE_BF16)
+_LONG = ModelShape(n_layers=24, d_model=1536, n_heads=24, d_ff=6144, k_heads=4, dtype=DTYPE_BF16)
+
+WORKLOADS: Dict[str, Workload] = {
+    "tiny": Workload(
+        "tiny", _TINY, K=2, top_k=3, batch=1, phon_len=(0, 0), ac_len=(32, 32),
+        max_new=64, eos_min=64,
+        description="2L d256 H4 F1024 fp32, K=2 top_k=3, 32-token prompt, 64 tokens"),
+    "valle_k4": Workload(
+        "valle_k4", _VALLE, K=4, top_k=4, batch=1, phon_len=(100, 100), ac_len=(225, 225),
+        max_new=750, eos_min=600,
+        description="12L d1024 H16 F4096 bf16, K=4 top_k=4, batch 1, 100 phon + 225 acoustic, <=750 tokens, EOS from 600"),
+    "valle_k8": Workload(
+        "valle_k8", _VALLE, K=8, top_k=8, batch=1, phon_len=(100, 100), ac_len=(225, 225),
+        max_new=750, eos_min=750,
+        description="12L d1024 H16 F4096 bf16, K=8 top_k=8, batch 1, 750 tokens"),
+    "valle_b32": Workload(
+        "valle_b32", _VALLE, K=4, top_k=4, batch=32, phon_len=(50, 150), ac_len=(150, 300),
+        max_new=750, eos_min=750,
+        description="12L d1024 H16 F4096 bf16, K=4 top_k=4, batch 32 ragged prompts, 750 tokens each"),
+    "long_b8": Workload(
+        "long_b8", _LONG, K=4, top_k=4, batch=8, phon_len=(200, 200), ac_len=(450, 450),
+        max_new=3000, eos_min=3000,
+        description="24L d1536 H24 F6144 bf16, K=4 top_k=4, batch 8, 200 phon + 450 acoustic, 3000 tokens"),
+}
+
+WEIGHT_SEED = 0
+Q_SEED = 1
+PROMPT_SEED_BASE = 100
+
+
+def bf16_round(x: np.ndarray) -> np.ndarray:
+    """Round float32 values to the nearest bfloat16 (ties to even); returns float32."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    u = x.view(np.uint32).astype(np.uint64)
+    rounded = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
+    return (rounded.astype(np.uint32) << 16).view(np.float32).reshape(x.shape)
+
+
+def bf16_bits(x: np.ndarray) -> np.ndarray:
+    """bfloat16 bit patterns (uint16) of float32 values that are already bf16-exact."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    return (x.view(np.uint32) >> 16).astype(np.uint16)
+
+
+def weight_names(m: ModelShape) -> List[Tuple[str, Tuple[int, ...]]]:
+    """Ordered (name, shape) list; the order fixes each tensor's seed index."""
+    d, f, v = m.d_model, m.d_ff, m.vocab
+    out: List[Tuple[str, Tuple[int, ...]]] = [
+        ("emb_phone", (m.n_phone, d)),
+        ("emb_ac", (v, d)),
+        ("pos", (m.max_pos, d)),
+    ]
+    for l in range(m.n_layers):
+        out += [
+            (f"l{l}.ln1_g", (d,)), (f"l{l}.ln1_b", (d,)),
+            (f"l{l}.w_qkv", (3 * d, d)), (f"l{l}.b_qkv", (3 * d,)),
+            (f"l{l}.w_o", (d, d)), (f"l{l}.b_o", (d,)),
+            (f"l{l}.ln2_g", (d,)), (f"l{l}.ln2_b", (d,)),
+            (f"l{l}.w_1", (f, d)), (f"l{l}.b_1", (f,)),
+            (f"l{l}.w_2", (d, f)), (f"l{l}.b_2", (d,)),
+        ]
+    out += [("lnf_g", (d,)), ("lnf_b", (d,)),
+            ("w_heads", (m.k_heads, v, d)), ("b_heads", (m.k_heads, v))]
+    return out
+
+
+def make_weights(m: ModelShape, seed: int = WEIGHT_SEED) -> Dict[str, np.ndarray]:
+    """Seeded float32 weights (bf16-exact values for bf16 models).
+
+    Linear weights/biases, embeddings and the position table are N(0, 0.02).
+    LayerNorm gains are 1 + N(0, 0.02) and shifts N(0, 0.02), so that a kernel
+    that ignores either is caught by parity.
+    """
+    w: Dict[str, np.ndarray] = {}
+    for idx, (name, shape) in enumerate(weight_names(m)):
+        rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, idx])))
+        a = rng.standard_normal(size=shape, dtype=np.float32) * np.float32(0.02)
+        if name.endswith("_g"):
+            a = a + np.float32(1.0)
+        a = a.astype(np.float32)
+        if m.dtype == DTYPE_BF16:
+            a = bf16_round(a)
+        w[name] = a
+    return w
+
+
+def make_logq(v: int = VOCAB, seed: int = Q_SEED, kind: str = "synthetic",
+              alpha: float = 0.5, eos_id: Optional[int] = EOS_ID) -> np.ndarray:
+    """log of a strictly positive row-stochastic transition table Q [v, v] (float32).
+
+    Row = previous token, column = next token.  The LibriTTS-estimated table is
+    not available, so values are invented:
+      uniform   -- every entry 1/v;
+      sticky    -- alpha * I + (1 - alpha) / v;
+      synthetic -- heavy-tailed per-row draws (Gamma(0.3)) with a boosted
+                   diagonal, since consecutive speech tokens are often similar;
+                   the EOS column gets the row's mean mass.
+    Built in float64, then log and rounded to float32.
+    """
+    if kind == "uniform":
+        q = np.full((v, v), 1.0 / v)
+    elif kind == "sticky":
+        q = np.full((v, v), (1.0 - alpha) / v) + alpha * np.eye(v)
+    elif kind == "synthetic":
+        rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, 7])))
+        raw = rng.gamma(0.3, size=(v, v)) + 1e-6
+        diag = np.arange(v)
+        raw[diag, diag] += 0.15 * raw.sum(axis=1)
+        if eos_id is not None:
+            raw[:, eos_id] = raw.mean(axis=1)
+        q = raw / raw.sum(axis=1, keepdims=True)
+    else:
+        raise ValueError(f"unknown Q kind {kind!r}")
+    return np.log(q).astype(np.float32)
+
+
+@dataclass
+class Prompts:
+    phon: List[np.ndarray]   # per sequence int32 phoneme ids
+    ac: List[np.ndarray]     # per sequence int32 acoustic-prompt codec ids
+
+    @property
+    def batch(self) -> int:
+        return len(self.phon)
+
+
+def make_prompts(wl: Workload, seed_base: int = PROMPT_SEED_BASE, batch: Optional[int] = None) -> Prompts:
+    """Per-sequence prompts: sequence b uses seed seed_base + b.
+
+    Lengths are uniform over the workload's inclusive ranges; phoneme ids are
+    uniform over 0..511 and acoustic ids uniform over 0..1023.
+    """
+    B = wl.batch if batch is None else batch
+    phon, ac = [], []
+    for b in range(B):
+        rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed_base + b])))
+        lp = int(rng.integers(wl.phon_len[0], wl.phon_len[1] + 1))
+        la = int(rng.integers(wl.ac_len[0], wl.ac_len[1] + 1))
+        phon.append(rng.integers(0, N_PHONE, size=lp).astype(np.int32))
+        ac.append(rng.integers(0, VOCAB - 1, size=la).astype(np.int32))
+    return Prompts(phon, ac)
+
+
+def random_logits(rng: np.random.Generator, shape, scale: float = 0.64) -> np.ndarray:
+    """iid N(0, scale^2) float32 logits, the spread of the VALL-E-shaped heads."""
+    return (rng.standard_normal(size=shape) * scale).astype(np.float32)
