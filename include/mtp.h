@@ -1,0 +1,207 @@
+/*
+ * mtp.h -- C ABI of the MI355X (gfx950) decode path for multi-token
+ * prediction with Viterbi-based speculative decoding.
+ *
+ * Paper: "Accelerating Codec-based Speech Synthesis with Multi-Token
+ * Prediction and Speculative Decoding" (arXiv 2410.13839).
+ *
+ * The problem (Sec. 3.1, Eq. 1): given a phoneme prompt p and an acoustic
+ * prompt (first-quantizer codec tokens), an autoregressive decoder-only
+ * Transformer generates the first-quantizer token sequence.  Sec. 3.2: n
+ * heads on the last hidden state predict the next n tokens in one step, and
+ * the number of heads used can be chosen per call without retraining
+ * (Fig. 1 caption).  Sec. 3.3 / Fig. 2: the n emitted tokens are the
+ * best-scoring path, under a token-transition table Q and each head's
+ * probabilities S_t, through each head's top_k candidates.
+ *
+ * One decode step = trunk forward of the pending tokens over the paged KV
+ * cache -> final LayerNorm -> K head projections -> EOS mask + per-head
+ * top_k -> Viterbi lattice -> accept.  All of it runs in HIP kernels on the
+ * caller's stream.
+ *
+ * Conventions
+ *  - Every call returns 0 on success or a negative MTP_E* code; no C++
+ *    exception crosses this boundary.  mtp_last_error() gives the text of
+ *    the last failure on a context.
+ *  - The library allocates NO device memory.  The caller allocates the
+ *    four device buffers (sizes from mtp_query_sizes) and owns them; they
+ *    must outlive the context.  The context owns only host bookkeeping.
+ *  - All work is ordered on the one HIP stream given to mtp_create.  A
+ *    context is not thread-safe.
+ *  - Pointers documented "host" are plain host memory; "device" pointers
+ *    are device memory on the current HIP device.
+ */
+#ifndef MTP_H
+#define MTP_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- error codes -------------------------------------------------------- */
+#define MTP_OK       0
+#define MTP_EINVAL  -1   /* bad argument, shape or limit                        */
+#define MTP_ENOMEM  -2   /* KV page pool or workspace too small for the request */
+#define MTP_ESTATE  -3   /* call out of order (e.g. decode before prefill)      */
+#define MTP_EHIP    -4   /* a HIP runtime error; text in mtp_last_error         */
+
+/* ---- element types ------------------------------------------------------ */
+#define MTP_DTYPE_F32   0   /* fp32 weights, activations and KV cache          */
+#define MTP_DTYPE_BF16  1   /* bf16 weights / GEMM inputs / KV, fp32 accumulate */
+
+/* ---- flags -------------------------------------------------------------- */
+#define MTP_FLAG_NO_GRAPH  1   /* launch the decode step eagerly (no hipGraph replay) */
+
+/* Model and capacity description.  Head dimension is fixed at 64
+ * (d_model / n_heads == 64). */
+typedef struct mtp_config {
+    int32_t n_layers;     /* Transformer blocks                                  */
+    int32_t d_model;      /* hidden size, multiple of 64                          */
+    int32_t n_heads;      /* attention heads, d_model / 64                        */
+    int32_t d_ff;         /* FFN hidden size, multiple of 64                      */
+    int32_t vocab;        /* codec vocabulary incl. EOS (1025)                    */
+    int32_t eos_id;       /* EOS token id (1024)                                  */
+    int32_t n_phone;      /* phoneme inventory size (512)                         */
+    int32_t max_pos;      /* rows of the learned position table                   */
+    int32_t k_heads;      /* prediction heads loaded, 1..8                        */
+    int32_t topk_max;     /* largest top_k a decode step may ask for, 1..32       */
+    int32_t max_batch;    /* sequences per prefill                                */
+    int32_t max_prompt;   /* phonemes + acoustic tokens per sequence              */
+    int32_t max_new;      /* generation budget per sequence (tokens)              */
+    int32_t eos_min;      /* EOS masked while the generated index is < eos_min    */
+    int32_t page_size;    /* tokens per KV page (power of two, 8..128)            */
+    int32_t num_pages;    /* pages in the pool; 0 = max_batch full sequences      */
+    int32_t dtype;        /* MTP_DTYPE_*                                          */
+    int32_t flags;        /* MTP_FLAG_*                                           */
+} mtp_config;
+
+/* Byte sizes of the caller-allocated device buffers. */
+typedef struct mtp_sizes {
+    uint64_t weights_bytes;    /* packed weights, layout from mtp_weight_offset  */
+    uint64_t logq_bytes;       /* log Q, float32 [vocab][vocab]                  */
+    uint64_t kv_bytes;         /* paged KV pool                                  */
+    uint64_t workspace_bytes;  /* activations, lattice, per-sequence state       */
+} mtp_sizes;
+
+/* Device buffers (all device pointers, 256-byte aligned, caller-owned). */
+typedef struct mtp_buffers {
+    void*        weights;      /* packed weights                                  */
+    const float* logq;         /* log Q: row = previous token, column = next token */
+    void*        kv_pool;      /* KV pages; contents need no initialisation       */
+    void*        workspace;    /* scratch + state; needs no initialisation        */
+} mtp_buffers;
+
+/* Weight tensors in packing order.  Matrices (_W_, tables) are stored in the
+ * model dtype, row-major [out][in] for Linear weights; vectors (biases,
+ * LayerNorm gain/shift) are always float32.  Per-layer tensors repeat for
+ * layer = 0 .. n_layers-1 in the order MTP_T_LN1_G .. MTP_T_B_2. */
+enum mtp_tensor {
+    MTP_T_EMB_PHONE = 0,  /* [n_phone][d]                  */
+    MTP_T_EMB_AC,         /* [vocab][d]                    */
+    MTP_T_POS,            /* [max_pos][d]                  */
+    MTP_T_LN1_G,          /* [d]   (per layer)             */
+    MTP_T_LN1_B,          /* [d]                           */
+    MTP_T_W_QKV,          /* [3d][d], rows q | k | v       */
+    MTP_T_B_QKV,          /* [3d]                          */
+    MTP_T_W_O,            /* [d][d]                        */
+    MTP_T_B_O,            /* [d]                           */
+    MTP_T_LN2_G,          /* [d]                           */
+    MTP_T_LN2_B,          /* [d]                           */
+    MTP_T_W_1,            /* [d_ff][d]                     */
+    MTP_T_B_1,            /* [d_ff]                        */
+    MTP_T_W_2,            /* [d][d_ff]                     */
+    MTP_T_B_2,            /* [d]   (last per-layer tensor) */
+    MTP_T_LNF_G,          /* [d]                           */
+    MTP_T_LNF_B,          /* [d]                           */
+    MTP_T_W_HEADS,        /* [k_heads][vocab][d]           */
+    MTP_T_B_HEADS,        /* [k_heads][vocab]              */
+    MTP_T_COUNT
+};
+
+typedef struct mtp_ctx mtp_ctx;
+
+/* Fills *out with the buffer sizes a config needs.  Returns MTP_EINVAL for an
+ * unsupported config (text via mtp_strerror only; there is no context). */
+int mtp_query_sizes(const mtp_config* cfg, mtp_sizes* out);
+
+/* Byte offset (from the start of the weights buffer) and element count of
+ * one tensor; `layer` is ignored for non-layer tensors.  Every tensor starts
+ * on a 256-byte boundary. */
+int mtp_weight_offset(const mtp_config* cfg, int tensor, int layer,
+                      uint64_t* offset_bytes, uint64_t* numel);
+
+/* Creates a context over caller-owned device buffers.  `hip_stream` is a
+ * hipStream_t (NULL = the null stream).  No device memory is allocated;
+ * the KV pool and workspace are not read before prefill writes them. */
+int mtp_create(const mtp_config* cfg, const mtp_buffers* bufs, void* hip_stream,
+               mtp_ctx** out);
+
+/* Prefill (Sec. 3.1: the AR module reads [phonemes; acoustic prompt] as one
+ * sequence).  Host arrays: phon / ac are the B sequences' ids concatenated
+ * (phon ids < n_phone, ac ids < vocab - 1), with per-sequence lengths
+ * phon_len[B] and ac_len[B]; phon_len + ac_len must be in 1..max_prompt.
+ * Resets all sequence state, reserves each sequence's KV pages for
+ * prompt + max_new tokens (MTP_ENOMEM if the pool is too small), runs the
+ * trunk over the prompts and keeps each last hidden state as the source of
+ * the first decode step.  Returns after the work is enqueued and the host
+ * inputs have been consumed. */
+int mtp_prefill(mtp_ctx* ctx, int B, const int32_t* phon, const int32_t* phon_len,
+                const int32_t* ac, const int32_t* ac_len);
+
+/* One decode step with heads 1..K (1 <= K <= k_heads) and top_k candidates
+ * per head (1 <= top_k <= topk_max).  Host outputs: out_tokens[B*K] gets
+ * each sequence's emitted tokens (entries past its count are -1) and
+ * out_count[B] the number emitted: K, fewer at the budget, up to and
+ * including the first EOS (which ends the sequence), 0 once a sequence has
+ * ended.  Blocks until the outputs are on the host. */
+int mtp_decode_step(mtp_ctx* ctx, int K, int top_k, int32_t* out_tokens, int32_t* out_count);
+
+/* Same step, outputs written to DEVICE buffers d_tokens[B*K] and d_count[B]
+ * on the context's stream, with no host synchronisation. */
+int mtp_decode_step_async(mtp_ctx* ctx, int K, int top_k, int32_t* d_tokens, int32_t* d_count);
+
+/* Parity hooks: copy the last decode step's intermediates to host memory
+ * (synchronises the stream).  logits: float32 [B][K][vocab] before the EOS
+ * mask.  cand: int32 [B][K][top_k] candidate ids (logit desc, id asc);
+ * ehat: float32 emission scores l[c] - max l; delta: float32 Viterbi
+ * scores; psi: int32 back-pointers (psi[.][0][.] = 0); slots: int32 [B][K]
+ * chosen slot per position.  Any pointer may be NULL. */
+int mtp_get_logits(mtp_ctx* ctx, float* logits);
+int mtp_get_lattice(mtp_ctx* ctx, int32_t* cand, float* ehat, float* delta,
+                    int32_t* psi, int32_t* slots);
+
+/* Per-sequence state to host (synchronises): cached tokens, pending chunk
+ * length, generated count and done flag, each int32 [B]; any may be NULL. */
+int mtp_get_seq_state(mtp_ctx* ctx, int32_t* ctx_len, int32_t* pend_len,
+                      int32_t* gen, int32_t* done);
+
+/* Every token emitted since prefill, to host (synchronises): int32
+ * [B][max_new]; entries at or past a sequence's generated count are
+ * unspecified. */
+int mtp_get_tokens(mtp_ctx* ctx, int32_t* tokens);
+
+/* Kernel timing for measurement.  While enabled, every launch of the
+ * kernel class `kclass` (MTP_KCLASS_*) in decode steps is bracketed by HIP
+ * events on the context stream and decode steps launch eagerly.
+ * mtp_profile_read synchronises and returns the summed event time (ms) and
+ * the number of launches since enabling. */
+#define MTP_KCLASS_GEMM_FFN1   1   /* LN2-output x W_1 with GELU epilogue      */
+#define MTP_KCLASS_GEMM_FFN2   2
+#define MTP_KCLASS_GEMM_QKV    3
+#define MTP_KCLASS_ATTENTION   4
+#define MTP_KCLASS_HEADS       5
+int mtp_profile(mtp_ctx* ctx, int kclass, int enable);
+int mtp_profile_read(mtp_ctx* ctx, double* total_ms, int64_t* launches);
+
+/* Drops all sequence state (the next call must be mtp_prefill). */
+int mtp_reset(mtp_ctx* ctx);
+void mtp_destroy(mtp_ctx* ctx);
+const char* mtp_last_error(const mtp_ctx* ctx);
+const char* mtp_strerror(int code);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MTP_H */

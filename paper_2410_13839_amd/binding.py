@@ -1,0 +1,291 @@
+"""ctypes binding of libmtp (include/mtp.h): argument marshalling only.
+
+Functions keep the C names.  PyTorch provides device memory (torch tensors'
+data_ptr()) and the HIP stream; every step of the decode path runs in the
+library's HIP kernels.  If libmtp.so is missing this module raises on import:
+there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Dict, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libmtp.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() (hipcc, gfx950)")
+_lib = ctypes.CDLL(LIB_PATH)
+
+MTP_OK, MTP_EINVAL, MTP_ENOMEM, MTP_ESTATE, MTP_EHIP = 0, -1, -2, -3, -4
+MTP_DTYPE_F32, MTP_DTYPE_BF16 = 0, 1
+MTP_FLAG_NO_GRAPH = 1
+(MTP_T_EMB_PHONE, MTP_T_EMB_AC, MTP_T_POS, MTP_T_LN1_G, MTP_T_LN1_B, MTP_T_W_QKV, MTP_T_B_QKV, MTP_T_W_O,
+ MTP_T_B_O, MTP_T_LN2_G, MTP_T_LN2_B, MTP_T_W_1, MTP_T_B_1, MTP_T_W_2, MTP_T_B_2, MTP_T_LNF_G, MTP_T_LNF_B,
+ MTP_T_W_HEADS, MTP_T_B_HEADS, MTP_T_COUNT) = range(20)
+MTP_KCLASS_GEMM_FFN1, MTP_KCLASS_GEMM_FFN2, MTP_KCLASS_GEMM_QKV, MTP_KCLASS_ATTENTION, MTP_KCLASS_HEADS = 1, 2, 3, 4, 5
+
+EXPORTED = ["mtp_query_sizes", "mtp_weight_offset", "mtp_create", "mtp_prefill", "mtp_decode_step",
+            "mtp_decode_step_async", "mtp_get_logits", "mtp_get_lattice", "mtp_get_seq_state", "mtp_get_tokens",
+            "mtp_profile", "mtp_profile_read", "mtp_reset", "mtp_destroy", "mtp_last_error", "mtp_strerror"]
+
+
+class mtp_config(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "n_layers", "d_model", "n_heads", "d_ff", "vocab", "eos_id", "n_phone", "max_pos", "k_heads",
+        "topk_max", "max_batch", "max_prompt", "max_new", "eos_min", "page_size", "num_pages", "dtype", "flags")]
+
+
+class mtp_sizes(ctypes.Structure):
+    _fields_ = [("weights_bytes", ctypes.c_uint64), ("logq_bytes", ctypes.c_uint64),
+                ("kv_bytes", ctypes.c_uint64), ("workspace_bytes", ctypes.c_uint64)]
+
+
+class mtp_buffers(ctypes.Structure):
+    _fields_ = [("weights", ctypes.c_void_p), ("logq", ctypes.c_void_p),
+                ("kv_pool", ctypes.c_void_p), ("workspace", ctypes.c_void_p)]
+
+
+_P = ctypes.POINTER
+_i32p = _P(ctypes.c_int32)
+_f32p = _P(ctypes.c_float)
+_ctx = ctypes.c_void_p
+
+_lib.mtp_query_sizes.argtypes = [_P(mtp_config), _P(mtp_sizes)]
+_lib.mtp_weight_offset.argtypes = [_P(mtp_config), ctypes.c_int, ctypes.c_int, _P(ctypes.c_uint64), _P(ctypes.c_uint64)]
+_lib.mtp_create.argtypes = [_P(mtp_config), _P(mtp_buffers), ctypes.c_void_p, _P(_ctx)]
+_lib.mtp_prefill.argtypes = [_ctx, ctypes.c_int, _i32p, _i32p, _i32p, _i32p]
+_lib.mtp_decode_step.argtypes = [_ctx, ctypes.c_int, ctypes.c_int, _i32p, _i32p]
+_lib.mtp_decode_step_async.argtypes = [_ctx, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+_lib.mtp_get_logits.argtypes = [_ctx, _f32p]
+_lib.mtp_get_lattice.argtypes = [_ctx, _i32p, _f32p, _f32p, _i32p, _i32p]
+_lib.mtp_get_seq_state.argtypes = [_ctx, _i32p, _i32p, _i32p, _i32p]
+_lib.mtp_get_tokens.argtypes = [_ctx, _i32p]
+_lib.mtp_profile.argtypes = [_ctx, ctypes.c_int, ctypes.c_int]
+_lib.mtp_profile_read.argtypes = [_ctx, _P(ctypes.c_double), _P(ctypes.c_int64)]
+_lib.mtp_reset.argtypes = [_ctx]
+_lib.mtp_destroy.argtypes = [_ctx]
+_lib.mtp_destroy.restype = None
+_lib.mtp_last_error.argtypes = [_ctx]
+_lib.mtp_last_error.restype = ctypes.c_char_p
+_lib.mtp_strerror.argtypes = [ctypes.c_int]
+_lib.mtp_strerror.restype = ctypes.c_char_p
+
+
+class MTPError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{msg} (code {code})")
+        self.code = code
+
+
+def _check(rc: int, ctx=None, what: str = ""):
+    if rc != MTP_OK:
+        detail = _lib.mtp_last_error(ctx).decode() if ctx else _lib.mtp_strerror(rc).decode()
+        raise MTPError(rc, f"{what}: {detail}")
+
+
+def _i32(a) -> Tuple[np.ndarray, object]:
+    arr = np.ascontiguousarray(np.asarray(a, dtype=np.int32))
+    return arr, arr.ctypes.data_as(_i32p)
+
+
+# ------------------------------------------------------------- C-named calls
+def mtp_query_sizes(cfg: mtp_config) -> mtp_sizes:
+    out = mtp_sizes()
+    _check(_lib.mtp_query_sizes(ctypes.byref(cfg), ctypes.byref(out)), None, "mtp_query_sizes")
+    return out
+
+
+def mtp_weight_offset(cfg: mtp_config, tensor: int, layer: int = 0) -> Tuple[int, int]:
+    off, n = ctypes.c_uint64(), ctypes.c_uint64()
+    _check(_lib.mtp_weight_offset(ctypes.byref(cfg), tensor, layer, ctypes.byref(off), ctypes.byref(n)),
+           None, "mtp_weight_offset")
+    return off.value, n.value
+
+
+def mtp_create(cfg: mtp_config, bufs: mtp_buffers, stream: int):
+    ctx = _ctx()
+    _check(_lib.mtp_create(ctypes.byref(cfg), ctypes.byref(bufs), ctypes.c_void_p(stream), ctypes.byref(ctx)),
+           None, "mtp_create")
+    return ctx
+
+
+def mtp_prefill(ctx, phon: Sequence[np.ndarray], ac: Sequence[np.ndarray]) -> None:
+    B = len(ac)
+    pl, plp = _i32([len(p) for p in phon])
+    al, alp = _i32([len(a) for a in ac])
+    pf, pfp = _i32(np.concatenate([np.asarray(p, np.int32) for p in phon]) if sum(pl) else np.zeros(1, np.int32))
+    af, afp = _i32(np.concatenate([np.asarray(a, np.int32) for a in ac]))
+    _check(_lib.mtp_prefill(ctx, B, pfp, plp, afp, alp), ctx, "mtp_prefill")
+
+
+def mtp_decode_step(ctx, B: int, K: int, top_k: int) -> Tuple[np.ndarray, np.ndarray]:
+    tok = np.zeros((B, K), np.int32)
+    cnt = np.zeros(B, np.int32)
+    _check(_lib.mtp_decode_step(ctx, K, top_k, tok.ctypes.data_as(_i32p), cnt.ctypes.data_as(_i32p)),
+           ctx, "mtp_decode_step")
+    return tok, cnt
+
+
+def mtp_decode_step_async(ctx, K: int, top_k: int, d_tokens: int = 0, d_count: int = 0) -> None:
+    _check(_lib.mtp_decode_step_async(ctx, K, top_k, ctypes.c_void_p(d_tokens or None),
+                                      ctypes.c_void_p(d_count or None)), ctx, "mtp_decode_step_async")
+
+
+def mtp_get_logits(ctx, B: int, K: int, V: int) -> np.ndarray:
+    out = np.zeros((B, K, V), np.float32)
+    _check(_lib.mtp_get_logits(ctx, out.ctypes.data_as(_f32p)), ctx, "mtp_get_logits")
+    return out
+
+
+def mtp_get_lattice(ctx, B: int, K: int, top_k: int) -> Dict[str, np.ndarray]:
+    cand = np.zeros((B, K, top_k), np.int32)
+    ehat = np.zeros((B, K, top_k), np.float32)
+    delta = np.zeros((B, K, top_k), np.float32)
+    psi = np.zeros((B, K, top_k), np.int32)
+    slots = np.zeros((B, K), np.int32)
+    _check(_lib.mtp_get_lattice(ctx, cand.ctypes.data_as(_i32p), ehat.ctypes.data_as(_f32p),
+                                delta.ctypes.data_as(_f32p), psi.ctypes.data_as(_i32p),
+                                slots.ctypes.data_as(_i32p)), ctx, "mtp_get_lattice")
+    return dict(cand=cand, ehat=ehat, delta=delta, psi=psi, slots=slots)
+
+
+def mtp_get_seq_state(ctx, B: int) -> Dict[str, np.ndarray]:
+    a = [np.zeros(B, np.int32) for _ in range(4)]
+    _check(_lib.mtp_get_seq_state(ctx, *[x.ctypes.data_as(_i32p) for x in a]), ctx, "mtp_get_seq_state")
+    return dict(ctx_len=a[0], pend_len=a[1], gen=a[2], done=a[3])
+
+
+def mtp_get_tokens(ctx, B: int, max_new: int) -> np.ndarray:
+    out = np.zeros((B, max_new), np.int32)
+    _check(_lib.mtp_get_tokens(ctx, out.ctypes.data_as(_i32p)), ctx, "mtp_get_tokens")
+    return out
+
+
+def mtp_profile(ctx, kclass: int, enable: bool) -> None:
+    _check(_lib.mtp_profile(ctx, kclass, 1 if enable else 0), ctx, "mtp_profile")
+
+
+def mtp_profile_read(ctx) -> Tuple[float, int]:
+    ms, n = ctypes.c_double(), ctypes.c_int64()
+    _check(_lib.mtp_profile_read(ctx, ctypes.byref(ms), ctypes.byref(n)), ctx, "mtp_profile_read")
+    return ms.value, n.value
+
+
+def mtp_reset(ctx) -> None:
+    _check(_lib.mtp_reset(ctx), ctx, "mtp_reset")
+
+
+def mtp_destroy(ctx) -> None:
+    _lib.mtp_destroy(ctx)
+
+
+def mtp_last_error(ctx) -> str:
+    return _lib.mtp_last_error(ctx).decode()
+
+
+def mtp_strerror(code: int) -> str:
+    return _lib.mtp_strerror(code).decode()
+
+
+# --------------------------------------------------------------- convenience
+def make_config(shape, max_batch: int, max_prompt: int, max_new: int, eos_min: int, topk_max: int = 32,
+                page_size: int = 16, num_pages: int = 0, flags: int = 0) -> mtp_config:
+    return mtp_config(
+        n_layers=shape.n_layers, d_model=shape.d_model, n_heads=shape.n_heads, d_ff=shape.d_ff,
+        vocab=shape.vocab, eos_id=shape.eos_id, n_phone=shape.n_phone, max_pos=shape.max_pos,
+        k_heads=shape.k_heads, topk_max=topk_max, max_batch=max_batch, max_prompt=max_prompt,
+        max_new=max_new, eos_min=eos_min, page_size=page_size, num_pages=num_pages,
+        dtype=MTP_DTYPE_BF16 if shape.dtype == "bf16" else MTP_DTYPE_F32, flags=flags)
+
+
+_TENSOR_OF = {"emb_phone": MTP_T_EMB_PHONE, "emb_ac": MTP_T_EMB_AC, "pos": MTP_T_POS,
+              "lnf_g": MTP_T_LNF_G, "lnf_b": MTP_T_LNF_B, "w_heads": MTP_T_W_HEADS, "b_heads": MTP_T_B_HEADS}
+_LAYER_TENSOR_OF = {"ln1_g": MTP_T_LN1_G, "ln1_b": MTP_T_LN1_B, "w_qkv": MTP_T_W_QKV, "b_qkv": MTP_T_B_QKV,
+                    "w_o": MTP_T_W_O, "b_o": MTP_T_B_O, "ln2_g": MTP_T_LN2_G, "ln2_b": MTP_T_LN2_B,
+                    "w_1": MTP_T_W_1, "b_1": MTP_T_B_1, "w_2": MTP_T_W_2, "b_2": MTP_T_B_2}
+_MATRICES = {MTP_T_EMB_PHONE, MTP_T_EMB_AC, MTP_T_POS, MTP_T_W_QKV, MTP_T_W_O, MTP_T_W_1, MTP_T_W_2, MTP_T_W_HEADS}
+
+
+def pack_weights(cfg: mtp_config, weights: Dict[str, np.ndarray]) -> np.ndarray:
+    """Host image of the packed weights buffer (uint8) in the library's layout."""
+    total = mtp_query_sizes(cfg).weights_bytes
+    img = np.zeros(total, np.uint8)
+    for name, arr in weights.items():
+        if name.startswith("l") and "." in name:
+            l, short = name.split(".", 1)
+            t, layer = _LAYER_TENSOR_OF[short], int(l[1:])
+        else:
+            t, layer = _TENSOR_OF[name], 0
+        off, n = mtp_weight_offset(cfg, t, layer)
+        a = np.ascontiguousarray(arr, dtype=np.float32).reshape(-1)
+        assert a.size == n, (name, a.size, n)
+        if t in _MATRICES and cfg.dtype == MTP_DTYPE_BF16:
+            raw = (a.view(np.uint32) >> 16).astype(np.uint16)
+            assert np.array_equal((raw.astype(np.uint32) << 16).view(np.float32), a), f"{name} is not bf16-exact"
+            img[off:off + 2 * n] = raw.view(np.uint8)
+        else:
+            img[off:off + 4 * n] = a.view(np.uint8)
+    return img
+
+
+class Session:
+    """Owns the torch device buffers of one context and its stream."""
+
+    def __init__(self, shape, weights: Dict[str, np.ndarray], logq: np.ndarray, max_batch: int,
+                 max_prompt: int, max_new: int, eos_min: int, topk_max: int = 32, page_size: int = 16,
+                 num_pages: int = 0, flags: int = 0, device: str = "cuda:0", stream=None):
+        import torch
+        self.torch = torch
+        self.shape = shape
+        self.cfg = make_config(shape, max_batch, max_prompt, max_new, eos_min, topk_max, page_size, num_pages, flags)
+        sz = mtp_query_sizes(self.cfg)
+        self.sizes = sz
+        self.device = torch.device(device)
+        self.weights_dev = torch.from_numpy(pack_weights(self.cfg, weights)).to(self.device)
+        self.logq_dev = torch.from_numpy(np.ascontiguousarray(logq, dtype=np.float32)).to(self.device)
+        self.kv = torch.empty(int(sz.kv_bytes), dtype=torch.uint8, device=self.device)
+        self.ws = torch.empty(int(sz.workspace_bytes), dtype=torch.uint8, device=self.device)
+        self.stream = stream if stream is not None else torch.cuda.Stream(device=self.device)
+        torch.cuda.synchronize(self.device)
+        bufs = mtp_buffers(self.weights_dev.data_ptr(), self.logq_dev.data_ptr(), self.kv.data_ptr(),
+                           self.ws.data_ptr())
+        self.ctx = mtp_create(self.cfg, bufs, self.stream.cuda_stream)
+        self.B = 0
+
+    def prefill(self, phon: Sequence[np.ndarray], ac: Sequence[np.ndarray]) -> None:
+        mtp_prefill(self.ctx, phon, ac)
+        self.B = len(ac)
+
+    def step(self, K: int, top_k: int) -> Tuple[np.ndarray, np.ndarray]:
+        return mtp_decode_step(self.ctx, self.B, K, top_k)
+
+    def step_async(self, K: int, top_k: int) -> None:
+        mtp_decode_step_async(self.ctx, K, top_k)
+
+    def logits(self, K: int) -> np.ndarray:
+        return mtp_get_logits(self.ctx, self.B, K, self.cfg.vocab)
+
+    def lattice(self, K: int, top_k: int) -> Dict[str, np.ndarray]:
+        return mtp_get_lattice(self.ctx, self.B, K, top_k)
+
+    def seq_state(self) -> Dict[str, np.ndarray]:
+        return mtp_get_seq_state(self.ctx, self.B)
+
+    def tokens(self) -> np.ndarray:
+        return mtp_get_tokens(self.ctx, self.B, self.cfg.max_new)
+
+    def close(self) -> None:
+        if getattr(self, "ctx", None):
+            mtp_destroy(self.ctx)
+            self.ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

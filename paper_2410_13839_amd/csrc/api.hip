@@ -1,0 +1,664 @@
+// libmtp: C ABI and host runtime of the MTP + Viterbi decode path.
+//
+// The context holds only host bookkeeping: the device layout of the
+// caller's buffers, the KV page assignment, the launch plan of a decode step
+// and the hipGraph instances that replay it.  Every step of the computation
+// runs in the kernels of gemm.hip, attention.hip, rowops.hip and select.hip.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <new>
+#include <string>
+#include <tuple>
+#include <vector>
+
+#include "../../include/mtp.h"
+#include "common.h"
+#include "launch.h"
+
+using namespace mtp;
+
+namespace {
+
+uint64_t align256(uint64_t x) { return (x + 255) & ~uint64_t(255); }
+
+bool is_matrix(int t) {
+    return t == MTP_T_EMB_PHONE || t == MTP_T_EMB_AC || t == MTP_T_POS || t == MTP_T_W_QKV || t == MTP_T_W_O ||
+           t == MTP_T_W_1 || t == MTP_T_W_2 || t == MTP_T_W_HEADS;
+}
+bool is_layer_tensor(int t) { return t >= MTP_T_LN1_G && t <= MTP_T_B_2; }
+
+uint64_t tensor_numel(const mtp_config& c, int t) {
+    const uint64_t d = c.d_model, f = c.d_ff, v = c.vocab;
+    switch (t) {
+    case MTP_T_EMB_PHONE: return (uint64_t)c.n_phone * d;
+    case MTP_T_EMB_AC: return v * d;
+    case MTP_T_POS: return (uint64_t)c.max_pos * d;
+    case MTP_T_LN1_G: case MTP_T_LN1_B: case MTP_T_B_O: case MTP_T_LN2_G: case MTP_T_LN2_B: case MTP_T_B_2:
+    case MTP_T_LNF_G: case MTP_T_LNF_B: return d;
+    case MTP_T_W_QKV: return 3 * d * d;
+    case MTP_T_B_QKV: return 3 * d;
+    case MTP_T_W_O: return d * d;
+    case MTP_T_W_1: return f * d;
+    case MTP_T_B_1: return f;
+    case MTP_T_W_2: return d * f;
+    case MTP_T_W_HEADS: return (uint64_t)c.k_heads * v * d;
+    case MTP_T_B_HEADS: return (uint64_t)c.k_heads * v;
+    }
+    return 0;
+}
+
+uint64_t tensor_bytes(const mtp_config& c, int t) {
+    return tensor_numel(c, t) * (is_matrix(t) ? (c.dtype == MTP_DTYPE_BF16 ? 2 : 4) : 4);
+}
+
+// Offsets of every tensor in packing order; returns total bytes.
+uint64_t weight_layout(const mtp_config& c, std::vector<uint64_t>* glob, std::vector<uint64_t>* lay) {
+    uint64_t off = 0;
+    if (glob) glob->assign(MTP_T_COUNT, 0);
+    if (lay) lay->assign((size_t)c.n_layers * MTP_T_COUNT, 0);
+    for (int t = MTP_T_EMB_PHONE; t <= MTP_T_POS; ++t) {
+        if (glob) (*glob)[t] = off;
+        off = align256(off + tensor_bytes(c, t));
+    }
+    for (int l = 0; l < c.n_layers; ++l)
+        for (int t = MTP_T_LN1_G; t <= MTP_T_B_2; ++t) {
+            if (lay) (*lay)[(size_t)l * MTP_T_COUNT + t] = off;
+            off = align256(off + tensor_bytes(c, t));
+        }
+    for (int t = MTP_T_LNF_G; t <= MTP_T_B_HEADS; ++t) {
+        if (glob) (*glob)[t] = off;
+        off = align256(off + tensor_bytes(c, t));
+    }
+    return off;
+}
+
+int validate(const mtp_config* c, std::string* why) {
+    auto bad = [&](const char* m) { if (why) *why = m; return MTP_EINVAL; };
+    if (!c) return bad("config is NULL");
+    if (c->n_layers < 1 || c->n_layers > 256) return bad("n_layers out of range");
+    if (c->d_model < 64 || c->d_model % 256 != 0 || c->d_model > 2048) return bad("d_model must be a multiple of 256 in 256..2048");
+    if (c->n_heads * MTP_HEAD_DIM != c->d_model) return bad("d_model / n_heads must be 64");
+    if (c->d_ff < 64 || c->d_ff % 256 != 0) return bad("d_ff must be a positive multiple of 256");
+    if (c->vocab < 2 || c->vocab > 64 * 17) return bad("vocab out of range (2..1088)");
+    if (c->eos_id < 0 || c->eos_id >= c->vocab) return bad("eos_id out of range");
+    if (c->n_phone < 1) return bad("n_phone must be positive");
+    if (c->k_heads < 1 || c->k_heads > MTP_MAX_HEADS_K) return bad("k_heads must be in 1..8");
+    if (c->topk_max < 1 || c->topk_max > MTP_MAX_TOPK || c->topk_max >= c->vocab) return bad("topk_max must be in 1..32 and below vocab");
+    if (c->max_batch < 1 || c->max_batch > 4096) return bad("max_batch out of range");
+    if (c->max_prompt < 1) return bad("max_prompt must be positive");
+    if (c->max_new < 1) return bad("max_new must be positive");
+    if ((int64_t)c->max_prompt + c->max_new > c->max_pos) return bad("max_prompt + max_new exceeds max_pos");
+    if (c->page_size < 8 || c->page_size > 128 || (c->page_size & (c->page_size - 1))) return bad("page_size must be a power of two in 8..128");
+    if (c->num_pages < 0) return bad("num_pages must be >= 0");
+    if (c->dtype != MTP_DTYPE_F32 && c->dtype != MTP_DTYPE_BF16) return bad("unknown dtype");
+    return MTP_OK;
+}
+
+struct WsLayout {
+    uint64_t rows, ids, tiles, last_row, state, btab, h, q, u, attn, ffn, part, apart, hz, z, logits, cand, ehat,
+        delta, psi, slots, out_tok, out_cnt, hist, total;
+    int64_t m_pre, m_dec, m_max, max_tiles, max_splits, maxp, num_pages;
+    int act_bytes;
+};
+
+WsLayout ws_layout(const mtp_config& c) {
+    WsLayout w{};
+    const int64_t B = c.max_batch, d = c.d_model, F = c.d_ff, KH = c.k_heads, V = c.vocab, TK = c.topk_max;
+    const int64_t H = c.n_heads;
+    w.act_bytes = c.dtype == MTP_DTYPE_BF16 ? 2 : 4;
+    w.m_pre = B * c.max_prompt;
+    w.m_dec = B * KH;
+    w.m_max = std::max(w.m_pre, w.m_dec);
+    w.max_tiles = w.m_pre / MTP_ATTN_QT + B + 1;
+    const int64_t max_ctx = (int64_t)c.max_prompt + c.max_new;
+    w.max_splits = (max_ctx + 63) / 64;
+    w.maxp = (max_ctx + c.page_size - 1) / c.page_size;
+    w.num_pages = c.num_pages > 0 ? c.num_pages : B * w.maxp;
+    uint64_t o = 0;
+    auto take = [&](uint64_t bytes) { uint64_t r = o; o = align256(o + bytes); return r; };
+    w.rows = take(w.m_max * sizeof(RowInfo));
+    w.ids = take(w.m_pre * 4);
+    w.tiles = take(w.max_tiles * 8);
+    w.last_row = take(B * 4);
+    w.state = take(B * sizeof(SeqState));
+    w.btab = take(B * w.maxp * 4);
+    w.h = take(w.m_max * d * 4);
+    w.q = take(w.m_max * d * 4);
+    w.u = take(w.m_max * d * w.act_bytes);
+    w.attn = take(w.m_max * d * w.act_bytes);
+    w.ffn = take(w.m_max * F * w.act_bytes);
+    w.part = take(std::max(w.m_pre, w.m_dec * (int64_t)MTP_SPLITK_MAX) * d * 4);
+    w.apart = take(B * H * w.max_splits * MTP_ATTN_QT * 66 * 4);
+    w.hz = take(B * d * 4);
+    w.z = take(B * d * w.act_bytes);
+    w.logits = take(B * KH * V * 4);
+    w.cand = take(B * KH * TK * 4);
+    w.ehat = take(B * KH * TK * 4);
+    w.delta = take(B * KH * TK * 4);
+    w.psi = take(B * KH * TK * 4);
+    w.slots = take(B * KH * 4);
+    w.out_tok = take(B * KH * 4);
+    w.out_cnt = take(B * 4);
+    w.hist = take(B * (int64_t)c.max_new * 4);
+    w.total = o;
+    return w;
+}
+
+uint64_t kv_bytes(const mtp_config& c, const WsLayout& w) {
+    return (uint64_t)c.n_layers * w.num_pages * 2 * c.n_heads * c.page_size * MTP_HEAD_DIM * (c.dtype == MTP_DTYPE_BF16 ? 2 : 4);
+}
+
+}  // namespace
+
+struct mtp_ctx {
+    mtp_config cfg;
+    mtp_buffers buf;
+    hipStream_t stream;
+    WsLayout ws;
+    std::vector<uint64_t> wglob, wlay;
+    std::string err;
+    // sequence bookkeeping
+    bool prefilled = false;
+    int B = 0;
+    int q_pad = 0;               // pending rows per sequence for the next step
+    int last_K = 0, last_topk = 0;
+    int split_len = 64, n_splits = 1;
+    std::vector<int32_t> h_ids, h_last, h_btab;
+    std::vector<RowInfo> h_rows;
+    std::vector<int2> h_tiles;
+    std::vector<SeqState> h_state;
+    int n_pre_rows = 0, n_pre_tiles = 0;
+    // graphs keyed by (K, top_k, q_pad, batch, split_len, n_splits)
+    std::map<std::tuple<int, int, int, int, int, int>, hipGraphExec_t> graphs;
+    // profiling
+    int prof_class = 0;
+    std::vector<std::pair<hipEvent_t, hipEvent_t>> prof_events;
+    size_t prof_used = 0;
+
+    char* W() const { return (char*)buf.weights; }
+    char* WS() const { return (char*)buf.workspace; }
+    template <typename T> T* ws_ptr(uint64_t off) const { return reinterpret_cast<T*>(WS() + off); }
+    const void* wt(int t) const { return W() + wglob[t]; }
+    const void* lt(int l, int t) const { return W() + wlay[(size_t)l * MTP_T_COUNT + t]; }
+    KVView kv(int layer) const {
+        KVView v;
+        v.pool = buf.kv_pool;
+        v.block_table = ws_ptr<int32_t>(ws.btab);
+        v.max_pages_per_seq = (int32_t)ws.maxp;
+        v.num_pages = (int32_t)ws.num_pages;
+        v.page_size = cfg.page_size;
+        int sh = 0;
+        while ((1 << sh) < cfg.page_size) ++sh;
+        v.page_shift = sh;
+        v.n_heads = cfg.n_heads;
+        v.layer = layer;
+        return v;
+    }
+};
+
+namespace {
+
+int hip_fail(mtp_ctx* c, hipError_t e, const char* where) {
+    c->err = std::string(where) + ": " + hipGetErrorString(e);
+    return MTP_EHIP;
+}
+#define HIPCHK(ctx, expr, where)                                  \
+    do {                                                          \
+        hipError_t _e = (expr);                                   \
+        if (_e != hipSuccess) return hip_fail((ctx), _e, (where)); \
+    } while (0)
+
+int pick_splits(const mtp_ctx* c, int M, int N, int K) {
+    if (c->cfg.dtype != MTP_DTYPE_BF16) return 1;
+    const int64_t cap_rows = std::max(c->ws.m_pre, c->ws.m_dec * (int64_t)MTP_SPLITK_MAX);
+    const int gran = gemm_split_granule(1, M);
+    int tiles = (M <= 32) ? (N + 15) / 16 : ((N + 31) / 32) * ((M + 127) / 128);
+    if (M > 256) tiles = ((N + 127) / 128) * ((M + 127) / 128);
+    int s = 1;
+    while (s < MTP_SPLITK_MAX && tiles * s < 256 && K % (gran * s * 2) == 0 && (int64_t)M * s * 2 <= cap_rows) s *= 2;
+    return s;
+}
+
+void prof_begin(mtp_ctx* c, int kclass) {
+    if (c->prof_class != kclass) return;
+    if (c->prof_used >= c->prof_events.size()) {
+        hipEvent_t a, b;
+        if (hipEventCreate(&a) != hipSuccess) return;
+        if (hipEventCreate(&b) != hipSuccess) { (void)hipEventDestroy(a); return; }
+        c->prof_events.push_back({a, b});
+    }
+    (void)hipEventRecord(c->prof_events[c->prof_used].first, c->stream);
+}
+void prof_end(mtp_ctx* c, int kclass) {
+    if (c->prof_class != kclass || c->prof_used >= c->prof_events.size()) return;
+    (void)hipEventRecord(c->prof_events[c->prof_used].second, c->stream);
+    c->prof_used++;
+}
+
+// One trunk layer over `rows` rows whose row/tile metadata is already on the device.
+int run_layer(mtp_ctx* c, int l, int rows, int n_tiles, int qt, int split_len, int n_splits, bool decode) {
+    const mtp_config& cf = c->cfg;
+    const int d = cf.d_model, F = cf.d_ff, dt = cf.dtype;
+    hipStream_t st = c->stream;
+    const int ab = c->ws.act_bytes;
+    GemmArgs g{};
+    g.dtype = dt;
+    // LN1 output u -> q, K/V cache
+    g.epi = EPI_QKV; g.X = c->WS() + c->ws.u; g.ldx = d; g.M = rows;
+    g.W = c->lt(l, MTP_T_W_QKV); g.N = 3 * d; g.K = d; g.splits = 1;
+    g.bias = (const float*)c->lt(l, MTP_T_B_QKV);
+    g.q = c->ws_ptr<float>(c->ws.q); g.rows = c->ws_ptr<RowInfo>(c->ws.rows); g.kv = c->kv(l); g.d = d;
+    if (decode) prof_begin(c, MTP_KCLASS_GEMM_QKV);
+    HIPCHK(c, gemm(st, g), "qkv gemm");
+    if (decode) prof_end(c, MTP_KCLASS_GEMM_QKV);
+    // attention
+    AttnArgs a{};
+    a.dtype = dt; a.q = c->ws_ptr<float>(c->ws.q); a.ldq = d; a.rows = c->ws_ptr<RowInfo>(c->ws.rows);
+    a.tiles = c->ws_ptr<int2>(c->ws.tiles); a.n_tiles = n_tiles; a.qt = qt; a.kv = c->kv(l);
+    a.split_len = split_len; a.n_splits = n_splits; a.out = c->WS() + c->ws.attn; a.ldo = d;
+    a.part = c->ws_ptr<float>(c->ws.apart);
+    if (decode) prof_begin(c, MTP_KCLASS_ATTENTION);
+    HIPCHK(c, attention(st, a), "attention");
+    if (decode) prof_end(c, MTP_KCLASS_ATTENTION);
+    // out projection -> partials, residual + LN2
+    const size_t sstride = (size_t)rows * d;
+    g = GemmArgs{};
+    g.dtype = dt; g.epi = EPI_PARTIAL; g.X = c->WS() + c->ws.attn; g.ldx = d; g.M = rows;
+    g.W = c->lt(l, MTP_T_W_O); g.N = d; g.K = d; g.splits = pick_splits(c, rows, d, d);
+    g.out = c->WS() + c->ws.part; g.ldo = d; g.split_stride = sstride;
+    HIPCHK(c, gemm(st, g), "out-proj gemm");
+    ResidArgs r{};
+    r.dtype = dt; r.n_rows = rows; r.d = d; r.h = c->ws_ptr<float>(c->ws.h); r.part = c->ws_ptr<float>(c->ws.part);
+    r.n_split = g.splits; r.split_stride = sstride; r.bias = (const float*)c->lt(l, MTP_T_B_O);
+    r.ln_g = (const float*)c->lt(l, MTP_T_LN2_G); r.ln_b = (const float*)c->lt(l, MTP_T_LN2_B); r.u = c->WS() + c->ws.u;
+    HIPCHK(c, resid_ln(st, r), "resid+ln2");
+    // FFN1 + GELU
+    g = GemmArgs{};
+    g.dtype = dt; g.epi = EPI_GELU; g.X = c->WS() + c->ws.u; g.ldx = d; g.M = rows;
+    g.W = c->lt(l, MTP_T_W_1); g.N = F; g.K = d; g.splits = 1;
+    g.bias = (const float*)c->lt(l, MTP_T_B_1); g.out = c->WS() + c->ws.ffn; g.ldo = F;
+    if (decode) prof_begin(c, MTP_KCLASS_GEMM_FFN1);
+    HIPCHK(c, gemm(st, g), "ffn1 gemm");
+    if (decode) prof_end(c, MTP_KCLASS_GEMM_FFN1);
+    // FFN2 -> partials, residual + next LN1
+    g = GemmArgs{};
+    g.dtype = dt; g.epi = EPI_PARTIAL; g.X = c->WS() + c->ws.ffn; g.ldx = F; g.M = rows;
+    g.W = c->lt(l, MTP_T_W_2); g.N = d; g.K = F; g.splits = pick_splits(c, rows, d, F);
+    g.out = c->WS() + c->ws.part; g.ldo = d; g.split_stride = sstride;
+    if (decode) prof_begin(c, MTP_KCLASS_GEMM_FFN2);
+    HIPCHK(c, gemm(st, g), "ffn2 gemm");
+    if (decode) prof_end(c, MTP_KCLASS_GEMM_FFN2);
+    r = ResidArgs{};
+    r.dtype = dt; r.n_rows = rows; r.d = d; r.h = c->ws_ptr<float>(c->ws.h); r.part = c->ws_ptr<float>(c->ws.part);
+    r.n_split = g.splits; r.split_stride = sstride; r.bias = (const float*)c->lt(l, MTP_T_B_2);
+    if (l + 1 < cf.n_layers) {
+        r.ln_g = (const float*)c->lt(l + 1, MTP_T_LN1_G); r.ln_b = (const float*)c->lt(l + 1, MTP_T_LN1_B);
+        r.u = c->WS() + c->ws.u;
+    }
+    HIPCHK(c, resid_ln(st, r), "resid+ln1");
+    (void)ab;
+    return MTP_OK;
+}
+
+int enqueue_step(mtp_ctx* c, int K, int top_k) {
+    const mtp_config& cf = c->cfg;
+    const int d = cf.d_model, dt = cf.dtype, B = c->B, Q = c->q_pad, V = cf.vocab;
+    hipStream_t st = c->stream;
+    if (Q > 0) {
+        const int rows = B * Q;
+        EmbedArgs e{};
+        e.dtype = dt; e.mode = 0; e.n_rows = rows; e.Q = Q; e.st = c->ws_ptr<SeqState>(c->ws.state);
+        e.ids = nullptr; e.rows = c->ws_ptr<RowInfo>(c->ws.rows); e.tiles = c->ws_ptr<int2>(c->ws.tiles);
+        e.emb_phone = c->wt(MTP_T_EMB_PHONE); e.emb_ac = c->wt(MTP_T_EMB_AC); e.pos = c->wt(MTP_T_POS);
+        e.ln_g = (const float*)c->lt(0, MTP_T_LN1_G); e.ln_b = (const float*)c->lt(0, MTP_T_LN1_B);
+        e.d = d; e.h = c->ws_ptr<float>(c->ws.h); e.u = c->WS() + c->ws.u;
+        HIPCHK(c, embed_ln(st, e), "embed");
+        int qt = 1;
+        while (qt < Q) qt <<= 1;
+        for (int l = 0; l < cf.n_layers; ++l) {
+            int rc = run_layer(c, l, rows, B, qt, c->split_len, c->n_splits, true);
+            if (rc) return rc;
+        }
+    }
+    FinalArgs f{};
+    f.dtype = dt; f.B = B; f.d = d; f.mode = 0; f.Q = Q; f.st = c->ws_ptr<SeqState>(c->ws.state);
+    f.h = c->ws_ptr<float>(c->ws.h); f.hz = c->ws_ptr<float>(c->ws.hz);
+    f.ln_g = (const float*)c->wt(MTP_T_LNF_G); f.ln_b = (const float*)c->wt(MTP_T_LNF_B); f.z = c->WS() + c->ws.z;
+    HIPCHK(c, final_ln(st, f), "final ln");
+    GemmArgs g{};
+    g.dtype = dt; g.epi = EPI_LOGITS; g.X = c->WS() + c->ws.z; g.ldx = d; g.M = B;
+    g.W = c->wt(MTP_T_W_HEADS); g.N = K * V; g.K = d; g.splits = 1;
+    g.bias = (const float*)c->wt(MTP_T_B_HEADS); g.out = c->WS() + c->ws.logits; g.ldo = K * V;
+    prof_begin(c, MTP_KCLASS_HEADS);
+    HIPCHK(c, gemm(st, g), "heads gemm");
+    prof_end(c, MTP_KCLASS_HEADS);
+    SelectArgs s{};
+    s.B = B; s.K = K; s.top_k = top_k; s.V = V; s.eos_id = cf.eos_id; s.eos_min = cf.eos_min; s.max_new = cf.max_new;
+    s.Q = Q; s.logits = c->ws_ptr<float>(c->ws.logits); s.ld_logits = K * V; s.logq = c->buf.logq;
+    s.st = c->ws_ptr<SeqState>(c->ws.state);
+    s.cand = c->ws_ptr<int32_t>(c->ws.cand); s.ehat = c->ws_ptr<float>(c->ws.ehat); s.delta = c->ws_ptr<float>(c->ws.delta);
+    s.psi = c->ws_ptr<int32_t>(c->ws.psi); s.slots = c->ws_ptr<int32_t>(c->ws.slots);
+    s.out_tokens = c->ws_ptr<int32_t>(c->ws.out_tok); s.out_count = c->ws_ptr<int32_t>(c->ws.out_cnt);
+    s.hist = c->ws_ptr<int32_t>(c->ws.hist); s.hist_ld = cf.max_new;
+    HIPCHK(c, topk(st, s), "topk");
+    HIPCHK(c, viterbi_accept(st, s), "viterbi");
+    return MTP_OK;
+}
+
+int step_common(mtp_ctx* c, int K, int top_k) {
+    if (!c) return MTP_EINVAL;
+    if (!c->prefilled) { c->err = "decode step before prefill"; return MTP_ESTATE; }
+    if (K < 1 || K > c->cfg.k_heads) { c->err = "K must be in 1..k_heads"; return MTP_EINVAL; }
+    if (top_k < 1 || top_k > c->cfg.topk_max) { c->err = "top_k must be in 1..topk_max"; return MTP_EINVAL; }
+    const bool use_graph = !(c->cfg.flags & MTP_FLAG_NO_GRAPH) && c->stream != nullptr && c->prof_class == 0;
+    int rc;
+    if (!use_graph) {
+        rc = enqueue_step(c, K, top_k);
+    } else {
+        auto key = std::make_tuple(K, top_k, c->q_pad, c->B, c->split_len, c->n_splits);
+        auto it = c->graphs.find(key);
+        if (it == c->graphs.end()) {
+            hipGraph_t graph;
+            HIPCHK(c, hipStreamBeginCapture(c->stream, hipStreamCaptureModeRelaxed), "begin capture");
+            rc = enqueue_step(c, K, top_k);
+            hipError_t e = hipStreamEndCapture(c->stream, &graph);
+            if (rc) { if (e == hipSuccess) (void)hipGraphDestroy(graph); return rc; }
+            if (e != hipSuccess) return hip_fail(c, e, "end capture");
+            hipGraphExec_t exec;
+            e = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+            (void)hipGraphDestroy(graph);
+            if (e != hipSuccess) return hip_fail(c, e, "graph instantiate");
+            it = c->graphs.emplace(key, exec).first;
+        }
+        HIPCHK(c, hipGraphLaunch(it->second, c->stream), "graph launch");
+        rc = MTP_OK;
+    }
+    if (rc == MTP_OK) {
+        c->q_pad = K;
+        c->last_K = K;
+        c->last_topk = top_k;
+    }
+    return rc;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* mtp_strerror(int code) {
+    switch (code) {
+    case MTP_OK: return "ok";
+    case MTP_EINVAL: return "invalid argument";
+    case MTP_ENOMEM: return "KV page pool or workspace too small";
+    case MTP_ESTATE: return "call out of order";
+    case MTP_EHIP: return "HIP runtime error";
+    }
+    return "unknown error";
+}
+
+int mtp_query_sizes(const mtp_config* cfg, mtp_sizes* out) {
+    if (!out) return MTP_EINVAL;
+    int rc = validate(cfg, nullptr);
+    if (rc) return rc;
+    WsLayout w = ws_layout(*cfg);
+    out->weights_bytes = weight_layout(*cfg, nullptr, nullptr);
+    out->logq_bytes = (uint64_t)cfg->vocab * cfg->vocab * 4;
+    out->kv_bytes = kv_bytes(*cfg, w);
+    out->workspace_bytes = w.total;
+    return MTP_OK;
+}
+
+int mtp_weight_offset(const mtp_config* cfg, int tensor, int layer, uint64_t* offset_bytes, uint64_t* numel) {
+    int rc = validate(cfg, nullptr);
+    if (rc) return rc;
+    if (tensor < 0 || tensor >= MTP_T_COUNT) return MTP_EINVAL;
+    std::vector<uint64_t> g, l;
+    weight_layout(*cfg, &g, &l);
+    uint64_t off;
+    if (is_layer_tensor(tensor)) {
+        if (layer < 0 || layer >= cfg->n_layers) return MTP_EINVAL;
+        off = l[(size_t)layer * MTP_T_COUNT + tensor];
+    } else {
+        off = g[tensor];
+    }
+    if (offset_bytes) *offset_bytes = off;
+    if (numel) *numel = tensor_numel(*cfg, tensor);
+    return MTP_OK;
+}
+
+int mtp_create(const mtp_config* cfg, const mtp_buffers* bufs, void* hip_stream, mtp_ctx** out) {
+    if (!out || !bufs) return MTP_EINVAL;
+    *out = nullptr;
+    int rc = validate(cfg, nullptr);
+    if (rc) return rc;
+    if (!bufs->weights || !bufs->logq || !bufs->kv_pool || !bufs->workspace) return MTP_EINVAL;
+    auto aligned = [](const void* p) { return ((uintptr_t)p & 255) == 0; };
+    if (!aligned(bufs->weights) || !aligned(bufs->logq) || !aligned(bufs->kv_pool) || !aligned(bufs->workspace))
+        return MTP_EINVAL;
+    mtp_ctx* c = new (std::nothrow) mtp_ctx();
+    if (!c) return MTP_ENOMEM;
+    c->cfg = *cfg;
+    c->buf = *bufs;
+    c->stream = (hipStream_t)hip_stream;
+    c->ws = ws_layout(*cfg);
+    weight_layout(*cfg, &c->wglob, &c->wlay);
+    *out = c;
+    return MTP_OK;
+}
+
+int mtp_prefill(mtp_ctx* c, int B, const int32_t* phon, const int32_t* phon_len, const int32_t* ac,
+                const int32_t* ac_len) {
+    if (!c) return MTP_EINVAL;
+    const mtp_config& cf = c->cfg;
+    if (B < 1 || B > cf.max_batch) { c->err = "batch out of range"; return MTP_EINVAL; }
+    if (!phon_len || !ac_len || !ac) { c->err = "NULL prompt array"; return MTP_EINVAL; }
+    int64_t n_phon = 0, n_ac = 0;
+    for (int b = 0; b < B; ++b) {
+        if (phon_len[b] < 0 || ac_len[b] < 0 || phon_len[b] + ac_len[b] < 1 || phon_len[b] + ac_len[b] > cf.max_prompt) {
+            c->err = "prompt length out of range";
+            return MTP_EINVAL;
+        }
+        n_phon += phon_len[b];
+        n_ac += ac_len[b];
+    }
+    if (n_phon > 0 && !phon) { c->err = "NULL phoneme array"; return MTP_EINVAL; }
+    for (int64_t i = 0; i < n_phon; ++i)
+        if (phon[i] < 0 || phon[i] >= cf.n_phone) { c->err = "phoneme id out of range"; return MTP_EINVAL; }
+    for (int64_t i = 0; i < n_ac; ++i)
+        if (ac[i] < 0 || ac[i] >= cf.vocab - 1) { c->err = "acoustic id out of range"; return MTP_EINVAL; }
+    // KV pages: each sequence reserves prompt + max_new positions; pages are
+    // handed out round-robin from the top of the pool so that consecutive
+    // pages of a sequence are not adjacent in memory.
+    const int64_t maxp = c->ws.maxp;
+    std::vector<int> need(B);
+    int64_t total_pages = 0;
+    for (int b = 0; b < B; ++b) {
+        need[b] = (int)((phon_len[b] + ac_len[b] + (int64_t)cf.max_new + cf.page_size - 1) / cf.page_size);
+        total_pages += need[b];
+    }
+    if (total_pages > c->ws.num_pages) { c->err = "KV page pool exhausted"; return MTP_ENOMEM; }
+    c->h_btab.assign((size_t)B * maxp, 0);
+    int next = (int)c->ws.num_pages - 1;
+    for (int p = 0; p < maxp; ++p)
+        for (int b = 0; b < B; ++b)
+            if (p < need[b]) c->h_btab[(size_t)b * maxp + p] = next--;
+    // packed rows and attention tiles
+    c->h_ids.clear(); c->h_rows.clear(); c->h_tiles.clear(); c->h_last.assign(B, 0); c->h_state.assign(B, SeqState{});
+    int64_t op = 0, oa = 0;
+    for (int b = 0; b < B; ++b) {
+        const int len = phon_len[b] + ac_len[b];
+        const int row0 = (int)c->h_ids.size();
+        for (int i = 0; i < phon_len[b]; ++i) c->h_ids.push_back(phon[op++]);
+        for (int i = 0; i < ac_len[b]; ++i) c->h_ids.push_back(ac[oa++]);
+        for (int i = 0; i < len; ++i) c->h_rows.push_back(RowInfo{b, i});
+        for (int i0 = 0; i0 < len; i0 += MTP_ATTN_QT) c->h_tiles.push_back(make_int2(row0 + i0, std::min(MTP_ATTN_QT, len - i0)));
+        c->h_last[b] = row0 + len - 1;
+        SeqState s{};
+        s.ctx_len = len; s.pend_len = 0; s.gen = 0; s.done = 0; s.phon_len = phon_len[b]; s.prompt_len = len;
+        c->h_state[b] = s;
+    }
+    const int rows = (int)c->h_ids.size();
+    const int n_tiles = (int)c->h_tiles.size();
+    hipStream_t st = c->stream;
+    HIPCHK(c, hipMemcpyAsync(c->WS() + c->ws.ids, c->h_ids.data(), rows * 4, hipMemcpyHostToDevice, st), "upload ids");
+    HIPCHK(c, hipMemcpyAsync(c->WS() + c->ws.rows, c->h_rows.data(), rows * sizeof(RowInfo), hipMemcpyHostToDevice, st), "upload rows");
+    HIPCHK(c, hipMemcpyAsync(c->WS() + c->ws.tiles, c->h_tiles.data(), n_tiles * sizeof(int2), hipMemcpyHostToDevice, st), "upload tiles");
+    HIPCHK(c, hipMemcpyAsync(c->WS() + c->ws.last_row, c->h_last.data(), B * 4, hipMemcpyHostToDevice, st), "upload last rows");
+    HIPCHK(c, hipMemcpyAsync(c->WS() + c->ws.state, c->h_state.data(), B * sizeof(SeqState), hipMemcpyHostToDevice, st), "upload state");
+    HIPCHK(c, hipMemcpyAsync(c->WS() + c->ws.btab, c->h_btab.data(), c->h_btab.size() * 4, hipMemcpyHostToDevice, st), "upload block table");
+    HIPCHK(c, hipStreamSynchronize(st), "prefill upload sync");
+
+    const int d = cf.d_model, dt = cf.dtype;
+    EmbedArgs e{};
+    e.dtype = dt; e.mode = 1; e.n_rows = rows; e.Q = 0; e.st = c->ws_ptr<SeqState>(c->ws.state);
+    e.ids = c->ws_ptr<int32_t>(c->ws.ids); e.rows = c->ws_ptr<RowInfo>(c->ws.rows); e.tiles = c->ws_ptr<int2>(c->ws.tiles);
+    e.emb_phone = c->wt(MTP_T_EMB_PHONE); e.emb_ac = c->wt(MTP_T_EMB_AC); e.pos = c->wt(MTP_T_POS);
+    e.ln_g = (const float*)c->lt(0, MTP_T_LN1_G); e.ln_b = (const float*)c->lt(0, MTP_T_LN1_B);
+    e.d = d; e.h = c->ws_ptr<float>(c->ws.h); e.u = c->WS() + c->ws.u;
+    HIPCHK(c, embed_ln(st, e), "prefill embed");
+    for (int l = 0; l < cf.n_layers; ++l) {
+        int rc = run_layer(c, l, rows, n_tiles, MTP_ATTN_QT, 1 << 30, 1, false);
+        if (rc) return rc;
+    }
+    FinalArgs f{};
+    f.dtype = dt; f.B = B; f.d = d; f.mode = 1; f.Q = 0; f.st = c->ws_ptr<SeqState>(c->ws.state);
+    f.last_row = c->ws_ptr<int32_t>(c->ws.last_row); f.h = c->ws_ptr<float>(c->ws.h); f.hz = c->ws_ptr<float>(c->ws.hz);
+    f.z = nullptr;
+    HIPCHK(c, final_ln(st, f), "prefill last rows");
+
+    // decode attention split plan: enough (sequence, head, split) workgroups
+    // to fill the chip at the longest context this batch can reach
+    int64_t max_ctx = 0;
+    for (int b = 0; b < B; ++b) max_ctx = std::max<int64_t>(max_ctx, phon_len[b] + ac_len[b] + (int64_t)cf.max_new);
+    const int64_t bh = (int64_t)B * cf.n_heads;
+    const int64_t want = std::max<int64_t>(1, (2048 + bh - 1) / bh);
+    int64_t sl = (max_ctx + want - 1) / want;
+    sl = std::max<int64_t>(64, (sl + 63) / 64 * 64);
+    c->split_len = (int)sl;
+    c->n_splits = (int)((max_ctx + sl - 1) / sl);
+    if (c->n_splits > c->ws.max_splits) { c->err = "attention split plan exceeds workspace"; return MTP_ENOMEM; }
+
+    c->B = B;
+    c->q_pad = 0;
+    c->prefilled = true;
+    c->n_pre_rows = rows;
+    c->n_pre_tiles = n_tiles;
+    return MTP_OK;
+}
+
+int mtp_decode_step_async(mtp_ctx* c, int K, int top_k, int32_t* d_tokens, int32_t* d_count) {
+    int rc = step_common(c, K, top_k);
+    if (rc) return rc;
+    if (d_tokens)
+        HIPCHK(c, hipMemcpyAsync(d_tokens, c->WS() + c->ws.out_tok, (size_t)c->B * K * 4, hipMemcpyDeviceToDevice, c->stream), "copy tokens");
+    if (d_count)
+        HIPCHK(c, hipMemcpyAsync(d_count, c->WS() + c->ws.out_cnt, (size_t)c->B * 4, hipMemcpyDeviceToDevice, c->stream), "copy counts");
+    return MTP_OK;
+}
+
+int mtp_decode_step(mtp_ctx* c, int K, int top_k, int32_t* out_tokens, int32_t* out_count) {
+    if (!out_tokens || !out_count) { if (c) c->err = "NULL output"; return MTP_EINVAL; }
+    int rc = step_common(c, K, top_k);
+    if (rc) return rc;
+    HIPCHK(c, hipMemcpyAsync(out_tokens, c->WS() + c->ws.out_tok, (size_t)c->B * K * 4, hipMemcpyDeviceToHost, c->stream), "tokens to host");
+    HIPCHK(c, hipMemcpyAsync(out_count, c->WS() + c->ws.out_cnt, (size_t)c->B * 4, hipMemcpyDeviceToHost, c->stream), "counts to host");
+    HIPCHK(c, hipStreamSynchronize(c->stream), "step sync");
+    return MTP_OK;
+}
+
+int mtp_get_logits(mtp_ctx* c, float* logits) {
+    if (!c) return MTP_EINVAL;
+    if (!c->last_K) { c->err = "no decode step yet"; return MTP_ESTATE; }
+    if (logits)
+        HIPCHK(c, hipMemcpyAsync(logits, c->WS() + c->ws.logits, (size_t)c->B * c->last_K * c->cfg.vocab * 4, hipMemcpyDeviceToHost, c->stream), "logits to host");
+    HIPCHK(c, hipStreamSynchronize(c->stream), "sync");
+    return MTP_OK;
+}
+
+int mtp_get_lattice(mtp_ctx* c, int32_t* cand, float* ehat, float* delta, int32_t* psi, int32_t* slots) {
+    if (!c) return MTP_EINVAL;
+    if (!c->last_K) { c->err = "no decode step yet"; return MTP_ESTATE; }
+    const size_t n = (size_t)c->B * c->last_K * c->last_topk * 4;
+    hipStream_t st = c->stream;
+    if (cand) HIPCHK(c, hipMemcpyAsync(cand, c->WS() + c->ws.cand, n, hipMemcpyDeviceToHost, st), "cand");
+    if (ehat) HIPCHK(c, hipMemcpyAsync(ehat, c->WS() + c->ws.ehat, n, hipMemcpyDeviceToHost, st), "ehat");
+    if (delta) HIPCHK(c, hipMemcpyAsync(delta, c->WS() + c->ws.delta, n, hipMemcpyDeviceToHost, st), "delta");
+    if (psi) HIPCHK(c, hipMemcpyAsync(psi, c->WS() + c->ws.psi, n, hipMemcpyDeviceToHost, st), "psi");
+    if (slots) HIPCHK(c, hipMemcpyAsync(slots, c->WS() + c->ws.slots, (size_t)c->B * c->last_K * 4, hipMemcpyDeviceToHost, st), "slots");
+    HIPCHK(c, hipStreamSynchronize(st), "sync");
+    return MTP_OK;
+}
+
+int mtp_get_seq_state(mtp_ctx* c, int32_t* ctx_len, int32_t* pend_len, int32_t* gen, int32_t* done) {
+    if (!c) return MTP_EINVAL;
+    if (!c->prefilled) { c->err = "no prefill yet"; return MTP_ESTATE; }
+    std::vector<SeqState> s(c->B);
+    HIPCHK(c, hipMemcpyAsync(s.data(), c->WS() + c->ws.state, c->B * sizeof(SeqState), hipMemcpyDeviceToHost, c->stream), "state to host");
+    HIPCHK(c, hipStreamSynchronize(c->stream), "sync");
+    for (int b = 0; b < c->B; ++b) {
+        if (ctx_len) ctx_len[b] = s[b].ctx_len;
+        if (pend_len) pend_len[b] = s[b].pend_len;
+        if (gen) gen[b] = s[b].gen;
+        if (done) done[b] = s[b].done;
+    }
+    return MTP_OK;
+}
+
+int mtp_get_tokens(mtp_ctx* c, int32_t* tokens) {
+    if (!c || !tokens) return MTP_EINVAL;
+    if (!c->prefilled) { c->err = "no prefill yet"; return MTP_ESTATE; }
+    HIPCHK(c, hipMemcpyAsync(tokens, c->WS() + c->ws.hist, (size_t)c->B * c->cfg.max_new * 4, hipMemcpyDeviceToHost, c->stream), "history to host");
+    HIPCHK(c, hipStreamSynchronize(c->stream), "sync");
+    return MTP_OK;
+}
+
+int mtp_profile(mtp_ctx* c, int kclass, int enable) {
+    if (!c) return MTP_EINVAL;
+    if (kclass < MTP_KCLASS_GEMM_FFN1 || kclass > MTP_KCLASS_HEADS) { c->err = "unknown kernel class"; return MTP_EINVAL; }
+    c->prof_class = enable ? kclass : 0;
+    c->prof_used = 0;
+    return MTP_OK;
+}
+
+int mtp_profile_read(mtp_ctx* c, double* total_ms, int64_t* launches) {
+    if (!c) return MTP_EINVAL;
+    HIPCHK(c, hipStreamSynchronize(c->stream), "sync");
+    double tot = 0;
+    for (size_t i = 0; i < c->prof_used; ++i) {
+        float ms = 0;
+        HIPCHK(c, hipEventElapsedTime(&ms, c->prof_events[i].first, c->prof_events[i].second), "event time");
+        tot += ms;
+    }
+    if (total_ms) *total_ms = tot;
+    if (launches) *launches = (int64_t)c->prof_used;
+    c->prof_used = 0;
+    return MTP_OK;
+}
+
+int mtp_reset(mtp_ctx* c) {
+    if (!c) return MTP_EINVAL;
+    c->prefilled = false;
+    c->B = 0;
+    c->q_pad = 0;
+    c->last_K = 0;
+    return MTP_OK;
+}
+
+void mtp_destroy(mtp_ctx* c) {
+    if (!c) return;
+    if (c->stream) (void)hipStreamSynchronize(c->stream);
+    for (auto& kv : c->graphs) (void)hipGraphExecDestroy(kv.second);
+    for (auto& p : c->prof_events) {
+        (void)hipEventDestroy(p.first);
+        (void)hipEventDestroy(p.second);
+    }
+    delete c;
+}
+
+const char* mtp_last_error(const mtp_ctx* c) { return c ? c->err.c_str() : "NULL context"; }
+
+}  // extern "C"

@@ -1,0 +1,82 @@
+// Shared device-side definitions for the MTP decode kernels (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#define MTP_HEAD_DIM 64
+#define MTP_MAX_HEADS_K 8      // prediction heads a step may use
+#define MTP_MAX_TOPK 32
+#define MTP_ATTN_QT 8          // query rows per attention tile
+#define MTP_SPLITK_MAX 8
+
+typedef uint16_t bf16_t;  // raw bfloat16 bits
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+// Per-sequence decode state, device resident (int32 fields).
+struct SeqState {
+    int32_t ctx_len;     // tokens whose K/V are in the cache
+    int32_t pend_len;    // accepted tokens not yet run through the trunk
+    int32_t gen;         // tokens emitted so far
+    int32_t done;        // 1 once EOS was emitted or the budget is used
+    int32_t phon_len;    // phoneme prefix length
+    int32_t prompt_len;  // phonemes + acoustic prompt
+    int32_t steps;       // decode steps taken
+    int32_t pad0;
+    int32_t pend_ids[MTP_MAX_HEADS_K];
+};
+static_assert(sizeof(SeqState) == 64, "SeqState layout");
+
+// Row metadata of a packed activation row: sequence and absolute position
+// (pos < 0 marks a padding row that must not touch the KV cache).
+struct RowInfo {
+    int32_t seq;
+    int32_t pos;
+};
+
+__device__ __forceinline__ float bf16_to_f32(bf16_t b) {
+    return __uint_as_float(((uint32_t)b) << 16);
+}
+
+// Round-to-nearest-even float -> bfloat16 bits (finite inputs).
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return (bf16_t)(u >> 16);
+}
+
+template <typename T> struct ActIO;
+template <> struct ActIO<float> {
+    __device__ static __forceinline__ float load(const float* p) { return *p; }
+    __device__ static __forceinline__ void store(float* p, float v) { *p = v; }
+};
+template <> struct ActIO<bf16_t> {
+    __device__ static __forceinline__ float load(const bf16_t* p) { return bf16_to_f32(*p); }
+    __device__ static __forceinline__ void store(bf16_t* p, float v) { *p = f32_to_bf16(v); }
+};
+
+// Exact GELU, x * Phi(x).
+__device__ __forceinline__ float gelu_erf(float x) {
+    return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f));
+}
+
+// Paged KV addressing.  Pool layout: [layer][page][kv(0=K,1=V)][head][slot][64].
+struct KVView {
+    void* pool;
+    const int32_t* block_table;  // [batch][max_pages_per_seq]
+    int32_t max_pages_per_seq;
+    int32_t num_pages;
+    int32_t page_size;           // power of two
+    int32_t page_shift;
+    int32_t n_heads;
+    int32_t layer;
+
+    __device__ __forceinline__ size_t offset(int seq, int pos, int kv, int head) const {
+        int page = block_table[(size_t)seq * max_pages_per_seq + (pos >> page_shift)];
+        int slot = pos & (page_size - 1);
+        size_t base = (((size_t)layer * num_pages + page) * 2 + kv) * (size_t)n_heads;
+        return ((base + head) * page_size + slot) * MTP_HEAD_DIM;
+    }
+};

@@ -1,0 +1,105 @@
+// Host-side launchers of the decode kernels (internal to libmtp).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "common.h"
+
+namespace mtp {
+
+enum EpiKind { EPI_QKV = 0, EPI_GELU = 1, EPI_PARTIAL = 2, EPI_LOGITS = 3 };
+
+struct GemmArgs {
+    int dtype;            // 0 fp32, 1 bf16 (both X and W)
+    int epi;              // EpiKind
+    const void* X; int ldx; int M;
+    const void* W; int N; int K;
+    int splits;           // split-K factor (EPI_PARTIAL only)
+    // epilogue operands
+    const float* bias;
+    void* out; int ldo; size_t split_stride;
+    float* q; const RowInfo* rows; KVView kv; int d;
+};
+
+hipError_t gemm(hipStream_t st, const GemmArgs& a);
+int gemm_split_granule(int dtype, int M);
+
+struct AttnArgs {
+    int dtype;                 // KV / output element type: 0 fp32, 1 bf16
+    const float* q; int ldq;   // [rows][d]
+    const RowInfo* rows;
+    const int2* tiles;         // (row0, nrows) per tile
+    int n_tiles;
+    int qt;                    // rows per tile (1, 2, 4 or 8)
+    KVView kv;
+    int split_len;             // keys per split (multiple of 32)
+    int n_splits;
+    void* out; int ldo;        // [rows][d] attention output (act type)
+    float* part;               // split partials when n_splits > 1
+};
+hipError_t attention(hipStream_t st, const AttnArgs& a);
+
+// Row embedding (+ first LayerNorm).  mode 0: decode rows derived from the
+// sequence state (Q rows per sequence); mode 1: prefill rows given by
+// ids/rows.
+struct EmbedArgs {
+    int dtype;
+    int mode;
+    int n_rows;
+    int Q;
+    const SeqState* st;
+    const int32_t* ids;
+    RowInfo* rows;
+    int2* tiles;
+    const void* emb_phone; const void* emb_ac; const void* pos;
+    const float* ln_g; const float* ln_b;
+    int d;
+    float* h;
+    void* u;
+};
+hipError_t embed_ln(hipStream_t st, const EmbedArgs& a);
+
+// h[r] += sum_s part[s][r] + bias; optionally u[r] = LN(h[r]).
+struct ResidArgs {
+    int dtype;
+    int n_rows; int d;
+    float* h;
+    const float* part; int n_split; size_t split_stride;
+    const float* bias;
+    const float* ln_g; const float* ln_b;   // NULL: no LayerNorm
+    void* u;
+};
+hipError_t resid_ln(hipStream_t st, const ResidArgs& a);
+
+// hz[b] = h[src row of b]; z[b] = LN_f(hz[b]).
+struct FinalArgs {
+    int dtype;
+    int B; int d;
+    int mode;                  // 0 decode (Q rows per seq, last pending row), 1 prefill (last_row[])
+    int Q;
+    const SeqState* st;
+    const int32_t* last_row;
+    const float* h;
+    float* hz;
+    const float* ln_g; const float* ln_b;
+    void* z;                   // NULL: copy only
+};
+hipError_t final_ln(hipStream_t st, const FinalArgs& a);
+
+struct SelectArgs {
+    int B; int K; int top_k; int V; int eos_id; int eos_min; int max_new;
+    int Q;                     // pending rows per sequence this step (0 right after prefill)
+    const float* logits;       // [B][ld_logits], head t at t*V
+    int ld_logits;
+    const float* logq;         // [V][V]
+    SeqState* st;
+    int32_t* cand; float* ehat; float* delta; int32_t* psi; int32_t* slots;  // [B][K][top_k] / [B][K]
+    int32_t* out_tokens;       // [B][K]
+    int32_t* out_count;        // [B]
+    int32_t* hist; int hist_ld;  // [B][max_new]
+};
+hipError_t topk(hipStream_t st, const SelectArgs& a);
+hipError_t viterbi_accept(hipStream_t st, const SelectArgs& a);
+
+}  // namespace mtp

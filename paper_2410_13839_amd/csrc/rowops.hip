@@ -1,0 +1,171 @@
+// Row-wise kernels of the trunk: embedding gather, residual reduction and
+// LayerNorm.  One workgroup per row; d_model <= 2048.
+#include "common.h"
+#include "launch.h"
+
+namespace mtp {
+
+namespace {
+constexpr int MAXC = 8;   // columns per thread (d <= 2048)
+
+template <typename T> __device__ __forceinline__ float ld(const T* p);
+template <> __device__ __forceinline__ float ld<float>(const float* p) { return *p; }
+template <> __device__ __forceinline__ float ld<bf16_t>(const bf16_t* p) { return bf16_to_f32(*p); }
+
+__device__ __forceinline__ float block_sum(float v, float* red) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    __syncthreads();
+    if (lane == 0) red[wave] = v;
+    __syncthreads();
+    return (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+// LayerNorm of the row held in x[0..nc) (columns c = tid + 256 j), eps 1e-5.
+template <typename OutT>
+__device__ __forceinline__ void layer_norm_store(const float (&x)[MAXC], int d, const float* g, const float* b,
+                                                 OutT* out, float* red) {
+    const int tid = threadIdx.x;
+    float s = 0.f;
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j) {
+        int c = tid + 256 * j;
+        if (c < d) s += x[j];
+    }
+    const float mean = block_sum(s, red) / (float)d;
+    float v = 0.f;
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j) {
+        int c = tid + 256 * j;
+        if (c < d) { float t = x[j] - mean; v = fmaf(t, t, v); }
+    }
+    const float var = block_sum(v, red) / (float)d;
+    const float rstd = rsqrtf(var + 1e-5f);
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j) {
+        int c = tid + 256 * j;
+        if (c < d) ActIO<OutT>::store(out + c, (x[j] - mean) * rstd * g[c] + b[c]);
+    }
+}
+}  // namespace
+
+template <typename WT>
+__global__ __launch_bounds__(256) void embed_ln_kernel(EmbedArgs a) {
+    __shared__ float red[4];
+    const int r = blockIdx.x, tid = threadIdx.x;
+    int seq, pos, tok;
+    if (a.mode == 0) {
+        seq = r / a.Q;
+        const int i = r - seq * a.Q;
+        const SeqState& s = a.st[seq];
+        const bool valid = i < s.pend_len;
+        pos = valid ? s.ctx_len + i : -1;
+        tok = valid ? s.pend_ids[i] : 0;
+        if (tid == 0) {
+            a.rows[r] = RowInfo{seq, pos};
+            if (i == 0) a.tiles[seq] = make_int2(r, s.pend_len);
+        }
+    } else {
+        RowInfo ri = a.rows[r];
+        seq = ri.seq;
+        pos = ri.pos;
+        tok = a.ids[r];
+    }
+    using ActT = WT;
+    float* h = a.h + (size_t)r * a.d;
+    ActT* u = reinterpret_cast<ActT*>(a.u) + (size_t)r * a.d;
+    if (pos < 0) {
+        for (int c = tid; c < a.d; c += 256) {
+            h[c] = 0.f;
+            ActIO<ActT>::store(u + c, 0.f);
+        }
+        return;
+    }
+    const WT* table = (pos < a.st[seq].phon_len) ? reinterpret_cast<const WT*>(a.emb_phone)
+                                                  : reinterpret_cast<const WT*>(a.emb_ac);
+    const WT* erow = table + (size_t)tok * a.d;
+    const WT* prow = reinterpret_cast<const WT*>(a.pos) + (size_t)pos * a.d;
+    float x[MAXC];
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j) {
+        int c = tid + 256 * j;
+        x[j] = 0.f;
+        if (c < a.d) {
+            x[j] = ld<WT>(erow + c) + ld<WT>(prow + c);
+            h[c] = x[j];
+        }
+    }
+    layer_norm_store<ActT>(x, a.d, a.ln_g, a.ln_b, u, red);
+}
+
+template <typename ActT>
+__global__ __launch_bounds__(256) void resid_ln_kernel(ResidArgs a) {
+    __shared__ float red[4];
+    const int r = blockIdx.x, tid = threadIdx.x;
+    float* h = a.h + (size_t)r * a.d;
+    float x[MAXC];
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j) {
+        int c = tid + 256 * j;
+        x[j] = 0.f;
+        if (c < a.d) {
+            float s = 0.f;
+            for (int sp = 0; sp < a.n_split; ++sp) s += a.part[sp * a.split_stride + (size_t)r * a.d + c];
+            x[j] = h[c] + (s + a.bias[c]);
+            h[c] = x[j];
+        }
+    }
+    if (a.ln_g) layer_norm_store<ActT>(x, a.d, a.ln_g, a.ln_b, reinterpret_cast<ActT*>(a.u) + (size_t)r * a.d, red);
+}
+
+template <typename ActT>
+__global__ __launch_bounds__(256) void final_ln_kernel(FinalArgs a) {
+    __shared__ float red[4];
+    const int b = blockIdx.x, tid = threadIdx.x;
+    int src = -1;
+    if (a.mode == 0) {
+        const int pl = a.st[b].pend_len;
+        if (a.Q > 0 && pl > 0) src = b * a.Q + pl - 1;
+    } else {
+        src = a.last_row[b];
+    }
+    float* hz = a.hz + (size_t)b * a.d;
+    float x[MAXC];
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j) {
+        int c = tid + 256 * j;
+        x[j] = 0.f;
+        if (c < a.d) {
+            if (src >= 0) {
+                x[j] = a.h[(size_t)src * a.d + c];
+                hz[c] = x[j];
+            } else {
+                x[j] = hz[c];
+            }
+        }
+    }
+    if (a.z) layer_norm_store<ActT>(x, a.d, a.ln_g, a.ln_b, reinterpret_cast<ActT*>(a.z) + (size_t)b * a.d, red);
+}
+
+hipError_t embed_ln(hipStream_t st, const EmbedArgs& a) {
+    if (a.n_rows <= 0) return hipSuccess;
+    if (a.dtype == 1) hipLaunchKernelGGL(embed_ln_kernel<bf16_t>, dim3(a.n_rows), dim3(256), 0, st, a);
+    else hipLaunchKernelGGL(embed_ln_kernel<float>, dim3(a.n_rows), dim3(256), 0, st, a);
+    return hipGetLastError();
+}
+
+hipError_t resid_ln(hipStream_t st, const ResidArgs& a) {
+    if (a.n_rows <= 0) return hipSuccess;
+    if (a.dtype == 1) hipLaunchKernelGGL(resid_ln_kernel<bf16_t>, dim3(a.n_rows), dim3(256), 0, st, a);
+    else hipLaunchKernelGGL(resid_ln_kernel<float>, dim3(a.n_rows), dim3(256), 0, st, a);
+    return hipGetLastError();
+}
+
+hipError_t final_ln(hipStream_t st, const FinalArgs& a) {
+    if (a.dtype == 1) hipLaunchKernelGGL(final_ln_kernel<bf16_t>, dim3(a.B), dim3(256), 0, st, a);
+    else hipLaunchKernelGGL(final_ln_kernel<float>, dim3(a.B), dim3(256), 0, st, a);
+    return hipGetLastError();
+}
+
+}  // namespace mtp

@@ -1,0 +1,164 @@
+// Selection kernels: EOS mask + per-head top_k, then the Viterbi lattice and
+// the accept rule (paper Sec. 3.3, Fig. 2).
+//
+// Every decision is made with the same float32 operations, in the same
+// association, as the plain definition: e_hat = l[c] - l[c_0];
+// delta_t(j) = max_i (delta_{t-1}(i) + logQ[c_{t-1,i}][c_{t,j}]) + e_hat_t(j),
+// with the lowest index winning ties in top_k (token id), in the predecessor
+// scan and in the final argmax (slot).  The (value, index) max-reductions use
+// a total order, so the shuffle tree cannot change their result.
+#include <limits.h>
+#include <math.h>
+
+#include "common.h"
+#include "launch.h"
+
+namespace mtp {
+
+namespace {
+constexpr int PER_LANE = 17;   // ceil(1025 / 64): logits held per lane
+
+__device__ __forceinline__ bool better(float va, int ia, float vb, int ib) {
+    return va > vb || (va == vb && ia < ib);
+}
+}  // namespace
+
+// One wavefront per (sequence, head).
+__global__ __launch_bounds__(64) void topk_kernel(SelectArgs a) {
+    const int bt = blockIdx.x;
+    const int b = bt / a.K, t = bt - b * a.K;
+    const int lane = threadIdx.x;
+    const float* lg = a.logits + (size_t)b * a.ld_logits + (size_t)t * a.V;
+    const bool mask_eos = (a.st[b].gen + t) < a.eos_min;
+    float v[PER_LANE];
+#pragma unroll
+    for (int j = 0; j < PER_LANE; ++j) {
+        const int idx = lane + 64 * j;
+        float x = (idx < a.V) ? lg[idx] : -INFINITY;
+        if (idx == a.eos_id && mask_eos) x = -INFINITY;
+        v[j] = x;
+    }
+    uint32_t taken = 0;
+    float top0 = 0.f;
+    const size_t out = ((size_t)b * a.K + t) * a.top_k;
+    for (int r = 0; r < a.top_k; ++r) {
+        float bv = -INFINITY;
+        int bi = INT_MAX;
+#pragma unroll
+        for (int j = 0; j < PER_LANE; ++j) {
+            const int idx = lane + 64 * j;
+            if (idx < a.V && !((taken >> j) & 1u) && better(v[j], idx, bv, bi)) {
+                bv = v[j];
+                bi = idx;
+            }
+        }
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) {
+            const float ov = __shfl_xor(bv, o);
+            const int oi = __shfl_xor(bi, o);
+            if (better(ov, oi, bv, bi)) {
+                bv = ov;
+                bi = oi;
+            }
+        }
+        if ((bi & 63) == lane) taken |= 1u << (bi >> 6);
+        if (r == 0) top0 = bv;
+        if (lane == 0) {
+            a.cand[out + r] = bi;
+            a.ehat[out + r] = bv - top0;
+        }
+    }
+}
+
+// One wavefront per sequence: lane j owns candidate slot j.
+__global__ __launch_bounds__(64) void viterbi_accept_kernel(SelectArgs a) {
+    const int b = blockIdx.x, j = threadIdx.x;
+    const int K = a.K, k = a.top_k, V = a.V;
+    __shared__ int s_psi[MTP_MAX_HEADS_K][MTP_MAX_TOPK];
+    const size_t base = (size_t)b * K * k;
+    const int32_t* cand = a.cand + base;
+    const float* ehat = a.ehat + base;
+
+    float delta = (j < k) ? ehat[j] : -INFINITY;
+    if (j < k) {
+        a.delta[base + j] = delta;
+        a.psi[base + j] = 0;
+        s_psi[0][j] = 0;
+    }
+    for (int t = 1; t < K; ++t) {
+        const int cj = (j < k) ? cand[t * k + j] : 0;
+        float best = 0.f;
+        int arg = 0;
+        for (int i = 0; i < k; ++i) {
+            const float di = __shfl(delta, i);
+            const int ci = cand[(t - 1) * k + i];
+            const float s = di + a.logq[(size_t)ci * V + cj];
+            if (i == 0 || s > best) {
+                best = s;
+                arg = i;
+            }
+        }
+        delta = (j < k) ? best + ehat[t * k + j] : -INFINITY;
+        if (j < k) {
+            a.delta[base + t * k + j] = delta;
+            a.psi[base + t * k + j] = arg;
+            s_psi[t][j] = arg;
+        }
+    }
+    int last = 0;
+    float bestd = __shfl(delta, 0);
+    for (int i = 1; i < k; ++i) {
+        const float di = __shfl(delta, i);
+        if (di > bestd) {
+            bestd = di;
+            last = i;
+        }
+    }
+    __syncthreads();
+    if (j != 0) return;
+
+    int slots[MTP_MAX_HEADS_K], toks[MTP_MAX_HEADS_K];
+    slots[K - 1] = last;
+    for (int t = K - 1; t > 0; --t) slots[t - 1] = s_psi[t][slots[t]];
+    for (int t = 0; t < K; ++t) {
+        toks[t] = cand[t * k + slots[t]];
+        a.slots[(size_t)b * K + t] = slots[t];
+    }
+
+    SeqState s = a.st[b];
+    int n = 0;
+    bool done = s.done != 0;
+    if (!done) {
+        n = min(K, a.max_new - s.gen);
+        for (int p = 0; p < n; ++p) {
+            if (toks[p] == a.eos_id) {
+                n = p + 1;
+                done = true;
+                break;
+            }
+        }
+        if (s.gen + n >= a.max_new) done = true;
+    }
+    for (int t = 0; t < K; ++t) a.out_tokens[(size_t)b * K + t] = (t < n) ? toks[t] : -1;
+    a.out_count[b] = n;
+    for (int t = 0; t < n; ++t) a.hist[(size_t)b * a.hist_ld + s.gen + t] = toks[t];
+    s.ctx_len += s.pend_len;
+    s.gen += n;
+    s.done = done ? 1 : 0;
+    s.pend_len = done ? 0 : n;
+    for (int t = 0; t < n && t < MTP_MAX_HEADS_K; ++t) s.pend_ids[t] = toks[t];
+    s.steps += 1;
+    a.st[b] = s;
+}
+
+hipError_t topk(hipStream_t st, const SelectArgs& a) {
+    hipLaunchKernelGGL(topk_kernel, dim3(a.B * a.K), dim3(64), 0, st, a);
+    return hipGetLastError();
+}
+
+hipError_t viterbi_accept(hipStream_t st, const SelectArgs& a) {
+    hipLaunchKernelGGL(viterbi_accept_kernel, dim3(a.B), dim3(64), 0, st, a);
+    return hipGetLastError();
+}
+
+}  // namespace mtp

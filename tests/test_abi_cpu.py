@@ -1,0 +1,115 @@
+"""The C ABI library loads, exports every call include/mtp.h declares, and
+rejects bad arguments before touching the GPU (no compute calls here)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mtp.h")
+
+
+def _declared():
+    src = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:int|void|const char\s*\*)\s*(mtp_\w+)\s*\(", src, re.M)))
+
+
+def test_library_exports_every_declared_call():
+    from paper_2410_13839_amd import binding
+    lib = ctypes.CDLL(binding.LIB_PATH)
+    names = _declared()
+    assert len(names) >= 15
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sorted(binding.EXPORTED) == names
+
+
+def _cfg(**kw):
+    from paper_2410_13839_amd import binding as b
+    from paper_2410_13839_amd.workloads import WORKLOADS
+    wl = WORKLOADS["valle_k4"]
+    cfg = b.make_config(wl.model, 1, wl.max_prompt, wl.max_new, wl.eos_min)
+    for k, v in kw.items():
+        setattr(cfg, k, v)
+    return cfg
+
+
+@pytest.mark.parametrize("field,value", [("d_model", 1000), ("n_heads", 15), ("k_heads", 9), ("k_heads", 0),
+                                         ("topk_max", 33), ("page_size", 12), ("dtype", 7), ("vocab", 5000),
+                                         ("max_new", 5000), ("eos_id", 1025), ("max_batch", 0)])
+def test_query_sizes_rejects_bad_configs(field, value):
+    from paper_2410_13839_amd import binding as b
+    with pytest.raises(b.MTPError) as e:
+        b.mtp_query_sizes(_cfg(**{field: value}))
+    assert e.value.code == b.MTP_EINVAL
+
+
+def test_weight_layout_is_aligned_and_disjoint():
+    from paper_2410_13839_amd import binding as b
+    cfg = _cfg()
+    spans = []
+    for t in range(b.MTP_T_COUNT):
+        layers = range(cfg.n_layers) if b.MTP_T_LN1_G <= t <= b.MTP_T_B_2 else [0]
+        for l in layers:
+            off, n = b.mtp_weight_offset(cfg, t, l)
+            assert off % 256 == 0
+            elt = 2 if t in b._MATRICES else 4
+            spans.append((off, off + n * elt))
+    spans.sort()
+    for (a0, a1), (b0, b1) in zip(spans, spans[1:]):
+        assert a1 <= b0
+    sz = b.mtp_query_sizes(cfg)
+    assert spans[-1][1] <= sz.weights_bytes
+    # 12 x (3d^2 + d^2 + 2 d f) + tables + 8 heads x V x d, bf16
+    d, f, V = 1024, 4096, 1025
+    mats = 12 * (4 * d * d + 2 * d * f) + (512 + V + 4096) * d + 8 * V * d
+    assert mats * 2 <= sz.weights_bytes < mats * 2 + 4 * 1024 * 1024
+    assert sz.logq_bytes == V * V * 4
+
+
+def test_calls_validate_before_gpu_work():
+    from paper_2410_13839_amd import binding as b
+    cfg = _cfg()
+    with pytest.raises(b.MTPError):
+        b.mtp_create(cfg, b.mtp_buffers(256, 512, 1024, 100), 0)   # misaligned workspace
+    ctx = b.mtp_create(cfg, b.mtp_buffers(256, 512, 1024, 2048), 0)
+    try:
+        with pytest.raises(b.MTPError) as e:
+            b.mtp_decode_step(ctx, 1, 4, 4)
+        assert e.value.code == b.MTP_ESTATE
+        with pytest.raises(b.MTPError) as e:       # prompt too long
+            b.mtp_prefill(ctx, [np.zeros(100, np.int32)], [np.zeros(cfg.max_prompt, np.int32)])
+        assert e.value.code == b.MTP_EINVAL
+        with pytest.raises(b.MTPError) as e:       # batch above max_batch
+            b.mtp_prefill(ctx, [np.zeros(1, np.int32)] * 2, [np.zeros(3, np.int32)] * 2)
+        assert e.value.code == b.MTP_EINVAL
+        with pytest.raises(b.MTPError) as e:       # acoustic id 1024 (EOS) is not a prompt token
+            b.mtp_prefill(ctx, [np.zeros(1, np.int32)], [np.full(3, 1024, np.int32)])
+        assert e.value.code == b.MTP_EINVAL
+        with pytest.raises(b.MTPError) as e:       # phoneme id out of range
+            b.mtp_prefill(ctx, [np.full(2, 512, np.int32)], [np.zeros(3, np.int32)])
+        assert e.value.code == b.MTP_EINVAL
+        with pytest.raises(b.MTPError) as e:
+            b.mtp_profile(ctx, 99, True)
+        assert e.value.code == b.MTP_EINVAL
+    finally:
+        b.mtp_destroy(ctx)
+
+
+def test_kv_pool_exhaustion_is_reported():
+    from paper_2410_13839_amd import binding as b
+    cfg = _cfg(num_pages=10)
+    ctx = b.mtp_create(cfg, b.mtp_buffers(256, 512, 1024, 2048), 0)
+    try:
+        with pytest.raises(b.MTPError) as e:
+            b.mtp_prefill(ctx, [np.zeros(10, np.int32)], [np.zeros(10, np.int32)])
+        assert e.value.code == b.MTP_ENOMEM
+    finally:
+        b.mtp_destroy(ctx)
+
+
+def test_strerror():
+    from paper_2410_13839_amd import binding as b
+    assert b.mtp_strerror(b.MTP_ENOMEM).startswith("KV")
