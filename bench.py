@@ -1,0 +1,246 @@
+"""Decode throughput of the MTP + Viterbi path on one MI355X.
+
+A step is one decode step of the whole hot path (trunk over the pending
+chunk and the paged KV cache, final LN, K head projections, EOS mask +
+top_k, Viterbi lattice, accept) for the whole batch.  Workload: the
+12-layer d1024 bf16 VALL-E-shaped decoder, K=4 heads, top_k=4, batch 1,
+prompt 100 phonemes + 225 acoustic tokens, up to 750 generated tokens (EOS
+allowed from index 600).  Inputs are seeded synthetic (weights N(0, 0.02),
+synthetic transition table, uniform prompt ids).
+
+Prints one JSON line.  `value` is emitted codec tokens per second over the
+timed decode steps (prefill excluded, inputs resident in HBM).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+
+
+def _parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=188)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="valle_k4")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-secondary", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--copy-probe", action="store_true", help="also run a 256 MiB device copy (PMC calibration)")
+    return ap.parse_args()
+
+
+def _steps_per_generation(wl):
+    return -(-wl.max_new // wl.K)
+
+
+def time_decode(sess, wl, prompts, steps, warmup, torch):
+    """Warm up, then time exactly `steps` decode steps (prefills in between
+    generations are outside the timed intervals).  Returns (ms, tokens)."""
+    per_gen = _steps_per_generation(wl)
+    st = sess.stream
+    # warmup (also instantiates the hipGraphs of the step)
+    sess.prefill(prompts.phon, prompts.ac)
+    for i in range(warmup):
+        if i and i % per_gen == 0:
+            sess.prefill(prompts.phon, prompts.ac)
+        sess.step_async(wl.K, wl.top_k)
+    torch.cuda.synchronize()
+    total_ms, tokens, done = 0.0, 0, 0
+    while done < steps:
+        sess.prefill(prompts.phon, prompts.ac)
+        n = min(per_gen, steps - done)
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(st)
+        for _ in range(n):
+            sess.step_async(wl.K, wl.top_k)
+        e1.record(st)
+        torch.cuda.synchronize()
+        total_ms += e0.elapsed_time(e1)
+        tokens += int(sess.seq_state()["gen"].sum())
+        done += n
+    return total_ms, tokens
+
+
+KCLASSES = {  # kernel class -> (name, launches per decode step as a function of layers)
+    4: ("attention (attn_mfma_kernel)", lambda L: L),
+    3: ("QKV projection (gemv_kernel<EpiQKVDec>)", lambda L: L),
+    1: ("FFN1 (gemv_kernel<EpiGeluB>)", lambda L: L),
+    5: ("heads (gemv_kernel<EpiLogitsB>)", lambda L: 1),
+    6: ("out-projection (gemv_kernel<EpiResid>, attention merge)", lambda L: L),
+    2: ("FFN2 (gemv_kernel<EpiResid>)", lambda L: L),
+}
+
+
+def launch_bytes(wl, kclass, ctx):
+    """Algorithmic HBM bytes of one launch of a kernel class at batch B, K
+    pending rows per sequence, `ctx` cached tokens per sequence (bf16 weights
+    and KV, fp32 residual stream)."""
+    m = wl.model
+    d, f, V, B, K = m.d_model, m.d_ff, m.vocab, wl.batch, wl.K
+    M = B * K
+    if kclass == 4:   # K and V rows of every head of every key + queries + output
+        return B * (ctx + K) * 2 * d * 2 + M * d * 4 + M * d * 2
+    if kclass == 3:
+        return 3 * d * d * 2 + 3 * d * 4 + M * d * 4 + 2 * d * 4 + M * d * 4 + 2 * M * d * 2
+    if kclass == 1:
+        return f * d * 2 + f * 4 + M * d * 4 + 2 * d * 4 + M * f * 2
+    if kclass == 5:
+        return K * V * d * 2 + K * V * 4 + B * d * 4 + 2 * d * 4 + B * K * V * 4
+    if kclass == 6:
+        return d * d * 2 + d * 4 + M * d * 2 + 2 * M * d * 4
+    if kclass == 2:
+        return d * f * 2 + d * 4 + M * f * 2 + 2 * M * d * 4
+    raise ValueError(kclass)
+
+
+def replay_kernels(sess, wl, prompts, steps, iters, torch):
+    """Per kernel class: average launch time (us) from `iters` back-to-back
+    replays of its last launch, mid-generation after `steps` decode steps."""
+    from paper_2410_13839_amd.binding import mtp_profile_replay
+    sess.prefill(prompts.phon, prompts.ac)
+    for _ in range(steps):
+        sess.step_async(wl.K, wl.top_k)
+    torch.cuda.synchronize()
+    ctx = int(sess.seq_state()["ctx_len"].max())
+    out = {}
+    for kc in KCLASSES:          # residual classes last: their replay alters the state
+        us = mtp_profile_replay(sess.ctx, kc, iters)
+        out[kc] = us
+    return out, ctx
+
+
+def cpu_baseline(wl, weights, logq, prompts, budget_s):
+    """The float64 oracle as it stands, on this host's cores: prefill, then
+    decode steps until about `budget_s` seconds of decode have run."""
+    from oracle.decoder import ARDecoder
+    from oracle.generate import Generator
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count()
+    model = ARDecoder(wl.model, weights)
+    g = Generator(model, logq, wl.eos_min, wl.max_new)
+    t0 = time.perf_counter()
+    g.prefill(prompts.phon[0], prompts.ac[0])
+    t_pre = time.perf_counter() - t0
+    t1 = time.perf_counter()
+    steps = 0
+    while not g.done and time.perf_counter() - t1 < budget_s:
+        g.step(wl.K, wl.top_k)
+        steps += 1
+    dt = time.perf_counter() - t1
+    toks = len(g.run.tokens)
+    return {"value": toks / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{wl.name}: prefill of {len(prompts.phon[0]) + len(prompts.ac[0])} tokens "
+                      f"({t_pre:.1f} s, excluded) then {steps} decode steps = {toks} tokens in {dt:.1f} s, "
+                      f"float64 numpy on {threads} BLAS threads of {len(os.sched_getaffinity(0))} visible cores"}
+
+
+def main():
+    args = _parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported by this build "
+              f"(the decode path runs on a single MI355X).", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2410_13839_amd.binding import Session
+    from paper_2410_13839_amd.workloads import WORKLOADS, make_logq, make_prompts, make_weights
+
+    wl = WORKLOADS[args.workload]
+    weights = make_weights(wl.model)
+    logq = make_logq()
+    prompts = make_prompts(wl)
+    sess = Session(wl.model, weights, logq, max_batch=wl.batch, max_prompt=wl.max_prompt, max_new=wl.max_new,
+                   eos_min=wl.eos_min, topk_max=max(8, wl.top_k))
+    print(f"[bench] {wl.name}: warmup {args.warmup}, timing {args.steps} steps", file=sys.stderr, flush=True)
+    ms, tokens = time_decode(sess, wl, prompts, args.steps, args.warmup, torch)
+    tok_s = tokens / (ms / 1000.0)
+    ms_step = ms / args.steps
+    ms_token = ms / (tokens / wl.batch)
+    print(f"[bench] {tokens} tokens in {ms:.2f} ms: {tok_s:.0f} tokens/s, {ms_step * 1000:.1f} us/step",
+          file=sys.stderr, flush=True)
+
+    # per-kernel launch times (back-to-back replays) and the dominant kernel
+    mid = _steps_per_generation(wl) // 2
+    times, ctx = replay_kernels(sess, wl, prompts, mid, 200, torch)
+    L = wl.model.n_layers
+    kernels = {}
+    for kc, us in times.items():
+        name, per_step = KCLASSES[kc]
+        nbytes = launch_bytes(wl, kc, ctx)
+        kernels[name] = {"avg_launch_us": round(us, 3), "launches_per_step": per_step(L),
+                         "bytes_per_launch": nbytes, "GB_s": round(nbytes / (us * 1e-6) / 1e9, 1),
+                         "share_of_step": round(us * per_step(L) / (ms_step * 1000.0), 3)}
+    dom = max(times, key=lambda kc: times[kc] * KCLASSES[kc][1](L))
+    dname = KCLASSES[dom][0]
+    dk = kernels[dname]
+    roof = {"kernel": dname, "bound": "hbm", "achieved": dk["GB_s"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(dk["GB_s"] / HBM_PEAK_GBS, 4), "traffic": None,
+            "bytes_per_launch": dk["bytes_per_launch"], "avg_launch_us": dk["avg_launch_us"],
+            "measured": f"200 back-to-back replays of the launch at step {mid} (context {ctx} tokens), HIP events on the library stream"}
+    print(f"[bench] dominant kernel {dname}: {dk}", file=sys.stderr, flush=True)
+    sess.close()
+    del sess
+    torch.cuda.empty_cache()
+
+    secondary = None
+    if not args.no_secondary and args.workload == "valle_k4":
+        wl2 = WORKLOADS["valle_b32"]
+        pr2 = make_prompts(wl2)
+        s2 = Session(wl2.model, weights, logq, max_batch=wl2.batch, max_prompt=wl2.max_prompt,
+                     max_new=wl2.max_new, eos_min=wl2.eos_min, topk_max=8)
+        steps2 = _steps_per_generation(wl2)
+        ms2, tok2 = time_decode(s2, wl2, pr2, steps2, 10, torch)
+        secondary = {"workload": wl2.name, "batch": wl2.batch, "K": wl2.K, "top_k": wl2.top_k, "steps": steps2,
+                     "tokens_per_s": round(tok2 / (ms2 / 1000.0), 1), "ms_per_step": round(ms2 / steps2, 4),
+                     "ms_per_token_per_seq": round(ms2 / (tok2 / wl2.batch), 4)}
+        print(f"[bench] {wl2.name}: {secondary}", file=sys.stderr, flush=True)
+        s2.close()
+        del s2
+        torch.cuda.empty_cache()
+
+    if args.copy_probe:
+        a = torch.empty(256 << 20, dtype=torch.uint8, device="cuda")
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(wl, weights, logq, prompts, args.cpu_seconds)
+        print(f"[bench] cpu oracle: {cpu['value']:.2f} tokens/s", file=sys.stderr, flush=True)
+
+    out = {
+        "metric": "codec tokens/sec (and ms/token) at batch 1, K=4 heads, top_k=4",
+        "value": round(tok_s, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4), "ms_per_token": round(ms_token, 5), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"{wl.name}: {wl.description}", "batch": wl.batch, "K": wl.K, "top_k": wl.top_k,
+                   "layers": wl.model.n_layers, "d_model": wl.model.d_model, "prompt": "100 phon + 225 acoustic",
+                   "max_new": wl.max_new, "parallelism": "single GPU"},
+        "roofline": roof,
+        "kernels": kernels,
+        "cpu_baseline": cpu,
+        "secondary": secondary,
+        "paper_context": "paper reports 20.5 -> 4.5 ms/token (x4.56, VALL-E, 8 heads) on unstated inference hardware",
+    }
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

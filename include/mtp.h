@@ -182,18 +182,22 @@ int mtp_get_seq_state(mtp_ctx* ctx, int32_t* ctx_len, int32_t* pend_len,
  * unspecified. */
 int mtp_get_tokens(mtp_ctx* ctx, int32_t* tokens);
 
-/* Kernel timing for measurement.  While enabled, every launch of the
- * kernel class `kclass` (MTP_KCLASS_*) in decode steps is bracketed by HIP
- * events on the context stream and decode steps launch eagerly.
- * mtp_profile_read synchronises and returns the summed event time (ms) and
- * the number of launches since enabling. */
-#define MTP_KCLASS_GEMM_FFN1   1   /* LN2-output x W_1 with GELU epilogue      */
-#define MTP_KCLASS_GEMM_FFN2   2
-#define MTP_KCLASS_GEMM_QKV    3
-#define MTP_KCLASS_ATTENTION   4
-#define MTP_KCLASS_HEADS       5
-int mtp_profile(mtp_ctx* ctx, int kclass, int enable);
-int mtp_profile_read(mtp_ctx* ctx, double* total_ms, int64_t* launches);
+/* Kernel timing for measurement.  Re-launches the most recent launch of kernel
+ * class `kclass` (MTP_KCLASS_*) `iters` times back to back on the context
+ * stream, bracketed by two HIP events, and returns the average time per
+ * launch in microseconds (synchronises).  The replayed launch keeps its
+ * arguments: QKV, FFN1, attention and heads launches rewrite the same outputs
+ * from the same inputs, but the out-projection and FFN2 launches add into
+ * the residual stream again, so replaying those leaves the sequence state
+ * unusable until the next mtp_prefill.  MTP_ESTATE if the class has not been
+ * launched since the context was created. */
+#define MTP_KCLASS_GEMM_FFN1   1   /* LN2 -> x W_1^T -> GELU                  */
+#define MTP_KCLASS_GEMM_FFN2   2   /* GELU out x W_2^T + residual             */
+#define MTP_KCLASS_GEMM_QKV    3   /* LN1 -> x W_qkv^T, K/V into the cache    */
+#define MTP_KCLASS_ATTENTION   4   /* decode attention over the paged cache   */
+#define MTP_KCLASS_HEADS       5   /* final LN -> K head projections          */
+#define MTP_KCLASS_GEMM_OPROJ  6   /* attention out x W_o^T + residual        */
+int mtp_profile_replay(mtp_ctx* ctx, int kclass, int iters, double* avg_us);
 
 /* Drops all sequence state (the next call must be mtp_prefill). */
 int mtp_reset(mtp_ctx* ctx);

@@ -27,11 +27,12 @@ MTP_FLAG_NO_GRAPH = 1
 (MTP_T_EMB_PHONE, MTP_T_EMB_AC, MTP_T_POS, MTP_T_LN1_G, MTP_T_LN1_B, MTP_T_W_QKV, MTP_T_B_QKV, MTP_T_W_O,
  MTP_T_B_O, MTP_T_LN2_G, MTP_T_LN2_B, MTP_T_W_1, MTP_T_B_1, MTP_T_W_2, MTP_T_B_2, MTP_T_LNF_G, MTP_T_LNF_B,
  MTP_T_W_HEADS, MTP_T_B_HEADS, MTP_T_COUNT) = range(20)
-MTP_KCLASS_GEMM_FFN1, MTP_KCLASS_GEMM_FFN2, MTP_KCLASS_GEMM_QKV, MTP_KCLASS_ATTENTION, MTP_KCLASS_HEADS = 1, 2, 3, 4, 5
+(MTP_KCLASS_GEMM_FFN1, MTP_KCLASS_GEMM_FFN2, MTP_KCLASS_GEMM_QKV, MTP_KCLASS_ATTENTION, MTP_KCLASS_HEADS,
+ MTP_KCLASS_GEMM_OPROJ) = 1, 2, 3, 4, 5, 6
 
 EXPORTED = ["mtp_query_sizes", "mtp_weight_offset", "mtp_create", "mtp_prefill", "mtp_decode_step",
             "mtp_decode_step_async", "mtp_get_logits", "mtp_get_lattice", "mtp_get_seq_state", "mtp_get_tokens",
-            "mtp_profile", "mtp_profile_read", "mtp_reset", "mtp_destroy", "mtp_last_error", "mtp_strerror"]
+            "mtp_profile_replay", "mtp_reset", "mtp_destroy", "mtp_last_error", "mtp_strerror"]
 
 
 class mtp_config(ctypes.Structure):
@@ -65,8 +66,7 @@ _lib.mtp_get_logits.argtypes = [_ctx, _f32p]
 _lib.mtp_get_lattice.argtypes = [_ctx, _i32p, _f32p, _f32p, _i32p, _i32p]
 _lib.mtp_get_seq_state.argtypes = [_ctx, _i32p, _i32p, _i32p, _i32p]
 _lib.mtp_get_tokens.argtypes = [_ctx, _i32p]
-_lib.mtp_profile.argtypes = [_ctx, ctypes.c_int, ctypes.c_int]
-_lib.mtp_profile_read.argtypes = [_ctx, _P(ctypes.c_double), _P(ctypes.c_int64)]
+_lib.mtp_profile_replay.argtypes = [_ctx, ctypes.c_int, ctypes.c_int, _P(ctypes.c_double)]
 _lib.mtp_reset.argtypes = [_ctx]
 _lib.mtp_destroy.argtypes = [_ctx]
 _lib.mtp_destroy.restype = None
@@ -166,14 +166,10 @@ def mtp_get_tokens(ctx, B: int, max_new: int) -> np.ndarray:
     return out
 
 
-def mtp_profile(ctx, kclass: int, enable: bool) -> None:
-    _check(_lib.mtp_profile(ctx, kclass, 1 if enable else 0), ctx, "mtp_profile")
-
-
-def mtp_profile_read(ctx) -> Tuple[float, int]:
-    ms, n = ctypes.c_double(), ctypes.c_int64()
-    _check(_lib.mtp_profile_read(ctx, ctypes.byref(ms), ctypes.byref(n)), ctx, "mtp_profile_read")
-    return ms.value, n.value
+def mtp_profile_replay(ctx, kclass: int, iters: int) -> float:
+    us = ctypes.c_double()
+    _check(_lib.mtp_profile_replay(ctx, kclass, iters, ctypes.byref(us)), ctx, "mtp_profile_replay")
+    return us.value
 
 
 def mtp_reset(ctx) -> None:

@@ -8,7 +8,9 @@
 
 #include <algorithm>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
+#include <functional>
 #include <map>
 #include <new>
 #include <string>
@@ -92,6 +94,7 @@ int validate(const mtp_config* c, std::string* why) {
     if (c->max_prompt < 1) return bad("max_prompt must be positive");
     if (c->max_new < 1) return bad("max_new must be positive");
     if ((int64_t)c->max_prompt + c->max_new > c->max_pos) return bad("max_prompt + max_new exceeds max_pos");
+    if ((int64_t)c->max_prompt + c->max_new > 16384) return bad("max_prompt + max_new exceeds 16384");
     if (c->page_size < 8 || c->page_size > 128 || (c->page_size & (c->page_size - 1))) return bad("page_size must be a power of two in 8..128");
     if (c->num_pages < 0) return bad("num_pages must be >= 0");
     if (c->dtype != MTP_DTYPE_F32 && c->dtype != MTP_DTYPE_BF16) return bad("unknown dtype");
@@ -132,7 +135,7 @@ WsLayout ws_layout(const mtp_config& c) {
     w.attn = take(w.m_max * d * w.act_bytes);
     w.ffn = take(w.m_max * F * w.act_bytes);
     w.part = take(std::max(w.m_pre, w.m_dec * (int64_t)MTP_SPLITK_MAX) * d * 4);
-    w.apart = take(B * H * w.max_splits * MTP_ATTN_QT * 66 * 4);
+    w.apart = take(B * H * w.max_splits * MTP_ATTN_QT * 68 * 4);
     w.hz = take(B * d * 4);
     w.z = take(B * d * w.act_bytes);
     w.logits = take(B * KH * V * 4);
@@ -174,10 +177,9 @@ struct mtp_ctx {
     int n_pre_rows = 0, n_pre_tiles = 0;
     // graphs keyed by (K, top_k, q_pad, batch, split_len, n_splits)
     std::map<std::tuple<int, int, int, int, int, int>, hipGraphExec_t> graphs;
-    // profiling
-    int prof_class = 0;
-    std::vector<std::pair<hipEvent_t, hipEvent_t>> prof_events;
-    size_t prof_used = 0;
+    // last launch of each kernel class (arguments captured by value), for
+    // back-to-back replay timing
+    std::function<hipError_t(hipStream_t)> last_launch[8];
 
     char* W() const { return (char*)buf.weights; }
     char* WS() const { return (char*)buf.workspace; }
@@ -223,20 +225,86 @@ int pick_splits(const mtp_ctx* c, int M, int N, int K) {
     return s;
 }
 
-void prof_begin(mtp_ctx* c, int kclass) {
-    if (c->prof_class != kclass) return;
-    if (c->prof_used >= c->prof_events.size()) {
-        hipEvent_t a, b;
-        if (hipEventCreate(&a) != hipSuccess) return;
-        if (hipEventCreate(&b) != hipSuccess) { (void)hipEventDestroy(a); return; }
-        c->prof_events.push_back({a, b});
-    }
-    (void)hipEventRecord(c->prof_events[c->prof_used].first, c->stream);
+// Launch through `f` and remember it as the last launch of class `kclass`.
+hipError_t launch_rec(mtp_ctx* c, int kclass, std::function<hipError_t(hipStream_t)> f) {
+    hipError_t e = f(c->stream);
+    if (kclass > 0 && kclass < 8) c->last_launch[kclass] = std::move(f);
+    return e;
 }
-void prof_end(mtp_ctx* c, int kclass) {
-    if (c->prof_class != kclass || c->prof_used >= c->prof_events.size()) return;
-    (void)hipEventRecord(c->prof_events[c->prof_used].second, c->stream);
-    c->prof_used++;
+
+AttnDecArgs dec_attn_args(mtp_ctx* c, int l, int qt) {
+    AttnDecArgs a{};
+    a.dtype = c->cfg.dtype; a.B = c->B; a.Q = c->q_pad; a.qt = qt; a.st = c->ws_ptr<SeqState>(c->ws.state);
+    a.q = c->ws_ptr<float>(c->ws.q); a.ldq = c->cfg.d_model; a.kv = c->kv(l);
+    a.split_len = c->split_len; a.n_splits = c->n_splits; a.out = c->WS() + c->ws.attn; a.ldo = c->cfg.d_model;
+    a.part = c->ws_ptr<float>(c->ws.apart); a.merge = 1;
+    return a;
+}
+
+// Decode attention of layer l: MFMA kernel for bf16 caches, VALU kernel for
+// fp32 caches.  With merge_launch, split partials are merged by a separate
+// launch; otherwise the consumer merges them.
+hipError_t decode_attention(mtp_ctx* c, int l, int qt, bool merge_launch) {
+    AttnDecArgs da = dec_attn_args(c, l, qt);
+    da.merge = merge_launch ? 1 : 0;
+    if (c->cfg.dtype != MTP_DTYPE_BF16)
+        return launch_rec(c, MTP_KCLASS_ATTENTION, [da](hipStream_t s) { return attention_decode(s, da); });
+    AttnMfmaArgs m{};
+    m.mode = 0; m.n_tiles = c->B; m.Q = c->q_pad; m.qt = qt; m.st = da.st;
+    m.q = da.q; m.ldq = da.ldq; m.kv = da.kv; m.split_len = da.split_len; m.n_splits = da.n_splits;
+    m.out = (bf16_t*)da.out; m.ldo = da.ldo; m.part = da.part;
+    hipError_t e = launch_rec(c, MTP_KCLASS_ATTENTION, [m](hipStream_t s) { return attention_mfma(s, m); });
+    if (e != hipSuccess || !merge_launch) return e;
+    return attention_decode_merge(c->stream, da);
+}
+
+// Whether the out-projection prologue merges the attention split partials
+// itself (small batches) instead of a separate merge launch.
+bool prologue_merge(const mtp_ctx* c, int rows) {
+    if (c->n_splits <= 1 || c->n_splits > 8) return false;
+    const int64_t bytes = (int64_t)rows * c->cfg.n_heads * c->n_splits * 68 * 4;
+    return bytes <= 96 * 1024;
+}
+
+// One layer of the fused small-M decode trunk (bf16, B*Q <= 32 rows).
+int run_layer_fused(mtp_ctx* c, int l, int rows, int qt) {
+    const mtp_config& cf = c->cfg;
+    const int d = cf.d_model, F = cf.d_ff;
+    hipStream_t st = c->stream;
+    float* h = c->ws_ptr<float>(c->ws.h);
+    GemvArgs g{};
+    g.epi = EPI_QKV; g.xmode = (l == 0) ? 2 : 1; g.M = rows; g.N = 3 * d; g.K = d; g.splits = 1;
+    g.W = (const bf16_t*)c->lt(l, MTP_T_W_QKV); g.h = h; g.ldh = d;
+    g.g = (const float*)c->lt(l, MTP_T_LN1_G); g.beta = (const float*)c->lt(l, MTP_T_LN1_B);
+    g.st = c->ws_ptr<SeqState>(c->ws.state); g.Q = c->q_pad;
+    g.emb = (const bf16_t*)c->wt(MTP_T_EMB_AC); g.pos = (const bf16_t*)c->wt(MTP_T_POS); g.h_out = h;
+    g.bias = (const float*)c->lt(l, MTP_T_B_QKV); g.q = c->ws_ptr<float>(c->ws.q); g.kv = c->kv(l); g.d = d;
+    HIPCHK(c, launch_rec(c, MTP_KCLASS_GEMM_QKV, [g](hipStream_t s) { return gemv(s, g); }), "qkv gemv");
+
+    const bool pm = prologue_merge(c, rows);
+    HIPCHK(c, decode_attention(c, l, qt, !pm), "decode attention");
+
+    g = GemvArgs{};
+    g.epi = EPI_RESID; g.xmode = pm ? 4 : 0; g.M = rows; g.N = d; g.K = d; g.splits = 1;
+    g.W = (const bf16_t*)c->lt(l, MTP_T_W_O); g.x = (const bf16_t*)(c->WS() + c->ws.attn); g.ldx = d;
+    g.st = c->ws_ptr<SeqState>(c->ws.state); g.Q = c->q_pad;
+    g.apart = c->ws_ptr<float>(c->ws.apart); g.qt = qt; g.split_len = c->split_len; g.n_splits = c->n_splits;
+    g.bias = (const float*)c->lt(l, MTP_T_B_O); g.h_res = h; g.ldo = d;
+    HIPCHK(c, launch_rec(c, MTP_KCLASS_GEMM_OPROJ, [g](hipStream_t s) { return gemv(s, g); }), "out-proj gemv");
+
+    g = GemvArgs{};
+    g.epi = EPI_GELU; g.xmode = 1; g.M = rows; g.N = F; g.K = d; g.splits = 1;
+    g.W = (const bf16_t*)c->lt(l, MTP_T_W_1); g.h = h; g.ldh = d;
+    g.g = (const float*)c->lt(l, MTP_T_LN2_G); g.beta = (const float*)c->lt(l, MTP_T_LN2_B);
+    g.bias = (const float*)c->lt(l, MTP_T_B_1); g.out = c->WS() + c->ws.ffn; g.ldo = F;
+    HIPCHK(c, launch_rec(c, MTP_KCLASS_GEMM_FFN1, [g](hipStream_t s) { return gemv(s, g); }), "ffn1 gemv");
+
+    g = GemvArgs{};
+    g.epi = EPI_RESID; g.xmode = 0; g.M = rows; g.N = d; g.K = F; g.splits = 1;
+    g.W = (const bf16_t*)c->lt(l, MTP_T_W_2); g.x = (const bf16_t*)(c->WS() + c->ws.ffn); g.ldx = F;
+    g.bias = (const float*)c->lt(l, MTP_T_B_2); g.h_res = h; g.ldo = d;
+    HIPCHK(c, launch_rec(c, MTP_KCLASS_GEMM_FFN2, [g](hipStream_t s) { return gemv(s, g); }), "ffn2 gemv");
+    return MTP_OK;
 }
 
 // One trunk layer over `rows` rows whose row/tile metadata is already on the device.
@@ -252,18 +320,25 @@ int run_layer(mtp_ctx* c, int l, int rows, int n_tiles, int qt, int split_len, i
     g.W = c->lt(l, MTP_T_W_QKV); g.N = 3 * d; g.K = d; g.splits = 1;
     g.bias = (const float*)c->lt(l, MTP_T_B_QKV);
     g.q = c->ws_ptr<float>(c->ws.q); g.rows = c->ws_ptr<RowInfo>(c->ws.rows); g.kv = c->kv(l); g.d = d;
-    if (decode) prof_begin(c, MTP_KCLASS_GEMM_QKV);
-    HIPCHK(c, gemm(st, g), "qkv gemm");
-    if (decode) prof_end(c, MTP_KCLASS_GEMM_QKV);
+    HIPCHK(c, launch_rec(c, decode ? MTP_KCLASS_GEMM_QKV : 0, [g](hipStream_t s) { return gemm(s, g); }), "qkv gemm");
     // attention
-    AttnArgs a{};
-    a.dtype = dt; a.q = c->ws_ptr<float>(c->ws.q); a.ldq = d; a.rows = c->ws_ptr<RowInfo>(c->ws.rows);
-    a.tiles = c->ws_ptr<int2>(c->ws.tiles); a.n_tiles = n_tiles; a.qt = qt; a.kv = c->kv(l);
-    a.split_len = split_len; a.n_splits = n_splits; a.out = c->WS() + c->ws.attn; a.ldo = d;
-    a.part = c->ws_ptr<float>(c->ws.apart);
-    if (decode) prof_begin(c, MTP_KCLASS_ATTENTION);
-    HIPCHK(c, attention(st, a), "attention");
-    if (decode) prof_end(c, MTP_KCLASS_ATTENTION);
+    if (decode) {
+        HIPCHK(c, decode_attention(c, l, qt, true), "decode attention");
+    } else if (dt == MTP_DTYPE_BF16) {
+        AttnMfmaArgs m{};
+        m.mode = 1; m.n_tiles = n_tiles; m.Q = 0; m.qt = 16; m.st = c->ws_ptr<SeqState>(c->ws.state);
+        m.tiles = c->ws_ptr<int2>(c->ws.tiles); m.rows = c->ws_ptr<RowInfo>(c->ws.rows);
+        m.q = c->ws_ptr<float>(c->ws.q); m.ldq = d; m.kv = c->kv(l); m.split_len = 1 << 30; m.n_splits = 1;
+        m.out = (bf16_t*)(c->WS() + c->ws.attn); m.ldo = d; m.part = nullptr;
+        HIPCHK(c, attention_mfma(st, m), "prefill attention");
+    } else {
+        AttnArgs a{};
+        a.dtype = dt; a.q = c->ws_ptr<float>(c->ws.q); a.ldq = d; a.rows = c->ws_ptr<RowInfo>(c->ws.rows);
+        a.tiles = c->ws_ptr<int2>(c->ws.tiles); a.n_tiles = n_tiles; a.qt = qt; a.kv = c->kv(l);
+        a.split_len = split_len; a.n_splits = n_splits; a.out = c->WS() + c->ws.attn; a.ldo = d;
+        a.part = c->ws_ptr<float>(c->ws.apart);
+        HIPCHK(c, attention(st, a), "attention");
+    }
     // out projection -> partials, residual + LN2
     const size_t sstride = (size_t)rows * d;
     g = GemmArgs{};
@@ -281,17 +356,13 @@ int run_layer(mtp_ctx* c, int l, int rows, int n_tiles, int qt, int split_len, i
     g.dtype = dt; g.epi = EPI_GELU; g.X = c->WS() + c->ws.u; g.ldx = d; g.M = rows;
     g.W = c->lt(l, MTP_T_W_1); g.N = F; g.K = d; g.splits = 1;
     g.bias = (const float*)c->lt(l, MTP_T_B_1); g.out = c->WS() + c->ws.ffn; g.ldo = F;
-    if (decode) prof_begin(c, MTP_KCLASS_GEMM_FFN1);
-    HIPCHK(c, gemm(st, g), "ffn1 gemm");
-    if (decode) prof_end(c, MTP_KCLASS_GEMM_FFN1);
+    HIPCHK(c, launch_rec(c, decode ? MTP_KCLASS_GEMM_FFN1 : 0, [g](hipStream_t s) { return gemm(s, g); }), "ffn1 gemm");
     // FFN2 -> partials, residual + next LN1
     g = GemmArgs{};
     g.dtype = dt; g.epi = EPI_PARTIAL; g.X = c->WS() + c->ws.ffn; g.ldx = F; g.M = rows;
     g.W = c->lt(l, MTP_T_W_2); g.N = d; g.K = F; g.splits = pick_splits(c, rows, d, F);
     g.out = c->WS() + c->ws.part; g.ldo = d; g.split_stride = sstride;
-    if (decode) prof_begin(c, MTP_KCLASS_GEMM_FFN2);
-    HIPCHK(c, gemm(st, g), "ffn2 gemm");
-    if (decode) prof_end(c, MTP_KCLASS_GEMM_FFN2);
+    HIPCHK(c, launch_rec(c, decode ? MTP_KCLASS_GEMM_FFN2 : 0, [g](hipStream_t s) { return gemm(s, g); }), "ffn2 gemm");
     r = ResidArgs{};
     r.dtype = dt; r.n_rows = rows; r.d = d; r.h = c->ws_ptr<float>(c->ws.h); r.part = c->ws_ptr<float>(c->ws.part);
     r.n_split = g.splits; r.split_stride = sstride; r.bias = (const float*)c->lt(l, MTP_T_B_2);
@@ -308,7 +379,15 @@ int enqueue_step(mtp_ctx* c, int K, int top_k) {
     const mtp_config& cf = c->cfg;
     const int d = cf.d_model, dt = cf.dtype, B = c->B, Q = c->q_pad, V = cf.vocab;
     hipStream_t st = c->stream;
-    if (Q > 0) {
+    const bool small = dt == MTP_DTYPE_BF16 && B * Q <= 32;
+    int qt = 1;
+    while (qt < Q) qt <<= 1;
+    if (Q > 0 && small) {
+        for (int l = 0; l < cf.n_layers; ++l) {
+            int rc = run_layer_fused(c, l, B * Q, qt);
+            if (rc) return rc;
+        }
+    } else if (Q > 0) {
         const int rows = B * Q;
         EmbedArgs e{};
         e.dtype = dt; e.mode = 0; e.n_rows = rows; e.Q = Q; e.st = c->ws_ptr<SeqState>(c->ws.state);
@@ -317,25 +396,31 @@ int enqueue_step(mtp_ctx* c, int K, int top_k) {
         e.ln_g = (const float*)c->lt(0, MTP_T_LN1_G); e.ln_b = (const float*)c->lt(0, MTP_T_LN1_B);
         e.d = d; e.h = c->ws_ptr<float>(c->ws.h); e.u = c->WS() + c->ws.u;
         HIPCHK(c, embed_ln(st, e), "embed");
-        int qt = 1;
-        while (qt < Q) qt <<= 1;
         for (int l = 0; l < cf.n_layers; ++l) {
             int rc = run_layer(c, l, rows, B, qt, c->split_len, c->n_splits, true);
             if (rc) return rc;
         }
     }
-    FinalArgs f{};
-    f.dtype = dt; f.B = B; f.d = d; f.mode = 0; f.Q = Q; f.st = c->ws_ptr<SeqState>(c->ws.state);
-    f.h = c->ws_ptr<float>(c->ws.h); f.hz = c->ws_ptr<float>(c->ws.hz);
-    f.ln_g = (const float*)c->wt(MTP_T_LNF_G); f.ln_b = (const float*)c->wt(MTP_T_LNF_B); f.z = c->WS() + c->ws.z;
-    HIPCHK(c, final_ln(st, f), "final ln");
-    GemmArgs g{};
-    g.dtype = dt; g.epi = EPI_LOGITS; g.X = c->WS() + c->ws.z; g.ldx = d; g.M = B;
-    g.W = c->wt(MTP_T_W_HEADS); g.N = K * V; g.K = d; g.splits = 1;
-    g.bias = (const float*)c->wt(MTP_T_B_HEADS); g.out = c->WS() + c->ws.logits; g.ldo = K * V;
-    prof_begin(c, MTP_KCLASS_HEADS);
-    HIPCHK(c, gemm(st, g), "heads gemm");
-    prof_end(c, MTP_KCLASS_HEADS);
+    if (dt == MTP_DTYPE_BF16 && B <= 32) {
+        GemvArgs g{};
+        g.epi = EPI_LOGITS; g.xmode = 3; g.M = B; g.N = K * V; g.K = d; g.splits = 1;
+        g.W = (const bf16_t*)c->wt(MTP_T_W_HEADS); g.h = c->ws_ptr<float>(c->ws.h); g.ldh = d;
+        g.hz = c->ws_ptr<float>(c->ws.hz); g.st = c->ws_ptr<SeqState>(c->ws.state); g.Q = Q;
+        g.g = (const float*)c->wt(MTP_T_LNF_G); g.beta = (const float*)c->wt(MTP_T_LNF_B);
+        g.bias = (const float*)c->wt(MTP_T_B_HEADS); g.out = c->WS() + c->ws.logits; g.ldo = K * V;
+        HIPCHK(c, launch_rec(c, MTP_KCLASS_HEADS, [g](hipStream_t s) { return gemv(s, g); }), "heads gemv");
+    } else {
+        FinalArgs f{};
+        f.dtype = dt; f.B = B; f.d = d; f.mode = 0; f.Q = Q; f.st = c->ws_ptr<SeqState>(c->ws.state);
+        f.h = c->ws_ptr<float>(c->ws.h); f.hz = c->ws_ptr<float>(c->ws.hz);
+        f.ln_g = (const float*)c->wt(MTP_T_LNF_G); f.ln_b = (const float*)c->wt(MTP_T_LNF_B); f.z = c->WS() + c->ws.z;
+        HIPCHK(c, final_ln(st, f), "final ln");
+        GemmArgs g{};
+        g.dtype = dt; g.epi = EPI_LOGITS; g.X = c->WS() + c->ws.z; g.ldx = d; g.M = B;
+        g.W = c->wt(MTP_T_W_HEADS); g.N = K * V; g.K = d; g.splits = 1;
+        g.bias = (const float*)c->wt(MTP_T_B_HEADS); g.out = c->WS() + c->ws.logits; g.ldo = K * V;
+        HIPCHK(c, launch_rec(c, MTP_KCLASS_HEADS, [g](hipStream_t s) { return gemm(s, g); }), "heads gemm");
+    }
     SelectArgs s{};
     s.B = B; s.K = K; s.top_k = top_k; s.V = V; s.eos_id = cf.eos_id; s.eos_min = cf.eos_min; s.max_new = cf.max_new;
     s.Q = Q; s.logits = c->ws_ptr<float>(c->ws.logits); s.ld_logits = K * V; s.logq = c->buf.logq;
@@ -344,8 +429,7 @@ int enqueue_step(mtp_ctx* c, int K, int top_k) {
     s.psi = c->ws_ptr<int32_t>(c->ws.psi); s.slots = c->ws_ptr<int32_t>(c->ws.slots);
     s.out_tokens = c->ws_ptr<int32_t>(c->ws.out_tok); s.out_count = c->ws_ptr<int32_t>(c->ws.out_cnt);
     s.hist = c->ws_ptr<int32_t>(c->ws.hist); s.hist_ld = cf.max_new;
-    HIPCHK(c, topk(st, s), "topk");
-    HIPCHK(c, viterbi_accept(st, s), "viterbi");
+    HIPCHK(c, select_fused(st, s), "select");
     return MTP_OK;
 }
 
@@ -354,7 +438,7 @@ int step_common(mtp_ctx* c, int K, int top_k) {
     if (!c->prefilled) { c->err = "decode step before prefill"; return MTP_ESTATE; }
     if (K < 1 || K > c->cfg.k_heads) { c->err = "K must be in 1..k_heads"; return MTP_EINVAL; }
     if (top_k < 1 || top_k > c->cfg.topk_max) { c->err = "top_k must be in 1..topk_max"; return MTP_EINVAL; }
-    const bool use_graph = !(c->cfg.flags & MTP_FLAG_NO_GRAPH) && c->stream != nullptr && c->prof_class == 0;
+    const bool use_graph = !(c->cfg.flags & MTP_FLAG_NO_GRAPH) && c->stream != nullptr;
     int rc;
     if (!use_graph) {
         rc = enqueue_step(c, K, top_k);
@@ -495,7 +579,8 @@ int mtp_prefill(mtp_ctx* c, int B, const int32_t* phon, const int32_t* phon_len,
         for (int i = 0; i < phon_len[b]; ++i) c->h_ids.push_back(phon[op++]);
         for (int i = 0; i < ac_len[b]; ++i) c->h_ids.push_back(ac[oa++]);
         for (int i = 0; i < len; ++i) c->h_rows.push_back(RowInfo{b, i});
-        for (int i0 = 0; i0 < len; i0 += MTP_ATTN_QT) c->h_tiles.push_back(make_int2(row0 + i0, std::min(MTP_ATTN_QT, len - i0)));
+        const int trows = (cf.dtype == MTP_DTYPE_BF16) ? 16 : MTP_ATTN_QT;
+        for (int i0 = 0; i0 < len; i0 += trows) c->h_tiles.push_back(make_int2(row0 + i0, std::min(trows, len - i0)));
         c->h_last[b] = row0 + len - 1;
         SeqState s{};
         s.ctx_len = len; s.pend_len = 0; s.gen = 0; s.done = 0; s.phon_len = phon_len[b]; s.prompt_len = len;
@@ -530,17 +615,28 @@ int mtp_prefill(mtp_ctx* c, int B, const int32_t* phon, const int32_t* phon_len,
     f.z = nullptr;
     HIPCHK(c, final_ln(st, f), "prefill last rows");
 
-    // decode attention split plan: enough (sequence, head, split) workgroups
-    // to fill the chip at the longest context this batch can reach
+    // decode attention split plan, fixed for the batch so one captured graph
+    // serves every step: small batches split the keys so that the
+    // out-projection prologue can merge the partials (at most 96 KB of them
+    // per workgroup); larger batches aim at ~512 (sequence, head, split)
+    // workgroups and merge in a separate launch.
     int64_t max_ctx = 0;
     for (int b = 0; b < B; ++b) max_ctx = std::max<int64_t>(max_ctx, phon_len[b] + ac_len[b] + (int64_t)cf.max_new);
     const int64_t bh = (int64_t)B * cf.n_heads;
-    const int64_t want = std::max<int64_t>(1, (2048 + bh - 1) / bh);
+    int64_t want;
+    const int64_t rows_max = (int64_t)B * cf.k_heads;
+    const int64_t per_split = rows_max * cf.n_heads * 68 * 4;
+    if (bh < 256 && per_split <= 48 * 1024) want = std::max<int64_t>(1, std::min<int64_t>(8, (96 * 1024) / per_split));
+    else want = std::max<int64_t>(1, (512 + bh - 1) / bh);
     int64_t sl = (max_ctx + want - 1) / want;
-    sl = std::max<int64_t>(64, (sl + 63) / 64 * 64);
+    sl = std::max<int64_t>(64, (sl + 31) / 32 * 32);
+    if (const char* env = getenv("MTP_SPLIT_LEN")) {
+        const int64_t v = atoll(env);
+        if (v >= 32 && v % 32 == 0) sl = v;
+    }
     c->split_len = (int)sl;
     c->n_splits = (int)((max_ctx + sl - 1) / sl);
-    if (c->n_splits > c->ws.max_splits) { c->err = "attention split plan exceeds workspace"; return MTP_ENOMEM; }
+    if (c->n_splits > 64 || c->n_splits > c->ws.max_splits) { c->err = "attention split plan exceeds workspace"; return MTP_ENOMEM; }
 
     c->B = B;
     c->q_pad = 0;
@@ -616,26 +712,24 @@ int mtp_get_tokens(mtp_ctx* c, int32_t* tokens) {
     return MTP_OK;
 }
 
-int mtp_profile(mtp_ctx* c, int kclass, int enable) {
-    if (!c) return MTP_EINVAL;
-    if (kclass < MTP_KCLASS_GEMM_FFN1 || kclass > MTP_KCLASS_HEADS) { c->err = "unknown kernel class"; return MTP_EINVAL; }
-    c->prof_class = enable ? kclass : 0;
-    c->prof_used = 0;
-    return MTP_OK;
-}
-
-int mtp_profile_read(mtp_ctx* c, double* total_ms, int64_t* launches) {
-    if (!c) return MTP_EINVAL;
-    HIPCHK(c, hipStreamSynchronize(c->stream), "sync");
-    double tot = 0;
-    for (size_t i = 0; i < c->prof_used; ++i) {
-        float ms = 0;
-        HIPCHK(c, hipEventElapsedTime(&ms, c->prof_events[i].first, c->prof_events[i].second), "event time");
-        tot += ms;
-    }
-    if (total_ms) *total_ms = tot;
-    if (launches) *launches = (int64_t)c->prof_used;
-    c->prof_used = 0;
+int mtp_profile_replay(mtp_ctx* c, int kclass, int iters, double* avg_us) {
+    if (!c || !avg_us || iters < 1) return MTP_EINVAL;
+    if (kclass < MTP_KCLASS_GEMM_FFN1 || kclass > MTP_KCLASS_GEMM_OPROJ) { c->err = "unknown kernel class"; return MTP_EINVAL; }
+    if (!c->last_launch[kclass]) { c->err = "no launch of this kernel class yet"; return MTP_ESTATE; }
+    hipEvent_t e0, e1;
+    HIPCHK(c, hipEventCreate(&e0), "event");
+    hipError_t e = hipEventCreate(&e1);
+    if (e != hipSuccess) { (void)hipEventDestroy(e0); return hip_fail(c, e, "event"); }
+    e = hipEventRecord(e0, c->stream);
+    for (int i = 0; i < iters && e == hipSuccess; ++i) e = c->last_launch[kclass](c->stream);
+    if (e == hipSuccess) e = hipEventRecord(e1, c->stream);
+    if (e == hipSuccess) e = hipEventSynchronize(e1);
+    float ms = 0.f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
+    (void)hipEventDestroy(e0);
+    (void)hipEventDestroy(e1);
+    if (e != hipSuccess) return hip_fail(c, e, "replay");
+    *avg_us = 1000.0 * ms / iters;
     return MTP_OK;
 }
 
@@ -652,10 +746,6 @@ void mtp_destroy(mtp_ctx* c) {
     if (!c) return;
     if (c->stream) (void)hipStreamSynchronize(c->stream);
     for (auto& kv : c->graphs) (void)hipGraphExecDestroy(kv.second);
-    for (auto& p : c->prof_events) {
-        (void)hipEventDestroy(p.first);
-        (void)hipEventDestroy(p.second);
-    }
     delete c;
 }
 

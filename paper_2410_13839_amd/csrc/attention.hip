@@ -14,12 +14,13 @@
 
 #include "common.h"
 #include "launch.h"
+#include "wave.h"
 
 namespace mtp {
 
 namespace {
 constexpr int CH = 256;        // keys per LDS chunk (== threads per block)
-constexpr int PSTRIDE = 66;    // floats per partial row: max, sum, 64 outputs
+constexpr int PSTRIDE = 68;    // floats per partial row: max, sum, 2 pad, 64 outputs (16-byte aligned)
 
 template <typename KVT> struct KVRow;
 template <> struct KVRow<bf16_t> {
@@ -40,16 +41,8 @@ template <> struct KVRow<float> {
     }
 };
 
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
-    return v;
-}
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
-    return v;
-}
+__device__ __forceinline__ float wave_max(float v) { return wave_max64(v); }
+__device__ __forceinline__ float wave_sum(float v) { return wave_sum64(v); }
 }  // namespace
 
 template <typename KVT, typename OutT, int QT>
@@ -124,11 +117,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs p) {
                 for (int i = 0; i < QT; ++i) sc[i] = 0.f;
             }
 #pragma unroll
-            for (int i = 0; i < QT; ++i) {
-                sc[i] += __shfl_xor(sc[i], 1);
-                sc[i] += __shfl_xor(sc[i], 2);
-                sc[i] += __shfl_xor(sc[i], 4);
-            }
+            for (int i = 0; i < QT; ++i) sc[i] = sum8(sc[i]);
             if (dc == 0 && kk < cn) {
 #pragma unroll
                 for (int i = 0; i < QT; ++i) s_p[i][kk] = (c0 + kk <= pos0 + i) ? sc[i] : -INFINITY;
@@ -195,11 +184,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs p) {
     for (int i = 0; i < QT; ++i)
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-            float a = acc[i][e];
-            a += __shfl_xor(a, 8);
-            a += __shfl_xor(a, 16);
-            a += __shfl_xor(a, 32);
-            acc[i][e] = a;
+            acc[i][e] = sum_stride8(acc[i][e]);
         }
     if (lane < 8) {
 #pragma unroll
@@ -213,7 +198,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs p) {
         if (i >= nrows) continue;
         const float o = (s_acc[0][i][dim] + s_acc[1][i][dim]) + (s_acc[2][i][dim] + s_acc[3][i][dim]);
         if (part) {
-            part[i * PSTRIDE + 2 + dim] = o;
+            part[i * PSTRIDE + 4 + dim] = o;
             if (dim == 0) {
                 part[i * PSTRIDE] = m_run[i];
                 part[i * PSTRIDE + 1] = l_run[i];
@@ -244,7 +229,7 @@ __global__ __launch_bounds__(256) void attn_combine(AttnArgs p) {
             if (m == -INFINITY) continue;
             const float w = __expf(m - M);
             den = fmaf(w, e[1], den);
-            num = fmaf(w, e[2 + dim], num);
+            num = fmaf(w, e[4 + dim], num);
         }
         ActIO<OutT>::store(reinterpret_cast<OutT*>(p.out) + (size_t)(row0 + i) * p.ldo + head * 64 + dim, num / den);
     }
@@ -269,6 +254,251 @@ static hipError_t attn_launch(hipStream_t st, const AttnArgs& a) {
 hipError_t attention(hipStream_t st, const AttnArgs& a) {
     if (a.dtype == 1) return attn_launch<bf16_t, bf16_t>(st, a);
     return attn_launch<float, float>(st, a);
+}
+
+}  // namespace mtp
+
+// ---------------------------------------------------------------- decode
+// One workgroup per (sequence, head, key split).  The sequence state gives
+// the rows (the pending chunk) and the context length directly; each chunk
+// of up to 256 keys requests every K and V row at once, and softmax
+// statistics run online across chunks.  With one split the normalised bf16
+// output is written; with several, each split writes (max, sum,
+// unnormalised output) and the merge happens in the consumer (the
+// out-projection prologue, or attn_decode_merge).
+namespace mtp {
+
+template <typename KVT, typename OutT, int QT>
+__global__ __launch_bounds__(256) void attn_decode_kernel(AttnDecArgs p) {
+    constexpr int NJ = 8;                     // keys per thread per chunk
+    const int b = blockIdx.x, head = blockIdx.y, split = blockIdx.z;
+    const int H = gridDim.y;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int kg = tid >> 3, dc = tid & 7;
+    __shared__ float s_p[QT][256];
+    __shared__ float s_red[4][QT];
+    __shared__ float s_acc[4][QT][64];
+    const KVT* pool = reinterpret_cast<const KVT*>(p.kv.pool);
+    const size_t vstride = (size_t)p.kv.n_heads * p.kv.page_size * MTP_HEAD_DIM;
+    const int kb = split * p.split_len;
+
+    // Issued together, before the sequence state is known: the state, the
+    // queries of every possible pending row, and the K/V rows of the first
+    // chunk (page table entries first).  Keys past the context are masked
+    // below; every address stays inside the sequence's block table row.
+    const int nrows = p.st[b].pend_len;
+    const int pos0 = p.st[b].ctx_len;
+    float qv[QT][8];
+#pragma unroll
+    for (int i = 0; i < QT; ++i) {
+        const float* qp = p.q + (size_t)(b * p.Q + min(i, p.Q - 1)) * p.ldq + head * 64 + dc * 8;
+        const float4 x0 = *reinterpret_cast<const float4*>(qp);
+        const float4 x1 = *reinterpret_cast<const float4*>(qp + 4);
+        qv[i][0] = x0.x * 0.125f; qv[i][1] = x0.y * 0.125f; qv[i][2] = x0.z * 0.125f; qv[i][3] = x0.w * 0.125f;
+        qv[i][4] = x1.x * 0.125f; qv[i][5] = x1.y * 0.125f; qv[i][6] = x1.z * 0.125f; qv[i][7] = x1.w * 0.125f;
+    }
+    const int max_key = p.kv.max_pages_per_seq * p.kv.page_size - 1;
+    float kf[NJ][8], vf[NJ][8];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+        const size_t off = p.kv.offset(b, min(kb + kg + 32 * j, max_key), 0, head) + dc * 8;
+        KVRow<KVT>::load8(pool + off, kf[j]);
+        KVRow<KVT>::load8(pool + off + vstride, vf[j]);
+    }
+    if (nrows <= 0) return;
+    const int kend = pos0 + nrows;
+    if (kb >= kend) return;
+    const int ke = min(kb + p.split_len, kend);
+#pragma unroll
+    for (int i = 0; i < QT; ++i)
+        if (i >= nrows)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) qv[i][e] = 0.f;
+    float m_run[QT], l_run[QT], acc[QT][8];
+#pragma unroll
+    for (int i = 0; i < QT; ++i) {
+        m_run[i] = -INFINITY;
+        l_run[i] = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[i][e] = 0.f;
+    }
+    for (int c0 = kb; c0 < ke; c0 += 256) {
+        const int cn = min(256, ke - c0);
+        if (c0 != kb) {
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) {
+                const size_t off = p.kv.offset(b, min(c0 + kg + 32 * j, max_key), 0, head) + dc * 8;
+                KVRow<KVT>::load8(pool + off, kf[j]);
+                KVRow<KVT>::load8(pool + off + vstride, vf[j]);
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+            const int kk = kg + 32 * j;
+            float sc[QT];
+#pragma unroll
+            for (int i = 0; i < QT; ++i) {
+                float s = 0.f;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) s = fmaf(qv[i][e], kf[j][e], s);
+                sc[i] = sum8(s);
+            }
+            if (dc == 0 && kk < cn) {
+#pragma unroll
+                for (int i = 0; i < QT; ++i) s_p[i][kk] = (c0 + kk <= pos0 + i) ? sc[i] : -INFINITY;
+            }
+        }
+        __syncthreads();
+        float v[QT];
+#pragma unroll
+        for (int i = 0; i < QT; ++i) {
+            v[i] = (tid < cn) ? s_p[i][tid] : -INFINITY;
+            const float mx = wave_max(v[i]);
+            if (lane == 0) s_red[wave][i] = mx;
+        }
+        __syncthreads();
+        float mnew[QT], scale[QT], pr[QT];
+#pragma unroll
+        for (int i = 0; i < QT; ++i) {
+            const float cm = fmaxf(fmaxf(s_red[0][i], s_red[1][i]), fmaxf(s_red[2][i], s_red[3][i]));
+            mnew[i] = fmaxf(m_run[i], cm);
+            scale[i] = (m_run[i] == -INFINITY) ? 0.f : __expf(m_run[i] - mnew[i]);
+            pr[i] = (v[i] == -INFINITY) ? 0.f : __expf(v[i] - mnew[i]);
+        }
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < QT; ++i) {
+            if (tid < cn) s_p[i][tid] = pr[i];
+            const float sm = wave_sum(pr[i]);
+            if (lane == 0) s_red[wave][i] = sm;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < QT; ++i) {
+            const float cs = (s_red[0][i] + s_red[1][i]) + (s_red[2][i] + s_red[3][i]);
+            l_run[i] = l_run[i] * scale[i] + cs;
+            m_run[i] = mnew[i];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) acc[i][e] *= scale[i];
+        }
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+            const int kk = kg + 32 * j;
+            if (kk < cn) {
+#pragma unroll
+                for (int i = 0; i < QT; ++i) {
+                    const float pp = s_p[i][kk];
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) acc[i][e] = fmaf(pp, vf[j][e], acc[i][e]);
+                }
+            }
+        }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int i = 0; i < QT; ++i)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            acc[i][e] = sum_stride8(acc[i][e]);
+        }
+    if (lane < 8) {
+#pragma unroll
+        for (int i = 0; i < QT; ++i)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) s_acc[wave][i][dc * 8 + e] = acc[i][e];
+    }
+    __syncthreads();
+    if (p.n_splits == 1) {
+        OutT* out = reinterpret_cast<OutT*>(p.out);
+        for (int idx = tid; idx < QT * 64; idx += 256) {
+            const int i = idx >> 6, dim = idx & 63;
+            if (i >= nrows) continue;
+            const float o = (s_acc[0][i][dim] + s_acc[1][i][dim]) + (s_acc[2][i][dim] + s_acc[3][i][dim]);
+            ActIO<OutT>::store(out + (size_t)(b * p.Q + i) * p.ldo + head * 64 + dim, o / l_run[i]);
+        }
+        return;
+    }
+    float* mine = p.part + ((size_t)(b * H + head) * p.n_splits + split) * (QT * PSTRIDE);
+    for (int idx = tid; idx < QT * 64; idx += 256) {
+        const int i = idx >> 6, dim = idx & 63;
+        if (i >= nrows) continue;
+        mine[i * PSTRIDE + 4 + dim] = (s_acc[0][i][dim] + s_acc[1][i][dim]) + (s_acc[2][i][dim] + s_acc[3][i][dim]);
+        if (dim == 0) {
+            mine[i * PSTRIDE] = m_run[i];
+            mine[i * PSTRIDE + 1] = l_run[i];
+        }
+    }
+}
+
+// Merge of the split partials: one workgroup per (sequence, head).
+template <typename OutT>
+__global__ __launch_bounds__(256) void attn_decode_merge(AttnDecArgs p) {
+    const int b = blockIdx.x, head = blockIdx.y, H = gridDim.y;
+    const int qt = p.qt;
+    __shared__ float s_w[64][MTP_ATTN_QT];
+    __shared__ float s_l[MTP_ATTN_QT];
+    const int nrows = p.st[b].pend_len;
+    if (nrows <= 0) return;
+    const int kend = p.st[b].ctx_len + nrows;
+    const int n_active = min(p.n_splits, (kend + p.split_len - 1) / p.split_len);
+    const float* base = p.part + (size_t)(b * H + head) * p.n_splits * (qt * PSTRIDE);
+    // (max, sum) of every (split, row) into LDS
+    for (int idx = threadIdx.x; idx < n_active * qt; idx += blockDim.x) {
+        const int s = idx / qt, i = idx - s * qt;
+        s_w[s][i] = (i < nrows) ? base[(size_t)s * qt * PSTRIDE + i * PSTRIDE] : 0.f;
+    }
+    __syncthreads();
+    if (threadIdx.x < qt && (int)threadIdx.x < nrows) {
+        const int i = threadIdx.x;
+        float M = -INFINITY;
+        for (int s = 0; s < n_active; ++s) M = fmaxf(M, s_w[s][i]);
+        float L = 0.f;
+        for (int s = 0; s < n_active; ++s) {
+            const float w = (s_w[s][i] == -INFINITY) ? 0.f : __expf(s_w[s][i] - M);
+            L = fmaf(w, base[(size_t)s * qt * PSTRIDE + i * PSTRIDE + 1], L);
+            s_w[s][i] = w;
+        }
+        s_l[i] = L;
+    }
+    __syncthreads();
+    OutT* out = reinterpret_cast<OutT*>(p.out);
+    for (int idx = threadIdx.x; idx < qt * 64; idx += blockDim.x) {
+        const int i = idx >> 6, dim = idx & 63;
+        if (i >= nrows) continue;
+        float o = 0.f;
+#pragma unroll 8
+        for (int s = 0; s < n_active; ++s) o = fmaf(s_w[s][i], base[(size_t)s * qt * PSTRIDE + i * PSTRIDE + 4 + dim], o);
+        ActIO<OutT>::store(out + (size_t)(b * p.Q + i) * p.ldo + head * 64 + dim, o / s_l[i]);
+    }
+}
+
+template <typename KVT, typename OutT>
+static hipError_t attn_dec_launch(hipStream_t st, const AttnDecArgs& a) {
+    dim3 grid(a.B, a.kv.n_heads, a.n_splits);
+    switch (a.qt) {
+    case 1: hipLaunchKernelGGL((attn_decode_kernel<KVT, OutT, 1>), grid, dim3(256), 0, st, a); break;
+    case 2: hipLaunchKernelGGL((attn_decode_kernel<KVT, OutT, 2>), grid, dim3(256), 0, st, a); break;
+    case 4: hipLaunchKernelGGL((attn_decode_kernel<KVT, OutT, 4>), grid, dim3(256), 0, st, a); break;
+    case 8: hipLaunchKernelGGL((attn_decode_kernel<KVT, OutT, 8>), grid, dim3(256), 0, st, a); break;
+    default: return hipErrorInvalidValue;
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || a.n_splits == 1 || !a.merge) return e;
+    hipLaunchKernelGGL((attn_decode_merge<OutT>), dim3(a.B, a.kv.n_heads), dim3(256), 0, st, a);
+    return hipGetLastError();
+}
+
+hipError_t attention_decode_merge(hipStream_t st, const AttnDecArgs& a) {
+    if (a.n_splits <= 1) return hipSuccess;
+    if (a.dtype == 1) hipLaunchKernelGGL((attn_decode_merge<bf16_t>), dim3(a.B, a.kv.n_heads), dim3(256), 0, st, a);
+    else hipLaunchKernelGGL((attn_decode_merge<float>), dim3(a.B, a.kv.n_heads), dim3(256), 0, st, a);
+    return hipGetLastError();
+}
+
+hipError_t attention_decode(hipStream_t st, const AttnDecArgs& a) {
+    if (a.split_len < 32 || a.split_len % 32 || a.n_splits < 1 || a.n_splits > 64) return hipErrorInvalidValue;
+    if (a.dtype == 1) return attn_dec_launch<bf16_t, bf16_t>(st, a);
+    return attn_dec_launch<float, float>(st, a);
 }
 
 }  // namespace mtp

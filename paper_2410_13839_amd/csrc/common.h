@@ -62,7 +62,10 @@ __device__ __forceinline__ float gelu_erf(float x) {
     return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f));
 }
 
-// Paged KV addressing.  Pool layout: [layer][page][kv(0=K,1=V)][head][slot][64].
+// Paged KV addressing.  Pool layout: [layer][page][kv(0=K,1=V)][head][P*64]
+// where the K block is [slot][64] (one key per row) and the V block is
+// [slot][64] for fp32 caches but transposed, [64][slot], for bf16 caches, so
+// that 8 consecutive keys of one dimension are one 16-byte MFMA operand.
 struct KVView {
     void* pool;
     const int32_t* block_table;  // [batch][max_pages_per_seq]
@@ -78,5 +81,12 @@ struct KVView {
         int slot = pos & (page_size - 1);
         size_t base = (((size_t)layer * num_pages + page) * 2 + kv) * (size_t)n_heads;
         return ((base + head) * page_size + slot) * MTP_HEAD_DIM;
+    }
+    // element (dim) of the transposed V block of key `pos`: base + dim * page_size
+    __device__ __forceinline__ size_t vt_offset(int seq, int pos, int head) const {
+        int page = block_table[(size_t)seq * max_pages_per_seq + (pos >> page_shift)];
+        int slot = pos & (page_size - 1);
+        size_t base = (((size_t)layer * num_pages + page) * 2 + 1) * (size_t)n_heads;
+        return (base + head) * page_size * MTP_HEAD_DIM + slot;
     }
 };

@@ -35,6 +35,17 @@ struct EpiQKV {
         RowInfo ri = rows[m];
         if (ri.pos < 0) return;
         int c = n - sec * d;
+        if constexpr (sizeof(KVT) == 2) {
+            if (sec == 2) {   // transposed V block
+                bf16_t* vt = reinterpret_cast<bf16_t*>(kv.pool) + kv.vt_offset(ri.seq, ri.pos, c >> 6);
+                const int dim = c & 63;
+                vt[(size_t)(dim + 0) * kv.page_size] = f32_to_bf16(r0);
+                vt[(size_t)(dim + 1) * kv.page_size] = f32_to_bf16(r1);
+                vt[(size_t)(dim + 2) * kv.page_size] = f32_to_bf16(r2);
+                vt[(size_t)(dim + 3) * kv.page_size] = f32_to_bf16(r3);
+                return;
+            }
+        }
         KVT* dst = reinterpret_cast<KVT*>(kv.pool) + kv.offset(ri.seq, ri.pos, sec - 1, c >> 6) + (c & 63);
         if constexpr (sizeof(KVT) == 2) {
             uint2 pk;

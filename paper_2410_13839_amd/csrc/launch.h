@@ -8,7 +8,7 @@
 
 namespace mtp {
 
-enum EpiKind { EPI_QKV = 0, EPI_GELU = 1, EPI_PARTIAL = 2, EPI_LOGITS = 3 };
+enum EpiKind { EPI_QKV = 0, EPI_GELU = 1, EPI_PARTIAL = 2, EPI_LOGITS = 3, EPI_RESID = 4 };
 
 struct GemmArgs {
     int dtype;            // 0 fp32, 1 bf16 (both X and W)
@@ -39,6 +39,63 @@ struct AttnArgs {
     float* part;               // split partials when n_splits > 1
 };
 hipError_t attention(hipStream_t st, const AttnArgs& a);
+
+// Decode attention: the pending chunk of each sequence (rows b*Q .. b*Q +
+// pend_len - 1) over its cache in splits of split_len keys.  With several
+// splits the partials are merged by attn_decode_merge when `merge` is set,
+// otherwise by the consumer (out-projection prologue, GemvArgs xmode 4).
+struct AttnDecArgs {
+    int dtype;
+    int B; int Q; int qt;
+    const SeqState* st;
+    const float* q; int ldq;
+    KVView kv;
+    int split_len; int n_splits;
+    void* out; int ldo;
+    float* part;               // [B][H][n_splits][qt][66]
+    int merge;                 // 1: launch the merge kernel after the splits
+};
+hipError_t attention_decode(hipStream_t st, const AttnDecArgs& a);
+// Only the merge of decode split partials (after attention_mfma).
+hipError_t attention_decode_merge(hipStream_t st, const AttnDecArgs& a);
+
+// MFMA attention for bf16 caches: mode 0 = decode (one tile per sequence, rows
+// from the sequence state), mode 1 = prefill (tiles of up to 16 rows).
+struct AttnMfmaArgs {
+    int mode;
+    int n_tiles;
+    int Q; int qt;
+    const SeqState* st;
+    const int2* tiles; const RowInfo* rows;
+    const float* q; int ldq;
+    KVView kv;
+    int split_len; int n_splits;
+    bf16_t* out; int ldo;
+    float* part;
+};
+hipError_t attention_mfma(hipStream_t st, const AttnMfmaArgs& a);
+
+// Small-M (<= 32) bf16 projection with fused row work; see gemv.hip.
+struct GemvArgs {
+    int epi;                   // EPI_QKV, EPI_GELU, EPI_RESID, EPI_LOGITS
+    int xmode;                 // 0 bf16 rows, 1 LN(h), 2 embed + LN, 3 final LN (heads),
+                               // 4 merge of decode-attention split partials
+    int M, N, K, splits;
+    const bf16_t* W;
+    const bf16_t* x; int ldx;                       // xmode 0
+    const float* h; int ldh;                        // xmode 1, 3
+    const float* g; const float* beta;              // LN gain / shift
+    const SeqState* st; int Q;                      // xmode 2, 3 and EPI_QKV
+    const bf16_t* emb; const bf16_t* pos;           // xmode 2
+    float* h_out;                                   // xmode 2: embedded rows written here
+    const float* hz;                                // xmode 3: last prefill hidden state
+    const float* bias;
+    void* out; int ldo;                             // EPI_GELU / EPI_LOGITS output, EPI_RESID ld
+    float* q; KVView kv; int d;                     // EPI_QKV
+    float* h_res;                                   // EPI_RESID target
+    const float* apart; int qt; int split_len; int n_splits;  // xmode 4
+};
+hipError_t gemv(hipStream_t st, const GemvArgs& a);
 
 // Row embedding (+ first LayerNorm).  mode 0: decode rows derived from the
 // sequence state (Q rows per sequence); mode 1: prefill rows given by
@@ -100,6 +157,8 @@ struct SelectArgs {
     int32_t* hist; int hist_ld;  // [B][max_new]
 };
 hipError_t topk(hipStream_t st, const SelectArgs& a);
+// top_k of all K heads, Viterbi and accept in one launch (one workgroup per sequence).
+hipError_t select_fused(hipStream_t st, const SelectArgs& a);
 hipError_t viterbi_accept(hipStream_t st, const SelectArgs& a);
 
 }  // namespace mtp

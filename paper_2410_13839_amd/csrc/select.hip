@@ -12,6 +12,7 @@
 
 #include "common.h"
 #include "launch.h"
+#include "wave.h"
 
 namespace mtp {
 
@@ -158,6 +159,150 @@ hipError_t topk(hipStream_t st, const SelectArgs& a) {
 
 hipError_t viterbi_accept(hipStream_t st, const SelectArgs& a) {
     hipLaunchKernelGGL(viterbi_accept_kernel, dim3(a.B), dim3(64), 0, st, a);
+    return hipGetLastError();
+}
+
+}  // namespace mtp
+
+// ---------------------------------------------------------------- fused
+// One workgroup per sequence, one wave per head: top_k of every head in
+// parallel, then all (K-1) x top_k x top_k transition entries are gathered
+// into LDS at once, then wave 0 runs the recursion, the backtrack and the
+// accept rule.  Same arithmetic and tie rules as the two kernels above.
+namespace mtp {
+
+__global__ __launch_bounds__(512) void select_fused_kernel(SelectArgs a) {
+    const int b = blockIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63, t = tid >> 6;
+    const int K = a.K, k = a.top_k, V = a.V;
+    __shared__ int s_cand[MTP_MAX_HEADS_K][MTP_MAX_TOPK];
+    __shared__ float s_ehat[MTP_MAX_HEADS_K][MTP_MAX_TOPK];
+    __shared__ float s_T[MTP_MAX_HEADS_K - 1][MTP_MAX_TOPK][MTP_MAX_TOPK];
+    __shared__ int s_psi[MTP_MAX_HEADS_K][MTP_MAX_TOPK];
+    __shared__ float s_delta[MTP_MAX_TOPK];
+    const SeqState st0 = a.st[b];
+    const size_t base = (size_t)b * K * k;
+
+    // top_k of head t (wave t)
+    {
+        const float* lg = a.logits + (size_t)b * a.ld_logits + (size_t)t * V;
+        const bool mask_eos = (st0.gen + t) < a.eos_min;
+        // unconditional loads from clamped indices (a predicated load would
+        // become a branch and a full wait per element); entries past the
+        // vocabulary are excluded by the idx < V test of the selection
+        float v[PER_LANE];
+#pragma unroll
+        for (int j = 0; j < PER_LANE; ++j) v[j] = lg[min(lane + 64 * j, V - 1)];
+#pragma unroll
+        for (int j = 0; j < PER_LANE; ++j)
+            if (lane + 64 * j == a.eos_id && mask_eos) v[j] = -INFINITY;
+        uint32_t taken = 0;
+        float top0 = 0.f;
+        for (int r = 0; r < k; ++r) {
+            float bv = -INFINITY;
+            int bi = INT_MAX;
+#pragma unroll
+            for (int j = 0; j < PER_LANE; ++j) {
+                const int idx = lane + 64 * j;
+                if (idx < V && !((taken >> j) & 1u) && better(v[j], idx, bv, bi)) {
+                    bv = v[j];
+                    bi = idx;
+                }
+            }
+            wave_argmax(bv, bi);
+            if ((bi & 63) == lane) taken |= 1u << (bi >> 6);
+            if (r == 0) top0 = bv;
+            if (lane == 0) {
+                const float e = bv - top0;
+                s_cand[t][r] = bi;
+                s_ehat[t][r] = e;
+                a.cand[base + t * k + r] = bi;
+                a.ehat[base + t * k + r] = e;
+            }
+        }
+    }
+    __syncthreads();
+    // transition sub-tables T[t-1][i][j] = logQ[c_{t-1,i}][c_{t,j}]
+    const int kk = k * k;
+    for (int idx = tid; idx < (K - 1) * kk; idx += blockDim.x) {
+        const int t1 = idx / kk, rem = idx - t1 * kk;
+        const int i = rem / k, j = rem - i * k;
+        s_T[t1][i][j] = a.logq[(size_t)s_cand[t1][i] * V + s_cand[t1 + 1][j]];
+    }
+    __syncthreads();
+    if (t != 0) return;
+
+    const int j = lane;
+    float delta = (j < k) ? s_ehat[0][j] : -INFINITY;
+    if (j < k) {
+        a.delta[base + j] = delta;
+        a.psi[base + j] = 0;
+    }
+    for (int tt = 1; tt < K; ++tt) {
+        float best = 0.f;
+        int arg = 0;
+        if (j < MTP_MAX_TOPK) s_delta[j] = delta;
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+        __builtin_amdgcn_wave_barrier();
+        for (int i = 0; i < k; ++i) {
+            const float di = s_delta[i];
+            const float s = di + s_T[tt - 1][i][j < k ? j : 0];
+            if (i == 0 || s > best) {
+                best = s;
+                arg = i;
+            }
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+        __builtin_amdgcn_wave_barrier();
+        delta = (j < k) ? best + s_ehat[tt][j] : -INFINITY;
+        if (j < k) {
+            a.delta[base + tt * k + j] = delta;
+            a.psi[base + tt * k + j] = arg;
+            s_psi[tt][j] = arg;
+        }
+    }
+    float bestd = (j < k) ? delta : -INFINITY;
+    int last = (j < k) ? j : MTP_MAX_TOPK + j;
+    wave_argmax(bestd, last);
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __builtin_amdgcn_wave_barrier();
+    if (j != 0) return;
+
+    int slots[MTP_MAX_HEADS_K], toks[MTP_MAX_HEADS_K];
+    slots[K - 1] = last;
+    for (int tt = K - 1; tt > 0; --tt) slots[tt - 1] = s_psi[tt][slots[tt]];
+    for (int tt = 0; tt < K; ++tt) {
+        toks[tt] = s_cand[tt][slots[tt]];
+        a.slots[(size_t)b * K + tt] = slots[tt];
+    }
+    SeqState s = st0;
+    int n = 0;
+    bool done = s.done != 0;
+    if (!done) {
+        n = min(K, a.max_new - s.gen);
+        for (int p = 0; p < n; ++p) {
+            if (toks[p] == a.eos_id) {
+                n = p + 1;
+                done = true;
+                break;
+            }
+        }
+        if (s.gen + n >= a.max_new) done = true;
+    }
+    for (int tt = 0; tt < K; ++tt) a.out_tokens[(size_t)b * K + tt] = (tt < n) ? toks[tt] : -1;
+    a.out_count[b] = n;
+    for (int tt = 0; tt < n; ++tt) a.hist[(size_t)b * a.hist_ld + s.gen + tt] = toks[tt];
+    s.ctx_len += s.pend_len;
+    s.gen += n;
+    s.done = done ? 1 : 0;
+    s.pend_len = done ? 0 : n;
+    for (int tt = 0; tt < n && tt < MTP_MAX_HEADS_K; ++tt) s.pend_ids[tt] = toks[tt];
+    s.steps += 1;
+    a.st[b] = s;
+}
+
+hipError_t select_fused(hipStream_t st, const SelectArgs& a) {
+    hipLaunchKernelGGL(select_fused_kernel, dim3(a.B), dim3(64 * a.K), 0, st, a);
     return hipGetLastError();
 }
 

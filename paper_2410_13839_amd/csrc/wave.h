@@ -1,0 +1,92 @@
+// Wavefront reductions for wave64 on gfx950.
+//
+// Steps inside a 16-lane row use DPP (quad_perm, row_half_mirror, row_ror),
+// which are plain VALU operands instead of LDS permutes; only the two steps
+// that cross rows go through ds_swizzle/bpermute.  Every lane of a group ends
+// with the same value: each step combines a lane with a partner that holds
+// the mirrored partial, and IEEE add/max are commutative.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+namespace mtp {
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+template <int CTRL>
+__device__ __forceinline__ int dpp_i(int v) {
+    return __builtin_amdgcn_mov_dpp(v, CTRL, 0xF, 0xF, false);
+}
+
+constexpr int DPP_XOR1 = 0xB1;          // quad_perm [1,0,3,2]
+constexpr int DPP_XOR2 = 0x4E;          // quad_perm [2,3,0,1]
+constexpr int DPP_HALF_MIRROR = 0x141;  // lane i <-> 7 - i within each 8 lanes
+constexpr int DPP_ROR8 = 0x128;         // rotate a 16-lane row by 8
+
+// Sum over each aligned group of 8 lanes.
+__device__ __forceinline__ float sum8(float v) {
+    v += dpp_f<DPP_XOR1>(v);
+    v += dpp_f<DPP_XOR2>(v);
+    v += dpp_f<DPP_HALF_MIRROR>(v);
+    return v;
+}
+__device__ __forceinline__ float sum16(float v) {
+    v = sum8(v);
+    v += dpp_f<DPP_ROR8>(v);
+    return v;
+}
+__device__ __forceinline__ float wave_sum64(float v) {
+    v = sum16(v);
+    v += __shfl_xor(v, 16);
+    v += __shfl_xor(v, 32);
+    return v;
+}
+__device__ __forceinline__ float max16(float v) {
+    v = fmaxf(v, dpp_f<DPP_XOR1>(v));
+    v = fmaxf(v, dpp_f<DPP_XOR2>(v));
+    v = fmaxf(v, dpp_f<DPP_HALF_MIRROR>(v));
+    v = fmaxf(v, dpp_f<DPP_ROR8>(v));
+    return v;
+}
+__device__ __forceinline__ float wave_max64(float v) {
+    v = max16(v);
+    v = fmaxf(v, __shfl_xor(v, 16));
+    v = fmaxf(v, __shfl_xor(v, 32));
+    return v;
+}
+// Sum over lanes that are 8, 16 and 32 apart (lanes with equal lane % 8).
+__device__ __forceinline__ float sum_stride8(float v) {
+    v += dpp_f<DPP_ROR8>(v);
+    v += __shfl_xor(v, 16);
+    v += __shfl_xor(v, 32);
+    return v;
+}
+
+// (value, index) maximum over the wave under the total order "larger value,
+// then smaller index"; every lane ends with the winner.
+__device__ __forceinline__ bool vi_better(float va, int ia, float vb, int ib) {
+    return va > vb || (va == vb && ia < ib);
+}
+template <int CTRL>
+__device__ __forceinline__ void vi_step_dpp(float& v, int& i) {
+    const float ov = dpp_f<CTRL>(v);
+    const int oi = dpp_i<CTRL>(i);
+    if (vi_better(ov, oi, v, i)) { v = ov; i = oi; }
+}
+__device__ __forceinline__ void vi_step_shfl(float& v, int& i, int mask) {
+    const float ov = __shfl_xor(v, mask);
+    const int oi = __shfl_xor(i, mask);
+    if (vi_better(ov, oi, v, i)) { v = ov; i = oi; }
+}
+__device__ __forceinline__ void wave_argmax(float& v, int& i) {
+    vi_step_dpp<DPP_XOR1>(v, i);
+    vi_step_dpp<DPP_XOR2>(v, i);
+    vi_step_dpp<DPP_HALF_MIRROR>(v, i);
+    vi_step_dpp<DPP_ROR8>(v, i);
+    vi_step_shfl(v, i, 16);
+    vi_step_shfl(v, i, 32);
+}
+
+}  // namespace mtp

@@ -92,8 +92,11 @@ def test_calls_validate_before_gpu_work():
             b.mtp_prefill(ctx, [np.full(2, 512, np.int32)], [np.zeros(3, np.int32)])
         assert e.value.code == b.MTP_EINVAL
         with pytest.raises(b.MTPError) as e:
-            b.mtp_profile(ctx, 99, True)
+            b.mtp_profile_replay(ctx, 99, 10)
         assert e.value.code == b.MTP_EINVAL
+        with pytest.raises(b.MTPError) as e:       # nothing launched yet
+            b.mtp_profile_replay(ctx, b.MTP_KCLASS_GEMM_FFN1, 10)
+        assert e.value.code == b.MTP_ESTATE
     finally:
         b.mtp_destroy(ctx)
 
