@@ -182,22 +182,27 @@ int mtp_get_seq_state(mtp_ctx* ctx, int32_t* ctx_len, int32_t* pend_len,
  * unspecified. */
 int mtp_get_tokens(mtp_ctx* ctx, int32_t* tokens);
 
-/* Kernel timing for measurement.  Re-launches the most recent launch of kernel
- * class `kclass` (MTP_KCLASS_*) `iters` times back to back on the context
- * stream, bracketed by two HIP events, and returns the average time per
- * launch in microseconds (synchronises).  The replayed launch keeps its
- * arguments: QKV, FFN1, attention and heads launches rewrite the same outputs
- * from the same inputs, but the out-projection and FFN2 launches add into
- * the residual stream again, so replaying those leaves the sequence state
- * unusable until the next mtp_prefill.  MTP_ESTATE if the class has not been
- * launched since the context was created. */
+/* Kernel timing for measurement.  Replays the launches of kernel class
+ * `kclass` (MTP_KCLASS_*) recorded for the most recent decode step (one per
+ * layer, or one for the heads), in order, `iters` times on the context
+ * stream; each pass is bracketed by two HIP events and, with `cold` != 0,
+ * preceded (outside the events) by a read of a 512 MiB buffer that evicts the
+ * weights from the L2 and last-level caches, as in a real step where the
+ * other layers' weights pass through them between two launches of a class.
+ * Returns the average time per launch in microseconds (synchronises; one
+ * launch latency per pass is included).  The replayed launches keep their
+ * arguments and may overwrite the residual stream and the cache rows of the
+ * next positions: the context needs mtp_prefill before the next decode step
+ * (MTP_ESTATE otherwise).  The first cold call allocates the eviction buffer
+ * (freed by mtp_destroy).  MTP_ESTATE if the last step launched nothing of
+ * the class. */
 #define MTP_KCLASS_GEMM_FFN1   1   /* LN2 -> x W_1^T -> GELU                  */
-#define MTP_KCLASS_GEMM_FFN2   2   /* GELU out x W_2^T + residual             */
+#define MTP_KCLASS_GEMM_FFN2   2   /* GELU out x W_2^T (residual partials)    */
 #define MTP_KCLASS_GEMM_QKV    3   /* LN1 -> x W_qkv^T, K/V into the cache    */
 #define MTP_KCLASS_ATTENTION   4   /* decode attention over the paged cache   */
 #define MTP_KCLASS_HEADS       5   /* final LN -> K head projections          */
-#define MTP_KCLASS_GEMM_OPROJ  6   /* attention out x W_o^T + residual        */
-int mtp_profile_replay(mtp_ctx* ctx, int kclass, int iters, double* avg_us);
+#define MTP_KCLASS_GEMM_OPROJ  6   /* attention out x W_o^T (residual part.)  */
+int mtp_profile_replay(mtp_ctx* ctx, int kclass, int iters, int cold, double* avg_us);
 
 /* Drops all sequence state (the next call must be mtp_prefill). */
 int mtp_reset(mtp_ctx* ctx);

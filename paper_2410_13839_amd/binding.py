@@ -66,7 +66,7 @@ _lib.mtp_get_logits.argtypes = [_ctx, _f32p]
 _lib.mtp_get_lattice.argtypes = [_ctx, _i32p, _f32p, _f32p, _i32p, _i32p]
 _lib.mtp_get_seq_state.argtypes = [_ctx, _i32p, _i32p, _i32p, _i32p]
 _lib.mtp_get_tokens.argtypes = [_ctx, _i32p]
-_lib.mtp_profile_replay.argtypes = [_ctx, ctypes.c_int, ctypes.c_int, _P(ctypes.c_double)]
+_lib.mtp_profile_replay.argtypes = [_ctx, ctypes.c_int, ctypes.c_int, ctypes.c_int, _P(ctypes.c_double)]
 _lib.mtp_reset.argtypes = [_ctx]
 _lib.mtp_destroy.argtypes = [_ctx]
 _lib.mtp_destroy.restype = None
@@ -166,9 +166,9 @@ def mtp_get_tokens(ctx, B: int, max_new: int) -> np.ndarray:
     return out
 
 
-def mtp_profile_replay(ctx, kclass: int, iters: int) -> float:
+def mtp_profile_replay(ctx, kclass: int, iters: int, cold: bool = True) -> float:
     us = ctypes.c_double()
-    _check(_lib.mtp_profile_replay(ctx, kclass, iters, ctypes.byref(us)), ctx, "mtp_profile_replay")
+    _check(_lib.mtp_profile_replay(ctx, kclass, iters, int(cold), ctypes.byref(us)), ctx, "mtp_profile_replay")
     return us.value
 
 

@@ -102,7 +102,7 @@ int validate(const mtp_config* c, std::string* why) {
 }
 
 struct WsLayout {
-    uint64_t rows, ids, tiles, last_row, state, btab, h, q, u, attn, ffn, part, apart, hz, z, logits, cand, ehat,
+    uint64_t rows, ids, tiles, last_row, state, btab, h, h2, q, u, attn, ffn, part, apart, hz, z, logits, cand, ehat,
         delta, psi, slots, out_tok, out_cnt, hist, total;
     int64_t m_pre, m_dec, m_max, max_tiles, max_splits, maxp, num_pages;
     int act_bytes;
@@ -130,6 +130,7 @@ WsLayout ws_layout(const mtp_config& c) {
     w.state = take(B * sizeof(SeqState));
     w.btab = take(B * w.maxp * 4);
     w.h = take(w.m_max * d * 4);
+    w.h2 = take(w.m_dec * d * 4);                 // second residual buffer of the fused decode trunk
     w.q = take(w.m_max * d * 4);
     w.u = take(w.m_max * d * w.act_bytes);
     w.attn = take(w.m_max * d * w.act_bytes);
@@ -176,10 +177,17 @@ struct mtp_ctx {
     std::vector<SeqState> h_state;
     int n_pre_rows = 0, n_pre_tiles = 0;
     // graphs keyed by (K, top_k, q_pad, batch, split_len, n_splits)
-    std::map<std::tuple<int, int, int, int, int, int>, hipGraphExec_t> graphs;
-    // last launch of each kernel class (arguments captured by value), for
-    // back-to-back replay timing
-    std::function<hipError_t(hipStream_t)> last_launch[8];
+    using StepKey = std::tuple<int, int, int, int, int, int>;
+    std::map<StepKey, hipGraphExec_t> graphs;
+    // every launch of each kernel class in the step of a key (arguments
+    // captured by value), for replay timing
+    using Launch = std::function<hipError_t(hipStream_t)>;
+    struct StepLaunches { std::vector<Launch> cls[8]; };
+    std::map<StepKey, StepLaunches> step_launches;
+    StepLaunches* recording = nullptr;
+    StepKey last_key{};
+    bool has_last = false;
+    void* flush_buf = nullptr;   // cache eviction source of cold replays
 
     char* W() const { return (char*)buf.weights; }
     char* WS() const { return (char*)buf.workspace; }
@@ -225,10 +233,10 @@ int pick_splits(const mtp_ctx* c, int M, int N, int K) {
     return s;
 }
 
-// Launch through `f` and remember it as the last launch of class `kclass`.
+// Launch through `f` and, while a step is being recorded, keep it under class `kclass`.
 hipError_t launch_rec(mtp_ctx* c, int kclass, std::function<hipError_t(hipStream_t)> f) {
     hipError_t e = f(c->stream);
-    if (kclass > 0 && kclass < 8) c->last_launch[kclass] = std::move(f);
+    if (kclass > 0 && kclass < 8 && c->recording) c->recording->cls[kclass].push_back(std::move(f));
     return e;
 }
 
@@ -261,23 +269,36 @@ hipError_t decode_attention(mtp_ctx* c, int l, int qt, bool merge_launch) {
 // Whether the out-projection prologue merges the attention split partials
 // itself (small batches) instead of a separate merge launch.
 bool prologue_merge(const mtp_ctx* c, int rows) {
-    if (c->n_splits <= 1 || c->n_splits > 8) return false;
-    const int64_t bytes = (int64_t)rows * c->cfg.n_heads * c->n_splits * 68 * 4;
-    return bytes <= 96 * 1024;
+    return c->n_splits >= 2 && c->n_splits <= gemv_merge_max_splits(rows, c->cfg.d_model);
 }
 
-// One layer of the fused small-M decode trunk (bf16, B*Q <= 32 rows).
-int run_layer_fused(mtp_ctx* c, int l, int rows, int qt) {
+// One layer of the fused small-M decode trunk (bf16, B*Q <= 16 rows).  The
+// residual stream alternates between two buffers: the out-projection and FFN2
+// leave four split-K partial sums, and the next LayerNorm consumer (FFN1, the
+// next layer's QKV, the heads) adds them and the bias to its input rows and
+// writes the completed rows to the other buffer.  `hcur` is the buffer holding
+// the layer's input rows before the call and the output rows after it (still
+// missing the FFN2 partials, whose bias is B_2 of this layer).
+int run_layer_fused(mtp_ctx* c, int l, int rows, int qt, float*& hcur) {
     const mtp_config& cf = c->cfg;
     const int d = cf.d_model, F = cf.d_ff;
-    hipStream_t st = c->stream;
-    float* h = c->ws_ptr<float>(c->ws.h);
+    float* ha = c->ws_ptr<float>(c->ws.h);
+    float* hb = c->ws_ptr<float>(c->ws.h2);
+    float* part = c->ws_ptr<float>(c->ws.part);
+    float* hnext = (hcur == ha) ? hb : ha;
     GemvArgs g{};
-    g.epi = EPI_QKV; g.xmode = (l == 0) ? 2 : 1; g.M = rows; g.N = 3 * d; g.K = d; g.splits = 1;
-    g.W = (const bf16_t*)c->lt(l, MTP_T_W_QKV); g.h = h; g.ldh = d;
+    g.epi = EPI_QKV; g.M = rows; g.N = 3 * d; g.K = d;
+    g.W = (const bf16_t*)c->lt(l, MTP_T_W_QKV); g.ldh = d;
+    if (l == 0) {
+        g.xmode = 2; g.h_out = hcur;
+        g.emb = (const bf16_t*)c->wt(MTP_T_EMB_AC); g.pos = (const bf16_t*)c->wt(MTP_T_POS);
+    } else {
+        g.xmode = 1; g.h = hcur; g.part = part; g.part_rows = rows; g.res_bias = (const float*)c->lt(l - 1, MTP_T_B_2);
+        g.h_out = hnext;
+        std::swap(hcur, hnext);
+    }
     g.g = (const float*)c->lt(l, MTP_T_LN1_G); g.beta = (const float*)c->lt(l, MTP_T_LN1_B);
     g.st = c->ws_ptr<SeqState>(c->ws.state); g.Q = c->q_pad;
-    g.emb = (const bf16_t*)c->wt(MTP_T_EMB_AC); g.pos = (const bf16_t*)c->wt(MTP_T_POS); g.h_out = h;
     g.bias = (const float*)c->lt(l, MTP_T_B_QKV); g.q = c->ws_ptr<float>(c->ws.q); g.kv = c->kv(l); g.d = d;
     HIPCHK(c, launch_rec(c, MTP_KCLASS_GEMM_QKV, [g](hipStream_t s) { return gemv(s, g); }), "qkv gemv");
 
@@ -285,24 +306,27 @@ int run_layer_fused(mtp_ctx* c, int l, int rows, int qt) {
     HIPCHK(c, decode_attention(c, l, qt, !pm), "decode attention");
 
     g = GemvArgs{};
-    g.epi = EPI_RESID; g.xmode = pm ? 4 : 0; g.M = rows; g.N = d; g.K = d; g.splits = 1;
+    g.epi = EPI_PARTIAL; g.xmode = pm ? 4 : 0; g.M = rows; g.N = d; g.K = d;
     g.W = (const bf16_t*)c->lt(l, MTP_T_W_O); g.x = (const bf16_t*)(c->WS() + c->ws.attn); g.ldx = d;
     g.st = c->ws_ptr<SeqState>(c->ws.state); g.Q = c->q_pad;
     g.apart = c->ws_ptr<float>(c->ws.apart); g.qt = qt; g.split_len = c->split_len; g.n_splits = c->n_splits;
-    g.bias = (const float*)c->lt(l, MTP_T_B_O); g.h_res = h; g.ldo = d;
+    g.part_out = part;
     HIPCHK(c, launch_rec(c, MTP_KCLASS_GEMM_OPROJ, [g](hipStream_t s) { return gemv(s, g); }), "out-proj gemv");
 
+    hnext = (hcur == ha) ? hb : ha;
     g = GemvArgs{};
-    g.epi = EPI_GELU; g.xmode = 1; g.M = rows; g.N = F; g.K = d; g.splits = 1;
-    g.W = (const bf16_t*)c->lt(l, MTP_T_W_1); g.h = h; g.ldh = d;
+    g.epi = EPI_GELU; g.xmode = 1; g.M = rows; g.N = F; g.K = d;
+    g.W = (const bf16_t*)c->lt(l, MTP_T_W_1); g.h = hcur; g.ldh = d;
+    g.part = part; g.part_rows = rows; g.res_bias = (const float*)c->lt(l, MTP_T_B_O); g.h_out = hnext;
     g.g = (const float*)c->lt(l, MTP_T_LN2_G); g.beta = (const float*)c->lt(l, MTP_T_LN2_B);
     g.bias = (const float*)c->lt(l, MTP_T_B_1); g.out = c->WS() + c->ws.ffn; g.ldo = F;
     HIPCHK(c, launch_rec(c, MTP_KCLASS_GEMM_FFN1, [g](hipStream_t s) { return gemv(s, g); }), "ffn1 gemv");
+    hcur = hnext;
 
     g = GemvArgs{};
-    g.epi = EPI_RESID; g.xmode = 0; g.M = rows; g.N = d; g.K = F; g.splits = 1;
+    g.epi = EPI_PARTIAL; g.xmode = 0; g.M = rows; g.N = d; g.K = F;
     g.W = (const bf16_t*)c->lt(l, MTP_T_W_2); g.x = (const bf16_t*)(c->WS() + c->ws.ffn); g.ldx = F;
-    g.bias = (const float*)c->lt(l, MTP_T_B_2); g.h_res = h; g.ldo = d;
+    g.part_out = part;
     HIPCHK(c, launch_rec(c, MTP_KCLASS_GEMM_FFN2, [g](hipStream_t s) { return gemv(s, g); }), "ffn2 gemv");
     return MTP_OK;
 }
@@ -379,14 +403,17 @@ int enqueue_step(mtp_ctx* c, int K, int top_k) {
     const mtp_config& cf = c->cfg;
     const int d = cf.d_model, dt = cf.dtype, B = c->B, Q = c->q_pad, V = cf.vocab;
     hipStream_t st = c->stream;
-    const bool small = dt == MTP_DTYPE_BF16 && B * Q <= 32;
+    const bool small = dt == MTP_DTYPE_BF16 && B * Q <= 16;
     int qt = 1;
     while (qt < Q) qt <<= 1;
+    float* hfin = c->ws_ptr<float>(c->ws.h);     // residual rows entering the heads
+    bool fin_part = false;                       // ... still missing the last FFN2 partials
     if (Q > 0 && small) {
         for (int l = 0; l < cf.n_layers; ++l) {
-            int rc = run_layer_fused(c, l, B * Q, qt);
+            int rc = run_layer_fused(c, l, B * Q, qt, hfin);
             if (rc) return rc;
         }
+        fin_part = true;
     } else if (Q > 0) {
         const int rows = B * Q;
         EmbedArgs e{};
@@ -401,10 +428,14 @@ int enqueue_step(mtp_ctx* c, int K, int top_k) {
             if (rc) return rc;
         }
     }
-    if (dt == MTP_DTYPE_BF16 && B <= 32) {
+    if (dt == MTP_DTYPE_BF16 && B <= 16) {
         GemvArgs g{};
-        g.epi = EPI_LOGITS; g.xmode = 3; g.M = B; g.N = K * V; g.K = d; g.splits = 1;
-        g.W = (const bf16_t*)c->wt(MTP_T_W_HEADS); g.h = c->ws_ptr<float>(c->ws.h); g.ldh = d;
+        g.epi = EPI_LOGITS; g.xmode = 3; g.M = B; g.N = K * V; g.K = d;
+        g.W = (const bf16_t*)c->wt(MTP_T_W_HEADS); g.h = hfin; g.ldh = d;
+        if (fin_part) {
+            g.part = c->ws_ptr<float>(c->ws.part); g.part_rows = B * Q;
+            g.res_bias = (const float*)c->lt(cf.n_layers - 1, MTP_T_B_2);
+        }
         g.hz = c->ws_ptr<float>(c->ws.hz); g.st = c->ws_ptr<SeqState>(c->ws.state); g.Q = Q;
         g.g = (const float*)c->wt(MTP_T_LNF_G); g.beta = (const float*)c->wt(MTP_T_LNF_B);
         g.bias = (const float*)c->wt(MTP_T_B_HEADS); g.out = c->WS() + c->ws.logits; g.ldo = K * V;
@@ -439,16 +470,25 @@ int step_common(mtp_ctx* c, int K, int top_k) {
     if (K < 1 || K > c->cfg.k_heads) { c->err = "K must be in 1..k_heads"; return MTP_EINVAL; }
     if (top_k < 1 || top_k > c->cfg.topk_max) { c->err = "top_k must be in 1..topk_max"; return MTP_EINVAL; }
     const bool use_graph = !(c->cfg.flags & MTP_FLAG_NO_GRAPH) && c->stream != nullptr;
+    const auto key = std::make_tuple(K, top_k, c->q_pad, c->B, c->split_len, c->n_splits);
+    auto record = [&]() {
+        mtp_ctx::StepLaunches& sl = c->step_launches[key];
+        for (auto& v : sl.cls) v.clear();
+        c->recording = &sl;
+        const int r = enqueue_step(c, K, top_k);
+        c->recording = nullptr;
+        return r;
+    };
+    c->has_last = false;
     int rc;
     if (!use_graph) {
-        rc = enqueue_step(c, K, top_k);
+        rc = record();
     } else {
-        auto key = std::make_tuple(K, top_k, c->q_pad, c->B, c->split_len, c->n_splits);
         auto it = c->graphs.find(key);
         if (it == c->graphs.end()) {
             hipGraph_t graph;
             HIPCHK(c, hipStreamBeginCapture(c->stream, hipStreamCaptureModeRelaxed), "begin capture");
-            rc = enqueue_step(c, K, top_k);
+            rc = record();
             hipError_t e = hipStreamEndCapture(c->stream, &graph);
             if (rc) { if (e == hipSuccess) (void)hipGraphDestroy(graph); return rc; }
             if (e != hipSuccess) return hip_fail(c, e, "end capture");
@@ -465,6 +505,8 @@ int step_common(mtp_ctx* c, int K, int top_k) {
         c->q_pad = K;
         c->last_K = K;
         c->last_topk = top_k;
+        c->last_key = key;
+        c->has_last = true;
     }
     return rc;
 }
@@ -616,20 +658,25 @@ int mtp_prefill(mtp_ctx* c, int B, const int32_t* phon, const int32_t* phon_len,
     HIPCHK(c, final_ln(st, f), "prefill last rows");
 
     // decode attention split plan, fixed for the batch so one captured graph
-    // serves every step: small batches split the keys so that the
-    // out-projection prologue can merge the partials (at most 96 KB of them
-    // per workgroup); larger batches aim at ~512 (sequence, head, split)
-    // workgroups and merge in a separate launch.
+    // serves every step: small batches split the keys into 256-key ranges
+    // (one chunk per workgroup) whose partials the out-projection prologue
+    // merges; larger batches aim at ~512 (sequence, head, split) workgroups
+    // and merge in a separate launch.
     int64_t max_ctx = 0;
     for (int b = 0; b < B; ++b) max_ctx = std::max<int64_t>(max_ctx, phon_len[b] + ac_len[b] + (int64_t)cf.max_new);
     const int64_t bh = (int64_t)B * cf.n_heads;
-    int64_t want;
     const int64_t rows_max = (int64_t)B * cf.k_heads;
-    const int64_t per_split = rows_max * cf.n_heads * 68 * 4;
-    if (bh < 256 && per_split <= 48 * 1024) want = std::max<int64_t>(1, std::min<int64_t>(8, (96 * 1024) / per_split));
-    else want = std::max<int64_t>(1, (512 + bh - 1) / bh);
-    int64_t sl = (max_ctx + want - 1) / want;
-    sl = std::max<int64_t>(64, (sl + 31) / 32 * 32);
+    const int merge_max = (dt == MTP_DTYPE_BF16 && rows_max <= 16) ? gemv_merge_max_splits((int)rows_max, d) : 0;
+    int64_t sl;
+    if (merge_max >= 2) {
+        // one 256-key chunk per workgroup while the out-projection can merge
+        // that many splits, longer splits beyond
+        sl = std::max<int64_t>(256, ((max_ctx + merge_max - 1) / merge_max + 31) / 32 * 32);
+    } else {
+        const int64_t want = std::max<int64_t>(1, (512 + bh - 1) / bh);
+        sl = (max_ctx + want - 1) / want;
+        sl = std::max<int64_t>(64, (sl + 31) / 32 * 32);
+    }
     if (const char* env = getenv("MTP_SPLIT_LEN")) {
         const int64_t v = atoll(env);
         if (v >= 32 && v % 32 == 0) sl = v;
@@ -712,24 +759,39 @@ int mtp_get_tokens(mtp_ctx* c, int32_t* tokens) {
     return MTP_OK;
 }
 
-int mtp_profile_replay(mtp_ctx* c, int kclass, int iters, double* avg_us) {
+int mtp_profile_replay(mtp_ctx* c, int kclass, int iters, int cold, double* avg_us) {
     if (!c || !avg_us || iters < 1) return MTP_EINVAL;
     if (kclass < MTP_KCLASS_GEMM_FFN1 || kclass > MTP_KCLASS_GEMM_OPROJ) { c->err = "unknown kernel class"; return MTP_EINVAL; }
-    if (!c->last_launch[kclass]) { c->err = "no launch of this kernel class yet"; return MTP_ESTATE; }
+    auto it = c->has_last ? c->step_launches.find(c->last_key) : c->step_launches.end();
+    if (it == c->step_launches.end() || it->second.cls[kclass].empty()) {
+        c->err = "the last decode step launched nothing of this kernel class";
+        return MTP_ESTATE;
+    }
+    const std::vector<mtp_ctx::Launch>& v = it->second.cls[kclass];
+    const size_t flush_bytes = (size_t)MTP_FLUSH_MB << 20;
+    if (cold && !c->flush_buf) HIPCHK(c, hipMalloc(&c->flush_buf, flush_bytes), "flush buffer");
+    // from here on the residual stream and the cache rows of the next
+    // positions no longer hold what the next step expects
+    c->prefilled = false;
     hipEvent_t e0, e1;
     HIPCHK(c, hipEventCreate(&e0), "event");
     hipError_t e = hipEventCreate(&e1);
     if (e != hipSuccess) { (void)hipEventDestroy(e0); return hip_fail(c, e, "event"); }
-    e = hipEventRecord(e0, c->stream);
-    for (int i = 0; i < iters && e == hipSuccess; ++i) e = c->last_launch[kclass](c->stream);
-    if (e == hipSuccess) e = hipEventRecord(e1, c->stream);
-    if (e == hipSuccess) e = hipEventSynchronize(e1);
-    float ms = 0.f;
-    if (e == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
+    double total_ms = 0.0;
+    for (int i = 0; i < iters && e == hipSuccess; ++i) {
+        if (cold) e = cache_flush(c->stream, c->flush_buf, flush_bytes);
+        if (e == hipSuccess) e = hipEventRecord(e0, c->stream);
+        for (size_t j = 0; j < v.size() && e == hipSuccess; ++j) e = v[j](c->stream);
+        if (e == hipSuccess) e = hipEventRecord(e1, c->stream);
+        if (e == hipSuccess) e = hipEventSynchronize(e1);
+        float ms = 0.f;
+        if (e == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
+        total_ms += ms;
+    }
     (void)hipEventDestroy(e0);
     (void)hipEventDestroy(e1);
     if (e != hipSuccess) return hip_fail(c, e, "replay");
-    *avg_us = 1000.0 * ms / iters;
+    *avg_us = 1000.0 * total_ms / ((double)iters * (double)v.size());
     return MTP_OK;
 }
 
@@ -746,6 +808,7 @@ void mtp_destroy(mtp_ctx* c) {
     if (!c) return;
     if (c->stream) (void)hipStreamSynchronize(c->stream);
     for (auto& kv : c->graphs) (void)hipGraphExecDestroy(kv.second);
+    if (c->flush_buf) (void)hipFree(c->flush_buf);
     delete c;
 }
 

@@ -9,6 +9,7 @@
 #define MTP_MAX_TOPK 32
 #define MTP_ATTN_QT 8          // query rows per attention tile
 #define MTP_SPLITK_MAX 8
+#define MTP_FLUSH_MB 512       // cache eviction read of cold replay timing
 
 typedef uint16_t bf16_t;  // raw bfloat16 bits
 

@@ -1,28 +1,35 @@
-// Small-M (decode) projections, bf16 MFMA, with the row-wise work fused in.
+// Small-M (decode, M <= 16 rows) projections, bf16 MFMA, with the row-wise
+// work fused in.
 //
-// At batch 1..8 a decode step is a chain of weight streams of 2-12 MB each;
-// every dependent global round trip costs about a microsecond, so this
-// kernel is built to have as few of them as possible on its critical path:
+// At batch 1..4 a decode step is a chain of weight streams of 2-8 MB; each
+// launch costs ~1.4 us before doing anything and every dependent global
+// round trip about a microsecond, so the kernel keeps its critical path to
+// one round trip plus the weight stream:
 //
-//  * every W fragment of the workgroup's 16 output columns (its K slice) is
-//    loaded into registers at kernel start, before anything else; W rows are
-//    read 64 contiguous bytes per row per load, one full 128-byte line per
-//    two consecutive fragments;
-//  * epilogue operands (bias, per-row KV-cache addresses) are fetched at
-//    kernel start too;
-//  * the activation rows are produced in a prologue while the weights are in
-//    flight: LayerNorm of the fp32 residual rows (LN1, LN2, final LN), or the
-//    token + position embedding followed by LN1 for the first layer; the
-//    bf16 result goes to LDS and feeds the MFMA B operand;
-//  * or, for the out-projection, the prologue merges the decode-attention
-//    split partials (max, sum, unnormalised output) into the bf16 rows;
-//  * each workgroup owns whole output columns (no split-K), so the residual
-//    epilogue adds into h directly and no cross-workgroup reduction, atomic
-//    or device-scope fence is needed: kernel boundaries are the only sync.
+//  * activation rows are loaded compactly (no padding rows), each thread a
+//    few float4 / 16-byte chunks, and before the weights: vmcnt retires in
+//    order, so loads issued after the weight stream could only be consumed
+//    after all weights landed; every load is unconditional from a clamped,
+//    valid address (a predicated load compiles to a branch plus a full wait);
+//  * the weight fragments of the workgroup's 16 output columns (its K range)
+//    then go out at once, straight into MFMA registers;
+//  * while they stream, the prologue builds the bf16 activation tile in LDS:
+//    LayerNorm of the residual rows (the residual itself is completed here:
+//    h_in + the previous projection's four split-K partial sums + its bias,
+//    written back once by workgroup 0), or token + position embedding + LN
+//    (first layer), or the final LN of each sequence's last pending row
+//    (heads), or plain bf16 rows;
+//  * projections whose N is only d (out-projection, FFN2) split K four ways
+//    and write partial sums, so 256 workgroups stream; their reduction is the
+//    consumer's prologue above.  No workgroup waits on another: kernel
+//    boundaries are the only synchronisation (device-scope fences between
+//    XCDs cost tens of microseconds on this chip).
 //
 // MFMA: v_mfma_f32_16x16x32_bf16 with A = 16 weight rows (output columns n)
-// and B = 16 activation rows (m); lane (r = l % 16, g = l / 16) supplies
-// row r and k = 8g..8g+7 of each 32-wide k step, the same k for A and B.
+// and B = 16 activation rows (m); lane (r = l % 16, g = l / 16) supplies row
+// r and k = 8g..8g+7 of each 32-wide k step, the same k for A and B.
+// Activation rows >= M are never written to LDS: their garbage only reaches
+// output columns >= M, which are never stored.
 #include "common.h"
 #include "launch.h"
 #include "wave.h"
@@ -101,26 +108,15 @@ struct EpiGeluB {
     }
 };
 
-// h[m][n] += v + bias  (the residual add of O-proj and FFN2).
-struct EpiResid {
-    float* h;
-    const float* bias;
-    int ldh;
-    struct Pre { float b[4]; float4 h0; };
-    __device__ __forceinline__ Pre prefetch(int m, int n, int) const {
-        Pre p;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) p.b[i] = bias[n + i];
-        p.h0 = *reinterpret_cast<const float4*>(h + (size_t)m * ldh + n);
-        return p;
-    }
-    __device__ __forceinline__ void store(const Pre& p, int m, int n, const float (&v)[4], int) const {
-        float4 o = p.h0;
-        o.x += v[0] + p.b[0];
-        o.y += v[1] + p.b[1];
-        o.z += v[2] + p.b[2];
-        o.w += v[3] + p.b[3];
-        *reinterpret_cast<float4*>(h + (size_t)m * ldh + n) = o;
+// split-K partial sums of the out-projection / FFN2: part[split][m][n]
+struct EpiPart {
+    float* part;
+    int ldp;        // N
+    int M;
+    struct Pre { int dummy; };
+    __device__ __forceinline__ Pre prefetch(int, int, int) const { return Pre{0}; }
+    __device__ __forceinline__ void store(const Pre&, int m, int n, const float (&v)[4], int) const {
+        *reinterpret_cast<float4*>(part + ((size_t)blockIdx.y * M + m) * ldp + n) = make_float4(v[0], v[1], v[2], v[3]);
     }
 };
 
@@ -138,312 +134,424 @@ struct EpiLogitsB {
     }
     __device__ __forceinline__ void store(const Pre& p, int m, int n, const float (&v)[4], int nvalid) const {
         float* o = out + (size_t)m * ldo + n;
-        for (int i = 0; i < nvalid; ++i) o[i] = v[i] + p.b[i];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            if (i < nvalid) o[i] = v[i] + p.b[i];
     }
 };
 
 }  // namespace
 
 // ------------------------------------------------------------------- kernel
-// XM: 0 = bf16 rows from global, 1 = LN(h rows), 2 = embed + LN (decode rows),
-//     3 = final LN of each sequence's last pending row (heads),
-//     4 = merge of decode-attention split partials (no LN).
-template <int MT, int XM, int MAXF, class Epi>
-__global__ __launch_bounds__(256) void gemv_kernel(GemvArgs a, Epi epi) {
-    extern __shared__ __attribute__((aligned(16))) bf16_t xs[];   // [MT*16][K + 8] (XM != 0)
-    __shared__ f32x4_t red[4][MT][64];
-    constexpr int ROWS = MT * 16;
-    constexpr int MAXS = 8;                       // attention splits merged in the prologue
+// XM: 0 = bf16 rows, 1 = LN of the completed residual rows, 2 = embedding +
+//     LN (decode rows of the first layer), 3 = final LN of each sequence's
+//     last pending row (heads), 4 = merge of the attention key-split partials
+//     of this workgroup's heads (out-projection).
+// MR: rows (power of two >= M, <= 16); MAXF: weight fragments per wave;
+// KCH: 1024-column chunks per row; MAXS: attention splits merged (XM 4).
+//
+// 16 waves per workgroup: a CU with one workgroup of four waves keeps too few
+// loads in flight to pull more than ~12-25 GB/s, with sixteen it pulls about
+// twice that (measured), and every launch here is a single wave of
+// workgroups, so the time is one workgroup's load latency and throughput.
+// LayerNorm-mode prologue: thread t owns the float4 column chunk t % (K/4) of
+// rows t / (K/4), t / (K/4) + RG, ... (RG = 1024 / (K/4) row groups), so the
+// LayerNorm parameters are loaded once per thread and a row's statistics
+// are a reduction over the K/4/64 waves of its row group.
+constexpr int GV_NW = 16;
+constexpr int GV_T = 64 * GV_NW;
+
+template <int MR, int XM, int MAXF, int KCH, int MAXS, class Epi>
+__global__ __launch_bounds__(GV_T) void gemv_kernel(GemvArgs a, Epi epi) {
+    constexpr int NW = GV_NW, T = GV_T;
+    extern __shared__ __attribute__((aligned(16))) bf16_t xs[];   // [16][K / S + 8], this K range
+    __shared__ f32x4_t red[NW][64];
+    constexpr bool LN = XM >= 1 && XM <= 3;
+    constexpr bool RES = XM == 1 || XM == 3;                           // residual completed here
+    constexpr int RPT = (MR * KCH + 3) / 4;                            // rows per thread (LN modes)
+    __shared__ float2 s_stat[NW][LN ? RPT : 1];
+    constexpr int XI = (MR * MAXF + 15) / 16;                          // 16-byte chunks per thread (XM 0)
+    constexpr int XP = (MR * KCH + 15) / 16;                           // float4 chunks per thread (XM 4)
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int r = lane & 15, g = lane >> 4;
     const int n0 = blockIdx.x * 16;
+    const int S = gridDim.y, split = blockIdx.y;
     const int K = a.K, M = a.M, N = a.N;
-    const int nfrag = K >> 5;
-    const int nf = (nfrag - wave + 3) >> 2;       // fragments f = wave + 4 i, i < nf
-    const int ldl = K + 8;                        // LDS row stride (bf16)
-    const int m0 = wave;                          // first activation row of this wave
+    const int ks = K / S;                         // this workgroup's K range
+    const int kb = split * ks;
+    const int nfrag = ks >> 5;
+    const int nf = (nfrag - wave + NW - 1) / NW;  // fragments f = wave + NW i, i < nf
+    const int ldl = ks + 8;
+    // LayerNorm-mode mapping
+    const int K4 = K >> 2;
+    const int RG = T / K4;                        // row groups (>= 2 for K <= 2048)
+    const int rg = tid / K4;
+    const int cc = min((tid - rg * K4) * 4, K - 4);
+    (void)RG; (void)rg; (void)cc; (void)K4;
 
-    // 1. Activation-side loads go out first.  vmcnt retires in order, so
-    //    anything issued after the weight stream could only be consumed once
-    //    all weights have landed; issued before, the prologue overlaps the
-    //    stream.  Every load below is unconditional from a clamped, valid
-    //    address: a predicated load becomes a branch plus a full vmcnt wait at
-    //    the join, which would serialise the round trips.  Rows, columns and
-    //    fragments outside the problem produce values that are never stored
-    //    or never enter a reduction.
-    const int mc = min(m0, M - 1);
-    uint4 xv[XM == 0 ? MAXF : 1][MT];
-    float4 gg[8], bb[8], x0[8], x1[8];
-    int st_pl = 0, st_ctx = 0;
+    // ---- A. activation-side loads (compact, unconditional, clamped) ----
+    float4 hv[LN ? RPT : 1];                     // residual / embedding rows
+    float4 pv[RES ? 4 : 1][RES ? RPT : 1];       // split-K partials of the producer
+    float4 zv[XM == 3 ? RPT : 1];                // prefill hidden state (heads, first step)
+    float4 gv, bv, rb;
+    uint4 xq[XM == 0 ? XI : 1];
+    int st_pl[XM == 3 ? RPT : 1];
+    int2 sti[XM == 4 ? XP : 1];                  // (ctx_len, pend_len) of the row's sequence
+    float2 ml[XM == 4 ? XP : 1][MAXS];           // (running max, sum) per split
+    float4 ov[XM == 4 ? XP : 1][MAXS];           // unnormalised outputs per split
+    (void)pv; (void)zv; (void)rb; (void)xq; (void)st_pl; (void)sti; (void)ml; (void)ov; (void)gv; (void)bv;
+    const bool has_part = a.part != nullptr;
     if constexpr (XM == 0) {
+        // rows [0, M) x columns [kb, kb + ks) as 16-byte chunks
+        const int cpr = ks >> 3;                 // chunks per row
+        const int total = M * cpr;
 #pragma unroll
-        for (int i = 0; i < MAXF; ++i)
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt) {
-                const int m = min(r + 16 * mt, M - 1);
-                const int f = min(wave + 4 * i, nfrag - 1);
-                xv[i][mt] = *reinterpret_cast<const uint4*>(a.x + (size_t)m * a.ldx + f * 32 + g * 8);
-            }
-    } else if constexpr (XM == 4) {
-        const SeqState& s = a.st[mc / a.Q];
-        st_pl = s.pend_len;
-        st_ctx = s.ctx_len;
-    } else {
-        const float* row0 = a.h + (size_t)mc * a.ldh;
-        if constexpr (XM == 3) row0 = a.h + (size_t)(a.Q > 0 ? mc * a.Q + a.Q - 1 : 0) * a.ldh;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const int c = min(lane * 4 + 256 * j, K - 4);
-            gg[j] = *reinterpret_cast<const float4*>(a.g + c);
-            bb[j] = *reinterpret_cast<const float4*>(a.beta + c);
-            if constexpr (XM == 1 || XM == 3) x0[j] = *reinterpret_cast<const float4*>(row0 + c);
-            if constexpr (XM == 3) x1[j] = *reinterpret_cast<const float4*>(a.hz + (size_t)mc * a.ldh + c);
+        for (int i = 0; i < XI; ++i) {
+            const int idx = min(tid + T * i, total - 1);
+            const int m = idx / cpr, c = (idx - m * cpr) * 8;
+            xq[i] = *reinterpret_cast<const uint4*>(a.x + (size_t)m * a.ldx + kb + c);
         }
-        if constexpr (XM == 3) st_pl = a.st[mc].pend_len;
+    } else if constexpr (XM == 4) {
+        // rows [0, M) x columns [kb, kb + ks) as float4 chunks; every split's
+        // partial is requested (clamped to the launched splits) and the ones
+        // past the sequence's context are discarded once its state is known
+        const int cpr = ks >> 2;
+        const int total = M * cpr;
+        const int H = K >> 6;
+        const size_t sstride = (size_t)a.qt * 68;
+#pragma unroll
+        for (int p = 0; p < XP; ++p) {
+            const int idx = min(tid + T * p, total - 1);
+            const int m = idx / cpr, c = kb + (idx - m * cpr) * 4;
+            const int seq = m / a.Q, i = m - seq * a.Q;
+            sti[p] = *reinterpret_cast<const int2*>(&a.st[seq]);
+            const float* e0 = a.apart + (size_t)(seq * H + (c >> 6)) * a.n_splits * sstride + (size_t)i * 68;
+#pragma unroll
+            for (int sp = 0; sp < MAXS; ++sp) {
+                const float* e = e0 + (size_t)min(sp, a.n_splits - 1) * sstride;
+                ml[p][sp] = *reinterpret_cast<const float2*>(e);
+                ov[p][sp] = *reinterpret_cast<const float4*>(e + 4 + (c & 63));
+            }
+        }
+    } else {
+        gv = *reinterpret_cast<const float4*>(a.g + cc);
+        bv = *reinterpret_cast<const float4*>(a.beta + cc);
+        if constexpr (RES) {
+            rb = *reinterpret_cast<const float4*>(has_part ? a.res_bias + cc : a.g + cc);
+            // XM 1: row m; XM 3: the last row of sequence m's pending chunk,
+            // plus the prefill state (chosen once the state is in)
+#pragma unroll
+            for (int j = 0; j < RPT; ++j) {
+                const int mc = min(rg + RG * j, M - 1);
+                const int row = (XM == 1) ? mc : ((a.Q > 0) ? mc * a.Q + a.Q - 1 : 0);
+                if constexpr (XM == 3) st_pl[j] = a.st[mc].pend_len;
+                const float* hp = a.h + (size_t)row * a.ldh + cc;
+                hv[j] = *reinterpret_cast<const float4*>(hp);
+#pragma unroll
+                for (int s2 = 0; s2 < 4; ++s2)
+                    pv[s2][j] = *reinterpret_cast<const float4*>(
+                        has_part ? a.part + ((size_t)s2 * a.part_rows + row) * a.ldh + cc : hp);
+                if constexpr (XM == 3) zv[j] = *reinterpret_cast<const float4*>(a.hz + (size_t)mc * a.ldh + cc);
+            }
+        }
     }
 
-    // 2. weights of this workgroup's 16 columns, all in flight at once
+    // ---- B. weights of this workgroup's 16 columns, all in flight ----
     const int nrow = min(n0 + r, N - 1);
-    const bf16_t* wp = a.W + (size_t)nrow * K + g * 8;
+    const bf16_t* wp = a.W + (size_t)nrow * K + kb + g * 8;
     uint4 wv[MAXF];
 #pragma unroll
     for (int i = 0; i < MAXF; ++i) {
-        const int f = min(wave + 4 * i, nfrag - 1);
+        const int f = min(wave + NW * i, nfrag - 1);
         wv[i] = *reinterpret_cast<const uint4*>(wp + f * 32);
     }
-    // 3. epilogue operands
-    const int em = r + 16 * (wave < MT ? wave : 0);
+    // ---- C. epilogue operands ----
+    const int em = r;
     const int en = n0 + 4 * g;
     const int envalid = min(4, N - en);
     const typename Epi::Pre pre = epi.prefetch(min(em, M - 1), min(en, N - 1), envalid);
 
-    // 4. activation rows -> bf16 in LDS
-    if constexpr (XM == 4) {
-        for (int m = wave; m < ROWS; m += 4) {
-            bf16_t* dst = xs + (size_t)m * ldl;
-            int pl = st_pl, ctx = st_ctx;
-            if (m != m0 && m < M) {
-                const SeqState& s = a.st[m / a.Q];
-                pl = s.pend_len;
-                ctx = s.ctx_len;
-            }
-            const int seq = m / a.Q, i = m - seq * a.Q;
-            if (m >= M || i >= pl) {
-                for (int c = lane * 4; c < K; c += 256) *reinterpret_cast<uint2*>(dst + c) = make_uint2(0, 0);
-                continue;
-            }
-            const int H = K >> 6;
-            const int n_active = min(a.n_splits, (ctx + pl + a.split_len - 1) / a.split_len);
+    // ---- D. activation tile in LDS ----
+    if constexpr (XM == 0) {
+        const int cpr = ks >> 3;
+        const int total = M * cpr;
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const int c = lane * 4 + 256 * j;
-                if (c >= K) continue;
-                const int head = c >> 6, dim = c & 63;
-                const float* e0 = a.apart + ((size_t)(seq * H + head) * a.n_splits) * (a.qt * 68) + i * 68;
-                float ms[MAXS], ls[MAXS];
-                float4 os[MAXS];
+        for (int i = 0; i < XI; ++i) {
+            const int idx = tid + T * i;
+            if (idx < total) {
+                const int m = idx / cpr, c = (idx - m * cpr) * 8;
+                *reinterpret_cast<uint4*>(xs + (size_t)m * ldl + c) = xq[i];
+            }
+        }
+    } else if constexpr (XM == 4) {
+        const int cpr = ks >> 2;
+        const int total = M * cpr;
 #pragma unroll
-                for (int sp = 0; sp < MAXS; ++sp) {
-                    const float* e = e0 + (size_t)min(sp, n_active - 1) * a.qt * 68;
-                    ms[sp] = e[0];
-                    ls[sp] = e[1];
-                    os[sp] = *reinterpret_cast<const float4*>(e + 4 + dim);
-                }
+        for (int p = 0; p < XP; ++p) {
+            const int idx = tid + T * p;
+            if (idx < total) {
+                const int m = idx / cpr, c = kb + (idx - m * cpr) * 4;
+                const int i = m - (m / a.Q) * a.Q;
+                const int ctx = sti[p].x, pl = sti[p].y;
+                const int n_active = min(a.n_splits, (ctx + pl + a.split_len - 1) / a.split_len);
+                float mx = -INFINITY;
 #pragma unroll
                 for (int sp = 0; sp < MAXS; ++sp)
-                    if (sp >= n_active) ms[sp] = -INFINITY;
-                float Mx = -INFINITY;
-#pragma unroll
-                for (int sp = 0; sp < MAXS; ++sp) Mx = fmaxf(Mx, ms[sp]);
+                    if (sp < n_active) mx = fmaxf(mx, ml[p][sp].x);
                 float L = 0.f;
                 float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
                 for (int sp = 0; sp < MAXS; ++sp) {
-                    const float w = (ms[sp] == -INFINITY) ? 0.f : __expf(ms[sp] - Mx);
-                    L = fmaf(w, ls[sp], L);
-                    o.x = fmaf(w, os[sp].x, o.x);
-                    o.y = fmaf(w, os[sp].y, o.y);
-                    o.z = fmaf(w, os[sp].z, o.z);
-                    o.w = fmaf(w, os[sp].w, o.w);
+                    // splits past the context (or a key range fully masked for
+                    // this row) contribute nothing; their words may be stale
+                    const bool live = sp < n_active && ml[p][sp].x != -INFINITY;
+                    const float w = live ? __expf(ml[p][sp].x - mx) : 0.f;
+                    const float lw = live ? ml[p][sp].y : 0.f;
+                    const float4 os = live ? ov[p][sp] : make_float4(0.f, 0.f, 0.f, 0.f);
+                    L = fmaf(w, lw, L);
+                    o.x = fmaf(w, os.x, o.x);
+                    o.y = fmaf(w, os.y, o.y);
+                    o.z = fmaf(w, os.z, o.z);
+                    o.w = fmaf(w, os.w, o.w);
                 }
+                const bool valid = i < pl;
                 const float inv = 1.f / L;
-                *reinterpret_cast<uint2*>(dst + c) = make_uint2(pack2(o.x * inv, o.y * inv), pack2(o.z * inv, o.w * inv));
+                const uint2 y = valid ? make_uint2(pack2(o.x * inv, o.y * inv), pack2(o.z * inv, o.w * inv)) : make_uint2(0u, 0u);
+                *reinterpret_cast<uint2*>(xs + (size_t)m * ldl + (c - kb)) = y;
             }
         }
-        __syncthreads();
-    } else if constexpr (XM != 0) {
-        for (int m = wave; m < ROWS; m += 4) {
-            bf16_t* dst = xs + (size_t)m * ldl;
-            if (m >= M) {
-                for (int c = lane * 4; c < K; c += 256) *reinterpret_cast<uint2*>(dst + c) = make_uint2(0, 0);
-                continue;
+    } else {
+        if constexpr (XM == 2) {
+            // embedding of each pending token at its position (first layer)
+#pragma unroll
+            for (int j = 0; j < RPT; ++j) {
+                const int mc = min(rg + RG * j, M - 1);
+                const int seq = mc / a.Q, i = mc - seq * a.Q;
+                const SeqState& st = a.st[seq];
+                const bool valid = i < st.pend_len;
+                const bf16_t* erow = a.emb + (size_t)(valid ? st.pend_ids[i] : 0) * K;
+                const bf16_t* prow = a.pos + (size_t)(valid ? st.ctx_len + i : 0) * K;
+                const uint2 e = *reinterpret_cast<const uint2*>(erow + cc);
+                const uint2 q = *reinterpret_cast<const uint2*>(prow + cc);
+                float4 x;
+                x.x = __uint_as_float(e.x << 16) + __uint_as_float(q.x << 16);
+                x.y = __uint_as_float(e.x & 0xFFFF0000u) + __uint_as_float(q.x & 0xFFFF0000u);
+                x.z = __uint_as_float(e.y << 16) + __uint_as_float(q.y << 16);
+                x.w = __uint_as_float(e.y & 0xFFFF0000u) + __uint_as_float(q.y & 0xFFFF0000u);
+                hv[j] = valid ? x : make_float4(0.f, 0.f, 0.f, 0.f);
             }
-            float4 x[8];
-            if (m == m0 && XM != 2) {
+        } else {
+            // complete the residual: h + (sum of the four partials + bias)
+#pragma unroll
+            for (int j = 0; j < RPT; ++j) {
+                bool use_z = false;
+                if constexpr (XM == 3) use_z = !(a.Q > 0 && st_pl[j] == a.Q);
+                float4 t;
+                t.x = ((pv[0][j].x + pv[1][j].x) + (pv[2][j].x + pv[3][j].x)) + rb.x;
+                t.y = ((pv[0][j].y + pv[1][j].y) + (pv[2][j].y + pv[3][j].y)) + rb.y;
+                t.z = ((pv[0][j].z + pv[1][j].z) + (pv[2][j].z + pv[3][j].z)) + rb.z;
+                t.w = ((pv[0][j].w + pv[1][j].w) + (pv[2][j].w + pv[3][j].w)) + rb.w;
+                if (!has_part) t = make_float4(0.f, 0.f, 0.f, 0.f);
+                float4 x = make_float4(hv[j].x + t.x, hv[j].y + t.y, hv[j].z + t.z, hv[j].w + t.w);
                 if constexpr (XM == 3) {
-                    const bool last_row = a.Q > 0 && st_pl == a.Q;
-                    const bool other = a.Q > 0 && st_pl > 0 && st_pl != a.Q;
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) {
-                        x[j] = last_row ? x0[j] : x1[j];
-                        if (other && lane * 4 + 256 * j < K)
-                            x[j] = *reinterpret_cast<const float4*>(a.h + (size_t)(m * a.Q + st_pl - 1) * a.ldh + lane * 4 + 256 * j);
-                    }
-                } else {
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) x[j] = x0[j];
+                    if (use_z) x = zv[j];
                 }
-            } else if constexpr (XM == 2) {
-                const int seq = m / a.Q, i = m - seq * a.Q;
-                const SeqState& s = a.st[seq];
-                const bool valid = i < s.pend_len;
-                const bf16_t* erow = a.emb + (size_t)(valid ? s.pend_ids[i] : 0) * K;
-                const bf16_t* prow = a.pos + (size_t)(valid ? s.ctx_len + i : 0) * K;
-#pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    const int c = lane * 4 + 256 * j;
-                    x[j] = make_float4(0.f, 0.f, 0.f, 0.f);
-                    if (c < K && valid) {
-                        const uint2 e = *reinterpret_cast<const uint2*>(erow + c);
-                        const uint2 q = *reinterpret_cast<const uint2*>(prow + c);
-                        x[j].x = __uint_as_float(e.x << 16) + __uint_as_float(q.x << 16);
-                        x[j].y = __uint_as_float(e.x & 0xFFFF0000u) + __uint_as_float(q.x & 0xFFFF0000u);
-                        x[j].z = __uint_as_float(e.y << 16) + __uint_as_float(q.y << 16);
-                        x[j].w = __uint_as_float(e.y & 0xFFFF0000u) + __uint_as_float(q.y & 0xFFFF0000u);
-                    }
-                }
-                if (blockIdx.x == 0) {
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) {
-                        const int c = lane * 4 + 256 * j;
-                        if (c < K) *reinterpret_cast<float4*>(a.h_out + (size_t)m * a.ldh + c) = x[j];
-                    }
-                }
-            } else {
-                const float* src;
-                if constexpr (XM == 3) {
-                    const int pl = a.st[m].pend_len;
-                    src = (a.Q > 0 && pl > 0) ? a.h + (size_t)(m * a.Q + pl - 1) * a.ldh : a.hz + (size_t)m * a.ldh;
-                } else {
-                    src = a.h + (size_t)m * a.ldh;
-                }
-#pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    const int c = lane * 4 + 256 * j;
-                    x[j] = (c < K) ? *reinterpret_cast<const float4*>(src + c) : make_float4(0.f, 0.f, 0.f, 0.f);
-                }
+                hv[j] = x;
             }
-            float s = 0.f;
+            if constexpr (XM == 3) {
+                // a partially filled pending chunk (not produced by the decode
+                // loop, which only ever leaves 0 or Q rows): recompute that row
 #pragma unroll
-            for (int j = 0; j < 8; ++j)
-                if (lane * 4 + 256 * j < K) s += (x[j].x + x[j].y) + (x[j].z + x[j].w);
-            const float mean = wsum(s) / (float)K;
-            float v = 0.f;
+                for (int j = 0; j < RPT; ++j) {
+                    const int m = rg + RG * j;
+                    if (m < M && rg < RG && a.Q > 0 && st_pl[j] > 0 && st_pl[j] < a.Q) {
+                        const int row = m * a.Q + st_pl[j] - 1;
+                        float4 x = *reinterpret_cast<const float4*>(a.h + (size_t)row * a.ldh + cc);
+                        float4 t = make_float4(0.f, 0.f, 0.f, 0.f);
+                        if (has_part) {
+                            float4 p4[4];
 #pragma unroll
-            for (int j = 0; j < 8; ++j)
-                if (lane * 4 + 256 * j < K) {
-                    const float dx = x[j].x - mean, dy = x[j].y - mean, dz = x[j].z - mean, dw = x[j].w - mean;
-                    v += (dx * dx + dy * dy) + (dz * dz + dw * dw);
-                }
-            const float rstd = rsqrtf(wsum(v) / (float)K + 1e-5f);
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const int c = lane * 4 + 256 * j;
-                if (c < K) {
-                    const float y0 = (x[j].x - mean) * rstd * gg[j].x + bb[j].x;
-                    const float y1 = (x[j].y - mean) * rstd * gg[j].y + bb[j].y;
-                    const float y2 = (x[j].z - mean) * rstd * gg[j].z + bb[j].z;
-                    const float y3 = (x[j].w - mean) * rstd * gg[j].w + bb[j].w;
-                    *reinterpret_cast<uint2*>(dst + c) = make_uint2(pack2(y0, y1), pack2(y2, y3));
+                            for (int s2 = 0; s2 < 4; ++s2)
+                                p4[s2] = *reinterpret_cast<const float4*>(a.part + ((size_t)s2 * a.part_rows + row) * a.ldh + cc);
+                            t.x = ((p4[0].x + p4[1].x) + (p4[2].x + p4[3].x)) + rb.x;
+                            t.y = ((p4[0].y + p4[1].y) + (p4[2].y + p4[3].y)) + rb.y;
+                            t.z = ((p4[0].z + p4[1].z) + (p4[2].z + p4[3].z)) + rb.z;
+                            t.w = ((p4[0].w + p4[1].w) + (p4[2].w + p4[3].w)) + rb.w;
+                        }
+                        hv[j] = make_float4(x.x + t.x, x.y + t.y, x.z + t.z, x.w + t.w);
+                    }
                 }
             }
         }
+        // workgroup 0 writes the completed rows (the next consumer's h)
+        if (a.h_out && blockIdx.x == 0 && blockIdx.y == 0 && rg < RG) {
+#pragma unroll
+            for (int j = 0; j < RPT; ++j) {
+                const int m = rg + RG * j;
+                if (m < M) *reinterpret_cast<float4*>(a.h_out + (size_t)m * a.ldh + cc) = hv[j];
+            }
+        }
+        // LayerNorm statistics: one pass (sum, sum of squares) per row; the
+        // waves of a row group cover its row exactly once
+#pragma unroll
+        for (int j = 0; j < RPT; ++j) {
+            const float4 x = hv[j];
+            float s1 = (x.x + x.y) + (x.z + x.w);
+            float s2 = (x.x * x.x + x.y * x.y) + (x.z * x.z + x.w * x.w);
+            s1 = wave_sum64(s1);
+            s2 = wave_sum64(s2);
+            if (lane == 0) s_stat[wave][j] = make_float2(s1, s2);
+        }
         __syncthreads();
+        const float inv_k = 1.f / (float)K;
+        const int wpg = K4 >> 6;                  // waves per row group
+#pragma unroll
+        for (int j = 0; j < RPT; ++j) {
+            const int m = rg + RG * j;
+            if (m >= M || rg >= RG) continue;
+            float t1 = 0.f, t2 = 0.f;
+            for (int w = rg * wpg; w < (rg + 1) * wpg; ++w) {
+                const float2 v = s_stat[w][j];
+                t1 += v.x;
+                t2 += v.y;
+            }
+            const float mean = t1 * inv_k;
+            const float var = fmaxf(t2 * inv_k - mean * mean, 0.f);
+            const float rstd = rsqrtf(var + 1e-5f);
+            const float4 x = hv[j];
+            const float y0 = (x.x - mean) * rstd * gv.x + bv.x;
+            const float y1 = (x.y - mean) * rstd * gv.y + bv.y;
+            const float y2 = (x.z - mean) * rstd * gv.z + bv.z;
+            const float y3 = (x.w - mean) * rstd * gv.w + bv.w;
+            *reinterpret_cast<uint2*>(xs + (size_t)m * ldl + cc) = make_uint2(pack2(y0, y1), pack2(y2, y3));
+        }
     }
+    __syncthreads();
 
-    // 5. MFMA over this wave's fragments
-    f32x4_t acc[MT];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    // ---- E. MFMA over this wave's fragments ----
+    f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int i = 0; i < MAXF; ++i)
         if (i < nf) {
-            const int f = wave + 4 * i;
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt) {
-                bf16x8_t xf;
-                if constexpr (XM == 0) xf = __builtin_bit_cast(bf16x8_t, xv[i][mt]);
-                else xf = *reinterpret_cast<const bf16x8_t*>(xs + (size_t)(r + 16 * mt) * ldl + f * 32 + g * 8);
-                acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, wv[i]), xf, acc[mt], 0, 0, 0);
-            }
+            const int f = wave + NW * i;
+            const bf16x8_t xf = *reinterpret_cast<const bf16x8_t*>(xs + (size_t)r * ldl + f * 32 + g * 8);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, wv[i]), xf, acc, 0, 0, 0);
         }
 
-    // 6. sum the four waves' K quarters, epilogue
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) red[wave][mt][lane] = acc[mt];
+    // ---- F. sum the waves' K slices, epilogue ----
+    red[wave][lane] = acc;
     __syncthreads();
-    if (wave < MT && em < M && en < N) {
-        const f32x4_t sum = (red[0][wave][lane] + red[1][wave][lane]) + (red[2][wave][lane] + red[3][wave][lane]);
+    if (wave == 0 && em < M && en < N) {
+        f32x4_t sum = red[0][lane];
+#pragma unroll
+        for (int w = 1; w < NW; ++w) sum += red[w][lane];
         const float v[4] = {sum[0], sum[1], sum[2], sum[3]};
         epi.store(pre, em, en, v, envalid);
     }
 }
 
 // --------------------------------------------------------------- launching
-template <int MT, int XM, int MAXF, class Epi>
-static hipError_t gemv_go(hipStream_t st, const GemvArgs& a, const Epi& e) {
-    dim3 grid((a.N + 15) / 16);
-    size_t lds = XM ? (size_t)MT * 16 * (a.K + 8) * 2 : 0;
+template <int MR, int XM, int MAXF, int KCH, int MAXS, class Epi>
+static hipError_t gemv_go(hipStream_t st, const GemvArgs& a, int splits, const Epi& e) {
+    dim3 grid((a.N + 15) / 16, splits);
+    const size_t lds = (size_t)16 * (a.K / splits + 8) * 2;
     static bool attr_set = false;
-    if (lds > 48 * 1024 && !attr_set) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemv_kernel<MT, XM, MAXF, Epi>),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, 140 * 1024);
-        if (e != hipSuccess) return e;
+    if (lds > 32 * 1024 && !attr_set) {
+        hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemv_kernel<MR, XM, MAXF, KCH, MAXS, Epi>),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, 128 * 1024);
+        if (err != hipSuccess) return err;
         attr_set = true;
     }
-    hipLaunchKernelGGL((gemv_kernel<MT, XM, MAXF, Epi>), grid, dim3(256), lds, st, a, e);
+    hipLaunchKernelGGL((gemv_kernel<MR, XM, MAXF, KCH, MAXS, Epi>), grid, dim3(GV_T), lds, st, a, e);
     return hipGetLastError();
 }
 
+// LayerNorm modes: K = d_model <= 2048, one K range
 template <int XM, class Epi>
-static hipError_t gemv_pick(hipStream_t st, const GemvArgs& a, const Epi& e) {
-    const int per_wave = (a.K / 32 + 3) / 4;
-    if (a.M <= 16) {
-        if (per_wave <= 8) return gemv_go<1, XM, 8>(st, a, e);
-        if (per_wave <= 16) return gemv_go<1, XM, 16>(st, a, e);
-        if (per_wave <= 32) return gemv_go<1, XM, 32>(st, a, e);
-        if (per_wave <= 48) return gemv_go<1, XM, 48>(st, a, e);
-    } else if (a.M <= 32) {
-        if (per_wave <= 8) return gemv_go<2, XM, 8>(st, a, e);
-        if (per_wave <= 16) return gemv_go<2, XM, 16>(st, a, e);
-        if (per_wave <= 32) return gemv_go<2, XM, 32>(st, a, e);
-        if (per_wave <= 48) return gemv_go<2, XM, 48>(st, a, e);
-    }
+static hipError_t gemv_ln(hipStream_t st, const GemvArgs& a, const Epi& e) {
+    const bool wide = a.K > 1024;
+#define MTP_GEMV_LN(MR) \
+    return wide ? gemv_go<MR, XM, 4, 2, 1>(st, a, 1, e) : gemv_go<MR, XM, 2, 1, 1>(st, a, 1, e)
+    if (a.M <= 1) MTP_GEMV_LN(1);
+    if (a.M <= 2) MTP_GEMV_LN(2);
+    if (a.M <= 4) MTP_GEMV_LN(4);
+    if (a.M <= 8) MTP_GEMV_LN(8);
+    MTP_GEMV_LN(16);
+#undef MTP_GEMV_LN
+}
+
+// split-K partial producers (four K ranges) over bf16 rows
+template <int MR>
+static hipError_t gemv_part_rows(hipStream_t st, const GemvArgs& a, const EpiPart& e) {
+    const int per_wave = (a.K / 4 / 32 + GV_NW - 1) / GV_NW;
+    if (per_wave <= 1) return gemv_go<MR, 0, 1, 1, 1>(st, a, 4, e);
+    if (per_wave <= 2) return gemv_go<MR, 0, 2, 1, 1>(st, a, 4, e);
+    if (per_wave <= 4) return gemv_go<MR, 0, 4, 1, 1>(st, a, 4, e);
+    return gemv_go<MR, 0, 8, 1, 1>(st, a, 4, e);
+}
+
+// split-K partial producer over merged attention partials (K = d <= 2048)
+template <int MR, int KCH>
+static hipError_t gemv_part_merge(hipStream_t st, const GemvArgs& a, const EpiPart& e) {
+    if (a.n_splits <= 2) return gemv_go<MR, 4, 1, KCH, 2>(st, a, 4, e);
+    if (a.n_splits <= 4) return gemv_go<MR, 4, 1, KCH, 4>(st, a, 4, e);
+    if constexpr (MR * KCH <= 16) return gemv_go<MR, 4, 1, KCH, 8>(st, a, 4, e);
     return hipErrorInvalidValue;
 }
 
+// Largest attention split count the out-projection can merge for M rows of
+// width d (register budget of the merge); 0 if none.
+int gemv_merge_max_splits(int M, int d) {
+    if (M < 1 || M > 16 || d > 2048) return 0;
+    int mr = 1;
+    while (mr < M) mr <<= 1;
+    const int kch = d > 1024 ? 2 : 1;
+    return mr * kch <= 16 ? 8 : 4;
+}
+
 hipError_t gemv(hipStream_t st, const GemvArgs& a) {
-    if (a.M < 1 || a.M > 32 || a.K % 32 || a.K > 48 * 4 * 32 || (a.xmode != 0 && a.K > 2048)) return hipErrorInvalidValue;
-    if (a.xmode == 4 && (a.n_splits > 8 || a.qt > MTP_ATTN_QT)) return hipErrorInvalidValue;
+    if (a.M < 1 || a.M > 16 || a.N < 4 || a.K % 128) return hipErrorInvalidValue;
+    if (a.epi == EPI_PARTIAL) {
+        if (a.N % 4 || a.K > 4 * 8 * GV_NW * 32) return hipErrorInvalidValue;
+        EpiPart e{a.part_out, a.N, a.M};
+        if (a.xmode == 4) {
+            if (a.K > 2048 || a.K % 256 || a.n_splits < 1 || a.Q < 1 ||
+                a.n_splits > gemv_merge_max_splits(a.M, a.K) || a.split_len < 1)
+                return hipErrorInvalidValue;
+            const bool wide = a.K > 1024;
+#define MTP_GEMV_MERGE(MR) return wide ? gemv_part_merge<MR, 2>(st, a, e) : gemv_part_merge<MR, 1>(st, a, e)
+            if (a.M <= 1) MTP_GEMV_MERGE(1);
+            if (a.M <= 2) MTP_GEMV_MERGE(2);
+            if (a.M <= 4) MTP_GEMV_MERGE(4);
+            if (a.M <= 8) MTP_GEMV_MERGE(8);
+            MTP_GEMV_MERGE(16);
+#undef MTP_GEMV_MERGE
+        }
+        if (a.xmode != 0) return hipErrorInvalidValue;
+        if (a.M <= 1) return gemv_part_rows<1>(st, a, e);
+        if (a.M <= 2) return gemv_part_rows<2>(st, a, e);
+        if (a.M <= 4) return gemv_part_rows<4>(st, a, e);
+        if (a.M <= 8) return gemv_part_rows<8>(st, a, e);
+        return gemv_part_rows<16>(st, a, e);
+    }
+    if (a.K > 2048 || a.K % 256 || (a.epi != EPI_LOGITS && a.N % 4)) return hipErrorInvalidValue;
     switch (a.epi) {
     case EPI_QKV: {
         EpiQKVDec e{a.q, a.bias, a.st, a.kv, a.d, a.Q};
-        if (a.xmode == 2) return gemv_pick<2>(st, a, e);
-        return gemv_pick<1>(st, a, e);
+        if (a.xmode == 2) return gemv_ln<2>(st, a, e);
+        if (a.xmode == 1) return gemv_ln<1>(st, a, e);
+        return hipErrorInvalidValue;
     }
     case EPI_GELU: {
         EpiGeluB e{(bf16_t*)a.out, a.bias, a.ldo};
-        return gemv_pick<1>(st, a, e);
-    }
-    case EPI_RESID: {
-        EpiResid e{a.h_res, a.bias, a.ldo};
-        if (a.xmode == 4) return gemv_pick<4>(st, a, e);
-        return gemv_pick<0>(st, a, e);
+        if (a.xmode == 1) return gemv_ln<1>(st, a, e);
+        return hipErrorInvalidValue;
     }
     case EPI_LOGITS: {
         EpiLogitsB e{(float*)a.out, a.bias, a.ldo, a.N};
-        return gemv_pick<3>(st, a, e);
+        if (a.xmode == 3) return gemv_ln<3>(st, a, e);
+        return hipErrorInvalidValue;
     }
     }
     return hipErrorInvalidValue;

@@ -75,26 +75,34 @@ struct AttnMfmaArgs {
 };
 hipError_t attention_mfma(hipStream_t st, const AttnMfmaArgs& a);
 
-// Small-M (<= 32) bf16 projection with fused row work; see gemv.hip.
+// Small-M (<= 16 rows) bf16 projection with fused row work; see gemv.hip.
 struct GemvArgs {
-    int epi;                   // EPI_QKV, EPI_GELU, EPI_RESID, EPI_LOGITS
-    int xmode;                 // 0 bf16 rows, 1 LN(h), 2 embed + LN, 3 final LN (heads),
-                               // 4 merge of decode-attention split partials
-    int M, N, K, splits;
+    int epi;                   // EPI_QKV, EPI_GELU, EPI_LOGITS (LayerNorm modes), EPI_PARTIAL (split-K x4)
+    int xmode;                 // 0 bf16 rows, 1 LN(h + partials + bias), 2 embed + LN, 3 final LN (heads),
+                               // 4 merged attention partials (EPI_PARTIAL only)
+    int M, N, K;
     const bf16_t* W;
     const bf16_t* x; int ldx;                       // xmode 0
-    const float* h; int ldh;                        // xmode 1, 3
+    const float* h; int ldh;                        // residual rows (xmode 1, 3), row stride = d
+    const float* part; int part_rows;               // [4][part_rows][d] split-K partials to add (xmode 1, 3; may be NULL)
+    const float* res_bias;                          // bias of the projection that produced `part`
     const float* g; const float* beta;              // LN gain / shift
-    const SeqState* st; int Q;                      // xmode 2, 3 and EPI_QKV
+    const SeqState* st; int Q;                      // xmode 2, 3, 4 and EPI_QKV
     const bf16_t* emb; const bf16_t* pos;           // xmode 2
-    float* h_out;                                   // xmode 2: embedded rows written here
+    float* h_out;                                   // completed residual rows, written by workgroup 0 (may be NULL;
+                                                    // must not alias h)
     const float* hz;                                // xmode 3: last prefill hidden state
+    const float* apart; int qt, split_len, n_splits;   // xmode 4: attention split partials
     const float* bias;
-    void* out; int ldo;                             // EPI_GELU / EPI_LOGITS output, EPI_RESID ld
+    void* out; int ldo;                             // EPI_GELU / EPI_LOGITS output
+    float* part_out;                                // EPI_PARTIAL output [4][M][N]
     float* q; KVView kv; int d;                     // EPI_QKV
-    float* h_res;                                   // EPI_RESID target
-    const float* apart; int qt; int split_len; int n_splits;  // xmode 4
 };
+int gemv_merge_max_splits(int M, int d);
+
+// Reads `bytes` (a multiple of 16) of `buf` so that earlier data leaves the
+// L2 and last-level caches (measurement only); writes a few words of `buf`.
+hipError_t cache_flush(hipStream_t st, void* buf, size_t bytes);
 hipError_t gemv(hipStream_t st, const GemvArgs& a);
 
 // Row embedding (+ first LayerNorm).  mode 0: decode rows derived from the

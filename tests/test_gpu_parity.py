@@ -216,3 +216,69 @@ def test_valle_k4_bf16_batch1():
     steps, emitted, chk = run_teacher_forced(wl, wl.K, wl.top_k, steps_checked={0, 1, 97, 160}, tol=3e-2)
     assert len(emitted[0]) >= wl.eos_min or emitted[0][-1] == EOS_ID
     log(f"valle_k4: {steps} steps, {len(emitted[0])} tokens, max logit err {chk.max_err:.3g}, tie-zone {chk.tie_zone}")
+
+
+def test_valle_k8_bf16_batch1():
+    """Eight heads (the paper's largest K), batch 1: 8 pending rows per step,
+    the out-projection merging up to eight attention key splits."""
+    wl = WORKLOADS["valle_k8"]
+    log("valle_k8: start")
+    steps, emitted, chk = run_teacher_forced(wl, wl.K, wl.top_k, steps_checked={0, 47, 93}, tol=3e-2)
+    assert steps == math.ceil(wl.max_new / wl.K)
+    log(f"valle_k8: {steps} steps, max logit err {chk.max_err:.3g}, tie-zone {chk.tie_zone}")
+
+
+def test_valle_batch2_k8_sixteen_rows():
+    """Two ragged sequences at K=8: 16 decode rows, the largest fused row
+    count, with the out-projection merge at its narrowest split budget."""
+    wl = WORKLOADS["valle_b32"]
+    log("valle batch 2, K=8: start")
+    steps, emitted, chk = run_teacher_forced(wl, 8, 8, steps_checked={0, 61}, tol=3e-2, batch=2)
+    assert steps == math.ceil(wl.max_new / 8)
+    log(f"valle batch 2: {steps} steps, max logit err {chk.max_err:.3g}, tie-zone {chk.tie_zone}")
+
+
+def test_valle_b32_batched():
+    """32 ragged sequences, K=4 (128 decode rows through the tiled path):
+    selection exact for every sequence at every step, logits of two sequences
+    against the oracle at two steps."""
+    wl = WORKLOADS["valle_b32"]
+    log("valle_b32: start")
+    steps, emitted, chk = run_teacher_forced(wl, wl.K, wl.top_k, steps_checked={0, 120}, tol=3e-2,
+                                             seqs_checked=[0, 17])
+    assert steps == math.ceil(wl.max_new / wl.K)
+    assert all(len(e) == wl.max_new for e in emitted)
+    log(f"valle_b32: {steps} steps, max logit err {chk.max_err:.3g}, tie-zone {chk.tie_zone}")
+
+
+def test_replay_timing_then_prefill_again():
+    """Kernel replay timing returns positive times for every class, forbids a
+    decode step until the next prefill, and leaves no trace in the next
+    generation (same tokens and logits as a fresh session)."""
+    from paper_2410_13839_amd.binding import MTP_ESTATE, MTPError, mtp_profile_replay
+    wl = WORKLOADS["valle_k4"]
+    w = make_weights(wl.model)
+    logq = make_logq()
+    pr = make_prompts(wl)
+
+    def run(s, n):
+        s.prefill(pr.phon, pr.ac)
+        lg = []
+        for _ in range(n):
+            s.step(wl.K, wl.top_k)
+            lg.append(s.logits(wl.K))
+        return s.tokens()[0][:n * wl.K].copy(), np.stack(lg)
+
+    s = new_session(wl, w, logq)
+    ref = run(s, 6)
+    for kc in (1, 2, 3, 4, 5, 6):
+        for cold in (True, False):
+            us = mtp_profile_replay(s.ctx, kc, 3, cold)
+            assert 0.5 < us < 1000.0, (kc, cold, us)
+    with pytest.raises(MTPError) as e:
+        s.step(wl.K, wl.top_k)
+    assert e.value.code == MTP_ESTATE
+    again = run(s, 6)
+    s.close()
+    assert np.array_equal(ref[0], again[0])
+    assert np.array_equal(ref[1].view(np.uint32), again[1].view(np.uint32))
