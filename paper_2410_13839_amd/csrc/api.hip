@@ -102,7 +102,7 @@ int validate(const mtp_config* c, std::string* why) {
 }
 
 struct WsLayout {
-    uint64_t rows, ids, tiles, last_row, state, btab, h, h2, q, u, attn, ffn, part, apart, hz, z, logits, cand, ehat,
+    uint64_t rows, ids, tiles, last_row, state, btab, h, q, u, attn, ffn, part, apart, hz, z, logits, cand, ehat,
         delta, psi, slots, out_tok, out_cnt, hist, total;
     int64_t m_pre, m_dec, m_max, max_tiles, max_splits, maxp, num_pages;
     int act_bytes;
@@ -130,7 +130,6 @@ WsLayout ws_layout(const mtp_config& c) {
     w.state = take(B * sizeof(SeqState));
     w.btab = take(B * w.maxp * 4);
     w.h = take(w.m_max * d * 4);
-    w.h2 = take(w.m_dec * d * 4);                 // second residual buffer of the fused decode trunk
     w.q = take(w.m_max * d * 4);
     w.u = take(w.m_max * d * w.act_bytes);
     w.attn = take(w.m_max * d * w.act_bytes);
@@ -273,29 +272,23 @@ bool prologue_merge(const mtp_ctx* c, int rows) {
 }
 
 // One layer of the fused small-M decode trunk (bf16, B*Q <= 16 rows).  The
-// residual stream alternates between two buffers: the out-projection and FFN2
-// leave four split-K partial sums, and the next LayerNorm consumer (FFN1, the
-// next layer's QKV, the heads) adds them and the bias to its input rows and
-// writes the completed rows to the other buffer.  `hcur` is the buffer holding
-// the layer's input rows before the call and the output rows after it (still
-// missing the FFN2 partials, whose bias is B_2 of this layer).
-int run_layer_fused(mtp_ctx* c, int l, int rows, int qt, float*& hcur) {
+// out-projection and FFN2 leave four split-K partial sums, the first of which
+// also carries the residual input and the bias; the next LayerNorm consumer
+// (FFN1, the next layer's QKV, the heads) sums them into its input rows and
+// writes the completed residual rows back to h for the next projection.
+int run_layer_fused(mtp_ctx* c, int l, int rows, int qt) {
     const mtp_config& cf = c->cfg;
     const int d = cf.d_model, F = cf.d_ff;
-    float* ha = c->ws_ptr<float>(c->ws.h);
-    float* hb = c->ws_ptr<float>(c->ws.h2);
+    float* h = c->ws_ptr<float>(c->ws.h);
     float* part = c->ws_ptr<float>(c->ws.part);
-    float* hnext = (hcur == ha) ? hb : ha;
     GemvArgs g{};
     g.epi = EPI_QKV; g.M = rows; g.N = 3 * d; g.K = d;
-    g.W = (const bf16_t*)c->lt(l, MTP_T_W_QKV); g.ldh = d;
+    g.W = (const bf16_t*)c->lt(l, MTP_T_W_QKV); g.ldh = d; g.h_out = h;
     if (l == 0) {
-        g.xmode = 2; g.h_out = hcur;
+        g.xmode = 2;
         g.emb = (const bf16_t*)c->wt(MTP_T_EMB_AC); g.pos = (const bf16_t*)c->wt(MTP_T_POS);
     } else {
-        g.xmode = 1; g.h = hcur; g.part = part; g.part_rows = rows; g.res_bias = (const float*)c->lt(l - 1, MTP_T_B_2);
-        g.h_out = hnext;
-        std::swap(hcur, hnext);
+        g.xmode = 1; g.part = part; g.part_rows = rows; g.part_on = 1;
     }
     g.g = (const float*)c->lt(l, MTP_T_LN1_G); g.beta = (const float*)c->lt(l, MTP_T_LN1_B);
     g.st = c->ws_ptr<SeqState>(c->ws.state); g.Q = c->q_pad;
@@ -310,23 +303,20 @@ int run_layer_fused(mtp_ctx* c, int l, int rows, int qt, float*& hcur) {
     g.W = (const bf16_t*)c->lt(l, MTP_T_W_O); g.x = (const bf16_t*)(c->WS() + c->ws.attn); g.ldx = d;
     g.st = c->ws_ptr<SeqState>(c->ws.state); g.Q = c->q_pad;
     g.apart = c->ws_ptr<float>(c->ws.apart); g.qt = qt; g.split_len = c->split_len; g.n_splits = c->n_splits;
-    g.part_out = part;
+    g.h = h; g.ldh = d; g.bias = (const float*)c->lt(l, MTP_T_B_O); g.part_out = part;
     HIPCHK(c, launch_rec(c, MTP_KCLASS_GEMM_OPROJ, [g](hipStream_t s) { return gemv(s, g); }), "out-proj gemv");
 
-    hnext = (hcur == ha) ? hb : ha;
     g = GemvArgs{};
-    g.epi = EPI_GELU; g.xmode = 1; g.M = rows; g.N = F; g.K = d;
-    g.W = (const bf16_t*)c->lt(l, MTP_T_W_1); g.h = hcur; g.ldh = d;
-    g.part = part; g.part_rows = rows; g.res_bias = (const float*)c->lt(l, MTP_T_B_O); g.h_out = hnext;
+    g.epi = EPI_GELU; g.xmode = 1; g.M = rows; g.N = F; g.K = d; g.ldh = d;
+    g.W = (const bf16_t*)c->lt(l, MTP_T_W_1); g.part = part; g.part_rows = rows; g.part_on = 1; g.h_out = h;
     g.g = (const float*)c->lt(l, MTP_T_LN2_G); g.beta = (const float*)c->lt(l, MTP_T_LN2_B);
     g.bias = (const float*)c->lt(l, MTP_T_B_1); g.out = c->WS() + c->ws.ffn; g.ldo = F;
     HIPCHK(c, launch_rec(c, MTP_KCLASS_GEMM_FFN1, [g](hipStream_t s) { return gemv(s, g); }), "ffn1 gemv");
-    hcur = hnext;
 
     g = GemvArgs{};
     g.epi = EPI_PARTIAL; g.xmode = 0; g.M = rows; g.N = d; g.K = F;
     g.W = (const bf16_t*)c->lt(l, MTP_T_W_2); g.x = (const bf16_t*)(c->WS() + c->ws.ffn); g.ldx = F;
-    g.part_out = part;
+    g.h = h; g.ldh = d; g.bias = (const float*)c->lt(l, MTP_T_B_2); g.part_out = part;
     HIPCHK(c, launch_rec(c, MTP_KCLASS_GEMM_FFN2, [g](hipStream_t s) { return gemv(s, g); }), "ffn2 gemv");
     return MTP_OK;
 }
@@ -406,11 +396,10 @@ int enqueue_step(mtp_ctx* c, int K, int top_k) {
     const bool small = dt == MTP_DTYPE_BF16 && B * Q <= 16;
     int qt = 1;
     while (qt < Q) qt <<= 1;
-    float* hfin = c->ws_ptr<float>(c->ws.h);     // residual rows entering the heads
-    bool fin_part = false;                       // ... still missing the last FFN2 partials
+    bool fin_part = false;                       // the heads' input is the last FFN2's partials
     if (Q > 0 && small) {
         for (int l = 0; l < cf.n_layers; ++l) {
-            int rc = run_layer_fused(c, l, B * Q, qt, hfin);
+            int rc = run_layer_fused(c, l, B * Q, qt);
             if (rc) return rc;
         }
         fin_part = true;
@@ -428,14 +417,11 @@ int enqueue_step(mtp_ctx* c, int K, int top_k) {
             if (rc) return rc;
         }
     }
-    if (dt == MTP_DTYPE_BF16 && B <= 16) {
+    if (dt == MTP_DTYPE_BF16 && B <= 4) {
         GemvArgs g{};
         g.epi = EPI_LOGITS; g.xmode = 3; g.M = B; g.N = K * V; g.K = d;
-        g.W = (const bf16_t*)c->wt(MTP_T_W_HEADS); g.h = hfin; g.ldh = d;
-        if (fin_part) {
-            g.part = c->ws_ptr<float>(c->ws.part); g.part_rows = B * Q;
-            g.res_bias = (const float*)c->lt(cf.n_layers - 1, MTP_T_B_2);
-        }
+        g.W = (const bf16_t*)c->wt(MTP_T_W_HEADS); g.h = c->ws_ptr<float>(c->ws.h); g.ldh = d;
+        g.part = c->ws_ptr<float>(c->ws.part); g.part_rows = B * Q; g.part_on = fin_part ? 1 : 0;
         g.hz = c->ws_ptr<float>(c->ws.hz); g.st = c->ws_ptr<SeqState>(c->ws.state); g.Q = Q;
         g.g = (const float*)c->wt(MTP_T_LNF_G); g.beta = (const float*)c->wt(MTP_T_LNF_B);
         g.bias = (const float*)c->wt(MTP_T_B_HEADS); g.out = c->WS() + c->ws.logits; g.ldo = K * V;

@@ -108,15 +108,32 @@ struct EpiGeluB {
     }
 };
 
-// split-K partial sums of the out-projection / FFN2: part[split][m][n]
+// split-K partial sums of the out-projection / FFN2: part[split][m][n]; the
+// first K range also carries the residual input row and the bias, so the
+// four partials sum to the complete new residual row
 struct EpiPart {
     float* part;
-    int ldp;        // N
+    int ldp;        // N (= d)
     int M;
-    struct Pre { int dummy; };
-    __device__ __forceinline__ Pre prefetch(int, int, int) const { return Pre{0}; }
-    __device__ __forceinline__ void store(const Pre&, int m, int n, const float (&v)[4], int) const {
-        *reinterpret_cast<float4*>(part + ((size_t)blockIdx.y * M + m) * ldp + n) = make_float4(v[0], v[1], v[2], v[3]);
+    const float* h;      // residual rows [M][N] entering the projection
+    const float* bias;   // [N]
+    struct Pre { float4 b, x; };
+    __device__ __forceinline__ Pre prefetch(int m, int n, int) const {
+        Pre p;
+        const int nn = min(n, ldp - 4);
+        p.b = *reinterpret_cast<const float4*>(bias + nn);
+        p.x = *reinterpret_cast<const float4*>(h + (size_t)m * ldp + nn);
+        return p;
+    }
+    __device__ __forceinline__ void store(const Pre& p, int m, int n, const float (&v)[4], int) const {
+        float4 o = make_float4(v[0], v[1], v[2], v[3]);
+        if (blockIdx.y == 0) {
+            o.x += p.b.x + p.x.x;
+            o.y += p.b.y + p.x.y;
+            o.z += p.b.z + p.x.z;
+            o.w += p.b.w + p.x.w;
+        }
+        *reinterpret_cast<float4*>(part + ((size_t)blockIdx.y * M + m) * ldp + n) = o;
     }
 };
 
@@ -159,19 +176,20 @@ struct EpiLogitsB {
 // LayerNorm parameters are loaded once per thread and a row's statistics
 // are a reduction over the K/4/64 waves of its row group.
 constexpr int GV_NW = 16;
-constexpr int GV_T = 64 * GV_NW;
 
-template <int MR, int XM, int MAXF, int KCH, int MAXS, class Epi>
-__global__ __launch_bounds__(GV_T) void gemv_kernel(GemvArgs a, Epi epi) {
-    constexpr int NW = GV_NW, T = GV_T;
+template <int MR, int XM, int MAXF, int KCH, int MAXS, int NW, class Epi>
+__global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
+    constexpr int T = 64 * NW;
     extern __shared__ __attribute__((aligned(16))) bf16_t xs[];   // [16][K / S + 8], this K range
-    __shared__ f32x4_t red[NW][64];
+    // wave partial sums of the MFMA phase; before it, the LayerNorm gain and
+    // shift ([2][K/4] float4, K <= 2048)
+    __shared__ f32x4_t red[1024];
     constexpr bool LN = XM >= 1 && XM <= 3;
     constexpr bool RES = XM == 1 || XM == 3;                           // residual completed here
-    constexpr int RPT = (MR * KCH + 3) / 4;                            // rows per thread (LN modes)
+    constexpr int RPT = (MR * KCH * 256 + T - 1) / T;                  // rows per thread (LN modes)
     __shared__ float2 s_stat[NW][LN ? RPT : 1];
     constexpr int XI = (MR * MAXF + 15) / 16;                          // 16-byte chunks per thread (XM 0)
-    constexpr int XP = (MR * KCH + 15) / 16;                           // float4 chunks per thread (XM 4)
+    constexpr int XP = (MR * KCH * 64 + T - 1) / T;                    // float4 chunks per thread (XM 4)
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int r = lane & 15, g = lane >> 4;
@@ -183,25 +201,29 @@ __global__ __launch_bounds__(GV_T) void gemv_kernel(GemvArgs a, Epi epi) {
     const int nfrag = ks >> 5;
     const int nf = (nfrag - wave + NW - 1) / NW;  // fragments f = wave + NW i, i < nf
     const int ldl = ks + 8;
-    // LayerNorm-mode mapping
+    // LayerNorm-mode mapping; rg is uniform over a wave (K/4 is a multiple of 64)
     const int K4 = K >> 2;
-    const int RG = T / K4;                        // row groups (>= 2 for K <= 2048)
-    const int rg = tid / K4;
+    const int RG = T / K4;                        // row groups (>= 1 for K <= 2048)
+    const int rg = __builtin_amdgcn_readfirstlane(tid / K4);
     const int cc = min((tid - rg * K4) * 4, K - 4);
     (void)RG; (void)rg; (void)cc; (void)K4;
 
-    // ---- A. activation-side loads (compact, unconditional, clamped) ----
+    // ---- A. activation-side loads (compact, from clamped addresses; branches
+    //      only on wave-uniform conditions, which cost no extra waits) ----
     float4 hv[LN ? RPT : 1];                     // residual / embedding rows
     float4 pv[RES ? 4 : 1][RES ? RPT : 1];       // split-K partials of the producer
     float4 zv[XM == 3 ? RPT : 1];                // prefill hidden state (heads, first step)
-    float4 gv, bv, rb;
-    uint4 xq[XM == 0 ? XI : 1];
+    float4 gv = make_float4(0.f, 0.f, 0.f, 0.f), bv = gv;
+    // bf16 chunks (XM 0) as one vector value: an array of uint4 held across
+    // the barrier below is demoted to scratch by the compiler
+    typedef unsigned int xq_t __attribute__((ext_vector_type(4 * XI)));
+    xq_t xq;
     int st_pl[XM == 3 ? RPT : 1];
     int2 sti[XM == 4 ? XP : 1];                  // (ctx_len, pend_len) of the row's sequence
     float2 ml[XM == 4 ? XP : 1][MAXS];           // (running max, sum) per split
     float4 ov[XM == 4 ? XP : 1][MAXS];           // unnormalised outputs per split
-    (void)pv; (void)zv; (void)rb; (void)xq; (void)st_pl; (void)sti; (void)ml; (void)ov; (void)gv; (void)bv;
-    const bool has_part = a.part != nullptr;
+    (void)pv; (void)zv; (void)xq; (void)st_pl; (void)sti; (void)ml; (void)ov; (void)gv; (void)bv; (void)hv;
+    const bool has_part = a.part_on != 0;      // kernel argument: uniform
     if constexpr (XM == 0) {
         // rows [0, M) x columns [kb, kb + ks) as 16-byte chunks
         const int cpr = ks >> 3;                 // chunks per row
@@ -210,7 +232,11 @@ __global__ __launch_bounds__(GV_T) void gemv_kernel(GemvArgs a, Epi epi) {
         for (int i = 0; i < XI; ++i) {
             const int idx = min(tid + T * i, total - 1);
             const int m = idx / cpr, c = (idx - m * cpr) * 8;
-            xq[i] = *reinterpret_cast<const uint4*>(a.x + (size_t)m * a.ldx + kb + c);
+            const uint4 t = *reinterpret_cast<const uint4*>(a.x + (size_t)m * a.ldx + kb + c);
+            xq[4 * i] = t.x;
+            xq[4 * i + 1] = t.y;
+            xq[4 * i + 2] = t.z;
+            xq[4 * i + 3] = t.w;
         }
     } else if constexpr (XM == 4) {
         // rows [0, M) x columns [kb, kb + ks) as float4 chunks; every split's
@@ -235,27 +261,39 @@ __global__ __launch_bounds__(GV_T) void gemv_kernel(GemvArgs a, Epi epi) {
             }
         }
     } else {
-        gv = *reinterpret_cast<const float4*>(a.g + cc);
-        bv = *reinterpret_cast<const float4*>(a.beta + cc);
+        // LayerNorm gain and shift: loaded by row group 0 only, shared through LDS
+        if (rg == 0) {
+            gv = *reinterpret_cast<const float4*>(a.g + cc);
+            bv = *reinterpret_cast<const float4*>(a.beta + cc);
+        }
         if constexpr (RES) {
-            rb = *reinterpret_cast<const float4*>(has_part ? a.res_bias + cc : a.g + cc);
             // XM 1: row m; XM 3: the last row of sequence m's pending chunk,
-            // plus the prefill state (chosen once the state is in)
+            // plus the prefill state (chosen once the state is in).  With
+            // partials the four of them sum to the row (the first carries the
+            // residual input and bias); without, the row is h itself.
 #pragma unroll
             for (int j = 0; j < RPT; ++j) {
-                const int mc = min(rg + RG * j, M - 1);
-                const int row = (XM == 1) ? mc : ((a.Q > 0) ? mc * a.Q + a.Q - 1 : 0);
-                if constexpr (XM == 3) st_pl[j] = a.st[mc].pend_len;
-                const float* hp = a.h + (size_t)row * a.ldh + cc;
-                hv[j] = *reinterpret_cast<const float4*>(hp);
+                const int m = rg + RG * j;
+                if (m < M && rg < RG) {
+                    const int row = (XM == 1) ? m : ((a.Q > 0) ? m * a.Q + a.Q - 1 : 0);
+                    if constexpr (XM == 3) st_pl[j] = a.st[m].pend_len;
+                    if (has_part) {
 #pragma unroll
-                for (int s2 = 0; s2 < 4; ++s2)
-                    pv[s2][j] = *reinterpret_cast<const float4*>(
-                        has_part ? a.part + ((size_t)s2 * a.part_rows + row) * a.ldh + cc : hp);
-                if constexpr (XM == 3) zv[j] = *reinterpret_cast<const float4*>(a.hz + (size_t)mc * a.ldh + cc);
+                        for (int s2 = 0; s2 < 4; ++s2)
+                            pv[s2][j] = *reinterpret_cast<const float4*>(a.part + ((size_t)s2 * a.part_rows + row) * a.ldh + cc);
+                    } else {
+                        hv[j] = *reinterpret_cast<const float4*>(a.h + (size_t)row * a.ldh + cc);
+                    }
+                    if constexpr (XM == 3) zv[j] = *reinterpret_cast<const float4*>(a.hz + (size_t)m * a.ldh + cc);
+                }
             }
         }
     }
+
+    // Every wave's activation loads go out before any weight load: a CU
+    // returns load data in request order, so an activation load queued behind
+    // another wave's weight loads (HBM misses) would wait for them.
+    __syncthreads();
 
     // ---- B. weights of this workgroup's 16 columns, all in flight ----
     const int nrow = min(n0 + r, N - 1);
@@ -271,6 +309,10 @@ __global__ __launch_bounds__(GV_T) void gemv_kernel(GemvArgs a, Epi epi) {
     const int en = n0 + 4 * g;
     const int envalid = min(4, N - en);
     const typename Epi::Pre pre = epi.prefetch(min(em, M - 1), min(en, N - 1), envalid);
+    // every load above is issued before any of the prologue below may be
+    // scheduled (the compiler otherwise sinks weight loads under the merge
+    // arithmetic, serialising two memory round trips)
+    __builtin_amdgcn_sched_barrier(0);
 
     // ---- D. activation tile in LDS ----
     if constexpr (XM == 0) {
@@ -281,7 +323,8 @@ __global__ __launch_bounds__(GV_T) void gemv_kernel(GemvArgs a, Epi epi) {
             const int idx = tid + T * i;
             if (idx < total) {
                 const int m = idx / cpr, c = (idx - m * cpr) * 8;
-                *reinterpret_cast<uint4*>(xs + (size_t)m * ldl + c) = xq[i];
+                *reinterpret_cast<uint4*>(xs + (size_t)m * ldl + c) =
+                    make_uint4(xq[4 * i], xq[4 * i + 1], xq[4 * i + 2], xq[4 * i + 3]);
             }
         }
     } else if constexpr (XM == 4) {
@@ -322,69 +365,72 @@ __global__ __launch_bounds__(GV_T) void gemv_kernel(GemvArgs a, Epi epi) {
             }
         }
     } else {
+        // row group 0 shares the LayerNorm gain and shift
+        f32x4_t* s_gb = red;                      // [2][K/4]
+        if (rg == 0) {
+            s_gb[cc >> 2] = f32x4_t{gv.x, gv.y, gv.z, gv.w};
+            s_gb[K4 + (cc >> 2)] = f32x4_t{bv.x, bv.y, bv.z, bv.w};
+        }
         if constexpr (XM == 2) {
             // embedding of each pending token at its position (first layer)
 #pragma unroll
             for (int j = 0; j < RPT; ++j) {
-                const int mc = min(rg + RG * j, M - 1);
-                const int seq = mc / a.Q, i = mc - seq * a.Q;
-                const SeqState& st = a.st[seq];
-                const bool valid = i < st.pend_len;
-                const bf16_t* erow = a.emb + (size_t)(valid ? st.pend_ids[i] : 0) * K;
-                const bf16_t* prow = a.pos + (size_t)(valid ? st.ctx_len + i : 0) * K;
-                const uint2 e = *reinterpret_cast<const uint2*>(erow + cc);
-                const uint2 q = *reinterpret_cast<const uint2*>(prow + cc);
-                float4 x;
-                x.x = __uint_as_float(e.x << 16) + __uint_as_float(q.x << 16);
-                x.y = __uint_as_float(e.x & 0xFFFF0000u) + __uint_as_float(q.x & 0xFFFF0000u);
-                x.z = __uint_as_float(e.y << 16) + __uint_as_float(q.y << 16);
-                x.w = __uint_as_float(e.y & 0xFFFF0000u) + __uint_as_float(q.y & 0xFFFF0000u);
-                hv[j] = valid ? x : make_float4(0.f, 0.f, 0.f, 0.f);
+                const int m = rg + RG * j;
+                if (m < M && rg < RG) {
+                    const int seq = m / a.Q, i = m - seq * a.Q;
+                    const SeqState& st = a.st[seq];
+                    const bool valid = i < st.pend_len;
+                    const bf16_t* erow = a.emb + (size_t)(valid ? st.pend_ids[i] : 0) * K;
+                    const bf16_t* prow = a.pos + (size_t)(valid ? st.ctx_len + i : 0) * K;
+                    const uint2 e = *reinterpret_cast<const uint2*>(erow + cc);
+                    const uint2 q = *reinterpret_cast<const uint2*>(prow + cc);
+                    float4 x;
+                    x.x = __uint_as_float(e.x << 16) + __uint_as_float(q.x << 16);
+                    x.y = __uint_as_float(e.x & 0xFFFF0000u) + __uint_as_float(q.x & 0xFFFF0000u);
+                    x.z = __uint_as_float(e.y << 16) + __uint_as_float(q.y << 16);
+                    x.w = __uint_as_float(e.y & 0xFFFF0000u) + __uint_as_float(q.y & 0xFFFF0000u);
+                    hv[j] = valid ? x : make_float4(0.f, 0.f, 0.f, 0.f);
+                }
             }
         } else {
-            // complete the residual: h + (sum of the four partials + bias)
+            // the residual row: the sum of the four partials, or h itself
 #pragma unroll
             for (int j = 0; j < RPT; ++j) {
-                bool use_z = false;
-                if constexpr (XM == 3) use_z = !(a.Q > 0 && st_pl[j] == a.Q);
-                float4 t;
-                t.x = ((pv[0][j].x + pv[1][j].x) + (pv[2][j].x + pv[3][j].x)) + rb.x;
-                t.y = ((pv[0][j].y + pv[1][j].y) + (pv[2][j].y + pv[3][j].y)) + rb.y;
-                t.z = ((pv[0][j].z + pv[1][j].z) + (pv[2][j].z + pv[3][j].z)) + rb.z;
-                t.w = ((pv[0][j].w + pv[1][j].w) + (pv[2][j].w + pv[3][j].w)) + rb.w;
-                if (!has_part) t = make_float4(0.f, 0.f, 0.f, 0.f);
-                float4 x = make_float4(hv[j].x + t.x, hv[j].y + t.y, hv[j].z + t.z, hv[j].w + t.w);
-                if constexpr (XM == 3) {
-                    if (use_z) x = zv[j];
-                }
-                hv[j] = x;
-            }
-            if constexpr (XM == 3) {
-                // a partially filled pending chunk (not produced by the decode
-                // loop, which only ever leaves 0 or Q rows): recompute that row
-#pragma unroll
-                for (int j = 0; j < RPT; ++j) {
-                    const int m = rg + RG * j;
-                    if (m < M && rg < RG && a.Q > 0 && st_pl[j] > 0 && st_pl[j] < a.Q) {
-                        const int row = m * a.Q + st_pl[j] - 1;
-                        float4 x = *reinterpret_cast<const float4*>(a.h + (size_t)row * a.ldh + cc);
-                        float4 t = make_float4(0.f, 0.f, 0.f, 0.f);
-                        if (has_part) {
-                            float4 p4[4];
-#pragma unroll
-                            for (int s2 = 0; s2 < 4; ++s2)
-                                p4[s2] = *reinterpret_cast<const float4*>(a.part + ((size_t)s2 * a.part_rows + row) * a.ldh + cc);
-                            t.x = ((p4[0].x + p4[1].x) + (p4[2].x + p4[3].x)) + rb.x;
-                            t.y = ((p4[0].y + p4[1].y) + (p4[2].y + p4[3].y)) + rb.y;
-                            t.z = ((p4[0].z + p4[1].z) + (p4[2].z + p4[3].z)) + rb.z;
-                            t.w = ((p4[0].w + p4[1].w) + (p4[2].w + p4[3].w)) + rb.w;
-                        }
-                        hv[j] = make_float4(x.x + t.x, x.y + t.y, x.z + t.z, x.w + t.w);
+                const int m = rg + RG * j;
+                if (m < M && rg < RG) {
+                    float4 x = hv[j];
+                    if (has_part) {
+                        x.x = (pv[0][j].x + pv[1][j].x) + (pv[2][j].x + pv[3][j].x);
+                        x.y = (pv[0][j].y + pv[1][j].y) + (pv[2][j].y + pv[3][j].y);
+                        x.z = (pv[0][j].z + pv[1][j].z) + (pv[2][j].z + pv[3][j].z);
+                        x.w = (pv[0][j].w + pv[1][j].w) + (pv[2][j].w + pv[3][j].w);
                     }
+                    if constexpr (XM == 3) {
+                        const int pl = st_pl[j];
+                        if (!(a.Q > 0 && pl == a.Q)) x = zv[j];
+                        // a partially filled pending chunk (not produced by the
+                        // decode loop, which leaves 0 or Q rows): that row instead
+                        if (a.Q > 0 && pl > 0 && pl < a.Q) {
+                            const int row = m * a.Q + pl - 1;
+                            if (has_part) {
+                                float4 p4[4];
+#pragma unroll
+                                for (int s2 = 0; s2 < 4; ++s2)
+                                    p4[s2] = *reinterpret_cast<const float4*>(a.part + ((size_t)s2 * a.part_rows + row) * a.ldh + cc);
+                                x.x = (p4[0].x + p4[1].x) + (p4[2].x + p4[3].x);
+                                x.y = (p4[0].y + p4[1].y) + (p4[2].y + p4[3].y);
+                                x.z = (p4[0].z + p4[1].z) + (p4[2].z + p4[3].z);
+                                x.w = (p4[0].w + p4[1].w) + (p4[2].w + p4[3].w);
+                            } else {
+                                x = *reinterpret_cast<const float4*>(a.h + (size_t)row * a.ldh + cc);
+                            }
+                        }
+                    }
+                    hv[j] = x;
                 }
             }
         }
-        // workgroup 0 writes the completed rows (the next consumer's h)
+        // workgroup 0 writes the completed rows (the next projection's residual input)
         if (a.h_out && blockIdx.x == 0 && blockIdx.y == 0 && rg < RG) {
 #pragma unroll
             for (int j = 0; j < RPT; ++j) {
@@ -396,16 +442,20 @@ __global__ __launch_bounds__(GV_T) void gemv_kernel(GemvArgs a, Epi epi) {
         // waves of a row group cover its row exactly once
 #pragma unroll
         for (int j = 0; j < RPT; ++j) {
-            const float4 x = hv[j];
-            float s1 = (x.x + x.y) + (x.z + x.w);
-            float s2 = (x.x * x.x + x.y * x.y) + (x.z * x.z + x.w * x.w);
-            s1 = wave_sum64(s1);
-            s2 = wave_sum64(s2);
-            if (lane == 0) s_stat[wave][j] = make_float2(s1, s2);
+            const int m = rg + RG * j;
+            if (m < M && rg < RG) {
+                const float4 x = hv[j];
+                float s1 = (x.x + x.y) + (x.z + x.w);
+                float s2 = (x.x * x.x + x.y * x.y) + (x.z * x.z + x.w * x.w);
+                s1 = wave_sum64(s1);
+                s2 = wave_sum64(s2);
+                if (lane == 0) s_stat[wave][j] = make_float2(s1, s2);
+            }
         }
         __syncthreads();
         const float inv_k = 1.f / (float)K;
         const int wpg = K4 >> 6;                  // waves per row group
+        const f32x4_t g4 = s_gb[cc >> 2], b4 = s_gb[K4 + (cc >> 2)];
 #pragma unroll
         for (int j = 0; j < RPT; ++j) {
             const int m = rg + RG * j;
@@ -420,10 +470,10 @@ __global__ __launch_bounds__(GV_T) void gemv_kernel(GemvArgs a, Epi epi) {
             const float var = fmaxf(t2 * inv_k - mean * mean, 0.f);
             const float rstd = rsqrtf(var + 1e-5f);
             const float4 x = hv[j];
-            const float y0 = (x.x - mean) * rstd * gv.x + bv.x;
-            const float y1 = (x.y - mean) * rstd * gv.y + bv.y;
-            const float y2 = (x.z - mean) * rstd * gv.z + bv.z;
-            const float y3 = (x.w - mean) * rstd * gv.w + bv.w;
+            const float y0 = (x.x - mean) * rstd * g4[0] + b4[0];
+            const float y1 = (x.y - mean) * rstd * g4[1] + b4[1];
+            const float y2 = (x.z - mean) * rstd * g4[2] + b4[2];
+            const float y3 = (x.w - mean) * rstd * g4[3] + b4[3];
             *reinterpret_cast<uint2*>(xs + (size_t)m * ldl + cc) = make_uint2(pack2(y0, y1), pack2(y2, y3));
         }
     }
@@ -440,39 +490,40 @@ __global__ __launch_bounds__(GV_T) void gemv_kernel(GemvArgs a, Epi epi) {
         }
 
     // ---- F. sum the waves' K slices, epilogue ----
-    red[wave][lane] = acc;
+    red[wave * 64 + lane] = acc;
     __syncthreads();
     if (wave == 0 && em < M && en < N) {
-        f32x4_t sum = red[0][lane];
+        f32x4_t sum = red[lane];
 #pragma unroll
-        for (int w = 1; w < NW; ++w) sum += red[w][lane];
+        for (int w = 1; w < NW; ++w) sum += red[w * 64 + lane];
         const float v[4] = {sum[0], sum[1], sum[2], sum[3]};
         epi.store(pre, em, en, v, envalid);
     }
 }
 
 // --------------------------------------------------------------- launching
-template <int MR, int XM, int MAXF, int KCH, int MAXS, class Epi>
+template <int MR, int XM, int MAXF, int KCH, int MAXS, class Epi, int NW = GV_NW>
 static hipError_t gemv_go(hipStream_t st, const GemvArgs& a, int splits, const Epi& e) {
     dim3 grid((a.N + 15) / 16, splits);
     const size_t lds = (size_t)16 * (a.K / splits + 8) * 2;
     static bool attr_set = false;
     if (lds > 32 * 1024 && !attr_set) {
-        hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemv_kernel<MR, XM, MAXF, KCH, MAXS, Epi>),
+        hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemv_kernel<MR, XM, MAXF, KCH, MAXS, NW, Epi>),
                                              hipFuncAttributeMaxDynamicSharedMemorySize, 128 * 1024);
         if (err != hipSuccess) return err;
         attr_set = true;
     }
-    hipLaunchKernelGGL((gemv_kernel<MR, XM, MAXF, KCH, MAXS, Epi>), grid, dim3(GV_T), lds, st, a, e);
+    hipLaunchKernelGGL((gemv_kernel<MR, XM, MAXF, KCH, MAXS, NW, Epi>), grid, dim3(64 * NW), lds, st, a, e);
     return hipGetLastError();
 }
 
 // LayerNorm modes: K = d_model <= 2048, one K range
-template <int XM, class Epi>
+template <int XM, class Epi, int NW = GV_NW>
 static hipError_t gemv_ln(hipStream_t st, const GemvArgs& a, const Epi& e) {
     const bool wide = a.K > 1024;
+    constexpr int MF = 32 / NW;                   // fragments per wave at K = 1024
 #define MTP_GEMV_LN(MR) \
-    return wide ? gemv_go<MR, XM, 4, 2, 1>(st, a, 1, e) : gemv_go<MR, XM, 2, 1, 1>(st, a, 1, e)
+    return wide ? gemv_go<MR, XM, 2 * MF, 2, 1, Epi, NW>(st, a, 1, e) : gemv_go<MR, XM, MF, 1, 1, Epi, NW>(st, a, 1, e)
     if (a.M <= 1) MTP_GEMV_LN(1);
     if (a.M <= 2) MTP_GEMV_LN(2);
     if (a.M <= 4) MTP_GEMV_LN(4);
@@ -514,7 +565,7 @@ hipError_t gemv(hipStream_t st, const GemvArgs& a) {
     if (a.M < 1 || a.M > 16 || a.N < 4 || a.K % 128) return hipErrorInvalidValue;
     if (a.epi == EPI_PARTIAL) {
         if (a.N % 4 || a.K > 4 * 8 * GV_NW * 32) return hipErrorInvalidValue;
-        EpiPart e{a.part_out, a.N, a.M};
+        EpiPart e{a.part_out, a.N, a.M, a.h, a.bias};
         if (a.xmode == 4) {
             if (a.K > 2048 || a.K % 256 || a.n_splits < 1 || a.Q < 1 ||
                 a.n_splits > gemv_merge_max_splits(a.M, a.K) || a.split_len < 1)
@@ -549,8 +600,10 @@ hipError_t gemv(hipStream_t st, const GemvArgs& a) {
         return hipErrorInvalidValue;
     }
     case EPI_LOGITS: {
+        // K x 1025 columns is a few tiles more than there are CUs: 8-wave
+        // workgroups, two per CU, so the extra tiles do not form a second round
         EpiLogitsB e{(float*)a.out, a.bias, a.ldo, a.N};
-        if (a.xmode == 3) return gemv_ln<3>(st, a, e);
+        if (a.xmode == 3) return gemv_ln<3, EpiLogitsB, 8>(st, a, e);
         return hipErrorInvalidValue;
     }
     }

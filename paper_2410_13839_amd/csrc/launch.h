@@ -83,9 +83,12 @@ struct GemvArgs {
     int M, N, K;
     const bf16_t* W;
     const bf16_t* x; int ldx;                       // xmode 0
-    const float* h; int ldh;                        // residual rows (xmode 1, 3), row stride = d
-    const float* part; int part_rows;               // [4][part_rows][d] split-K partials to add (xmode 1, 3; may be NULL)
-    const float* res_bias;                          // bias of the projection that produced `part`
+    const float* h; int ldh;                        // residual rows, row stride = d: the LayerNorm input of
+                                                    // xmode 1, 3 when part_on is 0; EPI_PARTIAL: the residual
+                                                    // input its first K range adds (with `bias`)
+    const float* part; int part_rows;               // [4][part_rows][d] split-K partials whose sum is the
+                                                    // LayerNorm input (xmode 1, 3 with part_on)
+    int part_on;
     const float* g; const float* beta;              // LN gain / shift
     const SeqState* st; int Q;                      // xmode 2, 3, 4 and EPI_QKV
     const bf16_t* emb; const bf16_t* pos;           // xmode 2
