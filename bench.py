@@ -37,6 +37,8 @@ def _parse():
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--copy-probe", action="store_true", help="also run a 256 MiB device copy (PMC calibration)")
+    ap.add_argument("--replay-passes", type=int, default=20, help="passes of the per-class replay timing")
+    ap.add_argument("--no-warm-replay", action="store_true", help="skip the cache-warm replay figures")
     return ap.parse_args()
 
 
@@ -111,6 +113,41 @@ def launch_bytes(wl, kclass, ctx):
     raise ValueError(kclass)
 
 
+def kernel_source_digest():
+    """Digest of the HIP sources: PMC traffic figures are valid only for the
+    kernels they were taken on."""
+    import glob
+    import hashlib
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2410_13839_amd", "csrc", "*"))):
+        if f.endswith((".hip", ".h")):
+            h.update(os.path.basename(f).encode())
+            with open(f, "rb") as fh:
+                h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def pmc_traffic(workload, kclass):
+    """HBM bytes per launch of kernel class `kclass` from the committed PMC
+    summary (FETCH_SIZE and WRITE_SIZE in KiB per dispatch, scaled by the
+    factors a copy of known size gives), or None when there is none for this
+    workload and class or the kernels changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    digest = kernel_source_digest()
+    with open(path) as fh:
+        for line in fh:
+            if not line.startswith("pmc:"):
+                continue
+            kv = dict(item.split("=", 1) for item in line[4:].split())
+            if int(kv["class"]) != kclass or kv["source"] != digest:
+                continue
+            return int(round(float(kv["fetch_kib"]) * 1024 * float(kv["fetch_factor"])
+                             + float(kv["write_kib"]) * 1024 * float(kv["write_factor"])))
+    return None
+
+
 def replay_kernels(sess, wl, prompts, steps, iters, torch, cold=True):
     """Per kernel class: average launch time (us) over `iters` replays of the
     class's launches in one decode step (one per layer), mid-generation after
@@ -118,13 +155,17 @@ def replay_kernels(sess, wl, prompts, steps, iters, torch, cold=True):
     as the other layers' weights evict them in a real step."""
     from paper_2410_13839_amd.binding import mtp_profile_replay
     sess.prefill(prompts.phon, prompts.ac)
-    for _ in range(steps):
+    for i in range(steps):
         sess.step_async(wl.K, wl.top_k)
+        if i % 25 == 24:
+            torch.cuda.synchronize()
+            print(f"[bench] replay set-up: step {i + 1}/{steps}", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     ctx = int(sess.seq_state()["ctx_len"].max())
     out = {}
     for kc in KCLASSES:
         out[kc] = mtp_profile_replay(sess.ctx, kc, iters, cold)
+        print(f"[bench] replay {'cold' if cold else 'warm'} class {kc}: {out[kc]:.3f} us", file=sys.stderr, flush=True)
     return out, ctx
 
 
@@ -182,9 +223,12 @@ def main():
 
     # per-kernel launch times (back-to-back replays) and the dominant kernel
     mid = _steps_per_generation(wl) // 2
-    passes = 20
+    passes = args.replay_passes
     times, ctx = replay_kernels(sess, wl, prompts, mid, passes, torch, cold=True)
-    warm, _ = replay_kernels(sess, wl, prompts, mid, passes, torch, cold=False)
+    if args.no_warm_replay:
+        warm = {kc: float("nan") for kc in times}
+    else:
+        warm, _ = replay_kernels(sess, wl, prompts, mid, passes, torch, cold=False)
     L = wl.model.n_layers
     kernels = {}
     for kc, us in times.items():
@@ -193,12 +237,12 @@ def main():
         kernels[name] = {"avg_launch_us": round(us, 3), "launches_per_step": per_step(L),
                          "bytes_per_launch": nbytes, "GB_s": round(nbytes / (us * 1e-6) / 1e9, 1),
                          "share_of_step": round(us * per_step(L) / (ms_step * 1000.0), 3),
-                         "avg_launch_us_cache_warm": round(warm[kc], 3)}
+                         "avg_launch_us_cache_warm": round(warm[kc], 3) if warm[kc] == warm[kc] else None}
     dom = max(times, key=lambda kc: times[kc] * KCLASSES[kc][1](L))
     dname = KCLASSES[dom][0]
     dk = kernels[dname]
     roof = {"kernel": dname, "bound": "hbm", "achieved": dk["GB_s"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(dk["GB_s"] / HBM_PEAK_GBS, 4), "traffic": None,
+            "frac": round(dk["GB_s"] / HBM_PEAK_GBS, 4), "traffic": pmc_traffic(wl.name, dom),
             "bytes_per_launch": dk["bytes_per_launch"], "avg_launch_us": dk["avg_launch_us"],
             "measured": f"{passes} passes over the {KCLASSES[dom][1](L)} launches of one step at step {mid} "
                         f"(context {ctx} tokens), caches evicted before each pass, HIP events on the library stream"}
