@@ -94,9 +94,20 @@ typedef struct mtp_buffers {
 } mtp_buffers;
 
 /* Weight tensors in packing order.  Matrices (_W_, tables) are stored in the
- * model dtype, row-major [out][in] for Linear weights; vectors (biases,
- * LayerNorm gain/shift) are always float32.  Per-layer tensors repeat for
- * layer = 0 .. n_layers-1 in the order MTP_T_LN1_G .. MTP_T_B_2. */
+ * model dtype; vectors (biases, LayerNorm gain/shift) are always float32.
+ * Per-layer tensors repeat for layer = 0 .. n_layers-1 in the order
+ * MTP_T_LN1_G .. MTP_T_B_2.
+ *
+ * The tables (EMB_PHONE, EMB_AC, POS) and the fp32 model's Linear weights are
+ * row-major [rows][d] / [out][in].  The bf16 model's Linear weights (W_QKV,
+ * W_O, W_1, W_2, and W_HEADS read as one [k_heads * vocab][d] matrix) are
+ * stored in MFMA fragment order so that every 16-row x 32-column fragment is
+ * one contiguous 1 KB: with N rows (out) and K columns (in, a multiple of 32),
+ * the rows are padded with zeros to a multiple of 16 and element (n, k) sits
+ * at index
+ *     ((n / 16) * (K / 32) + k / 32) * 512 + ((k % 32) / 8) * 128 + (n % 16) * 8 + k % 8,
+ * so a tensor occupies ceil(N / 16) * 16 * K elements (mtp_weight_offset
+ * still reports N * K). */
 enum mtp_tensor {
     MTP_T_EMB_PHONE = 0,  /* [n_phone][d]                  */
     MTP_T_EMB_AC,         /* [vocab][d]                    */

@@ -207,6 +207,21 @@ _LAYER_TENSOR_OF = {"ln1_g": MTP_T_LN1_G, "ln1_b": MTP_T_LN1_B, "w_qkv": MTP_T_W
 _MATRICES = {MTP_T_EMB_PHONE, MTP_T_EMB_AC, MTP_T_POS, MTP_T_W_QKV, MTP_T_W_O, MTP_T_W_1, MTP_T_W_2, MTP_T_W_HEADS}
 
 
+_TILED = {MTP_T_W_QKV, MTP_T_W_O, MTP_T_W_1, MTP_T_W_2, MTP_T_W_HEADS}
+
+
+def tile_bf16_matrix(w: np.ndarray) -> np.ndarray:
+    """[N][K] matrix (any dtype) -> flat MFMA fragment order of mtp.h: rows
+    padded to a multiple of 16, then per (16-row block, 32-column block) a
+    fragment whose slot 16 g + r holds row r, columns 8 g .. 8 g + 7."""
+    n, k = w.shape
+    assert k % 32 == 0, k
+    npad = (n + 15) // 16 * 16
+    p = np.zeros((npad, k), w.dtype)
+    p[:n] = w
+    return np.ascontiguousarray(p.reshape(npad // 16, 16, k // 32, 4, 8).transpose(0, 2, 3, 1, 4)).reshape(-1)
+
+
 def pack_weights(cfg: mtp_config, weights: Dict[str, np.ndarray]) -> np.ndarray:
     """Host image of the packed weights buffer (uint8) in the library's layout."""
     total = mtp_query_sizes(cfg).weights_bytes
@@ -223,7 +238,10 @@ def pack_weights(cfg: mtp_config, weights: Dict[str, np.ndarray]) -> np.ndarray:
         if t in _MATRICES and cfg.dtype == MTP_DTYPE_BF16:
             raw = (a.view(np.uint32) >> 16).astype(np.uint16)
             assert np.array_equal((raw.astype(np.uint32) << 16).view(np.float32), a), f"{name} is not bf16-exact"
-            img[off:off + 2 * n] = raw.view(np.uint8)
+            if t in _TILED:
+                k = cfg.d_ff if t == MTP_T_W_2 else cfg.d_model
+                raw = tile_bf16_matrix(raw.reshape(-1, k))
+            img[off:off + 2 * raw.size] = raw.view(np.uint8)
         else:
             img[off:off + 4 * n] = a.view(np.uint8)
     return img

@@ -53,7 +53,20 @@ uint64_t tensor_numel(const mtp_config& c, int t) {
     return 0;
 }
 
+// bf16 Linear weights are stored in MFMA fragment order with the rows padded
+// to a multiple of 16 (layout in mtp.h).
+bool is_tiled(const mtp_config& c, int t) {
+    return c.dtype == MTP_DTYPE_BF16 &&
+           (t == MTP_T_W_QKV || t == MTP_T_W_O || t == MTP_T_W_1 || t == MTP_T_W_2 || t == MTP_T_W_HEADS);
+}
+
+uint64_t tensor_cols(const mtp_config& c, int t) { return t == MTP_T_W_2 ? (uint64_t)c.d_ff : (uint64_t)c.d_model; }
+
 uint64_t tensor_bytes(const mtp_config& c, int t) {
+    if (is_tiled(c, t)) {
+        const uint64_t K = tensor_cols(c, t), N = tensor_numel(c, t) / K;
+        return (N + 15) / 16 * 16 * K * 2;
+    }
     return tensor_numel(c, t) * (is_matrix(t) ? (c.dtype == MTP_DTYPE_BF16 ? 2 : 4) : 4);
 }
 
@@ -170,6 +183,7 @@ struct mtp_ctx {
     int q_pad = 0;               // pending rows per sequence for the next step
     int last_K = 0, last_topk = 0;
     int split_len = 64, n_splits = 1;
+    int64_t plan_ctx = 0;        // longest prompt + budget of the batch (sizes the split plan)
     std::vector<int32_t> h_ids, h_last, h_btab;
     std::vector<RowInfo> h_rows;
     std::vector<int2> h_tiles;
@@ -450,12 +464,50 @@ int enqueue_step(mtp_ctx* c, int K, int top_k) {
     return MTP_OK;
 }
 
+// Decode attention split plan for a step with Q pending rows per sequence,
+// fixed per (batch, Q) so one captured graph serves every such step.  Small
+// batches split the keys into short ranges so that they spread over many CUs
+// (one CU streams only ~25 GB/s from HBM) and the out-projection merges the
+// partials of its own heads; larger batches aim at ~512 (sequence, head,
+// split) workgroups and merge in a separate launch.
+int plan_splits(mtp_ctx* c, int Q) {
+    const mtp_config& cf = c->cfg;
+    const int64_t max_ctx = std::max<int64_t>(c->plan_ctx, 1);
+    const int64_t B = std::max(c->B, 1);
+    const int64_t rows = B * std::max(Q, 1);
+    const int merge_max =
+        (cf.dtype == MTP_DTYPE_BF16 && rows <= 16) ? gemv_merge_max_splits((int)rows, cf.d_model) : 0;
+    int64_t sl;
+    if (merge_max >= 2) {
+        sl = std::max<int64_t>(128, ((max_ctx + merge_max - 1) / merge_max + 63) / 64 * 64);
+    } else {
+        const int64_t bh = B * cf.n_heads;
+        const int64_t want = std::max<int64_t>(1, (512 + bh - 1) / bh);
+        sl = (max_ctx + want - 1) / want;
+        sl = std::max<int64_t>(64, (sl + 63) / 64 * 64);
+    }
+    if (const char* env = getenv("MTP_SPLIT_LEN")) {
+        const int64_t v = atoll(env);
+        if (v >= 32 && v % 32 == 0) sl = v;
+    }
+    sl = std::max<int64_t>(sl, ((max_ctx + 63) / 64 + 63) / 64 * 64);   // at most 64 splits
+    const int64_t n = (max_ctx + sl - 1) / sl;
+    if (n > 64 || n > c->ws.max_splits) { c->err = "attention split plan exceeds workspace"; return MTP_ENOMEM; }
+    c->split_len = (int)sl;
+    c->n_splits = (int)n;
+    return MTP_OK;
+}
+
 int step_common(mtp_ctx* c, int K, int top_k) {
     if (!c) return MTP_EINVAL;
     if (!c->prefilled) { c->err = "decode step before prefill"; return MTP_ESTATE; }
     if (K < 1 || K > c->cfg.k_heads) { c->err = "K must be in 1..k_heads"; return MTP_EINVAL; }
     if (top_k < 1 || top_k > c->cfg.topk_max) { c->err = "top_k must be in 1..topk_max"; return MTP_EINVAL; }
     const bool use_graph = !(c->cfg.flags & MTP_FLAG_NO_GRAPH) && c->stream != nullptr;
+    {
+        const int rc0 = plan_splits(c, c->q_pad);
+        if (rc0) return rc0;
+    }
     const auto key = std::make_tuple(K, top_k, c->q_pad, c->B, c->split_len, c->n_splits);
     auto record = [&]() {
         mtp_ctx::StepLaunches& sl = c->step_launches[key];
@@ -643,35 +695,14 @@ int mtp_prefill(mtp_ctx* c, int B, const int32_t* phon, const int32_t* phon_len,
     f.z = nullptr;
     HIPCHK(c, final_ln(st, f), "prefill last rows");
 
-    // decode attention split plan, fixed for the batch so one captured graph
-    // serves every step: small batches split the keys into 256-key ranges
-    // (one chunk per workgroup) whose partials the out-projection prologue
-    // merges; larger batches aim at ~512 (sequence, head, split) workgroups
-    // and merge in a separate launch.
     int64_t max_ctx = 0;
     for (int b = 0; b < B; ++b) max_ctx = std::max<int64_t>(max_ctx, phon_len[b] + ac_len[b] + (int64_t)cf.max_new);
-    const int64_t bh = (int64_t)B * cf.n_heads;
-    const int64_t rows_max = (int64_t)B * cf.k_heads;
-    const int merge_max = (dt == MTP_DTYPE_BF16 && rows_max <= 16) ? gemv_merge_max_splits((int)rows_max, d) : 0;
-    int64_t sl;
-    if (merge_max >= 2) {
-        // one 256-key chunk per workgroup while the out-projection can merge
-        // that many splits, longer splits beyond
-        sl = std::max<int64_t>(256, ((max_ctx + merge_max - 1) / merge_max + 31) / 32 * 32);
-    } else {
-        const int64_t want = std::max<int64_t>(1, (512 + bh - 1) / bh);
-        sl = (max_ctx + want - 1) / want;
-        sl = std::max<int64_t>(64, (sl + 31) / 32 * 32);
-    }
-    if (const char* env = getenv("MTP_SPLIT_LEN")) {
-        const int64_t v = atoll(env);
-        if (v >= 32 && v % 32 == 0) sl = v;
-    }
-    c->split_len = (int)sl;
-    c->n_splits = (int)((max_ctx + sl - 1) / sl);
-    if (c->n_splits > 64 || c->n_splits > c->ws.max_splits) { c->err = "attention split plan exceeds workspace"; return MTP_ENOMEM; }
-
+    c->plan_ctx = max_ctx;
     c->B = B;
+    {
+        const int rc = plan_splits(c, 0);
+        if (rc) return rc;
+    }
     c->q_pad = 0;
     c->prefilled = true;
     c->n_pre_rows = rows;

@@ -110,9 +110,9 @@ __global__ __launch_bounds__(256) void gemm_skinny_bf16(const bf16_t* __restrict
     const int n0 = blockIdx.x * 16;
     const int split = blockIdx.y;
     const int kb = split * k_per_split;
-    const int nrow = n0 + r;
-    const bool wvalid = nrow < N;
-    const bf16_t* wp = W + (size_t)(wvalid ? nrow : 0) * K + kb + g * 8;
+    // W in the packed fragment order (rows padded to a multiple of 16): the
+    // fragment of k step s is 1 KB at wp + s * 512
+    const bf16_t* wp = W + ((size_t)blockIdx.x * (K >> 5) + (kb >> 5)) * 512 + lane * 8;
     const bf16_t* xp[MT];
     bool xvalid[MT];
 #pragma unroll
@@ -133,7 +133,7 @@ __global__ __launch_bounds__(256) void gemm_skinny_bf16(const bf16_t* __restrict
         for (int u = 0; u < UNROLL; ++u) {
             const int ss = s + 4 * u;
             const bool in = ss < nsteps;
-            wv[u] = (in && wvalid) ? *reinterpret_cast<const uint4*>(wp + ss * 32) : make_uint4(0, 0, 0, 0);
+            wv[u] = in ? *reinterpret_cast<const uint4*>(wp + (size_t)ss * 512) : make_uint4(0, 0, 0, 0);
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt)
                 xv[u][mt] = (in && xvalid[mt]) ? *reinterpret_cast<const uint4*>(xp[mt] + ss * 32)
@@ -202,12 +202,17 @@ __global__ __launch_bounds__(256) void gemm_tiled_bf16(const bf16_t* __restrict_
             int m = m0 + row;
             xr[c] = (m < M) ? *reinterpret_cast<const uint4*>(X + (size_t)m * ldx + k0 + col) : make_uint4(0, 0, 0, 0);
         }
+        // W tile in the packed fragment order: each wave load is one 1 KB
+        // fragment (16 rows x 32 columns); fragment t of the tile is row block
+        // t / 2, column block t % 2 (the row-block test is uniform per wave)
 #pragma unroll
         for (int c = 0; c < WCH; ++c) {
-            int ch = tid + c * 256;
-            int row = ch >> 3, col = (ch & 7) * 8;
-            int n = n0 + row;
-            wr[c] = (n < N) ? *reinterpret_cast<const uint4*>(W + (size_t)n * K + k0 + col) : make_uint4(0, 0, 0, 0);
+            const int ch = tid + c * 256;
+            const int t = ch >> 6, l = ch & 63;
+            const int rt = t >> 1, fk = t & 1;
+            wr[c] = (n0 + rt * 16 < N)
+                        ? *reinterpret_cast<const uint4*>(W + ((size_t)((n0 >> 4) + rt) * (K >> 5) + (k0 >> 5) + fk) * 512 + l * 8)
+                        : make_uint4(0, 0, 0, 0);
         }
     };
     auto sstore = [&](int buf) {
@@ -218,8 +223,9 @@ __global__ __launch_bounds__(256) void gemm_tiled_bf16(const bf16_t* __restrict_
         }
 #pragma unroll
         for (int c = 0; c < WCH; ++c) {
-            int ch = tid + c * 256;
-            *reinterpret_cast<uint4*>(&Ws[buf][ch >> 3][(ch & 7) * 8]) = wr[c];
+            const int ch = tid + c * 256;
+            const int t = ch >> 6, l = ch & 63;
+            *reinterpret_cast<uint4*>(&Ws[buf][(t >> 1) * 16 + (l & 15)][(t & 1) * 32 + (l >> 4) * 8]) = wr[c];
         }
     };
 

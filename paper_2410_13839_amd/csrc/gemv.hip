@@ -12,7 +12,8 @@
 //    after all weights landed; every load is unconditional from a clamped,
 //    valid address (a predicated load compiles to a branch plus a full wait);
 //  * the weight fragments of the workgroup's 16 output columns (its K range)
-//    then go out at once, straight into MFMA registers;
+//    then go out at once, straight into MFMA registers; the packed weight
+//    order makes every fragment one contiguous 1 KB wave load;
 //  * while they stream, the prologue builds the bf16 activation tile in LDS:
 //    LayerNorm of the residual rows (the residual itself is completed here:
 //    h_in + the previous projection's four split-K partial sums + its bias,
@@ -30,6 +31,8 @@
 // r and k = 8g..8g+7 of each 32-wide k step, the same k for A and B.
 // Activation rows >= M are never written to LDS: their garbage only reaches
 // output columns >= M, which are never stored.
+#include <algorithm>
+
 #include "common.h"
 #include "launch.h"
 #include "wave.h"
@@ -189,7 +192,13 @@ __global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
     constexpr int RPT = (MR * KCH * 256 + T - 1) / T;                  // rows per thread (LN modes)
     __shared__ float2 s_stat[NW][LN ? RPT : 1];
     constexpr int XI = (MR * MAXF + 15) / 16;                          // 16-byte chunks per thread (XM 0)
-    constexpr int XP = (MR * KCH * 64 + T - 1) / T;                    // float4 chunks per thread (XM 4)
+    // XM 4: the (row, float4 column chunk) items of this K range (at most
+    // MR * 64 * KCH) x the splits; GS groups of threads take every GS-th split
+    constexpr int CPRM = 64 * KCH;
+    constexpr int GS = (T / (MR * CPRM)) > 0 ? (T / (MR * CPRM)) : 1;
+    constexpr int SPT = (MAXS + GS - 1) / GS;                          // splits per thread
+    constexpr int MLP = (MR * 4 * KCH * MAXS + T - 1) / T;             // (max, sum) words per thread
+    __shared__ float2 s_ml[XM == 4 ? MR * 4 * KCH * MAXS : 1];
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int r = lane & 15, g = lane >> 4;
@@ -219,10 +228,12 @@ __global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
     typedef unsigned int xq_t __attribute__((ext_vector_type(4 * XI)));
     xq_t xq;
     int st_pl[XM == 3 ? RPT : 1];
-    int2 sti[XM == 4 ? XP : 1];                  // (ctx_len, pend_len) of the row's sequence
-    float2 ml[XM == 4 ? XP : 1][MAXS];           // (running max, sum) per split
-    float4 ov[XM == 4 ? XP : 1][MAXS];           // unnormalised outputs per split
-    (void)pv; (void)zv; (void)xq; (void)st_pl; (void)sti; (void)ml; (void)ov; (void)gv; (void)bv; (void)hv;
+    int2 sti = make_int2(0, 0);                  // XM 4: (ctx_len, pend_len) of the item's sequence
+    float2 mlv[XM == 4 ? MLP : 1];               // XM 4: (running max, sum) words
+    float4 ov[XM == 4 ? SPT : 1];                // XM 4: unnormalised outputs of the thread's splits
+#pragma unroll
+    for (int j = 0; j < (XM == 4 ? SPT : 1); ++j) ov[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+    (void)pv; (void)zv; (void)xq; (void)st_pl; (void)sti; (void)mlv; (void)ov; (void)gv; (void)bv; (void)hv;
     const bool has_part = a.part_on != 0;      // kernel argument: uniform
     if constexpr (XM == 0) {
         // rows [0, M) x columns [kb, kb + ks) as 16-byte chunks
@@ -239,27 +250,34 @@ __global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
             xq[4 * i + 3] = t.w;
         }
     } else if constexpr (XM == 4) {
-        // rows [0, M) x columns [kb, kb + ks) as float4 chunks; every split's
-        // partial is requested (clamped to the launched splits) and the ones
-        // past the sequence's context are discarded once its state is known
-        const int cpr = ks >> 2;
-        const int total = M * cpr;
-        const int H = K >> 6;
+        // the (max, sum) word of every (row, head, split) of this K range, and
+        // the thread's item (row, float4 chunk) in each of its splits; splits
+        // past the launched ones are clamped, the ones past the sequence's
+        // context are discarded once its state is known
+        const int cpr = ks >> 2, items = M * cpr, HW = ks >> 6, h0 = kb >> 6;
+        const int H = K >> 6, S = a.n_splits;
         const size_t sstride = (size_t)a.qt * 68;
+        const int nml = M * HW * S;
 #pragma unroll
-        for (int p = 0; p < XP; ++p) {
-            const int idx = min(tid + T * p, total - 1);
-            const int m = idx / cpr, c = kb + (idx - m * cpr) * 4;
+        for (int p = 0; p < MLP; ++p) {
+            const int idx = min(tid + T * p, nml - 1);
+            const int m = idx / (HW * S), rem = idx - m * (HW * S);
+            const int hd = rem / S, sp = rem - hd * S;
             const int seq = m / a.Q, i = m - seq * a.Q;
-            sti[p] = *reinterpret_cast<const int2*>(&a.st[seq]);
-            const float* e0 = a.apart + (size_t)(seq * H + (c >> 6)) * a.n_splits * sstride + (size_t)i * 68;
-#pragma unroll
-            for (int sp = 0; sp < MAXS; ++sp) {
-                const float* e = e0 + (size_t)min(sp, a.n_splits - 1) * sstride;
-                ml[p][sp] = *reinterpret_cast<const float2*>(e);
-                ov[p][sp] = *reinterpret_cast<const float4*>(e + 4 + (c & 63));
-            }
+            mlv[p] = *reinterpret_cast<const float2*>(a.apart + ((size_t)(seq * H + h0 + hd) * S + sp) * sstride + (size_t)i * 68);
         }
+        const int TG = T / GS, sg = __builtin_amdgcn_readfirstlane(tid / TG);
+        const int it = min(tid - sg * TG, items - 1);
+        const int m = it / cpr, c = kb + (it - m * cpr) * 4;
+        const int seq = m / a.Q, i = m - seq * a.Q;
+        sti = *reinterpret_cast<const int2*>(&a.st[seq]);
+        const float* e0 = a.apart + (size_t)(seq * H + (c >> 6)) * S * sstride + (size_t)i * 68 + 4 + (c & 63);
+        // sg is uniform over a wave (groups are 256 threads or more) and S is
+        // a kernel argument: skipping the splits that were not launched costs
+        // no wait
+#pragma unroll
+        for (int j = 0; j < SPT; ++j)
+            if (sg + GS * j < S) ov[j] = *reinterpret_cast<const float4*>(e0 + (size_t)(sg + GS * j) * sstride);
     } else {
         // LayerNorm gain and shift: loaded by row group 0 only, shared through LDS
         if (rg == 0) {
@@ -295,14 +313,14 @@ __global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
     // another wave's weight loads (HBM misses) would wait for them.
     __syncthreads();
 
-    // ---- B. weights of this workgroup's 16 columns, all in flight ----
-    const int nrow = min(n0 + r, N - 1);
-    const bf16_t* wp = a.W + (size_t)nrow * K + kb + g * 8;
+    // ---- B. weights of this workgroup's 16 columns, all in flight: in the
+    //      packed fragment order one 1 KB fragment per wave load ----
+    const bf16_t* wp = a.W + ((size_t)blockIdx.x * (K >> 5) + (kb >> 5)) * 512 + lane * 8;
     uint4 wv[MAXF];
 #pragma unroll
     for (int i = 0; i < MAXF; ++i) {
         const int f = min(wave + NW * i, nfrag - 1);
-        wv[i] = *reinterpret_cast<const uint4*>(wp + f * 32);
+        wv[i] = *reinterpret_cast<const uint4*>(wp + (size_t)f * 512);
     }
     // ---- C. epilogue operands ----
     const int em = r;
@@ -328,41 +346,55 @@ __global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
             }
         }
     } else if constexpr (XM == 4) {
-        const int cpr = ks >> 2;
-        const int total = M * cpr;
+        const int cpr = ks >> 2, items = M * cpr, HW = ks >> 6;
+        const int S = a.n_splits;
+        const int nml = M * HW * S;
 #pragma unroll
-        for (int p = 0; p < XP; ++p) {
+        for (int p = 0; p < MLP; ++p) {
             const int idx = tid + T * p;
-            if (idx < total) {
-                const int m = idx / cpr, c = kb + (idx - m * cpr) * 4;
-                const int i = m - (m / a.Q) * a.Q;
-                const int ctx = sti[p].x, pl = sti[p].y;
-                const int n_active = min(a.n_splits, (ctx + pl + a.split_len - 1) / a.split_len);
-                float mx = -INFINITY;
+            if (idx < nml) s_ml[idx] = mlv[p];
+        }
+        __syncthreads();
+        const int TG = T / GS, sg = tid / TG, it = tid - sg * TG;
+        const int m = min(it, items - 1) / cpr;
+        const int c = kb + (min(it, items - 1) - m * cpr) * 4;
+        const int i = m - (m / a.Q) * a.Q;
+        const int ctx = sti.x, pl = sti.y;
+        const int n_active = min(S, (ctx + pl + a.split_len - 1) / a.split_len);
+        const float2* ml = s_ml + (m * HW + ((c - kb) >> 6)) * S;
+        // splits past the context (or a key range fully masked for this row)
+        // contribute nothing; their words may be stale
+        float mx = -INFINITY;
+        for (int sp = 0; sp < n_active; ++sp) mx = fmaxf(mx, ml[sp].x);
+        float L = 0.f;
+        for (int sp = 0; sp < n_active; ++sp) {
+            const float2 v = ml[sp];
+            if (v.x != -INFINITY) L += __expf(v.x - mx) * v.y;
+        }
+        f32x4_t o = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int sp = 0; sp < MAXS; ++sp)
-                    if (sp < n_active) mx = fmaxf(mx, ml[p][sp].x);
-                float L = 0.f;
-                float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int j = 0; j < SPT; ++j) {
+            const int sp = sg + GS * j;
+            const float2 v = ml[min(sp, S - 1)];
+            const bool live = sp < n_active && v.x != -INFINITY;
+            const float w = live ? __expf(v.x - mx) : 0.f;
+            const float4 os = live ? ov[j] : make_float4(0.f, 0.f, 0.f, 0.f);
+            o[0] = fmaf(w, os.x, o[0]);
+            o[1] = fmaf(w, os.y, o[1]);
+            o[2] = fmaf(w, os.z, o[2]);
+            o[3] = fmaf(w, os.w, o[3]);
+        }
+        red[tid] = o;
+        __syncthreads();
+        if (sg == 0 && it < items) {
+            f32x4_t sum = red[it];
 #pragma unroll
-                for (int sp = 0; sp < MAXS; ++sp) {
-                    // splits past the context (or a key range fully masked for
-                    // this row) contribute nothing; their words may be stale
-                    const bool live = sp < n_active && ml[p][sp].x != -INFINITY;
-                    const float w = live ? __expf(ml[p][sp].x - mx) : 0.f;
-                    const float lw = live ? ml[p][sp].y : 0.f;
-                    const float4 os = live ? ov[p][sp] : make_float4(0.f, 0.f, 0.f, 0.f);
-                    L = fmaf(w, lw, L);
-                    o.x = fmaf(w, os.x, o.x);
-                    o.y = fmaf(w, os.y, o.y);
-                    o.z = fmaf(w, os.z, o.z);
-                    o.w = fmaf(w, os.w, o.w);
-                }
-                const bool valid = i < pl;
-                const float inv = 1.f / L;
-                const uint2 y = valid ? make_uint2(pack2(o.x * inv, o.y * inv), pack2(o.z * inv, o.w * inv)) : make_uint2(0u, 0u);
-                *reinterpret_cast<uint2*>(xs + (size_t)m * ldl + (c - kb)) = y;
-            }
+            for (int g2 = 1; g2 < GS; ++g2) sum += red[g2 * TG + it];
+            const bool valid = i < pl;
+            const float inv = 1.f / L;
+            const uint2 y = valid ? make_uint2(pack2(sum[0] * inv, sum[1] * inv), pack2(sum[2] * inv, sum[3] * inv))
+                                  : make_uint2(0u, 0u);
+            *reinterpret_cast<uint2*>(xs + (size_t)m * ldl + (c - kb)) = y;
         }
     } else {
         // row group 0 shares the LayerNorm gain and shift
@@ -545,20 +577,28 @@ static hipError_t gemv_part_rows(hipStream_t st, const GemvArgs& a, const EpiPar
 // split-K partial producer over merged attention partials (K = d <= 2048)
 template <int MR, int KCH>
 static hipError_t gemv_part_merge(hipStream_t st, const GemvArgs& a, const EpiPart& e) {
-    if (a.n_splits <= 2) return gemv_go<MR, 4, 1, KCH, 2>(st, a, 4, e);
-    if (a.n_splits <= 4) return gemv_go<MR, 4, 1, KCH, 4>(st, a, 4, e);
-    if constexpr (MR * KCH <= 16) return gemv_go<MR, 4, 1, KCH, 8>(st, a, 4, e);
+    constexpr int GS = (16 / (MR * KCH)) > 0 ? 16 / (MR * KCH) : 1;
+    if (a.n_splits <= 8) return gemv_go<MR, 4, 1, KCH, 8>(st, a, 4, e);
+    if constexpr (8 * GS >= 16) {
+        if (a.n_splits <= 16) return gemv_go<MR, 4, 1, KCH, 16>(st, a, 4, e);
+    }
+    if constexpr (8 * GS >= 32) {
+        if (a.n_splits <= 24) return gemv_go<MR, 4, 1, KCH, 24>(st, a, 4, e);
+        if (a.n_splits <= 32) return gemv_go<MR, 4, 1, KCH, 32>(st, a, 4, e);
+    }
     return hipErrorInvalidValue;
 }
 
 // Largest attention split count the out-projection can merge for M rows of
-// width d (register budget of the merge); 0 if none.
+// width d: each thread keeps at most 8 splits of one (row, float4) item, and
+// the workgroup's 1024 threads cover the items GS times over; 0 if none.
 int gemv_merge_max_splits(int M, int d) {
     if (M < 1 || M > 16 || d > 2048) return 0;
     int mr = 1;
     while (mr < M) mr <<= 1;
     const int kch = d > 1024 ? 2 : 1;
-    return mr * kch <= 16 ? 8 : 4;
+    const int gs = std::max(1, 16 / (mr * kch));
+    return std::min(32, 8 * gs);
 }
 
 hipError_t gemv(hipStream_t st, const GemvArgs& a) {

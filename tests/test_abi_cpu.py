@@ -116,3 +116,44 @@ def test_kv_pool_exhaustion_is_reported():
 def test_strerror():
     from paper_2410_13839_amd import binding as b
     assert b.mtp_strerror(b.MTP_ENOMEM).startswith("KV")
+
+
+def test_bf16_weight_fragment_order():
+    """The binding's packer follows the fragment order mtp.h documents for bf16
+    Linear weights: element (n, k) at ((n/16)(K/32) + k/32)*512 + ((k%32)/8)*128
+    + (n%16)*8 + k%8, rows padded with zeros to a multiple of 16."""
+    from paper_2410_13839_amd.binding import tile_bf16_matrix
+    rng = np.random.default_rng(5)
+    N, K = 37, 96
+    w = rng.integers(1, 65535, size=(N, K), dtype=np.uint16)
+    t = tile_bf16_matrix(w)
+    assert t.size == 48 * K
+    n, k = np.meshgrid(np.arange(N), np.arange(K), indexing="ij")
+    idx = ((n // 16) * (K // 32) + k // 32) * 512 + ((k % 32) // 8) * 128 + (n % 16) * 8 + k % 8
+    assert np.array_equal(t[idx], w)
+    mask = np.ones(t.size, bool)
+    mask[idx.reshape(-1)] = False
+    assert np.all(t[mask] == 0)
+
+
+def test_packed_weights_hold_every_tensor():
+    """pack_weights places each tensor of a bf16 model at its offset: row-major
+    tables and vectors as given, Linear weights in fragment order."""
+    from paper_2410_13839_amd import binding as b
+    from paper_2410_13839_amd.workloads import ModelShape, Workload, make_weights
+    shape = ModelShape(n_layers=1, d_model=256, n_heads=4, d_ff=512, k_heads=2, dtype="bf16", max_pos=64)
+    w = make_weights(shape, seed=3)
+    cfg = b.make_config(shape, 1, 16, 16, 16)
+    img = b.pack_weights(cfg, w)
+    u16 = lambda a: (np.ascontiguousarray(a, np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    off, n = b.mtp_weight_offset(cfg, b.MTP_T_EMB_AC, 0)
+    assert np.array_equal(img[off:off + 2 * n].view(np.uint16), u16(w["emb_ac"]).reshape(-1))
+    off, n = b.mtp_weight_offset(cfg, b.MTP_T_W_1, 0)
+    tiled = b.tile_bf16_matrix(u16(w["l0.w_1"]))
+    assert np.array_equal(img[off:off + 2 * tiled.size].view(np.uint16), tiled)
+    off, n = b.mtp_weight_offset(cfg, b.MTP_T_W_HEADS, 0)
+    tiled = b.tile_bf16_matrix(u16(w["w_heads"]).reshape(-1, 256))
+    assert tiled.size == (2 * 1025 + 15) // 16 * 16 * 256
+    assert np.array_equal(img[off:off + 2 * tiled.size].view(np.uint16), tiled)
+    off, n = b.mtp_weight_offset(cfg, b.MTP_T_B_1, 0)
+    assert np.array_equal(img[off:off + 4 * n].view(np.float32), w["l0.b_1"])
