@@ -20,7 +20,7 @@ namespace {
 constexpr int PER_LANE = 17;   // ceil(1025 / 64): logits held per lane
 
 __device__ __forceinline__ bool better(float va, int ia, float vb, int ib) {
-    return va > vb || (va == vb && ia < ib);
+    return (va > vb) | ((va == vb) & (ia < ib));
 }
 }  // namespace
 
@@ -177,7 +177,7 @@ __global__ __launch_bounds__(512) void select_fused_kernel(SelectArgs a) {
     const int K = a.K, k = a.top_k, V = a.V;
     __shared__ int s_cand[MTP_MAX_HEADS_K][MTP_MAX_TOPK];
     __shared__ float s_ehat[MTP_MAX_HEADS_K][MTP_MAX_TOPK];
-    __shared__ float s_T[MTP_MAX_HEADS_K - 1][MTP_MAX_TOPK][MTP_MAX_TOPK];
+    __shared__ float s_T[MTP_MAX_HEADS_K - 1][MTP_MAX_TOPK][MTP_MAX_TOPK];   // [t-1][j][i] (i contiguous)
     __shared__ int s_psi[MTP_MAX_HEADS_K][MTP_MAX_TOPK];
     __shared__ float s_delta[MTP_MAX_TOPK];
     const SeqState st0 = a.st[b];
@@ -198,107 +198,122 @@ __global__ __launch_bounds__(512) void select_fused_kernel(SelectArgs a) {
             if (lane + 64 * j == a.eos_id && mask_eos) v[j] = -INFINITY;
         uint32_t taken = 0;
         float top0 = 0.f;
+        int my_c = 0;
+        float my_e = 0.f;
         for (int r = 0; r < k; ++r) {
             float bv = -INFINITY;
             int bi = INT_MAX;
 #pragma unroll
             for (int j = 0; j < PER_LANE; ++j) {
                 const int idx = lane + 64 * j;
-                if (idx < V && !((taken >> j) & 1u) && better(v[j], idx, bv, bi)) {
-                    bv = v[j];
-                    bi = idx;
-                }
+                const bool ok = (idx < V) & (((taken >> j) & 1u) == 0u);
+                const bool bt = ok & better(v[j], idx, bv, bi);
+                bv = bt ? v[j] : bv;
+                bi = bt ? idx : bi;
             }
-            wave_argmax(bv, bi);
-            if ((bi & 63) == lane) taken |= 1u << (bi >> 6);
+            wave_argmax_uniform(bv, bi);
+            taken |= ((bi & 63) == lane) ? (1u << (bi >> 6)) : 0u;
             if (r == 0) top0 = bv;
-            if (lane == 0) {
-                const float e = bv - top0;
-                s_cand[t][r] = bi;
-                s_ehat[t][r] = e;
-                a.cand[base + t * k + r] = bi;
-                a.ehat[base + t * k + r] = e;
-            }
+            const float e = bv - top0;
+            my_c = (lane == r) ? bi : my_c;
+            my_e = (lane == r) ? e : my_e;
+        }
+        if (lane < k) {
+            s_cand[t][lane] = my_c;
+            s_ehat[t][lane] = my_e;
+            a.cand[base + t * k + lane] = my_c;
+            a.ehat[base + t * k + lane] = my_e;
         }
     }
     __syncthreads();
-    // transition sub-tables T[t-1][i][j] = logQ[c_{t-1,i}][c_{t,j}]
+    // transition sub-tables T[t-1][j][i] = logQ[c_{t-1,i}][c_{t,j}] (stored
+    // with i contiguous: the recursion reads one row per slot j)
     const int kk = k * k;
     for (int idx = tid; idx < (K - 1) * kk; idx += blockDim.x) {
         const int t1 = idx / kk, rem = idx - t1 * kk;
         const int i = rem / k, j = rem - i * k;
-        s_T[t1][i][j] = a.logq[(size_t)s_cand[t1][i] * V + s_cand[t1 + 1][j]];
+        s_T[t1][j][i] = a.logq[(size_t)s_cand[t1][i] * V + s_cand[t1 + 1][j]];
     }
     __syncthreads();
     if (t != 0) return;
 
+    // Viterbi on wave 0: lane j holds slot j's score; the scores of the other
+    // slots come from v_readlane with the (uniform) loop index, so a step is k
+    // adds and compares in registers plus one LDS row of transitions.
     const int j = lane;
-    float delta = (j < k) ? s_ehat[0][j] : -INFINITY;
+    const int jc = j < k ? j : 0;
+    float delta = (j < k) ? s_ehat[0][jc] : -INFINITY;
     if (j < k) {
         a.delta[base + j] = delta;
         a.psi[base + j] = 0;
     }
     for (int tt = 1; tt < K; ++tt) {
+        const float* Trow = &s_T[tt - 1][jc][0];
         float best = 0.f;
         int arg = 0;
-        if (j < MTP_MAX_TOPK) s_delta[j] = delta;
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-        __builtin_amdgcn_wave_barrier();
         for (int i = 0; i < k; ++i) {
-            const float di = s_delta[i];
-            const float s = di + s_T[tt - 1][i][j < k ? j : 0];
-            if (i == 0 || s > best) {
-                best = s;
+            const float di = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(delta), i));
+            const float sc = di + Trow[i];
+            if (i == 0 || sc > best) {
+                best = sc;
                 arg = i;
             }
         }
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-        __builtin_amdgcn_wave_barrier();
-        delta = (j < k) ? best + s_ehat[tt][j] : -INFINITY;
+        delta = (j < k) ? best + s_ehat[tt][jc] : -INFINITY;
         if (j < k) {
+            s_psi[tt][j] = arg;
             a.delta[base + tt * k + j] = delta;
             a.psi[base + tt * k + j] = arg;
-            s_psi[tt][j] = arg;
         }
     }
     float bestd = (j < k) ? delta : -INFINITY;
     int last = (j < k) ? j : MTP_MAX_TOPK + j;
-    wave_argmax(bestd, last);
+    wave_argmax_uniform(bestd, last);
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
     __builtin_amdgcn_wave_barrier();
-    if (j != 0) return;
 
-    int slots[MTP_MAX_HEADS_K], toks[MTP_MAX_HEADS_K];
-    slots[K - 1] = last;
-    for (int tt = K - 1; tt > 0; --tt) slots[tt - 1] = s_psi[tt][slots[tt]];
-    for (int tt = 0; tt < K; ++tt) {
-        toks[tt] = s_cand[tt][slots[tt]];
-        a.slots[(size_t)b * K + tt] = slots[tt];
-    }
-    SeqState s = st0;
-    int n = 0;
-    bool done = s.done != 0;
-    if (!done) {
-        n = min(K, a.max_new - s.gen);
-        for (int p = 0; p < n; ++p) {
-            if (toks[p] == a.eos_id) {
-                n = p + 1;
-                done = true;
-                break;
-            }
+    // backtrack with uniform slot indices (slot_{t-1} = psi_t(slot_t));
+    // lane t keeps position t
+    int my_slot = 0, my_tok = 0;
+    int cur = last;
+    for (int tt = K - 1; tt >= 0; --tt) {
+        const int tok = s_cand[tt][cur];
+        if (lane == tt) {
+            my_slot = cur;
+            my_tok = tok;
         }
-        if (s.gen + n >= a.max_new) done = true;
+        if (tt > 0) cur = s_psi[tt][cur];
     }
-    for (int tt = 0; tt < K; ++tt) a.out_tokens[(size_t)b * K + tt] = (tt < n) ? toks[tt] : -1;
-    a.out_count[b] = n;
-    for (int tt = 0; tt < n; ++tt) a.hist[(size_t)b * a.hist_ld + s.gen + tt] = toks[tt];
-    s.ctx_len += s.pend_len;
-    s.gen += n;
-    s.done = done ? 1 : 0;
-    s.pend_len = done ? 0 : n;
-    for (int tt = 0; tt < n && tt < MTP_MAX_HEADS_K; ++tt) s.pend_ids[tt] = toks[tt];
-    s.steps += 1;
-    a.st[b] = s;
+    // accept: the first min(K, budget) tokens, cut after the first EOS
+    const SeqState s0 = st0;
+    int n = 0;
+    bool done = s0.done != 0;
+    if (!done) {
+        n = min(K, a.max_new - s0.gen);
+        const uint64_t eos_lanes = __ballot(lane < n && my_tok == a.eos_id);
+        if (eos_lanes) {
+            n = __builtin_ctzll(eos_lanes) + 1;
+            done = true;
+        }
+        if (s0.gen + n >= a.max_new) done = true;
+    }
+    if (lane < K) {
+        a.slots[(size_t)b * K + lane] = my_slot;
+        a.out_tokens[(size_t)b * K + lane] = (lane < n) ? my_tok : -1;
+    }
+    if (lane < n) {
+        a.hist[(size_t)b * a.hist_ld + s0.gen + lane] = my_tok;
+        a.st[b].pend_ids[lane] = my_tok;
+    }
+    if (lane == 0) {
+        a.out_count[b] = n;
+        SeqState* sp = a.st + b;
+        sp->ctx_len = s0.ctx_len + s0.pend_len;
+        sp->gen = s0.gen + n;
+        sp->done = done ? 1 : 0;
+        sp->pend_len = done ? 0 : n;
+        sp->steps = s0.steps + 1;
+    }
 }
 
 hipError_t select_fused(hipStream_t st, const SelectArgs& a) {

@@ -66,20 +66,27 @@ __device__ __forceinline__ float sum_stride8(float v) {
 
 // (value, index) maximum over the wave under the total order "larger value,
 // then smaller index"; every lane ends with the winner.
+// (value, index) order: larger value first, lower index on ties.  Written
+// with bitwise ops and selects so that no step becomes a branch.
 __device__ __forceinline__ bool vi_better(float va, int ia, float vb, int ib) {
-    return va > vb || (va == vb && ia < ib);
+    return (va > vb) | ((va == vb) & (ia < ib));
 }
 template <int CTRL>
 __device__ __forceinline__ void vi_step_dpp(float& v, int& i) {
     const float ov = dpp_f<CTRL>(v);
     const int oi = dpp_i<CTRL>(i);
-    if (vi_better(ov, oi, v, i)) { v = ov; i = oi; }
+    const bool b = vi_better(ov, oi, v, i);
+    v = b ? ov : v;
+    i = b ? oi : i;
 }
 __device__ __forceinline__ void vi_step_shfl(float& v, int& i, int mask) {
     const float ov = __shfl_xor(v, mask);
     const int oi = __shfl_xor(i, mask);
-    if (vi_better(ov, oi, v, i)) { v = ov; i = oi; }
+    const bool b = vi_better(ov, oi, v, i);
+    v = b ? ov : v;
+    i = b ? oi : i;
 }
+// Every lane ends with the wave's best (value, index).
 __device__ __forceinline__ void wave_argmax(float& v, int& i) {
     vi_step_dpp<DPP_XOR1>(v, i);
     vi_step_dpp<DPP_XOR2>(v, i);
@@ -87,6 +94,28 @@ __device__ __forceinline__ void wave_argmax(float& v, int& i) {
     vi_step_dpp<DPP_ROR8>(v, i);
     vi_step_shfl(v, i, 16);
     vi_step_shfl(v, i, 32);
+}
+
+// The wave's best (value, index) as uniform values, crossing rows with DPP
+// row broadcasts (lane 15 -> rows 1 and 3, lane 31 -> rows 2 and 3) so that
+// lane 63 ends with the result; no LDS permute on the way.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ void vi_step_bcast(float& v, int& i) {
+    const float ov = __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(v), __float_as_int(v), CTRL, ROWS, 0xF, false));
+    const int oi = __builtin_amdgcn_update_dpp(i, i, CTRL, ROWS, 0xF, false);
+    const bool b = vi_better(ov, oi, v, i);
+    v = b ? ov : v;
+    i = b ? oi : i;
+}
+__device__ __forceinline__ void wave_argmax_uniform(float& v, int& i) {
+    vi_step_dpp<DPP_XOR1>(v, i);
+    vi_step_dpp<DPP_XOR2>(v, i);
+    vi_step_dpp<DPP_HALF_MIRROR>(v, i);
+    vi_step_dpp<DPP_ROR8>(v, i);
+    vi_step_bcast<0x142, 0xA>(v, i);   // row_bcast:15 into rows 1, 3
+    vi_step_bcast<0x143, 0xC>(v, i);   // row_bcast:31 into rows 2, 3
+    v = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+    i = __builtin_amdgcn_readlane(i, 63);
 }
 
 }  // namespace mtp
