@@ -62,7 +62,7 @@ struct EpiQKVDec {
         Pre p;
 #pragma unroll
         for (int i = 0; i < 4; ++i) p.b[i] = bias[n + i];
-        const SeqState& s = st[m / Q];
+        const SeqState& s = st[udiv_small(m, Q)];
         p.ctx = s.ctx_len;
         p.pl = s.pend_len;
         return p;
@@ -73,7 +73,7 @@ struct EpiQKVDec {
             *reinterpret_cast<float4*>(q + (size_t)m * d + n) = make_float4(r0, r1, r2, r3);
             return;
         }
-        const int seq = m / Q, i = m - seq * Q;
+        const int seq = udiv_small(m, Q), i = m - seq * Q;
         if (i >= p.pl) return;
         const int pos = p.ctx + i;
         const int c = (n < 2 * d) ? n - d : n - 2 * d;
@@ -213,7 +213,7 @@ __global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
     // LayerNorm-mode mapping; rg is uniform over a wave (K/4 is a multiple of 64)
     const int K4 = K >> 2;
     const int RG = T / K4;                        // row groups (>= 1 for K <= 2048)
-    const int rg = __builtin_amdgcn_readfirstlane(tid / K4);
+    const int rg = __builtin_amdgcn_readfirstlane(wave) / (K4 >> 6);   // scalar division
     const int cc = min((tid - rg * K4) * 4, K - 4);
     (void)RG; (void)rg; (void)cc; (void)K4;
 
@@ -242,7 +242,7 @@ __global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
 #pragma unroll
         for (int i = 0; i < XI; ++i) {
             const int idx = min(tid + T * i, total - 1);
-            const int m = idx / cpr, c = (idx - m * cpr) * 8;
+            const int m = udiv_small(idx, cpr), c = (idx - m * cpr) * 8;
             const uint4 t = *reinterpret_cast<const uint4*>(a.x + (size_t)m * a.ldx + kb + c);
             xq[4 * i] = t.x;
             xq[4 * i + 1] = t.y;
@@ -256,28 +256,29 @@ __global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
         // context are discarded once its state is known
         const int cpr = ks >> 2, items = M * cpr, HW = ks >> 6, h0 = kb >> 6;
         const int H = K >> 6, S = a.n_splits;
-        const size_t sstride = (size_t)a.qt * 68;
+        const uint32_t sstride = (uint32_t)a.qt * 68;   // offsets fit 32 bits (< B*H*S*qt*68)
         const int nml = M * HW * S;
 #pragma unroll
         for (int p = 0; p < MLP; ++p) {
             const int idx = min(tid + T * p, nml - 1);
-            const int m = idx / (HW * S), rem = idx - m * (HW * S);
-            const int hd = rem / S, sp = rem - hd * S;
-            const int seq = m / a.Q, i = m - seq * a.Q;
-            mlv[p] = *reinterpret_cast<const float2*>(a.apart + ((size_t)(seq * H + h0 + hd) * S + sp) * sstride + (size_t)i * 68);
+            const int m = udiv_small(idx, HW * S), rem = idx - m * (HW * S);
+            const int hd = udiv_small(rem, S), sp = rem - hd * S;
+            const int seq = udiv_small(m, a.Q), i = m - seq * a.Q;
+            const uint32_t off = ((uint32_t)(seq * H + h0 + hd) * S + sp) * sstride + (uint32_t)i * 68;
+            mlv[p] = *reinterpret_cast<const float2*>(a.apart + off);
         }
-        const int TG = T / GS, sg = __builtin_amdgcn_readfirstlane(tid / TG);
+        const int TG = T / GS, sg = __builtin_amdgcn_readfirstlane(wave) / (TG >> 6);
         const int it = min(tid - sg * TG, items - 1);
-        const int m = it / cpr, c = kb + (it - m * cpr) * 4;
-        const int seq = m / a.Q, i = m - seq * a.Q;
+        const int m = udiv_small(it, cpr), c = kb + (it - m * cpr) * 4;
+        const int seq = udiv_small(m, a.Q), i = m - seq * a.Q;
         sti = *reinterpret_cast<const int2*>(&a.st[seq]);
-        const float* e0 = a.apart + (size_t)(seq * H + (c >> 6)) * S * sstride + (size_t)i * 68 + 4 + (c & 63);
+        const float* e0 = a.apart + ((uint32_t)(seq * H + (c >> 6)) * S * sstride + (uint32_t)i * 68 + 4 + (c & 63));
         // sg is uniform over a wave (groups are 256 threads or more) and S is
         // a kernel argument: skipping the splits that were not launched costs
         // no wait
 #pragma unroll
         for (int j = 0; j < SPT; ++j)
-            if (sg + GS * j < S) ov[j] = *reinterpret_cast<const float4*>(e0 + (size_t)(sg + GS * j) * sstride);
+            if (sg + GS * j < S) ov[j] = *reinterpret_cast<const float4*>(e0 + (uint32_t)(sg + GS * j) * sstride);
     } else {
         // LayerNorm gain and shift: loaded by row group 0 only, shared through LDS
         if (rg == 0) {
@@ -340,7 +341,7 @@ __global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
         for (int i = 0; i < XI; ++i) {
             const int idx = tid + T * i;
             if (idx < total) {
-                const int m = idx / cpr, c = (idx - m * cpr) * 8;
+                const int m = udiv_small(idx, cpr), c = (idx - m * cpr) * 8;
                 *reinterpret_cast<uint4*>(xs + (size_t)m * ldl + c) =
                     make_uint4(xq[4 * i], xq[4 * i + 1], xq[4 * i + 2], xq[4 * i + 3]);
             }
@@ -355,12 +356,12 @@ __global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
             if (idx < nml) s_ml[idx] = mlv[p];
         }
         __syncthreads();
-        const int TG = T / GS, sg = tid / TG, it = tid - sg * TG;
-        const int m = min(it, items - 1) / cpr;
+        const int TG = T / GS, sg = __builtin_amdgcn_readfirstlane(wave) / (TG >> 6), it = tid - sg * TG;
+        const int m = udiv_small(min(it, items - 1), cpr);
         const int c = kb + (min(it, items - 1) - m * cpr) * 4;
-        const int i = m - (m / a.Q) * a.Q;
+        const int i = m - udiv_small(m, a.Q) * a.Q;
         const int ctx = sti.x, pl = sti.y;
-        const int n_active = min(S, (ctx + pl + a.split_len - 1) / a.split_len);
+        const int n_active = min(S, udiv_small(ctx + pl + a.split_len - 1, a.split_len));
         const float2* ml = s_ml + (m * HW + ((c - kb) >> 6)) * S;
         // splits past the context (or a key range fully masked for this row)
         // contribute nothing; their words may be stale
