@@ -113,17 +113,21 @@ def launch_bytes(wl, kclass, ctx):
     raise ValueError(kclass)
 
 
-def kernel_source_digest():
-    """Digest of the HIP sources: PMC traffic figures are valid only for the
-    kernels they were taken on."""
-    import glob
+KCLASS_SOURCES = {  # kernel class -> the sources its kernels are built from
+    4: ("attn_mfma.hip", "common.h", "launch.h"),
+}
+GEMV_SOURCES = ("gemv.hip", "common.h", "launch.h", "wave.h")
+
+
+def kernel_source_digest(kclass):
+    """Digest of the HIP sources of one kernel class: PMC traffic figures are
+    valid only for the kernels they were taken on."""
     import hashlib
     h = hashlib.sha256()
-    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2410_13839_amd", "csrc", "*"))):
-        if f.endswith((".hip", ".h")):
-            h.update(os.path.basename(f).encode())
-            with open(f, "rb") as fh:
-                h.update(fh.read())
+    for name in KCLASS_SOURCES.get(kclass, GEMV_SOURCES):
+        h.update(name.encode())
+        with open(os.path.join(ROOT, "paper_2410_13839_amd", "csrc", name), "rb") as fh:
+            h.update(fh.read())
     return h.hexdigest()[:16]
 
 
@@ -135,7 +139,7 @@ def pmc_traffic(workload, kclass):
     path = os.path.join(ROOT, "profiles", f"traffic_{workload}.md")
     if not os.path.exists(path):
         return None
-    digest = kernel_source_digest()
+    digest = kernel_source_digest(kclass)
     with open(path) as fh:
         for line in fh:
             if not line.startswith("pmc:"):

@@ -200,6 +200,8 @@ int mtp_get_tokens(mtp_ctx* ctx, int32_t* tokens);
  * preceded (outside the events) by a read of a 512 MiB buffer that evicts the
  * weights from the L2 and last-level caches, as in a real step where the
  * other layers' weights pass through them between two launches of a class.
+ * A pass repeats the recorded launches until it holds at least 12 (the
+ * heads' single launch is replayed 12 times, the later ones cache-warm).
  * Returns the average time per launch in microseconds (synchronises; one
  * launch latency per pass is included).  The replayed launches keep their
  * arguments and may overwrite the residual stream and the cache rows of the
