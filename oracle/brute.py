@@ -11,7 +11,7 @@ sign or dropped term in the recursion shows up as a different argmax.
 from __future__ import annotations
 
 import itertools
-from typing import List, Tuple
+from typing import List, Optional, Tuple
 
 import numpy as np
 
@@ -21,14 +21,18 @@ def all_paths(K: int, k: int) -> np.ndarray:
     return np.array(list(itertools.product(range(k), repeat=K)), dtype=np.int64).reshape(-1, K)
 
 
-def path_scores_log(cand: np.ndarray, ehat: np.ndarray, logq: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
-    """Log-domain score sum_t e_t(s_t) + sum_{t>=1} logQ(c_{t-1,s_{t-1}}, c_{t,s_t}) (float64)."""
+def path_scores_log(cand: np.ndarray, ehat: np.ndarray, logq: np.ndarray,
+                    anchor: Optional[int] = None) -> Tuple[np.ndarray, np.ndarray]:
+    """Log-domain score sum_t e_t(s_t) + sum_{t>=1} logQ(c_{t-1,s_{t-1}}, c_{t,s_t})
+    (+ logQ(anchor, c_{0,s_0}) for an anchored first position), float64."""
     cand = np.asarray(cand)
     K, k = cand.shape
     P = all_paths(K, k)
     e = np.asarray(ehat, dtype=np.float64)
     lq = np.asarray(logq, dtype=np.float64)
     score = np.zeros(P.shape[0])
+    if anchor is not None:
+        score += lq[anchor, cand[0, P[:, 0]]]
     for t in range(K):
         score += e[t, P[:, t]]
         if t > 0:

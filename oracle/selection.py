@@ -31,7 +31,7 @@ floats), the precision the GPU kernels take them in.
 from __future__ import annotations
 
 from dataclasses import dataclass
-from typing import Tuple
+from typing import Optional, Tuple
 
 import numpy as np
 
@@ -74,10 +74,11 @@ class Lattice:
     tokens: np.ndarray  # int32 [K]     chosen token per position
 
 
-def viterbi(cand: np.ndarray, ehat: np.ndarray, logq: np.ndarray) -> Lattice:
+def viterbi(cand: np.ndarray, ehat: np.ndarray, logq: np.ndarray, anchor: Optional[int] = None) -> Lattice:
     """Max-product Viterbi over K positions x k candidate slots (log domain).
 
-    delta_0(j) = e_0(j);
+    delta_0(j) = e_0(j), or logQ(anchor, c_{0,j}) + e_0(j) when the first
+    position is anchored to the previously emitted token `anchor`;
     delta_t(j) = max_i [delta_{t-1}(i) + logQ(c_{t-1,i}, c_{t,j})] + e_t(j),
     psi_t(j) = the maximising i (lowest on ties); the path ends in the lowest
     slot of maximal delta_{K-1} and is read back through psi.
@@ -89,7 +90,7 @@ def viterbi(cand: np.ndarray, ehat: np.ndarray, logq: np.ndarray) -> Lattice:
     delta = np.zeros((K, k), dtype=np.float32)
     psi = np.zeros((K, k), dtype=np.int32)
     for j in range(k):
-        delta[0, j] = ehat[0, j]
+        delta[0, j] = ehat[0, j] if anchor is None else F32(logq[anchor, cand[0, j]] + ehat[0, j])
     for t in range(1, K):
         for j in range(k):
             best = None
@@ -112,17 +113,52 @@ def viterbi(cand: np.ndarray, ehat: np.ndarray, logq: np.ndarray) -> Lattice:
     return Lattice(cand, ehat, delta, psi, slots, tokens)
 
 
-def select(logits: np.ndarray, logq: np.ndarray, k: int, gen: int, eos_min: int, eos_id: int) -> Lattice:
-    """One step's selection from the float32 logits of K heads ([K, V])."""
+def union_states(logits: np.ndarray, k: int, gen: int, eos_min: int, eos_id: int) -> np.ndarray:
+    """The m <= K*k distinct tokens among the K heads' top_k (EOS-masked per
+    head), in ascending token id: the reduced state space of Sec. 3.3, whose
+    transition table is the m x m sub-table of Q."""
+    logits = np.asarray(logits, dtype=np.float32)
+    ids = [top_k(mask_eos(logits[t], gen + t, eos_min, eos_id), k)[0] for t in range(logits.shape[0])]
+    return np.unique(np.concatenate(ids)).astype(np.int32)
+
+
+def union_inputs(logits: np.ndarray, k: int, gen: int, eos_min: int, eos_id: int) -> Tuple[np.ndarray, np.ndarray]:
+    """(cand, ehat) of the union lattice: every position has the same m states
+    (union_states), and position t scores state c with head t's own
+    distribution, e_t(c) = l_t[c] - max l_t (float32; -inf for a masked EOS)."""
     logits = np.asarray(logits, dtype=np.float32)
     K = logits.shape[0]
+    U = union_states(logits, k, gen, eos_min, eos_id)
+    cand = np.tile(U, (K, 1))
+    ehat = np.zeros((K, U.size), dtype=np.float32)
+    for t in range(K):
+        lt = mask_eos(logits[t], gen + t, eos_min, eos_id)
+        top = np.max(lt)
+        ehat[t] = np.array([F32(lt[c] - top) for c in U], dtype=np.float32)
+    return cand, ehat
+
+
+def select(logits: np.ndarray, logq: np.ndarray, k: int, gen: int, eos_min: int, eos_id: int,
+           lattice: str = "own", anchor: Optional[int] = None) -> Lattice:
+    """One step's selection from the float32 logits of K heads ([K, V]).
+
+    lattice="own": position t's states are head t's top_k (ordered by logit);
+    lattice="union": every position's states are the union of all heads'
+    top_k (ascending id), scored by head t at position t.  `anchor` (the last
+    emitted token, or None) adds its transition into the first position.
+    """
+    logits = np.asarray(logits, dtype=np.float32)
+    K = logits.shape[0]
+    if lattice == "union":
+        cand, ehat = union_inputs(logits, k, gen, eos_min, eos_id)
+        return viterbi(cand, ehat, logq, anchor)
     cand = np.zeros((K, k), dtype=np.int32)
     ehat = np.zeros((K, k), dtype=np.float32)
     for t in range(K):
         ids, vals = top_k(mask_eos(logits[t], gen + t, eos_min, eos_id), k)
         cand[t] = ids
         ehat[t] = emission(vals)
-    return viterbi(cand, ehat, logq)
+    return viterbi(cand, ehat, logq, anchor)
 
 
 def accept(tokens: np.ndarray, gen: int, max_new: int, eos_id: int) -> Tuple[int, bool]:
