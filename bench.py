@@ -39,6 +39,7 @@ def _parse():
     ap.add_argument("--copy-probe", action="store_true", help="also run a 256 MiB device copy (PMC calibration)")
     ap.add_argument("--replay-passes", type=int, default=20, help="passes of the per-class replay timing")
     ap.add_argument("--no-warm-replay", action="store_true", help="skip the cache-warm replay figures")
+    ap.add_argument("--no-variants", action="store_true", help="skip the selection-variant figures")
     return ap.parse_args()
 
 
@@ -46,9 +47,10 @@ def _steps_per_generation(wl):
     return -(-wl.max_new // wl.K)
 
 
-def time_decode(sess, wl, prompts, steps, warmup, torch):
+def time_decode(sess, wl, prompts, steps, warmup, torch, top_k=None):
     """Warm up, then time exactly `steps` decode steps (prefills in between
     generations are outside the timed intervals).  Returns (ms, tokens)."""
+    top_k = wl.top_k if top_k is None else top_k
     per_gen = _steps_per_generation(wl)
     st = sess.stream
     # warmup (also instantiates the hipGraphs of the step)
@@ -56,7 +58,7 @@ def time_decode(sess, wl, prompts, steps, warmup, torch):
     for i in range(warmup):
         if i and i % per_gen == 0:
             sess.prefill(prompts.phon, prompts.ac)
-        sess.step_async(wl.K, wl.top_k)
+        sess.step_async(wl.K, top_k)
     torch.cuda.synchronize()
     total_ms, tokens, done = 0.0, 0, 0
     while done < steps:
@@ -67,7 +69,7 @@ def time_decode(sess, wl, prompts, steps, warmup, torch):
         e1 = torch.cuda.Event(enable_timing=True)
         e0.record(st)
         for _ in range(n):
-            sess.step_async(wl.K, wl.top_k)
+            sess.step_async(wl.K, top_k)
         e1.record(st)
         torch.cuda.synchronize()
         total_ms += e0.elapsed_time(e1)
@@ -251,6 +253,30 @@ def main():
             "measured": f"{passes} passes over the {KCLASSES[dom][1](L)} launches of one step at step {mid} "
                         f"(context {ctx} tokens), caches evicted before each pass, HIP events on the library stream"}
     print(f"[bench] dominant kernel {dname}: {dk}", file=sys.stderr, flush=True)
+
+    # selection variants (Sec. 3.3): throughput of the whole step and the
+    # selection kernel's own launch time (cold passes at step `mid`)
+    from paper_2410_13839_amd.binding import MTP_KCLASS_SELECT, mtp_profile_replay
+    variants = []
+    if not args.no_variants:
+        for lat, anch, tk, what in ((0, False, wl.top_k, "each head's own top_k (default)"),
+                                    (1, False, wl.top_k, "union of all heads' top_k, m x m transitions"),
+                                    (0, True, wl.top_k, "own top_k, first position anchored"),
+                                    (1, True, wl.top_k, "union, first position anchored"),
+                                    (0, False, 1, "top_k = 1: per-head argmax, no Viterbi")):
+            sess.set_selection(lat, anch)
+            vms, vtok = time_decode(sess, wl, prompts, _steps_per_generation(wl), 5, torch, top_k=tk)
+            sess.prefill(prompts.phon, prompts.ac)
+            for _ in range(mid):
+                sess.step_async(wl.K, tk)
+            torch.cuda.synchronize()
+            sel_us = mtp_profile_replay(sess.ctx, MTP_KCLASS_SELECT, passes, True)
+            v = {"lattice": "union" if lat else "own", "anchored": anch, "top_k": tk, "selection": what,
+                 "tokens_per_s": round(vtok / (vms / 1000.0), 1), "us_per_step": round(vms * 1000.0 / _steps_per_generation(wl), 2),
+                 "select_kernel_us": round(sel_us, 3)}
+            variants.append(v)
+            print(f"[bench] variant {v}", file=sys.stderr, flush=True)
+        sess.set_selection(0, False)
     sess.close()
     del sess
     torch.cuda.empty_cache()
@@ -294,6 +320,7 @@ def main():
         "roofline": roof,
         "kernels": kernels,
         "cpu_baseline": cpu,
+        "selection_variants": variants,
         "secondary": secondary,
         "paper_context": "paper reports 20.5 -> 4.5 ms/token (x4.56, VALL-E, 8 heads) on unstated inference hardware",
     }

@@ -183,6 +183,29 @@ int mtp_get_logits(mtp_ctx* ctx, float* logits);
 int mtp_get_lattice(mtp_ctx* ctx, int32_t* cand, float* ehat, float* delta,
                     int32_t* psi, int32_t* slots);
 
+/* Selection options for the following decode steps (paper Sec. 3.3, Fig. 2).
+ * lattice MTP_LATTICE_OWN (default): position t's states are head t's own
+ * top_k.  MTP_LATTICE_UNION: every position's states are the m <= K*top_k
+ * distinct tokens of all heads' top_k in ascending id, scored at position t
+ * by head t (e_t(c) = l_t[c] - max l_t, -inf for a masked EOS), with the
+ * m x m sub-table of log Q (the paper's reduced transition matrix); steps
+ * then need K * top_k <= 64 (MTP_EINVAL otherwise).  anchored = 1 adds
+ * logQ[last emitted token][c] to the first position's scores (the acoustic
+ * prompt's last token before any token was emitted; no term when there is
+ * none).  Ties keep the lowest state index in both lattices.  MTP_EINVAL for
+ * other values. */
+#define MTP_LATTICE_OWN    0
+#define MTP_LATTICE_UNION  1
+int mtp_set_selection(mtp_ctx* ctx, int lattice, int anchored);
+
+/* The last step's union lattice (it must have used MTP_LATTICE_UNION, else
+ * MTP_ESTATE), to host (synchronises): m int32 [B] state counts; states
+ * int32 [B][64] (ascending ids, the first m valid); ehat, delta float32 and
+ * psi int32 [B][8][64] (position t, state j; psi[.][0][.] = 0); slots int32
+ * [B][K] chosen state index per position.  Any pointer may be NULL. */
+int mtp_get_union_lattice(mtp_ctx* ctx, int32_t* m, int32_t* states, float* ehat,
+                          float* delta, int32_t* psi, int32_t* slots);
+
 /* Per-sequence state to host (synchronises): cached tokens, pending chunk
  * length, generated count and done flag, each int32 [B]; any may be NULL. */
 int mtp_get_seq_state(mtp_ctx* ctx, int32_t* ctx_len, int32_t* pend_len,
@@ -215,6 +238,7 @@ int mtp_get_tokens(mtp_ctx* ctx, int32_t* tokens);
 #define MTP_KCLASS_ATTENTION   4   /* decode attention over the paged cache   */
 #define MTP_KCLASS_HEADS       5   /* final LN -> K head projections          */
 #define MTP_KCLASS_GEMM_OPROJ  6   /* attention out x W_o^T (residual part.)  */
+#define MTP_KCLASS_SELECT      7   /* top_k, Viterbi lattice and accept       */
 int mtp_profile_replay(mtp_ctx* ctx, int kclass, int iters, int cold, double* avg_us);
 
 /* Drops all sequence state (the next call must be mtp_prefill). */

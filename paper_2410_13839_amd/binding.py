@@ -28,11 +28,13 @@ MTP_FLAG_NO_GRAPH = 1
  MTP_T_B_O, MTP_T_LN2_G, MTP_T_LN2_B, MTP_T_W_1, MTP_T_B_1, MTP_T_W_2, MTP_T_B_2, MTP_T_LNF_G, MTP_T_LNF_B,
  MTP_T_W_HEADS, MTP_T_B_HEADS, MTP_T_COUNT) = range(20)
 (MTP_KCLASS_GEMM_FFN1, MTP_KCLASS_GEMM_FFN2, MTP_KCLASS_GEMM_QKV, MTP_KCLASS_ATTENTION, MTP_KCLASS_HEADS,
- MTP_KCLASS_GEMM_OPROJ) = 1, 2, 3, 4, 5, 6
+ MTP_KCLASS_GEMM_OPROJ, MTP_KCLASS_SELECT) = 1, 2, 3, 4, 5, 6, 7
 
 EXPORTED = ["mtp_query_sizes", "mtp_weight_offset", "mtp_create", "mtp_prefill", "mtp_decode_step",
             "mtp_decode_step_async", "mtp_get_logits", "mtp_get_lattice", "mtp_get_seq_state", "mtp_get_tokens",
-            "mtp_profile_replay", "mtp_reset", "mtp_destroy", "mtp_last_error", "mtp_strerror"]
+            "mtp_profile_replay", "mtp_reset", "mtp_destroy", "mtp_last_error", "mtp_strerror",
+            "mtp_set_selection", "mtp_get_union_lattice"]
+MTP_LATTICE_OWN, MTP_LATTICE_UNION = 0, 1
 
 
 class mtp_config(ctypes.Structure):
@@ -64,6 +66,8 @@ _lib.mtp_decode_step.argtypes = [_ctx, ctypes.c_int, ctypes.c_int, _i32p, _i32p]
 _lib.mtp_decode_step_async.argtypes = [_ctx, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
 _lib.mtp_get_logits.argtypes = [_ctx, _f32p]
 _lib.mtp_get_lattice.argtypes = [_ctx, _i32p, _f32p, _f32p, _i32p, _i32p]
+_lib.mtp_set_selection.argtypes = [_ctx, ctypes.c_int, ctypes.c_int]
+_lib.mtp_get_union_lattice.argtypes = [_ctx, _i32p, _i32p, _f32p, _f32p, _i32p, _i32p]
 _lib.mtp_get_seq_state.argtypes = [_ctx, _i32p, _i32p, _i32p, _i32p]
 _lib.mtp_get_tokens.argtypes = [_ctx, _i32p]
 _lib.mtp_profile_replay.argtypes = [_ctx, ctypes.c_int, ctypes.c_int, ctypes.c_int, _P(ctypes.c_double)]
@@ -140,6 +144,24 @@ def mtp_get_logits(ctx, B: int, K: int, V: int) -> np.ndarray:
     out = np.zeros((B, K, V), np.float32)
     _check(_lib.mtp_get_logits(ctx, out.ctypes.data_as(_f32p)), ctx, "mtp_get_logits")
     return out
+
+
+def mtp_set_selection(ctx, lattice: int, anchored: bool) -> None:
+    _check(_lib.mtp_set_selection(ctx, lattice, int(anchored)), ctx, "mtp_set_selection")
+
+
+def mtp_get_union_lattice(ctx, B: int, K: int) -> Dict[str, np.ndarray]:
+    m = np.zeros(B, np.int32)
+    states = np.zeros((B, 64), np.int32)
+    ehat = np.zeros((B, 8, 64), np.float32)
+    delta = np.zeros((B, 8, 64), np.float32)
+    psi = np.zeros((B, 8, 64), np.int32)
+    slots = np.zeros((B, K), np.int32)
+    _check(_lib.mtp_get_union_lattice(ctx, m.ctypes.data_as(_i32p), states.ctypes.data_as(_i32p),
+                                      ehat.ctypes.data_as(_f32p), delta.ctypes.data_as(_f32p),
+                                      psi.ctypes.data_as(_i32p), slots.ctypes.data_as(_i32p)),
+           ctx, "mtp_get_union_lattice")
+    return {"m": m, "states": states, "ehat": ehat[:, :K], "delta": delta[:, :K], "psi": psi[:, :K], "slots": slots}
 
 
 def mtp_get_lattice(ctx, B: int, K: int, top_k: int) -> Dict[str, np.ndarray]:
@@ -286,6 +308,12 @@ class Session:
 
     def lattice(self, K: int, top_k: int) -> Dict[str, np.ndarray]:
         return mtp_get_lattice(self.ctx, self.B, K, top_k)
+
+    def set_selection(self, lattice: int = MTP_LATTICE_OWN, anchored: bool = False) -> None:
+        mtp_set_selection(self.ctx, lattice, anchored)
+
+    def union_lattice(self, K: int) -> Dict[str, np.ndarray]:
+        return mtp_get_union_lattice(self.ctx, self.B, K)
 
     def seq_state(self) -> Dict[str, np.ndarray]:
         return mtp_get_seq_state(self.ctx, self.B)

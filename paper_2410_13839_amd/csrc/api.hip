@@ -116,6 +116,7 @@ int validate(const mtp_config* c, std::string* why) {
 
 struct WsLayout {
     uint64_t rows, ids, tiles, last_row, state, btab, h, q, u, attn, ffn, part, apart, hz, z, logits, cand, ehat,
+        u_states, u_m, u_ehat, u_delta, u_psi,
         delta, psi, slots, out_tok, out_cnt, hist, total;
     int64_t m_pre, m_dec, m_max, max_tiles, max_splits, maxp, num_pages;
     int act_bytes;
@@ -157,6 +158,11 @@ WsLayout ws_layout(const mtp_config& c) {
     w.delta = take(B * KH * TK * 4);
     w.psi = take(B * KH * TK * 4);
     w.slots = take(B * KH * 4);
+    w.u_states = take(B * 64 * 4);                // union lattice (K * top_k <= 64 states)
+    w.u_m = take(B * 4);
+    w.u_ehat = take(B * MTP_MAX_HEADS_K * 64 * 4);
+    w.u_delta = take(B * MTP_MAX_HEADS_K * 64 * 4);
+    w.u_psi = take(B * MTP_MAX_HEADS_K * 64 * 4);
     w.out_tok = take(B * KH * 4);
     w.out_cnt = take(B * 4);
     w.hist = take(B * (int64_t)c.max_new * 4);
@@ -181,16 +187,17 @@ struct mtp_ctx {
     bool prefilled = false;
     int B = 0;
     int q_pad = 0;               // pending rows per sequence for the next step
-    int last_K = 0, last_topk = 0;
+    int last_K = 0, last_topk = 0, last_lattice = 0;
     int split_len = 64, n_splits = 1;
+    int lattice = MTP_LATTICE_OWN, anchored = 0;   // selection options (mtp_set_selection)
     int64_t plan_ctx = 0;        // longest prompt + budget of the batch (sizes the split plan)
     std::vector<int32_t> h_ids, h_last, h_btab;
     std::vector<RowInfo> h_rows;
     std::vector<int2> h_tiles;
     std::vector<SeqState> h_state;
     int n_pre_rows = 0, n_pre_tiles = 0;
-    // graphs keyed by (K, top_k, q_pad, batch, split_len, n_splits)
-    using StepKey = std::tuple<int, int, int, int, int, int>;
+    // graphs keyed by (K, top_k, q_pad, batch, split_len, n_splits, lattice, anchored)
+    using StepKey = std::tuple<int, int, int, int, int, int, int, int>;
     std::map<StepKey, hipGraphExec_t> graphs;
     // every launch of each kernel class in the step of a key (arguments
     // captured by value), for replay timing
@@ -460,7 +467,11 @@ int enqueue_step(mtp_ctx* c, int K, int top_k) {
     s.psi = c->ws_ptr<int32_t>(c->ws.psi); s.slots = c->ws_ptr<int32_t>(c->ws.slots);
     s.out_tokens = c->ws_ptr<int32_t>(c->ws.out_tok); s.out_count = c->ws_ptr<int32_t>(c->ws.out_cnt);
     s.hist = c->ws_ptr<int32_t>(c->ws.hist); s.hist_ld = cf.max_new;
-    HIPCHK(c, select_fused(st, s), "select");
+    s.lattice = c->lattice; s.anchored = c->anchored;
+    s.u_states = c->ws_ptr<int32_t>(c->ws.u_states); s.u_m = c->ws_ptr<int32_t>(c->ws.u_m);
+    s.u_ehat = c->ws_ptr<float>(c->ws.u_ehat); s.u_delta = c->ws_ptr<float>(c->ws.u_delta);
+    s.u_psi = c->ws_ptr<int32_t>(c->ws.u_psi);
+    HIPCHK(c, launch_rec(c, MTP_KCLASS_SELECT, [s](hipStream_t q) { return select_fused(q, s); }), "select");
     return MTP_OK;
 }
 
@@ -508,7 +519,8 @@ int step_common(mtp_ctx* c, int K, int top_k) {
         const int rc0 = plan_splits(c, c->q_pad);
         if (rc0) return rc0;
     }
-    const auto key = std::make_tuple(K, top_k, c->q_pad, c->B, c->split_len, c->n_splits);
+    if (c->lattice == MTP_LATTICE_UNION && K * top_k > 64) { c->err = "union lattice needs K * top_k <= 64"; return MTP_EINVAL; }
+    const auto key = std::make_tuple(K, top_k, c->q_pad, c->B, c->split_len, c->n_splits, c->lattice, c->anchored);
     auto record = [&]() {
         mtp_ctx::StepLaunches& sl = c->step_launches[key];
         for (auto& v : sl.cls) v.clear();
@@ -543,6 +555,7 @@ int step_common(mtp_ctx* c, int K, int top_k) {
         c->q_pad = K;
         c->last_K = K;
         c->last_topk = top_k;
+        c->last_lattice = c->lattice;
         c->last_key = key;
         c->has_last = true;
     }
@@ -664,6 +677,7 @@ int mtp_prefill(mtp_ctx* c, int B, const int32_t* phon, const int32_t* phon_len,
         c->h_last[b] = row0 + len - 1;
         SeqState s{};
         s.ctx_len = len; s.pend_len = 0; s.gen = 0; s.done = 0; s.phon_len = phon_len[b]; s.prompt_len = len;
+        s.last_tok = ac_len[b] > 0 ? ac[oa - 1] : -1;     // the acoustic prompt's last codec token
         c->h_state[b] = s;
     }
     const int rows = (int)c->h_ids.size();
@@ -753,6 +767,32 @@ int mtp_get_lattice(mtp_ctx* c, int32_t* cand, float* ehat, float* delta, int32_
     return MTP_OK;
 }
 
+int mtp_set_selection(mtp_ctx* c, int lattice, int anchored) {
+    if (!c) return MTP_EINVAL;
+    if (lattice != MTP_LATTICE_OWN && lattice != MTP_LATTICE_UNION) { c->err = "unknown lattice"; return MTP_EINVAL; }
+    if (anchored != 0 && anchored != 1) { c->err = "anchored must be 0 or 1"; return MTP_EINVAL; }
+    c->lattice = lattice;
+    c->anchored = anchored;
+    return MTP_OK;
+}
+
+int mtp_get_union_lattice(mtp_ctx* c, int32_t* m, int32_t* states, float* ehat, float* delta, int32_t* psi,
+                          int32_t* slots) {
+    if (!c) return MTP_EINVAL;
+    if (!c->last_K) { c->err = "no decode step yet"; return MTP_ESTATE; }
+    if (c->last_lattice != MTP_LATTICE_UNION) { c->err = "the last step did not use the union lattice"; return MTP_ESTATE; }
+    const size_t B = c->B, n = B * MTP_MAX_HEADS_K * 64 * 4;
+    hipStream_t st = c->stream;
+    if (m) HIPCHK(c, hipMemcpyAsync(m, c->WS() + c->ws.u_m, B * 4, hipMemcpyDeviceToHost, st), "m");
+    if (states) HIPCHK(c, hipMemcpyAsync(states, c->WS() + c->ws.u_states, B * 64 * 4, hipMemcpyDeviceToHost, st), "states");
+    if (ehat) HIPCHK(c, hipMemcpyAsync(ehat, c->WS() + c->ws.u_ehat, n, hipMemcpyDeviceToHost, st), "ehat");
+    if (delta) HIPCHK(c, hipMemcpyAsync(delta, c->WS() + c->ws.u_delta, n, hipMemcpyDeviceToHost, st), "delta");
+    if (psi) HIPCHK(c, hipMemcpyAsync(psi, c->WS() + c->ws.u_psi, n, hipMemcpyDeviceToHost, st), "psi");
+    if (slots) HIPCHK(c, hipMemcpyAsync(slots, c->WS() + c->ws.slots, B * c->last_K * 4, hipMemcpyDeviceToHost, st), "slots");
+    HIPCHK(c, hipStreamSynchronize(st), "sync");
+    return MTP_OK;
+}
+
 int mtp_get_seq_state(mtp_ctx* c, int32_t* ctx_len, int32_t* pend_len, int32_t* gen, int32_t* done) {
     if (!c) return MTP_EINVAL;
     if (!c->prefilled) { c->err = "no prefill yet"; return MTP_ESTATE; }
@@ -778,7 +818,7 @@ int mtp_get_tokens(mtp_ctx* c, int32_t* tokens) {
 
 int mtp_profile_replay(mtp_ctx* c, int kclass, int iters, int cold, double* avg_us) {
     if (!c || !avg_us || iters < 1) return MTP_EINVAL;
-    if (kclass < MTP_KCLASS_GEMM_FFN1 || kclass > MTP_KCLASS_GEMM_OPROJ) { c->err = "unknown kernel class"; return MTP_EINVAL; }
+    if (kclass < MTP_KCLASS_GEMM_FFN1 || kclass > MTP_KCLASS_SELECT) { c->err = "unknown kernel class"; return MTP_EINVAL; }
     auto it = c->has_last ? c->step_launches.find(c->last_key) : c->step_launches.end();
     if (it == c->step_launches.end() || it->second.cls[kclass].empty()) {
         c->err = "the last decode step launched nothing of this kernel class";

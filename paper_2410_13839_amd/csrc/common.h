@@ -37,7 +37,7 @@ struct SeqState {
     int32_t phon_len;    // phoneme prefix length
     int32_t prompt_len;  // phonemes + acoustic prompt
     int32_t steps;       // decode steps taken
-    int32_t pad0;
+    int32_t last_tok;    // last emitted codec token (the prompt's last one before any), -1 if none
     int32_t pend_ids[MTP_MAX_HEADS_K];
 };
 static_assert(sizeof(SeqState) == 64, "SeqState layout");

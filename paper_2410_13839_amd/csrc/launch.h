@@ -166,6 +166,10 @@ struct SelectArgs {
     int32_t* out_tokens;       // [B][K]
     int32_t* out_count;        // [B]
     int32_t* hist; int hist_ld;  // [B][max_new]
+    int lattice;               // 0 own top_k per position, 1 union of all heads' top_k
+    int anchored;              // 1: delta_0 carries logQ[last emitted token][c]
+    int32_t* u_states; int32_t* u_m;        // union lattice: [B][64] states, [B] count
+    float* u_ehat; float* u_delta; int32_t* u_psi;   // [B][8][64]
 };
 hipError_t topk(hipStream_t st, const SelectArgs& a);
 // top_k of all K heads, Viterbi and accept in one launch (one workgroup per sequence).

@@ -166,22 +166,42 @@ hipError_t viterbi_accept(hipStream_t st, const SelectArgs& a) {
 
 // ---------------------------------------------------------------- fused
 // One workgroup per sequence, one wave per head: top_k of every head in
-// parallel, then all (K-1) x top_k x top_k transition entries are gathered
-// into LDS at once, then wave 0 runs the recursion, the backtrack and the
-// accept rule.  Same arithmetic and tie rules as the two kernels above.
+// parallel; then the lattice's emissions and transition sub-tables are
+// gathered into LDS at once, and wave 0 runs the recursion, the backtrack and
+// the accept rule.  Same arithmetic and tie rules as the two kernels above.
+//
+// Two lattices (Sec. 3.3):
+//   own    position t's states are head t's top_k (ordered by logit);
+//   union  every position's states are the m <= K*top_k distinct tokens of
+//          all heads' top_k in ascending id, scored at position t by head t
+//          (e_t(c) = l_t[c] - max l_t), with the m x m sub-table of log Q.
+// With `anchored`, delta_0 also carries logQ[last emitted token][c].
 namespace mtp {
+
+namespace {
+constexpr int UMAX = 64;   // union states at most (K * top_k <= 64)
+}
 
 __global__ __launch_bounds__(512) void select_fused_kernel(SelectArgs a) {
     const int b = blockIdx.x;
     const int tid = threadIdx.x, lane = tid & 63, t = tid >> 6;
     const int K = a.K, k = a.top_k, V = a.V;
+    const bool uni = a.lattice == 1;
     __shared__ int s_cand[MTP_MAX_HEADS_K][MTP_MAX_TOPK];
     __shared__ float s_ehat[MTP_MAX_HEADS_K][MTP_MAX_TOPK];
-    __shared__ float s_T[MTP_MAX_HEADS_K - 1][MTP_MAX_TOPK][MTP_MAX_TOPK];   // [t-1][j][i] (i contiguous)
-    __shared__ int s_psi[MTP_MAX_HEADS_K][MTP_MAX_TOPK];
-    __shared__ float s_delta[MTP_MAX_TOPK];
+    __shared__ float s_top[MTP_MAX_HEADS_K];
+    // own lattice: T[t-1][j][i] = logQ[c_{t-1,i}][c_{t,j}] (i contiguous)
+    __shared__ float s_T[MTP_MAX_HEADS_K - 1][MTP_MAX_TOPK][MTP_MAX_TOPK];
+    // union lattice: states, emissions [t][j], transitions [j][i]
+    __shared__ int s_U[UMAX];
+    __shared__ int s_m;
+    __shared__ float s_ue[MTP_MAX_HEADS_K][UMAX];
+    __shared__ float s_UT[UMAX][UMAX];
+    __shared__ float s_anc[UMAX];                // logQ[anchor][state of position 0]
+    __shared__ int s_psi[MTP_MAX_HEADS_K][UMAX];
     const SeqState st0 = a.st[b];
     const size_t base = (size_t)b * K * k;
+    const int prev = a.anchored ? st0.last_tok : -1;
 
     // top_k of head t (wave t)
     {
@@ -224,34 +244,80 @@ __global__ __launch_bounds__(512) void select_fused_kernel(SelectArgs a) {
             a.cand[base + t * k + lane] = my_c;
             a.ehat[base + t * k + lane] = my_e;
         }
+        if (lane == 0) s_top[t] = top0;
     }
     __syncthreads();
-    // transition sub-tables T[t-1][j][i] = logQ[c_{t-1,i}][c_{t,j}] (stored
-    // with i contiguous: the recursion reads one row per slot j)
-    const int kk = k * k;
-    for (int idx = tid; idx < (K - 1) * kk; idx += blockDim.x) {
-        const int t1 = idx / kk, rem = idx - t1 * kk;
-        const int i = rem / k, j = rem - i * k;
-        s_T[t1][j][i] = a.logq[(size_t)s_cand[t1][i] * V + s_cand[t1 + 1][j]];
+
+    int m = k;                                   // states per position
+    if (uni) {
+        // the distinct candidate ids in ascending order (wave 0): a lane keeps
+        // its id if no lower lane holds the same id; its rank is the number of
+        // kept ids below it
+        if (t == 0) {
+            const int n = K * k;
+            const int id = (lane < n) ? s_cand[udiv_small(lane, k)][lane - udiv_small(lane, k) * k] : INT_MAX;
+            bool dup = false;
+            for (int o = 0; o < n; ++o) dup |= (__builtin_amdgcn_readlane(id, o) == id) & (o < lane);
+            const bool keep = (lane < n) & !dup;
+            const uint64_t kept = __ballot(keep);
+            int rank = 0;
+            for (int o = 0; o < n; ++o)
+                rank += (int)(((kept >> o) & 1ull) != 0ull) & (__builtin_amdgcn_readlane(id, o) < id);
+            if (keep) s_U[rank] = id;
+            if (lane == 0) s_m = __popcll(kept);
+        }
+        __syncthreads();
+        m = s_m;
+        // emissions e_t(U_j) = l_t[U_j] - max l_t (EOS masked per head),
+        // transitions T[j][i] = logQ[U_i][U_j], anchor row
+        const float* lgb = a.logits + (size_t)b * a.ld_logits;
+        for (int idx = tid; idx < K * m; idx += blockDim.x) {
+            const int tt = udiv_small(idx, m), j = idx - tt * m;
+            const int c = s_U[j];
+            float l = lgb[(size_t)tt * V + c];
+            if (c == a.eos_id && (st0.gen + tt) < a.eos_min) l = -INFINITY;
+            s_ue[tt][j] = l - s_top[tt];
+        }
+        for (int idx = tid; idx < m * m; idx += blockDim.x) {
+            const int j = udiv_small(idx, m), i = idx - j * m;
+            s_UT[j][i] = a.logq[(size_t)s_U[i] * V + s_U[j]];
+        }
+        if (prev >= 0)
+            for (int j = tid; j < m; j += blockDim.x) s_anc[j] = a.logq[(size_t)prev * V + s_U[j]];
+    } else {
+        const int kk = k * k;
+        for (int idx = tid; idx < (K - 1) * kk; idx += blockDim.x) {
+            const int t1 = udiv_small(idx, kk), rem = idx - t1 * kk;
+            const int i = udiv_small(rem, k), j = rem - i * k;
+            s_T[t1][j][i] = a.logq[(size_t)s_cand[t1][i] * V + s_cand[t1 + 1][j]];
+        }
+        if (prev >= 0)
+            for (int j = tid; j < k; j += blockDim.x) s_anc[j] = a.logq[(size_t)prev * V + s_cand[0][j]];
     }
     __syncthreads();
     if (t != 0) return;
 
-    // Viterbi on wave 0: lane j holds slot j's score; the scores of the other
-    // slots come from v_readlane with the (uniform) loop index, so a step is k
-    // adds and compares in registers plus one LDS row of transitions.
+    // Viterbi on wave 0: lane j holds state j's score; the scores of the other
+    // states come from v_readlane with the (uniform) loop index, so a step is
+    // m adds and compares in registers plus one LDS row of transitions.
     const int j = lane;
-    const int jc = j < k ? j : 0;
-    float delta = (j < k) ? s_ehat[0][jc] : -INFINITY;
-    if (j < k) {
-        a.delta[base + j] = delta;
-        a.psi[base + j] = 0;
+    const int jc = j < m ? j : 0;
+    const int ld = uni ? UMAX : MTP_MAX_TOPK;    // row strides of the emission / delta outputs
+    float e0 = uni ? s_ue[0][jc] : s_ehat[0][jc];
+    float delta = (j < m) ? (prev >= 0 ? s_anc[jc] + e0 : e0) : -INFINITY;
+    float* out_delta = uni ? a.u_delta + (size_t)b * MTP_MAX_HEADS_K * UMAX : a.delta + base;
+    int32_t* out_psi = uni ? a.u_psi + (size_t)b * MTP_MAX_HEADS_K * UMAX : a.psi + base;
+    const int ostride = uni ? UMAX : k;
+    if (j < m) {
+        out_delta[j] = delta;
+        out_psi[j] = 0;
+        if (uni) a.u_ehat[(size_t)b * MTP_MAX_HEADS_K * UMAX + j] = e0;
     }
     for (int tt = 1; tt < K; ++tt) {
-        const float* Trow = &s_T[tt - 1][jc][0];
+        const float* Trow = uni ? &s_UT[jc][0] : &s_T[tt - 1][jc][0];
         float best = 0.f;
         int arg = 0;
-        for (int i = 0; i < k; ++i) {
+        for (int i = 0; i < m; ++i) {
             const float di = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(delta), i));
             const float sc = di + Trow[i];
             if (i == 0 || sc > best) {
@@ -259,30 +325,37 @@ __global__ __launch_bounds__(512) void select_fused_kernel(SelectArgs a) {
                 arg = i;
             }
         }
-        delta = (j < k) ? best + s_ehat[tt][jc] : -INFINITY;
-        if (j < k) {
+        const float et = uni ? s_ue[tt][jc] : s_ehat[tt][jc];
+        delta = (j < m) ? best + et : -INFINITY;
+        if (j < m) {
             s_psi[tt][j] = arg;
-            a.delta[base + tt * k + j] = delta;
-            a.psi[base + tt * k + j] = arg;
+            out_delta[tt * ostride + j] = delta;
+            out_psi[tt * ostride + j] = arg;
+            if (uni) a.u_ehat[(size_t)b * MTP_MAX_HEADS_K * UMAX + tt * UMAX + j] = et;
         }
     }
-    float bestd = (j < k) ? delta : -INFINITY;
-    int last = (j < k) ? j : MTP_MAX_TOPK + j;
+    (void)ld;
+    float bestd = (j < m) ? delta : -INFINITY;
+    int last = (j < m) ? j : UMAX + j;
     wave_argmax_uniform(bestd, last);
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
     __builtin_amdgcn_wave_barrier();
 
-    // backtrack with uniform slot indices (slot_{t-1} = psi_t(slot_t));
+    // backtrack with uniform state indices (state_{t-1} = psi_t(state_t));
     // lane t keeps position t
     int my_slot = 0, my_tok = 0;
     int cur = last;
     for (int tt = K - 1; tt >= 0; --tt) {
-        const int tok = s_cand[tt][cur];
+        const int tok = uni ? s_U[cur] : s_cand[tt][cur];
         if (lane == tt) {
             my_slot = cur;
             my_tok = tok;
         }
         if (tt > 0) cur = s_psi[tt][cur];
+    }
+    if (uni) {
+        if (lane < m) a.u_states[(size_t)b * UMAX + lane] = s_U[lane];
+        if (lane == 0) a.u_m[b] = m;
     }
     // accept: the first min(K, budget) tokens, cut after the first EOS
     const SeqState s0 = st0;
@@ -297,6 +370,7 @@ __global__ __launch_bounds__(512) void select_fused_kernel(SelectArgs a) {
         }
         if (s0.gen + n >= a.max_new) done = true;
     }
+    const int last_tok = __builtin_amdgcn_readlane(my_tok, max(n - 1, 0));
     if (lane < K) {
         a.slots[(size_t)b * K + lane] = my_slot;
         a.out_tokens[(size_t)b * K + lane] = (lane < n) ? my_tok : -1;
@@ -313,6 +387,7 @@ __global__ __launch_bounds__(512) void select_fused_kernel(SelectArgs a) {
         sp->done = done ? 1 : 0;
         sp->pend_len = done ? 0 : n;
         sp->steps = s0.steps + 1;
+        if (n > 0) sp->last_tok = last_tok;
     }
 }
 

@@ -157,3 +157,20 @@ def test_packed_weights_hold_every_tensor():
     assert np.array_equal(img[off:off + 2 * tiled.size].view(np.uint16), tiled)
     off, n = b.mtp_weight_offset(cfg, b.MTP_T_B_1, 0)
     assert np.array_equal(img[off:off + 4 * n].view(np.float32), w["l0.b_1"])
+
+
+def test_set_selection_validates():
+    from paper_2410_13839_amd import binding as b
+    cfg = _cfg()
+    ctx = b.mtp_create(cfg, b.mtp_buffers(256, 512, 1024, 2048), 0)
+    try:
+        for lattice, anchored in ((2, 0), (-1, 0), (0, 2)):
+            with pytest.raises(b.MTPError) as e:
+                b.mtp_set_selection(ctx, lattice, anchored)
+            assert e.value.code == b.MTP_EINVAL
+        b.mtp_set_selection(ctx, b.MTP_LATTICE_UNION, True)
+        with pytest.raises(b.MTPError) as e:       # no step yet
+            b.mtp_get_union_lattice(ctx, 1, 4)
+        assert e.value.code == b.MTP_ESTATE
+    finally:
+        b.mtp_destroy(ctx)

@@ -271,7 +271,7 @@ def test_replay_timing_then_prefill_again():
 
     s = new_session(wl, w, logq)
     ref = run(s, 6)
-    for kc in (1, 2, 3, 4, 5, 6):
+    for kc in (1, 2, 3, 4, 5, 6, 7):
         for cold in (True, False):
             us = mtp_profile_replay(s.ctx, kc, 3, cold)
             assert 0.5 < us < 1000.0, (kc, cold, us)
