@@ -16,8 +16,13 @@ Prediction and Speculative Decoding", arXiv 2410.13839):
                    candidates (Fig. 2 step 1-2), the Viterbi recursion over
                    Q(a_i, a_j) * S_t(a_j) (Sec. 3.3) and the accept rule.
                    float32, the precision the GPU takes its decisions in.
+  sampling.py   -- top_k sampling inside the lattice (Fig. 2 caption): the
+                   path drawn from prod exp(e_t / tau) Q by forward filtering,
+                   backward sampling, with Philox4x64-10 uniforms; float32
+                   arithmetic every IEEE implementation reproduces exactly.
   brute.py      -- exhaustive search over every candidate path; the definition
-                   the Viterbi recursion must reproduce.
+                   the Viterbi recursion must reproduce, and the enumerated
+                   path distribution the sampler must draw from.
   generate.py   -- the AR loop: n tokens per step (Fig. 1b, Sec. 3.2).
 
 Parity status: every function is pinned by tests under tests/ (closed forms,

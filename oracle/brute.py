@@ -71,3 +71,24 @@ def tie_rule_path(optimal: np.ndarray) -> np.ndarray:
     rev = optimal[:, ::-1]
     order = np.lexsort(rev.T[::-1])
     return optimal[order[0]]
+
+
+def path_weights(cand: np.ndarray, ehat: np.ndarray, logq: np.ndarray, tau: float,
+                 anchor: Optional[int] = None) -> Tuple[np.ndarray, np.ndarray]:
+    """Normalised probability of every slot path under the sampling
+    distribution prod_t exp(e_t / tau) * prod_{t>=1} Q(a_{t-1}, a_t)
+    [* Q(anchor, a_0)], float64 with numpy's exp."""
+    cand = np.asarray(cand)
+    K, k = cand.shape
+    P = all_paths(K, k)
+    e = np.asarray(ehat, dtype=np.float64)
+    lq = np.asarray(logq, dtype=np.float64)
+    logw = np.zeros(P.shape[0])
+    if anchor is not None:
+        logw += lq[anchor, cand[0, P[:, 0]]]
+    for t in range(K):
+        logw += e[t, P[:, t]] / tau
+        if t > 0:
+            logw += lq[cand[t - 1, P[:, t - 1]], cand[t, P[:, t]]]
+    w = np.exp(logw - logw.max())
+    return P, w / w.sum()
