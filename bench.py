@@ -256,27 +256,33 @@ def main():
 
     # selection variants (Sec. 3.3): throughput of the whole step and the
     # selection kernel's own launch time (cold passes at step `mid`)
-    from paper_2410_13839_amd.binding import MTP_KCLASS_SELECT, mtp_profile_replay
+    from paper_2410_13839_amd.binding import (MTP_KCLASS_SELECT, MTP_SELECT_BEST, MTP_SELECT_SAMPLE,
+                                              mtp_profile_replay)
     variants = []
     if not args.no_variants:
-        for lat, anch, tk, what in ((0, False, wl.top_k, "each head's own top_k (default)"),
-                                    (1, False, wl.top_k, "union of all heads' top_k, m x m transitions"),
-                                    (0, True, wl.top_k, "own top_k, first position anchored"),
-                                    (1, True, wl.top_k, "union, first position anchored"),
-                                    (0, False, 1, "top_k = 1: per-head argmax, no Viterbi")):
+        for lat, anch, tk, smp, what in (
+                (0, False, wl.top_k, False, "each head's own top_k (default)"),
+                (1, False, wl.top_k, False, "union of all heads' top_k, m x m transitions"),
+                (0, True, wl.top_k, False, "own top_k, first position anchored"),
+                (1, True, wl.top_k, False, "union, first position anchored"),
+                (0, False, 1, False, "top_k = 1: per-head argmax, no Viterbi"),
+                (0, False, wl.top_k, True, "top_k sampling in the own lattice, temperature 1"),
+                (1, False, wl.top_k, True, "top_k sampling in the union lattice, temperature 1")):
             sess.set_selection(lat, anch)
+            sess.set_sampling(MTP_SELECT_SAMPLE if smp else MTP_SELECT_BEST, 1.0, 2024)
             vms, vtok = time_decode(sess, wl, prompts, _steps_per_generation(wl), 5, torch, top_k=tk)
             sess.prefill(prompts.phon, prompts.ac)
             for _ in range(mid):
                 sess.step_async(wl.K, tk)
             torch.cuda.synchronize()
             sel_us = mtp_profile_replay(sess.ctx, MTP_KCLASS_SELECT, passes, True)
-            v = {"lattice": "union" if lat else "own", "anchored": anch, "top_k": tk, "selection": what,
+            v = {"lattice": "union" if lat else "own", "anchored": anch, "top_k": tk, "sampled": smp, "selection": what,
                  "tokens_per_s": round(vtok / (vms / 1000.0), 1), "us_per_step": round(vms * 1000.0 / _steps_per_generation(wl), 2),
                  "select_kernel_us": round(sel_us, 3)}
             variants.append(v)
             print(f"[bench] variant {v}", file=sys.stderr, flush=True)
         sess.set_selection(0, False)
+        sess.set_sampling(MTP_SELECT_BEST)
     sess.close()
     del sess
     torch.cuda.empty_cache()

@@ -198,6 +198,35 @@ int mtp_get_lattice(mtp_ctx* ctx, int32_t* cand, float* ehat, float* delta,
 #define MTP_LATTICE_UNION  1
 int mtp_set_selection(mtp_ctx* ctx, int lattice, int anchored);
 
+/* Path choice for the following decode steps.  MTP_SELECT_BEST (default):
+ * the highest-scoring path (Viterbi, Sec. 3.3).  MTP_SELECT_SAMPLE: top_k
+ * sampling inside the lattice (Fig. 2 caption) -- the path is drawn from the
+ * distribution over the lattice's paths (either lattice, anchored or not)
+ * proportional to prod_t exp(e_t(a_t) / temperature) * prod_{t>=1}
+ * Q(a_{t-1}, a_t), by forward filtering, backward sampling: forward weights
+ * alpha_t(j) = exp(e_t(j)/temperature) * sum_i alpha_{t-1}(i) Q(i, j), each
+ * position rescaled by a power of two, then position K-1 drawn from
+ * alpha_{K-1} and position t from alpha_t(i) Q(i, a_{t+1}).  One head gives
+ * ordinary top_k sampling at that temperature.  Draw r of a step (r = K-1-t
+ * for position t) of sequence b with generated count g uses word r % 4 of
+ * the Philox4x64-10 block (Salmon et al., SC 2011) at counter (g, b, r / 4, 0)
+ * with key (seed, 0), as u = (word >> 40) * 2^-24; the draw takes the first
+ * state whose running weight sum exceeds u times the total.  The arithmetic
+ * is IEEE float32 with one rounding per operation, products flushed to 0
+ * below 2^-100 and a fixed exp evaluation, so it is reproducible bit for bit
+ * on any IEEE float32 implementation.  In this mode the lattice hooks return
+ * the rescaled forward weights in place of delta and -1 in psi.
+ * temperature (sample mode only) must be finite and > 0 with a finite
+ * reciprocal; MTP_EINVAL otherwise or for an unknown mode.  Takes effect at
+ * the next step; every step uses the seed and temperature last set. */
+#define MTP_SELECT_BEST    0
+#define MTP_SELECT_SAMPLE  1
+int mtp_set_sampling(mtp_ctx* ctx, int mode, float temperature, uint64_t seed);
+
+/* The last step's uniforms, float32 [B][8] in draw order (entries r < K
+ * valid), to host (synchronises); MTP_ESTATE unless the last step sampled. */
+int mtp_get_uniforms(mtp_ctx* ctx, float* u);
+
 /* The last step's union lattice (it must have used MTP_LATTICE_UNION, else
  * MTP_ESTATE), to host (synchronises): m int32 [B] state counts; states
  * int32 [B][64] (ascending ids, the first m valid); ehat, delta float32 and

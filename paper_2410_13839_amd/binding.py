@@ -33,8 +33,9 @@ MTP_FLAG_NO_GRAPH = 1
 EXPORTED = ["mtp_query_sizes", "mtp_weight_offset", "mtp_create", "mtp_prefill", "mtp_decode_step",
             "mtp_decode_step_async", "mtp_get_logits", "mtp_get_lattice", "mtp_get_seq_state", "mtp_get_tokens",
             "mtp_profile_replay", "mtp_reset", "mtp_destroy", "mtp_last_error", "mtp_strerror",
-            "mtp_set_selection", "mtp_get_union_lattice"]
+            "mtp_set_selection", "mtp_get_union_lattice", "mtp_set_sampling", "mtp_get_uniforms"]
 MTP_LATTICE_OWN, MTP_LATTICE_UNION = 0, 1
+MTP_SELECT_BEST, MTP_SELECT_SAMPLE = 0, 1
 
 
 class mtp_config(ctypes.Structure):
@@ -68,6 +69,8 @@ _lib.mtp_get_logits.argtypes = [_ctx, _f32p]
 _lib.mtp_get_lattice.argtypes = [_ctx, _i32p, _f32p, _f32p, _i32p, _i32p]
 _lib.mtp_set_selection.argtypes = [_ctx, ctypes.c_int, ctypes.c_int]
 _lib.mtp_get_union_lattice.argtypes = [_ctx, _i32p, _i32p, _f32p, _f32p, _i32p, _i32p]
+_lib.mtp_set_sampling.argtypes = [_ctx, ctypes.c_int, ctypes.c_float, ctypes.c_uint64]
+_lib.mtp_get_uniforms.argtypes = [_ctx, _f32p]
 _lib.mtp_get_seq_state.argtypes = [_ctx, _i32p, _i32p, _i32p, _i32p]
 _lib.mtp_get_tokens.argtypes = [_ctx, _i32p]
 _lib.mtp_profile_replay.argtypes = [_ctx, ctypes.c_int, ctypes.c_int, ctypes.c_int, _P(ctypes.c_double)]
@@ -148,6 +151,16 @@ def mtp_get_logits(ctx, B: int, K: int, V: int) -> np.ndarray:
 
 def mtp_set_selection(ctx, lattice: int, anchored: bool) -> None:
     _check(_lib.mtp_set_selection(ctx, lattice, int(anchored)), ctx, "mtp_set_selection")
+
+
+def mtp_set_sampling(ctx, mode: int, temperature: float = 1.0, seed: int = 0) -> None:
+    _check(_lib.mtp_set_sampling(ctx, mode, temperature, seed & ((1 << 64) - 1)), ctx, "mtp_set_sampling")
+
+
+def mtp_get_uniforms(ctx, B: int, K: int) -> np.ndarray:
+    u = np.zeros((B, 8), np.float32)
+    _check(_lib.mtp_get_uniforms(ctx, u.ctypes.data_as(_f32p)), ctx, "mtp_get_uniforms")
+    return u[:, :K]
 
 
 def mtp_get_union_lattice(ctx, B: int, K: int) -> Dict[str, np.ndarray]:
@@ -314,6 +327,12 @@ class Session:
 
     def union_lattice(self, K: int) -> Dict[str, np.ndarray]:
         return mtp_get_union_lattice(self.ctx, self.B, K)
+
+    def set_sampling(self, mode: int, temperature: float = 1.0, seed: int = 0) -> None:
+        mtp_set_sampling(self.ctx, mode, temperature, seed)
+
+    def uniforms(self, K: int) -> np.ndarray:
+        return mtp_get_uniforms(self.ctx, self.B, K)
 
     def seq_state(self) -> Dict[str, np.ndarray]:
         return mtp_get_seq_state(self.ctx, self.B)

@@ -7,6 +7,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
@@ -116,7 +117,7 @@ int validate(const mtp_config* c, std::string* why) {
 
 struct WsLayout {
     uint64_t rows, ids, tiles, last_row, state, btab, h, q, u, attn, ffn, part, apart, hz, z, logits, cand, ehat,
-        u_states, u_m, u_ehat, u_delta, u_psi,
+        u_states, u_m, u_ehat, u_delta, u_psi, smp_cfg, smp_u,
         delta, psi, slots, out_tok, out_cnt, hist, total;
     int64_t m_pre, m_dec, m_max, max_tiles, max_splits, maxp, num_pages;
     int act_bytes;
@@ -163,6 +164,8 @@ WsLayout ws_layout(const mtp_config& c) {
     w.u_ehat = take(B * MTP_MAX_HEADS_K * 64 * 4);
     w.u_delta = take(B * MTP_MAX_HEADS_K * 64 * 4);
     w.u_psi = take(B * MTP_MAX_HEADS_K * 64 * 4);
+    w.smp_cfg = take(sizeof(SampleCfg));
+    w.smp_u = take(B * MTP_MAX_HEADS_K * 4);
     w.out_tok = take(B * KH * 4);
     w.out_cnt = take(B * 4);
     w.hist = take(B * (int64_t)c.max_new * 4);
@@ -187,9 +190,12 @@ struct mtp_ctx {
     bool prefilled = false;
     int B = 0;
     int q_pad = 0;               // pending rows per sequence for the next step
-    int last_K = 0, last_topk = 0, last_lattice = 0;
+    int last_K = 0, last_topk = 0, last_lattice = 0, last_sample = 0;
     int split_len = 64, n_splits = 1;
     int lattice = MTP_LATTICE_OWN, anchored = 0;   // selection options (mtp_set_selection)
+    int sample = 0;              // mtp_set_sampling: draw the path instead of the best one
+    SampleCfg h_smp{0, 1.0f, 0}; // copied to the workspace before the next step when dirty
+    bool smp_dirty = true;
     int64_t plan_ctx = 0;        // longest prompt + budget of the batch (sizes the split plan)
     std::vector<int32_t> h_ids, h_last, h_btab;
     std::vector<RowInfo> h_rows;
@@ -197,7 +203,7 @@ struct mtp_ctx {
     std::vector<SeqState> h_state;
     int n_pre_rows = 0, n_pre_tiles = 0;
     // graphs keyed by (K, top_k, q_pad, batch, split_len, n_splits, lattice, anchored)
-    using StepKey = std::tuple<int, int, int, int, int, int, int, int>;
+    using StepKey = std::tuple<int, int, int, int, int, int, int, int, int>;
     std::map<StepKey, hipGraphExec_t> graphs;
     // every launch of each kernel class in the step of a key (arguments
     // captured by value), for replay timing
@@ -471,6 +477,9 @@ int enqueue_step(mtp_ctx* c, int K, int top_k) {
     s.u_states = c->ws_ptr<int32_t>(c->ws.u_states); s.u_m = c->ws_ptr<int32_t>(c->ws.u_m);
     s.u_ehat = c->ws_ptr<float>(c->ws.u_ehat); s.u_delta = c->ws_ptr<float>(c->ws.u_delta);
     s.u_psi = c->ws_ptr<int32_t>(c->ws.u_psi);
+    s.sample = c->sample;
+    s.smp = c->ws_ptr<SampleCfg>(c->ws.smp_cfg);
+    s.smp_u = c->ws_ptr<float>(c->ws.smp_u);
     HIPCHK(c, launch_rec(c, MTP_KCLASS_SELECT, [s](hipStream_t q) { return select_fused(q, s); }), "select");
     return MTP_OK;
 }
@@ -520,7 +529,17 @@ int step_common(mtp_ctx* c, int K, int top_k) {
         if (rc0) return rc0;
     }
     if (c->lattice == MTP_LATTICE_UNION && K * top_k > 64) { c->err = "union lattice needs K * top_k <= 64"; return MTP_EINVAL; }
-    const auto key = std::make_tuple(K, top_k, c->q_pad, c->B, c->split_len, c->n_splits, c->lattice, c->anchored);
+    if (c->sample && c->smp_dirty) {
+        // stream-ordered before this step's launches (never inside a capture)
+        // (waits for the copy, so that a later mtp_set_sampling cannot
+        // change the source under it; only after a change of settings)
+        HIPCHK(c, hipMemcpyAsync(c->WS() + c->ws.smp_cfg, &c->h_smp, sizeof(SampleCfg), hipMemcpyHostToDevice, c->stream),
+               "sampling configuration");
+        HIPCHK(c, hipStreamSynchronize(c->stream), "sampling configuration");
+        c->smp_dirty = false;
+    }
+    const auto key = std::make_tuple(K, top_k, c->q_pad, c->B, c->split_len, c->n_splits, c->lattice, c->anchored,
+                                     c->sample);
     auto record = [&]() {
         mtp_ctx::StepLaunches& sl = c->step_launches[key];
         for (auto& v : sl.cls) v.clear();
@@ -556,6 +575,7 @@ int step_common(mtp_ctx* c, int K, int top_k) {
         c->last_K = K;
         c->last_topk = top_k;
         c->last_lattice = c->lattice;
+        c->last_sample = c->sample;
         c->last_key = key;
         c->has_last = true;
     }
@@ -790,6 +810,33 @@ int mtp_get_union_lattice(mtp_ctx* c, int32_t* m, int32_t* states, float* ehat, 
     if (psi) HIPCHK(c, hipMemcpyAsync(psi, c->WS() + c->ws.u_psi, n, hipMemcpyDeviceToHost, st), "psi");
     if (slots) HIPCHK(c, hipMemcpyAsync(slots, c->WS() + c->ws.slots, B * c->last_K * 4, hipMemcpyDeviceToHost, st), "slots");
     HIPCHK(c, hipStreamSynchronize(st), "sync");
+    return MTP_OK;
+}
+
+int mtp_set_sampling(mtp_ctx* c, int mode, float temperature, uint64_t seed) {
+    if (!c) return MTP_EINVAL;
+    if (mode != MTP_SELECT_BEST && mode != MTP_SELECT_SAMPLE) { c->err = "unknown selection mode"; return MTP_EINVAL; }
+    if (mode == MTP_SELECT_SAMPLE) {
+        const float inv = 1.0f / temperature;
+        if (!(temperature > 0.f) || !std::isfinite(temperature) || !std::isfinite(inv)) {
+            c->err = "temperature must be finite and positive";
+            return MTP_EINVAL;
+        }
+        c->h_smp.seed = seed;
+        c->h_smp.inv_tau = inv;
+        c->smp_dirty = true;
+    }
+    c->sample = mode == MTP_SELECT_SAMPLE ? 1 : 0;
+    return MTP_OK;
+}
+
+int mtp_get_uniforms(mtp_ctx* c, float* u) {
+    if (!c || !u) return MTP_EINVAL;
+    if (!c->last_K) { c->err = "no decode step yet"; return MTP_ESTATE; }
+    if (!c->last_sample) { c->err = "the last step did not sample"; return MTP_ESTATE; }
+    HIPCHK(c, hipMemcpyAsync(u, c->WS() + c->ws.smp_u, (size_t)c->B * MTP_MAX_HEADS_K * 4, hipMemcpyDeviceToHost, c->stream),
+           "uniforms");
+    HIPCHK(c, hipStreamSynchronize(c->stream), "sync");
     return MTP_OK;
 }
 

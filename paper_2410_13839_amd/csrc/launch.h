@@ -155,6 +155,14 @@ struct FinalArgs {
 };
 hipError_t final_ln(hipStream_t st, const FinalArgs& a);
 
+// Sampling configuration, read by the selection kernel from device memory so
+// that a captured step serves every seed and temperature.
+struct SampleCfg {
+    uint64_t seed;             // Philox key word 0
+    float inv_tau;             // float32(1 / temperature)
+    int32_t pad;
+};
+
 struct SelectArgs {
     int B; int K; int top_k; int V; int eos_id; int eos_min; int max_new;
     int Q;                     // pending rows per sequence this step (0 right after prefill)
@@ -170,10 +178,12 @@ struct SelectArgs {
     int anchored;              // 1: delta_0 carries logQ[last emitted token][c]
     int32_t* u_states; int32_t* u_m;        // union lattice: [B][64] states, [B] count
     float* u_ehat; float* u_delta; int32_t* u_psi;   // [B][8][64]
+    int sample;                // 0 best path (Viterbi), 1 path drawn from the lattice distribution
+    const SampleCfg* smp;      // sampling seed and inverse temperature (device)
+    float* smp_u;              // [B][8] the uniforms of the step, in draw order
 };
-hipError_t topk(hipStream_t st, const SelectArgs& a);
-// top_k of all K heads, Viterbi and accept in one launch (one workgroup per sequence).
+// top_k of all K heads, Viterbi (or the sampled path) and accept in one
+// launch (one workgroup per sequence).
 hipError_t select_fused(hipStream_t st, const SelectArgs& a);
-hipError_t viterbi_accept(hipStream_t st, const SelectArgs& a);
 
 }  // namespace mtp

@@ -1,5 +1,5 @@
-// Selection kernels: EOS mask + per-head top_k, then the Viterbi lattice and
-// the accept rule (paper Sec. 3.3, Fig. 2).
+// Selection kernel: EOS mask + per-head top_k, then the lattice over the
+// K positions (paper Sec. 3.3, Fig. 2) and the accept rule.
 //
 // Every decision is made with the same float32 operations, in the same
 // association, as the plain definition: e_hat = l[c] - l[c_0];
@@ -7,12 +7,23 @@
 // with the lowest index winning ties in top_k (token id), in the predecessor
 // scan and in the final argmax (slot).  The (value, index) max-reductions use
 // a total order, so the shuffle tree cannot change their result.
+//
+// Sampling (top_k sampling inside the lattice, Fig. 2 caption) draws the path
+// from the distribution prod_t exp(e_t / tau) * prod Q(a_{t-1}, a_t) by
+// forward filtering, backward sampling.  Its arithmetic is fixed so that any
+// IEEE float32 implementation reproduces every draw: one rounding per
+// operation (no contraction into fused multiply-adds anywhere in this file),
+// sums in ascending state order, products flushed to zero below 2^-100 (no
+// result depends on subnormal handling), rescaling by exact powers of two,
+// and the exp evaluation of `smp_exp`.
 #include <limits.h>
 #include <math.h>
 
 #include "common.h"
 #include "launch.h"
 #include "wave.h"
+
+#pragma clang fp contract(off)
 
 namespace mtp {
 
@@ -22,160 +33,97 @@ constexpr int PER_LANE = 17;   // ceil(1025 / 64): logits held per lane
 __device__ __forceinline__ bool better(float va, int ia, float vb, int ib) {
     return (va > vb) | ((va == vb) & (ia < ib));
 }
+
+// Philox4x64-10 (Salmon, Moraes, Dror and Shaw, SC 2011): per round, words 0
+// and 2 are multiplied by the two round multipliers into 128-bit products and
+// the block becomes (hi1 ^ c1 ^ k0, lo1, hi0 ^ c3 ^ k1, lo0); the key then
+// advances by the Weyl increments (64-bit golden ratio and sqrt(3) - 1).
+__device__ __forceinline__ void philox4x64_10(uint64_t& c0, uint64_t& c1, uint64_t& c2, uint64_t& c3,
+                                              uint64_t k0, uint64_t k1) {
+    constexpr uint64_t M0 = 0xD2E7470EE14C6C93ull, M1 = 0xCA5A826395121157ull;
+    constexpr uint64_t W0 = 0x9E3779B97F4A7C15ull, W1 = 0xBB67AE8584CAA73Bull;
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        const uint64_t lo0 = M0 * c0, hi0 = __umul64hi(M0, c0);
+        const uint64_t lo1 = M1 * c2, hi1 = __umul64hi(M1, c2);
+        c0 = hi1 ^ c1 ^ k0;
+        c1 = lo1;
+        c2 = hi0 ^ c3 ^ k1;
+        c3 = lo0;
+        k0 += W0;
+        k1 += W1;
+    }
+}
+
+// e^x in float32 for x <= 0: x = n ln2 + r with n = rint(x log2(e)); ln 2 is
+// split into a head with 16 significant bits (n * head is exact for |n| <
+// 128) and a float32 tail; e^r by its Taylor series to degree 7 in Horner
+// form (|r| <= ln2/2, truncation below 2^-27); then the exact scaling by 2^n.
+// 0 below -64 (e^-64 ~ 2^-92) and for -inf.
+__device__ __forceinline__ float smp_exp(float x) {
+    if (!(x >= -64.0f)) return 0.f;
+    const float n = rintf(x * __int_as_float(0x3fb8aa3b));              // log2(e)
+    const float r = (x - n * __int_as_float(0x3f317200)) - n * __int_as_float(0x35bfbe8e);
+    float p = 1.0f / 5040.0f;
+    p = p * r + 1.0f / 720.0f;
+    p = p * r + 1.0f / 120.0f;
+    p = p * r + 1.0f / 24.0f;
+    p = p * r + 1.0f / 6.0f;
+    p = p * r + 0.5f;
+    p = p * r + 1.0f;
+    p = p * r + 1.0f;
+    return ldexpf(p, (int)n);
+}
+
+__device__ __forceinline__ float smp_flush(float x) { return x >= 0x1p-100f ? x : 0.f; }
+
+__device__ __forceinline__ float lane_f(float v, int i) {
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), i));
+}
+
+// Scale the wave's weights by the power of two that puts their maximum in
+// [1/2, 1) (exact), then flush.
+__device__ __forceinline__ float smp_rescale(float v) {
+    const float mx = wave_max64(v);
+    if (!(mx > 0.f)) return v;
+    int e;
+    (void)frexpf(mx, &e);
+    return smp_flush(ldexpf(v, -e));
+}
+
+// Inverse-CDF draw over lanes 0..m-1 holding weights w: the first lane whose
+// running sum (in lane order) exceeds u * total; the last lane of positive
+// weight if none does; 0 if every weight is 0.  The result is uniform.
+__device__ __forceinline__ int smp_draw(float w, float u, int m, int lane) {
+    float run = 0.f, mine = 0.f;
+    for (int i = 0; i < m; ++i) {
+        run = run + lane_f(w, i);
+        mine = (lane == i) ? run : mine;
+    }
+    const float thr = u * run;
+    const uint64_t over = __ballot((lane < m) & (mine > thr));
+    if (over) return __builtin_ctzll(over);
+    const uint64_t pos = __ballot((lane < m) & (w > 0.f));
+    return pos ? 63 - __builtin_clzll(pos) : 0;
+}
 }  // namespace
-
-// One wavefront per (sequence, head).
-__global__ __launch_bounds__(64) void topk_kernel(SelectArgs a) {
-    const int bt = blockIdx.x;
-    const int b = bt / a.K, t = bt - b * a.K;
-    const int lane = threadIdx.x;
-    const float* lg = a.logits + (size_t)b * a.ld_logits + (size_t)t * a.V;
-    const bool mask_eos = (a.st[b].gen + t) < a.eos_min;
-    float v[PER_LANE];
-#pragma unroll
-    for (int j = 0; j < PER_LANE; ++j) {
-        const int idx = lane + 64 * j;
-        float x = (idx < a.V) ? lg[idx] : -INFINITY;
-        if (idx == a.eos_id && mask_eos) x = -INFINITY;
-        v[j] = x;
-    }
-    uint32_t taken = 0;
-    float top0 = 0.f;
-    const size_t out = ((size_t)b * a.K + t) * a.top_k;
-    for (int r = 0; r < a.top_k; ++r) {
-        float bv = -INFINITY;
-        int bi = INT_MAX;
-#pragma unroll
-        for (int j = 0; j < PER_LANE; ++j) {
-            const int idx = lane + 64 * j;
-            if (idx < a.V && !((taken >> j) & 1u) && better(v[j], idx, bv, bi)) {
-                bv = v[j];
-                bi = idx;
-            }
-        }
-#pragma unroll
-        for (int o = 32; o >= 1; o >>= 1) {
-            const float ov = __shfl_xor(bv, o);
-            const int oi = __shfl_xor(bi, o);
-            if (better(ov, oi, bv, bi)) {
-                bv = ov;
-                bi = oi;
-            }
-        }
-        if ((bi & 63) == lane) taken |= 1u << (bi >> 6);
-        if (r == 0) top0 = bv;
-        if (lane == 0) {
-            a.cand[out + r] = bi;
-            a.ehat[out + r] = bv - top0;
-        }
-    }
-}
-
-// One wavefront per sequence: lane j owns candidate slot j.
-__global__ __launch_bounds__(64) void viterbi_accept_kernel(SelectArgs a) {
-    const int b = blockIdx.x, j = threadIdx.x;
-    const int K = a.K, k = a.top_k, V = a.V;
-    __shared__ int s_psi[MTP_MAX_HEADS_K][MTP_MAX_TOPK];
-    const size_t base = (size_t)b * K * k;
-    const int32_t* cand = a.cand + base;
-    const float* ehat = a.ehat + base;
-
-    float delta = (j < k) ? ehat[j] : -INFINITY;
-    if (j < k) {
-        a.delta[base + j] = delta;
-        a.psi[base + j] = 0;
-        s_psi[0][j] = 0;
-    }
-    for (int t = 1; t < K; ++t) {
-        const int cj = (j < k) ? cand[t * k + j] : 0;
-        float best = 0.f;
-        int arg = 0;
-        for (int i = 0; i < k; ++i) {
-            const float di = __shfl(delta, i);
-            const int ci = cand[(t - 1) * k + i];
-            const float s = di + a.logq[(size_t)ci * V + cj];
-            if (i == 0 || s > best) {
-                best = s;
-                arg = i;
-            }
-        }
-        delta = (j < k) ? best + ehat[t * k + j] : -INFINITY;
-        if (j < k) {
-            a.delta[base + t * k + j] = delta;
-            a.psi[base + t * k + j] = arg;
-            s_psi[t][j] = arg;
-        }
-    }
-    int last = 0;
-    float bestd = __shfl(delta, 0);
-    for (int i = 1; i < k; ++i) {
-        const float di = __shfl(delta, i);
-        if (di > bestd) {
-            bestd = di;
-            last = i;
-        }
-    }
-    __syncthreads();
-    if (j != 0) return;
-
-    int slots[MTP_MAX_HEADS_K], toks[MTP_MAX_HEADS_K];
-    slots[K - 1] = last;
-    for (int t = K - 1; t > 0; --t) slots[t - 1] = s_psi[t][slots[t]];
-    for (int t = 0; t < K; ++t) {
-        toks[t] = cand[t * k + slots[t]];
-        a.slots[(size_t)b * K + t] = slots[t];
-    }
-
-    SeqState s = a.st[b];
-    int n = 0;
-    bool done = s.done != 0;
-    if (!done) {
-        n = min(K, a.max_new - s.gen);
-        for (int p = 0; p < n; ++p) {
-            if (toks[p] == a.eos_id) {
-                n = p + 1;
-                done = true;
-                break;
-            }
-        }
-        if (s.gen + n >= a.max_new) done = true;
-    }
-    for (int t = 0; t < K; ++t) a.out_tokens[(size_t)b * K + t] = (t < n) ? toks[t] : -1;
-    a.out_count[b] = n;
-    for (int t = 0; t < n; ++t) a.hist[(size_t)b * a.hist_ld + s.gen + t] = toks[t];
-    s.ctx_len += s.pend_len;
-    s.gen += n;
-    s.done = done ? 1 : 0;
-    s.pend_len = done ? 0 : n;
-    for (int t = 0; t < n && t < MTP_MAX_HEADS_K; ++t) s.pend_ids[t] = toks[t];
-    s.steps += 1;
-    a.st[b] = s;
-}
-
-hipError_t topk(hipStream_t st, const SelectArgs& a) {
-    hipLaunchKernelGGL(topk_kernel, dim3(a.B * a.K), dim3(64), 0, st, a);
-    return hipGetLastError();
-}
-
-hipError_t viterbi_accept(hipStream_t st, const SelectArgs& a) {
-    hipLaunchKernelGGL(viterbi_accept_kernel, dim3(a.B), dim3(64), 0, st, a);
-    return hipGetLastError();
-}
 
 }  // namespace mtp
 
 // ---------------------------------------------------------------- fused
 // One workgroup per sequence, one wave per head: top_k of every head in
 // parallel; then the lattice's emissions and transition sub-tables are
-// gathered into LDS at once, and wave 0 runs the recursion, the backtrack and
-// the accept rule.  Same arithmetic and tie rules as the two kernels above.
+// gathered into LDS at once, and wave 0 runs the recursion, the backtrack (or
+// the backward draws) and the accept rule.
 //
 // Two lattices (Sec. 3.3):
 //   own    position t's states are head t's top_k (ordered by logit);
 //   union  every position's states are the m <= K*top_k distinct tokens of
 //          all heads' top_k in ascending id, scored at position t by head t
 //          (e_t(c) = l_t[c] - max l_t), with the m x m sub-table of log Q.
-// With `anchored`, delta_0 also carries logQ[last emitted token][c].
+// With `anchored`, the first position also carries the transition from the
+// last emitted token.  When sampling, the gathered transitions are stored as
+// probabilities (smp_exp of log Q).
 namespace mtp {
 
 namespace {
@@ -192,16 +140,19 @@ __global__ __launch_bounds__(512) void select_fused_kernel(SelectArgs a) {
     __shared__ float s_top[MTP_MAX_HEADS_K];
     // own lattice: T[t-1][j][i] = logQ[c_{t-1,i}][c_{t,j}] (i contiguous)
     __shared__ float s_T[MTP_MAX_HEADS_K - 1][MTP_MAX_TOPK][MTP_MAX_TOPK];
-    // union lattice: states, emissions [t][j], transitions [j][i]
+    // union lattice: states, emissions [t][j], transitions [i][j] =
+    // logQ[U_i][U_j] (a row per previous state, padded against bank conflicts)
     __shared__ int s_U[UMAX];
     __shared__ int s_m;
     __shared__ float s_ue[MTP_MAX_HEADS_K][UMAX];
-    __shared__ float s_UT[UMAX][UMAX];
+    __shared__ float s_UT[UMAX][UMAX + 1];
     __shared__ float s_anc[UMAX];                // logQ[anchor][state of position 0]
     __shared__ int s_psi[MTP_MAX_HEADS_K][UMAX];
+    __shared__ float s_alpha[MTP_MAX_HEADS_K][UMAX];   // sampling: forward weights
     const SeqState st0 = a.st[b];
     const size_t base = (size_t)b * K * k;
     const int prev = a.anchored ? st0.last_tok : -1;
+    const bool smp = a.sample != 0;
 
     // top_k of head t (wave t)
     {
@@ -279,79 +230,148 @@ __global__ __launch_bounds__(512) void select_fused_kernel(SelectArgs a) {
             s_ue[tt][j] = l - s_top[tt];
         }
         for (int idx = tid; idx < m * m; idx += blockDim.x) {
-            const int j = udiv_small(idx, m), i = idx - j * m;
-            s_UT[j][i] = a.logq[(size_t)s_U[i] * V + s_U[j]];
+            const int i = udiv_small(idx, m), j = idx - i * m;
+            const float lq = a.logq[(size_t)s_U[i] * V + s_U[j]];
+            s_UT[i][j] = smp ? smp_exp(lq) : lq;
         }
         if (prev >= 0)
-            for (int j = tid; j < m; j += blockDim.x) s_anc[j] = a.logq[(size_t)prev * V + s_U[j]];
+            for (int j = tid; j < m; j += blockDim.x) {
+                const float lq = a.logq[(size_t)prev * V + s_U[j]];
+                s_anc[j] = smp ? smp_exp(lq) : lq;
+            }
     } else {
         const int kk = k * k;
         for (int idx = tid; idx < (K - 1) * kk; idx += blockDim.x) {
             const int t1 = udiv_small(idx, kk), rem = idx - t1 * kk;
             const int i = udiv_small(rem, k), j = rem - i * k;
-            s_T[t1][j][i] = a.logq[(size_t)s_cand[t1][i] * V + s_cand[t1 + 1][j]];
+            const float lq = a.logq[(size_t)s_cand[t1][i] * V + s_cand[t1 + 1][j]];
+            s_T[t1][j][i] = smp ? smp_exp(lq) : lq;
         }
         if (prev >= 0)
-            for (int j = tid; j < k; j += blockDim.x) s_anc[j] = a.logq[(size_t)prev * V + s_cand[0][j]];
+            for (int j = tid; j < k; j += blockDim.x) {
+                const float lq = a.logq[(size_t)prev * V + s_cand[0][j]];
+                s_anc[j] = smp ? smp_exp(lq) : lq;
+            }
     }
     __syncthreads();
     if (t != 0) return;
 
-    // Viterbi on wave 0: lane j holds state j's score; the scores of the other
-    // states come from v_readlane with the (uniform) loop index, so a step is
-    // m adds and compares in registers plus one LDS row of transitions.
+    // Wave 0: lane j holds state j; the other states' values come from
+    // v_readlane with the (uniform) loop index, so a position costs m
+    // operations in registers plus one LDS read of transitions per lane.
     const int j = lane;
     const int jc = j < m ? j : 0;
-    const int ld = uni ? UMAX : MTP_MAX_TOPK;    // row strides of the emission / delta outputs
-    float e0 = uni ? s_ue[0][jc] : s_ehat[0][jc];
-    float delta = (j < m) ? (prev >= 0 ? s_anc[jc] + e0 : e0) : -INFINITY;
     float* out_delta = uni ? a.u_delta + (size_t)b * MTP_MAX_HEADS_K * UMAX : a.delta + base;
     int32_t* out_psi = uni ? a.u_psi + (size_t)b * MTP_MAX_HEADS_K * UMAX : a.psi + base;
+    float* out_ue = a.u_ehat + (size_t)b * MTP_MAX_HEADS_K * UMAX;
     const int ostride = uni ? UMAX : k;
-    if (j < m) {
-        out_delta[j] = delta;
-        out_psi[j] = 0;
-        if (uni) a.u_ehat[(size_t)b * MTP_MAX_HEADS_K * UMAX + j] = e0;
-    }
-    for (int tt = 1; tt < K; ++tt) {
-        const float* Trow = uni ? &s_UT[jc][0] : &s_T[tt - 1][jc][0];
-        float best = 0.f;
-        int arg = 0;
-        for (int i = 0; i < m; ++i) {
-            const float di = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(delta), i));
-            const float sc = di + Trow[i];
-            if (i == 0 || sc > best) {
-                best = sc;
-                arg = i;
+    // transitions into state jc of position tt from state i of position tt-1
+    auto trow = [&](int tt) -> const float* { return uni ? &s_UT[0][jc] : &s_T[tt - 1][jc][0]; };
+    const int tstep = uni ? UMAX + 1 : 1;
+    auto emis = [&](int tt) -> float { return uni ? s_ue[tt][jc] : s_ehat[tt][jc]; };
+    int my_slot = 0, my_tok = 0;
+
+    if (!smp) {
+        // Viterbi
+        const float e0 = emis(0);
+        float delta = (j < m) ? (prev >= 0 ? s_anc[jc] + e0 : e0) : -INFINITY;
+        if (j < m) {
+            out_delta[j] = delta;
+            out_psi[j] = 0;
+            if (uni) out_ue[j] = e0;
+        }
+        for (int tt = 1; tt < K; ++tt) {
+            const float* T = trow(tt);
+            float best = 0.f;
+            int arg = 0;
+            for (int i = 0; i < m; ++i) {
+                const float sc = lane_f(delta, i) + T[i * tstep];
+                if (i == 0 || sc > best) {
+                    best = sc;
+                    arg = i;
+                }
+            }
+            const float et = emis(tt);
+            delta = (j < m) ? best + et : -INFINITY;
+            if (j < m) {
+                s_psi[tt][j] = arg;
+                out_delta[tt * ostride + j] = delta;
+                out_psi[tt * ostride + j] = arg;
+                if (uni) out_ue[tt * UMAX + j] = et;
             }
         }
-        const float et = uni ? s_ue[tt][jc] : s_ehat[tt][jc];
-        delta = (j < m) ? best + et : -INFINITY;
-        if (j < m) {
-            s_psi[tt][j] = arg;
-            out_delta[tt * ostride + j] = delta;
-            out_psi[tt * ostride + j] = arg;
-            if (uni) a.u_ehat[(size_t)b * MTP_MAX_HEADS_K * UMAX + tt * UMAX + j] = et;
-        }
-    }
-    (void)ld;
-    float bestd = (j < m) ? delta : -INFINITY;
-    int last = (j < m) ? j : UMAX + j;
-    wave_argmax_uniform(bestd, last);
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-    __builtin_amdgcn_wave_barrier();
+        float bestd = (j < m) ? delta : -INFINITY;
+        int last = (j < m) ? j : UMAX + j;
+        wave_argmax_uniform(bestd, last);
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+        __builtin_amdgcn_wave_barrier();
 
-    // backtrack with uniform state indices (state_{t-1} = psi_t(state_t));
-    // lane t keeps position t
-    int my_slot = 0, my_tok = 0;
-    int cur = last;
-    for (int tt = K - 1; tt >= 0; --tt) {
-        const int tok = uni ? s_U[cur] : s_cand[tt][cur];
-        if (lane == tt) {
-            my_slot = cur;
-            my_tok = tok;
+        // backtrack with uniform state indices (state_{t-1} = psi_t(state_t));
+        // lane t keeps position t
+        int cur = last;
+        for (int tt = K - 1; tt >= 0; --tt) {
+            const int tok = uni ? s_U[cur] : s_cand[tt][cur];
+            if (lane == tt) {
+                my_slot = cur;
+                my_tok = tok;
+            }
+            if (tt > 0) cur = s_psi[tt][cur];
         }
-        if (tt > 0) cur = s_psi[tt][cur];
+    } else {
+        // Forward filtering, backward sampling.  Uniforms: lane r < K takes
+        // word r % 4 of the Philox block at counter (generated count, sequence,
+        // r / 4, 0), key (seed, 0); draw r decides position K-1-r.
+        const float inv_tau = a.smp->inv_tau;
+        float u;
+        {
+            uint64_t c0 = (uint64_t)st0.gen, c1 = (uint64_t)b, c2 = (uint64_t)(lane >> 2), c3 = 0;
+            philox4x64_10(c0, c1, c2, c3, a.smp->seed, 0);
+            const int wsel = lane & 3;
+            const uint64_t x = wsel == 0 ? c0 : wsel == 1 ? c1 : wsel == 2 ? c2 : c3;
+            u = (float)(uint32_t)(x >> 40) * 0x1p-24f;
+        }
+        if (lane < K) a.smp_u[(size_t)b * MTP_MAX_HEADS_K + lane] = u;
+
+        const float e0 = emis(0);
+        float alpha = (j < m) ? smp_exp(e0 * inv_tau) : 0.f;
+        if (prev >= 0) alpha = (j < m) ? smp_flush(alpha * s_anc[jc]) : 0.f;
+        alpha = smp_rescale(alpha);
+        s_alpha[0][lane] = alpha;
+        if (j < m) {
+            out_delta[j] = alpha;
+            out_psi[j] = -1;
+            if (uni) out_ue[j] = e0;
+        }
+        for (int tt = 1; tt < K; ++tt) {
+            const float* T = trow(tt);
+            float sum = 0.f;
+            for (int i = 0; i < m; ++i) sum = sum + smp_flush(lane_f(alpha, i) * T[i * tstep]);
+            const float et = emis(tt);
+            alpha = (j < m) ? smp_flush(smp_exp(et * inv_tau) * sum) : 0.f;
+            alpha = smp_rescale(alpha);
+            s_alpha[tt][lane] = alpha;
+            if (j < m) {
+                out_delta[tt * ostride + j] = alpha;
+                out_psi[tt * ostride + j] = -1;
+                if (uni) out_ue[tt * UMAX + j] = et;
+            }
+        }
+        // backward: position K-1 from alpha_{K-1}; position tt from
+        // alpha_tt(i) * Q(state i, the state drawn at tt + 1)
+        int cur = smp_draw(alpha, lane_f(u, 0), m, lane);
+        if (lane == K - 1) {
+            my_slot = cur;
+            my_tok = uni ? s_U[cur] : s_cand[K - 1][cur];
+        }
+        for (int tt = K - 2; tt >= 0; --tt) {
+            const float g = uni ? s_UT[jc][cur] : s_T[tt][cur][jc];
+            const float w = (j < m) ? smp_flush(s_alpha[tt][jc] * g) : 0.f;
+            cur = smp_draw(w, lane_f(u, K - 1 - tt), m, lane);
+            if (lane == tt) {
+                my_slot = cur;
+                my_tok = uni ? s_U[cur] : s_cand[tt][cur];
+            }
+        }
     }
     if (uni) {
         if (lane < m) a.u_states[(size_t)b * UMAX + lane] = s_U[lane];

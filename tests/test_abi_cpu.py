@@ -174,3 +174,22 @@ def test_set_selection_validates():
         assert e.value.code == b.MTP_ESTATE
     finally:
         b.mtp_destroy(ctx)
+
+
+def test_set_sampling_validates():
+    from paper_2410_13839_amd import binding as b
+    cfg = _cfg()
+    ctx = b.mtp_create(cfg, b.mtp_buffers(256, 512, 1024, 2048), 0)
+    try:
+        for mode, tau in ((2, 1.0), (-1, 1.0), (1, 0.0), (1, -1.0), (1, float("nan")), (1, float("inf")),
+                          (1, 1e-45)):
+            with pytest.raises(b.MTPError) as e:
+                b.mtp_set_sampling(ctx, mode, tau, 1)
+            assert e.value.code == b.MTP_EINVAL, (mode, tau)
+        b.mtp_set_sampling(ctx, b.MTP_SELECT_SAMPLE, 0.7, (1 << 64) - 1)
+        b.mtp_set_sampling(ctx, b.MTP_SELECT_BEST, 0.0, 0)      # temperature unused when not sampling
+        with pytest.raises(b.MTPError) as e:                    # no step yet
+            b.mtp_get_uniforms(ctx, 1, 4)
+        assert e.value.code == b.MTP_ESTATE
+    finally:
+        b.mtp_destroy(ctx)
