@@ -223,3 +223,85 @@ def make_prompts(wl: Workload, seed_base: int = PROMPT_SEED_BASE, batch: Optiona
 def random_logits(rng: np.random.Generator, shape, scale: float = 0.64) -> np.ndarray:
     """iid N(0, scale^2) float32 logits, the spread of the VALL-E-shaped heads."""
     return (rng.standard_normal(size=shape) * scale).astype(np.float32)
+
+
+# ---------------------------------------------------------------- token corpora
+# Synthetic stand-ins for the codec-token streams a transition table is
+# counted from (the paper derives Q from the LibriTTS training set).
+
+
+@dataclass(frozen=True)
+class CorpusSpec:
+    """Token-stream corpus shape: `n_seqs` utterances whose lengths are
+    Gamma(2)-distributed with mean `mean_len`, clipped to [min_len, max_len]."""
+    name: str
+    n_seqs: int
+    mean_len: float
+    min_len: int
+    max_len: int
+    seed: int
+
+
+CORPORA: Dict[str, CorpusSpec] = {
+    # LibriTTS train-clean-100 + train-clean-360 + train-other-500: 354,780
+    # utterances, ~585 h, i.e. ~297 first-quantizer tokens per utterance at
+    # SpeechTokenizer's 50 Hz frame rate (~105 M tokens in all)
+    "libritts_train": CorpusSpec("libritts_train", 354780, 297.0, 13, 1750, seed=31),
+    "small": CorpusSpec("small", 257, 37.0, 0, 160, seed=32),
+}
+
+
+@dataclass
+class Corpus:
+    tokens: np.ndarray    # int32 [n_tokens], utterances back to back
+    offsets: np.ndarray   # int64 [n_seqs + 1], utterance u = tokens[offsets[u]:offsets[u+1]]
+
+
+def _alias_tables(p: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
+    """Walker's alias tables (Vose's construction) for every row of a
+    row-stochastic matrix: draw column c uniformly, keep it with probability
+    keep[r, c], else take alias[r, c]."""
+    R, n = p.shape
+    keep = np.ones((R, n))
+    alias = np.tile(np.arange(n, dtype=np.int32), (R, 1))
+    for r in range(R):
+        w = (p[r] * n).tolist()
+        small = [i for i in range(n) if w[i] < 1.0]
+        large = [i for i in range(n) if w[i] >= 1.0]
+        kr, ar = keep[r], alias[r]
+        while small and large:
+            s_, l_ = small.pop(), large.pop()
+            kr[s_] = w[s_]
+            ar[s_] = l_
+            w[l_] = (w[l_] + w[s_]) - 1.0
+            (small if w[l_] < 1.0 else large).append(l_)
+    return keep, alias
+
+
+def make_corpus(spec: CorpusSpec, logq: Optional[np.ndarray] = None, chains: int = 65536,
+                n_codes: int = EOS_ID) -> Corpus:
+    """Codec-token utterances drawn from the Markov chain of Q (rows and
+    columns of the first `n_codes` ids, renormalised; the synthetic table by
+    default).  `chains` chains run side by side from uniform starting tokens;
+    their concatenation is cut into the utterances."""
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([spec.seed, 5])))
+    lens = np.clip(np.rint(rng.gamma(2.0, spec.mean_len / 2.0, size=spec.n_seqs)), spec.min_len, spec.max_len)
+    lens = lens.astype(np.int64)
+    offsets = np.zeros(spec.n_seqs + 1, np.int64)
+    np.cumsum(lens, out=offsets[1:])
+    total = int(offsets[-1])
+    if logq is None:
+        logq = make_logq()
+    V = n_codes
+    q = np.exp(logq[:V, :V].astype(np.float64))
+    keep, alias = _alias_tables(q / q.sum(axis=1, keepdims=True))
+    C = max(1, min(chains, total))
+    steps = (total + C - 1) // C
+    x = rng.integers(0, V, size=C)
+    out = np.empty((steps, C), np.int32)
+    for s in range(steps):
+        out[s] = x
+        c = rng.integers(0, V, size=C)
+        x = np.where(rng.random(C) < keep[x, c], c, alias[x, c])
+    tokens = np.ascontiguousarray(out.T).ravel()[:total].astype(np.int32)
+    return Corpus(tokens, offsets)
