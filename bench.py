@@ -40,6 +40,7 @@ def _parse():
     ap.add_argument("--replay-passes", type=int, default=20, help="passes of the per-class replay timing")
     ap.add_argument("--no-warm-replay", action="store_true", help="skip the cache-warm replay figures")
     ap.add_argument("--no-variants", action="store_true", help="skip the selection-variant figures")
+    ap.add_argument("--no-qest", action="store_true", help="skip the transition-table estimation figures")
     return ap.parse_args()
 
 
@@ -203,6 +204,66 @@ def cpu_baseline(wl, weights, logq, prompts, budget_s):
                       f"float64 numpy on {threads} BLAS threads of {len(os.sched_getaffinity(0))} visible cores"}
 
 
+def bench_qest(torch, reps, cpu):
+    """Transition-table estimation over the LibriTTS-train-shaped corpus
+    (354,780 utterances, ~105 M tokens): zero the counts, count bigrams with
+    the end-of-utterance EOS pair, normalise to log Q (alpha = 1).  HIP events
+    on the stream the kernels run on."""
+    from paper_2410_13839_amd.binding import MTP_Q_COUNT_EOS, mtp_q_count, mtp_q_normalize, mtp_q_workspace_size
+    from paper_2410_13839_amd.workloads import CORPORA, EOS_ID, VOCAB, make_corpus
+    cp = make_corpus(CORPORA["libritts_train"])
+    n_tok, n_seq, V = int(cp.tokens.size), int(cp.offsets.size - 1), VOCAB
+    print(f"[bench] q estimation: {n_tok} tokens in {n_seq} utterances", file=sys.stderr, flush=True)
+    t = torch.from_numpy(cp.tokens).cuda()
+    o = torch.from_numpy(cp.offsets).cuda()
+    counts = torch.empty((V, V), dtype=torch.int32, device="cuda")
+    status = torch.empty(3, dtype=torch.int64, device="cuda")
+    ws_bytes = mtp_q_workspace_size(n_tok, n_seq, V)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+    logq = torch.empty((V, V), dtype=torch.float32, device="cuda")
+    st = torch.cuda.current_stream()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(reps + 1)]
+    for r in range(reps + 1):                       # pass 0 is a warm-up
+        e = ev[r]
+        e[0].record(st)
+        counts.zero_()
+        status.zero_()
+        e[1].record(st)
+        mtp_q_count(t.data_ptr(), n_tok, o.data_ptr(), n_seq, V, EOS_ID, MTP_Q_COUNT_EOS, counts.data_ptr(),
+                    status.data_ptr(), ws.data_ptr(), ws_bytes, st.cuda_stream)
+        e[2].record(st)
+        mtp_q_normalize(counts.data_ptr(), V, 1.0, logq.data_ptr(), st.cuda_stream)
+        e[3].record(st)
+    torch.cuda.synchronize()
+    tot = np.mean([ev[r][0].elapsed_time(ev[r][3]) for r in range(1, reps + 1)]) * 1e3
+    cnt = np.mean([ev[r][1].elapsed_time(ev[r][2]) for r in range(1, reps + 1)]) * 1e3
+    nrm = np.mean([ev[r][2].elapsed_time(ev[r][3]) for r in range(1, reps + 1)]) * 1e3
+    assert status.cpu().tolist() == [0, 0, 0]
+    count_bytes = n_tok * 4 + (n_seq + 1) * 8 + V * V * 4
+    out = {"corpus": "libritts_train (synthetic Markov chain of Q)", "tokens": n_tok, "utterances": n_seq,
+           "tokens_per_s": round(n_tok / (tot * 1e-6), 1), "us_total": round(tot, 2), "reps": reps,
+           "count_kernel_us": round(cnt, 2), "count_algorithmic_bytes": count_bytes,
+           "count_GB_s": round(count_bytes / (cnt * 1e-6) / 1e9, 1),
+           "count_bigrams_per_s": round((n_tok) / (cnt * 1e-6), 1),
+           "normalize_kernel_us": round(nrm, 2), "normalize_GB_s": round(2 * V * V * 4 / (nrm * 1e-6) / 1e9, 1),
+           "paper_context": "paper: the LibriTTS transition table takes 3 minutes (hardware and implementation unstated)"}
+    if cpu:
+        from oracle.qestimate import bigram_counts, log_q
+        n_s = 100000
+        sl = cp.offsets[:n_s + 1]
+        tk = cp.tokens[:int(sl[-1])]
+        t0 = time.perf_counter()
+        c, _, _ = bigram_counts(tk, sl, V, EOS_ID, True)
+        log_q(c, 1.0)
+        dt = time.perf_counter() - t0
+        out["cpu_baseline"] = {"value": round(tk.size / dt, 1), "unit": "tokens/s", "cores": 1, "kind": "oracle",
+                               "sample": f"first {n_s} utterances ({tk.size} tokens), counts + log Q"}
+    print(f"[bench] q estimation: {out}", file=sys.stderr, flush=True)
+    del t, o, counts, status, logq, ws
+    torch.cuda.empty_cache()
+    return out
+
+
 def main():
     args = _parse()
     if args.gpus != 1:
@@ -303,6 +364,10 @@ def main():
         del s2
         torch.cuda.empty_cache()
 
+    qest = None
+    if not args.no_qest:
+        qest = bench_qest(torch, 5, not args.no_cpu_baseline)
+
     if args.copy_probe:
         a = torch.empty(256 << 20, dtype=torch.uint8, device="cuda")
         b = torch.empty_like(a)
@@ -328,6 +393,7 @@ def main():
         "cpu_baseline": cpu,
         "selection_variants": variants,
         "secondary": secondary,
+        "q_estimation": qest,
         "paper_context": "paper reports 20.5 -> 4.5 ms/token (x4.56, VALL-E, 8 heads) on unstated inference hardware",
     }
     print(json.dumps(out))

@@ -270,6 +270,43 @@ int mtp_get_tokens(mtp_ctx* ctx, int32_t* tokens);
 #define MTP_KCLASS_SELECT      7   /* top_k, Viterbi lattice and accept       */
 int mtp_profile_replay(mtp_ctx* ctx, int kclass, int iters, int cold, double* avg_us);
 
+/* ---- Transition-table estimation (Sec. 3.3: Q is derived from the
+ * training corpus).  Context-free; all pointers are DEVICE pointers and the
+ * work is enqueued on `hip_stream` (a hipStream_t, NULL = the null stream)
+ * without host synchronisation.
+ *
+ * mtp_q_count adds bigram counts to counts (uint32 [vocab][vocab], row =
+ * previous token, caller-zeroed; uint32 arithmetic wraps past 2^32 - 1 per
+ * entry): for every utterance u = tokens[offsets[u] .. offsets[u+1]) (int32
+ * tokens, int64 offsets [n_seqs + 1]), each adjacent pair inside u, and with
+ * MTP_Q_COUNT_EOS also (last token of u, eos_id) for a non-empty u.  No pair
+ * spans two utterances.  Input errors are counted, not fatal: status (uint64
+ * [3], caller-zeroed, accumulated) gets in [0] the pairs skipped because an
+ * id is outside [0, vocab), in [1] the utterances skipped because
+ * 0 <= offsets[u] <= offsets[u+1] <= n_tokens does not hold, and in [2] one
+ * if the utterances overlap so that they hold more pairs than n_tokens (then
+ * nothing is counted).  workspace: device scratch of at least
+ * mtp_q_workspace_size bytes for the same sizes (about 4 bytes per token
+ * plus 60 MB for a 1025-token vocabulary), owned by the caller and not
+ * shared by calls in flight.  Sizes: 0 <= n_tokens < 2^31, n_seqs >= 0,
+ * 1 <= vocab <= 8192.  MTP_EINVAL for other sizes, eos_id outside
+ * [0, vocab), unknown flags or NULL pointers; MTP_ENOMEM if ws_bytes is too
+ * small; MTP_EHIP if a launch fails.  The counts are exact integer sums: the
+ * result does not depend on scheduling. */
+#define MTP_Q_COUNT_EOS 1
+int mtp_q_workspace_size(int64_t n_tokens, int64_t n_seqs, int vocab, uint64_t* bytes);
+int mtp_q_count(const int32_t* tokens, int64_t n_tokens, const int64_t* offsets, int64_t n_seqs,
+                int vocab, int eos_id, int flags, uint32_t* counts, uint64_t* status,
+                void* workspace, uint64_t ws_bytes, void* hip_stream);
+
+/* log Q from the counts: logq[i][j] = float32(log(counts[i][j] + alpha) -
+ * log(sum_j counts[i][j] + alpha * vocab)), evaluated in double (additive
+ * smoothing alpha >= 0; alpha = 0 gives -inf for unseen pairs); a row whose
+ * denominator is 0 is uniform, -log(vocab).  logq: float32 [vocab][vocab].
+ * MTP_EINVAL for NULL pointers, vocab outside 1..8192 or a negative or
+ * non-finite alpha. */
+int mtp_q_normalize(const uint32_t* counts, int vocab, float alpha, float* logq, void* hip_stream);
+
 /* Drops all sequence state (the next call must be mtp_prefill). */
 int mtp_reset(mtp_ctx* ctx);
 void mtp_destroy(mtp_ctx* ctx);

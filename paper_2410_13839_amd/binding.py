@@ -33,7 +33,9 @@ MTP_FLAG_NO_GRAPH = 1
 EXPORTED = ["mtp_query_sizes", "mtp_weight_offset", "mtp_create", "mtp_prefill", "mtp_decode_step",
             "mtp_decode_step_async", "mtp_get_logits", "mtp_get_lattice", "mtp_get_seq_state", "mtp_get_tokens",
             "mtp_profile_replay", "mtp_reset", "mtp_destroy", "mtp_last_error", "mtp_strerror",
-            "mtp_set_selection", "mtp_get_union_lattice", "mtp_set_sampling", "mtp_get_uniforms"]
+            "mtp_set_selection", "mtp_get_union_lattice", "mtp_set_sampling", "mtp_get_uniforms",
+            "mtp_q_workspace_size", "mtp_q_count", "mtp_q_normalize"]
+MTP_Q_COUNT_EOS = 1
 MTP_LATTICE_OWN, MTP_LATTICE_UNION = 0, 1
 MTP_SELECT_BEST, MTP_SELECT_SAMPLE = 0, 1
 
@@ -71,6 +73,11 @@ _lib.mtp_set_selection.argtypes = [_ctx, ctypes.c_int, ctypes.c_int]
 _lib.mtp_get_union_lattice.argtypes = [_ctx, _i32p, _i32p, _f32p, _f32p, _i32p, _i32p]
 _lib.mtp_set_sampling.argtypes = [_ctx, ctypes.c_int, ctypes.c_float, ctypes.c_uint64]
 _lib.mtp_get_uniforms.argtypes = [_ctx, _f32p]
+_lib.mtp_q_workspace_size.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int, _P(ctypes.c_uint64)]
+_lib.mtp_q_count.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int,
+                             ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                             ctypes.c_uint64, ctypes.c_void_p]
+_lib.mtp_q_normalize.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p]
 _lib.mtp_get_seq_state.argtypes = [_ctx, _i32p, _i32p, _i32p, _i32p]
 _lib.mtp_get_tokens.argtypes = [_ctx, _i32p]
 _lib.mtp_profile_replay.argtypes = [_ctx, ctypes.c_int, ctypes.c_int, ctypes.c_int, _P(ctypes.c_double)]
@@ -205,6 +212,53 @@ def mtp_profile_replay(ctx, kclass: int, iters: int, cold: bool = True) -> float
     us = ctypes.c_double()
     _check(_lib.mtp_profile_replay(ctx, kclass, iters, int(cold), ctypes.byref(us)), ctx, "mtp_profile_replay")
     return us.value
+
+
+def mtp_q_workspace_size(n_tokens: int, n_seqs: int, vocab: int) -> int:
+    out = ctypes.c_uint64()
+    _check(_lib.mtp_q_workspace_size(n_tokens, n_seqs, vocab, ctypes.byref(out)), None, "mtp_q_workspace_size")
+    return out.value
+
+
+def mtp_q_count(tokens: int, n_tokens: int, offsets: int, n_seqs: int, vocab: int, eos_id: int, flags: int,
+                counts: int, status: int, workspace: int, ws_bytes: int, stream: int) -> None:
+    """Device pointers as integers; see include/mtp.h."""
+    _check(_lib.mtp_q_count(ctypes.c_void_p(tokens or None), n_tokens, ctypes.c_void_p(offsets or None), n_seqs,
+                            vocab, eos_id, flags, ctypes.c_void_p(counts or None), ctypes.c_void_p(status or None),
+                            ctypes.c_void_p(workspace or None), ws_bytes, ctypes.c_void_p(stream or None)),
+           None, "mtp_q_count")
+
+
+def mtp_q_normalize(counts: int, vocab: int, alpha: float, logq: int, stream: int) -> None:
+    _check(_lib.mtp_q_normalize(ctypes.c_void_p(counts or None), vocab, alpha, ctypes.c_void_p(logq or None),
+                                ctypes.c_void_p(stream or None)), None, "mtp_q_normalize")
+
+
+def estimate_logq(tokens, offsets, vocab: int, eos_id: int, count_eos: bool, alpha: float, stream=None):
+    """Counts and log Q of a corpus held in device tensors (int32 tokens,
+    int64 offsets [n_seqs + 1]).  Allocates the outputs with torch and runs
+    mtp_q_count and mtp_q_normalize on `stream` (default: torch's current
+    stream).  Returns (counts as int32 bits of the uint32 counts [V, V],
+    log Q float32 [V, V], status int64 [3])."""
+    import torch
+    dev = tokens.device
+    assert tokens.dtype == torch.int32 and offsets.dtype == torch.int64 and tokens.is_cuda and offsets.is_cuda
+    st = stream if stream is not None else torch.cuda.current_stream(dev)
+    counts = torch.empty((vocab, vocab), dtype=torch.int32, device=dev)
+    logq = torch.empty((vocab, vocab), dtype=torch.float32, device=dev)
+    status = torch.empty(3, dtype=torch.int64, device=dev)
+    n_seqs = offsets.numel() - 1
+    ws_bytes = mtp_q_workspace_size(tokens.numel(), n_seqs, vocab)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    with torch.cuda.stream(st):
+        counts.zero_()
+        status.zero_()
+    mtp_q_count(tokens.data_ptr(), tokens.numel(), offsets.data_ptr(), n_seqs, vocab, eos_id,
+                MTP_Q_COUNT_EOS if count_eos else 0, counts.data_ptr(), status.data_ptr(), ws.data_ptr(), ws_bytes,
+                st.cuda_stream)
+    mtp_q_normalize(counts.data_ptr(), vocab, alpha, logq.data_ptr(), st.cuda_stream)
+    ws.record_stream(st)
+    return counts, logq, status
 
 
 def mtp_reset(ctx) -> None:

@@ -1,0 +1,376 @@
+// Transition-table estimation (paper Sec. 3.3: Q is derived from the
+// training corpus): bigram counts C[prev][next] over utterances (no pair
+// spans two utterances; optionally each non-empty utterance adds (last
+// token, EOS)), then log Q.
+//
+// Device-scope atomics run at only ~27 G/s on this part whatever the address
+// pattern, so one global atomic per pair (4 ms for LibriTTS' ~105 M tokens)
+// is replaced by a partition of the pairs by key range and workgroup-private
+// LDS histograms.  A key is prev * V + next; keys are split into buckets of
+// 2^15 consecutive keys (one bucket's histogram fills 128 KB of LDS).
+//
+//   q_bucket_count    utterance ranges per workgroup: validate, count each
+//                     range's pairs per bucket (LDS), row per workgroup;
+//   q_column_scan     per bucket: exclusive scan over workgroups (the
+//                     workgroups' write offsets inside the bucket), total;
+//   q_bucket_plan     bucket bases, slices of at most S keys per bucket,
+//                     overflow check (more pairs than tokens: nothing counted);
+//   q_bucket_scatter  the same pairs again, each key written to its bucket
+//                     at an LDS cursor (every range reads its tokens twice);
+//   q_slice_hist      one workgroup per slice: LDS histogram of its keys,
+//                     written whole to a partial row;
+//   q_reduce          per key: counts += the partials of its bucket's slices.
+// Only a few hundred global atomics remain (input-error tallies).  Every
+// count is an integer sum, so the result does not depend on scheduling.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "../../include/mtp.h"
+
+namespace mtp {
+namespace {
+
+constexpr int QB_LOG = 15;
+constexpr uint32_t QB_BIN = 1u << QB_LOG;       // keys per bucket
+constexpr int QB_MAX_NB = 2048;                 // buckets for vocab <= 8192
+constexpr int QB_MAX_WG = 4096;                 // utterance-range workgroups
+constexpr int QB_THREADS = 256;                 // count / scatter workgroups
+constexpr int QH_THREADS = 1024;                // histogram workgroups
+constexpr int QS_THREADS = 1024;                // scans
+
+struct QPlan {
+    int V, NB, NWG, upw;        // vocab, buckets, range workgroups, utterances per range
+    int64_t S;                  // keys per slice
+    int64_t max_slices;         // n_tokens / S + NB
+};
+
+struct QWs {
+    uint32_t* wg_cnt;           // [NWG][NB] counts, then write offsets within the bucket
+    uint32_t* b_cnt;            // [NB]
+    uint32_t* b_base;           // [NB + 1]
+    uint32_t* s_base;           // [NB + 1] first slice of each bucket
+    uint32_t* ctl;              // [0] 1 when the pairs exceed the key buffer
+    uint32_t* keys;             // [n_tokens]
+    uint32_t* part;             // [max_slices][QB_BIN]
+};
+
+struct QArgs {
+    const int32_t* tok; int64_t n_tokens;
+    const int64_t* off; int64_t n_seqs;
+    int eos; int count_eos;
+    uint32_t* counts;
+    unsigned long long* status;
+    QPlan p;
+    QWs w;
+};
+
+uint64_t align256(uint64_t x) { return (x + 255) & ~uint64_t(255); }
+
+QPlan make_plan(int64_t n_tokens, int64_t n_seqs, int V) {
+    QPlan p{};
+    p.V = V;
+    const uint64_t keys = (uint64_t)V * V;
+    p.NB = (int)((keys + QB_BIN - 1) >> QB_LOG);
+    int64_t nwg = (n_seqs + 15) / 16;
+    p.NWG = (int)(nwg < 1 ? 1 : nwg > QB_MAX_WG ? QB_MAX_WG : nwg);
+    p.upw = (int)((n_seqs + p.NWG - 1) / p.NWG);
+    const int64_t s = (n_tokens + 447) / 448;
+    p.S = s < 65536 ? 65536 : s;
+    p.max_slices = n_tokens / p.S + p.NB;
+    return p;
+}
+
+// Workspace carve-up; returns the bytes needed.
+uint64_t carve(const QPlan& p, int64_t n_tokens, char* base, QWs* w) {
+    uint64_t o = 0;
+    auto take = [&](uint64_t bytes) { char* r = base ? base + o : nullptr; o = align256(o + bytes); return r; };
+    QWs t{};
+    t.wg_cnt = (uint32_t*)take((uint64_t)p.NWG * p.NB * 4);
+    t.b_cnt = (uint32_t*)take((uint64_t)p.NB * 4);
+    t.b_base = (uint32_t*)take((uint64_t)(p.NB + 1) * 4);
+    t.s_base = (uint32_t*)take((uint64_t)(p.NB + 1) * 4);
+    t.ctl = (uint32_t*)take(16);
+    t.keys = (uint32_t*)take((uint64_t)(n_tokens > 0 ? n_tokens : 1) * 4);
+    t.part = (uint32_t*)take((uint64_t)p.max_slices * QB_BIN * 4);
+    if (w) *w = t;
+    return o;
+}
+
+// Every valid pair of workgroup `wg`'s utterance range, in a fixed order:
+// wave i of the workgroup takes the range's utterances i, i+4, ...; lane l
+// the pairs starting at positions start + l + 64 j.  Four positions per lane
+// are loaded together (clamped inside the utterance, so no load is
+// predicated) to keep enough reads in flight.  f(key) for each counted pair;
+// returns the (bad pairs, bad utterances) of this lane.
+template <typename F>
+__device__ __forceinline__ uint2 for_each_pair(const QArgs& a, int wg, F&& f) {
+    constexpr int U = 4;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t u0 = (int64_t)wg * a.p.upw;
+    int64_t u1 = u0 + a.p.upw;
+    if (u1 > a.n_seqs) u1 = a.n_seqs;
+    const uint32_t V = (uint32_t)a.p.V;
+    uint2 bad = {0u, 0u};
+    for (int64_t u = u0 + wave; u < u1; u += QB_THREADS / 64) {
+        const int64_t s = a.off[u], e = a.off[u + 1];
+        if (s < 0 || e < s || e > a.n_tokens) {
+            bad.y += lane == 0;
+            continue;
+        }
+        const int64_t pend = a.count_eos ? e : e - 1;       // pairs start at s .. pend-1
+        for (int64_t base = s; base < pend; base += 64 * U) {
+            int x[U], y[U];
+#pragma unroll
+            for (int j = 0; j < U; ++j) {
+                const int64_t pos = base + lane + 64 * j;
+                const int64_t p0 = pos < e - 1 ? pos : e - 1;
+                const int64_t p1 = pos + 1 < e - 1 ? pos + 1 : e - 1;
+                x[j] = a.tok[p0];
+                y[j] = a.tok[p1];
+            }
+#pragma unroll
+            for (int j = 0; j < U; ++j) {
+                const int64_t pos = base + lane + 64 * j;
+                if (pos < pend) {
+                    const int yy = pos + 1 == e ? a.eos : y[j];
+                    if ((uint32_t)x[j] >= V || (uint32_t)yy >= V)
+                        ++bad.x;
+                    else
+                        f((uint32_t)x[j] * V + (uint32_t)yy);
+                }
+            }
+        }
+    }
+    return bad;
+}
+
+__global__ __launch_bounds__(QB_THREADS) void q_bucket_count_kernel(QArgs a) {
+    __shared__ uint32_t h[QB_MAX_NB];
+    const int wg = blockIdx.x, NB = a.p.NB;
+    for (int i = threadIdx.x; i < NB; i += QB_THREADS) h[i] = 0;
+    __syncthreads();
+    uint2 bad = for_each_pair(a, wg, [&](uint32_t key) { atomicAdd(&h[key >> QB_LOG], 1u); });
+    for (int o = 32; o >= 1; o >>= 1) {
+        bad.x += __shfl_xor(bad.x, o);
+        bad.y += __shfl_xor(bad.y, o);
+    }
+    if ((threadIdx.x & 63) == 0 && bad.x)
+        __hip_atomic_fetch_add(a.status, (unsigned long long)bad.x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if ((threadIdx.x & 63) == 0 && bad.y)
+        __hip_atomic_fetch_add(a.status + 1, (unsigned long long)bad.y, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __syncthreads();
+    uint32_t* row = a.w.wg_cnt + (size_t)wg * NB;
+    for (int i = threadIdx.x; i < NB; i += QB_THREADS) row[i] = h[i];
+}
+
+// Exclusive block scan of one value per thread (1024 threads); returns the
+// thread's exclusive prefix and sets *total.
+__device__ __forceinline__ uint32_t block_scan_excl(uint32_t v, uint32_t* s_w, uint32_t* total) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    uint32_t x = v;
+    for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t y = __shfl_up(x, o);
+        if (lane >= o) x += y;
+    }
+    if (lane == 63) s_w[wave] = x;
+    __syncthreads();
+    if (wave == 0) {
+        uint32_t t = lane < QS_THREADS / 64 ? s_w[lane] : 0u;
+        for (int o = 1; o < 64; o <<= 1) {
+            const uint32_t y = __shfl_up(t, o);
+            if (lane >= o) t += y;
+        }
+        if (lane < QS_THREADS / 64) s_w[lane] = t;     // inclusive wave totals
+    }
+    __syncthreads();
+    const uint32_t before = wave ? s_w[wave - 1] : 0u;
+    *total = s_w[QS_THREADS / 64 - 1];
+    __syncthreads();
+    return before + x - v;
+}
+
+// One workgroup per bucket: prefix over the range workgroups.
+__global__ __launch_bounds__(QS_THREADS) void q_column_scan_kernel(QArgs a) {
+    __shared__ uint32_t s_w[QS_THREADS / 64];
+    const int b = blockIdx.x, NB = a.p.NB, NWG = a.p.NWG;
+    uint32_t carry = 0;
+    for (int w0 = 0; w0 < NWG; w0 += QS_THREADS) {
+        const int w = w0 + threadIdx.x;
+        uint32_t* cell = a.w.wg_cnt + (size_t)w * NB + b;
+        const uint32_t v = w < NWG ? *cell : 0u;
+        uint32_t tot;
+        const uint32_t ex = block_scan_excl(v, s_w, &tot);
+        if (w < NWG) *cell = carry + ex;
+        carry += tot;
+    }
+    if (threadIdx.x == 0) a.w.b_cnt[b] = carry;
+}
+
+// One workgroup: bucket bases, slice bases, overflow flag.
+__global__ __launch_bounds__(QS_THREADS) void q_bucket_plan_kernel(QArgs a) {
+    __shared__ uint32_t s_w[QS_THREADS / 64];
+    const int NB = a.p.NB;
+    uint64_t carry = 0, scarry = 0;
+    for (int b0 = 0; b0 < NB; b0 += QS_THREADS) {
+        const int b = b0 + threadIdx.x;
+        const uint32_t c = b < NB ? a.w.b_cnt[b] : 0u;
+        const uint32_t ns = (uint32_t)((c + a.p.S - 1) / a.p.S);
+        uint32_t tot, stot;
+        const uint32_t ex = block_scan_excl(c, s_w, &tot);
+        const uint32_t sex = block_scan_excl(ns, s_w, &stot);
+        if (b < NB) {
+            a.w.b_base[b] = (uint32_t)(carry + ex);
+            a.w.s_base[b] = (uint32_t)(scarry + sex);
+        }
+        carry += tot;
+        scarry += stot;
+    }
+    if (threadIdx.x == 0) {
+        a.w.b_base[NB] = (uint32_t)carry;
+        a.w.s_base[NB] = (uint32_t)scarry;
+        const bool over = carry > (uint64_t)a.n_tokens || scarry > (uint64_t)a.p.max_slices;
+        a.w.ctl[0] = over ? 1u : 0u;
+        if (over)
+            __hip_atomic_fetch_add(a.status + 2, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
+__global__ __launch_bounds__(QB_THREADS) void q_bucket_scatter_kernel(QArgs a) {
+    __shared__ uint32_t cur[QB_MAX_NB];
+    if (a.w.ctl[0]) return;
+    const int wg = blockIdx.x, NB = a.p.NB;
+    const uint32_t* row = a.w.wg_cnt + (size_t)wg * NB;
+    for (int i = threadIdx.x; i < NB; i += QB_THREADS) cur[i] = a.w.b_base[i] + row[i];
+    __syncthreads();
+    uint32_t* keys = a.w.keys;
+    (void)for_each_pair(a, wg, [&](uint32_t key) { keys[atomicAdd(&cur[key >> QB_LOG], 1u)] = key; });
+}
+
+__global__ __launch_bounds__(QH_THREADS) void q_slice_hist_kernel(QArgs a) {
+    extern __shared__ uint32_t hist[];            // QB_BIN entries
+    if (a.w.ctl[0]) return;
+    const int s = blockIdx.x, NB = a.p.NB;
+    if ((uint32_t)s >= a.w.s_base[NB]) return;
+    // the bucket holding slice s: the last b with s_base[b] <= s
+    int lo = 0, hi = NB;                          // s_base[lo] <= s < s_base[hi]
+    while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (a.w.s_base[mid] <= (uint32_t)s) lo = mid; else hi = mid;
+    }
+    const int b = lo;
+    const uint64_t k0 = a.w.b_base[b] + (uint64_t)(s - a.w.s_base[b]) * a.p.S;
+    uint64_t k1 = k0 + a.p.S;
+    if (k1 > a.w.b_base[b + 1]) k1 = a.w.b_base[b + 1];
+    const uint4 z = {0u, 0u, 0u, 0u};
+    for (uint32_t i = threadIdx.x; i < QB_BIN / 4; i += QH_THREADS) reinterpret_cast<uint4*>(hist)[i] = z;
+    __syncthreads();
+    const uint32_t* keys = a.w.keys;
+    constexpr int U = 8;                          // loads in flight per thread
+    for (uint64_t k = k0 + threadIdx.x; k < k1; k += (uint64_t)QH_THREADS * U) {
+        uint32_t v[U];
+#pragma unroll
+        for (int j = 0; j < U; ++j) {
+            const uint64_t kk = k + (uint64_t)j * QH_THREADS;
+            v[j] = keys[kk < k1 ? kk : k1 - 1];
+        }
+#pragma unroll
+        for (int j = 0; j < U; ++j)
+            if (k + (uint64_t)j * QH_THREADS < k1) atomicAdd(&hist[v[j] & (QB_BIN - 1)], 1u);
+    }
+    __syncthreads();
+    uint4* out = reinterpret_cast<uint4*>(a.w.part + (size_t)s * QB_BIN);
+    for (uint32_t i = threadIdx.x; i < QB_BIN / 4; i += QH_THREADS) out[i] = reinterpret_cast<const uint4*>(hist)[i];
+}
+
+__global__ __launch_bounds__(256) void q_reduce_kernel(QArgs a) {
+    if (a.w.ctl[0]) return;
+    const uint64_t nk = (uint64_t)a.p.V * a.p.V;
+    const uint64_t k = (uint64_t)blockIdx.x * 256 + threadIdx.x;
+    if (k >= nk) return;
+    const uint32_t b = (uint32_t)(k >> QB_LOG), bin = (uint32_t)(k & (QB_BIN - 1));
+    uint32_t sum = 0;
+    for (uint32_t s = a.w.s_base[b]; s < a.w.s_base[b + 1]; ++s) sum += a.w.part[(size_t)s * QB_BIN + bin];
+    if (sum) a.counts[k] += sum;
+}
+
+constexpr int QN_THREADS = 256;
+
+// One workgroup per row.
+__global__ __launch_bounds__(QN_THREADS) void q_normalize_kernel(const uint32_t* counts, int V, float alpha,
+                                                                 float* logq) {
+    __shared__ unsigned long long s_sum[QN_THREADS];
+    const int row = blockIdx.x, tid = threadIdx.x;
+    const uint32_t* cr = counts + (size_t)row * V;
+    unsigned long long s = 0;
+    for (int j = tid; j < V; j += QN_THREADS) s += cr[j];
+    s_sum[tid] = s;
+    __syncthreads();
+    for (int h = QN_THREADS / 2; h > 0; h >>= 1) {
+        if (tid < h) s_sum[tid] += s_sum[tid + h];
+        __syncthreads();
+    }
+    const double av = (double)alpha;
+    const double den = (double)s_sum[0] + av * (double)V;
+    float* out = logq + (size_t)row * V;
+    if (den == 0.0) {
+        const float uni = (float)(-log((double)V));
+        for (int j = tid; j < V; j += QN_THREADS) out[j] = uni;
+        return;
+    }
+    const double lden = log(den);
+    for (int j = tid; j < V; j += QN_THREADS) out[j] = (float)(log((double)cr[j] + av) - lden);
+}
+
+bool q_sizes_ok(int64_t n_tokens, int64_t n_seqs, int vocab) {
+    return n_tokens >= 0 && n_tokens < (int64_t(1) << 31) && n_seqs >= 0 && vocab >= 1 && vocab <= 8192;
+}
+
+}  // namespace
+}  // namespace mtp
+
+extern "C" {
+
+int mtp_q_workspace_size(int64_t n_tokens, int64_t n_seqs, int vocab, uint64_t* bytes) {
+    if (!bytes || !mtp::q_sizes_ok(n_tokens, n_seqs, vocab)) return MTP_EINVAL;
+    *bytes = mtp::carve(mtp::make_plan(n_tokens, n_seqs, vocab), n_tokens, nullptr, nullptr);
+    return MTP_OK;
+}
+
+int mtp_q_count(const int32_t* tokens, int64_t n_tokens, const int64_t* offsets, int64_t n_seqs, int vocab,
+                int eos_id, int flags, uint32_t* counts, uint64_t* status, void* workspace, uint64_t ws_bytes,
+                void* hip_stream) {
+    using namespace mtp;
+    if (!q_sizes_ok(n_tokens, n_seqs, vocab) || eos_id < 0 || eos_id >= vocab) return MTP_EINVAL;
+    if ((flags & ~MTP_Q_COUNT_EOS) != 0) return MTP_EINVAL;
+    if (!counts || !status || !offsets || !workspace || (n_tokens > 0 && !tokens)) return MTP_EINVAL;
+    const QPlan p = make_plan(n_tokens, n_seqs, vocab);
+    QWs w{};
+    if (carve(p, n_tokens, (char*)workspace, &w) > ws_bytes) return MTP_ENOMEM;
+    if (n_seqs == 0) return MTP_OK;
+    QArgs a{tokens, n_tokens, offsets, n_seqs, eos_id, (flags & MTP_Q_COUNT_EOS) ? 1 : 0, counts,
+            reinterpret_cast<unsigned long long*>(status), p, w};
+    hipStream_t st = (hipStream_t)hip_stream;
+    hipLaunchKernelGGL(q_bucket_count_kernel, dim3(p.NWG), dim3(QB_THREADS), 0, st, a);
+    hipLaunchKernelGGL(q_column_scan_kernel, dim3(p.NB), dim3(QS_THREADS), 0, st, a);
+    hipLaunchKernelGGL(q_bucket_plan_kernel, dim3(1), dim3(QS_THREADS), 0, st, a);
+    hipLaunchKernelGGL(q_bucket_scatter_kernel, dim3(p.NWG), dim3(QB_THREADS), 0, st, a);
+    // 128 KB of dynamic LDS: raise the function's limit (per device, cheap)
+    if (hipFuncSetAttribute((const void*)q_slice_hist_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            QB_BIN * 4) != hipSuccess)
+        return MTP_EHIP;
+    hipLaunchKernelGGL(q_slice_hist_kernel, dim3((unsigned)p.max_slices), dim3(QH_THREADS), QB_BIN * 4, st, a);
+    const uint64_t nk = (uint64_t)vocab * vocab;
+    hipLaunchKernelGGL(q_reduce_kernel, dim3((unsigned)((nk + 255) / 256)), dim3(256), 0, st, a);
+    return hipGetLastError() == hipSuccess ? MTP_OK : MTP_EHIP;
+}
+
+int mtp_q_normalize(const uint32_t* counts, int vocab, float alpha, float* logq, void* hip_stream) {
+    if (!counts || !logq || vocab < 1 || vocab > 8192) return MTP_EINVAL;
+    if (!(alpha >= 0.f) || !isfinite(alpha)) return MTP_EINVAL;
+    hipLaunchKernelGGL(mtp::q_normalize_kernel, dim3(vocab), dim3(mtp::QN_THREADS), 0, (hipStream_t)hip_stream,
+                       counts, vocab, alpha, logq);
+    return hipGetLastError() == hipSuccess ? MTP_OK : MTP_EHIP;
+}
+
+}  // extern "C"

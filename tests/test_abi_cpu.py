@@ -193,3 +193,29 @@ def test_set_sampling_validates():
         assert e.value.code == b.MTP_ESTATE
     finally:
         b.mtp_destroy(ctx)
+
+
+def test_q_estimation_validates_before_gpu_work():
+    from paper_2410_13839_amd import binding as b
+    need = b.mtp_q_workspace_size(10, 2, 1025)
+    assert need >= 10 * 4 + 33 * (1 << 17)
+    assert b.mtp_q_workspace_size(10 ** 8, 350000, 1025) > 4 * 10 ** 8
+    ok = dict(tokens=256, n_tokens=10, offsets=512, n_seqs=2, vocab=1025, eos_id=1024, flags=0, counts=1024,
+              status=2048, workspace=4096, ws_bytes=need, stream=0)
+    for k, v in (("n_tokens", -1), ("n_tokens", 1 << 31), ("n_seqs", -1), ("vocab", 0), ("vocab", 8193),
+                 ("eos_id", 1025), ("eos_id", -1), ("flags", 2), ("counts", 0), ("status", 0), ("offsets", 0),
+                 ("tokens", 0), ("workspace", 0)):
+        with pytest.raises(b.MTPError) as e:
+            b.mtp_q_count(**{**ok, k: v})
+        assert e.value.code == b.MTP_EINVAL, (k, v)
+    with pytest.raises(b.MTPError) as e:
+        b.mtp_q_count(**{**ok, "ws_bytes": need - 1})
+    assert e.value.code == b.MTP_ENOMEM
+    b.mtp_q_count(**{**ok, "n_seqs": 0, "ws_bytes": b.mtp_q_workspace_size(10, 0, 1025)})   # nothing launched
+    for k, v in (("alpha", -1.0), ("alpha", float("nan")), ("alpha", float("inf")), ("vocab", 0), ("counts", 0),
+                 ("logq", 0)):
+        args = dict(counts=256, vocab=1025, alpha=1.0, logq=512, stream=0)
+        args[k] = v
+        with pytest.raises(b.MTPError) as e:
+            b.mtp_q_normalize(**args)
+        assert e.value.code == b.MTP_EINVAL, (k, v)
