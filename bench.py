@@ -41,6 +41,8 @@ def _parse():
     ap.add_argument("--no-warm-replay", action="store_true", help="skip the cache-warm replay figures")
     ap.add_argument("--no-variants", action="store_true", help="skip the selection-variant figures")
     ap.add_argument("--no-qest", action="store_true", help="skip the transition-table estimation figures")
+    ap.add_argument("--qest-only", action="store_true",
+                    help="only the transition-table estimation figures (one JSON line of them)")
     return ap.parse_args()
 
 
@@ -273,6 +275,10 @@ def main():
     import torch
     from paper_2410_13839_amd.binding import Session
     from paper_2410_13839_amd.workloads import WORKLOADS, make_logq, make_prompts, make_weights
+
+    if args.qest_only:
+        print(json.dumps(bench_qest(torch, 5, not args.no_cpu_baseline)))
+        return
 
     wl = WORKLOADS[args.workload]
     weights = make_weights(wl.model)

@@ -289,8 +289,9 @@ int mtp_profile_replay(mtp_ctx* ctx, int kclass, int iters, int cold, double* av
  * mtp_q_workspace_size bytes for the same sizes (about 4 bytes per token
  * plus 60 MB for a 1025-token vocabulary), owned by the caller and not
  * shared by calls in flight.  Sizes: 0 <= n_tokens < 2^31, n_seqs >= 0,
- * 1 <= vocab <= 8192.  MTP_EINVAL for other sizes, eos_id outside
- * [0, vocab), unknown flags or NULL pointers; MTP_ENOMEM if ws_bytes is too
+ * 1 <= vocab <= 8192; tokens 16-byte and workspace 256-byte aligned.
+ * MTP_EINVAL for other sizes or alignments, eos_id outside [0, vocab),
+ * unknown flags or NULL pointers; MTP_ENOMEM if ws_bytes is too
  * small; MTP_EHIP if a launch fails.  The counts are exact integer sums: the
  * result does not depend on scheduling. */
 #define MTP_Q_COUNT_EOS 1

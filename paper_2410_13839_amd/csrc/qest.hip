@@ -91,55 +91,135 @@ uint64_t carve(const QPlan& p, int64_t n_tokens, char* base, QWs* w) {
     t.b_base = (uint32_t*)take((uint64_t)(p.NB + 1) * 4);
     t.s_base = (uint32_t*)take((uint64_t)(p.NB + 1) * 4);
     t.ctl = (uint32_t*)take(16);
-    t.keys = (uint32_t*)take((uint64_t)(n_tokens > 0 ? n_tokens : 1) * 4);
+    const int64_t cap = (n_tokens + 3) / 4 * 4;   // whole 16-byte groups for the vector loads
+    t.keys = (uint32_t*)take((uint64_t)(cap > 0 ? cap : 4) * 4);
     t.part = (uint32_t*)take((uint64_t)p.max_slices * QB_BIN * 4);
     if (w) *w = t;
     return o;
 }
 
-// Every valid pair of workgroup `wg`'s utterance range, in a fixed order:
-// wave i of the workgroup takes the range's utterances i, i+4, ...; lane l
-// the pairs starting at positions start + l + 64 j.  Four positions per lane
-// are loaded together (clamped inside the utterance, so no load is
-// predicated) to keep enough reads in flight.  f(key) for each counted pair;
-// returns the (bad pairs, bad utterances) of this lane.
-template <typename F>
-__device__ __forceinline__ uint2 for_each_pair(const QArgs& a, int wg, F&& f) {
-    constexpr int U = 4;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int64_t u0 = (int64_t)wg * a.p.upw;
-    int64_t u1 = u0 + a.p.upw;
-    if (u1 > a.n_seqs) u1 = a.n_seqs;
+// The pairs of workgroup `wg`'s utterance range.  The range's offsets are
+// staged in LDS.  When they are valid and non-decreasing, the range is one
+// contiguous span of tokens; if the span is at most QB_FLAT positions, the
+// whole workgroup sweeps it in 16-byte aligned groups of four positions
+// (one vector load per group, the fifth token from the next lane), and an
+// LDS bitmap marks each utterance's last position, where the pair is
+// (last, EOS) or none.  Otherwise each wave walks whole utterances (wave i
+// takes utterances i, i+4, ...).  Positions are 32-bit (n_tokens < 2^31).
+// Both passes over a range make the same choice, so they see the same pairs.
+constexpr int QB_MAX_UPW = 256;
+constexpr int QB_FLAT = 65536;
+
+struct QLds {
+    int64_t off[QB_MAX_UPW + 1];
+    uint32_t last[QB_FLAT / 32];
+};
+
+struct QRange {
+    int64_t u0, u1;
+    bool staged, flat;
+    int32_t S0, S1;              // the span when flat
+};
+
+__device__ __forceinline__ bool pair_key(const QArgs& a, int x, int y, uint32_t* key) {
     const uint32_t V = (uint32_t)a.p.V;
+    if ((uint32_t)x >= V || (uint32_t)y >= V) return false;
+    *key = (uint32_t)x * V + (uint32_t)y;
+    return true;
+}
+
+// Stages the offsets, decides flat or not, builds the bitmap.  All threads
+// of the workgroup call it (it synchronises).
+__device__ QRange range_setup(const QArgs& a, int wg, QLds& L) {
+    const int tid = threadIdx.x;
+    QRange r{};
+    r.u0 = (int64_t)wg * a.p.upw;
+    r.u1 = r.u0 + a.p.upw < a.n_seqs ? r.u0 + a.p.upw : a.n_seqs;
+    const int nu = (int)(r.u1 - r.u0);
+    r.staged = a.p.upw <= QB_MAX_UPW;
+    if (nu <= 0 || !r.staged) return r;            // nu: uniform; no range or too many utterances to stage
+    for (int i = tid; i <= nu; i += QB_THREADS) L.off[i] = a.off[r.u0 + i];
+    __syncthreads();
+    bool ok = true;
+    for (int i = tid; i < nu; i += QB_THREADS) ok &= L.off[i] <= L.off[i + 1];
+    ok &= L.off[0] >= 0 && L.off[nu] <= a.n_tokens && L.off[nu] - L.off[0] <= QB_FLAT;
+    r.flat = __syncthreads_and(ok) != 0;
+    if (r.flat) {
+        r.S0 = (int32_t)L.off[0];
+        r.S1 = (int32_t)L.off[nu];
+        for (int i = tid; i < QB_FLAT / 32; i += QB_THREADS) L.last[i] = 0u;
+        __syncthreads();
+        for (int i = tid; i < nu; i += QB_THREADS) {
+            const int32_t e = (int32_t)L.off[i + 1];
+            if (e > (int32_t)L.off[i]) atomicOr(&L.last[(e - 1 - r.S0) >> 5], 1u << ((e - 1 - r.S0) & 31));
+        }
+        __syncthreads();
+    }
+    return r;
+}
+
+// The four positions g .. g+3 (g a multiple of 4; every lane of the wave
+// calls it): key[j] and bit j of the returned mask for each counted pair,
+// *bad += the pairs with an id outside [0, V).
+__device__ __forceinline__ uint32_t sweep_group(const QArgs& a, const QLds& L, const QRange& r, int32_t g,
+                                                uint32_t key[4], uint32_t* bad) {
+    const int32_t n = (int32_t)a.n_tokens;
+    const int32_t* tok = a.tok;
+    int t0 = 0, t1 = 0, t2 = 0, t3 = 0;
+    if (g + 4 <= n) {
+        const int4 v = *reinterpret_cast<const int4*>(tok + g);
+        t0 = v.x; t1 = v.y; t2 = v.z; t3 = v.w;
+    } else if (g < n) {
+        t0 = tok[g];
+        t1 = tok[min(g + 1, n - 1)];
+        t2 = tok[min(g + 2, n - 1)];
+        t3 = tok[min(g + 3, n - 1)];
+    }
+    int t4 = __shfl_down(t0, 1);
+    if ((threadIdx.x & 63) == 63) t4 = tok[min(g + 4, n - 1)];
+    const int t[5] = {t0, t1, t2, t3, t4};
+    uint32_t mask = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int32_t pos = g + j;
+        if (pos >= r.S0 && pos < r.S1) {
+            const int32_t q = pos - r.S0;
+            const bool last = (L.last[q >> 5] >> (q & 31)) & 1u;
+            if (!last || a.count_eos) {
+                if (pair_key(a, t[j], last ? a.eos : t[j + 1], &key[j]))
+                    mask |= 1u << j;
+                else
+                    ++*bad;
+            }
+        }
+    }
+    return mask;
+}
+
+// The range's pairs utterance by utterance (the range is not flat): f(key)
+// per counted pair; returns this lane's (bad pairs, bad utterances).
+template <typename F>
+__device__ __forceinline__ uint2 per_utterance(const QArgs& a, const QLds& L, const QRange& r, F&& f) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int32_t* tok = a.tok;
     uint2 bad = {0u, 0u};
-    for (int64_t u = u0 + wave; u < u1; u += QB_THREADS / 64) {
-        const int64_t s = a.off[u], e = a.off[u + 1];
-        if (s < 0 || e < s || e > a.n_tokens) {
+    for (int64_t u = r.u0 + wave; u < r.u1; u += QB_THREADS / 64) {
+        const int64_t s64 = r.staged ? L.off[u - r.u0] : a.off[u];
+        const int64_t e64 = r.staged ? L.off[u - r.u0 + 1] : a.off[u + 1];
+        if (s64 < 0 || e64 < s64 || e64 > a.n_tokens) {
             bad.y += lane == 0;
             continue;
         }
-        const int64_t pend = a.count_eos ? e : e - 1;       // pairs start at s .. pend-1
-        for (int64_t base = s; base < pend; base += 64 * U) {
-            int x[U], y[U];
-#pragma unroll
-            for (int j = 0; j < U; ++j) {
-                const int64_t pos = base + lane + 64 * j;
-                const int64_t p0 = pos < e - 1 ? pos : e - 1;
-                const int64_t p1 = pos + 1 < e - 1 ? pos + 1 : e - 1;
-                x[j] = a.tok[p0];
-                y[j] = a.tok[p1];
-            }
-#pragma unroll
-            for (int j = 0; j < U; ++j) {
-                const int64_t pos = base + lane + 64 * j;
-                if (pos < pend) {
-                    const int yy = pos + 1 == e ? a.eos : y[j];
-                    if ((uint32_t)x[j] >= V || (uint32_t)yy >= V)
-                        ++bad.x;
-                    else
-                        f((uint32_t)x[j] * V + (uint32_t)yy);
-                }
-            }
+        const int32_t S = (int32_t)s64, E = (int32_t)e64;
+        const int32_t pend = a.count_eos ? E : E - 1;       // pairs start at S .. pend-1
+        for (int32_t pos = S + lane; pos < pend; pos += 64) {
+            const int x = tok[pos];
+            const int y = pos + 1 == E ? a.eos : tok[min(pos + 1, E - 1)];
+            uint32_t key;
+            if (pair_key(a, x, y, &key))
+                f(key);
+            else
+                ++bad.x;
         }
     }
     return bad;
@@ -147,10 +227,23 @@ __device__ __forceinline__ uint2 for_each_pair(const QArgs& a, int wg, F&& f) {
 
 __global__ __launch_bounds__(QB_THREADS) void q_bucket_count_kernel(QArgs a) {
     __shared__ uint32_t h[QB_MAX_NB];
+    __shared__ QLds L;
     const int wg = blockIdx.x, NB = a.p.NB;
     for (int i = threadIdx.x; i < NB; i += QB_THREADS) h[i] = 0;
     __syncthreads();
-    uint2 bad = for_each_pair(a, wg, [&](uint32_t key) { atomicAdd(&h[key >> QB_LOG], 1u); });
+    const QRange r = range_setup(a, wg, L);
+    uint2 bad = {0u, 0u};
+    if (r.flat) {
+        for (int32_t g0 = r.S0 & ~3; g0 < r.S1; g0 += 4 * QB_THREADS) {
+            uint32_t key[4];
+            const uint32_t m = sweep_group(a, L, r, g0 + 4 * (int)threadIdx.x, key, &bad.x);
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if ((m >> j) & 1u) atomicAdd(&h[key[j] >> QB_LOG], 1u);
+        }
+    } else {
+        bad = per_utterance(a, L, r, [&](uint32_t key) { atomicAdd(&h[key >> QB_LOG], 1u); });
+    }
     for (int o = 32; o >= 1; o >>= 1) {
         bad.x += __shfl_xor(bad.x, o);
         bad.y += __shfl_xor(bad.y, o);
@@ -236,15 +329,81 @@ __global__ __launch_bounds__(QS_THREADS) void q_bucket_plan_kernel(QArgs a) {
     }
 }
 
+// Writes each pair's key into its bucket.  A flat range with at most 64
+// buckets is written in rounds of 2048 positions sorted by bucket in LDS
+// first (rank of a key inside its bucket by an LDS atomic, bases by a
+// one-wave scan), so every bucket gets one contiguous run per round; other
+// ranges write key by key at an LDS cursor.
+constexpr int QS_LOCAL_NB = 64;
+constexpr int QS_GROUPS = 2;                        // 4-position groups per thread per round
+
 __global__ __launch_bounds__(QB_THREADS) void q_bucket_scatter_kernel(QArgs a) {
     __shared__ uint32_t cur[QB_MAX_NB];
+    __shared__ QLds L;
+    __shared__ uint32_t s_sorted[QB_THREADS * 4 * QS_GROUPS];
+    __shared__ uint32_t s_cnt[QS_LOCAL_NB], s_lb[QS_LOCAL_NB + 1];
     if (a.w.ctl[0]) return;
-    const int wg = blockIdx.x, NB = a.p.NB;
+    const int wg = blockIdx.x, NB = a.p.NB, tid = threadIdx.x;
     const uint32_t* row = a.w.wg_cnt + (size_t)wg * NB;
-    for (int i = threadIdx.x; i < NB; i += QB_THREADS) cur[i] = a.w.b_base[i] + row[i];
+    for (int i = tid; i < NB; i += QB_THREADS) cur[i] = a.w.b_base[i] + row[i];
+    if (tid < QS_LOCAL_NB) s_cnt[tid] = 0;
     __syncthreads();
+    const QRange r = range_setup(a, wg, L);
     uint32_t* keys = a.w.keys;
-    (void)for_each_pair(a, wg, [&](uint32_t key) { keys[atomicAdd(&cur[key >> QB_LOG], 1u)] = key; });
+    if (!r.flat) {
+        (void)per_utterance(a, L, r, [&](uint32_t key) { keys[atomicAdd(&cur[key >> QB_LOG], 1u)] = key; });
+        return;
+    }
+    uint32_t dummy = 0;
+    if (NB > QS_LOCAL_NB) {
+        for (int32_t g0 = r.S0 & ~3; g0 < r.S1; g0 += 4 * QB_THREADS) {
+            uint32_t key[4];
+            const uint32_t m = sweep_group(a, L, r, g0 + 4 * tid, key, &dummy);
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if ((m >> j) & 1u) keys[atomicAdd(&cur[key[j] >> QB_LOG], 1u)] = key[j];
+        }
+        return;
+    }
+    for (int32_t g0 = r.S0 & ~3; g0 < r.S1; g0 += 4 * QB_THREADS * QS_GROUPS) {
+        uint32_t key[QS_GROUPS][4], rank[QS_GROUPS][4], m[QS_GROUPS];
+#pragma unroll
+        for (int q = 0; q < QS_GROUPS; ++q) {
+            m[q] = sweep_group(a, L, r, g0 + 4 * QB_THREADS * q + 4 * tid, key[q], &dummy);
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if ((m[q] >> j) & 1u) rank[q][j] = atomicAdd(&s_cnt[key[q][j] >> QB_LOG], 1u);
+        }
+        __syncthreads();
+        if (tid < 64) {                              // bases of this round's runs
+            const uint32_t c = tid < NB ? s_cnt[tid] : 0u;
+            uint32_t x = c;
+            for (int o = 1; o < 64; o <<= 1) {
+                const uint32_t y = __shfl_up(x, o);
+                if (tid >= o) x += y;
+            }
+            if (tid < NB) s_lb[tid] = x - c;
+            if (tid == 63) s_lb[QS_LOCAL_NB] = x;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int q = 0; q < QS_GROUPS; ++q)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if ((m[q] >> j) & 1u) s_sorted[s_lb[key[q][j] >> QB_LOG] + rank[q][j]] = key[q][j];
+        __syncthreads();
+        const uint32_t total = s_lb[QS_LOCAL_NB];
+        for (uint32_t i = tid; i < total; i += QB_THREADS) {
+            const uint32_t k = s_sorted[i], b = k >> QB_LOG;
+            keys[cur[b] + (i - s_lb[b])] = k;
+        }
+        __syncthreads();
+        if (tid < NB) {
+            cur[tid] += s_cnt[tid];
+            s_cnt[tid] = 0;
+        }
+        __syncthreads();
+    }
 }
 
 __global__ __launch_bounds__(QH_THREADS) void q_slice_hist_kernel(QArgs a) {
@@ -265,18 +424,25 @@ __global__ __launch_bounds__(QH_THREADS) void q_slice_hist_kernel(QArgs a) {
     const uint4 z = {0u, 0u, 0u, 0u};
     for (uint32_t i = threadIdx.x; i < QB_BIN / 4; i += QH_THREADS) reinterpret_cast<uint4*>(hist)[i] = z;
     __syncthreads();
-    const uint32_t* keys = a.w.keys;
-    constexpr int U = 8;                          // loads in flight per thread
-    for (uint64_t k = k0 + threadIdx.x; k < k1; k += (uint64_t)QH_THREADS * U) {
-        uint32_t v[U];
+    // aligned 16-byte loads over [k0 & ~3, k1): the key buffer is padded to a
+    // multiple of 4 keys, entries outside [k0, k1) are skipped
+    const uint32_t K0 = (uint32_t)k0, K1 = (uint32_t)k1;
+    constexpr int U = 4;                          // vector loads in flight per thread
+    for (uint32_t blk = (K0 & ~3u) + 4 * threadIdx.x; blk < K1; blk += 4 * QH_THREADS * U) {
+        uint4 v[U];
 #pragma unroll
         for (int j = 0; j < U; ++j) {
-            const uint64_t kk = k + (uint64_t)j * QH_THREADS;
-            v[j] = keys[kk < k1 ? kk : k1 - 1];
+            const uint32_t b4 = blk + 4 * QH_THREADS * j;
+            v[j] = *reinterpret_cast<const uint4*>(a.w.keys + (b4 < K1 ? b4 : blk));
         }
 #pragma unroll
-        for (int j = 0; j < U; ++j)
-            if (k + (uint64_t)j * QH_THREADS < k1) atomicAdd(&hist[v[j] & (QB_BIN - 1)], 1u);
+        for (int j = 0; j < U; ++j) {
+            const uint32_t b4 = blk + 4 * QH_THREADS * j;
+            const uint32_t kv[4] = {v[j].x, v[j].y, v[j].z, v[j].w};
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+                if (b4 + c >= K0 && b4 + c < K1) atomicAdd(&hist[kv[c] & (QB_BIN - 1)], 1u);
+        }
     }
     __syncthreads();
     uint4* out = reinterpret_cast<uint4*>(a.w.part + (size_t)s * QB_BIN);
@@ -344,6 +510,7 @@ int mtp_q_count(const int32_t* tokens, int64_t n_tokens, const int64_t* offsets,
     if (!q_sizes_ok(n_tokens, n_seqs, vocab) || eos_id < 0 || eos_id >= vocab) return MTP_EINVAL;
     if ((flags & ~MTP_Q_COUNT_EOS) != 0) return MTP_EINVAL;
     if (!counts || !status || !offsets || !workspace || (n_tokens > 0 && !tokens)) return MTP_EINVAL;
+    if (((uintptr_t)tokens & 15) != 0 || ((uintptr_t)workspace & 255) != 0) return MTP_EINVAL;
     const QPlan p = make_plan(n_tokens, n_seqs, vocab);
     QWs w{};
     if (carve(p, n_tokens, (char*)workspace, &w) > ws_bytes) return MTP_ENOMEM;

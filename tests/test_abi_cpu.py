@@ -204,7 +204,7 @@ def test_q_estimation_validates_before_gpu_work():
               status=2048, workspace=4096, ws_bytes=need, stream=0)
     for k, v in (("n_tokens", -1), ("n_tokens", 1 << 31), ("n_seqs", -1), ("vocab", 0), ("vocab", 8193),
                  ("eos_id", 1025), ("eos_id", -1), ("flags", 2), ("counts", 0), ("status", 0), ("offsets", 0),
-                 ("tokens", 0), ("workspace", 0)):
+                 ("tokens", 0), ("workspace", 0), ("tokens", 260), ("workspace", 4096 + 64)):
         with pytest.raises(b.MTPError) as e:
             b.mtp_q_count(**{**ok, k: v})
         assert e.value.code == b.MTP_EINVAL, (k, v)

@@ -74,6 +74,28 @@ def test_ragged_corpora_exact(count_eos, bad, V, alpha):
         assert status[0] > 0 and status[1] >= 2
 
 
+@pytest.mark.parametrize("case", ["wide_vocab", "long_utterances", "many_utterances"])
+def test_every_counting_path(case):
+    """The count paths: a vocabulary with more than 64 key buckets (keys
+    written one by one), utterance ranges whose spans exceed the LDS bitmap
+    (per-utterance walk), and more than a million utterances (offsets read
+    from memory)."""
+    rng = np.random.default_rng({"wide_vocab": 1, "long_utterances": 2, "many_utterances": 3}[case])
+    if case == "wide_vocab":
+        V = 2000
+        lens = rng.integers(0, 300, size=900)
+    elif case == "long_utterances":
+        V = VOCAB
+        lens = np.array([70000, 3, 0, 90001, 5, 66000])
+    else:
+        V = 64
+        lens = rng.integers(0, 3, size=1_050_000)
+    offs = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    toks = rng.integers(0, V - 1, size=int(offs[-1])).astype(np.int32)
+    for count_eos in (False, True):
+        _check(toks, offs, V, V - 1, count_eos, 1.0)
+
+
 def test_empty_corpora():
     for toks, offs in ((np.zeros(0, np.int32), np.zeros(1, np.int64)),
                        (np.zeros(0, np.int32), np.zeros(4, np.int64)),
