@@ -24,6 +24,9 @@ Prediction and Speculative Decoding", arXiv 2410.13839):
                    the Viterbi recursion must reproduce, and the enumerated
                    path distribution the sampler must draw from.
   generate.py   -- the AR loop: n tokens per step (Fig. 1b, Sec. 3.2).
+  nar.py        -- the NAR module (Sec. 3.1, Eq. 2): codec layers 2..8 in one
+                   bidirectional pass each, conditioned on the phonemes, the
+                   whole prompt and the known lower layers.  float64.
   qestimate.py  -- the transition table Q from a token corpus (Sec. 3.3):
                    bigram counts within utterances, row-normalised with
                    additive smoothing, log Q in float32.

@@ -46,10 +46,16 @@ class ModelShape:
     eos_id: int = EOS_ID
     n_phone: int = N_PHONE
     max_pos: int = MAX_POS
+    nar: bool = False    # NAR module: k_heads stages predict codec layers 2..k_heads+1
 
     @property
     def head_dim(self) -> int:
         return self.d_model // self.n_heads
+
+    @property
+    def codebook(self) -> int:
+        """Codes per codec layer (the vocabulary without EOS)."""
+        return self.vocab - 1
 
 
 @dataclass(frozen=True)
@@ -122,11 +128,16 @@ def bf16_bits(x: np.ndarray) -> np.ndarray:
 
 
 def weight_names(m: ModelShape) -> List[Tuple[str, Tuple[int, ...]]]:
-    """Ordered (name, shape) list; the order fixes each tensor's seed index."""
+    """Ordered (name, shape) list; the order fixes each tensor's seed index.
+
+    NAR models (m.nar) have one codebook table per codec layer (emb_codes,
+    [k_heads + 1, codebook, d]), one head per predicted layer (w_heads
+    [k_heads, codebook, d]) and one stage vector per predicted layer (stage
+    [k_heads, d]) instead of the AR's codec table and next-token heads."""
     d, f, v = m.d_model, m.d_ff, m.vocab
     out: List[Tuple[str, Tuple[int, ...]]] = [
         ("emb_phone", (m.n_phone, d)),
-        ("emb_ac", (v, d)),
+        ("emb_codes", (m.k_heads + 1, m.codebook, d)) if m.nar else ("emb_ac", (v, d)),
         ("pos", (m.max_pos, d)),
     ]
     for l in range(m.n_layers):
@@ -138,8 +149,11 @@ def weight_names(m: ModelShape) -> List[Tuple[str, Tuple[int, ...]]]:
             (f"l{l}.w_1", (f, d)), (f"l{l}.b_1", (f,)),
             (f"l{l}.w_2", (d, f)), (f"l{l}.b_2", (d,)),
         ]
+    hv = m.codebook if m.nar else v
     out += [("lnf_g", (d,)), ("lnf_b", (d,)),
-            ("w_heads", (m.k_heads, v, d)), ("b_heads", (m.k_heads, v))]
+            ("w_heads", (m.k_heads, hv, d)), ("b_heads", (m.k_heads, hv))]
+    if m.nar:
+        out += [("stage", (m.k_heads, d))]
     return out
 
 
@@ -305,3 +319,63 @@ def make_corpus(spec: CorpusSpec, logq: Optional[np.ndarray] = None, chains: int
         x = np.where(rng.random(C) < keep[x, c], c, alias[x, c])
     tokens = np.ascontiguousarray(out.T).ravel()[:total].astype(np.int32)
     return Corpus(tokens, offsets)
+
+
+# ---------------------------------------------------------------- NAR inputs
+# The NAR module (Eq. 2) completes codec layers 2..8 of the utterance the AR
+# module generated; its inputs are the phonemes, all 8 layers of the acoustic
+# prompt and the generated first layer.
+
+
+@dataclass(frozen=True)
+class NarWorkload:
+    name: str
+    model: ModelShape
+    batch: int
+    phon_len: Tuple[int, int]      # inclusive ranges
+    prompt_len: Tuple[int, int]
+    target_len: Tuple[int, int]
+    description: str = ""
+
+    @property
+    def max_seq(self) -> int:
+        return self.phon_len[1] + self.prompt_len[1] + self.target_len[1]
+
+
+_NAR_TINY = ModelShape(n_layers=2, d_model=256, n_heads=4, d_ff=1024, k_heads=7, dtype=DTYPE_F32, max_pos=512,
+                       nar=True)
+_NAR_VALLE = ModelShape(n_layers=12, d_model=1024, n_heads=16, d_ff=4096, k_heads=7, dtype=DTYPE_BF16, nar=True)
+
+NAR_WORKLOADS: Dict[str, NarWorkload] = {
+    "nar_tiny": NarWorkload("nar_tiny", _NAR_TINY, batch=3, phon_len=(0, 9), prompt_len=(6, 20),
+                            target_len=(1, 40), description="2L d256 H4 F1024 fp32, 7 stages, batch 3 ragged"),
+    "nar_valle": NarWorkload("nar_valle", _NAR_VALLE, batch=1, phon_len=(100, 100), prompt_len=(225, 225),
+                             target_len=(750, 750),
+                             description="12L d1024 H16 F4096 bf16, 7 stages, 100 phon + 225 prompt + 750 target"),
+    "nar_valle_b8": NarWorkload("nar_valle_b8", _NAR_VALLE, batch=8, phon_len=(50, 150), prompt_len=(150, 300),
+                                target_len=(300, 750),
+                                description="12L d1024 H16 F4096 bf16, 7 stages, batch 8 ragged"),
+}
+
+
+@dataclass
+class NarInputs:
+    phon: List[np.ndarray]     # per utterance int32 phoneme ids
+    prompt: List[np.ndarray]   # per utterance int32 [n_q, P] codes of every codec layer
+    a1: List[np.ndarray]       # per utterance int32 [T] first-layer codes to complete
+
+
+def make_nar_inputs(wl: NarWorkload, seed_base: int = 300) -> NarInputs:
+    """Uniform ids: phonemes over 0..511, codes over 0..codebook-1; lengths
+    uniform over the inclusive ranges; utterance b uses seed seed_base + b."""
+    m = wl.model
+    phon, prompt, a1 = [], [], []
+    for b in range(wl.batch):
+        rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed_base + b])))
+        lp = int(rng.integers(wl.phon_len[0], wl.phon_len[1] + 1))
+        lq = int(rng.integers(wl.prompt_len[0], wl.prompt_len[1] + 1))
+        lt = int(rng.integers(wl.target_len[0], wl.target_len[1] + 1))
+        phon.append(rng.integers(0, m.n_phone, size=lp).astype(np.int32))
+        prompt.append(rng.integers(0, m.codebook, size=(m.k_heads + 1, lq)).astype(np.int32))
+        a1.append(rng.integers(0, m.codebook, size=lt).astype(np.int32))
+    return NarInputs(phon, prompt, a1)
