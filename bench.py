@@ -41,6 +41,8 @@ def _parse():
     ap.add_argument("--no-warm-replay", action="store_true", help="skip the cache-warm replay figures")
     ap.add_argument("--no-variants", action="store_true", help="skip the selection-variant figures")
     ap.add_argument("--no-qest", action="store_true", help="skip the transition-table estimation figures")
+    ap.add_argument("--no-nar", action="store_true", help="skip the NAR module figures")
+    ap.add_argument("--nar-only", action="store_true", help="only the NAR module figures (one JSON line of them)")
     ap.add_argument("--qest-only", action="store_true",
                     help="only the transition-table estimation figures (one JSON line of them)")
     return ap.parse_args()
@@ -266,6 +268,65 @@ def bench_qest(torch, reps, cpu):
     return out
 
 
+def nar_flops(wl, inp):
+    """Algorithmic flops of one NAR forward (all stages): the GEMMs (QKV,
+    out-projection, FFN, the stage head) and the attention products
+    (2 * 2 * len^2 * d per layer and utterance, bidirectional)."""
+    m = wl.model
+    d, F, cb = m.d_model, m.d_ff, m.codebook
+    lens = [len(p) + q.shape[1] + len(a) for p, q, a in zip(inp.phon, inp.prompt, inp.a1)]
+    rows = sum(lens)
+    per_layer = 2 * rows * (3 * d * d + d * d + 2 * d * F) + sum(4 * L * L * d for L in lens)
+    return m.k_heads * (m.n_layers * per_layer + 2 * rows * d * cb)
+
+
+def bench_nar(torch, reps, cpu):
+    """NAR module (codec layers 2..8) on the VALL-E-shaped bf16 model: one
+    utterance of 100 phonemes + 225 prompt + 750 target rows, and a ragged
+    batch of 8.  HIP events around mtp_nar_run on the session's stream."""
+    from paper_2410_13839_amd.binding import NarSession
+    from paper_2410_13839_amd.workloads import NAR_WORKLOADS, make_nar_inputs, make_weights
+    out = {}
+    w = make_weights(NAR_WORKLOADS["nar_valle"].model)
+    for name in ("nar_valle", "nar_valle_b8"):
+        wl = NAR_WORKLOADS[name]
+        inp = make_nar_inputs(wl)
+        s = NarSession(wl.model, w, max_batch=wl.batch, max_seq=wl.max_seq)
+        s.prepare(inp.phon, inp.prompt, inp.a1)
+        s.run()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(s.stream)
+        for _ in range(reps):
+            s.run()
+        e1.record(s.stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        fl = nar_flops(wl, inp)
+        n_codes = wl.model.k_heads * sum(len(a) for a in inp.a1)
+        out[name] = {"workload": wl.description, "ms_per_forward": round(ms, 3), "reps": reps,
+                     "codes_per_s": round(n_codes / (ms * 1e-3), 1),
+                     "tflops": round(fl / (ms * 1e-3) / 1e12, 1), "flops_per_forward": fl,
+                     "mfma_frac_bf16": round(fl / (ms * 1e-3) / 2.5e15, 3)}
+        print(f"[bench] {name}: {out[name]}", file=sys.stderr, flush=True)
+        s.close()
+        del s
+        torch.cuda.empty_cache()
+    if cpu:
+        from oracle.nar import NARModel
+        wl = NAR_WORKLOADS["nar_valle"]
+        inp = make_nar_inputs(wl)
+        m = NARModel(wl.model, w)
+        teacher = np.vstack([inp.a1[0][None], np.zeros((wl.model.k_heads, len(inp.a1[0])), np.int64)])
+        import os as _os
+        t0 = time.perf_counter()
+        m.forward(m.embed(2, inp.phon[0], inp.prompt[0], teacher))
+        dt = time.perf_counter() - t0
+        out["cpu_baseline"] = {"value": round(len(inp.a1[0]) / dt, 1), "unit": "codes/s", "kind": "oracle",
+                               "cores": _os.cpu_count(), "sample": "one stage (layer 2) of nar_valle, float64"}
+    return out
+
+
 def main():
     args = _parse()
     if args.gpus != 1:
@@ -278,6 +339,9 @@ def main():
 
     if args.qest_only:
         print(json.dumps(bench_qest(torch, 5, not args.no_cpu_baseline)))
+        return
+    if args.nar_only:
+        print(json.dumps(bench_nar(torch, 3, not args.no_cpu_baseline)))
         return
 
     wl = WORKLOADS[args.workload]
@@ -373,6 +437,9 @@ def main():
     qest = None
     if not args.no_qest:
         qest = bench_qest(torch, 5, not args.no_cpu_baseline)
+    nar = None
+    if not args.no_nar:
+        nar = bench_nar(torch, 3, not args.no_cpu_baseline)
 
     if args.copy_probe:
         a = torch.empty(256 << 20, dtype=torch.uint8, device="cuda")
@@ -400,6 +467,7 @@ def main():
         "selection_variants": variants,
         "secondary": secondary,
         "q_estimation": qest,
+        "nar": nar,
         "paper_context": "paper reports 20.5 -> 4.5 ms/token (x4.56, VALL-E, 8 heads) on unstated inference hardware",
     }
     print(json.dumps(out))

@@ -53,6 +53,7 @@ extern "C" {
 
 /* ---- flags -------------------------------------------------------------- */
 #define MTP_FLAG_NO_GRAPH  1   /* launch the decode step eagerly (no hipGraph replay) */
+#define MTP_FLAG_NAR       2   /* the context holds the NAR module (mtp_nar_*), not the AR decoder */
 
 /* Model and capacity description.  Head dimension is fixed at 64
  * (d_model / n_heads == 64). */
@@ -128,8 +129,19 @@ enum mtp_tensor {
     MTP_T_LNF_B,          /* [d]                           */
     MTP_T_W_HEADS,        /* [k_heads][vocab][d]           */
     MTP_T_B_HEADS,        /* [k_heads][vocab]              */
+    MTP_T_STAGE,          /* [k_heads][d] float32, NAR only (0 elements otherwise) */
     MTP_T_COUNT
 };
+
+/* NAR module (MTP_FLAG_NAR; Sec. 3.1, Eq. 2): the same config fields with
+ * these meanings.  n_q = k_heads + 1 codec layers (k_heads <= 7), vocab - 1
+ * codes per layer (vocab counts one extra entry, as for the AR's EOS; it is
+ * not used).  EMB_AC holds the n_q codebook tables, [n_q][vocab - 1][d];
+ * W_HEADS [k_heads][vocab - 1][d] and B_HEADS [k_heads][vocab - 1] are the
+ * heads of layers 2..n_q; STAGE [k_heads][d] their stage vectors.
+ * max_prompt bounds phonemes + prompt + target per utterance; max_new,
+ * eos_min and topk_max are unused (they must still be valid); log Q is not
+ * used (logq_bytes is 0 and buffers.logq may be NULL). */
 
 typedef struct mtp_ctx mtp_ctx;
 
@@ -307,6 +319,35 @@ int mtp_q_count(const int32_t* tokens, int64_t n_tokens, const int64_t* offsets,
  * MTP_EINVAL for NULL pointers, vocab outside 1..8192 or a negative or
  * non-finite alpha. */
 int mtp_q_normalize(const uint32_t* counts, int vocab, float alpha, float* logq, void* hip_stream);
+
+/* ---- NAR module (context created with MTP_FLAG_NAR) ---------------------
+ * For stage j = 2..n_q the trunk runs over each utterance's rows [phonemes;
+ * prompt; target] with BIDIRECTIONAL attention (every row sees its whole
+ * utterance).  Row inputs: phoneme rows the phoneme table; prompt rows the
+ * sum of all n_q codebook tables at the prompt's codes; target rows the sum
+ * of tables 1..j-1 at the known codes; every row adds its position (one
+ * running index) and the stage vector of j.  After the final LayerNorm,
+ * head j - 2 gives the target rows' logits over the vocab - 1 codes and
+ * layer j is their argmax (lowest code on ties).
+ *
+ * mtp_nar_prepare (host arrays, copied; synchronises): B utterances with
+ * phon (ids < n_phone) and phon_len[B]; prompt codes, per utterance an
+ * [n_q][prompt_len[b]] block (layer-major), blocks concatenated; a1, the
+ * first-layer codes of the targets, target_len[B], concatenated; codes <
+ * vocab - 1; 1 <= phon + prompt + target <= max_prompt per utterance.
+ * mtp_nar_run enqueues every stage on the context's stream (no host
+ * synchronisation).  mtp_nar_get_codes (synchronises): per utterance
+ * [k_heads][target_len[b]] (layers 2..n_q), concatenated.
+ * mtp_nar_get_logits (synchronises): float32 [sum target_len][vocab - 1],
+ * stage s = 0..k_heads-1 (layer s + 2), of the last run.
+ * MTP_EINVAL for bad arguments or an AR context, MTP_ENOMEM if the KV pool is
+ * too small, MTP_ESTATE for a run before a prepare or a get before a run. */
+int mtp_nar_prepare(mtp_ctx* ctx, int B, const int32_t* phon, const int32_t* phon_len,
+                    const int32_t* prompt, const int32_t* prompt_len,
+                    const int32_t* a1, const int32_t* target_len);
+int mtp_nar_run(mtp_ctx* ctx);
+int mtp_nar_get_codes(mtp_ctx* ctx, int32_t* codes);
+int mtp_nar_get_logits(mtp_ctx* ctx, int stage, float* logits);
 
 /* Drops all sequence state (the next call must be mtp_prefill). */
 int mtp_reset(mtp_ctx* ctx);

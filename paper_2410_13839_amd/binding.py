@@ -23,10 +23,10 @@ _lib = ctypes.CDLL(LIB_PATH)
 
 MTP_OK, MTP_EINVAL, MTP_ENOMEM, MTP_ESTATE, MTP_EHIP = 0, -1, -2, -3, -4
 MTP_DTYPE_F32, MTP_DTYPE_BF16 = 0, 1
-MTP_FLAG_NO_GRAPH = 1
+MTP_FLAG_NO_GRAPH, MTP_FLAG_NAR = 1, 2
 (MTP_T_EMB_PHONE, MTP_T_EMB_AC, MTP_T_POS, MTP_T_LN1_G, MTP_T_LN1_B, MTP_T_W_QKV, MTP_T_B_QKV, MTP_T_W_O,
  MTP_T_B_O, MTP_T_LN2_G, MTP_T_LN2_B, MTP_T_W_1, MTP_T_B_1, MTP_T_W_2, MTP_T_B_2, MTP_T_LNF_G, MTP_T_LNF_B,
- MTP_T_W_HEADS, MTP_T_B_HEADS, MTP_T_COUNT) = range(20)
+ MTP_T_W_HEADS, MTP_T_B_HEADS, MTP_T_STAGE, MTP_T_COUNT) = range(21)
 (MTP_KCLASS_GEMM_FFN1, MTP_KCLASS_GEMM_FFN2, MTP_KCLASS_GEMM_QKV, MTP_KCLASS_ATTENTION, MTP_KCLASS_HEADS,
  MTP_KCLASS_GEMM_OPROJ, MTP_KCLASS_SELECT) = 1, 2, 3, 4, 5, 6, 7
 
@@ -34,7 +34,8 @@ EXPORTED = ["mtp_query_sizes", "mtp_weight_offset", "mtp_create", "mtp_prefill",
             "mtp_decode_step_async", "mtp_get_logits", "mtp_get_lattice", "mtp_get_seq_state", "mtp_get_tokens",
             "mtp_profile_replay", "mtp_reset", "mtp_destroy", "mtp_last_error", "mtp_strerror",
             "mtp_set_selection", "mtp_get_union_lattice", "mtp_set_sampling", "mtp_get_uniforms",
-            "mtp_q_workspace_size", "mtp_q_count", "mtp_q_normalize"]
+            "mtp_q_workspace_size", "mtp_q_count", "mtp_q_normalize",
+            "mtp_nar_prepare", "mtp_nar_run", "mtp_nar_get_codes", "mtp_nar_get_logits"]
 MTP_Q_COUNT_EOS = 1
 MTP_LATTICE_OWN, MTP_LATTICE_UNION = 0, 1
 MTP_SELECT_BEST, MTP_SELECT_SAMPLE = 0, 1
@@ -78,6 +79,10 @@ _lib.mtp_q_count.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, c
                              ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                              ctypes.c_uint64, ctypes.c_void_p]
 _lib.mtp_q_normalize.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p]
+_lib.mtp_nar_prepare.argtypes = [_ctx, ctypes.c_int, _i32p, _i32p, _i32p, _i32p, _i32p, _i32p]
+_lib.mtp_nar_run.argtypes = [_ctx]
+_lib.mtp_nar_get_codes.argtypes = [_ctx, _i32p]
+_lib.mtp_nar_get_logits.argtypes = [_ctx, ctypes.c_int, _f32p]
 _lib.mtp_get_seq_state.argtypes = [_ctx, _i32p, _i32p, _i32p, _i32p]
 _lib.mtp_get_tokens.argtypes = [_ctx, _i32p]
 _lib.mtp_profile_replay.argtypes = [_ctx, ctypes.c_int, ctypes.c_int, ctypes.c_int, _P(ctypes.c_double)]
@@ -135,6 +140,40 @@ def mtp_prefill(ctx, phon: Sequence[np.ndarray], ac: Sequence[np.ndarray]) -> No
     pf, pfp = _i32(np.concatenate([np.asarray(p, np.int32) for p in phon]) if sum(pl) else np.zeros(1, np.int32))
     af, afp = _i32(np.concatenate([np.asarray(a, np.int32) for a in ac]))
     _check(_lib.mtp_prefill(ctx, B, pfp, plp, afp, alp), ctx, "mtp_prefill")
+
+
+def mtp_nar_prepare(ctx, phon: Sequence[np.ndarray], prompt: Sequence[np.ndarray], a1: Sequence[np.ndarray]) -> None:
+    """prompt[b]: [n_q, P_b] codes of every layer; a1[b]: [T_b] first-layer codes."""
+    B = len(a1)
+    pl, plp = _i32([len(p) for p in phon])
+    ql, qlp = _i32([np.asarray(q).shape[1] for q in prompt])
+    tl, tlp = _i32([len(a) for a in a1])
+    cat = lambda xs: np.concatenate([np.asarray(x, np.int32).reshape(-1) for x in xs]) if xs else np.zeros(1, np.int32)
+    pf, pfp = _i32(cat(phon) if sum(pl) else np.zeros(1, np.int32))
+    qf, qfp = _i32(cat(prompt) if sum(ql) else np.zeros(1, np.int32))
+    af, afp = _i32(cat(a1) if sum(tl) else np.zeros(1, np.int32))
+    _check(_lib.mtp_nar_prepare(ctx, B, pfp, plp, qfp, qlp, afp, tlp), ctx, "mtp_nar_prepare")
+
+
+def mtp_nar_run(ctx) -> None:
+    _check(_lib.mtp_nar_run(ctx), ctx, "mtp_nar_run")
+
+
+def mtp_nar_get_codes(ctx, k_heads: int, target_lens: Sequence[int]) -> List[np.ndarray]:
+    """Per utterance [k_heads, T_b]: the codes of layers 2..k_heads+1."""
+    out = np.zeros(max(1, k_heads * int(sum(target_lens))), np.int32)
+    _check(_lib.mtp_nar_get_codes(ctx, out.ctypes.data_as(_i32p)), ctx, "mtp_nar_get_codes")
+    res, o = [], 0
+    for t in target_lens:
+        res.append(out[o:o + k_heads * t].reshape(k_heads, t).copy())
+        o += k_heads * t
+    return res
+
+
+def mtp_nar_get_logits(ctx, stage: int, n_target: int, codebook: int) -> np.ndarray:
+    out = np.zeros((max(1, n_target), codebook), np.float32)
+    _check(_lib.mtp_nar_get_logits(ctx, stage, out.ctypes.data_as(_f32p)), ctx, "mtp_nar_get_logits")
+    return out[:n_target]
 
 
 def mtp_decode_step(ctx, B: int, K: int, top_k: int) -> Tuple[np.ndarray, np.ndarray]:
@@ -285,11 +324,13 @@ def make_config(shape, max_batch: int, max_prompt: int, max_new: int, eos_min: i
         vocab=shape.vocab, eos_id=shape.eos_id, n_phone=shape.n_phone, max_pos=shape.max_pos,
         k_heads=shape.k_heads, topk_max=topk_max, max_batch=max_batch, max_prompt=max_prompt,
         max_new=max_new, eos_min=eos_min, page_size=page_size, num_pages=num_pages,
-        dtype=MTP_DTYPE_BF16 if shape.dtype == "bf16" else MTP_DTYPE_F32, flags=flags)
+        dtype=MTP_DTYPE_BF16 if shape.dtype == "bf16" else MTP_DTYPE_F32,
+        flags=flags | (MTP_FLAG_NAR if getattr(shape, "nar", False) else 0))
 
 
-_TENSOR_OF = {"emb_phone": MTP_T_EMB_PHONE, "emb_ac": MTP_T_EMB_AC, "pos": MTP_T_POS,
-              "lnf_g": MTP_T_LNF_G, "lnf_b": MTP_T_LNF_B, "w_heads": MTP_T_W_HEADS, "b_heads": MTP_T_B_HEADS}
+_TENSOR_OF = {"emb_phone": MTP_T_EMB_PHONE, "emb_ac": MTP_T_EMB_AC, "emb_codes": MTP_T_EMB_AC, "pos": MTP_T_POS,
+              "lnf_g": MTP_T_LNF_G, "lnf_b": MTP_T_LNF_B, "w_heads": MTP_T_W_HEADS, "b_heads": MTP_T_B_HEADS,
+              "stage": MTP_T_STAGE}
 _LAYER_TENSOR_OF = {"ln1_g": MTP_T_LN1_G, "ln1_b": MTP_T_LN1_B, "w_qkv": MTP_T_W_QKV, "b_qkv": MTP_T_B_QKV,
                     "w_o": MTP_T_W_O, "b_o": MTP_T_B_O, "ln2_g": MTP_T_LN2_G, "ln2_b": MTP_T_LN2_B,
                     "w_1": MTP_T_W_1, "b_1": MTP_T_B_1, "w_2": MTP_T_W_2, "b_2": MTP_T_B_2}
@@ -393,6 +434,53 @@ class Session:
 
     def tokens(self) -> np.ndarray:
         return mtp_get_tokens(self.ctx, self.B, self.cfg.max_new)
+
+    def close(self) -> None:
+        if getattr(self, "ctx", None):
+            mtp_destroy(self.ctx)
+            self.ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class NarSession:
+    """Device buffers, stream and context of one NAR module (MTP_FLAG_NAR)."""
+
+    def __init__(self, shape, weights: Dict[str, np.ndarray], max_batch: int, max_seq: int, page_size: int = 16,
+                 flags: int = 0, device: str = "cuda:0", stream=None):
+        import torch
+        assert shape.nar
+        self.torch = torch
+        self.shape = shape
+        self.cfg = make_config(shape, max_batch, max_seq, 1, 1, 1, page_size, 0, flags)
+        sz = mtp_query_sizes(self.cfg)
+        self.sizes = sz
+        self.device = torch.device(device)
+        self.weights_dev = torch.from_numpy(pack_weights(self.cfg, weights)).to(self.device)
+        self.kv = torch.empty(int(sz.kv_bytes), dtype=torch.uint8, device=self.device)
+        self.ws = torch.empty(int(sz.workspace_bytes), dtype=torch.uint8, device=self.device)
+        self.stream = stream if stream is not None else torch.cuda.Stream(device=self.device)
+        torch.cuda.synchronize(self.device)
+        bufs = mtp_buffers(self.weights_dev.data_ptr(), None, self.kv.data_ptr(), self.ws.data_ptr())
+        self.ctx = mtp_create(self.cfg, bufs, self.stream.cuda_stream)
+        self.tlens: List[int] = []
+
+    def prepare(self, phon, prompt, a1) -> None:
+        mtp_nar_prepare(self.ctx, phon, prompt, a1)
+        self.tlens = [len(a) for a in a1]
+
+    def run(self) -> None:
+        mtp_nar_run(self.ctx)
+
+    def codes(self) -> List[np.ndarray]:
+        return mtp_nar_get_codes(self.ctx, self.cfg.k_heads, self.tlens)
+
+    def logits(self, stage: int) -> np.ndarray:
+        return mtp_nar_get_logits(self.ctx, stage, int(sum(self.tlens)), self.cfg.vocab - 1)
 
     def close(self) -> None:
         if getattr(self, "ctx", None):

@@ -34,11 +34,18 @@ bool is_matrix(int t) {
 }
 bool is_layer_tensor(int t) { return t >= MTP_T_LN1_G && t <= MTP_T_B_2; }
 
+bool is_nar(const mtp_config& c) { return (c.flags & MTP_FLAG_NAR) != 0; }
+
+// The NAR module has one codebook table per codec layer (k_heads + 1 of
+// them, vocab - 1 codes each), one head and one stage vector per predicted
+// layer; the AR decoder has one codec table (vocab entries) and no stage
+// vectors.
 uint64_t tensor_numel(const mtp_config& c, int t) {
     const uint64_t d = c.d_model, f = c.d_ff, v = c.vocab;
+    const uint64_t hv = is_nar(c) ? v - 1 : v;      // rows per head
     switch (t) {
     case MTP_T_EMB_PHONE: return (uint64_t)c.n_phone * d;
-    case MTP_T_EMB_AC: return v * d;
+    case MTP_T_EMB_AC: return is_nar(c) ? (uint64_t)(c.k_heads + 1) * (v - 1) * d : v * d;
     case MTP_T_POS: return (uint64_t)c.max_pos * d;
     case MTP_T_LN1_G: case MTP_T_LN1_B: case MTP_T_B_O: case MTP_T_LN2_G: case MTP_T_LN2_B: case MTP_T_B_2:
     case MTP_T_LNF_G: case MTP_T_LNF_B: return d;
@@ -48,8 +55,9 @@ uint64_t tensor_numel(const mtp_config& c, int t) {
     case MTP_T_W_1: return f * d;
     case MTP_T_B_1: return f;
     case MTP_T_W_2: return d * f;
-    case MTP_T_W_HEADS: return (uint64_t)c.k_heads * v * d;
-    case MTP_T_B_HEADS: return (uint64_t)c.k_heads * v;
+    case MTP_T_W_HEADS: return (uint64_t)c.k_heads * hv * d;
+    case MTP_T_B_HEADS: return (uint64_t)c.k_heads * hv;
+    case MTP_T_STAGE: return is_nar(c) ? (uint64_t)c.k_heads * d : 0;
     }
     return 0;
 }
@@ -85,7 +93,7 @@ uint64_t weight_layout(const mtp_config& c, std::vector<uint64_t>* glob, std::ve
             if (lay) (*lay)[(size_t)l * MTP_T_COUNT + t] = off;
             off = align256(off + tensor_bytes(c, t));
         }
-    for (int t = MTP_T_LNF_G; t <= MTP_T_B_HEADS; ++t) {
+    for (int t = MTP_T_LNF_G; t <= MTP_T_STAGE; ++t) {
         if (glob) (*glob)[t] = off;
         off = align256(off + tensor_bytes(c, t));
     }
@@ -112,12 +120,14 @@ int validate(const mtp_config* c, std::string* why) {
     if (c->page_size < 8 || c->page_size > 128 || (c->page_size & (c->page_size - 1))) return bad("page_size must be a power of two in 8..128");
     if (c->num_pages < 0) return bad("num_pages must be >= 0");
     if (c->dtype != MTP_DTYPE_F32 && c->dtype != MTP_DTYPE_BF16) return bad("unknown dtype");
+    if ((c->flags & ~(MTP_FLAG_NO_GRAPH | MTP_FLAG_NAR)) != 0) return bad("unknown flags");
+    if ((c->flags & MTP_FLAG_NAR) && c->k_heads > 7) return bad("a NAR module predicts at most 7 layers (k_heads <= 7)");
     return MTP_OK;
 }
 
 struct WsLayout {
     uint64_t rows, ids, tiles, last_row, state, btab, h, q, u, attn, ffn, part, apart, hz, z, logits, cand, ehat,
-        u_states, u_m, u_ehat, u_delta, u_psi, smp_cfg, smp_u,
+        u_states, u_m, u_ehat, u_delta, u_psi, smp_cfg, smp_u, codes, tgt_rows, nar_logits,
         delta, psi, slots, out_tok, out_cnt, hist, total;
     int64_t m_pre, m_dec, m_max, max_tiles, max_splits, maxp, num_pages;
     int act_bytes;
@@ -132,7 +142,7 @@ WsLayout ws_layout(const mtp_config& c) {
     w.m_dec = B * KH;
     w.m_max = std::max(w.m_pre, w.m_dec);
     w.max_tiles = w.m_pre / MTP_ATTN_QT + B + 1;
-    const int64_t max_ctx = (int64_t)c.max_prompt + c.max_new;
+    const int64_t max_ctx = (int64_t)c.max_prompt + (is_nar(c) ? 0 : c.max_new);
     w.max_splits = (max_ctx + 63) / 64;
     w.maxp = (max_ctx + c.page_size - 1) / c.page_size;
     w.num_pages = c.num_pages > 0 ? c.num_pages : B * w.maxp;
@@ -169,6 +179,10 @@ WsLayout ws_layout(const mtp_config& c) {
     w.out_tok = take(B * KH * 4);
     w.out_cnt = take(B * 4);
     w.hist = take(B * (int64_t)c.max_new * 4);
+    const bool nar = is_nar(c);
+    w.codes = take(nar ? w.m_pre * 8 * 4 : 0);                         // NAR: codec codes per row
+    w.tgt_rows = take(nar ? w.m_pre * 4 : 0);                         // NAR: rows of the target positions
+    w.nar_logits = take(nar ? (uint64_t)KH * w.m_pre * (V - 1) * 4 : 0);   // NAR: every stage's logits
     w.total = o;
     return w;
 }
@@ -197,6 +211,10 @@ struct mtp_ctx {
     SampleCfg h_smp{0, 1.0f, 0}; // copied to the workspace before the next step when dirty
     bool smp_dirty = true;
     int64_t plan_ctx = 0;        // longest prompt + budget of the batch (sizes the split plan)
+    // NAR module
+    bool nar_ready = false, nar_ran = false;
+    int nar_rows = 0, nar_tiles = 0;
+    std::vector<int32_t> h_codes, h_tgt, h_tlen;
     std::vector<int32_t> h_ids, h_last, h_btab;
     std::vector<RowInfo> h_rows;
     std::vector<int2> h_tiles;
@@ -349,7 +367,8 @@ int run_layer_fused(mtp_ctx* c, int l, int rows, int qt) {
 }
 
 // One trunk layer over `rows` rows whose row/tile metadata is already on the device.
-int run_layer(mtp_ctx* c, int l, int rows, int n_tiles, int qt, int split_len, int n_splits, bool decode) {
+int run_layer(mtp_ctx* c, int l, int rows, int n_tiles, int qt, int split_len, int n_splits, bool decode,
+              bool bidir = false) {
     const mtp_config& cf = c->cfg;
     const int d = cf.d_model, F = cf.d_ff, dt = cf.dtype;
     hipStream_t st = c->stream;
@@ -370,7 +389,7 @@ int run_layer(mtp_ctx* c, int l, int rows, int n_tiles, int qt, int split_len, i
         m.mode = 1; m.n_tiles = n_tiles; m.Q = 0; m.qt = 16; m.st = c->ws_ptr<SeqState>(c->ws.state);
         m.tiles = c->ws_ptr<int2>(c->ws.tiles); m.rows = c->ws_ptr<RowInfo>(c->ws.rows);
         m.q = c->ws_ptr<float>(c->ws.q); m.ldq = d; m.kv = c->kv(l); m.split_len = 1 << 30; m.n_splits = 1;
-        m.out = (bf16_t*)(c->WS() + c->ws.attn); m.ldo = d; m.part = nullptr;
+        m.out = (bf16_t*)(c->WS() + c->ws.attn); m.ldo = d; m.part = nullptr; m.bidir = bidir ? 1 : 0;
         HIPCHK(c, attention_mfma(st, m), "prefill attention");
     } else {
         AttnArgs a{};
@@ -378,6 +397,7 @@ int run_layer(mtp_ctx* c, int l, int rows, int n_tiles, int qt, int split_len, i
         a.tiles = c->ws_ptr<int2>(c->ws.tiles); a.n_tiles = n_tiles; a.qt = qt; a.kv = c->kv(l);
         a.split_len = split_len; a.n_splits = n_splits; a.out = c->WS() + c->ws.attn; a.ldo = d;
         a.part = c->ws_ptr<float>(c->ws.apart);
+        a.bidir = bidir ? 1 : 0; a.st = c->ws_ptr<SeqState>(c->ws.state);
         HIPCHK(c, attention(st, a), "attention");
     }
     // out projection -> partials, residual + LN2
@@ -603,7 +623,7 @@ int mtp_query_sizes(const mtp_config* cfg, mtp_sizes* out) {
     if (rc) return rc;
     WsLayout w = ws_layout(*cfg);
     out->weights_bytes = weight_layout(*cfg, nullptr, nullptr);
-    out->logq_bytes = (uint64_t)cfg->vocab * cfg->vocab * 4;
+    out->logq_bytes = is_nar(*cfg) ? 0 : (uint64_t)cfg->vocab * cfg->vocab * 4;
     out->kv_bytes = kv_bytes(*cfg, w);
     out->workspace_bytes = w.total;
     return MTP_OK;
@@ -632,7 +652,7 @@ int mtp_create(const mtp_config* cfg, const mtp_buffers* bufs, void* hip_stream,
     *out = nullptr;
     int rc = validate(cfg, nullptr);
     if (rc) return rc;
-    if (!bufs->weights || !bufs->logq || !bufs->kv_pool || !bufs->workspace) return MTP_EINVAL;
+    if (!bufs->weights || (!bufs->logq && !is_nar(*cfg)) || !bufs->kv_pool || !bufs->workspace) return MTP_EINVAL;
     auto aligned = [](const void* p) { return ((uintptr_t)p & 255) == 0; };
     if (!aligned(bufs->weights) || !aligned(bufs->logq) || !aligned(bufs->kv_pool) || !aligned(bufs->workspace))
         return MTP_EINVAL;
@@ -650,6 +670,7 @@ int mtp_create(const mtp_config* cfg, const mtp_buffers* bufs, void* hip_stream,
 int mtp_prefill(mtp_ctx* c, int B, const int32_t* phon, const int32_t* phon_len, const int32_t* ac,
                 const int32_t* ac_len) {
     if (!c) return MTP_EINVAL;
+    if (is_nar(c->cfg)) { c->err = "a NAR context has no AR prefill"; return MTP_EINVAL; }
     const mtp_config& cf = c->cfg;
     if (B < 1 || B > cf.max_batch) { c->err = "batch out of range"; return MTP_EINVAL; }
     if (!phon_len || !ac_len || !ac) { c->err = "NULL prompt array"; return MTP_EINVAL; }
@@ -837,6 +858,170 @@ int mtp_get_uniforms(mtp_ctx* c, float* u) {
     HIPCHK(c, hipMemcpyAsync(u, c->WS() + c->ws.smp_u, (size_t)c->B * MTP_MAX_HEADS_K * 4, hipMemcpyDeviceToHost, c->stream),
            "uniforms");
     HIPCHK(c, hipStreamSynchronize(c->stream), "sync");
+    return MTP_OK;
+}
+
+// ---------------------------------------------------------------- NAR module
+int mtp_nar_prepare(mtp_ctx* c, int B, const int32_t* phon, const int32_t* phon_len, const int32_t* prompt,
+                    const int32_t* prompt_len, const int32_t* a1, const int32_t* target_len) {
+    if (!c) return MTP_EINVAL;
+    const mtp_config& cf = c->cfg;
+    if (!is_nar(cf)) { c->err = "not a NAR context"; return MTP_EINVAL; }
+    if (B < 1 || B > cf.max_batch) { c->err = "batch out of range"; return MTP_EINVAL; }
+    if (!phon_len || !prompt_len || !target_len) { c->err = "NULL length array"; return MTP_EINVAL; }
+    const int nq = cf.k_heads + 1, cb = cf.vocab - 1;
+    int64_t n_ph = 0, n_pr = 0, n_tg = 0;
+    for (int b = 0; b < B; ++b) {
+        const int64_t len = (int64_t)phon_len[b] + prompt_len[b] + target_len[b];
+        if (phon_len[b] < 0 || prompt_len[b] < 0 || target_len[b] < 0 || len < 1 || len > cf.max_prompt) {
+            c->err = "utterance length out of range";
+            return MTP_EINVAL;
+        }
+        n_ph += phon_len[b];
+        n_pr += prompt_len[b];
+        n_tg += target_len[b];
+    }
+    if ((n_ph > 0 && !phon) || (n_pr > 0 && !prompt) || (n_tg > 0 && !a1)) { c->err = "NULL input array"; return MTP_EINVAL; }
+    for (int64_t i = 0; i < n_ph; ++i)
+        if (phon[i] < 0 || phon[i] >= cf.n_phone) { c->err = "phoneme id out of range"; return MTP_EINVAL; }
+    for (int64_t i = 0; i < n_pr * nq; ++i)
+        if (prompt[i] < 0 || prompt[i] >= cb) { c->err = "prompt code out of range"; return MTP_EINVAL; }
+    for (int64_t i = 0; i < n_tg; ++i)
+        if (a1[i] < 0 || a1[i] >= cb) { c->err = "target code out of range"; return MTP_EINVAL; }
+    const int64_t maxp = c->ws.maxp;
+    std::vector<int> need(B);
+    int64_t total_pages = 0;
+    for (int b = 0; b < B; ++b) {
+        need[b] = (int)((phon_len[b] + prompt_len[b] + (int64_t)target_len[b] + cf.page_size - 1) / cf.page_size);
+        total_pages += need[b];
+    }
+    if (total_pages > c->ws.num_pages) { c->err = "KV page pool exhausted"; return MTP_ENOMEM; }
+    c->h_btab.assign((size_t)B * maxp, 0);
+    int next = (int)c->ws.num_pages - 1;
+    for (int p = 0; p < maxp; ++p)
+        for (int b = 0; b < B; ++b)
+            if (p < need[b]) c->h_btab[(size_t)b * maxp + p] = next--;
+    c->h_rows.clear(); c->h_tiles.clear(); c->h_codes.clear(); c->h_tgt.clear();
+    c->h_state.assign(B, SeqState{});
+    c->h_tlen.assign(target_len, target_len + B);
+    int64_t oph = 0, opr = 0, otg = 0;
+    const int trows = (cf.dtype == MTP_DTYPE_BF16) ? 16 : MTP_ATTN_QT;
+    for (int b = 0; b < B; ++b) {
+        const int lp = phon_len[b], lq = prompt_len[b], lt = target_len[b], len = lp + lq + lt;
+        const int row0 = (int)c->h_rows.size();
+        for (int i = 0; i < len; ++i) c->h_rows.push_back(RowInfo{b, i});
+        for (int i = 0; i < lp; ++i) {
+            int32_t cr[8] = {phon[oph + i], 0, 0, 0, 0, 0, 0, 0};
+            c->h_codes.insert(c->h_codes.end(), cr, cr + 8);
+        }
+        for (int t = 0; t < lq; ++t) {
+            int32_t cr[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+            for (int q = 0; q < nq; ++q) cr[q] = prompt[opr * nq + (int64_t)q * lq + t];
+            c->h_codes.insert(c->h_codes.end(), cr, cr + 8);
+        }
+        for (int t = 0; t < lt; ++t) {
+            int32_t cr[8] = {a1[otg + t], 0, 0, 0, 0, 0, 0, 0};
+            c->h_codes.insert(c->h_codes.end(), cr, cr + 8);
+            c->h_tgt.push_back(row0 + lp + lq + t);
+        }
+        oph += lp;
+        opr += lq;
+        otg += lt;
+        for (int i0 = 0; i0 < len; i0 += trows) c->h_tiles.push_back(make_int2(row0 + i0, std::min(trows, len - i0)));
+        SeqState s{};
+        s.ctx_len = len; s.phon_len = lp; s.prompt_len = lp + lq; s.last_tok = -1; s.done = 1;
+        c->h_state[b] = s;
+    }
+    const int rows = (int)c->h_rows.size(), n_tiles = (int)c->h_tiles.size();
+    hipStream_t st = c->stream;
+    HIPCHK(c, hipMemcpyAsync(c->WS() + c->ws.rows, c->h_rows.data(), rows * sizeof(RowInfo), hipMemcpyHostToDevice, st), "upload rows");
+    HIPCHK(c, hipMemcpyAsync(c->WS() + c->ws.tiles, c->h_tiles.data(), n_tiles * sizeof(int2), hipMemcpyHostToDevice, st), "upload tiles");
+    HIPCHK(c, hipMemcpyAsync(c->WS() + c->ws.state, c->h_state.data(), B * sizeof(SeqState), hipMemcpyHostToDevice, st), "upload state");
+    HIPCHK(c, hipMemcpyAsync(c->WS() + c->ws.btab, c->h_btab.data(), c->h_btab.size() * 4, hipMemcpyHostToDevice, st), "upload block table");
+    HIPCHK(c, hipMemcpyAsync(c->WS() + c->ws.codes, c->h_codes.data(), c->h_codes.size() * 4, hipMemcpyHostToDevice, st), "upload codes");
+    if (!c->h_tgt.empty())
+        HIPCHK(c, hipMemcpyAsync(c->WS() + c->ws.tgt_rows, c->h_tgt.data(), c->h_tgt.size() * 4, hipMemcpyHostToDevice, st), "upload target rows");
+    HIPCHK(c, hipStreamSynchronize(st), "nar upload sync");
+    c->B = B;
+    c->nar_rows = rows;
+    c->nar_tiles = n_tiles;
+    c->nar_ready = true;
+    c->nar_ran = false;
+    return MTP_OK;
+}
+
+int mtp_nar_run(mtp_ctx* c) {
+    if (!c) return MTP_EINVAL;
+    const mtp_config& cf = c->cfg;
+    if (!is_nar(cf)) { c->err = "not a NAR context"; return MTP_EINVAL; }
+    if (!c->nar_ready) { c->err = "NAR run before prepare"; return MTP_ESTATE; }
+    const int d = cf.d_model, dt = cf.dtype, cb = cf.vocab - 1, rows = c->nar_rows;
+    const size_t esz = dt == MTP_DTYPE_BF16 ? 2 : 4;
+    hipStream_t st = c->stream;
+    for (int s = 0; s < cf.k_heads; ++s) {
+        NarEmbedArgs e{};
+        e.dtype = dt; e.n_rows = rows; e.d = d; e.stage = s; e.n_q = cf.k_heads + 1; e.cb = cb;
+        e.st = c->ws_ptr<SeqState>(c->ws.state); e.rows = c->ws_ptr<RowInfo>(c->ws.rows);
+        e.codes = c->ws_ptr<int32_t>(c->ws.codes);
+        e.emb_phone = c->wt(MTP_T_EMB_PHONE); e.emb_codes = c->wt(MTP_T_EMB_AC); e.pos = c->wt(MTP_T_POS);
+        e.stage_vec = (const float*)c->wt(MTP_T_STAGE);
+        e.ln_g = (const float*)c->lt(0, MTP_T_LN1_G); e.ln_b = (const float*)c->lt(0, MTP_T_LN1_B);
+        e.h = c->ws_ptr<float>(c->ws.h); e.u = c->WS() + c->ws.u;
+        HIPCHK(c, nar_embed_ln(st, e), "nar embed");
+        for (int l = 0; l < cf.n_layers; ++l) {
+            const int rc = run_layer(c, l, rows, c->nar_tiles, MTP_ATTN_QT, 1 << 30, 1, false, true);
+            if (rc) return rc;
+        }
+        RowsLnArgs r{};
+        r.dtype = dt; r.n_rows = rows; r.d = d; r.h = c->ws_ptr<float>(c->ws.h);
+        r.ln_g = (const float*)c->wt(MTP_T_LNF_G); r.ln_b = (const float*)c->wt(MTP_T_LNF_B); r.u = c->WS() + c->ws.u;
+        HIPCHK(c, rows_ln(st, r), "nar final ln");
+        float* lg = c->ws_ptr<float>(c->ws.nar_logits) + (size_t)s * c->ws.m_pre * cb;
+        GemmArgs g{};
+        g.dtype = dt; g.epi = EPI_LOGITS; g.X = c->WS() + c->ws.u; g.ldx = d; g.M = rows;
+        g.W = (const char*)c->wt(MTP_T_W_HEADS) + (size_t)s * cb * d * esz; g.N = cb; g.K = d; g.splits = 1;
+        g.bias = (const float*)c->wt(MTP_T_B_HEADS) + (size_t)s * cb; g.out = lg; g.ldo = cb;
+        HIPCHK(c, gemm(st, g), "nar head gemm");
+        ArgmaxArgs am{};
+        am.n = (int)c->h_tgt.size(); am.tgt_rows = c->ws_ptr<int32_t>(c->ws.tgt_rows); am.logits = lg; am.ld = cb;
+        am.cb = cb; am.codes = c->ws_ptr<int32_t>(c->ws.codes); am.slot = s + 1;
+        HIPCHK(c, rows_argmax(st, am), "nar argmax");
+    }
+    c->nar_ran = true;
+    return MTP_OK;
+}
+
+int mtp_nar_get_codes(mtp_ctx* c, int32_t* codes) {
+    if (!c || !codes) return MTP_EINVAL;
+    if (!is_nar(c->cfg)) { c->err = "not a NAR context"; return MTP_EINVAL; }
+    if (!c->nar_ran) { c->err = "no NAR run yet"; return MTP_ESTATE; }
+    std::vector<int32_t> all((size_t)c->nar_rows * 8);
+    HIPCHK(c, hipMemcpyAsync(all.data(), c->WS() + c->ws.codes, all.size() * 4, hipMemcpyDeviceToHost, c->stream), "codes to host");
+    HIPCHK(c, hipStreamSynchronize(c->stream), "sync");
+    const int k = c->cfg.k_heads;
+    size_t o = 0, ti = 0;
+    for (int b = 0; b < c->B; ++b) {
+        const int lt = c->h_tlen[b];
+        for (int s = 0; s < k; ++s)
+            for (int t = 0; t < lt; ++t) codes[o + (size_t)s * lt + t] = all[(size_t)c->h_tgt[ti + t] * 8 + s + 1];
+        o += (size_t)k * lt;
+        ti += lt;
+    }
+    return MTP_OK;
+}
+
+int mtp_nar_get_logits(mtp_ctx* c, int stage, float* logits) {
+    if (!c || !logits) return MTP_EINVAL;
+    if (!is_nar(c->cfg)) { c->err = "not a NAR context"; return MTP_EINVAL; }
+    if (stage < 0 || stage >= c->cfg.k_heads) { c->err = "stage out of range"; return MTP_EINVAL; }
+    if (!c->nar_ran) { c->err = "no NAR run yet"; return MTP_ESTATE; }
+    const int cb = c->cfg.vocab - 1;
+    std::vector<float> all((size_t)c->nar_rows * cb);
+    const char* src = c->WS() + c->ws.nar_logits + (size_t)stage * c->ws.m_pre * cb * 4;
+    HIPCHK(c, hipMemcpyAsync(all.data(), src, all.size() * 4, hipMemcpyDeviceToHost, c->stream), "logits to host");
+    HIPCHK(c, hipStreamSynchronize(c->stream), "sync");
+    for (size_t i = 0; i < c->h_tgt.size(); ++i)
+        std::memcpy(logits + i * cb, all.data() + (size_t)c->h_tgt[i] * cb, (size_t)cb * 4);
     return MTP_OK;
 }
 

@@ -62,7 +62,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs p) {
         part = p.part + ((size_t)(tile * gridDim.y + head) * p.n_splits + split) * (QT * PSTRIDE);
     const int seq = p.rows[row0].seq;
     const int pos0 = p.rows[row0].pos;
-    const int kend = pos0 + nrows;
+    const int kend = p.bidir ? p.st[seq].ctx_len : pos0 + nrows;
     const int kb = split * p.split_len;
     const int ke = min(kb + p.split_len, kend);
     if (kb >= ke) {
@@ -120,7 +120,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs p) {
             for (int i = 0; i < QT; ++i) sc[i] = sum8(sc[i]);
             if (dc == 0 && kk < cn) {
 #pragma unroll
-                for (int i = 0; i < QT; ++i) s_p[i][kk] = (c0 + kk <= pos0 + i) ? sc[i] : -INFINITY;
+                for (int i = 0; i < QT; ++i) s_p[i][kk] = (p.bidir || c0 + kk <= pos0 + i) ? sc[i] : -INFINITY;
             }
         }
         __syncthreads();

@@ -93,7 +93,8 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnMfmaArgs p) {
         qb[1] = *reinterpret_cast<const float4*>(qp + 36);
     }
     if (nrows <= 0) return;
-    const int kend = pos0 + nrows;
+    const bool bidir = p.mode == 1 && p.bidir;
+    const int kend = bidir ? p.st[b].ctx_len : pos0 + nrows;
     if (kb >= kend) return;
     const int ke = min(kb + p.split_len, kend);
 
@@ -125,7 +126,7 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnMfmaArgs p) {
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
                 const int key = wk + 16 * t + 4 * g + v;
-                const bool ok = (key < ke) && (key <= pos0 + r) && (r < nrows);
+                const bool ok = (key < ke) && (bidir || key <= pos0 + r) && (r < nrows);
                 sc[t][v] = ok ? s[v] : -INFINITY;
                 mx = fmaxf(mx, sc[t][v]);
             }

@@ -37,6 +37,8 @@ struct AttnArgs {
     int n_splits;
     void* out; int ldo;        // [rows][d] attention output (act type)
     float* part;               // split partials when n_splits > 1
+    int bidir;                 // 1: every row sees its sequence's ctx_len keys (no causal mask)
+    const SeqState* st;        // sequence lengths when bidir
 };
 hipError_t attention(hipStream_t st, const AttnArgs& a);
 
@@ -72,6 +74,7 @@ struct AttnMfmaArgs {
     int split_len; int n_splits;
     bf16_t* out; int ldo;
     float* part;
+    int bidir;                 // prefill mode: 1 = every row sees its sequence's ctx_len keys
 };
 hipError_t attention_mfma(hipStream_t st, const AttnMfmaArgs& a);
 
@@ -154,6 +157,41 @@ struct FinalArgs {
     void* z;                   // NULL: copy only
 };
 hipError_t final_ln(hipStream_t st, const FinalArgs& a);
+
+// NAR module input of one stage: row r (sequence ri.seq, position ri.pos) is
+// the phoneme table at codes[r][0] (pos < phon_len), the sum of the n_q
+// codebook tables at codes[r][0..n_q) (pos < prompt_len), or the sum of the
+// tables 0..stage at codes[r][0..stage] (target); plus position and stage
+// vectors; h = that row, u = LN1 of layer 0.
+struct NarEmbedArgs {
+    int dtype;
+    int n_rows; int d;
+    int stage; int n_q; int cb;        // predicted layer = stage + 2; codebook size
+    const SeqState* st; const RowInfo* rows;
+    const int32_t* codes;              // [rows][8]
+    const void* emb_phone; const void* emb_codes; const void* pos;
+    const float* stage_vec;            // [k_heads][d]
+    const float* ln_g; const float* ln_b;
+    float* h; void* u;
+};
+hipError_t nar_embed_ln(hipStream_t st, const NarEmbedArgs& a);
+
+// u[r] = LN(h[r]) for every row.
+struct RowsLnArgs {
+    int dtype; int n_rows; int d;
+    const float* h; const float* ln_g; const float* ln_b;
+    void* u;
+};
+hipError_t rows_ln(hipStream_t st, const RowsLnArgs& a);
+
+// codes[row][slot] = argmax (lowest index on ties) of logits[row][0..cb) for
+// the rows listed in tgt_rows.
+struct ArgmaxArgs {
+    int n; const int32_t* tgt_rows;
+    const float* logits; int ld; int cb;
+    int32_t* codes; int slot;
+};
+hipError_t rows_argmax(hipStream_t st, const ArgmaxArgs& a);
 
 // Sampling configuration, read by the selection kernel from device memory so
 // that a captured step serves every seed and temperature.

@@ -168,6 +168,99 @@ hipError_t final_ln(hipStream_t st, const FinalArgs& a) {
     return hipGetLastError();
 }
 
+// ------------------------------------------------------------ NAR rows
+template <typename WT>
+__global__ __launch_bounds__(256) void nar_embed_ln_kernel(NarEmbedArgs a) {
+    using ActT = WT;
+    __shared__ float red[4];
+    const int r = blockIdx.x, tid = threadIdx.x;
+    const RowInfo ri = a.rows[r];
+    const SeqState& s = a.st[ri.seq];
+    int code[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) code[i] = a.codes[(size_t)r * 8 + i];
+    const bool phon = ri.pos < s.phon_len;
+    const int nt = phon ? 0 : (ri.pos < s.prompt_len ? a.n_q : a.stage + 1);   // codebook tables summed
+    const WT* ep = reinterpret_cast<const WT*>(a.emb_phone) + (size_t)code[0] * a.d;
+    const WT* ec = reinterpret_cast<const WT*>(a.emb_codes);
+    const WT* prow = reinterpret_cast<const WT*>(a.pos) + (size_t)ri.pos * a.d;
+    const float* sv = a.stage_vec + (size_t)a.stage * a.d;
+    float* h = a.h + (size_t)r * a.d;
+    float x[MAXC];
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j) {
+        const int c = tid + 256 * j;
+        x[j] = 0.f;
+        if (c < a.d) {
+            float e = phon ? ld<WT>(ep + c) : 0.f;
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+                if (i < nt) e += ld<WT>(ec + ((size_t)i * a.cb + code[i]) * a.d + c);
+            x[j] = (e + ld<WT>(prow + c)) + sv[c];
+            h[c] = x[j];
+        }
+    }
+    layer_norm_store<ActT>(x, a.d, a.ln_g, a.ln_b, reinterpret_cast<ActT*>(a.u) + (size_t)r * a.d, red);
+}
+
+template <typename ActT>
+__global__ __launch_bounds__(256) void rows_ln_kernel(RowsLnArgs a) {
+    __shared__ float red[4];
+    const int r = blockIdx.x, tid = threadIdx.x;
+    const float* h = a.h + (size_t)r * a.d;
+    float x[MAXC];
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j) {
+        const int c = tid + 256 * j;
+        x[j] = c < a.d ? h[c] : 0.f;
+    }
+    layer_norm_store<ActT>(x, a.d, a.ln_g, a.ln_b, reinterpret_cast<ActT*>(a.u) + (size_t)r * a.d, red);
+}
+
+// One wave per listed row.
+__global__ __launch_bounds__(256) void rows_argmax_kernel(ArgmaxArgs a) {
+    const int i = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+    if (i >= a.n) return;
+    const int row = a.tgt_rows[i];
+    const float* lg = a.logits + (size_t)row * a.ld;
+    float bv = -INFINITY;
+    int bi = 0x7fffffff;
+    for (int c = lane; c < a.cb; c += 64) {
+        const float v = lg[c];
+        const bool b = (v > bv) | ((v == bv) & (c < bi));
+        bv = b ? v : bv;
+        bi = b ? c : bi;
+    }
+    for (int o = 32; o >= 1; o >>= 1) {
+        const float ov = __shfl_xor(bv, o);
+        const int oi = __shfl_xor(bi, o);
+        const bool b = (ov > bv) | ((ov == bv) & (oi < bi));
+        bv = b ? ov : bv;
+        bi = b ? oi : bi;
+    }
+    if (lane == 0) a.codes[(size_t)row * 8 + a.slot] = bi < a.cb ? bi : 0;   // (all-NaN row: code 0)
+}
+
+hipError_t nar_embed_ln(hipStream_t st, const NarEmbedArgs& a) {
+    if (a.n_rows <= 0) return hipSuccess;
+    if (a.dtype == 1) hipLaunchKernelGGL(nar_embed_ln_kernel<bf16_t>, dim3(a.n_rows), dim3(256), 0, st, a);
+    else hipLaunchKernelGGL(nar_embed_ln_kernel<float>, dim3(a.n_rows), dim3(256), 0, st, a);
+    return hipGetLastError();
+}
+
+hipError_t rows_ln(hipStream_t st, const RowsLnArgs& a) {
+    if (a.n_rows <= 0) return hipSuccess;
+    if (a.dtype == 1) hipLaunchKernelGGL(rows_ln_kernel<bf16_t>, dim3(a.n_rows), dim3(256), 0, st, a);
+    else hipLaunchKernelGGL(rows_ln_kernel<float>, dim3(a.n_rows), dim3(256), 0, st, a);
+    return hipGetLastError();
+}
+
+hipError_t rows_argmax(hipStream_t st, const ArgmaxArgs& a) {
+    if (a.n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(rows_argmax_kernel, dim3((a.n + 3) / 4), dim3(256), 0, st, a);
+    return hipGetLastError();
+}
+
 // ------------------------------------------------------------ cache flush
 __global__ __launch_bounds__(256) void cache_flush_kernel(const uint4* p, size_t n16, uint32_t* sink) {
     uint32_t acc = 0;
