@@ -84,7 +84,7 @@ def time_decode(sess, wl, prompts, steps, warmup, torch, top_k=None):
 
 
 KCLASSES = {  # kernel class -> (name, launches per decode step as a function of layers)
-    4: ("attention (attn_mfma_kernel)", lambda L: L),
+    4: ("attention (attn_dec_kernel)", lambda L: L),
     3: ("QKV projection (gemv_kernel<EpiQKVDec>)", lambda L: L),
     1: ("FFN1 (gemv_kernel<EpiGeluB>)", lambda L: L),
     5: ("heads (gemv_kernel<EpiLogitsB>)", lambda L: 1),

@@ -159,7 +159,8 @@ WsLayout ws_layout(const mtp_config& c) {
     w.u = take(w.m_max * d * w.act_bytes);
     w.attn = take(w.m_max * d * w.act_bytes);
     w.ffn = take(w.m_max * F * w.act_bytes);
-    w.part = take(std::max(w.m_pre, w.m_dec * (int64_t)MTP_SPLITK_MAX) * d * 4);
+    // split-K partials: up to 4 splits of a prefill-sized GEMM, 8 of a decode one
+    w.part = take(std::max(w.m_pre * 4, w.m_dec * (int64_t)MTP_SPLITK_MAX) * d * 4);
     w.apart = take(B * H * w.max_splits * MTP_ATTN_QT * 68 * 4);
     w.hz = take(B * d * 4);
     w.z = take(B * d * w.act_bytes);
@@ -268,7 +269,7 @@ int hip_fail(mtp_ctx* c, hipError_t e, const char* where) {
 
 int pick_splits(const mtp_ctx* c, int M, int N, int K) {
     if (c->cfg.dtype != MTP_DTYPE_BF16) return 1;
-    const int64_t cap_rows = std::max(c->ws.m_pre, c->ws.m_dec * (int64_t)MTP_SPLITK_MAX);
+    const int64_t cap_rows = std::max(c->ws.m_pre * 4, c->ws.m_dec * (int64_t)MTP_SPLITK_MAX);
     const int gran = gemm_split_granule(1, M);
     int tiles = (M <= 32) ? (N + 15) / 16 : ((N + 31) / 32) * ((M + 127) / 128);
     if (M > 256) tiles = ((N + 127) / 128) * ((M + 127) / 128);
@@ -386,7 +387,7 @@ int run_layer(mtp_ctx* c, int l, int rows, int n_tiles, int qt, int split_len, i
         HIPCHK(c, decode_attention(c, l, qt, true), "decode attention");
     } else if (dt == MTP_DTYPE_BF16) {
         AttnMfmaArgs m{};
-        m.mode = 1; m.n_tiles = n_tiles; m.Q = 0; m.qt = 16; m.st = c->ws_ptr<SeqState>(c->ws.state);
+        m.mode = 1; m.n_tiles = n_tiles; m.Q = 0; m.qt = MTP_PREFILL_ROWS; m.st = c->ws_ptr<SeqState>(c->ws.state);
         m.tiles = c->ws_ptr<int2>(c->ws.tiles); m.rows = c->ws_ptr<RowInfo>(c->ws.rows);
         m.q = c->ws_ptr<float>(c->ws.q); m.ldq = d; m.kv = c->kv(l); m.split_len = 1 << 30; m.n_splits = 1;
         m.out = (bf16_t*)(c->WS() + c->ws.attn); m.ldo = d; m.part = nullptr; m.bidir = bidir ? 1 : 0;
@@ -713,7 +714,7 @@ int mtp_prefill(mtp_ctx* c, int B, const int32_t* phon, const int32_t* phon_len,
         for (int i = 0; i < phon_len[b]; ++i) c->h_ids.push_back(phon[op++]);
         for (int i = 0; i < ac_len[b]; ++i) c->h_ids.push_back(ac[oa++]);
         for (int i = 0; i < len; ++i) c->h_rows.push_back(RowInfo{b, i});
-        const int trows = (cf.dtype == MTP_DTYPE_BF16) ? 16 : MTP_ATTN_QT;
+        const int trows = (cf.dtype == MTP_DTYPE_BF16) ? MTP_PREFILL_ROWS : MTP_ATTN_QT;
         for (int i0 = 0; i0 < len; i0 += trows) c->h_tiles.push_back(make_int2(row0 + i0, std::min(trows, len - i0)));
         c->h_last[b] = row0 + len - 1;
         SeqState s{};
@@ -905,7 +906,7 @@ int mtp_nar_prepare(mtp_ctx* c, int B, const int32_t* phon, const int32_t* phon_
     c->h_state.assign(B, SeqState{});
     c->h_tlen.assign(target_len, target_len + B);
     int64_t oph = 0, opr = 0, otg = 0;
-    const int trows = (cf.dtype == MTP_DTYPE_BF16) ? 16 : MTP_ATTN_QT;
+    const int trows = (cf.dtype == MTP_DTYPE_BF16) ? MTP_PREFILL_ROWS : MTP_ATTN_QT;
     for (int b = 0; b < B; ++b) {
         const int lp = phon_len[b], lq = prompt_len[b], lt = target_len[b], len = lp + lq + lt;
         const int row0 = (int)c->h_rows.size();

@@ -1,22 +1,6 @@
-// Causal attention for the bf16 cache on MFMA (decode and prefill).
-//
-// One workgroup per (query tile, head, key split); a query tile is up to 16
-// rows of one sequence (decode: the pending chunk; prefill: 16 prompt rows).
-// Keys are processed in chunks of 256, 64 per wave:
-//
-//   S^T[key][q] = K[key][:] . Q[q][:] / 8     v_mfma_f32_16x16x32_bf16, A = 16
-//                                              key rows of the page (16 bytes per
-//                                              lane, one 128-byte key row per 4
-//                                              lanes x 2 loads), B = the queries
-//   online softmax per query (running max / sum shared by the four waves)
-//   O^T[dim][q] += V^T[dim][keys] . P^T[keys][q]   A = the transposed V block
-//                                              (8 consecutive keys of one dim are
-//                                              16 contiguous bytes), B = P from LDS
-//
-// so all arithmetic on keys runs on the matrix cores; the VALU only does the
-// exponentials.  Every K and V^T fragment of a chunk is requested before the
-// first MFMA.  With several splits a split writes (max, sum, unnormalised
-// output) per row; otherwise the normalised bf16 output.
+// Attention for the bf16 cache on MFMA: decode (attn_dec_kernel) and prefill
+// (attn_prefill_kernel), flash-style online softmax with every key product on
+// the matrix cores and the probabilities kept in registers.
 #include <math.h>
 
 #include "common.h"
@@ -32,181 +16,6 @@ __device__ __forceinline__ uint32_t pk2(float a, float b) {
     return (uint32_t)f32_to_bf16(a) | ((uint32_t)f32_to_bf16(b) << 16);
 }
 }  // namespace
-
-__global__ __launch_bounds__(256) void attn_mfma_kernel(AttnMfmaArgs p) {
-    const int head = blockIdx.y, split = blockIdx.z;
-    const int H = gridDim.y;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int r = lane & 15, g = lane >> 4;
-    __shared__ __attribute__((aligned(16))) bf16_t s_P[16][256 + 8];
-    __shared__ float s_red[4][16];
-    __shared__ float s_o[4][16][65];
-    const bf16_t* pool = reinterpret_cast<const bf16_t*>(p.kv.pool);
-    const int P = p.kv.page_size;
-    const int max_key = p.kv.max_pages_per_seq * P - 1;
-    const int kb = split * p.split_len;
-
-    int b, row0, nrows, pos0, rmax;
-    if (p.mode == 0) {
-        b = blockIdx.x;
-        row0 = b * p.Q;
-        nrows = p.st[b].pend_len;
-        pos0 = p.st[b].ctx_len;
-        rmax = p.Q - 1;
-    } else {
-        const int2 t = p.tiles[blockIdx.x];
-        row0 = t.x;
-        nrows = t.y;
-        b = p.rows[row0].seq;
-        pos0 = p.rows[row0].pos;
-        rmax = max(nrows - 1, 0);
-    }
-
-    // Loads of the first key chunk and of the queries go out before the
-    // sequence state is examined (all unconditional, from clamped addresses;
-    // keys past the context are masked later).
-    uint4 kfr[4][2], vfr[2][4];
-    auto load_chunk = [&](int c0) {
-        const int wk = c0 + 64 * wave;
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-            const int key = min(wk + 16 * t + r, max_key);
-            const bf16_t* kp = pool + p.kv.offset(b, key, 0, head) + g * 8;
-            kfr[t][0] = *reinterpret_cast<const uint4*>(kp);
-            kfr[t][1] = *reinterpret_cast<const uint4*>(kp + 32);
-        }
-#pragma unroll
-        for (int kb2 = 0; kb2 < 2; ++kb2) {
-            const int key0 = min(wk + 32 * kb2 + 8 * g, max_key & ~7);
-            const bf16_t* vp = pool + p.kv.vt_offset(b, key0, head);
-#pragma unroll
-            for (int dt = 0; dt < 4; ++dt) vfr[kb2][dt] = *reinterpret_cast<const uint4*>(vp + (size_t)(16 * dt + r) * P);
-        }
-    };
-    load_chunk(kb);
-    float4 qa[2], qb[2];
-    {
-        const float* qp = p.q + (size_t)(row0 + min(r, rmax)) * p.ldq + head * 64 + g * 8;
-        qa[0] = *reinterpret_cast<const float4*>(qp);
-        qb[0] = *reinterpret_cast<const float4*>(qp + 4);
-        qa[1] = *reinterpret_cast<const float4*>(qp + 32);
-        qb[1] = *reinterpret_cast<const float4*>(qp + 36);
-    }
-    if (nrows <= 0) return;
-    const bool bidir = p.mode == 1 && p.bidir;
-    const int kend = bidir ? p.st[b].ctx_len : pos0 + nrows;
-    if (kb >= kend) return;
-    const int ke = min(kb + p.split_len, kend);
-
-    // queries (B operand of S^T): lane (r, g) holds query r, dims 32 h + 8 g .. +8
-    bf16x8_t qf[2];
-#pragma unroll
-    for (int h2 = 0; h2 < 2; ++h2)
-        qf[h2] = __builtin_bit_cast(bf16x8_t, make_uint4(pk2(qa[h2].x * 0.125f, qa[h2].y * 0.125f),
-                                                         pk2(qa[h2].z * 0.125f, qa[h2].w * 0.125f),
-                                                         pk2(qb[h2].x * 0.125f, qb[h2].y * 0.125f),
-                                                         pk2(qb[h2].z * 0.125f, qb[h2].w * 0.125f)));
-
-    float m_run = -INFINITY, l_run = 0.f;       // statistics of query r
-    f32x4_t acc[4];                             // O^T rows 16 dt + 4 g + v, query r
-#pragma unroll
-    for (int dt = 0; dt < 4; ++dt) acc[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-
-    for (int c0 = kb; c0 < ke; c0 += 256) {
-        if (c0 != kb) load_chunk(c0);
-        const int wk = c0 + 64 * wave;           // this wave's first key
-        // scores: lane holds keys wk + 16 t + 4 g + v for query r
-        float sc[4][4];
-        float mx = -INFINITY;
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-            f32x4_t s = f32x4_t{0.f, 0.f, 0.f, 0.f};
-            s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kfr[t][0]), qf[0], s, 0, 0, 0);
-            s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kfr[t][1]), qf[1], s, 0, 0, 0);
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const int key = wk + 16 * t + 4 * g + v;
-                const bool ok = (key < ke) && (bidir || key <= pos0 + r) && (r < nrows);
-                sc[t][v] = ok ? s[v] : -INFINITY;
-                mx = fmaxf(mx, sc[t][v]);
-            }
-        }
-        mx = fmaxf(mx, __shfl_xor(mx, 16));
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        if (g == 0) s_red[wave][r] = mx;
-        __syncthreads();
-        const float cm = fmaxf(fmaxf(s_red[0][r], s_red[1][r]), fmaxf(s_red[2][r], s_red[3][r]));
-        const float m_new = fmaxf(m_run, cm);
-        const float scale = (m_run == -INFINITY) ? 0.f : __expf(m_run - m_new);
-        float sum = 0.f;
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-            float e[4];
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                e[v] = (sc[t][v] == -INFINITY) ? 0.f : __expf(sc[t][v] - m_new);
-                sum += e[v];
-            }
-            *reinterpret_cast<uint2*>(&s_P[r][64 * wave + 16 * t + 4 * g]) = make_uint2(pk2(e[0], e[1]), pk2(e[2], e[3]));
-        }
-        sum += __shfl_xor(sum, 16);
-        sum += __shfl_xor(sum, 32);
-        __syncthreads();                        // everyone has read s_red (max)
-        if (g == 0) s_red[wave][r] = sum;
-        __syncthreads();
-        const float cs = (s_red[0][r] + s_red[1][r]) + (s_red[2][r] + s_red[3][r]);
-        l_run = l_run * scale + cs;
-        m_run = m_new;
-#pragma unroll
-        for (int dt = 0; dt < 4; ++dt) acc[dt] *= scale;
-        // P^T fragments (this wave's keys only): query r, keys 32 kb2 + 8 g .. +8;
-        // V^T keys past the context may hold anything: zero them (0 x NaN is NaN)
-#pragma unroll
-        for (int kb2 = 0; kb2 < 2; ++kb2) {
-            const bf16x8_t pf = *reinterpret_cast<const bf16x8_t*>(&s_P[r][64 * wave + 32 * kb2 + 8 * g]);
-            const int nvalid = ke - (wk + 32 * kb2 + 8 * g);
-#pragma unroll
-            for (int dt = 0; dt < 4; ++dt) {
-                uint4 v = vfr[kb2][dt];
-                if (nvalid < 8) {
-                    uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-                    for (int e = 0; e < 8; ++e)
-                        if (e >= nvalid) w[e >> 1] &= (e & 1) ? 0x0000FFFFu : 0xFFFF0000u;
-                    v = make_uint4(w[0], w[1], w[2], w[3]);
-                }
-                acc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, v), pf, acc[dt], 0, 0, 0);
-            }
-        }
-        __syncthreads();                        // s_red / s_P reuse
-    }
-
-    // sum the four waves' partial O^T
-#pragma unroll
-    for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) s_o[wave][r][16 * dt + 4 * g + v] = acc[dt][v];
-    if (wave == 0 && g == 0) {
-        s_red[0][r] = m_run;
-        s_red[1][r] = l_run;
-    }
-    __syncthreads();
-    for (int idx = tid; idx < 16 * 64; idx += 256) {
-        const int q = idx >> 6, dim = idx & 63;
-        if (q >= nrows) continue;
-        const float o = (s_o[0][q][dim] + s_o[1][q][dim]) + (s_o[2][q][dim] + s_o[3][q][dim]);
-        if (p.n_splits == 1) {
-            p.out[(size_t)(row0 + q) * p.ldo + head * 64 + dim] = f32_to_bf16(o / s_red[1][q]);
-        } else {
-            float* e = p.part + ((size_t)(b * H + head) * p.n_splits + split) * (p.qt * PSTR) + q * PSTR;
-            e[4 + dim] = o;
-            if (dim == 0) {
-                e[0] = s_red[0][q];
-                e[1] = s_red[1][q];
-            }
-        }
-    }
-}
 
 // Decode attention over a bf16 cache, NW waves per workgroup: one workgroup
 // per (sequence, head, key split); within a 16*NW-key chunk each wave owns 16
@@ -380,6 +189,188 @@ static hipError_t attn_dec_go(hipStream_t st, const AttnMfmaArgs& a) {
     return hipGetLastError();
 }
 
+// Prefill attention: one workgroup of 4 waves per (query tile, head); a tile
+// is at most 16 QT rows of one sequence (tiles[blockIdx.x] = first row, row
+// count), taken as QT sub-tiles of 16 queries.  Same arithmetic as the
+// decode kernel above: within a 64-key chunk each wave owns 16 consecutive
+// keys and keeps its own online-softmax state per sub-tile across the chunks,
+// so the chunk loop has no barrier, and every K / V^T fragment a wave loads
+// serves all QT sub-tiles; the four states are merged through LDS once.
+// Causal, or bidirectional (every row sees its sequence's ctx_len keys) with
+// p.bidir.
+template <int QT>
+__global__ __launch_bounds__(256) void attn_prefill_kernel(AttnMfmaArgs p) {
+    constexpr int NW = 4;
+    const int head = blockIdx.y, split = blockIdx.z;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int r = lane & 15, g = lane >> 4;
+    extern __shared__ float s_o[];               // [NW waves][QT][64 dims][17]
+    __shared__ float s_m[NW][QT * 16], s_l[NW][QT * 16];
+    constexpr int CH = 16 * NW;                  // keys per chunk
+    const bf16_t* pool = reinterpret_cast<const bf16_t*>(p.kv.pool);
+    const int P = p.kv.page_size;
+    const int max_key = p.kv.max_pages_per_seq * P - 1;
+    const int kb = split * p.split_len;
+    const int2 tile = p.tiles[blockIdx.x];
+    const int row0 = tile.x, nrows = tile.y;
+    const int b = p.rows[row0].seq;
+    const int rmax = max(nrows - 1, 0);
+
+    uint4 kf[2];
+    uint2 vf[4];
+    auto load_keys = [&](int c0) {
+        const int wk = c0 + 16 * wave;
+        const bf16_t* kp = pool + p.kv.offset(b, min(wk + r, max_key), 0, head) + g * 8;
+        kf[0] = *reinterpret_cast<const uint4*>(kp);
+        kf[1] = *reinterpret_cast<const uint4*>(kp + 32);
+        const bf16_t* vp = pool + p.kv.vt_offset(b, min(wk + 4 * g, max_key & ~3), head);
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt) vf[dt] = *reinterpret_cast<const uint2*>(vp + (size_t)(16 * dt + r) * P);
+    };
+    load_keys(kb);
+    float4 qa[QT][2], qb[QT][2];
+#pragma unroll
+    for (int j = 0; j < QT; ++j) {
+        const float* qp = p.q + (size_t)(row0 + min(16 * j + r, rmax)) * p.ldq + head * 64 + g * 8;
+        qa[j][0] = *reinterpret_cast<const float4*>(qp);
+        qb[j][0] = *reinterpret_cast<const float4*>(qp + 4);
+        qa[j][1] = *reinterpret_cast<const float4*>(qp + 32);
+        qb[j][1] = *reinterpret_cast<const float4*>(qp + 36);
+    }
+    const int pos0 = p.rows[row0].pos;
+    const bool bidir = p.bidir != 0;
+    const int kend = bidir ? p.st[b].ctx_len : pos0 + nrows;
+    if (nrows <= 0 || kb >= kend) return;       // uniform over the workgroup
+    const int ke = min(kb + p.split_len, kend);
+
+    bf16x8_t qf[QT][2];
+#pragma unroll
+    for (int j = 0; j < QT; ++j)
+#pragma unroll
+        for (int h2 = 0; h2 < 2; ++h2)
+            qf[j][h2] = __builtin_bit_cast(bf16x8_t, make_uint4(pk2(qa[j][h2].x * 0.125f, qa[j][h2].y * 0.125f),
+                                                                pk2(qa[j][h2].z * 0.125f, qa[j][h2].w * 0.125f),
+                                                                pk2(qb[j][h2].x * 0.125f, qb[j][h2].y * 0.125f),
+                                                                pk2(qb[j][h2].z * 0.125f, qb[j][h2].w * 0.125f)));
+
+    float m_run[QT], l_run[QT];                 // query 16 j + r, this wave's keys
+    f32x4_t acc[QT][4];                         // O^T rows 16 dt + 4 g + v, query 16 j + r
+#pragma unroll
+    for (int j = 0; j < QT; ++j) {
+        m_run[j] = -INFINITY;
+        l_run[j] = 0.f;
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt) acc[j][dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    }
+
+    for (int c0 = kb; c0 < ke; c0 += CH) {
+        const uint4 k0 = kf[0], k1 = kf[1];
+        uint2 v[4];
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt) v[dt] = vf[dt];
+        if (c0 + CH < ke) load_keys(c0 + CH);    // next chunk in flight (uniform branch)
+        const int wk = c0 + 16 * wave;
+        // V^T entries of keys past the context may hold anything: zero them
+        const int nvalid = ke - (wk + 4 * g);
+        if (nvalid < 4) {
+#pragma unroll
+            for (int dt = 0; dt < 4; ++dt) {
+                uint32_t w0 = v[dt].x, w1 = v[dt].y;
+                if (nvalid <= 0) w0 = 0u;
+                else if (nvalid == 1) w0 &= 0x0000FFFFu;
+                if (nvalid <= 2) w1 = 0u;
+                else w1 &= 0x0000FFFFu;
+                v[dt] = make_uint2(w0, w1);
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < QT; ++j) {
+            f32x4_t s = f32x4_t{0.f, 0.f, 0.f, 0.f};
+            s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, k0), qf[j][0], s, 0, 0, 0);
+            s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, k1), qf[j][1], s, 0, 0, 0);
+            const int qi = 16 * j + r;
+            float sc[4];
+            float mx = -INFINITY;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int key = wk + 4 * g + e;
+                const bool ok = (key < ke) && (bidir || key <= pos0 + qi) && (qi < nrows);
+                sc[e] = ok ? s[e] : -INFINITY;
+                mx = fmaxf(mx, sc[e]);
+            }
+            mx = fmaxf(mx, __shfl_xor(mx, 16));
+            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            const float m_new = fmaxf(m_run[j], mx);
+            const float scale = (m_run[j] == -INFINITY) ? 0.f : __expf(m_run[j] - m_new);
+            float pe[4], sum = 0.f;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                pe[e] = (sc[e] == -INFINITY) ? 0.f : __expf(sc[e] - m_new);
+                sum += pe[e];
+            }
+            sum += __shfl_xor(sum, 16);
+            sum += __shfl_xor(sum, 32);
+            l_run[j] = l_run[j] * scale + sum;
+            m_run[j] = m_new;
+            const s16x4_t pf = __builtin_bit_cast(s16x4_t, make_uint2(pk2(pe[0], pe[1]), pk2(pe[2], pe[3])));
+#pragma unroll
+            for (int dt = 0; dt < 4; ++dt) {
+                acc[j][dt] *= scale;
+                acc[j][dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4_t, v[dt]), pf,
+                                                                       acc[j][dt], 0, 0, 0);
+            }
+        }
+    }
+
+    // merge the NW waves' states
+#pragma unroll
+    for (int j = 0; j < QT; ++j)
+        if (g == 0) s_m[wave][16 * j + r] = m_run[j];
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < QT; ++j) {
+        float M = -INFINITY;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) M = fmaxf(M, s_m[w][16 * j + r]);
+        const float wsc = (m_run[j] == -INFINITY) ? 0.f : __expf(m_run[j] - M);
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                s_o[((wave * QT + j) * 64 + 16 * dt + 4 * g + e) * 17 + r] = acc[j][dt][e] * wsc;
+        if (g == 0) s_l[wave][16 * j + r] = l_run[j] * wsc;
+    }
+    __syncthreads();
+    // output: (dim, query) pairs over the workgroup's threads
+    for (int idx = tid; idx < 64 * 16 * QT; idx += 64 * NW) {
+        const int dim = idx / (16 * QT), q = idx % (16 * QT);
+        if (q >= nrows) continue;
+        const int j = q >> 4, rr = q & 15;
+        float o = 0.f, L = 0.f, Mq = -INFINITY;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) {
+            o += s_o[((w * QT + j) * 64 + dim) * 17 + rr];
+            L += s_l[w][q];
+            Mq = fmaxf(Mq, s_m[w][q]);
+        }
+        p.out[(size_t)(row0 + q) * p.ldo + head * 64 + dim] = f32_to_bf16(o / L);
+    }
+}
+
+template <int QT>
+static hipError_t attn_prefill_go(hipStream_t st, const AttnMfmaArgs& a) {
+    const size_t lds = (size_t)4 * QT * 64 * 17 * sizeof(float);
+    static bool attr_set = false;               // the dynamic-LDS limit, raised once per process
+    if (!attr_set && lds > 48 * 1024) {
+        hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_prefill_kernel<QT>),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (err != hipSuccess) return err;
+        attr_set = true;
+    }
+    hipLaunchKernelGGL((attn_prefill_kernel<QT>), dim3(a.n_tiles, a.kv.n_heads, 1), dim3(256), lds, st, a);
+    return hipGetLastError();
+}
+
 hipError_t attention_mfma(hipStream_t st, const AttnMfmaArgs& a) {
     if (a.split_len < 32 || a.n_splits < 1 || a.n_splits > 64 || a.kv.page_size < 8) return hipErrorInvalidValue;
     if (a.mode == 0) {
@@ -389,8 +380,12 @@ hipError_t attention_mfma(hipStream_t st, const AttnMfmaArgs& a) {
         if (a.split_len >= 128) return attn_dec_go<8>(st, a);
         return attn_dec_go<4>(st, a);
     }
-    hipLaunchKernelGGL(attn_mfma_kernel, dim3(a.n_tiles, a.kv.n_heads, a.n_splits), dim3(256), 0, st, a);
-    return hipGetLastError();
+    // prefill: tiles of at most a.qt rows (16, 32 or 64), one split
+    if (a.n_splits != 1) return hipErrorInvalidValue;
+    if (a.qt == 64) return attn_prefill_go<4>(st, a);
+    if (a.qt == 32) return attn_prefill_go<2>(st, a);
+    if (a.qt == 16) return attn_prefill_go<1>(st, a);
+    return hipErrorInvalidValue;
 }
 
 }  // namespace mtp

@@ -7,6 +7,7 @@
 #define MTP_HEAD_DIM 64
 #define MTP_MAX_HEADS_K 8      // prediction heads a step may use
 #define MTP_MAX_TOPK 32
+#define MTP_PREFILL_ROWS 64    // query rows per prefill attention tile (bf16)
 #define MTP_ATTN_QT 8          // query rows per attention tile
 #define MTP_SPLITK_MAX 8
 #define MTP_FLUSH_MB 512       // cache eviction read of cold replay timing
