@@ -271,8 +271,7 @@ int pick_splits(const mtp_ctx* c, int M, int N, int K) {
     if (c->cfg.dtype != MTP_DTYPE_BF16) return 1;
     const int64_t cap_rows = std::max(c->ws.m_pre * 4, c->ws.m_dec * (int64_t)MTP_SPLITK_MAX);
     const int gran = gemm_split_granule(1, M);
-    int tiles = (M <= 32) ? (N + 15) / 16 : ((N + 31) / 32) * ((M + 127) / 128);
-    if (M > 256) tiles = ((N + 127) / 128) * ((M + 127) / 128);
+    const int tiles = gemm_tiles(M, N);
     int s = 1;
     while (s < MTP_SPLITK_MAX && tiles * s < 256 && K % (gran * s * 2) == 0 && (int64_t)M * s * 2 <= cap_rows) s *= 2;
     return s;

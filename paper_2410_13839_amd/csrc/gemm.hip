@@ -5,11 +5,14 @@
 // so both operands are K-contiguous.  Outputs go through an epilogue functor
 // that receives 4 consecutive n of one row m.
 //
-//  * gemm_skinny_bf16: M <= 32 (decode at small batch).  The weight stream is
-//    the whole cost, so W fragments are loaded straight from HBM into MFMA
-//    registers (no LDS round trip), four waves split K, and the grid is sized
-//    so every CU streams.  X is tiny and read through L2.
-//  * gemm_tiled_bf16: M > 32 (batched decode, prefill).  LDS double-buffered
+//  * gemm_med_bf16: M <= 256 (decode rows of the batched path, the heads).
+//    A weight stream (M = 128 rows is ~128 flop per weight byte, below the
+//    MFMA / HBM ridge), so W fragments go straight from HBM into MFMA
+//    registers (no LDS round trip), 16 waves per workgroup split the K range,
+//    each wave loading its own activation fragments from L2 (no LDS staging:
+//    no two waves read the same k), and one LDS reduction over the waves
+//    precedes the epilogue.  The grid is sized so every CU streams.
+//  * gemm_tiled_bf16: M > 256 (prefill).  LDS double-buffered
 //    BMxBN tiles, BK = 64, 2x2 waves of v_mfma_f32_16x16x32_bf16.
 //  * gemm_f32: the fp32 model; LDS-tiled VALU FMA.
 #include "common.h"
@@ -99,72 +102,95 @@ struct EpiLogits {
     }
 };
 
-// --------------------------------------------------------------- skinny bf16
-template <int MT, int UNROLL, class Epi>
-__global__ __launch_bounds__(256) void gemm_skinny_bf16(const bf16_t* __restrict__ X, int ldx, int M,
-                                                        const bf16_t* __restrict__ W, int N, int K,
-                                                        int k_per_split, Epi epi) {
+// ---------------------------------------------------------------- medium bf16
+// Workgroup (x, y, z) = (16-column tile, 16*MT-row group, K split).  Wave w
+// takes k steps w, w + 16, ... of its split (32 k per step), up to MAXST at a
+// time, all loads of a round in flight together: the weight fragment (packed
+// order, one contiguous 1 KB wave load) and one 16 x 32 activation fragment
+// per row tile, rows beyond M read from the last valid row (never stored).
+// The wave index is made scalar so the step guards are uniform branches.
+constexpr int GM_NW = 16;
+
+template <int MT, int MAXST, class Epi>
+__global__ __launch_bounds__(64 * GM_NW) void gemm_med_bf16(const bf16_t* __restrict__ X, int ldx, int M,
+                                                            const bf16_t* __restrict__ W, int N, int K,
+                                                            int k_per_split, Epi epi) {
     const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int r = lane & 15, g = lane >> 4;
-    const int n0 = blockIdx.x * 16;
-    const int split = blockIdx.y;
+    const int nt = blockIdx.x;
+    const int m0 = blockIdx.y * 16 * MT;
+    const int split = blockIdx.z;
     const int kb = split * k_per_split;
-    // W in the packed fragment order (rows padded to a multiple of 16): the
-    // fragment of k step s is 1 KB at wp + s * 512
-    const bf16_t* wp = W + ((size_t)blockIdx.x * (K >> 5) + (kb >> 5)) * 512 + lane * 8;
+    const int nsteps = k_per_split >> 5;
+    const bf16_t* wp = W + ((size_t)nt * (K >> 5) + (kb >> 5)) * 512 + lane * 8;
     const bf16_t* xp[MT];
-    bool xvalid[MT];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
-        int m = r + 16 * mt;
-        xvalid[mt] = m < M;
-        xp[mt] = X + (size_t)(xvalid[mt] ? m : 0) * ldx + kb + g * 8;
+        const int m = min(m0 + 16 * mt + r, M - 1);
+        xp[mt] = X + (size_t)m * ldx + kb + g * 8;
     }
     f32x4_t acc[MT];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-    const int nsteps = k_per_split >> 5;
-    for (int s = wave; s < nsteps; s += 4 * UNROLL) {
-        uint4 wv[UNROLL];
-        uint4 xv[UNROLL][MT];
+    for (int s0 = wave; s0 < nsteps; s0 += GM_NW * MAXST) {
+        uint4 wv[MAXST];
+        uint4 xv[MAXST][MT];
 #pragma unroll
-        for (int u = 0; u < UNROLL; ++u) {
-            const int ss = s + 4 * u;
-            const bool in = ss < nsteps;
-            wv[u] = in ? *reinterpret_cast<const uint4*>(wp + (size_t)ss * 512) : make_uint4(0, 0, 0, 0);
+        for (int u = 0; u < MAXST; ++u) {
+            const int ss = s0 + GM_NW * u;
+            if (ss < nsteps) {
+                wv[u] = *reinterpret_cast<const uint4*>(wp + (size_t)ss * 512);
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
-                xv[u][mt] = (in && xvalid[mt]) ? *reinterpret_cast<const uint4*>(xp[mt] + ss * 32)
-                                               : make_uint4(0, 0, 0, 0);
+                for (int mt = 0; mt < MT; ++mt) xv[u][mt] = *reinterpret_cast<const uint4*>(xp[mt] + ss * 32);
+            }
         }
 #pragma unroll
-        for (int u = 0; u < UNROLL; ++u) {
+        for (int u = 0; u < MAXST; ++u) {
+            if (s0 + GM_NW * u < nsteps) {
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
-                acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, wv[u]),
-                                                                  __builtin_bit_cast(bf16x8_t, xv[u][mt]),
-                                                                  acc[mt], 0, 0, 0);
+                for (int mt = 0; mt < MT; ++mt)
+                    acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, wv[u]),
+                                                                      __builtin_bit_cast(bf16x8_t, xv[u][mt]),
+                                                                      acc[mt], 0, 0, 0);
+            }
         }
     }
 
-    __shared__ f32x4_t red[4][MT][64];
+    __shared__ f32x4_t red[GM_NW][MT][64];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) red[wave][mt][lane] = acc[mt];
     __syncthreads();
-    if (wave < MT) {
-        const int mt = wave;
+    if (threadIdx.x < MT * 64) {
+        const int mt = threadIdx.x >> 6;
         f32x4_t s = red[0][mt][lane];
 #pragma unroll
-        for (int w = 1; w < 4; ++w) s += red[w][mt][lane];
-        const int m = r + 16 * mt;
-        const int n = n0 + 4 * g;
+        for (int w = 1; w < GM_NW; ++w) s += red[w][mt][lane];
+        const int m = m0 + 16 * mt + r;
+        const int n = nt * 16 + 4 * g;
         if (m < M && n < N) {
             float v[4] = {s[0], s[1], s[2], s[3]};
             epi.store4(m, n, v, split, min(4, N - n));
         }
     }
+}
+
+template <int MT, class Epi>
+static void launch_med(hipStream_t st, const bf16_t* X, int ldx, int M, const bf16_t* W, int N, int K, int splits,
+                       Epi epi) {
+    const int kps = K / splits;
+    const int per_wave = ((kps >> 5) + GM_NW - 1) / GM_NW;   // k steps per wave
+    dim3 grid((N + 15) / 16, (M + 16 * MT - 1) / (16 * MT), splits);
+    dim3 block(64 * GM_NW);
+    if (per_wave <= 1)
+        hipLaunchKernelGGL((gemm_med_bf16<MT, 1, Epi>), grid, block, 0, st, X, ldx, M, W, N, K, kps, epi);
+    else if (per_wave == 2)
+        hipLaunchKernelGGL((gemm_med_bf16<MT, 2, Epi>), grid, block, 0, st, X, ldx, M, W, N, K, kps, epi);
+    else if (per_wave == 3)
+        hipLaunchKernelGGL((gemm_med_bf16<MT, 3, Epi>), grid, block, 0, st, X, ldx, M, W, N, K, kps, epi);
+    else
+        hipLaunchKernelGGL((gemm_med_bf16<MT, 4, Epi>), grid, block, 0, st, X, ldx, M, W, N, K, kps, epi);
 }
 
 // ---------------------------------------------------------------- tiled bf16
@@ -318,14 +344,11 @@ static hipError_t launch_bf16(hipStream_t st, const bf16_t* X, int ldx, int M, c
                               int splits, Epi epi) {
     const int kps = K / splits;
     if (M <= 16) {
-        dim3 grid((N + 15) / 16, splits);
-        hipLaunchKernelGGL((gemm_skinny_bf16<1, 8, Epi>), grid, dim3(256), 0, st, X, ldx, M, W, N, K, kps, epi);
+        launch_med<1>(st, X, ldx, M, W, N, K, splits, epi);
     } else if (M <= 32) {
-        dim3 grid((N + 15) / 16, splits);
-        hipLaunchKernelGGL((gemm_skinny_bf16<2, 8, Epi>), grid, dim3(256), 0, st, X, ldx, M, W, N, K, kps, epi);
+        launch_med<2>(st, X, ldx, M, W, N, K, splits, epi);
     } else if (M <= 256) {
-        dim3 grid((N + 31) / 32, (M + 127) / 128, splits);
-        hipLaunchKernelGGL((gemm_tiled_bf16<128, 32, Epi>), grid, dim3(256), 0, st, X, ldx, M, W, N, K, kps, epi);
+        launch_med<4>(st, X, ldx, M, W, N, K, splits, epi);
     } else {
         dim3 grid((N + 127) / 128, (M + 127) / 128, splits);
         hipLaunchKernelGGL((gemm_tiled_bf16<128, 128, Epi>), grid, dim3(256), 0, st, X, ldx, M, W, N, K, kps, epi);
@@ -343,8 +366,16 @@ static hipError_t launch_f32(hipStream_t st, const float* X, int ldx, int M, con
 
 int gemm_split_granule(int dtype, int M) {
     if (dtype == 0) return 32;
-    if (M <= 32) return 128;
+    if (M <= 256) return 32;
     return 64;
+}
+
+// Workgroups of one bf16 launch for M rows and N columns before K splitting.
+int gemm_tiles(int M, int N) {
+    if (M <= 16) return (N + 15) / 16;
+    if (M <= 32) return (N + 15) / 16;
+    if (M <= 256) return ((N + 15) / 16) * ((M + 63) / 64);
+    return ((N + 127) / 128) * ((M + 127) / 128);
 }
 
 hipError_t gemm(hipStream_t st, const GemmArgs& a) {

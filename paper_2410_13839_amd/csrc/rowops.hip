@@ -99,24 +99,73 @@ __global__ __launch_bounds__(256) void embed_ln_kernel(EmbedArgs a) {
     layer_norm_store<ActT>(x, a.d, a.ln_g, a.ln_b, u, red);
 }
 
-template <typename ActT>
+// One row per workgroup, thread t owning the float4 column chunks t and
+// t + 256.  Every load of the row (the residual, the bias, all NS split-K
+// partial sums) is issued before the first store, so the kernel costs one
+// global round trip; the partial sums are added in split order.
+template <typename ActT, int NS>
 __global__ __launch_bounds__(256) void resid_ln_kernel(ResidArgs a) {
     __shared__ float red[4];
     const int r = blockIdx.x, tid = threadIdx.x;
-    float* h = a.h + (size_t)r * a.d;
-    float x[MAXC];
+    const int d = a.d;
+    float* h = a.h + (size_t)r * d;
+    const float* __restrict__ part = a.part + (size_t)r * d;
+    float4 hv[2], bv[2], pv[NS][2];
 #pragma unroll
-    for (int j = 0; j < MAXC; ++j) {
-        int c = tid + 256 * j;
-        x[j] = 0.f;
-        if (c < a.d) {
-            float s = 0.f;
-            for (int sp = 0; sp < a.n_split; ++sp) s += a.part[sp * a.split_stride + (size_t)r * a.d + c];
-            x[j] = h[c] + (s + a.bias[c]);
-            h[c] = x[j];
+    for (int j = 0; j < 2; ++j) {
+        const int c = 4 * (tid + 256 * j);
+        const int cc = c < d ? c : 0;
+        hv[j] = *reinterpret_cast<const float4*>(h + cc);
+        bv[j] = *reinterpret_cast<const float4*>(a.bias + cc);
+#pragma unroll
+        for (int sp = 0; sp < NS; ++sp)
+            pv[sp][j] = *reinterpret_cast<const float4*>(part + sp * a.split_stride + cc);
+    }
+    float x[8];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        float4 s = pv[0][j];
+#pragma unroll
+        for (int sp = 1; sp < NS; ++sp) {
+            s.x += pv[sp][j].x; s.y += pv[sp][j].y; s.z += pv[sp][j].z; s.w += pv[sp][j].w;
+        }
+        x[4 * j + 0] = hv[j].x + (s.x + bv[j].x);
+        x[4 * j + 1] = hv[j].y + (s.y + bv[j].y);
+        x[4 * j + 2] = hv[j].z + (s.z + bv[j].z);
+        x[4 * j + 3] = hv[j].w + (s.w + bv[j].w);
+    }
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        const int c = 4 * (tid + 256 * j);
+        if (c < d) *reinterpret_cast<float4*>(h + c) = make_float4(x[4 * j], x[4 * j + 1], x[4 * j + 2], x[4 * j + 3]);
+    }
+    if (!a.ln_g) return;
+    float sum = 0.f;
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+        if (4 * (tid + 256 * j) < d) sum += (x[4 * j] + x[4 * j + 1]) + (x[4 * j + 2] + x[4 * j + 3]);
+    const float mean = block_sum(sum, red) / (float)d;
+    float var = 0.f;
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+        if (4 * (tid + 256 * j) < d) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) { const float t = x[4 * j + i] - mean; var = fmaf(t, t, var); }
+        }
+    const float rstd = rsqrtf(block_sum(var, red) / (float)d + 1e-5f);
+    ActT* u = reinterpret_cast<ActT*>(a.u) + (size_t)r * d;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        const int c = 4 * (tid + 256 * j);
+        if (c < d) {
+            const float4 gv = *reinterpret_cast<const float4*>(a.ln_g + c);
+            const float4 be = *reinterpret_cast<const float4*>(a.ln_b + c);
+            ActIO<ActT>::store(u + c + 0, (x[4 * j + 0] - mean) * rstd * gv.x + be.x);
+            ActIO<ActT>::store(u + c + 1, (x[4 * j + 1] - mean) * rstd * gv.y + be.y);
+            ActIO<ActT>::store(u + c + 2, (x[4 * j + 2] - mean) * rstd * gv.z + be.z);
+            ActIO<ActT>::store(u + c + 3, (x[4 * j + 3] - mean) * rstd * gv.w + be.w);
         }
     }
-    if (a.ln_g) layer_norm_store<ActT>(x, a.d, a.ln_g, a.ln_b, reinterpret_cast<ActT*>(a.u) + (size_t)r * a.d, red);
 }
 
 template <typename ActT>
@@ -155,11 +204,23 @@ hipError_t embed_ln(hipStream_t st, const EmbedArgs& a) {
     return hipGetLastError();
 }
 
+template <typename ActT>
+static hipError_t resid_ln_t(hipStream_t st, const ResidArgs& a) {
+    const dim3 g(a.n_rows), b(256);
+    switch (a.n_split) {
+    case 1: hipLaunchKernelGGL((resid_ln_kernel<ActT, 1>), g, b, 0, st, a); break;
+    case 2: hipLaunchKernelGGL((resid_ln_kernel<ActT, 2>), g, b, 0, st, a); break;
+    case 4: hipLaunchKernelGGL((resid_ln_kernel<ActT, 4>), g, b, 0, st, a); break;
+    case 8: hipLaunchKernelGGL((resid_ln_kernel<ActT, 8>), g, b, 0, st, a); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
 hipError_t resid_ln(hipStream_t st, const ResidArgs& a) {
     if (a.n_rows <= 0) return hipSuccess;
-    if (a.dtype == 1) hipLaunchKernelGGL(resid_ln_kernel<bf16_t>, dim3(a.n_rows), dim3(256), 0, st, a);
-    else hipLaunchKernelGGL(resid_ln_kernel<float>, dim3(a.n_rows), dim3(256), 0, st, a);
-    return hipGetLastError();
+    if (a.d % 4 != 0 || a.d > 2048) return hipErrorInvalidValue;
+    return a.dtype == 1 ? resid_ln_t<bf16_t>(st, a) : resid_ln_t<float>(st, a);
 }
 
 hipError_t final_ln(hipStream_t st, const FinalArgs& a) {

@@ -251,6 +251,20 @@ def test_valle_b32_batched():
     log(f"valle_b32: {steps} steps, max logit err {chk.max_err:.3g}, tie-zone {chk.tie_zone}")
 
 
+def test_long_b8_batched():
+    """24-layer d1536 decoder (24 heads of 64), batch 8, K=4, 3000 tokens
+    each: 32 decode rows through the batched path over a paged cache that
+    grows to 3650 keys per sequence; selection exact for every sequence at
+    every step, logits of one sequence against the oracle at two steps."""
+    wl = WORKLOADS["long_b8"]
+    log("long_b8: start")
+    steps, emitted, chk = run_teacher_forced(wl, wl.K, wl.top_k, steps_checked={0, 40}, tol=3e-2,
+                                             seqs_checked=[5])
+    assert steps == math.ceil(wl.max_new / wl.K)
+    assert all(len(e) == wl.max_new for e in emitted)
+    log(f"long_b8: {steps} steps, max logit err {chk.max_err:.3g}, tie-zone {chk.tie_zone}")
+
+
 def test_replay_timing_then_prefill_again():
     """Kernel replay timing returns positive times for every class, forbids a
     decode step until the next prefill, and leaves no trace in the next
