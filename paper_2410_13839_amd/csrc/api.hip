@@ -156,14 +156,16 @@ WsLayout ws_layout(const mtp_config& c) {
     w.btab = take(B * w.maxp * 4);
     w.h = take(w.m_max * d * 4);
     w.q = take(w.m_max * d * 4);
-    w.u = take(w.m_max * d * w.act_bytes);
-    w.attn = take(w.m_max * d * w.act_bytes);
-    w.ffn = take(w.m_max * F * w.act_bytes);
+    // bf16 activations may be stored in fragment order: rows padded to 16
+    const int64_t m_act = (w.m_max + 15) / 16 * 16;
+    w.u = take(m_act * d * w.act_bytes);
+    w.attn = take(m_act * d * w.act_bytes);
+    w.ffn = take(m_act * F * w.act_bytes);
     // split-K partials: up to 4 splits of a prefill-sized GEMM, 8 of a decode one
     w.part = take(std::max(w.m_pre * 4, w.m_dec * (int64_t)MTP_SPLITK_MAX) * d * 4);
     w.apart = take(B * H * w.max_splits * MTP_ATTN_QT * 68 * 4);
     w.hz = take(B * d * 4);
-    w.z = take(B * d * w.act_bytes);
+    w.z = take((B + 15) / 16 * 16 * d * w.act_bytes);
     w.logits = take(B * KH * V * 4);
     w.cand = take(B * KH * TK * 4);
     w.ehat = take(B * KH * TK * 4);
@@ -296,15 +298,16 @@ AttnDecArgs dec_attn_args(mtp_ctx* c, int l, int qt) {
 // Decode attention of layer l: MFMA kernel for bf16 caches, VALU kernel for
 // fp32 caches.  With merge_launch, split partials are merged by a separate
 // launch; otherwise the consumer merges them.
-hipError_t decode_attention(mtp_ctx* c, int l, int qt, bool merge_launch) {
+hipError_t decode_attention(mtp_ctx* c, int l, int qt, bool merge_launch, bool packed = false) {
     AttnDecArgs da = dec_attn_args(c, l, qt);
     da.merge = merge_launch ? 1 : 0;
+    da.packed = packed ? 1 : 0;
     if (c->cfg.dtype != MTP_DTYPE_BF16)
         return launch_rec(c, MTP_KCLASS_ATTENTION, [da](hipStream_t s) { return attention_decode(s, da); });
     AttnMfmaArgs m{};
     m.mode = 0; m.n_tiles = c->B; m.Q = c->q_pad; m.qt = qt; m.st = da.st;
     m.q = da.q; m.ldq = da.ldq; m.kv = da.kv; m.split_len = da.split_len; m.n_splits = da.n_splits;
-    m.out = (bf16_t*)da.out; m.ldo = da.ldo; m.part = da.part;
+    m.out = (bf16_t*)da.out; m.ldo = da.ldo; m.part = da.part; m.packed = da.packed;
     hipError_t e = launch_rec(c, MTP_KCLASS_ATTENTION, [m](hipStream_t s) { return attention_mfma(s, m); });
     if (e != hipSuccess || !merge_launch) return e;
     return attention_decode_merge(c->stream, da);
@@ -373,17 +376,19 @@ int run_layer(mtp_ctx* c, int l, int rows, int n_tiles, int qt, int split_len, i
     const int d = cf.d_model, F = cf.d_ff, dt = cf.dtype;
     hipStream_t st = c->stream;
     const int ab = c->ws.act_bytes;
+    // decode rows of the medium-M GEMMs travel in fragment order
+    const int pk = (decode && dt == MTP_DTYPE_BF16 && rows <= 256) ? 1 : 0;
     GemmArgs g{};
     g.dtype = dt;
     // LN1 output u -> q, K/V cache
-    g.epi = EPI_QKV; g.X = c->WS() + c->ws.u; g.ldx = d; g.M = rows;
+    g.epi = EPI_QKV; g.X = c->WS() + c->ws.u; g.ldx = d; g.M = rows; g.xpk = pk;
     g.W = c->lt(l, MTP_T_W_QKV); g.N = 3 * d; g.K = d; g.splits = 1;
     g.bias = (const float*)c->lt(l, MTP_T_B_QKV);
     g.q = c->ws_ptr<float>(c->ws.q); g.rows = c->ws_ptr<RowInfo>(c->ws.rows); g.kv = c->kv(l); g.d = d;
     HIPCHK(c, launch_rec(c, decode ? MTP_KCLASS_GEMM_QKV : 0, [g](hipStream_t s) { return gemm(s, g); }), "qkv gemm");
     // attention
     if (decode) {
-        HIPCHK(c, decode_attention(c, l, qt, true), "decode attention");
+        HIPCHK(c, decode_attention(c, l, qt, true, pk != 0), "decode attention");
     } else if (dt == MTP_DTYPE_BF16) {
         AttnMfmaArgs m{};
         m.mode = 1; m.n_tiles = n_tiles; m.Q = 0; m.qt = MTP_PREFILL_ROWS; m.st = c->ws_ptr<SeqState>(c->ws.state);
@@ -403,7 +408,7 @@ int run_layer(mtp_ctx* c, int l, int rows, int n_tiles, int qt, int split_len, i
     // out projection -> partials, residual + LN2
     const size_t sstride = (size_t)rows * d;
     g = GemmArgs{};
-    g.dtype = dt; g.epi = EPI_PARTIAL; g.X = c->WS() + c->ws.attn; g.ldx = d; g.M = rows;
+    g.dtype = dt; g.epi = EPI_PARTIAL; g.X = c->WS() + c->ws.attn; g.ldx = d; g.M = rows; g.xpk = pk;
     g.W = c->lt(l, MTP_T_W_O); g.N = d; g.K = d; g.splits = pick_splits(c, rows, d, d);
     g.out = c->WS() + c->ws.part; g.ldo = d; g.split_stride = sstride;
     HIPCHK(c, gemm(st, g), "out-proj gemm");
@@ -411,16 +416,17 @@ int run_layer(mtp_ctx* c, int l, int rows, int n_tiles, int qt, int split_len, i
     r.dtype = dt; r.n_rows = rows; r.d = d; r.h = c->ws_ptr<float>(c->ws.h); r.part = c->ws_ptr<float>(c->ws.part);
     r.n_split = g.splits; r.split_stride = sstride; r.bias = (const float*)c->lt(l, MTP_T_B_O);
     r.ln_g = (const float*)c->lt(l, MTP_T_LN2_G); r.ln_b = (const float*)c->lt(l, MTP_T_LN2_B); r.u = c->WS() + c->ws.u;
+    r.packed = pk;
     HIPCHK(c, resid_ln(st, r), "resid+ln2");
     // FFN1 + GELU
     g = GemmArgs{};
-    g.dtype = dt; g.epi = EPI_GELU; g.X = c->WS() + c->ws.u; g.ldx = d; g.M = rows;
+    g.dtype = dt; g.epi = EPI_GELU; g.X = c->WS() + c->ws.u; g.ldx = d; g.M = rows; g.xpk = pk; g.opk = pk;
     g.W = c->lt(l, MTP_T_W_1); g.N = F; g.K = d; g.splits = 1;
     g.bias = (const float*)c->lt(l, MTP_T_B_1); g.out = c->WS() + c->ws.ffn; g.ldo = F;
     HIPCHK(c, launch_rec(c, decode ? MTP_KCLASS_GEMM_FFN1 : 0, [g](hipStream_t s) { return gemm(s, g); }), "ffn1 gemm");
     // FFN2 -> partials, residual + next LN1
     g = GemmArgs{};
-    g.dtype = dt; g.epi = EPI_PARTIAL; g.X = c->WS() + c->ws.ffn; g.ldx = F; g.M = rows;
+    g.dtype = dt; g.epi = EPI_PARTIAL; g.X = c->WS() + c->ws.ffn; g.ldx = F; g.M = rows; g.xpk = pk;
     g.W = c->lt(l, MTP_T_W_2); g.N = d; g.K = F; g.splits = pick_splits(c, rows, d, F);
     g.out = c->WS() + c->ws.part; g.ldo = d; g.split_stride = sstride;
     HIPCHK(c, launch_rec(c, decode ? MTP_KCLASS_GEMM_FFN2 : 0, [g](hipStream_t s) { return gemm(s, g); }), "ffn2 gemm");
@@ -431,6 +437,7 @@ int run_layer(mtp_ctx* c, int l, int rows, int n_tiles, int qt, int split_len, i
         r.ln_g = (const float*)c->lt(l + 1, MTP_T_LN1_G); r.ln_b = (const float*)c->lt(l + 1, MTP_T_LN1_B);
         r.u = c->WS() + c->ws.u;
     }
+    r.packed = pk;
     HIPCHK(c, resid_ln(st, r), "resid+ln1");
     (void)ab;
     return MTP_OK;
@@ -458,6 +465,7 @@ int enqueue_step(mtp_ctx* c, int K, int top_k) {
         e.emb_phone = c->wt(MTP_T_EMB_PHONE); e.emb_ac = c->wt(MTP_T_EMB_AC); e.pos = c->wt(MTP_T_POS);
         e.ln_g = (const float*)c->lt(0, MTP_T_LN1_G); e.ln_b = (const float*)c->lt(0, MTP_T_LN1_B);
         e.d = d; e.h = c->ws_ptr<float>(c->ws.h); e.u = c->WS() + c->ws.u;
+        e.packed = (dt == MTP_DTYPE_BF16 && rows <= 256) ? 1 : 0;   // as run_layer's decode rows
         HIPCHK(c, embed_ln(st, e), "embed");
         for (int l = 0; l < cf.n_layers; ++l) {
             int rc = run_layer(c, l, rows, B, qt, c->split_len, c->n_splits, true);
@@ -478,9 +486,10 @@ int enqueue_step(mtp_ctx* c, int K, int top_k) {
         f.dtype = dt; f.B = B; f.d = d; f.mode = 0; f.Q = Q; f.st = c->ws_ptr<SeqState>(c->ws.state);
         f.h = c->ws_ptr<float>(c->ws.h); f.hz = c->ws_ptr<float>(c->ws.hz);
         f.ln_g = (const float*)c->wt(MTP_T_LNF_G); f.ln_b = (const float*)c->wt(MTP_T_LNF_B); f.z = c->WS() + c->ws.z;
+        f.packed = (dt == MTP_DTYPE_BF16 && B <= 256) ? 1 : 0;
         HIPCHK(c, final_ln(st, f), "final ln");
         GemmArgs g{};
-        g.dtype = dt; g.epi = EPI_LOGITS; g.X = c->WS() + c->ws.z; g.ldx = d; g.M = B;
+        g.dtype = dt; g.epi = EPI_LOGITS; g.X = c->WS() + c->ws.z; g.ldx = d; g.M = B; g.xpk = f.packed;
         g.W = c->wt(MTP_T_W_HEADS); g.N = K * V; g.K = d; g.splits = 1;
         g.bias = (const float*)c->wt(MTP_T_B_HEADS); g.out = c->WS() + c->ws.logits; g.ldo = K * V;
         HIPCHK(c, launch_rec(c, MTP_KCLASS_HEADS, [g](hipStream_t s) { return gemm(s, g); }), "heads gemm");

@@ -468,7 +468,8 @@ __global__ __launch_bounds__(256) void attn_decode_merge(AttnDecArgs p) {
         float o = 0.f;
 #pragma unroll 8
         for (int s = 0; s < n_active; ++s) o = fmaf(s_w[s][i], base[(size_t)s * qt * PSTRIDE + i * PSTRIDE + 4 + dim], o);
-        ActIO<OutT>::store(out + (size_t)(b * p.Q + i) * p.ldo + head * 64 + dim, o / s_l[i]);
+        const int row = b * p.Q + i, col = head * 64 + dim;
+        ActIO<OutT>::store(out + (p.packed ? frag_off(row, col, p.ldo) : (size_t)row * p.ldo + col), o / s_l[i]);
     }
 }
 

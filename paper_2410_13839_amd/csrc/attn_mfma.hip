@@ -29,10 +29,12 @@ __device__ __forceinline__ uint32_t pk2(float a, float b) {
 //                                             after exp, so P never leaves registers
 // A CU streams only ~25 GB/s from HBM, so short splits spread a small batch's
 // keys over many CUs (64-key splits, 4 waves, at batch 1); long splits use up
-// to 16 waves.
+// to 16 waves.  With long splits each wave keeps PD of its 16-key groups in
+// flight (a register ring, rotated by unrolling), so a CU's outstanding KV
+// reads grow with PD instead of stalling on one round trip per chunk.
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
 
-template <int NW>
+template <int NW, int PD>
 __global__ __launch_bounds__(64 * NW) void attn_dec_kernel(AttnMfmaArgs p) {
     const int b = blockIdx.x, head = blockIdx.y, split = blockIdx.z;
     const int H = gridDim.y;
@@ -47,18 +49,21 @@ __global__ __launch_bounds__(64 * NW) void attn_dec_kernel(AttnMfmaArgs p) {
     const int kb = split * p.split_len;
     const int row0 = b * p.Q;
 
-    uint4 kf[2];
-    uint2 vf[4];
-    auto load_keys = [&](int c0) {
+    uint4 kf[PD][2];
+    uint2 vf[PD][4];
+    // every address is clamped to the sequence's block table, whose unused
+    // entries name page 0, so loads past the context stay in the pool
+    auto load_keys = [&](int u, int c0) {
         const int wk = c0 + 16 * wave;
         const bf16_t* kp = pool + p.kv.offset(b, min(wk + r, max_key), 0, head) + g * 8;
-        kf[0] = *reinterpret_cast<const uint4*>(kp);
-        kf[1] = *reinterpret_cast<const uint4*>(kp + 32);
+        kf[u][0] = *reinterpret_cast<const uint4*>(kp);
+        kf[u][1] = *reinterpret_cast<const uint4*>(kp + 32);
         const bf16_t* vp = pool + p.kv.vt_offset(b, min(wk + 4 * g, max_key & ~3), head);
 #pragma unroll
-        for (int dt = 0; dt < 4; ++dt) vf[dt] = *reinterpret_cast<const uint2*>(vp + (size_t)(16 * dt + r) * P);
+        for (int dt = 0; dt < 4; ++dt) vf[u][dt] = *reinterpret_cast<const uint2*>(vp + (size_t)(16 * dt + r) * P);
     };
-    load_keys(kb);
+#pragma unroll
+    for (int u = 0; u < PD; ++u) load_keys(u, kb + u * CH);
     float4 qa[2], qb[2];
     {
         const float* qp = p.q + (size_t)(row0 + min(r, p.Q - 1)) * p.ldq + head * 64 + g * 8;
@@ -86,12 +91,16 @@ __global__ __launch_bounds__(64 * NW) void attn_dec_kernel(AttnMfmaArgs p) {
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt) acc[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-    for (int c0 = kb; c0 < ke; c0 += CH) {
-        const uint4 k0 = kf[0], k1 = kf[1];
+    for (int cb = kb; cb < ke; cb += CH * PD) {
+#pragma unroll
+      for (int u = 0; u < PD; ++u) {
+        const int c0 = cb + u * CH;
+        if (c0 >= ke) break;                     // uniform over the workgroup
+        const uint4 k0 = kf[u][0], k1 = kf[u][1];
         uint2 v[4];
 #pragma unroll
-        for (int dt = 0; dt < 4; ++dt) v[dt] = vf[dt];
-        if (c0 + CH < ke) load_keys(c0 + CH);    // next chunk in flight (uniform branch)
+        for (int dt = 0; dt < 4; ++dt) v[dt] = vf[u][dt];
+        if (c0 + PD * CH < ke) load_keys(u, c0 + PD * CH);   // refill this ring slot (uniform branch)
         const int wk = c0 + 16 * wave;
         f32x4_t s = f32x4_t{0.f, 0.f, 0.f, 0.f};
         s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, k0), qf[0], s, 0, 0, 0);
@@ -136,6 +145,7 @@ __global__ __launch_bounds__(64 * NW) void attn_dec_kernel(AttnMfmaArgs p) {
             acc[dt] *= scale;
             acc[dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4_t, vv), pf, acc[dt], 0, 0, 0);
         }
+      }
     }
 
     // merge the NW waves' states
@@ -163,7 +173,8 @@ __global__ __launch_bounds__(64 * NW) void attn_dec_kernel(AttnMfmaArgs p) {
             Mq = fmaxf(Mq, s_m[w][q]);
         }
         if (p.n_splits == 1) {
-            p.out[(size_t)(row0 + q) * p.ldo + head * 64 + dim] = f32_to_bf16(o / L);
+            const int row = row0 + q, col = head * 64 + dim;
+            p.out[p.packed ? frag_off(row, col, p.ldo) : (size_t)row * p.ldo + col] = f32_to_bf16(o / L);
         } else {
             float* e = p.part + ((size_t)(b * H + head) * p.n_splits + split) * (p.qt * PSTR) + q * PSTR;
             e[4 + dim] = o;
@@ -175,18 +186,27 @@ __global__ __launch_bounds__(64 * NW) void attn_dec_kernel(AttnMfmaArgs p) {
     }
 }
 
-template <int NW>
-static hipError_t attn_dec_go(hipStream_t st, const AttnMfmaArgs& a) {
+template <int NW, int PD>
+static hipError_t attn_dec_go_pd(hipStream_t st, const AttnMfmaArgs& a) {
     const size_t lds = (size_t)NW * 64 * 17 * sizeof(float);
     static bool attr_set = false;
     if (!attr_set && lds > 48 * 1024) {
-        hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_dec_kernel<NW>),
+        hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_dec_kernel<NW, PD>),
                                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         if (err != hipSuccess) return err;
         attr_set = true;
     }
-    hipLaunchKernelGGL(attn_dec_kernel<NW>, dim3(a.n_tiles, a.kv.n_heads, a.n_splits), dim3(64 * NW), lds, st, a);
+    hipLaunchKernelGGL((attn_dec_kernel<NW, PD>), dim3(a.n_tiles, a.kv.n_heads, a.n_splits), dim3(64 * NW), lds, st, a);
     return hipGetLastError();
+}
+
+// Ring depth: two 16-key groups per wave once a split holds that many (a
+// third ring slot no longer fits 128 registers at 16 waves).
+template <int NW>
+static hipError_t attn_dec_go(hipStream_t st, const AttnMfmaArgs& a) {
+    const int groups = (a.split_len + 16 * NW - 1) / (16 * NW);
+    if (groups >= 2) return attn_dec_go_pd<NW, 2>(st, a);
+    return attn_dec_go_pd<NW, 1>(st, a);
 }
 
 // Prefill attention: one workgroup of 4 waves per (query tile, head); a tile

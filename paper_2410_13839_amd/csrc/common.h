@@ -61,6 +61,16 @@ __device__ __forceinline__ bf16_t f32_to_bf16(float f) {
     return (bf16_t)(u >> 16);
 }
 
+// Element (row, k) of a bf16 activation matrix with K columns (K a multiple
+// of 32) stored in MFMA fragment order, the order of the packed weights: 16 x
+// 32 blocks of 1 KB, block (row / 16, k / 32) at ((row / 16) * (K / 32) +
+// k / 32) * 512 elements, inside which lane r + 16 g holds row r's k = 8 g ..
+// 8 g + 7.  A wave loads one block as one contiguous 1 KB read (row-major
+// rows would be 16 separate 64-byte pieces).  Rows are padded to 16.
+__device__ __forceinline__ size_t frag_off(int row, int k, int K) {
+    return ((((size_t)(row >> 4) * (K >> 5) + (k >> 5)) * 64 + (row & 15) + 16 * ((k >> 3) & 3)) << 3) + (k & 7);
+}
+
 template <typename T> struct ActIO;
 template <> struct ActIO<float> {
     __device__ static __forceinline__ float load(const float* p) { return *p; }

@@ -66,11 +66,12 @@ struct EpiGelu {
     OutT* out;
     const float* bias;
     int ldo;
+    int pk;               // bf16 output in fragment order (K = ldo)
     __device__ __forceinline__ void store4(int m, int n, const float (&v)[4], int, int) const {
         float r[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) r[i] = gelu_erf(v[i] + bias[n + i]);
-        OutT* p = out + (size_t)m * ldo + n;
+        OutT* p = out + (pk ? frag_off(m, n, ldo) : (size_t)m * ldo + n);
         if constexpr (sizeof(OutT) == 2) {
             uint2 pk;
             pk.x = (uint32_t)f32_to_bf16(r[0]) | ((uint32_t)f32_to_bf16(r[1]) << 16);
@@ -103,72 +104,95 @@ struct EpiLogits {
 };
 
 // ---------------------------------------------------------------- medium bf16
-// Workgroup (x, y, z) = (16-column tile, 16*MT-row group, K split).  Wave w
-// takes k steps w, w + 16, ... of its split (32 k per step), up to MAXST at a
-// time, all loads of a round in flight together: the weight fragment (packed
-// order, one contiguous 1 KB wave load) and one 16 x 32 activation fragment
-// per row tile, rows beyond M read from the last valid row (never stored).
-// The wave index is made scalar so the step guards are uniform branches.
+// Workgroup (x, y, z) = (NT 16-column tiles, 16*MT-row group, K split).  Wave
+// w takes k steps w, w + 16, ... of its split (32 k per step), up to MAXST at
+// a time, all loads of a round in flight together: NT weight fragments
+// (packed order, each one contiguous 1 KB wave load) and one 16 x 32
+// activation fragment per row tile, which serves all NT column tiles (the
+// activations are re-read from L2 once per column group, so wider groups
+// cut that traffic).  Rows beyond M read the last valid row and column tiles
+// beyond N the last valid tile; neither is stored.  The wave index is made
+// scalar so the step guards are uniform branches.
 constexpr int GM_NW = 16;
 
-template <int MT, int MAXST, class Epi>
+template <int MT, int NT, int MAXST, int XP, class Epi>
 __global__ __launch_bounds__(64 * GM_NW) void gemm_med_bf16(const bf16_t* __restrict__ X, int ldx, int M,
                                                             const bf16_t* __restrict__ W, int N, int K,
                                                             int k_per_split, Epi epi) {
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int r = lane & 15, g = lane >> 4;
-    const int nt = blockIdx.x;
+    const int ntiles = (N + 15) >> 4;
+    const int nt0 = blockIdx.x * NT;
     const int m0 = blockIdx.y * 16 * MT;
     const int split = blockIdx.z;
     const int kb = split * k_per_split;
     const int nsteps = k_per_split >> 5;
-    const bf16_t* wp = W + ((size_t)nt * (K >> 5) + (kb >> 5)) * 512 + lane * 8;
+    const bf16_t* wp[NT];
+#pragma unroll
+    for (int j = 0; j < NT; ++j)
+        wp[j] = W + ((size_t)min(nt0 + j, ntiles - 1) * (K >> 5) + (kb >> 5)) * 512 + lane * 8;
+    // XP: X in fragment order (one contiguous 1 KB block per row tile and k
+    // step, rows padded to 16), else row-major
     const bf16_t* xp[MT];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
-        const int m = min(m0 + 16 * mt + r, M - 1);
-        xp[mt] = X + (size_t)m * ldx + kb + g * 8;
+        if (XP) {
+            const int t = min(m0 / 16 + mt, (M - 1) >> 4);
+            xp[mt] = X + ((size_t)t * (K >> 5) + (kb >> 5)) * 512 + lane * 8;
+        } else {
+            const int m = min(m0 + 16 * mt + r, M - 1);
+            xp[mt] = X + (size_t)m * ldx + kb + g * 8;
+        }
     }
-    f32x4_t acc[MT];
+    f32x4_t acc[NT][MT];
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < NT; ++j)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) acc[j][mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
     for (int s0 = wave; s0 < nsteps; s0 += GM_NW * MAXST) {
-        uint4 wv[MAXST];
+        uint4 wv[MAXST][NT];
         uint4 xv[MAXST][MT];
 #pragma unroll
         for (int u = 0; u < MAXST; ++u) {
             const int ss = s0 + GM_NW * u;
             if (ss < nsteps) {
-                wv[u] = *reinterpret_cast<const uint4*>(wp + (size_t)ss * 512);
 #pragma unroll
-                for (int mt = 0; mt < MT; ++mt) xv[u][mt] = *reinterpret_cast<const uint4*>(xp[mt] + ss * 32);
+                for (int j = 0; j < NT; ++j) wv[u][j] = *reinterpret_cast<const uint4*>(wp[j] + (size_t)ss * 512);
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt)
+                    xv[u][mt] = *reinterpret_cast<const uint4*>(xp[mt] + (XP ? (size_t)ss * 512 : (size_t)ss * 32));
             }
         }
 #pragma unroll
         for (int u = 0; u < MAXST; ++u) {
             if (s0 + GM_NW * u < nsteps) {
 #pragma unroll
-                for (int mt = 0; mt < MT; ++mt)
-                    acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, wv[u]),
-                                                                      __builtin_bit_cast(bf16x8_t, xv[u][mt]),
-                                                                      acc[mt], 0, 0, 0);
+                for (int j = 0; j < NT; ++j)
+#pragma unroll
+                    for (int mt = 0; mt < MT; ++mt)
+                        acc[j][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, wv[u][j]),
+                                                                             __builtin_bit_cast(bf16x8_t, xv[u][mt]),
+                                                                             acc[j][mt], 0, 0, 0);
             }
         }
     }
 
-    __shared__ f32x4_t red[GM_NW][MT][64];
+    __shared__ f32x4_t red[GM_NW][NT * MT][64];
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) red[wave][mt][lane] = acc[mt];
+    for (int j = 0; j < NT; ++j)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) red[wave][j * MT + mt][lane] = acc[j][mt];
     __syncthreads();
-    if (threadIdx.x < MT * 64) {
-        const int mt = threadIdx.x >> 6;
-        f32x4_t s = red[0][mt][lane];
+    for (int t = threadIdx.x; t < NT * MT * 64; t += 64 * GM_NW) {
+        const int jm = t >> 6, l = t & 63;
+        const int j = jm / MT, mt = jm - j * MT;
+        f32x4_t s = red[0][jm][l];
 #pragma unroll
-        for (int w = 1; w < GM_NW; ++w) s += red[w][mt][lane];
-        const int m = m0 + 16 * mt + r;
-        const int n = nt * 16 + 4 * g;
+        for (int w = 1; w < GM_NW; ++w) s += red[w][jm][l];
+        const int m = m0 + 16 * mt + (l & 15);
+        const int n = (nt0 + j) * 16 + 4 * (l >> 4);
         if (m < M && n < N) {
             float v[4] = {s[0], s[1], s[2], s[3]};
             epi.store4(m, n, v, split, min(4, N - n));
@@ -176,21 +200,37 @@ __global__ __launch_bounds__(64 * GM_NW) void gemm_med_bf16(const bf16_t* __rest
     }
 }
 
-template <int MT, class Epi>
+// Column tiles per workgroup: two, so every activation fragment serves two
+// weight fragments (the activations are re-read once per workgroup), with
+// the LDS reduction holding 16 waves x NT x MT tiles (at most 8).
+constexpr int GM_NT = 2;
+
+template <int MT, int XP, class Epi>
 static void launch_med(hipStream_t st, const bf16_t* X, int ldx, int M, const bf16_t* W, int N, int K, int splits,
                        Epi epi) {
+    constexpr int NT = GM_NT;
+    static_assert(NT * MT <= 8, "LDS reduction");
     const int kps = K / splits;
     const int per_wave = ((kps >> 5) + GM_NW - 1) / GM_NW;   // k steps per wave
-    dim3 grid((N + 15) / 16, (M + 16 * MT - 1) / (16 * MT), splits);
+    dim3 grid(((N + 15) / 16 + NT - 1) / NT, (M + 16 * MT - 1) / (16 * MT), splits);
     dim3 block(64 * GM_NW);
+    // one round of loads holds at most MAXST x (NT + MT) fragments per wave
+    constexpr int CAP = NT * MT >= 8 ? 2 : 4;
     if (per_wave <= 1)
-        hipLaunchKernelGGL((gemm_med_bf16<MT, 1, Epi>), grid, block, 0, st, X, ldx, M, W, N, K, kps, epi);
-    else if (per_wave == 2)
-        hipLaunchKernelGGL((gemm_med_bf16<MT, 2, Epi>), grid, block, 0, st, X, ldx, M, W, N, K, kps, epi);
+        hipLaunchKernelGGL((gemm_med_bf16<MT, NT, 1, XP, Epi>), grid, block, 0, st, X, ldx, M, W, N, K, kps, epi);
+    else if (per_wave == 2 || CAP == 2)
+        hipLaunchKernelGGL((gemm_med_bf16<MT, NT, 2, XP, Epi>), grid, block, 0, st, X, ldx, M, W, N, K, kps, epi);
     else if (per_wave == 3)
-        hipLaunchKernelGGL((gemm_med_bf16<MT, 3, Epi>), grid, block, 0, st, X, ldx, M, W, N, K, kps, epi);
+        hipLaunchKernelGGL((gemm_med_bf16<MT, NT, 3, XP, Epi>), grid, block, 0, st, X, ldx, M, W, N, K, kps, epi);
     else
-        hipLaunchKernelGGL((gemm_med_bf16<MT, 4, Epi>), grid, block, 0, st, X, ldx, M, W, N, K, kps, epi);
+        hipLaunchKernelGGL((gemm_med_bf16<MT, NT, 4, XP, Epi>), grid, block, 0, st, X, ldx, M, W, N, K, kps, epi);
+}
+
+template <int MT, class Epi>
+static void launch_med_x(hipStream_t st, const bf16_t* X, int ldx, int M, const bf16_t* W, int N, int K, int splits,
+                         int xpk, Epi epi) {
+    if (xpk) launch_med<MT, 1>(st, X, ldx, M, W, N, K, splits, epi);
+    else launch_med<MT, 0>(st, X, ldx, M, W, N, K, splits, epi);
 }
 
 // ---------------------------------------------------------------- tiled bf16
@@ -341,15 +381,16 @@ __global__ __launch_bounds__(256) void gemm_f32(const float* __restrict__ X, int
 // ------------------------------------------------------------------ launchers
 template <class Epi>
 static hipError_t launch_bf16(hipStream_t st, const bf16_t* X, int ldx, int M, const bf16_t* W, int N, int K,
-                              int splits, Epi epi) {
+                              int splits, int xpk, Epi epi) {
     const int kps = K / splits;
     if (M <= 16) {
-        launch_med<1>(st, X, ldx, M, W, N, K, splits, epi);
+        launch_med_x<1>(st, X, ldx, M, W, N, K, splits, xpk, epi);
     } else if (M <= 32) {
-        launch_med<2>(st, X, ldx, M, W, N, K, splits, epi);
+        launch_med_x<2>(st, X, ldx, M, W, N, K, splits, xpk, epi);
     } else if (M <= 256) {
-        launch_med<4>(st, X, ldx, M, W, N, K, splits, epi);
+        launch_med_x<4>(st, X, ldx, M, W, N, K, splits, xpk, epi);
     } else {
+        if (xpk) return hipErrorInvalidValue;
         dim3 grid((N + 127) / 128, (M + 127) / 128, splits);
         hipLaunchKernelGGL((gemm_tiled_bf16<128, 128, Epi>), grid, dim3(256), 0, st, X, ldx, M, W, N, K, kps, epi);
     }
@@ -372,9 +413,9 @@ int gemm_split_granule(int dtype, int M) {
 
 // Workgroups of one bf16 launch for M rows and N columns before K splitting.
 int gemm_tiles(int M, int N) {
-    if (M <= 16) return (N + 15) / 16;
-    if (M <= 32) return (N + 15) / 16;
-    if (M <= 256) return ((N + 15) / 16) * ((M + 63) / 64);
+    const int groups = ((N + 15) / 16 + GM_NT - 1) / GM_NT;
+    if (M <= 32) return groups;
+    if (M <= 256) return groups * ((M + 63) / 64);
     return ((N + 127) / 128) * ((M + 127) / 128);
 }
 
@@ -384,27 +425,27 @@ hipError_t gemm(hipStream_t st, const GemmArgs& a) {
     case EPI_QKV: {
         if (bf) {
             EpiQKV<bf16_t> e{a.q, a.bias, a.rows, a.kv, a.d};
-            return launch_bf16(st, (const bf16_t*)a.X, a.ldx, a.M, (const bf16_t*)a.W, a.N, a.K, 1, e);
+            return launch_bf16(st, (const bf16_t*)a.X, a.ldx, a.M, (const bf16_t*)a.W, a.N, a.K, 1, a.xpk, e);
         }
         EpiQKV<float> e{a.q, a.bias, a.rows, a.kv, a.d};
         return launch_f32(st, (const float*)a.X, a.ldx, a.M, (const float*)a.W, a.N, a.K, 1, e);
     }
     case EPI_GELU: {
         if (bf) {
-            EpiGelu<bf16_t> e{(bf16_t*)a.out, a.bias, a.ldo};
-            return launch_bf16(st, (const bf16_t*)a.X, a.ldx, a.M, (const bf16_t*)a.W, a.N, a.K, 1, e);
+            EpiGelu<bf16_t> e{(bf16_t*)a.out, a.bias, a.ldo, a.opk};
+            return launch_bf16(st, (const bf16_t*)a.X, a.ldx, a.M, (const bf16_t*)a.W, a.N, a.K, 1, a.xpk, e);
         }
-        EpiGelu<float> e{(float*)a.out, a.bias, a.ldo};
+        EpiGelu<float> e{(float*)a.out, a.bias, a.ldo, 0};
         return launch_f32(st, (const float*)a.X, a.ldx, a.M, (const float*)a.W, a.N, a.K, 1, e);
     }
     case EPI_PARTIAL: {
         EpiPartial e{(float*)a.out, a.ldo, a.split_stride};
-        if (bf) return launch_bf16(st, (const bf16_t*)a.X, a.ldx, a.M, (const bf16_t*)a.W, a.N, a.K, a.splits, e);
+        if (bf) return launch_bf16(st, (const bf16_t*)a.X, a.ldx, a.M, (const bf16_t*)a.W, a.N, a.K, a.splits, a.xpk, e);
         return launch_f32(st, (const float*)a.X, a.ldx, a.M, (const float*)a.W, a.N, a.K, a.splits, e);
     }
     case EPI_LOGITS: {
         EpiLogits e{(float*)a.out, a.bias, a.ldo};
-        if (bf) return launch_bf16(st, (const bf16_t*)a.X, a.ldx, a.M, (const bf16_t*)a.W, a.N, a.K, 1, e);
+        if (bf) return launch_bf16(st, (const bf16_t*)a.X, a.ldx, a.M, (const bf16_t*)a.W, a.N, a.K, 1, a.xpk, e);
         return launch_f32(st, (const float*)a.X, a.ldx, a.M, (const float*)a.W, a.N, a.K, 1, e);
     }
     }

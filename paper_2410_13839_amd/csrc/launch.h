@@ -16,6 +16,8 @@ struct GemmArgs {
     const void* X; int ldx; int M;
     const void* W; int N; int K;
     int splits;           // split-K factor (EPI_PARTIAL only)
+    int xpk;              // bf16 X in MFMA fragment order (frag_off), M <= 256 only
+    int opk;              // EPI_GELU: bf16 output in fragment order
     // epilogue operands
     const float* bias;
     void* out; int ldo; size_t split_stride;
@@ -57,6 +59,7 @@ struct AttnDecArgs {
     void* out; int ldo;
     float* part;               // [B][H][n_splits][qt][66]
     int merge;                 // 1: launch the merge kernel after the splits
+    int packed;                // bf16 out in fragment order (frag_off, K = ldo)
 };
 hipError_t attention_decode(hipStream_t st, const AttnDecArgs& a);
 // Only the merge of decode split partials (after attention_mfma).
@@ -76,6 +79,7 @@ struct AttnMfmaArgs {
     bf16_t* out; int ldo;
     float* part;
     int bidir;                 // prefill mode: 1 = every row sees its sequence's ctx_len keys
+    int packed;                // decode mode: out in fragment order (frag_off, K = ldo)
 };
 hipError_t attention_mfma(hipStream_t st, const AttnMfmaArgs& a);
 
@@ -129,6 +133,7 @@ struct EmbedArgs {
     int d;
     float* h;
     void* u;
+    int packed;                // bf16 u in fragment order (frag_off, K = d)
 };
 hipError_t embed_ln(hipStream_t st, const EmbedArgs& a);
 
@@ -141,6 +146,7 @@ struct ResidArgs {
     const float* bias;
     const float* ln_g; const float* ln_b;   // NULL: no LayerNorm
     void* u;
+    int packed;                // bf16 u in fragment order (frag_off, K = d)
 };
 hipError_t resid_ln(hipStream_t st, const ResidArgs& a);
 
@@ -156,6 +162,7 @@ struct FinalArgs {
     float* hz;
     const float* ln_g; const float* ln_b;
     void* z;                   // NULL: copy only
+    int packed;                // bf16 z in fragment order (frag_off, K = d)
 };
 hipError_t final_ln(hipStream_t st, const FinalArgs& a);
 

@@ -48,6 +48,32 @@ __device__ __forceinline__ void layer_norm_store(const float (&x)[MAXC], int d, 
         if (c < d) ActIO<OutT>::store(out + c, (x[j] - mean) * rstd * g[c] + b[c]);
     }
 }
+// The same LayerNorm, the output row `row` in fragment order (K = d).
+template <typename OutT>
+__device__ __forceinline__ void layer_norm_store_pk(const float (&x)[MAXC], int d, const float* g, const float* b,
+                                                    OutT* out, int row, float* red) {
+    const int tid = threadIdx.x;
+    float s = 0.f;
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j) {
+        int c = tid + 256 * j;
+        if (c < d) s += x[j];
+    }
+    const float mean = block_sum(s, red) / (float)d;
+    float v = 0.f;
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j) {
+        int c = tid + 256 * j;
+        if (c < d) { float t = x[j] - mean; v = fmaf(t, t, v); }
+    }
+    const float var = block_sum(v, red) / (float)d;
+    const float rstd = rsqrtf(var + 1e-5f);
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j) {
+        int c = tid + 256 * j;
+        if (c < d) ActIO<OutT>::store(out + frag_off(row, c, d), (x[j] - mean) * rstd * g[c] + b[c]);
+    }
+}
 }  // namespace
 
 template <typename WT>
@@ -78,7 +104,7 @@ __global__ __launch_bounds__(256) void embed_ln_kernel(EmbedArgs a) {
     if (pos < 0) {
         for (int c = tid; c < a.d; c += 256) {
             h[c] = 0.f;
-            ActIO<ActT>::store(u + c, 0.f);
+            ActIO<ActT>::store(a.packed ? reinterpret_cast<ActT*>(a.u) + frag_off(r, c, a.d) : u + c, 0.f);
         }
         return;
     }
@@ -96,7 +122,8 @@ __global__ __launch_bounds__(256) void embed_ln_kernel(EmbedArgs a) {
             h[c] = x[j];
         }
     }
-    layer_norm_store<ActT>(x, a.d, a.ln_g, a.ln_b, u, red);
+    if (a.packed) layer_norm_store_pk<ActT>(x, a.d, a.ln_g, a.ln_b, reinterpret_cast<ActT*>(a.u), r, red);
+    else layer_norm_store<ActT>(x, a.d, a.ln_g, a.ln_b, u, red);
 }
 
 // One row per workgroup, thread t owning the float4 column chunks t and
@@ -153,17 +180,18 @@ __global__ __launch_bounds__(256) void resid_ln_kernel(ResidArgs a) {
             for (int i = 0; i < 4; ++i) { const float t = x[4 * j + i] - mean; var = fmaf(t, t, var); }
         }
     const float rstd = rsqrtf(block_sum(var, red) / (float)d + 1e-5f);
-    ActT* u = reinterpret_cast<ActT*>(a.u) + (size_t)r * d;
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
         const int c = 4 * (tid + 256 * j);
         if (c < d) {
+            // four consecutive columns stay consecutive in fragment order
+            ActT* u = reinterpret_cast<ActT*>(a.u) + (a.packed ? frag_off(r, c, d) : (size_t)r * d + c);
             const float4 gv = *reinterpret_cast<const float4*>(a.ln_g + c);
             const float4 be = *reinterpret_cast<const float4*>(a.ln_b + c);
-            ActIO<ActT>::store(u + c + 0, (x[4 * j + 0] - mean) * rstd * gv.x + be.x);
-            ActIO<ActT>::store(u + c + 1, (x[4 * j + 1] - mean) * rstd * gv.y + be.y);
-            ActIO<ActT>::store(u + c + 2, (x[4 * j + 2] - mean) * rstd * gv.z + be.z);
-            ActIO<ActT>::store(u + c + 3, (x[4 * j + 3] - mean) * rstd * gv.w + be.w);
+            ActIO<ActT>::store(u + 0, (x[4 * j + 0] - mean) * rstd * gv.x + be.x);
+            ActIO<ActT>::store(u + 1, (x[4 * j + 1] - mean) * rstd * gv.y + be.y);
+            ActIO<ActT>::store(u + 2, (x[4 * j + 2] - mean) * rstd * gv.z + be.z);
+            ActIO<ActT>::store(u + 3, (x[4 * j + 3] - mean) * rstd * gv.w + be.w);
         }
     }
 }
@@ -194,7 +222,8 @@ __global__ __launch_bounds__(256) void final_ln_kernel(FinalArgs a) {
             }
         }
     }
-    if (a.z) layer_norm_store<ActT>(x, a.d, a.ln_g, a.ln_b, reinterpret_cast<ActT*>(a.z) + (size_t)b * a.d, red);
+    if (a.z && a.packed) layer_norm_store_pk<ActT>(x, a.d, a.ln_g, a.ln_b, reinterpret_cast<ActT*>(a.z), b, red);
+    else if (a.z) layer_norm_store<ActT>(x, a.d, a.ln_g, a.ln_b, reinterpret_cast<ActT*>(a.z) + (size_t)b * a.d, red);
 }
 
 hipError_t embed_ln(hipStream_t st, const EmbedArgs& a) {
