@@ -517,8 +517,9 @@ int enqueue_step(mtp_ctx* c, int K, int top_k) {
 // fixed per (batch, Q) so one captured graph serves every such step.  Small
 // batches split the keys into short ranges so that they spread over many CUs
 // (one CU streams only ~25 GB/s from HBM) and the out-projection merges the
-// partials of its own heads; larger batches aim at ~512 (sequence, head,
-// split) workgroups and merge in a separate launch.
+// partials of its own heads; larger batches aim at ~192 (sequence, head,
+// split) workgroups (one split once the batch's heads alone reach that, so
+// no merge launch) and merge in a separate launch otherwise.
 int plan_splits(mtp_ctx* c, int Q) {
     const mtp_config& cf = c->cfg;
     const int64_t max_ctx = std::max<int64_t>(c->plan_ctx, 1);
@@ -531,7 +532,7 @@ int plan_splits(mtp_ctx* c, int Q) {
         sl = std::max<int64_t>(128, ((max_ctx + merge_max - 1) / merge_max + 63) / 64 * 64);
     } else {
         const int64_t bh = B * cf.n_heads;
-        const int64_t want = std::max<int64_t>(1, (512 + bh - 1) / bh);
+        const int64_t want = std::max<int64_t>(1, (192 + bh - 1) / bh);
         sl = (max_ctx + want - 1) / want;
         sl = std::max<int64_t>(64, (sl + 63) / 64 * 64);
     }

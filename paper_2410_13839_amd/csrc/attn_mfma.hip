@@ -396,8 +396,15 @@ hipError_t attention_mfma(hipStream_t st, const AttnMfmaArgs& a) {
     if (a.mode == 0) {
         // decode: pending chunk of at most 16 rows per sequence
         if (a.Q < 1 || a.Q > 16 || a.qt < a.Q) return hipErrorInvalidValue;
-        if (a.split_len >= 256) return attn_dec_go<16>(st, a);
-        if (a.split_len >= 128) return attn_dec_go<8>(st, a);
+        // waves per workgroup: at most one per 16-key group of a split, and
+        // few enough that the whole grid is resident at once (16 waves per CU
+        // at this kernel's register count)
+        const int grid = a.n_tiles * a.kv.n_heads * a.n_splits;
+        const int nw_split = a.split_len >= 256 ? 16 : (a.split_len >= 128 ? 8 : 4);
+        const int nw_grid = grid <= 256 ? 16 : (grid <= 512 ? 8 : 4);
+        const int nw = nw_split < nw_grid ? nw_split : nw_grid;
+        if (nw == 16) return attn_dec_go<16>(st, a);
+        if (nw == 8) return attn_dec_go<8>(st, a);
         return attn_dec_go<4>(st, a);
     }
     // prefill: tiles of at most a.qt rows (16, 32 or 64), one split
