@@ -34,7 +34,7 @@ def _parse():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="valle_k4")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-secondary", action="store_true")
+    ap.add_argument("--no-secondary", action="store_true", help="skip the per-workload generation lines")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--copy-probe", action="store_true", help="also run a 256 MiB device copy (PMC calibration)")
     ap.add_argument("--replay-passes", type=int, default=20, help="passes of the per-class replay timing")
@@ -206,6 +206,102 @@ def cpu_baseline(wl, weights, logq, prompts, budget_s):
             "sample": f"{wl.name}: prefill of {len(prompts.phon[0]) + len(prompts.ac[0])} tokens "
                       f"({t_pre:.1f} s, excluded) then {steps} decode steps = {toks} tokens in {dt:.1f} s, "
                       f"float64 numpy on {threads} BLAS threads of {len(os.sched_getaffinity(0))} visible cores"}
+
+
+def trunk_params(m):
+    """Parameters one token streams through the trunk (per layer: QKV, out,
+    FFN1, FFN2 weights and biases, two LayerNorms)."""
+    d, F = m.d_model, m.d_ff
+    return m.n_layers * (4 * d * d + 2 * d * F + 3 * d + d + F + d + 4 * d)
+
+
+def head_params(m, K):
+    return K * m.vocab * (m.d_model + 1)
+
+
+def step_bytes(wl, ctx, trunk=True):
+    """Algorithmic HBM bytes of one decode step at batch-wide cached lengths
+    `ctx` (one entry per sequence): every weight of the trunk, the final LN
+    and the first K heads once (bf16 matrices, fp32 vectors counted as bf16
+    is close enough at these sizes), the K and V rows of every cached key of
+    every layer (4 d bytes per key per layer for a bf16 cache), the new
+    chunk's K and V, and the logits written and read."""
+    m = wl.model
+    d, L, B, K = m.d_model, m.n_layers, wl.batch, wl.K
+    wb = 2 if m.dtype == "bf16" else 4
+    heads = wb * (head_params(m, K) + 2 * d) + 8 * B * K * m.vocab
+    if not trunk:
+        return heads
+    kv_read = wb * 2 * L * d * float(np.sum(ctx))
+    kv_write = wb * 2 * L * d * B * K
+    return wb * trunk_params(m) + kv_read + kv_write + heads
+
+
+def prefill_flops(wl, lens):
+    """Trunk flops of a prefill over prompts of lengths `lens`: the GEMMs
+    (2 flops per weight per row) and causal attention (2 products of
+    len * (len + 1) / 2 key-query pairs x d per layer)."""
+    m = wl.model
+    rows = float(np.sum(lens))
+    attn = sum(2.0 * 2.0 * (n * (n + 1) / 2.0) * m.d_model for n in lens) * m.n_layers
+    return 2.0 * rows * (trunk_params(m) - m.n_layers * (m.d_ff + 9 * m.d_model)) + attn
+
+
+def bench_config(torch, name, weights_cache, logq):
+    """One workload end to end: a warm-up generation, then one timed prefill
+    and one timed full generation (every decode step until all sequences
+    finish), HIP events on the library stream.  Reports codec tokens/s, the
+    step time, the whole step's algorithmic bytes against the HBM peak and
+    the prefill's flops against the bf16 MFMA peak."""
+    from paper_2410_13839_amd.binding import Session
+    from paper_2410_13839_amd.workloads import WORKLOADS, make_prompts, make_weights
+    wl = WORKLOADS[name]
+    key = wl.model
+    if key not in weights_cache:
+        weights_cache.clear()
+        weights_cache[key] = make_weights(wl.model)
+    w = weights_cache[key]
+    pr = make_prompts(wl)
+    s = Session(wl.model, w, logq, max_batch=wl.batch, max_prompt=wl.max_prompt, max_new=wl.max_new,
+                eos_min=wl.eos_min, topk_max=max(8, wl.top_k))
+    per_gen = _steps_per_generation(wl)
+    st = s.stream
+    lens = [len(p) + len(a) for p, a in zip(pr.phon, pr.ac)]
+    res = None
+    for rep in range(2):
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        ev[0].record(st)
+        s.prefill(pr.phon, pr.ac)
+        ev[1].record(st)
+        for _ in range(per_gen):
+            s.step_async(wl.K, wl.top_k)
+        ev[2].record(st)
+        torch.cuda.synchronize()
+        pre_ms, dec_ms = ev[0].elapsed_time(ev[1]), ev[1].elapsed_time(ev[2])
+        gen = s.seq_state()["gen"]
+        res = (pre_ms, dec_ms, int(gen.sum()))
+    s.close()
+    del s
+    torch.cuda.empty_cache()
+    pre_ms, dec_ms, toks = res
+    # the first step after the prefill runs the heads only; step i >= 1 runs
+    # the K pending rows over the prompt and the K (i - 1) tokens before them
+    tot_bytes = sum(step_bytes(wl, [n + wl.K * i for n in lens], trunk=i > 0) for i in range(per_gen))
+    us_step = dec_ms * 1000.0 / per_gen
+    fl = prefill_flops(wl, lens)
+    out = {"workload": f"{wl.name}: {wl.description}", "batch": wl.batch, "K": wl.K, "top_k": wl.top_k,
+           "dtype": wl.model.dtype, "steps": per_gen, "tokens": toks,
+           "tokens_per_s": round(toks / (dec_ms * 1e-3), 1), "us_per_step": round(us_step, 2),
+           "ms_per_token_per_seq": round(dec_ms / (toks / wl.batch), 5),
+           "step_algorithmic_bytes_avg": int(tot_bytes / per_gen),
+           "step_hbm_GB_s": round(tot_bytes / (dec_ms * 1e-3) / 1e9, 1),
+           "step_hbm_frac": round(tot_bytes / (dec_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+           "prefill_rows": int(np.sum(lens)), "prefill_ms": round(pre_ms, 3),
+           "prefill_tflops": round(fl / (pre_ms * 1e-3) / 1e12, 1),
+           "prefill_mfma_frac_bf16": round(fl / (pre_ms * 1e-3) / 2.5e15, 4) if wl.model.dtype == "bf16" else None}
+    print(f"[bench] config {name}: {out}", file=sys.stderr, flush=True)
+    return out
 
 
 def bench_qest(torch, reps, cpu):
@@ -418,21 +514,13 @@ def main():
     del sess
     torch.cuda.empty_cache()
 
-    secondary = None
+    configs = None
     if not args.no_secondary and args.workload == "valle_k4":
-        wl2 = WORKLOADS["valle_b32"]
-        pr2 = make_prompts(wl2)
-        s2 = Session(wl2.model, weights, logq, max_batch=wl2.batch, max_prompt=wl2.max_prompt,
-                     max_new=wl2.max_new, eos_min=wl2.eos_min, topk_max=8)
-        steps2 = _steps_per_generation(wl2)
-        ms2, tok2 = time_decode(s2, wl2, pr2, steps2, 10, torch)
-        secondary = {"workload": wl2.name, "batch": wl2.batch, "K": wl2.K, "top_k": wl2.top_k, "steps": steps2,
-                     "tokens_per_s": round(tok2 / (ms2 / 1000.0), 1), "ms_per_step": round(ms2 / steps2, 4),
-                     "ms_per_token_per_seq": round(ms2 / (tok2 / wl2.batch), 4)}
-        print(f"[bench] {wl2.name}: {secondary}", file=sys.stderr, flush=True)
-        s2.close()
-        del s2
-        torch.cuda.empty_cache()
+        configs = []
+        wcache = {}
+        for name in ("tiny", "valle_k4", "valle_k8", "valle_b32", "long_b8"):
+            configs.append(bench_config(torch, name, wcache, logq))
+        wcache.clear()
 
     qest = None
     if not args.no_qest:
@@ -465,7 +553,7 @@ def main():
         "kernels": kernels,
         "cpu_baseline": cpu,
         "selection_variants": variants,
-        "secondary": secondary,
+        "configs": configs,
         "q_estimation": qest,
         "nar": nar,
         "paper_context": "paper reports 20.5 -> 4.5 ms/token (x4.56, VALL-E, 8 heads) on unstated inference hardware",

@@ -376,8 +376,8 @@ int run_layer(mtp_ctx* c, int l, int rows, int n_tiles, int qt, int split_len, i
     const int d = cf.d_model, F = cf.d_ff, dt = cf.dtype;
     hipStream_t st = c->stream;
     const int ab = c->ws.act_bytes;
-    // decode rows of the medium-M GEMMs travel in fragment order
-    const int pk = (decode && dt == MTP_DTYPE_BF16 && rows <= 256) ? 1 : 0;
+    // bf16 activations travel between kernels in MFMA fragment order
+    const int pk = dt == MTP_DTYPE_BF16 ? 1 : 0;
     GemmArgs g{};
     g.dtype = dt;
     // LN1 output u -> q, K/V cache
@@ -395,6 +395,7 @@ int run_layer(mtp_ctx* c, int l, int rows, int n_tiles, int qt, int split_len, i
         m.tiles = c->ws_ptr<int2>(c->ws.tiles); m.rows = c->ws_ptr<RowInfo>(c->ws.rows);
         m.q = c->ws_ptr<float>(c->ws.q); m.ldq = d; m.kv = c->kv(l); m.split_len = 1 << 30; m.n_splits = 1;
         m.out = (bf16_t*)(c->WS() + c->ws.attn); m.ldo = d; m.part = nullptr; m.bidir = bidir ? 1 : 0;
+        m.packed = pk;
         HIPCHK(c, attention_mfma(st, m), "prefill attention");
     } else {
         AttnArgs a{};
@@ -465,7 +466,7 @@ int enqueue_step(mtp_ctx* c, int K, int top_k) {
         e.emb_phone = c->wt(MTP_T_EMB_PHONE); e.emb_ac = c->wt(MTP_T_EMB_AC); e.pos = c->wt(MTP_T_POS);
         e.ln_g = (const float*)c->lt(0, MTP_T_LN1_G); e.ln_b = (const float*)c->lt(0, MTP_T_LN1_B);
         e.d = d; e.h = c->ws_ptr<float>(c->ws.h); e.u = c->WS() + c->ws.u;
-        e.packed = (dt == MTP_DTYPE_BF16 && rows <= 256) ? 1 : 0;   // as run_layer's decode rows
+        e.packed = dt == MTP_DTYPE_BF16 ? 1 : 0;   // fragment order, as in run_layer
         HIPCHK(c, embed_ln(st, e), "embed");
         for (int l = 0; l < cf.n_layers; ++l) {
             int rc = run_layer(c, l, rows, B, qt, c->split_len, c->n_splits, true);
@@ -486,7 +487,7 @@ int enqueue_step(mtp_ctx* c, int K, int top_k) {
         f.dtype = dt; f.B = B; f.d = d; f.mode = 0; f.Q = Q; f.st = c->ws_ptr<SeqState>(c->ws.state);
         f.h = c->ws_ptr<float>(c->ws.h); f.hz = c->ws_ptr<float>(c->ws.hz);
         f.ln_g = (const float*)c->wt(MTP_T_LNF_G); f.ln_b = (const float*)c->wt(MTP_T_LNF_B); f.z = c->WS() + c->ws.z;
-        f.packed = (dt == MTP_DTYPE_BF16 && B <= 256) ? 1 : 0;
+        f.packed = dt == MTP_DTYPE_BF16 ? 1 : 0;
         HIPCHK(c, final_ln(st, f), "final ln");
         GemmArgs g{};
         g.dtype = dt; g.epi = EPI_LOGITS; g.X = c->WS() + c->ws.z; g.ldx = d; g.M = B; g.xpk = f.packed;
@@ -749,6 +750,7 @@ int mtp_prefill(mtp_ctx* c, int B, const int32_t* phon, const int32_t* phon_len,
     e.emb_phone = c->wt(MTP_T_EMB_PHONE); e.emb_ac = c->wt(MTP_T_EMB_AC); e.pos = c->wt(MTP_T_POS);
     e.ln_g = (const float*)c->lt(0, MTP_T_LN1_G); e.ln_b = (const float*)c->lt(0, MTP_T_LN1_B);
     e.d = d; e.h = c->ws_ptr<float>(c->ws.h); e.u = c->WS() + c->ws.u;
+    e.packed = dt == MTP_DTYPE_BF16 ? 1 : 0;
     HIPCHK(c, embed_ln(st, e), "prefill embed");
     for (int l = 0; l < cf.n_layers; ++l) {
         int rc = run_layer(c, l, rows, n_tiles, MTP_ATTN_QT, 1 << 30, 1, false);
@@ -977,6 +979,7 @@ int mtp_nar_run(mtp_ctx* c) {
         e.stage_vec = (const float*)c->wt(MTP_T_STAGE);
         e.ln_g = (const float*)c->lt(0, MTP_T_LN1_G); e.ln_b = (const float*)c->lt(0, MTP_T_LN1_B);
         e.h = c->ws_ptr<float>(c->ws.h); e.u = c->WS() + c->ws.u;
+        e.packed = dt == MTP_DTYPE_BF16 ? 1 : 0;
         HIPCHK(c, nar_embed_ln(st, e), "nar embed");
         for (int l = 0; l < cf.n_layers; ++l) {
             const int rc = run_layer(c, l, rows, c->nar_tiles, MTP_ATTN_QT, 1 << 30, 1, false, true);
@@ -985,10 +988,11 @@ int mtp_nar_run(mtp_ctx* c) {
         RowsLnArgs r{};
         r.dtype = dt; r.n_rows = rows; r.d = d; r.h = c->ws_ptr<float>(c->ws.h);
         r.ln_g = (const float*)c->wt(MTP_T_LNF_G); r.ln_b = (const float*)c->wt(MTP_T_LNF_B); r.u = c->WS() + c->ws.u;
+        r.packed = dt == MTP_DTYPE_BF16 ? 1 : 0;
         HIPCHK(c, rows_ln(st, r), "nar final ln");
         float* lg = c->ws_ptr<float>(c->ws.nar_logits) + (size_t)s * c->ws.m_pre * cb;
         GemmArgs g{};
-        g.dtype = dt; g.epi = EPI_LOGITS; g.X = c->WS() + c->ws.u; g.ldx = d; g.M = rows;
+        g.dtype = dt; g.epi = EPI_LOGITS; g.X = c->WS() + c->ws.u; g.ldx = d; g.M = rows; g.xpk = r.packed;
         g.W = (const char*)c->wt(MTP_T_W_HEADS) + (size_t)s * cb * d * esz; g.N = cb; g.K = d; g.splits = 1;
         g.bias = (const float*)c->wt(MTP_T_B_HEADS) + (size_t)s * cb; g.out = lg; g.ldo = cb;
         HIPCHK(c, gemm(st, g), "nar head gemm");

@@ -373,7 +373,8 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(AttnMfmaArgs p) {
             L += s_l[w][q];
             Mq = fmaxf(Mq, s_m[w][q]);
         }
-        p.out[(size_t)(row0 + q) * p.ldo + head * 64 + dim] = f32_to_bf16(o / L);
+        const int row = row0 + q, col = head * 64 + dim;
+        p.out[p.packed ? frag_off(row, col, p.ldo) : (size_t)row * p.ldo + col] = f32_to_bf16(o / L);
     }
 }
 

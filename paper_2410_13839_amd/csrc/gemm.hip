@@ -12,8 +12,8 @@
 //    each wave loading its own activation fragments from L2 (no LDS staging:
 //    no two waves read the same k), and one LDS reduction over the waves
 //    precedes the epilogue.  The grid is sized so every CU streams.
-//  * gemm_tiled_bf16: M > 256 (prefill).  LDS double-buffered
-//    BMxBN tiles, BK = 64, 2x2 waves of v_mfma_f32_16x16x32_bf16.
+//  * gemm_big_bf16: M > 256 (prefill, NAR).  256 x 256 tiles on MFMA with
+//    both operands streamed global -> LDS in fragment order.
 //  * gemm_f32: the fp32 model; LDS-tiled VALU FMA.
 #include "common.h"
 #include "launch.h"
@@ -233,112 +233,188 @@ static void launch_med_x(hipStream_t st, const bf16_t* X, int ldx, int M, const 
     else launch_med<MT, 0>(st, X, ldx, M, W, N, K, splits, epi);
 }
 
-// ---------------------------------------------------------------- tiled bf16
-template <int BM, int BN, class Epi>
-__global__ __launch_bounds__(256) void gemm_tiled_bf16(const bf16_t* __restrict__ X, int ldx, int M,
-                                                       const bf16_t* __restrict__ W, int N, int K,
-                                                       int k_per_split, Epi epi) {
-    constexpr int BK = 64;
-    constexpr int LDSK = BK + 8;           // padded row (bf16 elements)
-    constexpr int TM = BM / 32;            // 16-row MFMA tiles per wave along m
-    constexpr int TN = BN / 32;            // along n
-    constexpr int XCH = BM * BK / 8 / 256; // 16-byte chunks per thread per stage
-    constexpr int WCH = BN * BK / 8 / 256;
-    static_assert(XCH >= 1 && WCH >= 1, "tile too small");
-    __shared__ __attribute__((aligned(16))) bf16_t Xs[2][BM][LDSK];
-    __shared__ __attribute__((aligned(16))) bf16_t Ws[2][BN][LDSK];
+// ---------------------------------------------------------------- large bf16
+// M > 256 (prefill, NAR).  Tiles of 256 rows x BN columns (BN = 256 or 128),
+// 4 waves in a 2 x 2 grid each owning 128 x BN/2 outputs as 8 x BN/32
+// v_mfma_f32_16x16x32_bf16 tiles (accumulators 256 or 128 registers).  Both
+// operands are in fragment order (activations written so by their producers,
+// weights packed at load), so a 16 x 32 fragment is one contiguous 1 KB; it
+// travels global -> LDS by one global_load_lds_dwordx4 per wave (lane l's 16
+// bytes land at byte 16 l, the order the MFMA operand read wants: every
+// ds_read_b128 is conflict free) with no register staging.  K advances 32 per
+// stage through NS = 4 LDS stages, NS - 1 of them in flight while one is
+// consumed.  Each stage buffer is its own LDS object and the stage loop is
+// unrolled by NS, so the compiler's LDS-DMA waits see which buffer a read
+// touches.  Workgroups are numbered so that the ones sharing an XCD (the
+// dispatcher deals workgroups to the 8 XCDs in turn) take neighbouring tiles
+// of one row band, which they share through that XCD's L2.
+constexpr int GB_NS = 4;
 
-    const int tid = threadIdx.x;
-    const int lane = tid & 63, wave = tid >> 6;
-    const int r = lane & 15, g = lane >> 4;
-    const int wm = wave >> 1, wn = wave & 1;
-    const int m0 = blockIdx.y * BM;
-    const int n0 = blockIdx.x * BN;
-    const int split = blockIdx.z;
-    const int kb = split * k_per_split;
-    const int nk = k_per_split / BK;
+__device__ __forceinline__ constexpr int vmcnt_imm(int n) {
+    // s_waitcnt immediate: vmcnt = n, expcnt and lgkmcnt not waited on
+    return (n & 15) | (((n >> 4) & 3) << 14) | (7 << 4) | (15 << 8);
+}
 
-    uint4 xr[XCH], wr[WCH];
-    auto gload = [&](int kt) {
-        const int k0 = kb + kt * BK;
-#pragma unroll
-        for (int c = 0; c < XCH; ++c) {
-            int ch = tid + c * 256;
-            int row = ch >> 3, col = (ch & 7) * 8;
-            int m = m0 + row;
-            xr[c] = (m < M) ? *reinterpret_cast<const uint4*>(X + (size_t)m * ldx + k0 + col) : make_uint4(0, 0, 0, 0);
-        }
-        // W tile in the packed fragment order: each wave load is one 1 KB
-        // fragment (16 rows x 32 columns); fragment t of the tile is row block
-        // t / 2, column block t % 2 (the row-block test is uniform per wave)
-#pragma unroll
-        for (int c = 0; c < WCH; ++c) {
-            const int ch = tid + c * 256;
-            const int t = ch >> 6, l = ch & 63;
-            const int rt = t >> 1, fk = t & 1;
-            wr[c] = (n0 + rt * 16 < N)
-                        ? *reinterpret_cast<const uint4*>(W + ((size_t)((n0 >> 4) + rt) * (K >> 5) + (k0 >> 5) + fk) * 512 + l * 8)
-                        : make_uint4(0, 0, 0, 0);
-        }
-    };
-    auto sstore = [&](int buf) {
-#pragma unroll
-        for (int c = 0; c < XCH; ++c) {
-            int ch = tid + c * 256;
-            *reinterpret_cast<uint4*>(&Xs[buf][ch >> 3][(ch & 7) * 8]) = xr[c];
-        }
-#pragma unroll
-        for (int c = 0; c < WCH; ++c) {
-            const int ch = tid + c * 256;
-            const int t = ch >> 6, l = ch & 63;
-            *reinterpret_cast<uint4*>(&Ws[buf][(t >> 1) * 16 + (l & 15)][(t & 1) * 32 + (l >> 4) * 8]) = wr[c];
-        }
-    };
+// Workgroup barrier without the memory fence __syncthreads() adds: that
+// fence waits for every outstanding global load, the stages still in flight
+// included.  The explicit vmcnt wait before it covers the stage consumed.
+__device__ __forceinline__ void gb_barrier() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
 
-    f32x4_t acc[TN][TM];
-#pragma unroll
-    for (int i = 0; i < TN; ++i)
-#pragma unroll
-        for (int j = 0; j < TM; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+template <int BN, int NWV, class Epi>
+__global__ __launch_bounds__(64 * NWV) void gemm_big_bf16(const bf16_t* __restrict__ X, int M,
+                                                          const bf16_t* __restrict__ W, int N, int K, int k_per_split,
+                                                          int tiles_m, int tiles_n, Epi epi) {
+    constexpr int FM = 16, FN = BN / 16;        // 16-row fragments of a stage
+    constexpr int NF = FM + FN;                 // fragments per stage (one 32-k step)
+    constexpr int NL = NF / NWV;                // global_load_lds per wave per stage
+    constexpr int WGN = NWV / 2;                // waves along n (two along m)
+    constexpr int WFM = FM / 2, WFN = FN / WGN; // fragments per wave
+    static_assert(NF % NWV == 0 && WFM == 8 && WFN >= 1, "tile shape");
+    typedef __attribute__((address_space(3))) void lds_void;
+    __shared__ __attribute__((aligned(1024))) bf16_t s0[NF * 512];
+    __shared__ __attribute__((aligned(1024))) bf16_t s1[NF * 512];
+    __shared__ __attribute__((aligned(1024))) bf16_t s2[NF * 512];
+    __shared__ __attribute__((aligned(1024))) bf16_t s3[NF * 512];
 
-    gload(0);
-    sstore(0);
-    __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-        const int buf = kt & 1;
-        if (kt + 1 < nk) gload(kt + 1);
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wm = wave / WGN, wn = wave - wm * WGN;
+    // tile of this workgroup: XCD x (= bid % 8) takes the x-th eighth of the
+    // tiles in row-band order (n fastest)
+    const int ntile = tiles_m * tiles_n;
+    const int bid = blockIdx.x;
+    const int per = (ntile + 7) >> 3;
+    const int t = (bid & 7) * per + (bid >> 3);
+    if (t >= ntile) return;                     // uniform: whole workgroup
+    const int tm = t / tiles_n, tn = t - tm * tiles_n;
+    const int mfr0 = tm * FM, nfr0 = tn * FN;   // first 16-row fragment of each operand
+    const int mfr_last = ((M + 15) >> 4) - 1, nfr_last = ((N + 15) >> 4) - 1;
+    const int split = blockIdx.y;
+    const int ks0 = (split * k_per_split) >> 5; // first 32-k step
+    const int nst = k_per_split >> 5;
+    const int K32 = K >> 5;
+
+    // fragment f of a stage: f < FM is activation rows 16 f.., else weight
+    // rows 16 (f - FM)..; wave w issues f = w, w + NWV, ...
+    const bf16_t* src[NL];
 #pragma unroll
-        for (int kk = 0; kk < BK / 32; ++kk) {
-            bf16x8_t a[TN], b[TM];
-#pragma unroll
-            for (int i = 0; i < TN; ++i)
-                a[i] = *reinterpret_cast<const bf16x8_t*>(&Ws[buf][wn * (BN / 2) + i * 16 + r][kk * 32 + g * 8]);
-#pragma unroll
-            for (int j = 0; j < TM; ++j)
-                b[j] = *reinterpret_cast<const bf16x8_t*>(&Xs[buf][wm * (BM / 2) + j * 16 + r][kk * 32 + g * 8]);
-#pragma unroll
-            for (int i = 0; i < TN; ++i)
-#pragma unroll
-                for (int j = 0; j < TM; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-        }
-        if (kt + 1 < nk) {
-            sstore(buf ^ 1);
-        }
-        __syncthreads();
+    for (int i = 0; i < NL; ++i) {
+        const int f = wave + NWV * i;
+        const bf16_t* base;
+        if (f < FM) base = X + (size_t)min(mfr0 + f, mfr_last) * K32 * 512;
+        else base = W + (size_t)min(nfr0 + f - FM, nfr_last) * K32 * 512;
+        src[i] = base + (size_t)ks0 * 512 + lane * 8;
     }
+    auto issue = [&](bf16_t* buf, int st) {
+#pragma unroll
+        for (int i = 0; i < NL; ++i)
+            __builtin_amdgcn_global_load_lds((const void*)(src[i] + (size_t)st * 512),
+                                             (lds_void*)(buf + (wave + NWV * i) * 512), 16, 0, 0);
+    };
 
+    f32x4_t acc[WFN][WFM];
 #pragma unroll
-    for (int i = 0; i < TN; ++i)
+    for (int i = 0; i < WFN; ++i)
 #pragma unroll
-        for (int j = 0; j < TM; ++j) {
-            const int n = n0 + wn * (BN / 2) + i * 16 + 4 * g;
-            const int m = m0 + wm * (BM / 2) + j * 16 + r;
+        for (int j = 0; j < WFM; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+    // Operand reads are written as ds_read_b128 in asm: the compiler cannot
+    // tell the stage being read from the stages the LDS DMA is still filling
+    // and would wait for every load in flight before each read.  The stage
+    // read is complete (the vmcnt wait and barrier before it); the reads
+    // return in order, so after lgkmcnt(4) the weight fragments and the first
+    // four activation fragments are in (half the products), after lgkmcnt(0)
+    // the rest.  Empty asm statements after each wait hand the registers on
+    // to the MFMAs, which therefore cannot be scheduled before the wait.
+    auto compute = [&](const bf16_t* buf) {
+        const uint32_t lb = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) bf16_t*)buf + lane * 16;
+        const uint32_t la = lb + (FM + wn * WFN) * 1024, lbm = lb + wm * WFM * 1024;
+        bf16x8_t a[WFN], b[WFM];
+#pragma unroll
+        for (int i = 0; i < WFN; ++i)
+            asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(a[i]) : "v"(la), "i"(i * 1024));
+#pragma unroll
+        for (int j = 0; j < WFM; ++j)
+            asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(b[j]) : "v"(lbm), "i"(j * 1024));
+        asm volatile("s_waitcnt lgkmcnt(4)" ::: "memory");
+#pragma unroll
+        for (int i = 0; i < WFN; ++i) asm volatile("" : "+v"(a[i]));
+#pragma unroll
+        for (int j = 0; j < 4; ++j) asm volatile("" : "+v"(b[j]));
+#pragma unroll
+        for (int i = 0; i < WFN; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+        for (int j = 4; j < 8; ++j) asm volatile("" : "+v"(b[j]));
+#pragma unroll
+        for (int i = 0; i < WFN; ++i)
+#pragma unroll
+            for (int j = 4; j < 8; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    };
+
+    // prologue: stages 0 .. NS-2 in flight
+    if (0 < nst) issue(s0, 0);
+    if (1 < nst) issue(s1, 1);
+    if (2 < nst) issue(s2, 2);
+    // step st: wait for stage st (the NS-2 later stages may stay in flight),
+    // barrier (stage st visible to all waves, and every wave is done with the
+    // buffer stage st + NS - 1 refills), refill, consume
+#define GB_STEP(BUF, NEXT, U)                                                          \
+    {                                                                                  \
+        const int st = st0 + (U);                                                      \
+        if (st < nst) {                                                                \
+            if (st + 2 < nst) __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * NL));           \
+            else if (st + 1 < nst) __builtin_amdgcn_s_waitcnt(vmcnt_imm(NL));          \
+            else __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));                             \
+            gb_barrier();                                                              \
+            if (st + GB_NS - 1 < nst) issue(NEXT, st + GB_NS - 1);                     \
+            compute(BUF);                                                              \
+        }                                                                              \
+    }
+    for (int st0 = 0; st0 < nst; st0 += GB_NS) {
+        GB_STEP(s0, s3, 0)
+        GB_STEP(s1, s0, 1)
+        GB_STEP(s2, s1, 2)
+        GB_STEP(s3, s2, 3)
+    }
+#undef GB_STEP
+
+    // epilogue: lane (r, g) of tile (i, j) holds outputs n = 4 g .. 4 g + 3
+    // of weight fragment i, row m = r of activation fragment j
+    const int r = lane & 15, g = lane >> 4;
+#pragma unroll
+    for (int i = 0; i < WFN; ++i)
+#pragma unroll
+        for (int j = 0; j < WFM; ++j) {
+            const int n = (nfr0 + wn * WFN + i) * 16 + 4 * g;
+            const int m = (mfr0 + wm * WFM + j) * 16 + r;
             if (m < M && n < N) {
                 float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
                 epi.store4(m, n, v, split, min(4, N - n));
             }
         }
+}
+
+template <int BN, int NWV, class Epi>
+static hipError_t launch_big(hipStream_t st, const bf16_t* X, int M, const bf16_t* W, int N, int K, int splits,
+                             Epi epi) {
+    const int kps = K / splits;
+    if (kps % 32) return hipErrorInvalidValue;
+    const int tm = (M + 255) / 256, tn = (N + BN - 1) / BN;
+    const int ntile = tm * tn;
+    // the tile numbering deals eighths of the tiles to the XCDs: the grid is
+    // 8 x ceil(tiles / 8) workgroups, the surplus ones return at once
+    dim3 grid(8 * ((ntile + 7) / 8), splits);
+    hipLaunchKernelGGL((gemm_big_bf16<BN, NWV, Epi>), grid, dim3(64 * NWV), 0, st, X, M, W, N, K, kps, tm, tn, epi);
+    return hipGetLastError();
 }
 
 // ----------------------------------------------------------------- fp32 VALU
@@ -379,20 +455,33 @@ __global__ __launch_bounds__(256) void gemm_f32(const float* __restrict__ X, int
 }
 
 // ------------------------------------------------------------------ launchers
+// Tile width of the large-M kernel for an M x N product (M > 256): 256 when
+// that gives at least 128 tiles (half the CUs), else 128 when that gives 64,
+// else 0: the product is too small for either and goes to the medium kernel
+// (64-row groups, one workgroup per 32 columns).
+static int big_tile_n(int M, int N) {
+    const int tm = (M + 255) / 256;
+    if (tm * ((N + 255) / 256) >= 128) return 256;
+    if (tm * ((N + 127) / 128) >= 64) return 128;
+    return 0;
+}
 template <class Epi>
 static hipError_t launch_bf16(hipStream_t st, const bf16_t* X, int ldx, int M, const bf16_t* W, int N, int K,
                               int splits, int xpk, Epi epi) {
-    const int kps = K / splits;
+    if (splits < 1 || K % (32 * splits)) return hipErrorInvalidValue;
     if (M <= 16) {
         launch_med_x<1>(st, X, ldx, M, W, N, K, splits, xpk, epi);
     } else if (M <= 32) {
         launch_med_x<2>(st, X, ldx, M, W, N, K, splits, xpk, epi);
-    } else if (M <= 256) {
-        launch_med_x<4>(st, X, ldx, M, W, N, K, splits, xpk, epi);
     } else {
-        if (xpk) return hipErrorInvalidValue;
-        dim3 grid((N + 127) / 128, (M + 127) / 128, splits);
-        hipLaunchKernelGGL((gemm_tiled_bf16<128, 128, Epi>), grid, dim3(256), 0, st, X, ldx, M, W, N, K, kps, epi);
+        const int bn = big_tile_n(M, N);
+        if (bn == 0) {
+            launch_med_x<4>(st, X, ldx, M, W, N, K, splits, xpk, epi);
+        } else {
+            if (!xpk) return hipErrorInvalidValue;   // large products take fragment-order activations only
+            return bn == 256 ? launch_big<256, 8>(st, X, M, W, N, K, splits, epi)
+                             : launch_big<128, 8>(st, X, M, W, N, K, splits, epi);
+        }
     }
     return hipGetLastError();
 }
@@ -406,17 +495,18 @@ static hipError_t launch_f32(hipStream_t st, const float* X, int ldx, int M, con
 }
 
 int gemm_split_granule(int dtype, int M) {
-    if (dtype == 0) return 32;
-    if (M <= 256) return 32;
-    return 64;
+    (void)dtype;
+    (void)M;
+    return 32;   // one k step of the bf16 kernels, one LDS tile of the fp32 one
 }
 
 // Workgroups of one bf16 launch for M rows and N columns before K splitting.
 int gemm_tiles(int M, int N) {
     const int groups = ((N + 15) / 16 + GM_NT - 1) / GM_NT;
     if (M <= 32) return groups;
-    if (M <= 256) return groups * ((M + 63) / 64);
-    return ((N + 127) / 128) * ((M + 127) / 128);
+    const int bn = M <= 256 ? 0 : big_tile_n(M, N);
+    if (bn == 0) return groups * ((M + 63) / 64);
+    return ((N + bn - 1) / bn) * ((M + 255) / 256);
 }
 
 hipError_t gemm(hipStream_t st, const GemmArgs& a) {

@@ -181,6 +181,7 @@ struct NarEmbedArgs {
     const float* stage_vec;            // [k_heads][d]
     const float* ln_g; const float* ln_b;
     float* h; void* u;
+    int packed;                        // bf16 u in fragment order (frag_off, K = d)
 };
 hipError_t nar_embed_ln(hipStream_t st, const NarEmbedArgs& a);
 
@@ -189,6 +190,7 @@ struct RowsLnArgs {
     int dtype; int n_rows; int d;
     const float* h; const float* ln_g; const float* ln_b;
     void* u;
+    int packed;                        // bf16 u in fragment order (frag_off, K = d)
 };
 hipError_t rows_ln(hipStream_t st, const RowsLnArgs& a);
 

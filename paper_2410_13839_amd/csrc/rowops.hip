@@ -290,7 +290,8 @@ __global__ __launch_bounds__(256) void nar_embed_ln_kernel(NarEmbedArgs a) {
             h[c] = x[j];
         }
     }
-    layer_norm_store<ActT>(x, a.d, a.ln_g, a.ln_b, reinterpret_cast<ActT*>(a.u) + (size_t)r * a.d, red);
+    if (a.packed) layer_norm_store_pk<ActT>(x, a.d, a.ln_g, a.ln_b, reinterpret_cast<ActT*>(a.u), r, red);
+    else layer_norm_store<ActT>(x, a.d, a.ln_g, a.ln_b, reinterpret_cast<ActT*>(a.u) + (size_t)r * a.d, red);
 }
 
 template <typename ActT>
@@ -304,7 +305,8 @@ __global__ __launch_bounds__(256) void rows_ln_kernel(RowsLnArgs a) {
         const int c = tid + 256 * j;
         x[j] = c < a.d ? h[c] : 0.f;
     }
-    layer_norm_store<ActT>(x, a.d, a.ln_g, a.ln_b, reinterpret_cast<ActT*>(a.u) + (size_t)r * a.d, red);
+    if (a.packed) layer_norm_store_pk<ActT>(x, a.d, a.ln_g, a.ln_b, reinterpret_cast<ActT*>(a.u), r, red);
+    else layer_norm_store<ActT>(x, a.d, a.ln_g, a.ln_b, reinterpret_cast<ActT*>(a.u) + (size_t)r * a.d, red);
 }
 
 // One wave per listed row.
