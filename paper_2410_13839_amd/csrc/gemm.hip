@@ -223,7 +223,7 @@ static void launch_med(hipStream_t st, const bf16_t* X, int ldx, int M, const bf
     else if (per_wave == 3)
         hipLaunchKernelGGL((gemm_med_bf16<MT, NT, 3, XP, Epi>), grid, block, 0, st, X, ldx, M, W, N, K, kps, epi);
     else
-        hipLaunchKernelGGL((gemm_med_bf16<MT, NT, 4, XP, Epi>), grid, block, 0, st, X, ldx, M, W, N, K, kps, epi);
+        hipLaunchKernelGGL((gemm_med_bf16<MT, NT, CAP, XP, Epi>), grid, block, 0, st, X, ldx, M, W, N, K, kps, epi);
 }
 
 template <int MT, class Epi>
@@ -322,41 +322,58 @@ __global__ __launch_bounds__(64 * NWV) void gemm_big_bf16(const bf16_t* __restri
 #pragma unroll
         for (int j = 0; j < WFM; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-    // Operand reads are written as ds_read_b128 in asm: the compiler cannot
-    // tell the stage being read from the stages the LDS DMA is still filling
-    // and would wait for every load in flight before each read.  The stage
-    // read is complete (the vmcnt wait and barrier before it); the reads
-    // return in order, so after lgkmcnt(4) the weight fragments and the first
-    // four activation fragments are in (half the products), after lgkmcnt(0)
-    // the rest.  Empty asm statements after each wait hand the registers on
-    // to the MFMAs, which therefore cannot be scheduled before the wait.
+    // Operand reads are ds_read_b128 in asm: the compiler cannot tell the
+    // stage being read from the stages the LDS DMA is still filling and would
+    // wait for every load in flight before each read.  The stage read is
+    // complete (the vmcnt wait and barrier before it).  Each asm block issues
+    // its reads and waits for them itself, so its outputs are valid when it
+    // ends whatever the compiler does with the registers afterwards.
     auto compute = [&](const bf16_t* buf) {
         const uint32_t lb = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) bf16_t*)buf + lane * 16;
         const uint32_t la = lb + (FM + wn * WFN) * 1024, lbm = lb + wm * WFM * 1024;
         bf16x8_t a[WFN], b[WFM];
+        static_assert(WFM == 8 && (WFN == 8 || WFN == 4 || WFN == 2), "operand counts");
+        if constexpr (WFN == 8) {
+            asm volatile(
+                "ds_read_b128 %0, %8 offset:0\n\tds_read_b128 %1, %8 offset:1024\n\t"
+                "ds_read_b128 %2, %8 offset:2048\n\tds_read_b128 %3, %8 offset:3072\n\t"
+                "ds_read_b128 %4, %8 offset:4096\n\tds_read_b128 %5, %8 offset:5120\n\t"
+                "ds_read_b128 %6, %8 offset:6144\n\tds_read_b128 %7, %8 offset:7168\n\t"
+                "s_waitcnt lgkmcnt(0)"
+                : "=&v"(a[0]), "=&v"(a[1]), "=&v"(a[2]), "=&v"(a[3]), "=&v"(a[4]), "=&v"(a[5]), "=&v"(a[6]),
+                  "=&v"(a[7])
+                : "v"(la)
+                : "memory");
+        } else if constexpr (WFN == 4) {
+            asm volatile(
+                "ds_read_b128 %0, %4 offset:0\n\tds_read_b128 %1, %4 offset:1024\n\t"
+                "ds_read_b128 %2, %4 offset:2048\n\tds_read_b128 %3, %4 offset:3072\n\t"
+                "s_waitcnt lgkmcnt(0)"
+                : "=&v"(a[0]), "=&v"(a[1]), "=&v"(a[2]), "=&v"(a[3])
+                : "v"(la)
+                : "memory");
+        } else {
+            asm volatile(
+                "ds_read_b128 %0, %2 offset:0\n\tds_read_b128 %1, %2 offset:1024\n\t"
+                "s_waitcnt lgkmcnt(0)"
+                : "=&v"(a[0]), "=&v"(a[1])
+                : "v"(la)
+                : "memory");
+        }
+        asm volatile(
+            "ds_read_b128 %0, %8 offset:0\n\tds_read_b128 %1, %8 offset:1024\n\t"
+            "ds_read_b128 %2, %8 offset:2048\n\tds_read_b128 %3, %8 offset:3072\n\t"
+            "ds_read_b128 %4, %8 offset:4096\n\tds_read_b128 %5, %8 offset:5120\n\t"
+            "ds_read_b128 %6, %8 offset:6144\n\tds_read_b128 %7, %8 offset:7168\n\t"
+            "s_waitcnt lgkmcnt(0)"
+            : "=&v"(b[0]), "=&v"(b[1]), "=&v"(b[2]), "=&v"(b[3]), "=&v"(b[4]), "=&v"(b[5]), "=&v"(b[6]),
+              "=&v"(b[7])
+            : "v"(lbm)
+            : "memory");
 #pragma unroll
         for (int i = 0; i < WFN; ++i)
-            asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(a[i]) : "v"(la), "i"(i * 1024));
 #pragma unroll
-        for (int j = 0; j < WFM; ++j)
-            asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(b[j]) : "v"(lbm), "i"(j * 1024));
-        asm volatile("s_waitcnt lgkmcnt(4)" ::: "memory");
-#pragma unroll
-        for (int i = 0; i < WFN; ++i) asm volatile("" : "+v"(a[i]));
-#pragma unroll
-        for (int j = 0; j < 4; ++j) asm volatile("" : "+v"(b[j]));
-#pragma unroll
-        for (int i = 0; i < WFN; ++i)
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-#pragma unroll
-        for (int j = 4; j < 8; ++j) asm volatile("" : "+v"(b[j]));
-#pragma unroll
-        for (int i = 0; i < WFN; ++i)
-#pragma unroll
-            for (int j = 4; j < 8; ++j)
+            for (int j = 0; j < WFM; ++j)
                 acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
     };
 
