@@ -29,8 +29,9 @@ struct EpiQKV {
     KVView kv;
     int d;
     __device__ __forceinline__ void store4(int m, int n, const float (&v)[4], int, int) const {
-        float r0 = v[0] + bias[n], r1 = v[1] + bias[n + 1], r2 = v[2] + bias[n + 2], r3 = v[3] + bias[n + 3];
-        int sec = n / d;
+        const float4 bv = *reinterpret_cast<const float4*>(bias + n);
+        const float r0 = v[0] + bv.x, r1 = v[1] + bv.y, r2 = v[2] + bv.z, r3 = v[3] + bv.w;
+        const int sec = (n >= d) + (n >= 2 * d);      // q, k or v (no integer division)
         if (sec == 0) {
             *reinterpret_cast<float4*>(q + (size_t)m * d + n) = make_float4(r0, r1, r2, r3);
             return;
@@ -68,9 +69,8 @@ struct EpiGelu {
     int ldo;
     int pk;               // bf16 output in fragment order (K = ldo)
     __device__ __forceinline__ void store4(int m, int n, const float (&v)[4], int, int) const {
-        float r[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) r[i] = gelu_erf(v[i] + bias[n + i]);
+        const float4 bv = *reinterpret_cast<const float4*>(bias + n);
+        const float r[4] = {gelu_erf(v[0] + bv.x), gelu_erf(v[1] + bv.y), gelu_erf(v[2] + bv.z), gelu_erf(v[3] + bv.w)};
         OutT* p = out + (pk ? frag_off(m, n, ldo) : (size_t)m * ldo + n);
         if constexpr (sizeof(OutT) == 2) {
             uint2 pk;
