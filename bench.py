@@ -43,6 +43,8 @@ def _parse():
     ap.add_argument("--no-qest", action="store_true", help="skip the transition-table estimation figures")
     ap.add_argument("--no-nar", action="store_true", help="skip the NAR module figures")
     ap.add_argument("--nar-only", action="store_true", help="only the NAR module figures (one JSON line of them)")
+    ap.add_argument("--config-only", default=None,
+                    help="only one workload's generation line (tiny, valle_k4, valle_k8, valle_b32, long_b8)")
     ap.add_argument("--qest-only", action="store_true",
                     help="only the transition-table estimation figures (one JSON line of them)")
     return ap.parse_args()
@@ -438,6 +440,9 @@ def main():
         return
     if args.nar_only:
         print(json.dumps(bench_nar(torch, 3, not args.no_cpu_baseline)))
+        return
+    if args.config_only:
+        print(json.dumps(bench_config(torch, args.config_only, {}, make_logq())))
         return
 
     wl = WORKLOADS[args.workload]
