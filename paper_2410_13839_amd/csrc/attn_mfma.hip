@@ -378,6 +378,178 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(AttnMfmaArgs p) {
     }
 }
 
+// Prefill attention, flash style (bf16 cache, 16-key pages): one workgroup
+// of 4 waves per (64-row query tile, head); wave w owns the tile's query rows
+// 16 w .. 16 w + 15 and runs over the keys in blocks of 64 (four pages).
+// Each block's K rows and V^T rows are staged once in LDS for the four waves
+// (double-buffered: the next block's loads sit in registers while the
+// current one is consumed; keys past the context are zeroed in V^T, whose
+// products with a zero probability must not meet a NaN), and each wave makes
+// one online-softmax update per block:
+//   S^T[key][q] = K[key][:] . Q[q][:]       16 x 16 x 32 MFMA, 2 k steps per
+//                                          16-key tile; Q is pre-scaled by
+//                                          log2(e) / 8, so exp2 applies
+//   O^T[dim][q] += V^T[dim][key] P^T[key][q] 16 x 16 x 32 MFMA whose 32-deep
+//                                          k index takes keys 4 g .. 4 g + 3
+//                                          of two 16-key tiles: lane (r, g)'s
+//                                          P^T operand is then exactly its own
+//                                          S^T values after exp2.
+// Causal, or bidirectional (every row sees its sequence's ctx_len keys) with
+// p.bidir.  Rows of the tile past its row count compute and are not stored.
+__global__ __launch_bounds__(256) void attn_prefill_fa_kernel(AttnMfmaArgs p) {
+    constexpr int KP = 72;                       // padded staged row (bf16): 144 B
+    __shared__ __attribute__((aligned(16))) bf16_t sk[2][64 * KP];   // [key][dim]
+    __shared__ __attribute__((aligned(16))) bf16_t sv[2][64 * KP];   // [dim][key]
+    const int head = blockIdx.y;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int r = lane & 15, g = lane >> 4;
+    const int2 tile = p.tiles[blockIdx.x];
+    const int row0 = tile.x, nrows = tile.y;
+    if (nrows <= 0) return;                      // uniform over the workgroup
+    const int b = p.rows[row0].seq;
+    const int pos0 = p.rows[row0].pos;
+    const bool bidir = p.bidir != 0;
+    const int kend = bidir ? p.st[b].ctx_len : pos0 + nrows;
+    const int nblk = (kend + 63) >> 6;
+    const bf16_t* pool = reinterpret_cast<const bf16_t*>(p.kv.pool);
+    const int last_page_key = (p.kv.max_pages_per_seq - 1) * 16;
+
+    // staging: thread t moves the 16-byte chunks t and t + 256 of the block's
+    // four 2 KB K blocks and of its four 2 KB V^T blocks
+    uint4 kreg[2], vreg[2];
+    auto gload = [&](int blk) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int c = tid + 256 * i, pg = c >> 7, w = c & 127;
+            const int key = min(blk * 64 + pg * 16, last_page_key);   // first key of the page
+            kreg[i] = *reinterpret_cast<const uint4*>(pool + p.kv.offset(b, key, 0, head) + w * 8);
+            vreg[i] = *reinterpret_cast<const uint4*>(pool + p.kv.vt_offset(b, key, head) + w * 8);
+        }
+    };
+    auto sstore = [&](int buf, int blk) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int c = tid + 256 * i, pg = c >> 7, w = c & 127;
+            // K chunk w: slot w / 8, dims 8 (w % 8) ..; V^T chunk w: dim w / 2, keys 8 (w % 2) ..
+            *reinterpret_cast<uint4*>(&sk[buf][(pg * 16 + (w >> 3)) * KP + (w & 7) * 8]) = kreg[i];
+            uint4 v = vreg[i];
+            const int k0 = blk * 64 + pg * 16 + (w & 1) * 8;
+            if (k0 + 8 > kend) {
+                uint32_t u[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    if (k0 + e >= kend) u[e >> 1] &= (e & 1) ? 0x0000FFFFu : 0xFFFF0000u;
+                v = make_uint4(u[0], u[1], u[2], u[3]);
+            }
+            *reinterpret_cast<uint4*>(&sv[buf][(w >> 1) * KP + pg * 16 + (w & 1) * 8]) = v;
+        }
+    };
+
+    gload(0);
+    bf16x8_t qf[2];
+    {
+        const float sc = 0.18033688011112042f;   // log2(e) / sqrt(64)
+        const float* qp = p.q + (size_t)(row0 + min(16 * wave + r, nrows - 1)) * p.ldq + head * 64 + g * 8;
+#pragma unroll
+        for (int h2 = 0; h2 < 2; ++h2) {
+            const float4 x = *reinterpret_cast<const float4*>(qp + 32 * h2);
+            const float4 y = *reinterpret_cast<const float4*>(qp + 32 * h2 + 4);
+            qf[h2] = __builtin_bit_cast(bf16x8_t, make_uint4(pk2(x.x * sc, x.y * sc), pk2(x.z * sc, x.w * sc),
+                                                             pk2(y.x * sc, y.y * sc), pk2(y.z * sc, y.w * sc)));
+        }
+    }
+    const int qpos = pos0 + 16 * wave + r;       // this lane's query position
+    const int qlast = pos0 + 16 * wave + 15;     // the wave's last query position
+    float m_run = -INFINITY, l_run = 0.f;
+    f32x4_t acc[4];
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) acc[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+    sstore(0, 0);
+    __syncthreads();
+    for (int blk = 0; blk < nblk; ++blk) {
+        const int buf = blk & 1;
+        if (blk + 1 < nblk) gload(blk + 1);
+        const int kb0 = blk * 64;
+        if (bidir || kb0 <= qlast) {             // uniform per wave: some key of the block is visible
+            const bf16_t* K = sk[buf];
+            const bf16_t* VT = sv[buf];
+            f32x4_t sc4[4];
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                const bf16_t* kr = K + (16 * t + r) * KP + 8 * g;
+                sc4[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*reinterpret_cast<const bf16x8_t*>(kr), qf[0],
+                                                                 f32x4_t{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+                sc4[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*reinterpret_cast<const bf16x8_t*>(kr + 32), qf[1],
+                                                                 sc4[t], 0, 0, 0);
+            }
+            if (kb0 + 64 > kend || (!bidir && kb0 + 63 > pos0 + 16 * wave)) {   // uniform per wave
+#pragma unroll
+                for (int t = 0; t < 4; ++t)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int key = kb0 + 16 * t + 4 * g + e;
+                        const bool ok = key < kend && (bidir || key <= qpos);
+                        sc4[t][e] = ok ? sc4[t][e] : -INFINITY;
+                    }
+            }
+            float mx = -INFINITY;
+#pragma unroll
+            for (int t = 0; t < 4; ++t)
+                mx = fmaxf(mx, fmaxf(fmaxf(sc4[t][0], sc4[t][1]), fmaxf(sc4[t][2], sc4[t][3])));
+            mx = fmaxf(mx, __shfl_xor(mx, 16));
+            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            const float m_new = fmaxf(m_run, mx);
+            const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+            const float scale = __builtin_amdgcn_exp2f(m_run - m_use);
+            float sum = 0.f;
+#pragma unroll
+            for (int t = 0; t < 4; ++t)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    sc4[t][e] = __builtin_amdgcn_exp2f(sc4[t][e] - m_use);
+                    sum += sc4[t][e];
+                }
+            sum += __shfl_xor(sum, 16);
+            sum += __shfl_xor(sum, 32);
+            l_run = l_run * scale + sum;
+            m_run = m_new;
+#pragma unroll
+            for (int dt = 0; dt < 4; ++dt) acc[dt] *= scale;
+#pragma unroll
+            for (int pr = 0; pr < 2; ++pr) {
+                const int t0 = 2 * pr, t1 = 2 * pr + 1;
+                const bf16x8_t pf = __builtin_bit_cast(
+                    bf16x8_t, make_uint4(pk2(sc4[t0][0], sc4[t0][1]), pk2(sc4[t0][2], sc4[t0][3]),
+                                         pk2(sc4[t1][0], sc4[t1][1]), pk2(sc4[t1][2], sc4[t1][3])));
+#pragma unroll
+                for (int dt = 0; dt < 4; ++dt) {
+                    const bf16_t* vr = VT + (16 * dt + r) * KP + 4 * g;
+                    const uint2 va = *reinterpret_cast<const uint2*>(vr + 16 * t0);
+                    const uint2 vb = *reinterpret_cast<const uint2*>(vr + 16 * t1);
+                    const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, make_uint4(va.x, va.y, vb.x, vb.y));
+                    acc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, acc[dt], 0, 0, 0);
+                }
+            }
+        }
+        if (blk + 1 < nblk) sstore(buf ^ 1, blk + 1);
+        __syncthreads();
+    }
+
+    // O = O^T / l: lane (r, g) holds dims 16 dt + 4 g .. + 3 of query row r
+    const int q = 16 * wave + r;
+    if (q < nrows) {
+        const float inv = 1.0f / l_run;
+        const int row = row0 + q;
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt) {
+            const int col = head * 64 + 16 * dt + 4 * g;
+            const uint2 o = make_uint2(pk2(acc[dt][0] * inv, acc[dt][1] * inv), pk2(acc[dt][2] * inv, acc[dt][3] * inv));
+            *reinterpret_cast<uint2*>(p.out + (p.packed ? frag_off(row, col, p.ldo) : (size_t)row * p.ldo + col)) = o;
+        }
+    }
+}
+
 template <int QT>
 static hipError_t attn_prefill_go(hipStream_t st, const AttnMfmaArgs& a) {
     const size_t lds = (size_t)4 * QT * 64 * 17 * sizeof(float);
@@ -410,6 +582,10 @@ hipError_t attention_mfma(hipStream_t st, const AttnMfmaArgs& a) {
     }
     // prefill: tiles of at most a.qt rows (16, 32 or 64), one split
     if (a.n_splits != 1) return hipErrorInvalidValue;
+    if (a.qt == 64 && a.kv.page_size == 16) {
+        hipLaunchKernelGGL(attn_prefill_fa_kernel, dim3(a.n_tiles, a.kv.n_heads, 1), dim3(256), 0, st, a);
+        return hipGetLastError();
+    }
     if (a.qt == 64) return attn_prefill_go<4>(st, a);
     if (a.qt == 32) return attn_prefill_go<2>(st, a);
     if (a.qt == 16) return attn_prefill_go<1>(st, a);
