@@ -210,6 +210,20 @@ def cpu_baseline(wl, weights, logq, prompts, budget_s):
                       f"float64 numpy on {threads} BLAS threads of {len(os.sched_getaffinity(0))} visible cores"}
 
 
+def cpu_baseline_1thread(wl, weights, logq, prompts, budget_s):
+    """The same oracle limited to one BLAS thread (threadpoolctl), on a
+    bounded sample: prefill, then decode steps for about `budget_s` s."""
+    try:
+        from threadpoolctl import threadpool_limits
+    except Exception:
+        return None
+    with threadpool_limits(limits=1):
+        out = cpu_baseline(wl, weights, logq, prompts, budget_s)
+    out["cores"] = 1
+    out["sample"] = out["sample"].split(", float64")[0] + ", float64 numpy on 1 BLAS thread"
+    return out
+
+
 def trunk_params(m):
     """Parameters one token streams through the trunk (per layer: QKV, out,
     FFN1, FFN2 weights and biases, two LayerNorms)."""
@@ -300,6 +314,8 @@ def bench_config(torch, name, weights_cache, logq):
            "step_hbm_GB_s": round(tot_bytes / (dec_ms * 1e-3) / 1e9, 1),
            "step_hbm_frac": round(tot_bytes / (dec_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
            "prefill_rows": int(np.sum(lens)), "prefill_ms": round(pre_ms, 3),
+           "end_to_end_ms": round(pre_ms + dec_ms, 3),
+           "end_to_end_tokens_per_s": round(toks / ((pre_ms + dec_ms) * 1e-3), 1),
            "prefill_tflops": round(fl / (pre_ms * 1e-3) / 1e12, 1),
            "prefill_mfma_frac_bf16": round(fl / (pre_ms * 1e-3) / 2.5e15, 4) if wl.model.dtype == "bf16" else None}
     print(f"[bench] config {name}: {out}", file=sys.stderr, flush=True)
@@ -542,9 +558,16 @@ def main():
         torch.cuda.synchronize()
 
     cpu = None
+    cpu1 = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(wl, weights, logq, prompts, args.cpu_seconds)
         print(f"[bench] cpu oracle: {cpu['value']:.2f} tokens/s", file=sys.stderr, flush=True)
+        # one-thread figures for the two batch-1 parity workloads (small samples)
+        cpu1 = {}
+        wt = WORKLOADS["tiny"]
+        cpu1["tiny"] = cpu_baseline_1thread(wt, make_weights(wt.model), logq, make_prompts(wt), 3.0)
+        cpu1[wl.name] = cpu_baseline_1thread(wl, weights, logq, prompts, 5.0)
+        print(f"[bench] cpu oracle, one thread: {cpu1}", file=sys.stderr, flush=True)
 
     out = {
         "metric": "codec tokens/sec (and ms/token) at batch 1, K=4 heads, top_k=4",
@@ -557,6 +580,7 @@ def main():
         "roofline": roof,
         "kernels": kernels,
         "cpu_baseline": cpu,
+        "cpu_baseline_one_thread": cpu1,
         "selection_variants": variants,
         "configs": configs,
         "q_estimation": qest,
