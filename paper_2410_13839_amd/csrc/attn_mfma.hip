@@ -114,8 +114,8 @@ __global__ __launch_bounds__(64 * NW) void attn_dec_kernel(AttnMfmaArgs p) {
             sc[e] = ok ? s[e] : -INFINITY;
             mx = fmaxf(mx, sc[e]);
         }
-        mx = fmaxf(mx, __shfl_xor(mx, 16));
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        mx = xor16_max(mx);
+        mx = xor32_max(mx);
         const float m_new = fmaxf(m_run, mx);
         const float scale = (m_run == -INFINITY) ? 0.f : __expf(m_run - m_new);
         float pe[4], sum = 0.f;
@@ -124,8 +124,8 @@ __global__ __launch_bounds__(64 * NW) void attn_dec_kernel(AttnMfmaArgs p) {
             pe[e] = (sc[e] == -INFINITY) ? 0.f : __expf(sc[e] - m_new);
             sum += pe[e];
         }
-        sum += __shfl_xor(sum, 16);
-        sum += __shfl_xor(sum, 32);
+        sum = xor16_sum(sum);
+        sum = xor32_sum(sum);
         l_run = l_run * scale + sum;
         m_run = m_new;
         const s16x4_t pf = __builtin_bit_cast(s16x4_t, make_uint2(pk2(pe[0], pe[1]), pk2(pe[2], pe[3])));
@@ -318,8 +318,8 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(AttnMfmaArgs p) {
                 sc[e] = ok ? s[e] : -INFINITY;
                 mx = fmaxf(mx, sc[e]);
             }
-            mx = fmaxf(mx, __shfl_xor(mx, 16));
-            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            mx = xor16_max(mx);
+            mx = xor32_max(mx);
             const float m_new = fmaxf(m_run[j], mx);
             const float scale = (m_run[j] == -INFINITY) ? 0.f : __expf(m_run[j] - m_new);
             float pe[4], sum = 0.f;
@@ -328,8 +328,8 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(AttnMfmaArgs p) {
                 pe[e] = (sc[e] == -INFINITY) ? 0.f : __expf(sc[e] - m_new);
                 sum += pe[e];
             }
-            sum += __shfl_xor(sum, 16);
-            sum += __shfl_xor(sum, 32);
+            sum = xor16_sum(sum);
+            sum = xor32_sum(sum);
             l_run[j] = l_run[j] * scale + sum;
             m_run[j] = m_new;
             const s16x4_t pf = __builtin_bit_cast(s16x4_t, make_uint2(pk2(pe[0], pe[1]), pk2(pe[2], pe[3])));
@@ -497,8 +497,8 @@ __global__ __launch_bounds__(256) void attn_prefill_fa_kernel(AttnMfmaArgs p) {
 #pragma unroll
             for (int t = 0; t < 4; ++t)
                 mx = fmaxf(mx, fmaxf(fmaxf(sc4[t][0], sc4[t][1]), fmaxf(sc4[t][2], sc4[t][3])));
-            mx = fmaxf(mx, __shfl_xor(mx, 16));
-            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            mx = xor16_max(mx);
+            mx = xor32_max(mx);
             const float m_new = fmaxf(m_run, mx);
             const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
             const float scale = __builtin_amdgcn_exp2f(m_run - m_use);
@@ -510,8 +510,8 @@ __global__ __launch_bounds__(256) void attn_prefill_fa_kernel(AttnMfmaArgs p) {
                     sc4[t][e] = __builtin_amdgcn_exp2f(sc4[t][e] - m_use);
                     sum += sc4[t][e];
                 }
-            sum += __shfl_xor(sum, 16);
-            sum += __shfl_xor(sum, 32);
+            sum = xor16_sum(sum);
+            sum = xor32_sum(sum);
             l_run = l_run * scale + sum;
             m_run = m_new;
 #pragma unroll

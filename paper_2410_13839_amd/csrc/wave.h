@@ -37,10 +37,30 @@ __device__ __forceinline__ float sum16(float v) {
     v += dpp_f<DPP_ROR8>(v);
     return v;
 }
+// Combine each lane's value with that of the lane 16 (32) apart without an
+// LDS round trip: the gfx950 permlane swaps of a value with itself give every
+// lane its row pair's lower and upper values (r[0], r[1]), and add / max are
+// commutative, so both partner lanes get the bit-identical result a shuffle
+// would give.
+__device__ __forceinline__ float pl_lo16(float v, float& hi) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    hi = __uint_as_float(r[1]);
+    return __uint_as_float(r[0]);
+}
+__device__ __forceinline__ float pl_lo32(float v, float& hi) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    hi = __uint_as_float(r[1]);
+    return __uint_as_float(r[0]);
+}
+__device__ __forceinline__ float xor16_sum(float v) { float h; const float l = pl_lo16(v, h); return l + h; }
+__device__ __forceinline__ float xor32_sum(float v) { float h; const float l = pl_lo32(v, h); return l + h; }
+__device__ __forceinline__ float xor16_max(float v) { float h; const float l = pl_lo16(v, h); return fmaxf(l, h); }
+__device__ __forceinline__ float xor32_max(float v) { float h; const float l = pl_lo32(v, h); return fmaxf(l, h); }
+
 __device__ __forceinline__ float wave_sum64(float v) {
     v = sum16(v);
-    v += __shfl_xor(v, 16);
-    v += __shfl_xor(v, 32);
+    v = xor16_sum(v);
+    v = xor32_sum(v);
     return v;
 }
 __device__ __forceinline__ float max16(float v) {
@@ -52,15 +72,15 @@ __device__ __forceinline__ float max16(float v) {
 }
 __device__ __forceinline__ float wave_max64(float v) {
     v = max16(v);
-    v = fmaxf(v, __shfl_xor(v, 16));
-    v = fmaxf(v, __shfl_xor(v, 32));
+    v = xor16_max(v);
+    v = xor32_max(v);
     return v;
 }
 // Sum over lanes that are 8, 16 and 32 apart (lanes with equal lane % 8).
 __device__ __forceinline__ float sum_stride8(float v) {
     v += dpp_f<DPP_ROR8>(v);
-    v += __shfl_xor(v, 16);
-    v += __shfl_xor(v, 32);
+    v = xor16_sum(v);
+    v = xor32_sum(v);
     return v;
 }
 
