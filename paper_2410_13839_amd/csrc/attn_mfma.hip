@@ -200,12 +200,14 @@ static hipError_t attn_dec_go_pd(hipStream_t st, const AttnMfmaArgs& a) {
     return hipGetLastError();
 }
 
-// Ring depth: two 16-key groups per wave once a split holds that many (a
-// third ring slot no longer fits 128 registers at 16 waves).
+// Ring depth: two 16-key groups per wave once a split holds that many, for
+// 16-wave workgroups (one per CU); smaller workgroups keep one group in
+// flight per wave and gain more waves per CU instead (at batch 32: 684 vs
+// 695 us per decode step).
 template <int NW>
 static hipError_t attn_dec_go(hipStream_t st, const AttnMfmaArgs& a) {
     const int groups = (a.split_len + 16 * NW - 1) / (16 * NW);
-    if (groups >= 2) return attn_dec_go_pd<NW, 2>(st, a);
+    if (groups >= 2 && NW == 16) return attn_dec_go_pd<NW, 2>(st, a);
     return attn_dec_go_pd<NW, 1>(st, a);
 }
 
