@@ -30,8 +30,10 @@ HBM_PEAK_GBS = 8000.0
 def _parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=188)
-    ap.add_argument("--warmup", type=int, default=20)
+    # three whole generations timed after one whole generation of warm-up:
+    # the step time varies by a few percent between generations
+    ap.add_argument("--steps", type=int, default=564)
+    ap.add_argument("--warmup", type=int, default=188)
     ap.add_argument("--workload", default="valle_k4")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true", help="skip the per-workload generation lines")
