@@ -15,6 +15,8 @@
 //  * gemm_big_bf16: M > 256 (prefill, NAR).  256 x 256 tiles on MFMA with
 //    both operands streamed global -> LDS in fragment order.
 //  * gemm_f32: the fp32 model; LDS-tiled VALU FMA.
+#include <type_traits>
+
 #include "common.h"
 #include "launch.h"
 
@@ -234,9 +236,11 @@ static void launch_med_x(hipStream_t st, const bf16_t* X, int ldx, int M, const 
 }
 
 // ---------------------------------------------------------------- large bf16
-// M > 256 (prefill, NAR).  Tiles of 256 rows x BN columns (BN = 256 or 128),
-// 4 waves in a 2 x 2 grid each owning 128 x BN/2 outputs as 8 x BN/32
-// v_mfma_f32_16x16x32_bf16 tiles (accumulators 256 or 128 registers).  Both
+// M > 256 (prefill, NAR).  Tiles of BM rows x BN columns (256 x 256 and
+// 256 x 128 with 8 waves in a 2 x 4 grid, each wave owning 128 x BN/4
+// outputs as 8 x BN/64 v_mfma_f32_16x16x32_bf16 tiles; 128 x 128 with 4
+// waves in a 2 x 2 grid, 64 x 64 outputs each, for products too small to
+// give the CUs enough of the larger tiles).  Both
 // operands are in fragment order (activations written so by their producers,
 // weights packed at load), so a 16 x 32 fragment is one contiguous 1 KB; it
 // travels global -> LDS by one global_load_lds_dwordx4 per wave (lane l's 16
@@ -264,16 +268,16 @@ __device__ __forceinline__ void gb_barrier() {
     asm volatile("" ::: "memory");
 }
 
-template <int BN, int NWV, class Epi>
+template <int BM, int BN, int NWV, class Epi>
 __global__ __launch_bounds__(64 * NWV) void gemm_big_bf16(const bf16_t* __restrict__ X, int M,
                                                           const bf16_t* __restrict__ W, int N, int K, int k_per_split,
                                                           int tiles_m, int tiles_n, Epi epi) {
-    constexpr int FM = 16, FN = BN / 16;        // 16-row fragments of a stage
+    constexpr int FM = BM / 16, FN = BN / 16;   // 16-row fragments of a stage
     constexpr int NF = FM + FN;                 // fragments per stage (one 32-k step)
     constexpr int NL = NF / NWV;                // global_load_lds per wave per stage
     constexpr int WGN = NWV / 2;                // waves along n (two along m)
     constexpr int WFM = FM / 2, WFN = FN / WGN; // fragments per wave
-    static_assert(NF % NWV == 0 && WFM == 8 && WFN >= 1, "tile shape");
+    static_assert(NF % NWV == 0 && (WFM == 8 || WFM == 4) && WFN >= 1, "tile shape");
     typedef __attribute__((address_space(3))) void lds_void;
     __shared__ __attribute__((aligned(1024))) bf16_t s0[NF * 512];
     __shared__ __attribute__((aligned(1024))) bf16_t s1[NF * 512];
@@ -332,7 +336,7 @@ __global__ __launch_bounds__(64 * NWV) void gemm_big_bf16(const bf16_t* __restri
         const uint32_t lb = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) bf16_t*)buf + lane * 16;
         const uint32_t la = lb + (FM + wn * WFN) * 1024, lbm = lb + wm * WFM * 1024;
         bf16x8_t a[WFN], b[WFM];
-        static_assert(WFM == 8 && (WFN == 8 || WFN == 4 || WFN == 2), "operand counts");
+        static_assert((WFN == 8 || WFN == 4 || WFN == 2), "operand counts");
         if constexpr (WFN == 8) {
             asm volatile(
                 "ds_read_b128 %0, %8 offset:0\n\tds_read_b128 %1, %8 offset:1024\n\t"
@@ -360,16 +364,26 @@ __global__ __launch_bounds__(64 * NWV) void gemm_big_bf16(const bf16_t* __restri
                 : "v"(la)
                 : "memory");
         }
-        asm volatile(
-            "ds_read_b128 %0, %8 offset:0\n\tds_read_b128 %1, %8 offset:1024\n\t"
-            "ds_read_b128 %2, %8 offset:2048\n\tds_read_b128 %3, %8 offset:3072\n\t"
-            "ds_read_b128 %4, %8 offset:4096\n\tds_read_b128 %5, %8 offset:5120\n\t"
-            "ds_read_b128 %6, %8 offset:6144\n\tds_read_b128 %7, %8 offset:7168\n\t"
-            "s_waitcnt lgkmcnt(0)"
-            : "=&v"(b[0]), "=&v"(b[1]), "=&v"(b[2]), "=&v"(b[3]), "=&v"(b[4]), "=&v"(b[5]), "=&v"(b[6]),
-              "=&v"(b[7])
-            : "v"(lbm)
-            : "memory");
+        if constexpr (WFM == 8) {
+            asm volatile(
+                "ds_read_b128 %0, %8 offset:0\n\tds_read_b128 %1, %8 offset:1024\n\t"
+                "ds_read_b128 %2, %8 offset:2048\n\tds_read_b128 %3, %8 offset:3072\n\t"
+                "ds_read_b128 %4, %8 offset:4096\n\tds_read_b128 %5, %8 offset:5120\n\t"
+                "ds_read_b128 %6, %8 offset:6144\n\tds_read_b128 %7, %8 offset:7168\n\t"
+                "s_waitcnt lgkmcnt(0)"
+                : "=&v"(b[0]), "=&v"(b[1]), "=&v"(b[2]), "=&v"(b[3]), "=&v"(b[4]), "=&v"(b[5]), "=&v"(b[6]),
+                  "=&v"(b[7])
+                : "v"(lbm)
+                : "memory");
+        } else {
+            asm volatile(
+                "ds_read_b128 %0, %4 offset:0\n\tds_read_b128 %1, %4 offset:1024\n\t"
+                "ds_read_b128 %2, %4 offset:2048\n\tds_read_b128 %3, %4 offset:3072\n\t"
+                "s_waitcnt lgkmcnt(0)"
+                : "=&v"(b[0]), "=&v"(b[1]), "=&v"(b[2]), "=&v"(b[3])
+                : "v"(lbm)
+                : "memory");
+        }
 #pragma unroll
         for (int i = 0; i < WFN; ++i)
 #pragma unroll
@@ -420,17 +434,17 @@ __global__ __launch_bounds__(64 * NWV) void gemm_big_bf16(const bf16_t* __restri
         }
 }
 
-template <int BN, int NWV, class Epi>
+template <int BM, int BN, int NWV, class Epi>
 static hipError_t launch_big(hipStream_t st, const bf16_t* X, int M, const bf16_t* W, int N, int K, int splits,
                              Epi epi) {
     const int kps = K / splits;
     if (kps % 32) return hipErrorInvalidValue;
-    const int tm = (M + 255) / 256, tn = (N + BN - 1) / BN;
+    const int tm = (M + BM - 1) / BM, tn = (N + BN - 1) / BN;
     const int ntile = tm * tn;
     // the tile numbering deals eighths of the tiles to the XCDs: the grid is
     // 8 x ceil(tiles / 8) workgroups, the surplus ones return at once
     dim3 grid(8 * ((ntile + 7) / 8), splits);
-    hipLaunchKernelGGL((gemm_big_bf16<BN, NWV, Epi>), grid, dim3(64 * NWV), 0, st, X, M, W, N, K, kps, tm, tn, epi);
+    hipLaunchKernelGGL((gemm_big_bf16<BM, BN, NWV, Epi>), grid, dim3(64 * NWV), 0, st, X, M, W, N, K, kps, tm, tn, epi);
     return hipGetLastError();
 }
 
@@ -472,15 +486,22 @@ __global__ __launch_bounds__(256) void gemm_f32(const float* __restrict__ X, int
 }
 
 // ------------------------------------------------------------------ launchers
-// Tile width of the large-M kernel for an M x N product (M > 256): 256 when
-// that gives at least 128 tiles (half the CUs), else 128 when that gives 64,
-// else 0: the product is too small for either and goes to the medium kernel
-// (64-row groups, one workgroup per 32 columns).
-static int big_tile_n(int M, int N) {
-    const int tm = (M + 255) / 256;
-    if (tm * ((N + 255) / 256) >= 128) return 256;
-    if (tm * ((N + 127) / 128) >= 64) return 128;
-    return 0;
+// Tile of the large-M kernel for an M x N product (M > 256): 256 x 256 when
+// that gives at least 128 tiles (half the CUs), 256 x 128 when that gives
+// 192, else 128 x 128 when that gives 96 (64 for a split-K product, whose
+// K splits multiply the workgroups), else 256 x 128 when that gives 64;
+// otherwise {0, 0}: the product is too small for any and goes to the medium
+// kernel (64-row groups, one workgroup per 32 columns).  Measured at M =
+// 325 and 1,075: 72-81 tiles of 128 x 128 without K splits lose to the
+// medium kernel, 96 and more win against it and against 256 x 128.
+struct BigTile { int bm, bn; };
+static int tile_count(int M, int N, int bm, int bn) { return ((M + bm - 1) / bm) * ((N + bn - 1) / bn); }
+static BigTile big_tile(int M, int N, bool splittable) {
+    if (tile_count(M, N, 256, 256) >= 128) return {256, 256};
+    if (tile_count(M, N, 256, 128) >= 192) return {256, 128};
+    if (tile_count(M, N, 128, 128) >= (splittable ? 64 : 96)) return {128, 128};
+    if (tile_count(M, N, 256, 128) >= 64) return {256, 128};
+    return {0, 0};
 }
 template <class Epi>
 static hipError_t launch_bf16(hipStream_t st, const bf16_t* X, int ldx, int M, const bf16_t* W, int N, int K,
@@ -491,13 +512,14 @@ static hipError_t launch_bf16(hipStream_t st, const bf16_t* X, int ldx, int M, c
     } else if (M <= 32) {
         launch_med_x<2>(st, X, ldx, M, W, N, K, splits, xpk, epi);
     } else {
-        const int bn = big_tile_n(M, N);
-        if (bn == 0) {
+        const BigTile bt = big_tile(M, N, std::is_same<Epi, EpiPartial>::value);
+        if (bt.bm == 0) {
             launch_med_x<4>(st, X, ldx, M, W, N, K, splits, xpk, epi);
         } else {
             if (!xpk) return hipErrorInvalidValue;   // large products take fragment-order activations only
-            return bn == 256 ? launch_big<256, 8>(st, X, M, W, N, K, splits, epi)
-                             : launch_big<128, 8>(st, X, M, W, N, K, splits, epi);
+            if (bt.bm == 128) return launch_big<128, 128, 4>(st, X, M, W, N, K, splits, epi);
+            return bt.bn == 256 ? launch_big<256, 256, 8>(st, X, M, W, N, K, splits, epi)
+                                : launch_big<256, 128, 8>(st, X, M, W, N, K, splits, epi);
         }
     }
     return hipGetLastError();
@@ -517,13 +539,14 @@ int gemm_split_granule(int dtype, int M) {
     return 32;   // one k step of the bf16 kernels, one LDS tile of the fp32 one
 }
 
-// Workgroups of one bf16 launch for M rows and N columns before K splitting.
+// Workgroups of one split-K-able (partial-sum) bf16 launch for M rows and N
+// columns before K splitting.
 int gemm_tiles(int M, int N) {
     const int groups = ((N + 15) / 16 + GM_NT - 1) / GM_NT;
     if (M <= 32) return groups;
-    const int bn = M <= 256 ? 0 : big_tile_n(M, N);
-    if (bn == 0) return groups * ((M + 63) / 64);
-    return ((N + bn - 1) / bn) * ((M + 255) / 256);
+    const BigTile bt = M <= 256 ? BigTile{0, 0} : big_tile(M, N, true);
+    if (bt.bm == 0) return groups * ((M + 63) / 64);
+    return tile_count(M, N, bt.bm, bt.bn);
 }
 
 hipError_t gemm(hipStream_t st, const GemmArgs& a) {
