@@ -26,7 +26,7 @@ struct GemmArgs {
 
 hipError_t gemm(hipStream_t st, const GemmArgs& a);
 int gemm_split_granule(int dtype, int M);
-int gemm_tiles(int M, int N);   // split-K-able (partial-sum) products
+int gemm_tiles(int M, int N);
 
 struct AttnArgs {
     int dtype;                 // KV / output element type: 0 fp32, 1 bf16
