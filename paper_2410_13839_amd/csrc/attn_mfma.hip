@@ -9,6 +9,13 @@
 
 namespace mtp {
 
+// Element offset of the K (sec 0) or transposed V (sec 1) block of one head
+// in cache page `page` (the page table already looked up).
+__device__ __forceinline__ size_t kv_page_block(const KVView& kv, int page, int sec, int head) {
+    return ((((size_t)kv.layer * kv.num_pages + page) * 2 + sec) * kv.n_heads + head) * (size_t)kv.page_size *
+           MTP_HEAD_DIM;
+}
+
 namespace {
 constexpr int PSTR = 68;     // floats per partial row: max, sum, 2 pad, 64 outputs
 
@@ -398,6 +405,13 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(AttnMfmaArgs p) {
 //                                          S^T values after exp2.
 // Causal, or bidirectional (every row sees its sequence's ctx_len keys) with
 // p.bidir.  Rows of the tile past its row count compute and are not stored.
+// Workgroup barrier for LDS hand-offs: waits for this wave's LDS operations
+// only, so global loads issued for later blocks stay in flight across it
+// (__syncthreads() would wait for them too).
+__device__ __forceinline__ void lds_barrier() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 __global__ __launch_bounds__(256) void attn_prefill_fa_kernel(AttnMfmaArgs p) {
     constexpr int KP = 72;                       // padded staged row (bf16): 144 B
     __shared__ __attribute__((aligned(16))) bf16_t sk[2][64 * KP];   // [key][dim]
@@ -414,40 +428,60 @@ __global__ __launch_bounds__(256) void attn_prefill_fa_kernel(AttnMfmaArgs p) {
     const int kend = bidir ? p.st[b].ctx_len : pos0 + nrows;
     const int nblk = (kend + 63) >> 6;
     const bf16_t* pool = reinterpret_cast<const bf16_t*>(p.kv.pool);
-    const int last_page_key = (p.kv.max_pages_per_seq - 1) * 16;
+    // the sequence's pages up to the last block, looked up once into LDS (a
+    // load whose address waits on a page-table load would also wait for the
+    // loads of the block in flight before it)
+    extern __shared__ int s_pg[];
+    const int npg = min(p.kv.max_pages_per_seq, nblk * 4);
+    for (int i = tid; i < npg; i += 256) s_pg[i] = p.kv.block_table[(size_t)b * p.kv.max_pages_per_seq + i];
+    __syncthreads();
 
     // staging: thread t moves the 16-byte chunks t and t + 256 of the block's
     // four 2 KB K blocks and of its four 2 KB V^T blocks
-    uint4 kreg[2], vreg[2];
-    auto gload = [&](int blk) {
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const int c = tid + 256 * i, pg = c >> 7, w = c & 127;
-            const int key = min(blk * 64 + pg * 16, last_page_key);   // first key of the page
-            kreg[i] = *reinterpret_cast<const uint4*>(pool + p.kv.offset(b, key, 0, head) + w * 8);
-            vreg[i] = *reinterpret_cast<const uint4*>(pool + p.kv.vt_offset(b, key, head) + w * 8);
-        }
-    };
-    auto sstore = [&](int buf, int blk) {
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const int c = tid + 256 * i, pg = c >> 7, w = c & 127;
-            // K chunk w: slot w / 8, dims 8 (w % 8) ..; V^T chunk w: dim w / 2, keys 8 (w % 2) ..
-            *reinterpret_cast<uint4*>(&sk[buf][(pg * 16 + (w >> 3)) * KP + (w & 7) * 8]) = kreg[i];
-            uint4 v = vreg[i];
-            const int k0 = blk * 64 + pg * 16 + (w & 1) * 8;
-            if (k0 + 8 > kend) {
-                uint32_t u[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-                for (int e = 0; e < 8; ++e)
-                    if (k0 + e >= kend) u[e >> 1] &= (e & 1) ? 0x0000FFFFu : 0xFFFF0000u;
-                v = make_uint4(u[0], u[1], u[2], u[3]);
-            }
-            *reinterpret_cast<uint4*>(&sv[buf][(w >> 1) * KP + pg * 16 + (w & 1) * 8]) = v;
-        }
-    };
+    // Two register sets (A, B): a block's loads go out two blocks before its
+    // compute (one block of compute hid too little of the load latency).
+    // Thread t moves the 16-byte chunks t and t + 256 of the block's four
+    // 2 KB K blocks and of its four 2 KB V^T blocks; the chunks are plain
+    // variables (arrays of them ended up in scratch memory).
+#define MTP_FA_GLOAD1(KR, VR, I, BLK)                                                             \
+    {                                                                                             \
+        const int c = tid + 256 * (I), pg = c >> 7, w = c & 127;                                  \
+        const int page = s_pg[min((BLK) * 4 + pg, npg - 1)];                                      \
+        KR = *reinterpret_cast<const uint4*>(pool + kv_page_block(p.kv, page, 0, head) + w * 8);  \
+        VR = *reinterpret_cast<const uint4*>(pool + kv_page_block(p.kv, page, 1, head) + w * 8);  \
+    }
+#define MTP_FA_SSTORE1(KR, VR, I, BUF, BLK)                                                       \
+    {                                                                                             \
+        const int c = tid + 256 * (I), pg = c >> 7, w = c & 127;                                  \
+        /* K chunk w: slot w / 8, dims 8 (w % 8) ..; V^T chunk w: dim w / 2, keys 8 (w % 2) .. */ \
+        *reinterpret_cast<uint4*>(&sk[BUF][(pg * 16 + (w >> 3)) * KP + (w & 7) * 8]) = KR;        \
+        uint4 v = VR;                                                                             \
+        const int k0 = (BLK) * 64 + pg * 16 + (w & 1) * 8;                                        \
+        if (k0 + 8 > kend) { /* keys past the context: zero */                                    \
+            uint32_t m[4];                                                                        \
+            _Pragma("unroll") for (int j = 0; j < 4; ++j) {                                       \
+                const uint32_t lo = k0 + 2 * j < kend ? 0x0000FFFFu : 0u;                         \
+                const uint32_t hi = k0 + 2 * j + 1 < kend ? 0xFFFF0000u : 0u;                     \
+                m[j] = lo | hi;                                                                   \
+            }                                                                                     \
+            v = make_uint4(v.x & m[0], v.y & m[1], v.z & m[2], v.w & m[3]);                       \
+        }                                                                                         \
+        *reinterpret_cast<uint4*>(&sv[BUF][(w >> 1) * KP + pg * 16 + (w & 1) * 8]) = v;           \
+    }
+    uint4 kA0, kA1, vA0, vA1, kB0, kB1, vB0, vB1;
+    auto gloadA = [&](int blk) { MTP_FA_GLOAD1(kA0, vA0, 0, blk) MTP_FA_GLOAD1(kA1, vA1, 1, blk) };
+    auto gloadB = [&](int blk) { MTP_FA_GLOAD1(kB0, vB0, 0, blk) MTP_FA_GLOAD1(kB1, vB1, 1, blk) };
+    auto sstoreA = [&](int buf, int blk) { MTP_FA_SSTORE1(kA0, vA0, 0, buf, blk) MTP_FA_SSTORE1(kA1, vA1, 1, buf, blk) };
+    auto sstoreB = [&](int buf, int blk) { MTP_FA_SSTORE1(kB0, vB0, 0, buf, blk) MTP_FA_SSTORE1(kB1, vB1, 1, buf, blk) };
+#undef MTP_FA_GLOAD1
+#undef MTP_FA_SSTORE1
 
-    gload(0);
+    // every stage issues its loads and its LDS stores, the last ones of a
+    // clamped (repeated) block into a buffer nobody reads: with conditional
+    // ones the compiler's wait counts become the conservative merge of both
+    // paths and wait for the newest loads too
+    gloadA(0);
+    gloadB(min(1, nblk - 1));
     bf16x8_t qf[2];
     {
         const float sc = 0.18033688011112042f;   // log2(e) / sqrt(64)
@@ -467,11 +501,7 @@ __global__ __launch_bounds__(256) void attn_prefill_fa_kernel(AttnMfmaArgs p) {
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt) acc[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-    sstore(0, 0);
-    __syncthreads();
-    for (int blk = 0; blk < nblk; ++blk) {
-        const int buf = blk & 1;
-        if (blk + 1 < nblk) gload(blk + 1);
+    auto compute = [&](int buf, int blk) {
         const int kb0 = blk * 64;
         if (bidir || kb0 <= qlast) {             // uniform per wave: some key of the block is visible
             const bf16_t* K = sk[buf];
@@ -534,8 +564,21 @@ __global__ __launch_bounds__(256) void attn_prefill_fa_kernel(AttnMfmaArgs p) {
                 }
             }
         }
-        if (blk + 1 < nblk) sstore(buf ^ 1, blk + 1);
-        __syncthreads();
+    };
+    sstoreA(0, 0);
+    lds_barrier();
+    for (int blk = 0; blk < nblk; blk += 2) {
+        // block blk in LDS buffer 0, block blk + 1 in registers B
+        gloadA(min(blk + 2, nblk - 1));
+        compute(0, blk);
+        sstoreB(1, min(blk + 1, nblk - 1));
+        lds_barrier();
+        if (blk + 1 >= nblk) break;
+        // block blk + 1 in LDS buffer 1, block blk + 2 in registers A
+        gloadB(min(blk + 3, nblk - 1));
+        compute(1, blk + 1);
+        sstoreA(0, min(blk + 2, nblk - 1));
+        lds_barrier();
     }
 
     // O = O^T / l: lane (r, g) holds dims 16 dt + 4 g .. + 3 of query row r
@@ -585,7 +628,10 @@ hipError_t attention_mfma(hipStream_t st, const AttnMfmaArgs& a) {
     // prefill: tiles of at most a.qt rows (16, 32 or 64), one split
     if (a.n_splits != 1) return hipErrorInvalidValue;
     if (a.qt == 64 && a.kv.page_size == 16) {
-        hipLaunchKernelGGL(attn_prefill_fa_kernel, dim3(a.n_tiles, a.kv.n_heads, 1), dim3(256), 0, st, a);
+        // dynamic LDS: one page number per page of a sequence
+        const size_t lds = (size_t)a.kv.max_pages_per_seq * sizeof(int);
+        if (lds > 48 * 1024) return hipErrorInvalidValue;
+        hipLaunchKernelGGL(attn_prefill_fa_kernel, dim3(a.n_tiles, a.kv.n_heads, 1), dim3(256), lds, st, a);
         return hipGetLastError();
     }
     if (a.qt == 64) return attn_prefill_go<4>(st, a);
