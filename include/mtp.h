@@ -178,7 +178,12 @@ int mtp_prefill(mtp_ctx* ctx, int B, const int32_t* phon, const int32_t* phon_le
  * each sequence's emitted tokens (entries past its count are -1) and
  * out_count[B] the number emitted: K, fewer at the budget, up to and
  * including the first EOS (which ends the sequence), 0 once a sequence has
- * ended.  Blocks until the outputs are on the host. */
+ * ended.  Blocks until the outputs are on the host.
+ * Tuning override: the environment variable MTP_SPLIT_LEN, a multiple of
+ * 32 from 32 up, sets the keys per decode-attention split of the steps
+ * planned after it is set (raised where needed to keep at most 64 splits;
+ * the library otherwise chooses it from the batch and the longest
+ * context).  Results are the same up to floating-point rounding. */
 int mtp_decode_step(mtp_ctx* ctx, int K, int top_k, int32_t* out_tokens, int32_t* out_count);
 
 /* Same step, outputs written to DEVICE buffers d_tokens[B*K] and d_count[B]
