@@ -103,22 +103,32 @@ class ARDecoder:
             out[r] = table[int(tok)] + self.w["pos"][int(pos)]
         return out
 
-    def attention(self, q: np.ndarray, k_all: np.ndarray, v_all: np.ndarray, q_pos: np.ndarray) -> np.ndarray:
+    def attention(self, q: np.ndarray, k_all: np.ndarray, v_all: np.ndarray, q_pos: np.ndarray,
+                  rows_per_block: int = 256) -> np.ndarray:
         """Causal multi-head attention of the query rows over cached rows.
 
         q: [n, d]; k_all, v_all: [T, d] with row index = absolute position;
-        query r at position q_pos[r] sees keys 0..q_pos[r].
+        query r at position q_pos[r] sees keys 0..q_pos[r].  Per head h the
+        textbook form softmax(Q_h K_h^T / sqrt(64) + M) V_h, with M = -inf
+        where the key's position exceeds the query's.  Query rows are taken
+        `rows_per_block` at a time only to bound the size of the score
+        matrix; each row's result does not depend on the blocking.
         """
         n = q.shape[0]
         out = np.zeros((n, self.d))
         scale = 1.0 / np.sqrt(self.hd)
+        q_pos = np.asarray(q_pos, dtype=np.int64)
+        key_pos = np.arange(k_all.shape[0])
         for h in range(self.H):
             sl = slice(h * self.hd, (h + 1) * self.hd)
-            for r in range(n):
-                T = int(q_pos[r]) + 1
-                s = (k_all[:T, sl] @ q[r, sl]) * scale
-                p = softmax(s)
-                out[r, sl] = p @ v_all[:T, sl]
+            k_h = np.ascontiguousarray(k_all[:, sl])
+            v_h = np.ascontiguousarray(v_all[:, sl])
+            for r0 in range(0, n, rows_per_block):
+                r1 = min(n, r0 + rows_per_block)
+                T = int(q_pos[r0:r1].max()) + 1          # keys any row of the block can see
+                s = (q[r0:r1, sl] @ k_h[:T].T) * scale
+                s = np.where(key_pos[None, :T] <= q_pos[r0:r1, None], s, -np.inf)
+                out[r0:r1, sl] = softmax(s, axis=-1) @ v_h[:T]
         return out
 
     def forward(self, cache: KVCache, ids: np.ndarray, phon_len: int) -> np.ndarray:

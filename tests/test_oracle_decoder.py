@@ -7,6 +7,7 @@ that computes the same decoder-only block, written by someone else.  The KV
 cache is checked against full recomputation, and the loop against the step
 count the method implies (Sec. 3.2: about L/n AR steps for L tokens).
 """
+import dataclasses
 import math
 
 import numpy as np
@@ -66,17 +67,19 @@ def _torch_reference(shape, w, ids, phon_len, n_heads_out):
     return x[0].numpy(), torch.stack(heads).numpy()
 
 
-@pytest.mark.parametrize("phon_len", [0, 7])
-def test_trunk_and_heads_match_torch_transformer(phon_len):
-    w = make_weights(SMALL, seed=3)
+@pytest.mark.parametrize("phon_len,T", [(0, 21), (7, 21), (5, 600)])
+def test_trunk_and_heads_match_torch_transformer(phon_len, T):
+    """T = 600 spans three of the oracle's 256-row attention blocks and a
+    ragged last one."""
+    shape = dataclasses.replace(SMALL, max_pos=1024)
+    w = make_weights(shape, seed=3)
     rng = np.random.default_rng(0)
-    T = 21
     ids = np.concatenate([rng.integers(0, 512, phon_len), rng.integers(0, 1024, T - phon_len)])
-    m = ARDecoder(SMALL, w)
+    m = ARDecoder(shape, w)
     cache = m.new_cache()
     h = m.forward(cache, ids, phon_len)
     logits = m.heads(h[-1], 3)
-    h_ref, logits_ref = _torch_reference(SMALL, w, ids, phon_len, 3)
+    h_ref, logits_ref = _torch_reference(shape, w, ids, phon_len, 3)
     np.testing.assert_allclose(h, h_ref, atol=1e-10, rtol=1e-10)
     np.testing.assert_allclose(logits, logits_ref, atol=1e-10, rtol=1e-10)
 
