@@ -30,9 +30,10 @@ HBM_PEAK_GBS = 8000.0
 def _parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    # three whole generations timed after one whole generation of warm-up:
-    # the step time varies by a few percent between generations
-    ap.add_argument("--steps", type=int, default=564)
+    # three whole generations (187 full steps each) timed after one whole
+    # generation of warm-up: the step time varies by a few percent between
+    # generations
+    ap.add_argument("--steps", type=int, default=561)
     ap.add_argument("--warmup", type=int, default=188)
     ap.add_argument("--workload", default="valle_k4")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -57,10 +58,17 @@ def _steps_per_generation(wl):
 
 
 def time_decode(sess, wl, prompts, steps, warmup, torch, top_k=None):
-    """Warm up, then time exactly `steps` decode steps (prefills in between
-    generations are outside the timed intervals).  Returns (ms, tokens)."""
+    """Warm up, then time exactly `steps` decode steps that each run the whole
+    path.  The first step after a prefill has no pending chunk (it runs the
+    heads and the selection on the prompt's last hidden state), so it is never
+    timed; a generation's remaining steps 1 .. S-1 are.  Whole generations
+    are timed while `steps` covers them; the rest (or all of a shorter run) is
+    the window of consecutive steps centred on the middle of a generation, so
+    its mean context, and with it the step time, is the generation's mean.
+    Prefills are outside the timed intervals.  Returns (ms, tokens)."""
     top_k = wl.top_k if top_k is None else top_k
     per_gen = _steps_per_generation(wl)
+    full = per_gen - 1                       # steps with a pending chunk per generation
     st = sess.stream
     # warmup (also instantiates the hipGraphs of the step)
     sess.prefill(prompts.phon, prompts.ac)
@@ -71,9 +79,13 @@ def time_decode(sess, wl, prompts, steps, warmup, torch, top_k=None):
     torch.cuda.synchronize()
     total_ms, tokens, done = 0.0, 0, 0
     while done < steps:
+        n = min(full, steps - done)
+        first = 1 + (full - n) // 2          # window start (step index within the generation)
         sess.prefill(prompts.phon, prompts.ac)
-        n = min(per_gen, steps - done)
+        for _ in range(first):
+            sess.step_async(wl.K, top_k)
         torch.cuda.synchronize()
+        gen0 = int(sess.seq_state()["gen"].sum())
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
         e0.record(st)
@@ -82,7 +94,7 @@ def time_decode(sess, wl, prompts, steps, warmup, torch, top_k=None):
         e1.record(st)
         torch.cuda.synchronize()
         total_ms += e0.elapsed_time(e1)
-        tokens += int(sess.seq_state()["gen"].sum())
+        tokens += int(sess.seq_state()["gen"].sum()) - gen0
         done += n
     return total_ms, tokens
 
@@ -168,7 +180,6 @@ def replay_kernels(sess, wl, prompts, steps, iters, torch, cold=True):
     class's launches in one decode step (one per layer), mid-generation after
     `steps` decode steps; with `cold`, the caches are evicted before each pass
     as the other layers' weights evict them in a real step."""
-    from paper_2410_13839_amd.binding import mtp_profile_replay
     sess.prefill(prompts.phon, prompts.ac)
     for i in range(steps):
         sess.step_async(wl.K, wl.top_k)
@@ -179,7 +190,7 @@ def replay_kernels(sess, wl, prompts, steps, iters, torch, cold=True):
     ctx = int(sess.seq_state()["ctx_len"].max())
     out = {}
     for kc in KCLASSES:
-        out[kc] = mtp_profile_replay(sess.ctx, kc, iters, cold)
+        out[kc] = sess.replay(kc, iters, cold)
         print(f"[bench] replay {'cold' if cold else 'warm'} class {kc}: {out[kc]:.3f} us", file=sys.stderr, flush=True)
     return out, ctx
 
@@ -506,8 +517,7 @@ def main():
 
     # selection variants (Sec. 3.3): throughput of the whole step and the
     # selection kernel's own launch time (cold passes at step `mid`)
-    from paper_2410_13839_amd.binding import (MTP_KCLASS_SELECT, MTP_SELECT_BEST, MTP_SELECT_SAMPLE,
-                                              mtp_profile_replay)
+    from paper_2410_13839_amd.binding import MTP_KCLASS_SELECT, MTP_SELECT_BEST, MTP_SELECT_SAMPLE
     variants = []
     if not args.no_variants:
         for lat, anch, tk, smp, what in (
@@ -520,14 +530,15 @@ def main():
                 (1, False, wl.top_k, True, "top_k sampling in the union lattice, temperature 1")):
             sess.set_selection(lat, anch)
             sess.set_sampling(MTP_SELECT_SAMPLE if smp else MTP_SELECT_BEST, 1.0, 2024)
-            vms, vtok = time_decode(sess, wl, prompts, _steps_per_generation(wl), 5, torch, top_k=tk)
+            n_full = _steps_per_generation(wl) - 1
+            vms, vtok = time_decode(sess, wl, prompts, n_full, 5, torch, top_k=tk)
             sess.prefill(prompts.phon, prompts.ac)
             for _ in range(mid):
                 sess.step_async(wl.K, tk)
             torch.cuda.synchronize()
-            sel_us = mtp_profile_replay(sess.ctx, MTP_KCLASS_SELECT, passes, True)
+            sel_us = sess.replay(MTP_KCLASS_SELECT, passes, True)
             v = {"lattice": "union" if lat else "own", "anchored": anch, "top_k": tk, "sampled": smp, "selection": what,
-                 "tokens_per_s": round(vtok / (vms / 1000.0), 1), "us_per_step": round(vms * 1000.0 / _steps_per_generation(wl), 2),
+                 "tokens_per_s": round(vtok / (vms / 1000.0), 1), "us_per_step": round(vms * 1000.0 / n_full, 2),
                  "select_kernel_us": round(sel_us, 3)}
             variants.append(v)
             print(f"[bench] variant {v}", file=sys.stderr, flush=True)

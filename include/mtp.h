@@ -72,7 +72,7 @@ typedef struct mtp_config {
     int32_t max_prompt;   /* phonemes + acoustic tokens per sequence              */
     int32_t max_new;      /* generation budget per sequence (tokens)              */
     int32_t eos_min;      /* EOS masked while the generated index is < eos_min    */
-    int32_t page_size;    /* tokens per KV page (power of two, 8..128)            */
+    int32_t page_size;    /* tokens per KV page: 16 (MTP_EINVAL otherwise)        */
     int32_t num_pages;    /* pages in the pool; 0 = max_batch full sequences      */
     int32_t dtype;        /* MTP_DTYPE_*                                          */
     int32_t flags;        /* MTP_FLAG_*                                           */
@@ -200,6 +200,23 @@ int mtp_get_logits(mtp_ctx* ctx, float* logits);
 int mtp_get_lattice(mtp_ctx* ctx, int32_t* cand, float* ehat, float* delta,
                     int32_t* psi, int32_t* slots);
 
+/* Teacher forcing (Sec. 3.1, Eq. 1: each token is generated conditioned on
+ * the given history).  Replaces the tokens the last decode step emitted with
+ * the caller's, as if the step had selected them: host arrays tokens[B*K]
+ * (K of that step; row b's first count[b] entries are used) and count[B].
+ * A sequence the step ran (it emitted at least one token) takes 1 <= count[b]
+ * <= min(K, max_new - generated count before the step); a sequence that had
+ * ended before the step takes count[b] = 0.  Ids must be in [0, vocab); EOS
+ * (eos_id) only as a sequence's last forced token and at a generated index
+ * >= eos_min.  The forced tokens replace the step's outputs (the values
+ * mtp_decode_step returned, the emitted history, the generated count, the
+ * anchor token) and become the pending chunk of the next step; EOS or the
+ * budget ends the sequence.  The step's logits and lattice are kept.  May be
+ * called again for the same step.  Synchronises.  MTP_ESTATE unless a decode
+ * step ran since the last prefill (and no profile replay since); MTP_EINVAL
+ * for bad arguments, with nothing changed. */
+int mtp_force_tokens(mtp_ctx* ctx, const int32_t* tokens, const int32_t* count);
+
 /* Selection options for the following decode steps (paper Sec. 3.3, Fig. 2).
  * lattice MTP_LATTICE_OWN (default): position t's states are head t's own
  * top_k.  MTP_LATTICE_UNION: every position's states are the m <= K*top_k
@@ -265,19 +282,21 @@ int mtp_get_tokens(mtp_ctx* ctx, int32_t* tokens);
 /* Kernel timing for measurement.  Replays the launches of kernel class
  * `kclass` (MTP_KCLASS_*) recorded for the most recent decode step (one per
  * layer, or one for the heads), in order, `iters` times on the context
- * stream; each pass is bracketed by two HIP events and, with `cold` != 0,
- * preceded (outside the events) by a read of a 512 MiB buffer that evicts the
- * weights from the L2 and last-level caches, as in a real step where the
- * other layers' weights pass through them between two launches of a class.
- * A pass repeats the recorded launches until it holds at least 12 (the
- * heads' single launch is replayed 12 times, the later ones cache-warm).
+ * stream; each pass is bracketed by two HIP events.  With a non-NULL
+ * flush_buf (DEVICE memory owned by the caller, flush_bytes long, 16-byte
+ * aligned, a multiple of 16 bytes and at least 1 KiB) each pass is preceded,
+ * outside the events, by a read of that buffer; 512 MiB evicts the weights
+ * from the L2 and last-level caches, as in a real step where the other
+ * layers' weights pass through them between two launches of a class.  The
+ * read may write one word into the buffer.  NULL and 0 time cache-warm
+ * passes.  A pass repeats the recorded launches until it holds at least 12
+ * (the heads' single launch is replayed 12 times, the later ones cache-warm).
  * Returns the average time per launch in microseconds (synchronises; one
  * launch latency per pass is included).  The replayed launches keep their
  * arguments and may overwrite the residual stream and the cache rows of the
  * next positions: the context needs mtp_prefill before the next decode step
- * (MTP_ESTATE otherwise).  The first cold call allocates the eviction buffer
- * (freed by mtp_destroy).  MTP_ESTATE if the last step launched nothing of
- * the class. */
+ * (MTP_ESTATE otherwise).  MTP_ESTATE if the last step launched nothing of
+ * the class; MTP_EINVAL for a bad class, iters < 1 or a bad buffer. */
 #define MTP_KCLASS_GEMM_FFN1   1   /* LN2 -> x W_1^T -> GELU                  */
 #define MTP_KCLASS_GEMM_FFN2   2   /* GELU out x W_2^T (residual partials)    */
 #define MTP_KCLASS_GEMM_QKV    3   /* LN1 -> x W_qkv^T, K/V into the cache    */
@@ -285,7 +304,8 @@ int mtp_get_tokens(mtp_ctx* ctx, int32_t* tokens);
 #define MTP_KCLASS_HEADS       5   /* final LN -> K head projections          */
 #define MTP_KCLASS_GEMM_OPROJ  6   /* attention out x W_o^T (residual part.)  */
 #define MTP_KCLASS_SELECT      7   /* top_k, Viterbi lattice and accept       */
-int mtp_profile_replay(mtp_ctx* ctx, int kclass, int iters, int cold, double* avg_us);
+int mtp_profile_replay(mtp_ctx* ctx, int kclass, int iters, void* flush_buf, uint64_t flush_bytes,
+                       double* avg_us);
 
 /* ---- Transition-table estimation (Sec. 3.3: Q is derived from the
  * training corpus).  Context-free; all pointers are DEVICE pointers and the

@@ -29,6 +29,7 @@ from dataclasses import dataclass, field
 from typing import Dict, List, Optional
 
 import numpy as np
+import torch
 from scipy.special import erf
 
 LN_EPS = 1e-5
@@ -110,26 +111,30 @@ class ARDecoder:
         q: [n, d]; k_all, v_all: [T, d] with row index = absolute position;
         query r at position q_pos[r] sees keys 0..q_pos[r].  Per head h the
         textbook form softmax(Q_h K_h^T / sqrt(64) + M) V_h, with M = -inf
-        where the key's position exceeds the query's.  Query rows are taken
-        `rows_per_block` at a time only to bound the size of the score
-        matrix; each row's result does not depend on the blocking.
+        where the key's position exceeds the query's, evaluated with plain
+        float64 PyTorch CPU operations (multi-threaded; the arithmetic is the
+        formula as written).  Query rows are taken `rows_per_block` at a time
+        only to bound the size of the score matrix; each row's result does
+        not depend on the blocking.
         """
         n = q.shape[0]
-        out = np.zeros((n, self.d))
+        out = torch.zeros((n, self.d), dtype=torch.float64)
         scale = 1.0 / np.sqrt(self.hd)
-        q_pos = np.asarray(q_pos, dtype=np.int64)
-        key_pos = np.arange(k_all.shape[0])
+        qt = torch.from_numpy(np.ascontiguousarray(q, dtype=np.float64))
+        kt = torch.from_numpy(np.ascontiguousarray(k_all, dtype=np.float64))
+        vt = torch.from_numpy(np.ascontiguousarray(v_all, dtype=np.float64))
+        qp = torch.as_tensor(np.asarray(q_pos, dtype=np.int64))
+        kp = torch.arange(kt.shape[0])
         for h in range(self.H):
             sl = slice(h * self.hd, (h + 1) * self.hd)
-            k_h = np.ascontiguousarray(k_all[:, sl])
-            v_h = np.ascontiguousarray(v_all[:, sl])
+            k_h, v_h = kt[:, sl].contiguous(), vt[:, sl].contiguous()
             for r0 in range(0, n, rows_per_block):
                 r1 = min(n, r0 + rows_per_block)
-                T = int(q_pos[r0:r1].max()) + 1          # keys any row of the block can see
-                s = (q[r0:r1, sl] @ k_h[:T].T) * scale
-                s = np.where(key_pos[None, :T] <= q_pos[r0:r1, None], s, -np.inf)
-                out[r0:r1, sl] = softmax(s, axis=-1) @ v_h[:T]
-        return out
+                T = int(qp[r0:r1].max()) + 1            # keys any row of the block can see
+                s = (qt[r0:r1, sl] @ k_h[:T].T) * scale
+                s = s.masked_fill(kp[None, :T] > qp[r0:r1, None], float("-inf"))
+                out[r0:r1, sl] = torch.softmax(s, dim=-1) @ v_h[:T]
+        return out.numpy()
 
     def forward(self, cache: KVCache, ids: np.ndarray, phon_len: int) -> np.ndarray:
         """Run the trunk over new tokens appended after the cached prefix.

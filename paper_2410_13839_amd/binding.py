@@ -31,7 +31,8 @@ MTP_FLAG_NO_GRAPH, MTP_FLAG_NAR = 1, 2
  MTP_KCLASS_GEMM_OPROJ, MTP_KCLASS_SELECT) = 1, 2, 3, 4, 5, 6, 7
 
 EXPORTED = ["mtp_query_sizes", "mtp_weight_offset", "mtp_create", "mtp_prefill", "mtp_decode_step",
-            "mtp_decode_step_async", "mtp_get_logits", "mtp_get_lattice", "mtp_get_seq_state", "mtp_get_tokens",
+            "mtp_decode_step_async", "mtp_get_logits", "mtp_get_lattice", "mtp_force_tokens", "mtp_get_seq_state",
+            "mtp_get_tokens",
             "mtp_profile_replay", "mtp_reset", "mtp_destroy", "mtp_last_error", "mtp_strerror",
             "mtp_set_selection", "mtp_get_union_lattice", "mtp_set_sampling", "mtp_get_uniforms",
             "mtp_q_workspace_size", "mtp_q_count", "mtp_q_normalize",
@@ -70,6 +71,7 @@ _lib.mtp_decode_step.argtypes = [_ctx, ctypes.c_int, ctypes.c_int, _i32p, _i32p]
 _lib.mtp_decode_step_async.argtypes = [_ctx, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
 _lib.mtp_get_logits.argtypes = [_ctx, _f32p]
 _lib.mtp_get_lattice.argtypes = [_ctx, _i32p, _f32p, _f32p, _i32p, _i32p]
+_lib.mtp_force_tokens.argtypes = [_ctx, _i32p, _i32p]
 _lib.mtp_set_selection.argtypes = [_ctx, ctypes.c_int, ctypes.c_int]
 _lib.mtp_get_union_lattice.argtypes = [_ctx, _i32p, _i32p, _f32p, _f32p, _i32p, _i32p]
 _lib.mtp_set_sampling.argtypes = [_ctx, ctypes.c_int, ctypes.c_float, ctypes.c_uint64]
@@ -85,7 +87,8 @@ _lib.mtp_nar_get_codes.argtypes = [_ctx, _i32p]
 _lib.mtp_nar_get_logits.argtypes = [_ctx, ctypes.c_int, _f32p]
 _lib.mtp_get_seq_state.argtypes = [_ctx, _i32p, _i32p, _i32p, _i32p]
 _lib.mtp_get_tokens.argtypes = [_ctx, _i32p]
-_lib.mtp_profile_replay.argtypes = [_ctx, ctypes.c_int, ctypes.c_int, ctypes.c_int, _P(ctypes.c_double)]
+_lib.mtp_profile_replay.argtypes = [_ctx, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_uint64,
+                                    _P(ctypes.c_double)]
 _lib.mtp_reset.argtypes = [_ctx]
 _lib.mtp_destroy.argtypes = [_ctx]
 _lib.mtp_destroy.restype = None
@@ -247,10 +250,19 @@ def mtp_get_tokens(ctx, B: int, max_new: int) -> np.ndarray:
     return out
 
 
-def mtp_profile_replay(ctx, kclass: int, iters: int, cold: bool = True) -> float:
+def mtp_profile_replay(ctx, kclass: int, iters: int, flush_buf: int = 0, flush_bytes: int = 0) -> float:
+    """flush_buf: device pointer (integer) of the caller's eviction buffer, 0 for cache-warm passes."""
     us = ctypes.c_double()
-    _check(_lib.mtp_profile_replay(ctx, kclass, iters, int(cold), ctypes.byref(us)), ctx, "mtp_profile_replay")
+    _check(_lib.mtp_profile_replay(ctx, kclass, iters, ctypes.c_void_p(flush_buf or None), flush_bytes,
+                                   ctypes.byref(us)), ctx, "mtp_profile_replay")
     return us.value
+
+
+def mtp_force_tokens(ctx, tokens: np.ndarray, count: Sequence[int]) -> None:
+    """tokens: [B, K] of the last step (row b's first count[b] entries used)."""
+    tk, tkp = _i32(tokens)
+    cn, cnp = _i32(count)
+    _check(_lib.mtp_force_tokens(ctx, tkp, cnp), ctx, "mtp_force_tokens")
 
 
 def mtp_q_workspace_size(n_tokens: int, n_seqs: int, vocab: int) -> int:
@@ -416,6 +428,21 @@ class Session:
 
     def lattice(self, K: int, top_k: int) -> Dict[str, np.ndarray]:
         return mtp_get_lattice(self.ctx, self.B, K, top_k)
+
+    def force(self, tokens: np.ndarray, count: Sequence[int]) -> None:
+        mtp_force_tokens(self.ctx, tokens, count)
+
+    FLUSH_BYTES = 512 << 20
+
+    def replay(self, kclass: int, iters: int, cold: bool = True) -> float:
+        """Average launch time of one kernel class of the last step (us); cold
+        passes read a 512 MiB buffer of this session first (evicting L2 and
+        the last-level cache)."""
+        if not cold:
+            return mtp_profile_replay(self.ctx, kclass, iters)
+        if getattr(self, "flush", None) is None:
+            self.flush = self.torch.empty(self.FLUSH_BYTES, dtype=self.torch.uint8, device=self.device)
+        return mtp_profile_replay(self.ctx, kclass, iters, self.flush.data_ptr(), self.FLUSH_BYTES)
 
     def set_selection(self, lattice: int = MTP_LATTICE_OWN, anchored: bool = False) -> None:
         mtp_set_selection(self.ctx, lattice, anchored)

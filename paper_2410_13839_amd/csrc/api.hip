@@ -117,7 +117,9 @@ int validate(const mtp_config* c, std::string* why) {
     if (c->max_new < 1) return bad("max_new must be positive");
     if ((int64_t)c->max_prompt + c->max_new > c->max_pos) return bad("max_prompt + max_new exceeds max_pos");
     if ((int64_t)c->max_prompt + c->max_new > 16384) return bad("max_prompt + max_new exceeds 16384");
-    if (c->page_size < 8 || c->page_size > 128 || (c->page_size & (c->page_size - 1))) return bad("page_size must be a power of two in 8..128");
+    // 16-key pages: one 16-key MFMA tile per page in the attention kernels
+    // and the transposed V block of a page is one 16-byte operand per dimension
+    if (c->page_size != 16) return bad("page_size must be 16");
     if (c->num_pages < 0) return bad("num_pages must be >= 0");
     if (c->dtype != MTP_DTYPE_F32 && c->dtype != MTP_DTYPE_BF16) return bad("unknown dtype");
     if ((c->flags & ~(MTP_FLAG_NO_GRAPH | MTP_FLAG_NAR)) != 0) return bad("unknown flags");
@@ -234,7 +236,6 @@ struct mtp_ctx {
     StepLaunches* recording = nullptr;
     StepKey last_key{};
     bool has_last = false;
-    void* flush_buf = nullptr;   // cache eviction source of cold replays
 
     char* W() const { return (char*)buf.weights; }
     char* WS() const { return (char*)buf.workspace; }
@@ -820,6 +821,62 @@ int mtp_get_lattice(mtp_ctx* c, int32_t* cand, float* ehat, float* delta, int32_
     return MTP_OK;
 }
 
+int mtp_force_tokens(mtp_ctx* c, const int32_t* tokens, const int32_t* count) {
+    if (!c) return MTP_EINVAL;
+    if (is_nar(c->cfg)) { c->err = "a NAR context has no decode steps"; return MTP_EINVAL; }
+    if (!c->prefilled || !c->last_K) { c->err = "no decode step to force since the last prefill"; return MTP_ESTATE; }
+    if (!tokens || !count) { c->err = "NULL token or count array"; return MTP_EINVAL; }
+    const mtp_config& cf = c->cfg;
+    const int B = c->B, K = c->last_K;
+    hipStream_t st = c->stream;
+    std::vector<SeqState> s(B);
+    std::vector<int32_t> n_old(B);
+    HIPCHK(c, hipMemcpyAsync(s.data(), c->WS() + c->ws.state, B * sizeof(SeqState), hipMemcpyDeviceToHost, st), "state to host");
+    HIPCHK(c, hipMemcpyAsync(n_old.data(), c->WS() + c->ws.out_cnt, B * 4, hipMemcpyDeviceToHost, st), "counts to host");
+    HIPCHK(c, hipStreamSynchronize(st), "sync");
+    // validate everything before changing anything
+    for (int b = 0; b < B; ++b) {
+        const int n = count[b], g0 = s[b].gen - n_old[b];
+        if (n_old[b] == 0) {
+            if (n != 0) { c->err = "a sequence that had ended before the step takes count 0"; return MTP_EINVAL; }
+            continue;
+        }
+        if (n < 1 || n > K || n > cf.max_new - g0) { c->err = "forced count out of range"; return MTP_EINVAL; }
+        for (int i = 0; i < n; ++i) {
+            const int32_t t = tokens[(size_t)b * K + i];
+            if (t < 0 || t >= cf.vocab) { c->err = "forced token id out of range"; return MTP_EINVAL; }
+            if (t == cf.eos_id && (i != n - 1 || g0 + i < cf.eos_min)) {
+                c->err = "a forced EOS must be the last forced token and at a generated index >= eos_min";
+                return MTP_EINVAL;
+            }
+        }
+    }
+    std::vector<int32_t> out_tok((size_t)B * K, -1), out_cnt(B);
+    for (int b = 0; b < B; ++b) {
+        const int n = count[b];
+        out_cnt[b] = n;
+        if (n_old[b] == 0) continue;
+        const int g0 = s[b].gen - n_old[b];
+        const int32_t* tb = tokens + (size_t)b * K;
+        for (int i = 0; i < n; ++i) {
+            out_tok[(size_t)b * K + i] = tb[i];
+            s[b].pend_ids[i] = tb[i];
+        }
+        const bool done = tb[n - 1] == cf.eos_id || g0 + n >= cf.max_new;
+        s[b].gen = g0 + n;
+        s[b].done = done ? 1 : 0;
+        s[b].pend_len = done ? 0 : n;
+        s[b].last_tok = tb[n - 1];
+        HIPCHK(c, hipMemcpyAsync(c->WS() + c->ws.hist + ((size_t)b * cf.max_new + g0) * 4, tb, (size_t)n * 4,
+                                 hipMemcpyHostToDevice, st), "history");
+    }
+    HIPCHK(c, hipMemcpyAsync(c->WS() + c->ws.state, s.data(), B * sizeof(SeqState), hipMemcpyHostToDevice, st), "state");
+    HIPCHK(c, hipMemcpyAsync(c->WS() + c->ws.out_tok, out_tok.data(), out_tok.size() * 4, hipMemcpyHostToDevice, st), "tokens");
+    HIPCHK(c, hipMemcpyAsync(c->WS() + c->ws.out_cnt, out_cnt.data(), B * 4, hipMemcpyHostToDevice, st), "counts");
+    HIPCHK(c, hipStreamSynchronize(st), "sync");
+    return MTP_OK;
+}
+
 int mtp_set_selection(mtp_ctx* c, int lattice, int anchored) {
     if (!c) return MTP_EINVAL;
     if (lattice != MTP_LATTICE_OWN && lattice != MTP_LATTICE_UNION) { c->err = "unknown lattice"; return MTP_EINVAL; }
@@ -1062,8 +1119,14 @@ int mtp_get_tokens(mtp_ctx* c, int32_t* tokens) {
     return MTP_OK;
 }
 
-int mtp_profile_replay(mtp_ctx* c, int kclass, int iters, int cold, double* avg_us) {
+int mtp_profile_replay(mtp_ctx* c, int kclass, int iters, void* flush_buf, uint64_t flush_bytes, double* avg_us) {
     if (!c || !avg_us || iters < 1) return MTP_EINVAL;
+    if ((flush_buf == nullptr) != (flush_bytes == 0)) { c->err = "eviction buffer and size must be given together"; return MTP_EINVAL; }
+    if (flush_buf && (flush_bytes < 1024 || flush_bytes % 16 || ((uintptr_t)flush_buf & 15))) {
+        c->err = "eviction buffer must be 16-byte aligned and a multiple of 16 bytes, at least 1 KiB";
+        return MTP_EINVAL;
+    }
+    const bool cold = flush_buf != nullptr;
     if (kclass < MTP_KCLASS_GEMM_FFN1 || kclass > MTP_KCLASS_SELECT) { c->err = "unknown kernel class"; return MTP_EINVAL; }
     auto it = c->has_last ? c->step_launches.find(c->last_key) : c->step_launches.end();
     if (it == c->step_launches.end() || it->second.cls[kclass].empty()) {
@@ -1071,8 +1134,6 @@ int mtp_profile_replay(mtp_ctx* c, int kclass, int iters, int cold, double* avg_
         return MTP_ESTATE;
     }
     const std::vector<mtp_ctx::Launch>& v = it->second.cls[kclass];
-    const size_t flush_bytes = (size_t)MTP_FLUSH_MB << 20;
-    if (cold && !c->flush_buf) HIPCHK(c, hipMalloc(&c->flush_buf, flush_bytes), "flush buffer");
     // from here on the residual stream and the cache rows of the next
     // positions no longer hold what the next step expects
     c->prefilled = false;
@@ -1085,7 +1146,7 @@ int mtp_profile_replay(mtp_ctx* c, int kclass, int iters, int cold, double* avg_
     const size_t reps = (12 + v.size() - 1) / v.size();
     double total_ms = 0.0;
     for (int i = 0; i < iters && e == hipSuccess; ++i) {
-        if (cold) e = cache_flush(c->stream, c->flush_buf, flush_bytes);
+        if (cold) e = cache_flush(c->stream, flush_buf, (size_t)flush_bytes);
         if (e == hipSuccess) e = hipEventRecord(e0, c->stream);
         for (size_t j = 0; j < v.size() * reps && e == hipSuccess; ++j) e = v[j % v.size()](c->stream);
         if (e == hipSuccess) e = hipEventRecord(e1, c->stream);
@@ -1114,7 +1175,6 @@ void mtp_destroy(mtp_ctx* c) {
     if (!c) return;
     if (c->stream) (void)hipStreamSynchronize(c->stream);
     for (auto& kv : c->graphs) (void)hipGraphExecDestroy(kv.second);
-    if (c->flush_buf) (void)hipFree(c->flush_buf);
     delete c;
 }
 

@@ -1,6 +1,6 @@
-// Causal attention of up to 8 query rows of one sequence over its paged KV
-// cache (decode: the pending chunk of K tokens; prefill: 8-row tiles of the
-// prompt).  Memory-bound at decode, so it is VALU, not MFMA:
+// Causal attention of up to 8 query rows of one sequence over its paged fp32
+// KV cache (decode: the pending chunk of K tokens; prefill: 8-row tiles of
+// the prompt), for the fp32 model.  Memory-bound at decode, so it is VALU:
 //
 //  * one workgroup per (tile, head, key split); 256 threads = 32 key groups
 //    x 8 dimension chunks, so 8 consecutive lanes read one key's 128-byte
@@ -23,15 +23,6 @@ constexpr int CH = 256;        // keys per LDS chunk (== threads per block)
 constexpr int PSTRIDE = 68;    // floats per partial row: max, sum, 2 pad, 64 outputs (16-byte aligned)
 
 template <typename KVT> struct KVRow;
-template <> struct KVRow<bf16_t> {
-    __device__ static __forceinline__ void load8(const bf16_t* p, float (&f)[8]) {
-        uint4 v = *reinterpret_cast<const uint4*>(p);
-        f[0] = __uint_as_float(v.x << 16); f[1] = __uint_as_float(v.x & 0xFFFF0000u);
-        f[2] = __uint_as_float(v.y << 16); f[3] = __uint_as_float(v.y & 0xFFFF0000u);
-        f[4] = __uint_as_float(v.z << 16); f[5] = __uint_as_float(v.z & 0xFFFF0000u);
-        f[6] = __uint_as_float(v.w << 16); f[7] = __uint_as_float(v.w & 0xFFFF0000u);
-    }
-};
 template <> struct KVRow<float> {
     __device__ static __forceinline__ void load8(const float* p, float (&f)[8]) {
         float4 a = *reinterpret_cast<const float4*>(p);
@@ -251,8 +242,9 @@ static hipError_t attn_launch(hipStream_t st, const AttnArgs& a) {
     return hipGetLastError();
 }
 
+// fp32 caches only: bf16 caches take the MFMA kernels of attn_mfma.hip
 hipError_t attention(hipStream_t st, const AttnArgs& a) {
-    if (a.dtype == 1) return attn_launch<bf16_t, bf16_t>(st, a);
+    if (a.dtype != 0) return hipErrorInvalidValue;
     return attn_launch<float, float>(st, a);
 }
 
@@ -496,9 +488,11 @@ hipError_t attention_decode_merge(hipStream_t st, const AttnDecArgs& a) {
     return hipGetLastError();
 }
 
+// fp32 caches only (bf16 decode runs attn_dec_kernel of attn_mfma.hip, whose
+// split partials attention_decode_merge also merges)
 hipError_t attention_decode(hipStream_t st, const AttnDecArgs& a) {
     if (a.split_len < 32 || a.split_len % 32 || a.n_splits < 1 || a.n_splits > 64) return hipErrorInvalidValue;
-    if (a.dtype == 1) return attn_dec_launch<bf16_t, bf16_t>(st, a);
+    if (a.dtype != 0) return hipErrorInvalidValue;
     return attn_dec_launch<float, float>(st, a);
 }
 

@@ -1,5 +1,5 @@
 // Attention for the bf16 cache on MFMA: decode (attn_dec_kernel) and prefill
-// (attn_prefill_kernel), flash-style online softmax with every key product on
+// (attn_prefill_fa_kernel), flash-style online softmax with every key product on
 // the matrix cores and the probabilities kept in registers.
 #include <math.h>
 
@@ -218,175 +218,6 @@ static hipError_t attn_dec_go(hipStream_t st, const AttnMfmaArgs& a) {
     return attn_dec_go_pd<NW, 1>(st, a);
 }
 
-// Prefill attention: one workgroup of 4 waves per (query tile, head); a tile
-// is at most 16 QT rows of one sequence (tiles[blockIdx.x] = first row, row
-// count), taken as QT sub-tiles of 16 queries.  Same arithmetic as the
-// decode kernel above: within a 64-key chunk each wave owns 16 consecutive
-// keys and keeps its own online-softmax state per sub-tile across the chunks,
-// so the chunk loop has no barrier, and every K / V^T fragment a wave loads
-// serves all QT sub-tiles; the four states are merged through LDS once.
-// Causal, or bidirectional (every row sees its sequence's ctx_len keys) with
-// p.bidir.
-template <int QT>
-__global__ __launch_bounds__(256) void attn_prefill_kernel(AttnMfmaArgs p) {
-    constexpr int NW = 4;
-    const int head = blockIdx.y, split = blockIdx.z;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int r = lane & 15, g = lane >> 4;
-    extern __shared__ float s_o[];               // [NW waves][QT][64 dims][17]
-    __shared__ float s_m[NW][QT * 16], s_l[NW][QT * 16];
-    constexpr int CH = 16 * NW;                  // keys per chunk
-    const bf16_t* pool = reinterpret_cast<const bf16_t*>(p.kv.pool);
-    const int P = p.kv.page_size;
-    const int max_key = p.kv.max_pages_per_seq * P - 1;
-    const int kb = split * p.split_len;
-    const int2 tile = p.tiles[blockIdx.x];
-    const int row0 = tile.x, nrows = tile.y;
-    const int b = p.rows[row0].seq;
-    const int rmax = max(nrows - 1, 0);
-
-    uint4 kf[2];
-    uint2 vf[4];
-    auto load_keys = [&](int c0) {
-        const int wk = c0 + 16 * wave;
-        const bf16_t* kp = pool + p.kv.offset(b, min(wk + r, max_key), 0, head) + g * 8;
-        kf[0] = *reinterpret_cast<const uint4*>(kp);
-        kf[1] = *reinterpret_cast<const uint4*>(kp + 32);
-        const bf16_t* vp = pool + p.kv.vt_offset(b, min(wk + 4 * g, max_key & ~3), head);
-#pragma unroll
-        for (int dt = 0; dt < 4; ++dt) vf[dt] = *reinterpret_cast<const uint2*>(vp + (size_t)(16 * dt + r) * P);
-    };
-    load_keys(kb);
-    float4 qa[QT][2], qb[QT][2];
-#pragma unroll
-    for (int j = 0; j < QT; ++j) {
-        const float* qp = p.q + (size_t)(row0 + min(16 * j + r, rmax)) * p.ldq + head * 64 + g * 8;
-        qa[j][0] = *reinterpret_cast<const float4*>(qp);
-        qb[j][0] = *reinterpret_cast<const float4*>(qp + 4);
-        qa[j][1] = *reinterpret_cast<const float4*>(qp + 32);
-        qb[j][1] = *reinterpret_cast<const float4*>(qp + 36);
-    }
-    const int pos0 = p.rows[row0].pos;
-    const bool bidir = p.bidir != 0;
-    const int kend = bidir ? p.st[b].ctx_len : pos0 + nrows;
-    if (nrows <= 0 || kb >= kend) return;       // uniform over the workgroup
-    const int ke = min(kb + p.split_len, kend);
-
-    bf16x8_t qf[QT][2];
-#pragma unroll
-    for (int j = 0; j < QT; ++j)
-#pragma unroll
-        for (int h2 = 0; h2 < 2; ++h2)
-            qf[j][h2] = __builtin_bit_cast(bf16x8_t, make_uint4(pk2(qa[j][h2].x * 0.125f, qa[j][h2].y * 0.125f),
-                                                                pk2(qa[j][h2].z * 0.125f, qa[j][h2].w * 0.125f),
-                                                                pk2(qb[j][h2].x * 0.125f, qb[j][h2].y * 0.125f),
-                                                                pk2(qb[j][h2].z * 0.125f, qb[j][h2].w * 0.125f)));
-
-    float m_run[QT], l_run[QT];                 // query 16 j + r, this wave's keys
-    f32x4_t acc[QT][4];                         // O^T rows 16 dt + 4 g + v, query 16 j + r
-#pragma unroll
-    for (int j = 0; j < QT; ++j) {
-        m_run[j] = -INFINITY;
-        l_run[j] = 0.f;
-#pragma unroll
-        for (int dt = 0; dt < 4; ++dt) acc[j][dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    }
-
-    for (int c0 = kb; c0 < ke; c0 += CH) {
-        const uint4 k0 = kf[0], k1 = kf[1];
-        uint2 v[4];
-#pragma unroll
-        for (int dt = 0; dt < 4; ++dt) v[dt] = vf[dt];
-        if (c0 + CH < ke) load_keys(c0 + CH);    // next chunk in flight (uniform branch)
-        const int wk = c0 + 16 * wave;
-        // V^T entries of keys past the context may hold anything: zero them
-        const int nvalid = ke - (wk + 4 * g);
-        if (nvalid < 4) {
-#pragma unroll
-            for (int dt = 0; dt < 4; ++dt) {
-                uint32_t w0 = v[dt].x, w1 = v[dt].y;
-                if (nvalid <= 0) w0 = 0u;
-                else if (nvalid == 1) w0 &= 0x0000FFFFu;
-                if (nvalid <= 2) w1 = 0u;
-                else w1 &= 0x0000FFFFu;
-                v[dt] = make_uint2(w0, w1);
-            }
-        }
-#pragma unroll
-        for (int j = 0; j < QT; ++j) {
-            f32x4_t s = f32x4_t{0.f, 0.f, 0.f, 0.f};
-            s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, k0), qf[j][0], s, 0, 0, 0);
-            s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, k1), qf[j][1], s, 0, 0, 0);
-            const int qi = 16 * j + r;
-            float sc[4];
-            float mx = -INFINITY;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int key = wk + 4 * g + e;
-                const bool ok = (key < ke) && (bidir || key <= pos0 + qi) && (qi < nrows);
-                sc[e] = ok ? s[e] : -INFINITY;
-                mx = fmaxf(mx, sc[e]);
-            }
-            mx = xor16_max(mx);
-            mx = xor32_max(mx);
-            const float m_new = fmaxf(m_run[j], mx);
-            const float scale = (m_run[j] == -INFINITY) ? 0.f : __expf(m_run[j] - m_new);
-            float pe[4], sum = 0.f;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                pe[e] = (sc[e] == -INFINITY) ? 0.f : __expf(sc[e] - m_new);
-                sum += pe[e];
-            }
-            sum = xor16_sum(sum);
-            sum = xor32_sum(sum);
-            l_run[j] = l_run[j] * scale + sum;
-            m_run[j] = m_new;
-            const s16x4_t pf = __builtin_bit_cast(s16x4_t, make_uint2(pk2(pe[0], pe[1]), pk2(pe[2], pe[3])));
-#pragma unroll
-            for (int dt = 0; dt < 4; ++dt) {
-                acc[j][dt] *= scale;
-                acc[j][dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4_t, v[dt]), pf,
-                                                                       acc[j][dt], 0, 0, 0);
-            }
-        }
-    }
-
-    // merge the NW waves' states
-#pragma unroll
-    for (int j = 0; j < QT; ++j)
-        if (g == 0) s_m[wave][16 * j + r] = m_run[j];
-    __syncthreads();
-#pragma unroll
-    for (int j = 0; j < QT; ++j) {
-        float M = -INFINITY;
-#pragma unroll
-        for (int w = 0; w < NW; ++w) M = fmaxf(M, s_m[w][16 * j + r]);
-        const float wsc = (m_run[j] == -INFINITY) ? 0.f : __expf(m_run[j] - M);
-#pragma unroll
-        for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-                s_o[((wave * QT + j) * 64 + 16 * dt + 4 * g + e) * 17 + r] = acc[j][dt][e] * wsc;
-        if (g == 0) s_l[wave][16 * j + r] = l_run[j] * wsc;
-    }
-    __syncthreads();
-    // output: (dim, query) pairs over the workgroup's threads
-    for (int idx = tid; idx < 64 * 16 * QT; idx += 64 * NW) {
-        const int dim = idx / (16 * QT), q = idx % (16 * QT);
-        if (q >= nrows) continue;
-        const int j = q >> 4, rr = q & 15;
-        float o = 0.f, L = 0.f, Mq = -INFINITY;
-#pragma unroll
-        for (int w = 0; w < NW; ++w) {
-            o += s_o[((w * QT + j) * 64 + dim) * 17 + rr];
-            L += s_l[w][q];
-            Mq = fmaxf(Mq, s_m[w][q]);
-        }
-        const int row = row0 + q, col = head * 64 + dim;
-        p.out[p.packed ? frag_off(row, col, p.ldo) : (size_t)row * p.ldo + col] = f32_to_bf16(o / L);
-    }
-}
-
 // Prefill attention, flash style (bf16 cache, 16-key pages): one workgroup
 // of 4 waves per (64-row query tile, head); wave w owns the tile's query rows
 // 16 w .. 16 w + 15 and runs over the keys in blocks of 64 (four pages).
@@ -595,22 +426,8 @@ __global__ __launch_bounds__(256) void attn_prefill_fa_kernel(AttnMfmaArgs p) {
     }
 }
 
-template <int QT>
-static hipError_t attn_prefill_go(hipStream_t st, const AttnMfmaArgs& a) {
-    const size_t lds = (size_t)4 * QT * 64 * 17 * sizeof(float);
-    static bool attr_set = false;               // the dynamic-LDS limit, raised once per process
-    if (!attr_set && lds > 48 * 1024) {
-        hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_prefill_kernel<QT>),
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        if (err != hipSuccess) return err;
-        attr_set = true;
-    }
-    hipLaunchKernelGGL((attn_prefill_kernel<QT>), dim3(a.n_tiles, a.kv.n_heads, 1), dim3(256), lds, st, a);
-    return hipGetLastError();
-}
-
 hipError_t attention_mfma(hipStream_t st, const AttnMfmaArgs& a) {
-    if (a.split_len < 32 || a.n_splits < 1 || a.n_splits > 64 || a.kv.page_size < 8) return hipErrorInvalidValue;
+    if (a.split_len < 32 || a.n_splits < 1 || a.n_splits > 64 || a.kv.page_size != 16) return hipErrorInvalidValue;
     if (a.mode == 0) {
         // decode: pending chunk of at most 16 rows per sequence
         if (a.Q < 1 || a.Q > 16 || a.qt < a.Q) return hipErrorInvalidValue;
@@ -627,17 +444,12 @@ hipError_t attention_mfma(hipStream_t st, const AttnMfmaArgs& a) {
     }
     // prefill: tiles of at most a.qt rows (16, 32 or 64), one split
     if (a.n_splits != 1) return hipErrorInvalidValue;
-    if (a.qt == 64 && a.kv.page_size == 16) {
-        // dynamic LDS: one page number per page of a sequence
-        const size_t lds = (size_t)a.kv.max_pages_per_seq * sizeof(int);
-        if (lds > 48 * 1024) return hipErrorInvalidValue;
-        hipLaunchKernelGGL(attn_prefill_fa_kernel, dim3(a.n_tiles, a.kv.n_heads, 1), dim3(256), lds, st, a);
-        return hipGetLastError();
-    }
-    if (a.qt == 64) return attn_prefill_go<4>(st, a);
-    if (a.qt == 32) return attn_prefill_go<2>(st, a);
-    if (a.qt == 16) return attn_prefill_go<1>(st, a);
-    return hipErrorInvalidValue;
+    if (a.qt != 64) return hipErrorInvalidValue;
+    // dynamic LDS: one page number per page of a sequence
+    const size_t lds = (size_t)a.kv.max_pages_per_seq * sizeof(int);
+    if (lds > 48 * 1024) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(attn_prefill_fa_kernel, dim3(a.n_tiles, a.kv.n_heads, 1), dim3(256), lds, st, a);
+    return hipGetLastError();
 }
 
 }  // namespace mtp

@@ -10,7 +10,6 @@
 #define MTP_PREFILL_ROWS 64    // query rows per prefill attention tile (bf16)
 #define MTP_ATTN_QT 8          // query rows per attention tile
 #define MTP_SPLITK_MAX 8
-#define MTP_FLUSH_MB 512       // cache eviction read of cold replay timing
 
 typedef uint16_t bf16_t;  // raw bfloat16 bits
 

@@ -37,7 +37,8 @@ def _cfg(**kw):
 
 
 @pytest.mark.parametrize("field,value", [("d_model", 1000), ("n_heads", 15), ("k_heads", 9), ("k_heads", 0),
-                                         ("topk_max", 33), ("page_size", 12), ("dtype", 7), ("vocab", 5000),
+                                         ("topk_max", 33), ("page_size", 12), ("page_size", 8), ("page_size", 32),
+                                         ("page_size", 64), ("dtype", 7), ("vocab", 5000),
                                          ("max_new", 5000), ("eos_id", 1025), ("max_batch", 0)])
 def test_query_sizes_rejects_bad_configs(field, value):
     from paper_2410_13839_amd import binding as b
@@ -96,6 +97,13 @@ def test_calls_validate_before_gpu_work():
         assert e.value.code == b.MTP_EINVAL
         with pytest.raises(b.MTPError) as e:       # nothing launched yet
             b.mtp_profile_replay(ctx, b.MTP_KCLASS_GEMM_FFN1, 10)
+        assert e.value.code == b.MTP_ESTATE
+        for buf, nbytes in ((4096, 0), (0, 4096), (4096, 1000), (4104, 4096), (4096, 512)):
+            with pytest.raises(b.MTPError) as e:   # eviction buffer without size, unaligned or too small
+                b.mtp_profile_replay(ctx, b.MTP_KCLASS_GEMM_FFN1, 10, buf, nbytes)
+            assert e.value.code == b.MTP_EINVAL
+        with pytest.raises(b.MTPError) as e:       # teacher forcing before any decode step
+            b.mtp_force_tokens(ctx, np.zeros((1, 4), np.int32), [4])
         assert e.value.code == b.MTP_ESTATE
     finally:
         b.mtp_destroy(ctx)
