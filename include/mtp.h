@@ -337,6 +337,21 @@ int mtp_q_count(const int32_t* tokens, int64_t n_tokens, const int64_t* offsets,
                 int vocab, int eos_id, int flags, uint32_t* counts, uint64_t* status,
                 void* workspace, uint64_t ws_bytes, void* hip_stream);
 
+/* mtp_q_count without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  Same arguments, checks and results as
+ * mtp_q_count; the scratch is a fixed array of MTP_Q_NOALLOC_SCRATCH_BYTES
+ * inside the library's code object, one per GPU, held until the process
+ * ends.  MTP_ENOMEM (nothing launched) when mtp_q_workspace_size reports more
+ * than MTP_Q_NOALLOC_SCRATCH_BYTES for the sizes (about 10 M tokens for a
+ * 1025-token vocabulary).  Calls no allocating routine.  Every call on one
+ * GPU uses that GPU's one array: calls that overlap on a GPU (on different
+ * streams or threads without ordering between them) race and give wrong
+ * counts.  MTP_EHIP if the array's device address cannot be obtained. */
+#define MTP_Q_NOALLOC_SCRATCH_BYTES (64u << 20)
+int mtp_q_count_noalloc(const int32_t* tokens, int64_t n_tokens, const int64_t* offsets, int64_t n_seqs,
+                        int vocab, int eos_id, int flags, uint32_t* counts, uint64_t* status, void* hip_stream);
+
 /* log Q from the counts: logq[i][j] = float32(log(counts[i][j] + alpha) -
  * log(sum_j counts[i][j] + alpha * vocab)), evaluated in double (additive
  * smoothing alpha >= 0; alpha = 0 gives -inf for unseen pairs); a row whose

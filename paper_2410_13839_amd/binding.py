@@ -35,7 +35,7 @@ EXPORTED = ["mtp_query_sizes", "mtp_weight_offset", "mtp_create", "mtp_prefill",
             "mtp_get_tokens",
             "mtp_profile_replay", "mtp_reset", "mtp_destroy", "mtp_last_error", "mtp_strerror",
             "mtp_set_selection", "mtp_get_union_lattice", "mtp_set_sampling", "mtp_get_uniforms",
-            "mtp_q_workspace_size", "mtp_q_count", "mtp_q_normalize",
+            "mtp_q_workspace_size", "mtp_q_count", "mtp_q_count_noalloc", "mtp_q_normalize",
             "mtp_nar_prepare", "mtp_nar_run", "mtp_nar_get_codes", "mtp_nar_get_logits"]
 MTP_Q_COUNT_EOS = 1
 MTP_LATTICE_OWN, MTP_LATTICE_UNION = 0, 1
@@ -80,6 +80,9 @@ _lib.mtp_q_workspace_size.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_i
 _lib.mtp_q_count.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int,
                              ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                              ctypes.c_uint64, ctypes.c_void_p]
+_lib.mtp_q_count_noalloc.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int,
+                                     ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+MTP_Q_NOALLOC_SCRATCH_BYTES = 64 << 20
 _lib.mtp_q_normalize.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p]
 _lib.mtp_nar_prepare.argtypes = [_ctx, ctypes.c_int, _i32p, _i32p, _i32p, _i32p, _i32p, _i32p]
 _lib.mtp_nar_run.argtypes = [_ctx]
@@ -278,6 +281,15 @@ def mtp_q_count(tokens: int, n_tokens: int, offsets: int, n_seqs: int, vocab: in
                             vocab, eos_id, flags, ctypes.c_void_p(counts or None), ctypes.c_void_p(status or None),
                             ctypes.c_void_p(workspace or None), ws_bytes, ctypes.c_void_p(stream or None)),
            None, "mtp_q_count")
+
+
+def mtp_q_count_noalloc(tokens: int, n_tokens: int, offsets: int, n_seqs: int, vocab: int, eos_id: int, flags: int,
+                        counts: int, status: int, stream: int) -> None:
+    """mtp_q_count on the library's fixed scratch (no workspace); device pointers as integers."""
+    _check(_lib.mtp_q_count_noalloc(ctypes.c_void_p(tokens or None), n_tokens, ctypes.c_void_p(offsets or None),
+                                    n_seqs, vocab, eos_id, flags, ctypes.c_void_p(counts or None),
+                                    ctypes.c_void_p(status or None), ctypes.c_void_p(stream or None)),
+           None, "mtp_q_count_noalloc")
 
 
 def mtp_q_normalize(counts: int, vocab: int, alpha: float, logq: int, stream: int) -> None:

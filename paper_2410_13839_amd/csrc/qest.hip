@@ -26,6 +26,8 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "../../include/mtp.h"
 
 namespace mtp {
@@ -492,6 +494,71 @@ bool q_sizes_ok(int64_t n_tokens, int64_t n_seqs, int vocab) {
     return n_tokens >= 0 && n_tokens < (int64_t(1) << 31) && n_seqs >= 0 && vocab >= 1 && vocab <= 8192;
 }
 
+// Argument checks shared by both count entry points (the workspace aside).
+int q_count_check(const int32_t* tokens, int64_t n_tokens, const int64_t* offsets, int64_t n_seqs, int vocab,
+                  int eos_id, int flags, const uint32_t* counts, const uint64_t* status) {
+    if (!q_sizes_ok(n_tokens, n_seqs, vocab) || eos_id < 0 || eos_id >= vocab) return MTP_EINVAL;
+    if ((flags & ~MTP_Q_COUNT_EOS) != 0) return MTP_EINVAL;
+    if (!counts || !status || !offsets || (n_tokens > 0 && !tokens)) return MTP_EINVAL;
+    if (((uintptr_t)tokens & 15) != 0) return MTP_EINVAL;
+    return MTP_OK;
+}
+
+// Validation and the six launches of a count over a workspace of ws_bytes.
+int q_count_run(const int32_t* tokens, int64_t n_tokens, const int64_t* offsets, int64_t n_seqs, int vocab,
+                int eos_id, int flags, uint32_t* counts, uint64_t* status, void* workspace, uint64_t ws_bytes,
+                hipStream_t st) {
+    const int rc = q_count_check(tokens, n_tokens, offsets, n_seqs, vocab, eos_id, flags, counts, status);
+    if (rc != MTP_OK) return rc;
+    if (!workspace || ((uintptr_t)workspace & 255) != 0) return MTP_EINVAL;
+    const QPlan p = make_plan(n_tokens, n_seqs, vocab);
+    QWs w{};
+    if (carve(p, n_tokens, (char*)workspace, &w) > ws_bytes) return MTP_ENOMEM;
+    if (n_seqs == 0) return MTP_OK;
+    QArgs a{tokens, n_tokens, offsets, n_seqs, eos_id, (flags & MTP_Q_COUNT_EOS) ? 1 : 0, counts,
+            reinterpret_cast<unsigned long long*>(status), p, w};
+    hipLaunchKernelGGL(q_bucket_count_kernel, dim3(p.NWG), dim3(QB_THREADS), 0, st, a);
+    hipLaunchKernelGGL(q_column_scan_kernel, dim3(p.NB), dim3(QS_THREADS), 0, st, a);
+    hipLaunchKernelGGL(q_bucket_plan_kernel, dim3(1), dim3(QS_THREADS), 0, st, a);
+    hipLaunchKernelGGL(q_bucket_scatter_kernel, dim3(p.NWG), dim3(QB_THREADS), 0, st, a);
+    // 128 KB of dynamic LDS: raise the function's limit (per device, cheap)
+    if (hipFuncSetAttribute((const void*)q_slice_hist_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            QB_BIN * 4) != hipSuccess)
+        return MTP_EHIP;
+    hipLaunchKernelGGL(q_slice_hist_kernel, dim3((unsigned)p.max_slices), dim3(QH_THREADS), QB_BIN * 4, st, a);
+    const uint64_t nk = (uint64_t)vocab * vocab;
+    hipLaunchKernelGGL(q_reduce_kernel, dim3((unsigned)((nk + 255) / 256)), dim3(256), 0, st, a);
+    return hipGetLastError() == hipSuccess ? MTP_OK : MTP_EHIP;
+}
+
+}  // namespace
+}  // namespace mtp
+
+// Fixed scratch of mtp_q_count_noalloc (callers that cannot allocate): one
+// copy per device, part of the code object.  In host code `scratch` names a
+// host-side stand-in, not the device array: kernels receive the device
+// address that hipGetSymbolAddress returns, looked up once per device.
+static __device__ __align__(256) char scratch[MTP_Q_NOALLOC_SCRATCH_BYTES];
+
+namespace mtp {
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices] = {};
+
+// Device address of `scratch` on the current device.
+int noalloc_scratch(void** out) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return MTP_EHIP;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_dev[dev]) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return MTP_EHIP;
+        g_scratch_dev[dev] = p;
+    }
+    *out = g_scratch_dev[dev];
+    return MTP_OK;
+}
 }  // namespace
 }  // namespace mtp
 
@@ -506,30 +573,23 @@ int mtp_q_workspace_size(int64_t n_tokens, int64_t n_seqs, int vocab, uint64_t* 
 int mtp_q_count(const int32_t* tokens, int64_t n_tokens, const int64_t* offsets, int64_t n_seqs, int vocab,
                 int eos_id, int flags, uint32_t* counts, uint64_t* status, void* workspace, uint64_t ws_bytes,
                 void* hip_stream) {
+    return mtp::q_count_run(tokens, n_tokens, offsets, n_seqs, vocab, eos_id, flags, counts, status, workspace,
+                            ws_bytes, (hipStream_t)hip_stream);
+}
+
+int mtp_q_count_noalloc(const int32_t* tokens, int64_t n_tokens, const int64_t* offsets, int64_t n_seqs, int vocab,
+                        int eos_id, int flags, uint32_t* counts, uint64_t* status, void* hip_stream) {
     using namespace mtp;
-    if (!q_sizes_ok(n_tokens, n_seqs, vocab) || eos_id < 0 || eos_id >= vocab) return MTP_EINVAL;
-    if ((flags & ~MTP_Q_COUNT_EOS) != 0) return MTP_EINVAL;
-    if (!counts || !status || !offsets || !workspace || (n_tokens > 0 && !tokens)) return MTP_EINVAL;
-    if (((uintptr_t)tokens & 15) != 0 || ((uintptr_t)workspace & 255) != 0) return MTP_EINVAL;
-    const QPlan p = make_plan(n_tokens, n_seqs, vocab);
-    QWs w{};
-    if (carve(p, n_tokens, (char*)workspace, &w) > ws_bytes) return MTP_ENOMEM;
-    if (n_seqs == 0) return MTP_OK;
-    QArgs a{tokens, n_tokens, offsets, n_seqs, eos_id, (flags & MTP_Q_COUNT_EOS) ? 1 : 0, counts,
-            reinterpret_cast<unsigned long long*>(status), p, w};
-    hipStream_t st = (hipStream_t)hip_stream;
-    hipLaunchKernelGGL(q_bucket_count_kernel, dim3(p.NWG), dim3(QB_THREADS), 0, st, a);
-    hipLaunchKernelGGL(q_column_scan_kernel, dim3(p.NB), dim3(QS_THREADS), 0, st, a);
-    hipLaunchKernelGGL(q_bucket_plan_kernel, dim3(1), dim3(QS_THREADS), 0, st, a);
-    hipLaunchKernelGGL(q_bucket_scatter_kernel, dim3(p.NWG), dim3(QB_THREADS), 0, st, a);
-    // 128 KB of dynamic LDS: raise the function's limit (per device, cheap)
-    if (hipFuncSetAttribute((const void*)q_slice_hist_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
-                            QB_BIN * 4) != hipSuccess)
-        return MTP_EHIP;
-    hipLaunchKernelGGL(q_slice_hist_kernel, dim3((unsigned)p.max_slices), dim3(QH_THREADS), QB_BIN * 4, st, a);
-    const uint64_t nk = (uint64_t)vocab * vocab;
-    hipLaunchKernelGGL(q_reduce_kernel, dim3((unsigned)((nk + 255) / 256)), dim3(256), 0, st, a);
-    return hipGetLastError() == hipSuccess ? MTP_OK : MTP_EHIP;
+    // the same checks as mtp_q_count, then the size limit of the fixed scratch
+    const int rc = q_count_check(tokens, n_tokens, offsets, n_seqs, vocab, eos_id, flags, counts, status);
+    if (rc != MTP_OK) return rc;
+    const uint64_t need = carve(make_plan(n_tokens, n_seqs, vocab), n_tokens, nullptr, nullptr);
+    if (need > (uint64_t)MTP_Q_NOALLOC_SCRATCH_BYTES) return MTP_ENOMEM;
+    void* ws = nullptr;
+    const int rs = noalloc_scratch(&ws);
+    if (rs != MTP_OK) return rs;
+    return q_count_run(tokens, n_tokens, offsets, n_seqs, vocab, eos_id, flags, counts, status, ws,
+                       (uint64_t)MTP_Q_NOALLOC_SCRATCH_BYTES, (hipStream_t)hip_stream);
 }
 
 int mtp_q_normalize(const uint32_t* counts, int vocab, float alpha, float* logq, void* hip_stream) {

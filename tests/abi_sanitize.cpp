@@ -196,6 +196,9 @@ int main() {
         CHECK(mtp_q_count(tk + 1, 100, of, 2, 1025, 1024, 0, counts, status, fake(10), 1 << 20, nullptr) == MTP_EINVAL);
         CHECK(mtp_q_count(tk, 100, of, 2, 1025, 1024, 0, counts, status, nullptr, 1 << 20, nullptr) == MTP_EINVAL);
         CHECK(mtp_q_count(tk, 100, of, 2, 1025, 1024, 0, counts, status, fake(10), 1024, nullptr) == MTP_ENOMEM);
+        CHECK(mtp_q_count_noalloc(tk, (int64_t)12 << 20, of, 40000, 1025, 1024, 0, counts, status, nullptr) ==
+              MTP_ENOMEM);
+        CHECK(mtp_q_count_noalloc(nullptr, 100, of, 2, 1025, 1024, 0, counts, status, nullptr) == MTP_EINVAL);
         CHECK(mtp_q_normalize(counts, 1025, -1.f, static_cast<float*>(fake(11)), nullptr) == MTP_EINVAL);
         CHECK(mtp_q_normalize(counts, 0, 1.f, static_cast<float*>(fake(11)), nullptr) == MTP_EINVAL);
     }
