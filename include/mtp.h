@@ -304,6 +304,7 @@ int mtp_get_tokens(mtp_ctx* ctx, int32_t* tokens);
 #define MTP_KCLASS_HEADS       5   /* final LN -> K head projections          */
 #define MTP_KCLASS_GEMM_OPROJ  6   /* attention out x W_o^T (residual part.)  */
 #define MTP_KCLASS_SELECT      7   /* top_k, Viterbi lattice and accept       */
+#define MTP_KCLASS_RESID_LN    8   /* residual + LayerNorm rows (batched path, two per layer) */
 int mtp_profile_replay(mtp_ctx* ctx, int kclass, int iters, void* flush_buf, uint64_t flush_bytes,
                        double* avg_us);
 

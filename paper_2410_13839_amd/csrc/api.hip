@@ -231,7 +231,7 @@ struct mtp_ctx {
     // every launch of each kernel class in the step of a key (arguments
     // captured by value), for replay timing
     using Launch = std::function<hipError_t(hipStream_t)>;
-    struct StepLaunches { std::vector<Launch> cls[8]; };
+    struct StepLaunches { std::vector<Launch> cls[MTP_KCLASS_RESID_LN + 1]; };
     std::map<StepKey, StepLaunches> step_launches;
     StepLaunches* recording = nullptr;
     StepKey last_key{};
@@ -283,7 +283,7 @@ int pick_splits(const mtp_ctx* c, int M, int N, int K) {
 // Launch through `f` and, while a step is being recorded, keep it under class `kclass`.
 hipError_t launch_rec(mtp_ctx* c, int kclass, std::function<hipError_t(hipStream_t)> f) {
     hipError_t e = f(c->stream);
-    if (kclass > 0 && kclass < 8 && c->recording) c->recording->cls[kclass].push_back(std::move(f));
+    if (kclass > 0 && kclass <= MTP_KCLASS_RESID_LN && c->recording) c->recording->cls[kclass].push_back(std::move(f));
     return e;
 }
 
@@ -413,13 +413,15 @@ int run_layer(mtp_ctx* c, int l, int rows, int n_tiles, int qt, int split_len, i
     g.dtype = dt; g.epi = EPI_PARTIAL; g.X = c->WS() + c->ws.attn; g.ldx = d; g.M = rows; g.xpk = pk;
     g.W = c->lt(l, MTP_T_W_O); g.N = d; g.K = d; g.splits = pick_splits(c, rows, d, d);
     g.out = c->WS() + c->ws.part; g.ldo = d; g.split_stride = sstride;
-    HIPCHK(c, gemm(st, g), "out-proj gemm");
+    HIPCHK(c, launch_rec(c, decode ? MTP_KCLASS_GEMM_OPROJ : 0, [g](hipStream_t s) { return gemm(s, g); }),
+           "out-proj gemm");
     ResidArgs r{};
     r.dtype = dt; r.n_rows = rows; r.d = d; r.h = c->ws_ptr<float>(c->ws.h); r.part = c->ws_ptr<float>(c->ws.part);
     r.n_split = g.splits; r.split_stride = sstride; r.bias = (const float*)c->lt(l, MTP_T_B_O);
     r.ln_g = (const float*)c->lt(l, MTP_T_LN2_G); r.ln_b = (const float*)c->lt(l, MTP_T_LN2_B); r.u = c->WS() + c->ws.u;
     r.packed = pk;
-    HIPCHK(c, resid_ln(st, r), "resid+ln2");
+    HIPCHK(c, launch_rec(c, decode ? MTP_KCLASS_RESID_LN : 0, [r](hipStream_t s) { return resid_ln(s, r); }),
+           "resid+ln2");
     // FFN1 + GELU
     g = GemmArgs{};
     g.dtype = dt; g.epi = EPI_GELU; g.X = c->WS() + c->ws.u; g.ldx = d; g.M = rows; g.xpk = pk; g.opk = pk;
@@ -440,7 +442,8 @@ int run_layer(mtp_ctx* c, int l, int rows, int n_tiles, int qt, int split_len, i
         r.u = c->WS() + c->ws.u;
     }
     r.packed = pk;
-    HIPCHK(c, resid_ln(st, r), "resid+ln1");
+    HIPCHK(c, launch_rec(c, decode ? MTP_KCLASS_RESID_LN : 0, [r](hipStream_t s) { return resid_ln(s, r); }),
+           "resid+ln1");
     (void)ab;
     return MTP_OK;
 }
@@ -1127,7 +1130,7 @@ int mtp_profile_replay(mtp_ctx* c, int kclass, int iters, void* flush_buf, uint6
         return MTP_EINVAL;
     }
     const bool cold = flush_buf != nullptr;
-    if (kclass < MTP_KCLASS_GEMM_FFN1 || kclass > MTP_KCLASS_SELECT) { c->err = "unknown kernel class"; return MTP_EINVAL; }
+    if (kclass < MTP_KCLASS_GEMM_FFN1 || kclass > MTP_KCLASS_RESID_LN) { c->err = "unknown kernel class"; return MTP_EINVAL; }
     auto it = c->has_last ? c->step_launches.find(c->last_key) : c->step_launches.end();
     if (it == c->step_launches.end() || it->second.cls[kclass].empty()) {
         c->err = "the last decode step launched nothing of this kernel class";

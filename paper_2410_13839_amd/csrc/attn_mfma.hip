@@ -45,32 +45,43 @@ template <int NW, int PD>
 __global__ __launch_bounds__(64 * NW) void attn_dec_kernel(AttnMfmaArgs p) {
     const int b = blockIdx.x, head = blockIdx.y, split = blockIdx.z;
     const int H = gridDim.y;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int r = lane & 15, g = lane >> 4;
     extern __shared__ float s_o[];               // [NW waves][64 dims][17]
     __shared__ float s_m[NW][16], s_l[NW][16];
     constexpr int CH = 16 * NW;                  // keys per chunk
     const bf16_t* pool = reinterpret_cast<const bf16_t*>(p.kv.pool);
-    const int P = p.kv.page_size;
-    const int max_key = p.kv.max_pages_per_seq * P - 1;
     const int kb = split * p.split_len;
     const int row0 = b * p.Q;
 
+    // Key groups start at multiples of 16 (splits and chunks are multiples of
+    // 16 keys), so each wave's 16-key group is exactly one cache page; group i
+    // of this wave is page (kb / 16) + wave + NW i of the sequence.  Lane j
+    // holds the page number of group j (64 groups at a time, reloaded every
+    // 64): a group's addresses then come from a register read, not from a
+    // page-table load that, completing in order with the vector loads before
+    // it, would hold each group's K / V loads behind the previous group's.
+    // Page indexes are clamped to the sequence's block table, whose unused
+    // entries name page 0, so loads past the context stay in the pool.
+    const int maxp = p.kv.max_pages_per_seq;
+    const int32_t* btab = p.kv.block_table + (size_t)b * maxp;
+    const int pg0 = (kb >> 4) + wave;
+    int pages = btab[min(pg0 + NW * lane, maxp - 1)];
     uint4 kf[PD][2];
     uint2 vf[PD][4];
-    // every address is clamped to the sequence's block table, whose unused
-    // entries name page 0, so loads past the context stay in the pool
-    auto load_keys = [&](int u, int c0) {
-        const int wk = c0 + 16 * wave;
-        const bf16_t* kp = pool + p.kv.offset(b, min(wk + r, max_key), 0, head) + g * 8;
+    auto load_keys = [&](int u, int gi) {        // gi: this wave's group index (uniform)
+        if ((gi & 63) == 0 && gi > 0) pages = btab[min(pg0 + NW * (gi + lane), maxp - 1)];
+        const int page = __builtin_amdgcn_readlane(pages, gi & 63);
+        const bf16_t* kp = pool + kv_page_block(p.kv, page, 0, head) + r * MTP_HEAD_DIM + g * 8;
         kf[u][0] = *reinterpret_cast<const uint4*>(kp);
         kf[u][1] = *reinterpret_cast<const uint4*>(kp + 32);
-        const bf16_t* vp = pool + p.kv.vt_offset(b, min(wk + 4 * g, max_key & ~3), head);
+        const bf16_t* vp = pool + kv_page_block(p.kv, page, 1, head) + 4 * g;
 #pragma unroll
-        for (int dt = 0; dt < 4; ++dt) vf[u][dt] = *reinterpret_cast<const uint2*>(vp + (size_t)(16 * dt + r) * P);
+        for (int dt = 0; dt < 4; ++dt) vf[u][dt] = *reinterpret_cast<const uint2*>(vp + (16 * dt + r) * 16);
     };
 #pragma unroll
-    for (int u = 0; u < PD; ++u) load_keys(u, kb + u * CH);
+    for (int u = 0; u < PD; ++u) load_keys(u, u);
     float4 qa[2], qb[2];
     {
         const float* qp = p.q + (size_t)(row0 + min(r, p.Q - 1)) * p.ldq + head * 64 + g * 8;
@@ -107,7 +118,7 @@ __global__ __launch_bounds__(64 * NW) void attn_dec_kernel(AttnMfmaArgs p) {
         uint2 v[4];
 #pragma unroll
         for (int dt = 0; dt < 4; ++dt) v[dt] = vf[u][dt];
-        if (c0 + PD * CH < ke) load_keys(u, c0 + PD * CH);   // refill this ring slot (uniform branch)
+        if (c0 + PD * CH < ke) load_keys(u, (c0 - kb) / CH + PD);   // refill this ring slot (uniform branch)
         const int wk = c0 + 16 * wave;
         f32x4_t s = f32x4_t{0.f, 0.f, 0.f, 0.f};
         s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, k0), qf[0], s, 0, 0, 0);
@@ -430,7 +441,7 @@ hipError_t attention_mfma(hipStream_t st, const AttnMfmaArgs& a) {
     if (a.split_len < 32 || a.n_splits < 1 || a.n_splits > 64 || a.kv.page_size != 16) return hipErrorInvalidValue;
     if (a.mode == 0) {
         // decode: pending chunk of at most 16 rows per sequence
-        if (a.Q < 1 || a.Q > 16 || a.qt < a.Q) return hipErrorInvalidValue;
+        if (a.Q < 1 || a.Q > 16 || a.qt < a.Q || a.split_len % 16) return hipErrorInvalidValue;
         // waves per workgroup: at most one per 16-key group of a split, and
         // few enough that the whole grid is resident at once (16 waves per CU
         // at this kernel's register count)
