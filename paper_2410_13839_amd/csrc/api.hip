@@ -407,6 +407,38 @@ int run_layer(mtp_ctx* c, int l, int rows, int n_tiles, int qt, int split_len, i
         a.bidir = bidir ? 1 : 0; a.st = c->ws_ptr<SeqState>(c->ws.state);
         HIPCHK(c, attention(st, a), "attention");
     }
+    // Prefill / NAR rows on the large-M kernel: the out-projection and FFN2
+    // add their product and bias into the residual stream in their epilogue
+    // (no K split: the split partials and the separate residual pass would
+    // move three times the bytes), then a LayerNorm pass writes the next
+    // product's rows.
+    if (!decode && pk && gemm_resid_in_place(rows, d)) {
+        float* h = c->ws_ptr<float>(c->ws.h);
+        g = GemmArgs{};
+        g.dtype = dt; g.epi = EPI_RESID; g.X = c->WS() + c->ws.attn; g.ldx = d; g.M = rows; g.xpk = pk;
+        g.W = c->lt(l, MTP_T_W_O); g.N = d; g.K = d; g.splits = 1;
+        g.bias = (const float*)c->lt(l, MTP_T_B_O); g.out = h; g.ldo = d;
+        HIPCHK(c, gemm(st, g), "out-proj gemm");
+        RowsLnArgs ln{};
+        ln.dtype = dt; ln.n_rows = rows; ln.d = d; ln.h = h; ln.packed = pk; ln.u = c->WS() + c->ws.u;
+        ln.ln_g = (const float*)c->lt(l, MTP_T_LN2_G); ln.ln_b = (const float*)c->lt(l, MTP_T_LN2_B);
+        HIPCHK(c, rows_ln(st, ln), "ln2");
+        g = GemmArgs{};
+        g.dtype = dt; g.epi = EPI_GELU; g.X = c->WS() + c->ws.u; g.ldx = d; g.M = rows; g.xpk = pk; g.opk = pk;
+        g.W = c->lt(l, MTP_T_W_1); g.N = F; g.K = d; g.splits = 1;
+        g.bias = (const float*)c->lt(l, MTP_T_B_1); g.out = c->WS() + c->ws.ffn; g.ldo = F;
+        HIPCHK(c, gemm(st, g), "ffn1 gemm");
+        g = GemmArgs{};
+        g.dtype = dt; g.epi = EPI_RESID; g.X = c->WS() + c->ws.ffn; g.ldx = F; g.M = rows; g.xpk = pk;
+        g.W = c->lt(l, MTP_T_W_2); g.N = d; g.K = F; g.splits = 1;
+        g.bias = (const float*)c->lt(l, MTP_T_B_2); g.out = h; g.ldo = d;
+        HIPCHK(c, gemm(st, g), "ffn2 gemm");
+        if (l + 1 < cf.n_layers) {
+            ln.ln_g = (const float*)c->lt(l + 1, MTP_T_LN1_G); ln.ln_b = (const float*)c->lt(l + 1, MTP_T_LN1_B);
+            HIPCHK(c, rows_ln(st, ln), "ln1");
+        }
+        return MTP_OK;
+    }
     // out projection -> partials, residual + LN2
     const size_t sstride = (size_t)rows * d;
     g = GemmArgs{};

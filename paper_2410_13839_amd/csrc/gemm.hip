@@ -15,6 +15,7 @@
 //  * gemm_big_bf16: M > 256 (prefill, NAR).  256 x 256 tiles on MFMA with
 //    both operands streamed global -> LDS in fragment order.
 //  * gemm_f32: the fp32 model; LDS-tiled VALU FMA.
+#include <algorithm>
 #include <type_traits>
 
 #include "common.h"
@@ -92,6 +93,21 @@ struct EpiPartial {
     __device__ __forceinline__ void store4(int m, int n, const float (&v)[4], int split, int) const {
         *reinterpret_cast<float4*>(part + split * split_stride + (size_t)m * ldo + n) =
             make_float4(v[0], v[1], v[2], v[3]);
+    }
+};
+
+// h[m][n..n+3] += product + bias: the residual stream updated in place by a
+// projection with no K split (every (m, n) belongs to one workgroup, so the
+// read-modify-write is race free); the same association as resid_ln_kernel.
+struct EpiResid {
+    float* h;             // [M][ldh]
+    const float* bias;    // [N]
+    int ldh;
+    __device__ __forceinline__ void store4(int m, int n, const float (&v)[4], int, int) const {
+        const float4 bv = *reinterpret_cast<const float4*>(bias + n);
+        float4* p = reinterpret_cast<float4*>(h + (size_t)m * ldh + n);
+        const float4 x = *p;
+        *p = make_float4(x.x + (v[0] + bv.x), x.y + (v[1] + bv.y), x.z + (v[2] + bv.z), x.w + (v[3] + bv.w));
     }
 };
 
@@ -287,15 +303,17 @@ __global__ __launch_bounds__(64 * NWV) void gemm_big_bf16(const bf16_t* __restri
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int wm = wave / WGN, wn = wave - wm * WGN;
-    // tile of this workgroup: XCD x (= bid % 8) takes the x-th eighth of the
-    // tiles in row-band order (n fastest)
+    // tiles of this workgroup: XCD x (= bid % 8) takes the x-th eighth of the
+    // tiles in row-band order (n fastest), and its workgroups take them in
+    // turn (workgroup j of the XCD: tiles j, j + wgx, ...), so the ones in
+    // flight on an XCD are neighbours in a row band
     const int ntile = tiles_m * tiles_n;
     const int bid = blockIdx.x;
     const int per = (ntile + 7) >> 3;
-    const int t = (bid & 7) * per + (bid >> 3);
-    if (t >= ntile) return;                     // uniform: whole workgroup
-    const int tm = t / tiles_n, tn = t - tm * tiles_n;
-    const int mfr0 = tm * FM, nfr0 = tn * FN;   // first 16-row fragment of each operand
+    const int wgx = gridDim.x >> 3;             // workgroups per XCD
+    const int t_end = min(((bid & 7) + 1) * per, ntile);
+    int t = (bid & 7) * per + (bid >> 3);
+    if (t >= t_end) return;                     // uniform: whole workgroup
     const int mfr_last = ((M + 15) >> 4) - 1, nfr_last = ((N + 15) >> 4) - 1;
     const int split = blockIdx.y;
     const int ks0 = (split * k_per_split) >> 5; // first 32-k step
@@ -304,15 +322,22 @@ __global__ __launch_bounds__(64 * NWV) void gemm_big_bf16(const bf16_t* __restri
 
     // fragment f of a stage: f < FM is activation rows 16 f.., else weight
     // rows 16 (f - FM)..; wave w issues f = w, w + NWV, ...
+    int mfr0 = 0, nfr0 = 0;                     // first 16-row fragment of each operand
     const bf16_t* src[NL];
+    auto set_tile = [&](int tt) {
+        const int tm = tt / tiles_n, tn = tt - tm * tiles_n;
+        mfr0 = tm * FM;
+        nfr0 = tn * FN;
 #pragma unroll
-    for (int i = 0; i < NL; ++i) {
-        const int f = wave + NWV * i;
-        const bf16_t* base;
-        if (f < FM) base = X + (size_t)min(mfr0 + f, mfr_last) * K32 * 512;
-        else base = W + (size_t)min(nfr0 + f - FM, nfr_last) * K32 * 512;
-        src[i] = base + (size_t)ks0 * 512 + lane * 8;
-    }
+        for (int i = 0; i < NL; ++i) {
+            const int f = wave + NWV * i;
+            const bf16_t* base;
+            if (f < FM) base = X + (size_t)min(mfr0 + f, mfr_last) * K32 * 512;
+            else base = W + (size_t)min(nfr0 + f - FM, nfr_last) * K32 * 512;
+            src[i] = base + (size_t)ks0 * 512 + lane * 8;
+        }
+    };
+    set_tile(t);
     auto issue = [&](bf16_t* buf, int st) {
 #pragma unroll
         for (int i = 0; i < NL; ++i)
@@ -395,43 +420,62 @@ __global__ __launch_bounds__(64 * NWV) void gemm_big_bf16(const bf16_t* __restri
     if (0 < nst) issue(s0, 0);
     if (1 < nst) issue(s1, 1);
     if (2 < nst) issue(s2, 2);
-    // step st: wait for stage st (the NS-2 later stages may stay in flight),
-    // barrier (stage st visible to all waves, and every wave is done with the
-    // buffer stage st + NS - 1 refills), refill, consume
-#define GB_STEP(BUF, NEXT, U)                                                          \
-    {                                                                                  \
-        const int st = st0 + (U);                                                      \
-        if (st < nst) {                                                                \
-            if (st + 2 < nst) __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * NL));           \
-            else if (st + 1 < nst) __builtin_amdgcn_s_waitcnt(vmcnt_imm(NL));          \
-            else __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));                             \
-            gb_barrier();                                                              \
-            if (st + GB_NS - 1 < nst) issue(NEXT, st + GB_NS - 1);                     \
-            compute(BUF);                                                              \
-        }                                                                              \
-    }
-    for (int st0 = 0; st0 < nst; st0 += GB_NS) {
-        GB_STEP(s0, s3, 0)
-        GB_STEP(s1, s0, 1)
-        GB_STEP(s2, s1, 2)
-        GB_STEP(s3, s2, 3)
-    }
-#undef GB_STEP
-
-    // epilogue: lane (r, g) of tile (i, j) holds outputs n = 4 g .. 4 g + 3
-    // of weight fragment i, row m = r of activation fragment j
     const int r = lane & 15, g = lane >> 4;
-#pragma unroll
-    for (int i = 0; i < WFN; ++i)
-#pragma unroll
-        for (int j = 0; j < WFM; ++j) {
-            const int n = (nfr0 + wn * WFN + i) * 16 + 4 * g;
-            const int m = (mfr0 + wm * WFM + j) * 16 + r;
-            if (m < M && n < N) {
-                float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
-                epi.store4(m, n, v, split, min(4, N - n));
-            }
+    for (bool later = false;; later = true) {
+        // step st: wait for stage st (the NS-2 later stages may stay in
+        // flight; on a later tile the first step waits for everything, the
+        // previous tile's output stores included), barrier (stage st visible
+        // to all waves, and every wave is done with the buffer stage st +
+        // NS - 1 refills), refill, consume
+#define GB_STEP(BUF, NEXT, U)                                                          \
+        {                                                                              \
+            const int st = st0 + (U);                                                  \
+            if (st < nst) {                                                            \
+                if (later && st == 0) __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));        \
+                else if (st + 2 < nst) __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * NL));  \
+                else if (st + 1 < nst) __builtin_amdgcn_s_waitcnt(vmcnt_imm(NL));      \
+                else __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));                         \
+                gb_barrier();                                                          \
+                if (st + GB_NS - 1 < nst) issue(NEXT, st + GB_NS - 1);                 \
+                compute(BUF);                                                          \
+            }                                                                          \
         }
+        for (int st0 = 0; st0 < nst; st0 += GB_NS) {
+            GB_STEP(s0, s3, 0)
+            GB_STEP(s1, s0, 1)
+            GB_STEP(s2, s1, 2)
+            GB_STEP(s3, s2, 3)
+        }
+#undef GB_STEP
+        // the next tile's first stages go out before this tile's outputs are
+        // stored, once every wave is done reading the stage buffers
+        const int em0 = mfr0, en0 = nfr0;
+        const int t_next = t + wgx;
+        const bool more = t_next < t_end;      // uniform
+        if (more) {
+            gb_barrier();
+            set_tile(t_next);
+            if (0 < nst) issue(s0, 0);
+            if (1 < nst) issue(s1, 1);
+            if (2 < nst) issue(s2, 2);
+        }
+        // epilogue: lane (r, g) of tile (i, j) holds outputs n = 4 g .. 4 g + 3
+        // of weight fragment i, row m = r of activation fragment j
+#pragma unroll
+        for (int i = 0; i < WFN; ++i)
+#pragma unroll
+            for (int j = 0; j < WFM; ++j) {
+                const int n = (en0 + wn * WFN + i) * 16 + 4 * g;
+                const int m = (em0 + wm * WFM + j) * 16 + r;
+                if (m < M && n < N) {
+                    float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+                    epi.store4(m, n, v, split, min(4, N - n));
+                }
+                acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+            }
+        if (!more) break;
+        t = t_next;
+    }
 }
 
 template <int BM, int BN, int NWV, class Epi>
@@ -441,9 +485,22 @@ static hipError_t launch_big(hipStream_t st, const bf16_t* X, int M, const bf16_
     if (kps % 32) return hipErrorInvalidValue;
     const int tm = (M + BM - 1) / BM, tn = (N + BN - 1) / BN;
     const int ntile = tm * tn;
-    // the tile numbering deals eighths of the tiles to the XCDs: the grid is
-    // 8 x ceil(tiles / 8) workgroups, the surplus ones return at once
-    dim3 grid(8 * ((ntile + 7) / 8), splits);
+    // the tile numbering deals eighths of the tiles to the XCDs; each XCD
+    // gets at most as many workgroups as it holds at once (its CUs times the
+    // workgroups per CU the LDS stages allow), and those take its tiles in
+    // turn, so a workgroup's next tile streams in while it stores the last
+    static int n_cu = 0;
+    if (n_cu == 0) {
+        int dev = 0, v = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v < 8)
+            v = 256;
+        n_cu = v;
+    }
+    constexpr int lds_kb = GB_NS * (BM / 16 + BN / 16);   // 1 KB per fragment per stage
+    const int per_cu = lds_kb <= 80 ? 2 : 1;               // 160 KB of LDS per CU
+    const int per_xcd = std::min((ntile + 7) / 8, std::max(1, n_cu / 8) * per_cu);
+    dim3 grid(8 * per_xcd, splits);
     hipLaunchKernelGGL((gemm_big_bf16<BM, BN, NWV, Epi>), grid, dim3(64 * NWV), 0, st, X, M, W, N, K, kps, tm, tn, epi);
     return hipGetLastError();
 }
@@ -539,6 +596,13 @@ int gemm_split_granule(int dtype, int M) {
     return 32;   // one k step of the bf16 kernels, one LDS tile of the fp32 one
 }
 
+// Whether an M x N bf16 product takes the large-M kernel (the prefill and
+// NAR trunk), where a residual projection updates the residual stream in its
+// epilogue (EPI_RESID) instead of writing split-K partial sums.
+int gemm_resid_in_place(int M, int N) {
+    return M > 256 && big_tile(M, N, false).bm != 0;
+}
+
 // Workgroups of one split-K-able (partial-sum) bf16 launch for M rows and N
 // columns before K splitting.
 int gemm_tiles(int M, int N) {
@@ -572,6 +636,12 @@ hipError_t gemm(hipStream_t st, const GemmArgs& a) {
         EpiPartial e{(float*)a.out, a.ldo, a.split_stride};
         if (bf) return launch_bf16(st, (const bf16_t*)a.X, a.ldx, a.M, (const bf16_t*)a.W, a.N, a.K, a.splits, a.xpk, e);
         return launch_f32(st, (const float*)a.X, a.ldx, a.M, (const float*)a.W, a.N, a.K, a.splits, e);
+    }
+    case EPI_RESID: {
+        // large-M bf16 products only, no K split
+        if (!bf || a.splits != 1 || !gemm_resid_in_place(a.M, a.N) || a.N % 4) return hipErrorInvalidValue;
+        EpiResid e{(float*)a.out, a.bias, a.ldo};
+        return launch_bf16(st, (const bf16_t*)a.X, a.ldx, a.M, (const bf16_t*)a.W, a.N, a.K, 1, a.xpk, e);
     }
     case EPI_LOGITS: {
         EpiLogits e{(float*)a.out, a.bias, a.ldo};

@@ -20,13 +20,14 @@ struct GemmArgs {
     int opk;              // EPI_GELU: bf16 output in fragment order
     // epilogue operands
     const float* bias;
-    void* out; int ldo; size_t split_stride;
+    void* out; int ldo; size_t split_stride;   // EPI_RESID: out = the fp32 residual stream
     float* q; const RowInfo* rows; KVView kv; int d;
 };
 
 hipError_t gemm(hipStream_t st, const GemmArgs& a);
 int gemm_split_granule(int dtype, int M);
 int gemm_tiles(int M, int N);
+int gemm_resid_in_place(int M, int N);
 
 struct AttnArgs {
     int dtype;                 // KV / output element type: 0 fp32, 1 bf16
