@@ -197,8 +197,9 @@ __global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
     constexpr int CPRM = 64 * KCH;
     constexpr int GS = (T / (MR * CPRM)) > 0 ? (T / (MR * CPRM)) : 1;
     constexpr int SPT = (MAXS + GS - 1) / GS;                          // splits per thread
-    constexpr int MLP = (MR * 4 * KCH * MAXS + T - 1) / T;             // (max, sum) words per thread
-    __shared__ float2 s_ml[XM == 4 ? MR * 4 * KCH * MAXS : 1];
+    // each thread merges its own splits (group max, sum and weighted output)
+    // and the GS groups combine through LDS once
+    __shared__ float2 s_ml[XM == 4 ? T : 1];
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int r = lane & 15, g = lane >> 4;
@@ -229,11 +230,15 @@ __global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
     xq_t xq;
     int st_pl[XM == 3 ? RPT : 1];
     int2 sti = make_int2(0, 0);                  // XM 4: (ctx_len, pend_len) of the item's sequence
-    float2 mlv[XM == 4 ? MLP : 1];               // XM 4: (running max, sum) words
+    float2 mlv[XM == 4 ? SPT : 1];               // XM 4: (running max, sum) words of the thread's splits
     float4 ov[XM == 4 ? SPT : 1];                // XM 4: unnormalised outputs of the thread's splits
 #pragma unroll
-    for (int j = 0; j < (XM == 4 ? SPT : 1); ++j) ov[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int j = 0; j < (XM == 4 ? SPT : 1); ++j) {
+        ov[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+        mlv[j] = make_float2(-INFINITY, 0.f);
+    }
     (void)pv; (void)zv; (void)xq; (void)st_pl; (void)sti; (void)mlv; (void)ov; (void)gv; (void)bv; (void)hv;
+    (void)s_ml;
     const bool has_part = a.part_on != 0;      // kernel argument: uniform
     if constexpr (XM == 0) {
         // rows [0, M) x columns [kb, kb + ks) as 16-byte chunks
@@ -250,35 +255,29 @@ __global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
             xq[4 * i + 3] = t.w;
         }
     } else if constexpr (XM == 4) {
-        // the (max, sum) word of every (row, head, split) of this K range, and
-        // the thread's item (row, float4 chunk) in each of its splits; splits
-        // past the launched ones are clamped, the ones past the sequence's
-        // context are discarded once its state is known
-        const int cpr = ks >> 2, items = M * cpr, HW = ks >> 6, h0 = kb >> 6;
+        // the thread's item (row, float4 chunk) in each of its splits
+        // (sg, sg + GS, ...): the split's (max, sum) word of that row and
+        // head and the item's unnormalised outputs; splits past the context
+        // are discarded once the sequence's state is known
+        const int cpr = ks >> 2, items = M * cpr;
         const int H = K >> 6, S = a.n_splits;
         const uint32_t sstride = (uint32_t)a.qt * 68;   // offsets fit 32 bits (< B*H*S*qt*68)
-        const int nml = M * HW * S;
-#pragma unroll
-        for (int p = 0; p < MLP; ++p) {
-            const int idx = min(tid + T * p, nml - 1);
-            const int m = udiv_small(idx, HW * S), rem = idx - m * (HW * S);
-            const int hd = udiv_small(rem, S), sp = rem - hd * S;
-            const int seq = udiv_small(m, a.Q), i = m - seq * a.Q;
-            const uint32_t off = ((uint32_t)(seq * H + h0 + hd) * S + sp) * sstride + (uint32_t)i * 68;
-            mlv[p] = *reinterpret_cast<const float2*>(a.apart + off);
-        }
         const int TG = T / GS, sg = __builtin_amdgcn_readfirstlane(wave) / (TG >> 6);
         const int it = min(tid - sg * TG, items - 1);
         const int m = udiv_small(it, cpr), c = kb + (it - m * cpr) * 4;
         const int seq = udiv_small(m, a.Q), i = m - seq * a.Q;
         sti = *reinterpret_cast<const int2*>(&a.st[seq]);
-        const float* e0 = a.apart + ((uint32_t)(seq * H + (c >> 6)) * S * sstride + (uint32_t)i * 68 + 4 + (c & 63));
+        const float* e0 = a.apart + ((uint32_t)(seq * H + (c >> 6)) * S * sstride + (uint32_t)i * 68);
         // sg is uniform over a wave (groups are 256 threads or more) and S is
         // a kernel argument: skipping the splits that were not launched costs
         // no wait
 #pragma unroll
         for (int j = 0; j < SPT; ++j)
-            if (sg + GS * j < S) ov[j] = *reinterpret_cast<const float4*>(e0 + (uint32_t)(sg + GS * j) * sstride);
+            if (sg + GS * j < S) {
+                const float* e = e0 + (uint32_t)(sg + GS * j) * sstride;
+                mlv[j] = *reinterpret_cast<const float2*>(e);
+                ov[j] = *reinterpret_cast<const float4*>(e + 4 + (c & 63));
+            }
     } else {
         // LayerNorm gain and shift: loaded by row group 0 only, shared through LDS
         if (rg == 0) {
@@ -347,52 +346,56 @@ __global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
             }
         }
     } else if constexpr (XM == 4) {
-        const int cpr = ks >> 2, items = M * cpr, HW = ks >> 6;
+        const int cpr = ks >> 2, items = M * cpr;
         const int S = a.n_splits;
-        const int nml = M * HW * S;
-#pragma unroll
-        for (int p = 0; p < MLP; ++p) {
-            const int idx = tid + T * p;
-            if (idx < nml) s_ml[idx] = mlv[p];
-        }
-        __syncthreads();
         const int TG = T / GS, sg = __builtin_amdgcn_readfirstlane(wave) / (TG >> 6), it = tid - sg * TG;
         const int m = udiv_small(min(it, items - 1), cpr);
         const int c = kb + (min(it, items - 1) - m * cpr) * 4;
         const int i = m - udiv_small(m, a.Q) * a.Q;
         const int ctx = sti.x, pl = sti.y;
         const int n_active = min(S, udiv_small(ctx + pl + a.split_len - 1, a.split_len));
-        const float2* ml = s_ml + (m * HW + ((c - kb) >> 6)) * S;
-        // splits past the context (or a key range fully masked for this row)
-        // contribute nothing; their words may be stale
+        // this thread's splits: splits past the context (or a key range fully
+        // masked for this row) contribute nothing; their words may be stale
+        bool live[SPT];
         float mx = -INFINITY;
-        for (int sp = 0; sp < n_active; ++sp) mx = fmaxf(mx, ml[sp].x);
-        float L = 0.f;
-        for (int sp = 0; sp < n_active; ++sp) {
-            const float2 v = ml[sp];
-            if (v.x != -INFINITY) L += __expf(v.x - mx) * v.y;
+#pragma unroll
+        for (int j = 0; j < SPT; ++j) {
+            live[j] = sg + GS * j < n_active && mlv[j].x != -INFINITY;
+            if (live[j]) mx = fmaxf(mx, mlv[j].x);
         }
+        float L = 0.f;
         f32x4_t o = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int j = 0; j < SPT; ++j) {
-            const int sp = sg + GS * j;
-            const float2 v = ml[min(sp, S - 1)];
-            const bool live = sp < n_active && v.x != -INFINITY;
-            const float w = live ? __expf(v.x - mx) : 0.f;
-            const float4 os = live ? ov[j] : make_float4(0.f, 0.f, 0.f, 0.f);
+            const float w = live[j] ? __expf(mlv[j].x - mx) : 0.f;
+            const float4 os = live[j] ? ov[j] : make_float4(0.f, 0.f, 0.f, 0.f);
+            L = fmaf(w, live[j] ? mlv[j].y : 0.f, L);
             o[0] = fmaf(w, os.x, o[0]);
             o[1] = fmaf(w, os.y, o[1]);
             o[2] = fmaf(w, os.z, o[2]);
             o[3] = fmaf(w, os.w, o[3]);
         }
         red[tid] = o;
+        s_ml[tid] = make_float2(mx, L);
         __syncthreads();
         if (sg == 0 && it < items) {
-            f32x4_t sum = red[it];
+            float gm[GS];
+            float M2 = -INFINITY;
 #pragma unroll
-            for (int g2 = 1; g2 < GS; ++g2) sum += red[g2 * TG + it];
+            for (int g2 = 0; g2 < GS; ++g2) {
+                gm[g2] = s_ml[g2 * TG + it].x;
+                M2 = fmaxf(M2, gm[g2]);
+            }
+            f32x4_t sum = f32x4_t{0.f, 0.f, 0.f, 0.f};
+            float Lt = 0.f;
+#pragma unroll
+            for (int g2 = 0; g2 < GS; ++g2) {
+                const float w = gm[g2] == -INFINITY ? 0.f : __expf(gm[g2] - M2);
+                sum += w * red[g2 * TG + it];
+                Lt = fmaf(w, s_ml[g2 * TG + it].y, Lt);
+            }
             const bool valid = i < pl;
-            const float inv = 1.f / L;
+            const float inv = 1.f / Lt;
             const uint2 y = valid ? make_uint2(pack2(sum[0] * inv, sum[1] * inv), pack2(sum[2] * inv, sum[3] * inv))
                                   : make_uint2(0u, 0u);
             *reinterpret_cast<uint2*>(xs + (size_t)m * ldl + (c - kb)) = y;
