@@ -23,9 +23,11 @@
  *  - Every call returns 0 on success or a negative MTP_E* code; no C++
  *    exception crosses this boundary.  mtp_last_error() gives the text of
  *    the last failure on a context.
- *  - The library allocates NO device memory.  The caller allocates the
- *    four device buffers (sizes from mtp_query_sizes) and owns them; they
- *    must outlive the context.  The context owns only host bookkeeping.
+ *  - The library allocates NO device memory at run time.  The caller
+ *    allocates the four device buffers (sizes from mtp_query_sizes) and owns
+ *    them; they must outlive the context.  The context owns only host
+ *    bookkeeping.  The one fixed device array, the scratch of
+ *    mtp_q_count_noalloc, is part of the library's code object.
  *  - All work is ordered on the one HIP stream given to mtp_create.  A
  *    context is not thread-safe.
  *  - Pointers documented "host" are plain host memory; "device" pointers
