@@ -111,19 +111,39 @@ class ARDecoder:
         q: [n, d]; k_all, v_all: [T, d] with row index = absolute position;
         query r at position q_pos[r] sees keys 0..q_pos[r].  Per head h the
         textbook form softmax(Q_h K_h^T / sqrt(64) + M) V_h, with M = -inf
-        where the key's position exceeds the query's, evaluated with plain
-        float64 PyTorch CPU operations (multi-threaded; the arithmetic is the
-        formula as written).  Query rows are taken `rows_per_block` at a time
-        only to bound the size of the score matrix; each row's result does
-        not depend on the blocking.
+        where the key's position exceeds the query's.  Query rows are taken
+        `rows_per_block` at a time only to bound the size of the score
+        matrix; each row's result does not depend on the blocking.  A few
+        query rows (a decode chunk) are evaluated with numpy, many (a prompt
+        or a full recompute) with float64 PyTorch CPU operations, which run
+        the large score matrices multi-threaded; both evaluate the same
+        formula in float64.
         """
+        q_pos = np.asarray(q_pos, dtype=np.int64)
+        if q.shape[0] <= 64:
+            return self._attention_np(q, k_all, v_all, q_pos)
+        return self._attention_torch(q, k_all, v_all, q_pos, rows_per_block)
+
+    def _attention_np(self, q, k_all, v_all, q_pos):
+        n = q.shape[0]
+        out = np.zeros((n, self.d))
+        scale = 1.0 / np.sqrt(self.hd)
+        T = int(q_pos.max()) + 1
+        visible = np.arange(T)[None, :] <= q_pos[:, None]
+        for h in range(self.H):
+            sl = slice(h * self.hd, (h + 1) * self.hd)
+            s = np.where(visible, (q[:, sl] @ k_all[:T, sl].T) * scale, -np.inf)
+            out[:, sl] = softmax(s, axis=-1) @ v_all[:T, sl]
+        return out
+
+    def _attention_torch(self, q, k_all, v_all, q_pos, rows_per_block):
         n = q.shape[0]
         out = torch.zeros((n, self.d), dtype=torch.float64)
         scale = 1.0 / np.sqrt(self.hd)
         qt = torch.from_numpy(np.ascontiguousarray(q, dtype=np.float64))
         kt = torch.from_numpy(np.ascontiguousarray(k_all, dtype=np.float64))
         vt = torch.from_numpy(np.ascontiguousarray(v_all, dtype=np.float64))
-        qp = torch.as_tensor(np.asarray(q_pos, dtype=np.int64))
+        qp = torch.as_tensor(q_pos)
         kp = torch.arange(kt.shape[0])
         for h in range(self.H):
             sl = slice(h * self.hd, (h + 1) * self.hd)

@@ -179,3 +179,19 @@ def test_workloads_shapes():
     assert all(p.max() < 512 for p in pr.phon) and all(a.max() < 1024 for a in pr.ac)
     pr2 = make_prompts(wl)
     assert all(np.array_equal(a, b) for a, b in zip(pr.ac, pr2.ac))
+
+
+def test_attention_paths_agree():
+    """The oracle evaluates the same causal attention formula with numpy for
+    a few query rows and with PyTorch for many: on the same inputs (query
+    rows at arbitrary positions, ragged blocks) both give the same rows."""
+    m = ARDecoder(SMALL, make_weights(SMALL, seed=5))
+    rng = np.random.default_rng(7)
+    T = 300
+    k = rng.standard_normal((T, SMALL.d_model))
+    v = rng.standard_normal((T, SMALL.d_model))
+    pos = np.sort(rng.choice(T, size=40, replace=False))
+    q = rng.standard_normal((40, SMALL.d_model))
+    a = m._attention_np(q, k, v, pos)
+    b = m._attention_torch(q, k, v, pos, rows_per_block=16)
+    np.testing.assert_allclose(a, b, rtol=1e-12, atol=1e-12)
