@@ -284,11 +284,22 @@ __global__ __launch_bounds__(512) void select_fused_kernel(SelectArgs a) {
             const float* T = trow(tt);
             float best = 0.f;
             int arg = 0;
-            for (int i = 0; i < m; ++i) {
-                const float sc = lane_f(delta, i) + T[i * tstep];
-                if (i == 0 || sc > best) {
-                    best = sc;
-                    arg = i;
+            // predecessors in chunks of 8: the chunk's transition entries are
+            // read from LDS together (one wait), then scanned in ascending i
+            for (int i0 = 0; i0 < m; i0 += 8) {
+                float tv[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) tv[u] = T[min(i0 + u, m - 1) * tstep];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    const int i = i0 + u;
+                    if (i < m) {                                  // uniform
+                        const float sc = lane_f(delta, i) + tv[u];
+                        if (i == 0 || sc > best) {
+                            best = sc;
+                            arg = i;
+                        }
+                    }
                 }
             }
             const float et = emis(tt);
@@ -345,7 +356,14 @@ __global__ __launch_bounds__(512) void select_fused_kernel(SelectArgs a) {
         for (int tt = 1; tt < K; ++tt) {
             const float* T = trow(tt);
             float sum = 0.f;
-            for (int i = 0; i < m; ++i) sum = sum + smp_flush(lane_f(alpha, i) * T[i * tstep]);
+            for (int i0 = 0; i0 < m; i0 += 8) {
+                float tv[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) tv[u] = T[min(i0 + u, m - 1) * tstep];
+#pragma unroll
+                for (int u = 0; u < 8; ++u)
+                    if (i0 + u < m) sum = sum + smp_flush(lane_f(alpha, i0 + u) * tv[u]);   // ascending i
+            }
             const float et = emis(tt);
             alpha = (j < m) ? smp_flush(smp_exp(et * inv_tau) * sum) : 0.f;
             alpha = smp_rescale(alpha);
