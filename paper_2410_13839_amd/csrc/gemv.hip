@@ -223,6 +223,8 @@ __global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
     float4 hv[LN ? RPT : 1];                     // residual / embedding rows
     float4 pv[RES ? 4 : 1][RES ? RPT : 1];       // split-K partials of the producer
     float4 zv[XM == 3 ? RPT : 1];                // prefill hidden state (heads, first step)
+    uint2 emb_e[XM == 2 ? RPT : 1], emb_p[XM == 2 ? RPT : 1];   // first layer: embedding, position rows
+    bool emb_ok[XM == 2 ? RPT : 1];
     float4 gv = make_float4(0.f, 0.f, 0.f, 0.f), bv = gv;
     // bf16 chunks (XM 0) as one vector value: an array of uint4 held across
     // the barrier below is demoted to scratch by the compiler
@@ -238,7 +240,7 @@ __global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
         mlv[j] = make_float2(-INFINITY, 0.f);
     }
     (void)pv; (void)zv; (void)xq; (void)st_pl; (void)sti; (void)mlv; (void)ov; (void)gv; (void)bv; (void)hv;
-    (void)s_ml;
+    (void)s_ml; (void)emb_e; (void)emb_p; (void)emb_ok;
     const bool has_part = a.part_on != 0;      // kernel argument: uniform
     if constexpr (XM == 0) {
         // rows [0, M) x columns [kb, kb + ks) as 16-byte chunks
@@ -283,6 +285,23 @@ __global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
         if (rg == 0) {
             gv = *reinterpret_cast<const float4*>(a.g + cc);
             bv = *reinterpret_cast<const float4*>(a.beta + cc);
+        }
+        if constexpr (XM == 2) {
+            // first layer: each pending token's embedding and position rows;
+            // the sequence state first, then the rows it names, so that they
+            // arrive ahead of the weights (loads return in request order)
+#pragma unroll
+            for (int j = 0; j < RPT; ++j) {
+                const int m = rg + RG * j;
+                if (m < M && rg < RG) {
+                    const int seq = m / a.Q, i = m - seq * a.Q;
+                    const SeqState& st = a.st[seq];
+                    const bool valid = i < st.pend_len;
+                    emb_ok[j] = valid;
+                    emb_e[j] = *reinterpret_cast<const uint2*>(a.emb + (size_t)(valid ? st.pend_ids[i] : 0) * K + cc);
+                    emb_p[j] = *reinterpret_cast<const uint2*>(a.pos + (size_t)(valid ? st.ctx_len + i : 0) * K + cc);
+                }
+            }
         }
         if constexpr (RES) {
             // XM 1: row m; XM 3: the last row of sequence m's pending chunk,
@@ -413,13 +432,9 @@ __global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
             for (int j = 0; j < RPT; ++j) {
                 const int m = rg + RG * j;
                 if (m < M && rg < RG) {
-                    const int seq = m / a.Q, i = m - seq * a.Q;
-                    const SeqState& st = a.st[seq];
-                    const bool valid = i < st.pend_len;
-                    const bf16_t* erow = a.emb + (size_t)(valid ? st.pend_ids[i] : 0) * K;
-                    const bf16_t* prow = a.pos + (size_t)(valid ? st.ctx_len + i : 0) * K;
-                    const uint2 e = *reinterpret_cast<const uint2*>(erow + cc);
-                    const uint2 q = *reinterpret_cast<const uint2*>(prow + cc);
+                    const bool valid = emb_ok[j];
+                    const uint2 e = emb_e[j];
+                    const uint2 q = emb_p[j];
                     float4 x;
                     x.x = __uint_as_float(e.x << 16) + __uint_as_float(q.x << 16);
                     x.y = __uint_as_float(e.x & 0xFFFF0000u) + __uint_as_float(q.x & 0xFFFF0000u);
