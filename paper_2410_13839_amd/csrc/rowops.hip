@@ -2,6 +2,7 @@
 // LayerNorm.  One workgroup per row; d_model <= 2048.
 #include "common.h"
 #include "launch.h"
+#include "wave.h"
 
 namespace mtp {
 
@@ -128,8 +129,9 @@ __global__ __launch_bounds__(256) void embed_ln_kernel(EmbedArgs a) {
 
 // One row per workgroup, thread t owning the float4 column chunks t and
 // t + 256.  Every load of the row (the residual, the bias, all NS split-K
-// partial sums) is issued before the first store, so the kernel costs one
-// global round trip; the partial sums are added in split order.
+// partial sums, the LayerNorm gamma and beta) is issued before the first
+// store, so the kernel costs one global round trip; the partial sums are
+// added in split order.
 template <typename ActT, int NS>
 __global__ __launch_bounds__(256) void resid_ln_kernel(ResidArgs a) {
     __shared__ float red[4];
@@ -137,13 +139,17 @@ __global__ __launch_bounds__(256) void resid_ln_kernel(ResidArgs a) {
     const int d = a.d;
     float* h = a.h + (size_t)r * d;
     const float* __restrict__ part = a.part + (size_t)r * d;
-    float4 hv[2], bv[2], pv[NS][2];
+    float4 hv[2], bv[2], pv[NS][2], gv[2], be[2];
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
         const int c = 4 * (tid + 256 * j);
         const int cc = c < d ? c : 0;
         hv[j] = *reinterpret_cast<const float4*>(h + cc);
         bv[j] = *reinterpret_cast<const float4*>(a.bias + cc);
+        if (a.ln_g) {
+            gv[j] = *reinterpret_cast<const float4*>(a.ln_g + cc);
+            be[j] = *reinterpret_cast<const float4*>(a.ln_b + cc);
+        }
 #pragma unroll
         for (int sp = 0; sp < NS; ++sp)
             pv[sp][j] = *reinterpret_cast<const float4*>(part + sp * a.split_stride + cc);
@@ -186,12 +192,17 @@ __global__ __launch_bounds__(256) void resid_ln_kernel(ResidArgs a) {
         if (c < d) {
             // four consecutive columns stay consecutive in fragment order
             ActT* u = reinterpret_cast<ActT*>(a.u) + (a.packed ? frag_off(r, c, d) : (size_t)r * d + c);
-            const float4 gv = *reinterpret_cast<const float4*>(a.ln_g + c);
-            const float4 be = *reinterpret_cast<const float4*>(a.ln_b + c);
-            ActIO<ActT>::store(u + 0, (x[4 * j + 0] - mean) * rstd * gv.x + be.x);
-            ActIO<ActT>::store(u + 1, (x[4 * j + 1] - mean) * rstd * gv.y + be.y);
-            ActIO<ActT>::store(u + 2, (x[4 * j + 2] - mean) * rstd * gv.z + be.z);
-            ActIO<ActT>::store(u + 3, (x[4 * j + 3] - mean) * rstd * gv.w + be.w);
+            const float y0 = (x[4 * j + 0] - mean) * rstd * gv[j].x + be[j].x;
+            const float y1 = (x[4 * j + 1] - mean) * rstd * gv[j].y + be[j].y;
+            const float y2 = (x[4 * j + 2] - mean) * rstd * gv[j].z + be[j].z;
+            const float y3 = (x[4 * j + 3] - mean) * rstd * gv[j].w + be[j].w;
+            if constexpr (sizeof(ActT) == 2) {
+                *reinterpret_cast<uint2*>(u) =
+                    make_uint2((uint32_t)f32_to_bf16(y0) | ((uint32_t)f32_to_bf16(y1) << 16),
+                               (uint32_t)f32_to_bf16(y2) | ((uint32_t)f32_to_bf16(y3) << 16));
+            } else {
+                *reinterpret_cast<float4*>(u) = make_float4(y0, y1, y2, y3);
+            }
         }
     }
 }
@@ -309,6 +320,67 @@ __global__ __launch_bounds__(256) void rows_ln_kernel(RowsLnArgs a) {
     else layer_norm_store<ActT>(x, a.d, a.ln_g, a.ln_b, reinterpret_cast<ActT*>(a.u) + (size_t)r * a.d, red);
 }
 
+// bf16 rows: one wave per row, four rows per workgroup.  Lane l owns the
+// eight-column chunks starting at 8 (l + 64 j); eight consecutive columns are
+// also consecutive in fragment order, so every chunk leaves as one 16-byte
+// store.  Both statistics are wave reductions: no LDS and no barrier.
+template <int NCH>
+__global__ __launch_bounds__(256) void rows_ln_wave_kernel(RowsLnArgs a) {
+    const int r = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+    if (r >= a.n_rows) return;   // wave-uniform
+    const int d = a.d;
+    const float* h = a.h + (size_t)r * d;
+    // the row, gamma and beta all in flight together
+    float x[NCH][8];
+    float4 gb[NCH][4];
+#pragma unroll
+    for (int j = 0; j < NCH; ++j) {
+        const int c = 8 * (lane + 64 * j);
+        const int cc = c < d ? c : 0;
+        const float4 lo = *reinterpret_cast<const float4*>(h + cc);
+        const float4 hi = *reinterpret_cast<const float4*>(h + cc + 4);
+        gb[j][0] = *reinterpret_cast<const float4*>(a.ln_g + cc);
+        gb[j][1] = *reinterpret_cast<const float4*>(a.ln_g + cc + 4);
+        gb[j][2] = *reinterpret_cast<const float4*>(a.ln_b + cc);
+        gb[j][3] = *reinterpret_cast<const float4*>(a.ln_b + cc + 4);
+        const bool ok = c < d;
+        x[j][0] = ok ? lo.x : 0.f; x[j][1] = ok ? lo.y : 0.f; x[j][2] = ok ? lo.z : 0.f; x[j][3] = ok ? lo.w : 0.f;
+        x[j][4] = ok ? hi.x : 0.f; x[j][5] = ok ? hi.y : 0.f; x[j][6] = ok ? hi.z : 0.f; x[j][7] = ok ? hi.w : 0.f;
+    }
+    float s = 0.f;
+#pragma unroll
+    for (int j = 0; j < NCH; ++j)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) s += x[j][i];
+    const float mean = wave_sum64(s) / (float)d;
+    float v = 0.f;
+#pragma unroll
+    for (int j = 0; j < NCH; ++j)
+        if (8 * (lane + 64 * j) < d) {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) { const float t = x[j][i] - mean; v = fmaf(t, t, v); }
+        }
+    const float rstd = rsqrtf(wave_sum64(v) / (float)d + 1e-5f);
+    bf16_t* u = reinterpret_cast<bf16_t*>(a.u);
+#pragma unroll
+    for (int j = 0; j < NCH; ++j) {
+        const int c = 8 * (lane + 64 * j);
+        if (c >= d) continue;
+        const float4 g0 = gb[j][0], g1 = gb[j][1], b0 = gb[j][2], b1 = gb[j][3];
+        const float g[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
+        const float b[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+        uint32_t w[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const bf16_t e0 = f32_to_bf16((x[j][2 * i] - mean) * rstd * g[2 * i] + b[2 * i]);
+            const bf16_t e1 = f32_to_bf16((x[j][2 * i + 1] - mean) * rstd * g[2 * i + 1] + b[2 * i + 1]);
+            w[i] = (uint32_t)e0 | ((uint32_t)e1 << 16);
+        }
+        bf16_t* dst = u + (a.packed ? frag_off(r, c, d) : (size_t)r * d + c);
+        *reinterpret_cast<uint4*>(dst) = make_uint4(w[0], w[1], w[2], w[3]);
+    }
+}
+
 // One wave per listed row.
 __global__ __launch_bounds__(256) void rows_argmax_kernel(ArgmaxArgs a) {
     const int i = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
@@ -342,6 +414,16 @@ hipError_t nar_embed_ln(hipStream_t st, const NarEmbedArgs& a) {
 
 hipError_t rows_ln(hipStream_t st, const RowsLnArgs& a) {
     if (a.n_rows <= 0) return hipSuccess;
+    if (a.dtype == 1 && a.d % 8 == 0 && a.d <= 2048) {
+        const dim3 g((a.n_rows + 3) / 4), b(256);
+        switch ((a.d + 511) / 512) {
+        case 1: hipLaunchKernelGGL(rows_ln_wave_kernel<1>, g, b, 0, st, a); break;
+        case 2: hipLaunchKernelGGL(rows_ln_wave_kernel<2>, g, b, 0, st, a); break;
+        case 3: hipLaunchKernelGGL(rows_ln_wave_kernel<3>, g, b, 0, st, a); break;
+        default: hipLaunchKernelGGL(rows_ln_wave_kernel<4>, g, b, 0, st, a); break;
+        }
+        return hipGetLastError();
+    }
     if (a.dtype == 1) hipLaunchKernelGGL(rows_ln_kernel<bf16_t>, dim3(a.n_rows), dim3(256), 0, st, a);
     else hipLaunchKernelGGL(rows_ln_kernel<float>, dim3(a.n_rows), dim3(256), 0, st, a);
     return hipGetLastError();
