@@ -185,7 +185,14 @@ int mtp_prefill(mtp_ctx* ctx, int B, const int32_t* phon, const int32_t* phon_le
  * 32 from 32 up, sets the keys per decode-attention split of the steps
  * planned after it is set (raised where needed to keep at most 64 splits;
  * the library otherwise chooses it from the batch and the longest
- * context).  Results are the same up to floating-point rounding. */
+ * context).  Results are the same up to floating-point rounding.
+ * Second override: MTP_QKV_ATTN = 8 or 16 runs, for B * K <= 8 rows of a
+ * bf16 model with d_model <= 1024 and contexts of at most 256 * that many
+ * keys, the QKV projection and the attention over the cached keys as one
+ * launch with that many workgroups (key splits) per head, the pending
+ * chunk's attention to its own keys merged by the out-projection; unset or
+ * 0, separate QKV and attention launches (the faster on MI355X).  Again the
+ * same results up to rounding; read when a step is planned. */
 int mtp_decode_step(mtp_ctx* ctx, int K, int top_k, int32_t* out_tokens, int32_t* out_count);
 
 /* Same step, outputs written to DEVICE buffers d_tokens[B*K] and d_count[B]
@@ -307,6 +314,8 @@ int mtp_get_tokens(mtp_ctx* ctx, int32_t* tokens);
 #define MTP_KCLASS_GEMM_OPROJ  6   /* attention out x W_o^T (residual part.)  */
 #define MTP_KCLASS_SELECT      7   /* top_k, Viterbi lattice and accept       */
 #define MTP_KCLASS_RESID_LN    8   /* residual + LayerNorm rows (batched path, two per layer) */
+#define MTP_KCLASS_QKV_ATTN    9   /* LN1 -> x W_qkv^T, K/V into the cache, attention over the
+                                      cached keys, in one launch (B * K <= 8 rows, d <= 1024) */
 int mtp_profile_replay(mtp_ctx* ctx, int kclass, int iters, void* flush_buf, uint64_t flush_bytes,
                        double* avg_us);
 

@@ -9,7 +9,8 @@ from concurrent.futures import ThreadPoolExecutor
 PKG = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libmtp.so")
-SOURCES = ["api.hip", "gemm.hip", "gemv.hip", "attention.hip", "attn_mfma.hip", "rowops.hip", "select.hip", "qest.hip"]
+SOURCES = ["api.hip", "gemm.hip", "gemv.hip", "attention.hip", "attn_mfma.hip", "rowops.hip", "select.hip", "qest.hip",
+           "qkv_attn.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-function",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]

@@ -128,7 +128,7 @@ int validate(const mtp_config* c, std::string* why) {
 }
 
 struct WsLayout {
-    uint64_t rows, ids, tiles, last_row, state, btab, h, q, u, attn, ffn, part, apart, hz, z, logits, cand, ehat,
+    uint64_t rows, ids, tiles, last_row, state, btab, h, q, u, attn, ffn, part, apart, kvnew, hz, z, logits, cand, ehat,
         u_states, u_m, u_ehat, u_delta, u_psi, smp_cfg, smp_u, codes, tgt_rows, nar_logits,
         delta, psi, slots, out_tok, out_cnt, hist, total;
     int64_t m_pre, m_dec, m_max, max_tiles, max_splits, maxp, num_pages;
@@ -146,6 +146,10 @@ WsLayout ws_layout(const mtp_config& c) {
     w.max_tiles = w.m_pre / MTP_ATTN_QT + B + 1;
     const int64_t max_ctx = (int64_t)c.max_prompt + (is_nar(c) ? 0 : c.max_new);
     w.max_splits = (max_ctx + 63) / 64;
+    // the fused QKV + attention front of small batches writes one word per
+    // workgroup of a head (up to 16) whatever the context
+    const bool front = c.dtype == MTP_DTYPE_BF16 && w.m_dec <= 8 && d <= 1024 && !is_nar(c);
+    if (front) w.max_splits = std::max<int64_t>(w.max_splits, 16);
     w.maxp = (max_ctx + c.page_size - 1) / c.page_size;
     w.num_pages = c.num_pages > 0 ? c.num_pages : B * w.maxp;
     uint64_t o = 0;
@@ -166,6 +170,7 @@ WsLayout ws_layout(const mtp_config& c) {
     // split-K partials: up to 4 splits of a prefill-sized GEMM, 8 of a decode one
     w.part = take(std::max(w.m_pre * 4, w.m_dec * (int64_t)MTP_SPLITK_MAX) * d * 4);
     w.apart = take(B * H * w.max_splits * MTP_ATTN_QT * 68 * 4);
+    w.kvnew = take(front ? 2 * w.m_dec * d * 2 : 0);   // the pending rows' keys and values (bf16)
     w.hz = take(B * d * 4);
     w.z = take((B + 15) / 16 * 16 * d * w.act_bytes);
     w.logits = take(B * KH * V * 4);
@@ -211,6 +216,7 @@ struct mtp_ctx {
     int q_pad = 0;               // pending rows per sequence for the next step
     int last_K = 0, last_topk = 0, last_lattice = 0, last_sample = 0;
     int split_len = 64, n_splits = 1;
+    bool front_fused = false;    // the step's layers start with one qkv_attn launch (small batches)
     int lattice = MTP_LATTICE_OWN, anchored = 0;   // selection options (mtp_set_selection)
     int sample = 0;              // mtp_set_sampling: draw the path instead of the best one
     SampleCfg h_smp{0, 1.0f, 0}; // copied to the workspace before the next step when dirty
@@ -225,13 +231,13 @@ struct mtp_ctx {
     std::vector<int2> h_tiles;
     std::vector<SeqState> h_state;
     int n_pre_rows = 0, n_pre_tiles = 0;
-    // graphs keyed by (K, top_k, q_pad, batch, split_len, n_splits, lattice, anchored)
-    using StepKey = std::tuple<int, int, int, int, int, int, int, int, int>;
+    // graphs keyed by (K, top_k, q_pad, batch, split_len, n_splits, lattice, anchored, sampling, fused front)
+    using StepKey = std::tuple<int, int, int, int, int, int, int, int, int, int>;
     std::map<StepKey, hipGraphExec_t> graphs;
     // every launch of each kernel class in the step of a key (arguments
     // captured by value), for replay timing
     using Launch = std::function<hipError_t(hipStream_t)>;
-    struct StepLaunches { std::vector<Launch> cls[MTP_KCLASS_RESID_LN + 1]; };
+    struct StepLaunches { std::vector<Launch> cls[MTP_KCLASS_QKV_ATTN + 1]; };
     std::map<StepKey, StepLaunches> step_launches;
     StepLaunches* recording = nullptr;
     StepKey last_key{};
@@ -283,7 +289,7 @@ int pick_splits(const mtp_ctx* c, int M, int N, int K) {
 // Launch through `f` and, while a step is being recorded, keep it under class `kclass`.
 hipError_t launch_rec(mtp_ctx* c, int kclass, std::function<hipError_t(hipStream_t)> f) {
     hipError_t e = f(c->stream);
-    if (kclass > 0 && kclass <= MTP_KCLASS_RESID_LN && c->recording) c->recording->cls[kclass].push_back(std::move(f));
+    if (kclass > 0 && kclass <= MTP_KCLASS_QKV_ATTN && c->recording) c->recording->cls[kclass].push_back(std::move(f));
     return e;
 }
 
@@ -342,16 +348,27 @@ int run_layer_fused(mtp_ctx* c, int l, int rows, int qt) {
     g.g = (const float*)c->lt(l, MTP_T_LN1_G); g.beta = (const float*)c->lt(l, MTP_T_LN1_B);
     g.st = c->ws_ptr<SeqState>(c->ws.state); g.Q = c->q_pad;
     g.bias = (const float*)c->lt(l, MTP_T_B_QKV); g.q = c->ws_ptr<float>(c->ws.q); g.kv = c->kv(l); g.d = d;
-    HIPCHK(c, launch_rec(c, MTP_KCLASS_GEMM_QKV, [g](hipStream_t s) { return gemv(s, g); }), "qkv gemv");
-
-    const bool pm = prologue_merge(c, rows);
-    HIPCHK(c, decode_attention(c, l, qt, !pm), "decode attention");
+    bf16_t* kvnew = c->ws_ptr<bf16_t>(c->ws.kvnew);
+    bool pm;
+    if (c->front_fused) {
+        // LN1 + QKV + attention over the cached keys in one launch; the
+        // out-projection merges the splits and the chunk's own keys
+        g.apart = c->ws_ptr<float>(c->ws.apart); g.qt = qt; g.split_len = c->split_len; g.n_splits = c->n_splits;
+        g.kvnew = kvnew;
+        HIPCHK(c, launch_rec(c, MTP_KCLASS_QKV_ATTN, [g](hipStream_t s) { return qkv_attn(s, g); }), "qkv + attention");
+        pm = true;
+    } else {
+        HIPCHK(c, launch_rec(c, MTP_KCLASS_GEMM_QKV, [g](hipStream_t s) { return gemv(s, g); }), "qkv gemv");
+        pm = prologue_merge(c, rows);
+        HIPCHK(c, decode_attention(c, l, qt, !pm), "decode attention");
+    }
 
     g = GemvArgs{};
-    g.epi = EPI_PARTIAL; g.xmode = pm ? 4 : 0; g.M = rows; g.N = d; g.K = d;
+    g.epi = EPI_PARTIAL; g.xmode = c->front_fused ? 5 : pm ? 4 : 0; g.M = rows; g.N = d; g.K = d;
     g.W = (const bf16_t*)c->lt(l, MTP_T_W_O); g.x = (const bf16_t*)(c->WS() + c->ws.attn); g.ldx = d;
     g.st = c->ws_ptr<SeqState>(c->ws.state); g.Q = c->q_pad;
     g.apart = c->ws_ptr<float>(c->ws.apart); g.qt = qt; g.split_len = c->split_len; g.n_splits = c->n_splits;
+    g.q = c->ws_ptr<float>(c->ws.q); g.kvnew = kvnew;
     g.h = h; g.ldh = d; g.bias = (const float*)c->lt(l, MTP_T_B_O); g.part_out = part;
     HIPCHK(c, launch_rec(c, MTP_KCLASS_GEMM_OPROJ, [g](hipStream_t s) { return gemv(s, g); }), "out-proj gemv");
 
@@ -509,7 +526,9 @@ int enqueue_step(mtp_ctx* c, int K, int top_k) {
             if (rc) return rc;
         }
     }
-    if (dt == MTP_DTYPE_BF16 && B <= 4) {
+    // the fused small-batch layers leave the last FFN2 as split-K partials,
+    // which only the heads' LayerNorm prologue completes (B <= B * Q <= 16)
+    if (dt == MTP_DTYPE_BF16 && (B <= 4 || fin_part)) {
         GemvArgs g{};
         g.epi = EPI_LOGITS; g.xmode = 3; g.M = B; g.N = K * V; g.K = d;
         g.W = (const bf16_t*)c->wt(MTP_T_W_HEADS); g.h = c->ws_ptr<float>(c->ws.h); g.ldh = d;
@@ -564,6 +583,24 @@ int plan_splits(mtp_ctx* c, int Q) {
     const int64_t rows = B * std::max(Q, 1);
     const int merge_max =
         (cf.dtype == MTP_DTYPE_BF16 && rows <= 16) ? gemv_merge_max_splits((int)rows, cf.d_model) : 0;
+    // small batches, on request: QKV and the attention over the cached keys
+    // in one launch with G workgroups (key splits) per head.  Not the
+    // default: every workgroup streams its head's 128 KB of query weights,
+    // so the launch takes about as long as the two it replaces (10.7 vs
+    // 5.97 + 5.13 us at batch 1, K = 4) and the out-projection's merge of
+    // the chunk's own keys adds ~1 us (323 vs 312 us per step)
+    c->front_fused = false;
+    if (cf.dtype == MTP_DTYPE_BF16 && Q > 0 && !(cf.flags & MTP_FLAG_NAR)) {
+        int G = 0;
+        if (const char* env = getenv("MTP_QKV_ATTN")) G = atoi(env);
+        if ((G == 8 || G == 16) && G <= c->ws.max_splits && G <= merge_max &&
+            qkv_attn_ok((int)rows, cf.d_model, cf.n_heads, max_ctx, G)) {
+            c->front_fused = true;
+            c->split_len = qkv_attn_split_len(max_ctx, G);
+            c->n_splits = G;
+            return MTP_OK;
+        }
+    }
     int64_t sl;
     if (merge_max >= 2) {
         sl = std::max<int64_t>(128, ((max_ctx + merge_max - 1) / merge_max + 63) / 64 * 64);
@@ -606,7 +643,7 @@ int step_common(mtp_ctx* c, int K, int top_k) {
         c->smp_dirty = false;
     }
     const auto key = std::make_tuple(K, top_k, c->q_pad, c->B, c->split_len, c->n_splits, c->lattice, c->anchored,
-                                     c->sample);
+                                     c->sample, c->front_fused ? 1 : 0);
     auto record = [&]() {
         mtp_ctx::StepLaunches& sl = c->step_launches[key];
         for (auto& v : sl.cls) v.clear();
@@ -1162,7 +1199,7 @@ int mtp_profile_replay(mtp_ctx* c, int kclass, int iters, void* flush_buf, uint6
         return MTP_EINVAL;
     }
     const bool cold = flush_buf != nullptr;
-    if (kclass < MTP_KCLASS_GEMM_FFN1 || kclass > MTP_KCLASS_RESID_LN) { c->err = "unknown kernel class"; return MTP_EINVAL; }
+    if (kclass < MTP_KCLASS_GEMM_FFN1 || kclass > MTP_KCLASS_QKV_ATTN) { c->err = "unknown kernel class"; return MTP_EINVAL; }
     auto it = c->has_last ? c->step_launches.find(c->last_key) : c->step_launches.end();
     if (it == c->step_launches.end() || it->second.cls[kclass].empty()) {
         c->err = "the last decode step launched nothing of this kernel class";

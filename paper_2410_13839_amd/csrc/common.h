@@ -130,3 +130,10 @@ struct KVView {
         return (base + head) * page_size * MTP_HEAD_DIM + slot;
     }
 };
+
+// Element offset of the K (sec 0) or transposed V (sec 1) block of one head
+// in cache page `page` (the page table already looked up).
+__device__ __forceinline__ size_t kv_page_block(const KVView& kv, int page, int sec, int head) {
+    return ((((size_t)kv.layer * kv.num_pages + page) * 2 + sec) * kv.n_heads + head) * (size_t)kv.page_size *
+           MTP_HEAD_DIM;
+}

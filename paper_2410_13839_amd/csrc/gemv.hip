@@ -35,6 +35,7 @@
 
 #include "common.h"
 #include "launch.h"
+#include "ln_rows.h"
 #include "wave.h"
 
 namespace mtp {
@@ -166,18 +167,16 @@ struct EpiLogitsB {
 // XM: 0 = bf16 rows, 1 = LN of the completed residual rows, 2 = embedding +
 //     LN (decode rows of the first layer), 3 = final LN of each sequence's
 //     last pending row (heads), 4 = merge of the attention key-split partials
-//     of this workgroup's heads (out-projection).
+//     of this workgroup's heads (out-projection), 5 = that merge plus the
+//     pending chunk's own keys (after qkv_attn, which leaves them out).
 // MR: rows (power of two >= M, <= 16); MAXF: weight fragments per wave;
-// KCH: 1024-column chunks per row; MAXS: attention splits merged (XM 4).
+// KCH: 1024-column chunks per row; MAXS: attention splits merged (XM 4, 5).
 //
 // 16 waves per workgroup: a CU with one workgroup of four waves keeps too few
 // loads in flight to pull more than ~12-25 GB/s, with sixteen it pulls about
 // twice that (measured), and every launch here is a single wave of
 // workgroups, so the time is one workgroup's load latency and throughput.
-// LayerNorm-mode prologue: thread t owns the float4 column chunk t % (K/4) of
-// rows t / (K/4), t / (K/4) + RG, ... (RG = 1024 / (K/4) row groups), so the
-// LayerNorm parameters are loaded once per thread and a row's statistics
-// are a reduction over the K/4/64 waves of its row group.
+// The LayerNorm modes' prologue is LnRows (ln_rows.h).
 constexpr int GV_NW = 16;
 
 template <int MR, int XM, int MAXF, int KCH, int MAXS, int NW, class Epi>
@@ -188,9 +187,8 @@ __global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
     // shift ([2][K/4] float4, K <= 2048)
     __shared__ f32x4_t red[1024];
     constexpr bool LN = XM >= 1 && XM <= 3;
-    constexpr bool RES = XM == 1 || XM == 3;                           // residual completed here
-    constexpr int RPT = (MR * KCH * 256 + T - 1) / T;                  // rows per thread (LN modes)
-    __shared__ float2 s_stat[NW][LN ? RPT : 1];
+    using Rows = LnRows<MR, LN ? XM : 1, KCH, T>;
+    __shared__ float2 s_stat[NW][LN ? Rows::RPT : 1];
     constexpr int XI = (MR * MAXF + 15) / 16;                          // 16-byte chunks per thread (XM 0)
     // XM 4: the (row, float4 column chunk) items of this K range (at most
     // MR * 64 * KCH) x the splits; GS groups of threads take every GS-th split
@@ -199,7 +197,10 @@ __global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
     constexpr int SPT = (MAXS + GS - 1) / GS;                          // splits per thread
     // each thread merges its own splits (group max, sum and weighted output)
     // and the GS groups combine through LDS once
-    __shared__ float2 s_ml[XM == 4 ? T : 1];
+    constexpr bool MERGE = XM == 4 || XM == 5;
+    constexpr bool NK = XM == 5;                                       // the chunk's own keys merged here
+    constexpr int NQ = NK ? MR : 1;                                    // pending rows per sequence <= MR
+    __shared__ float2 s_ml[MERGE ? T : 1];
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int r = lane & 15, g = lane >> 4;
@@ -211,37 +212,30 @@ __global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
     const int nfrag = ks >> 5;
     const int nf = (nfrag - wave + NW - 1) / NW;  // fragments f = wave + NW i, i < nf
     const int ldl = ks + 8;
-    // LayerNorm-mode mapping; rg is uniform over a wave (K/4 is a multiple of 64)
-    const int K4 = K >> 2;
-    const int RG = T / K4;                        // row groups (>= 1 for K <= 2048)
-    const int rg = __builtin_amdgcn_readfirstlane(wave) / (K4 >> 6);   // scalar division
-    const int cc = min((tid - rg * K4) * 4, K - 4);
-    (void)RG; (void)rg; (void)cc; (void)K4;
-
     // ---- A. activation-side loads (compact, from clamped addresses; branches
     //      only on wave-uniform conditions, which cost no extra waits) ----
-    float4 hv[LN ? RPT : 1];                     // residual / embedding rows
-    float4 pv[RES ? 4 : 1][RES ? RPT : 1];       // split-K partials of the producer
-    float4 zv[XM == 3 ? RPT : 1];                // prefill hidden state (heads, first step)
-    uint2 emb_e[XM == 2 ? RPT : 1], emb_p[XM == 2 ? RPT : 1];   // first layer: embedding, position rows
-    bool emb_ok[XM == 2 ? RPT : 1];
-    float4 gv = make_float4(0.f, 0.f, 0.f, 0.f), bv = gv;
+    // LayerNorm rows (XM 1..3): the register arrays are the kernel's own
+    float4 ln_hv[Rows::RPT], ln_pv[Rows::RES ? 4 : 1][Rows::RES ? Rows::RPT : 1], ln_zv[XM == 3 ? Rows::RPT : 1];
+    uint2 ln_ee[XM == 2 ? Rows::RPT : 1], ln_ep[XM == 2 ? Rows::RPT : 1];
+    bool ln_eok[XM == 2 ? Rows::RPT : 1];
+    int ln_pl[XM == 3 ? Rows::RPT : 1];
+    Rows lr{ln_hv, ln_pv, ln_zv, ln_ee, ln_ep, ln_eok, ln_pl};
     // bf16 chunks (XM 0) as one vector value: an array of uint4 held across
     // the barrier below is demoted to scratch by the compiler
     typedef unsigned int xq_t __attribute__((ext_vector_type(4 * XI)));
     xq_t xq;
-    int st_pl[XM == 3 ? RPT : 1];
-    int2 sti = make_int2(0, 0);                  // XM 4: (ctx_len, pend_len) of the item's sequence
-    float2 mlv[XM == 4 ? SPT : 1];               // XM 4: (running max, sum) words of the thread's splits
-    float4 ov[XM == 4 ? SPT : 1];                // XM 4: unnormalised outputs of the thread's splits
+    int2 sti = make_int2(0, 0);                  // XM 4, 5: (ctx_len, pend_len) of the item's sequence
+    float2 mlv[MERGE ? SPT : 1];                 // XM 4, 5: (running max, sum) words of the thread's splits
+    float4 ov[MERGE ? SPT : 1];                  // XM 4, 5: unnormalised outputs of the thread's splits
+    float4 qn = make_float4(0.f, 0.f, 0.f, 0.f); // XM 5: the item's query dims, and the four dims of
+    uint2 kn[NQ], vn[NQ];                        //   each pending key / value of its sequence (bf16)
+    (void)qn; (void)kn; (void)vn;
 #pragma unroll
-    for (int j = 0; j < (XM == 4 ? SPT : 1); ++j) {
+    for (int j = 0; j < (MERGE ? SPT : 1); ++j) {
         ov[j] = make_float4(0.f, 0.f, 0.f, 0.f);
         mlv[j] = make_float2(-INFINITY, 0.f);
     }
-    (void)pv; (void)zv; (void)xq; (void)st_pl; (void)sti; (void)mlv; (void)ov; (void)gv; (void)bv; (void)hv;
-    (void)s_ml; (void)emb_e; (void)emb_p; (void)emb_ok;
-    const bool has_part = a.part_on != 0;      // kernel argument: uniform
+    (void)xq; (void)sti; (void)mlv; (void)ov; (void)s_ml; (void)lr;
     if constexpr (XM == 0) {
         // rows [0, M) x columns [kb, kb + ks) as 16-byte chunks
         const int cpr = ks >> 3;                 // chunks per row
@@ -256,7 +250,7 @@ __global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
             xq[4 * i + 2] = t.z;
             xq[4 * i + 3] = t.w;
         }
-    } else if constexpr (XM == 4) {
+    } else if constexpr (MERGE) {
         // the thread's item (row, float4 chunk) in each of its splits
         // (sg, sg + GS, ...): the split's (max, sum) word of that row and
         // head and the item's unnormalised outputs; splits past the context
@@ -280,51 +274,24 @@ __global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
                 mlv[j] = *reinterpret_cast<const float2*>(e);
                 ov[j] = *reinterpret_cast<const float4*>(e + 4 + (c & 63));
             }
-    } else {
-        // LayerNorm gain and shift: loaded by row group 0 only, shared through LDS
-        if (rg == 0) {
-            gv = *reinterpret_cast<const float4*>(a.g + cc);
-            bv = *reinterpret_cast<const float4*>(a.beta + cc);
-        }
-        if constexpr (XM == 2) {
-            // first layer: each pending token's embedding and position rows;
-            // the sequence state first, then the rows it names, so that they
-            // arrive ahead of the weights (loads return in request order)
+        if constexpr (NK) {
+            // group 0 merges the pending chunk's own keys: the item's query
+            // dims and those dims of each pending key and value of its
+            // sequence (row seq Q + j of the side buffer)
+            if (sg == 0) {
+                qn = *reinterpret_cast<const float4*>(a.q + (size_t)m * K + c);
 #pragma unroll
-            for (int j = 0; j < RPT; ++j) {
-                const int m = rg + RG * j;
-                if (m < M && rg < RG) {
-                    const int seq = m / a.Q, i = m - seq * a.Q;
-                    const SeqState& st = a.st[seq];
-                    const bool valid = i < st.pend_len;
-                    emb_ok[j] = valid;
-                    emb_e[j] = *reinterpret_cast<const uint2*>(a.emb + (size_t)(valid ? st.pend_ids[i] : 0) * K + cc);
-                    emb_p[j] = *reinterpret_cast<const uint2*>(a.pos + (size_t)(valid ? st.ctx_len + i : 0) * K + cc);
-                }
-            }
-        }
-        if constexpr (RES) {
-            // XM 1: row m; XM 3: the last row of sequence m's pending chunk,
-            // plus the prefill state (chosen once the state is in).  With
-            // partials the four of them sum to the row (the first carries the
-            // residual input and bias); without, the row is h itself.
-#pragma unroll
-            for (int j = 0; j < RPT; ++j) {
-                const int m = rg + RG * j;
-                if (m < M && rg < RG) {
-                    const int row = (XM == 1) ? m : ((a.Q > 0) ? m * a.Q + a.Q - 1 : 0);
-                    if constexpr (XM == 3) st_pl[j] = a.st[m].pend_len;
-                    if (has_part) {
-#pragma unroll
-                        for (int s2 = 0; s2 < 4; ++s2)
-                            pv[s2][j] = *reinterpret_cast<const float4*>(a.part + ((size_t)s2 * a.part_rows + row) * a.ldh + cc);
-                    } else {
-                        hv[j] = *reinterpret_cast<const float4*>(a.h + (size_t)row * a.ldh + cc);
+                for (int j = 0; j < NQ; ++j)
+                    if (j < a.Q) {
+                        const size_t kr = (size_t)(seq * a.Q + j) * K + c;
+                        kn[j] = *reinterpret_cast<const uint2*>(a.kvnew + kr);
+                        vn[j] = *reinterpret_cast<const uint2*>(a.kvnew + (size_t)M * K + kr);
                     }
-                    if constexpr (XM == 3) zv[j] = *reinterpret_cast<const float4*>(a.hz + (size_t)m * a.ldh + cc);
-                }
             }
         }
+    } else {
+        lr.init(a, tid, wave);
+        lr.load(a);
     }
 
     // Every wave's activation loads go out before any weight load: a CU
@@ -364,7 +331,7 @@ __global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
                     make_uint4(xq[4 * i], xq[4 * i + 1], xq[4 * i + 2], xq[4 * i + 3]);
             }
         }
-    } else if constexpr (XM == 4) {
+    } else if constexpr (MERGE) {
         const int cpr = ks >> 2, items = M * cpr;
         const int S = a.n_splits;
         const int TG = T / GS, sg = __builtin_amdgcn_readfirstlane(wave) / (TG >> 6), it = tid - sg * TG;
@@ -372,9 +339,10 @@ __global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
         const int c = kb + (min(it, items - 1) - m * cpr) * 4;
         const int i = m - udiv_small(m, a.Q) * a.Q;
         const int ctx = sti.x, pl = sti.y;
-        const int n_active = min(S, udiv_small(ctx + pl + a.split_len - 1, a.split_len));
-        // this thread's splits: splits past the context (or a key range fully
-        // masked for this row) contribute nothing; their words may be stale
+        // XM 4: splits past the context are not launched, their words may be
+        // stale; XM 5: every split's word is written (max -inf when empty).
+        // A key range fully masked for this row contributes nothing.
+        const int n_active = NK ? S : min(S, udiv_small(ctx + pl + a.split_len - 1, a.split_len));
         bool live[SPT];
         float mx = -INFINITY;
 #pragma unroll
@@ -397,6 +365,28 @@ __global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
         red[tid] = o;
         s_ml[tid] = make_float2(mx, L);
         __syncthreads();
+        // XM 5: scores of the pending keys, q . k / 8 with q rounded to bf16
+        // after the scale (as the cached keys' scores are taken): each lane
+        // sums its four dims and the 16 lanes of the head (consecutive items,
+        // K / 4 a multiple of 16) add theirs
+        float scn[NQ];
+        if constexpr (NK) {
+            if (sg == 0) {
+                const float q0 = bf16_to_f32(f32_to_bf16(qn.x * 0.125f)), q1 = bf16_to_f32(f32_to_bf16(qn.y * 0.125f));
+                const float q2 = bf16_to_f32(f32_to_bf16(qn.z * 0.125f)), q3 = bf16_to_f32(f32_to_bf16(qn.w * 0.125f));
+#pragma unroll
+                for (int j = 0; j < NQ; ++j) {
+                    float p = 0.f;
+                    if (j < a.Q) {
+                        p = q0 * __uint_as_float(kn[j].x << 16);
+                        p = fmaf(q1, __uint_as_float(kn[j].x & 0xFFFF0000u), p);
+                        p = fmaf(q2, __uint_as_float(kn[j].y << 16), p);
+                        p = fmaf(q3, __uint_as_float(kn[j].y & 0xFFFF0000u), p);
+                    }
+                    scn[j] = sum16(p);
+                }
+            }
+        }
         if (sg == 0 && it < items) {
             float gm[GS];
             float M2 = -INFINITY;
@@ -413,6 +403,26 @@ __global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
                 sum += w * red[g2 * TG + it];
                 Lt = fmaf(w, s_ml[g2 * TG + it].y, Lt);
             }
+            if constexpr (NK) {
+                // row i attends the chunk's keys 0 .. i (its own position last)
+                float M3 = M2;
+#pragma unroll
+                for (int j = 0; j < NQ; ++j)
+                    if (j < a.Q && j <= i) M3 = fmaxf(M3, scn[j]);
+                const float wo = M2 == -INFINITY ? 0.f : __expf(M2 - M3);
+                sum *= wo;
+                Lt *= wo;
+#pragma unroll
+                for (int j = 0; j < NQ; ++j)
+                    if (j < a.Q && j <= i) {
+                        const float p = __expf(scn[j] - M3);
+                        Lt += p;
+                        sum[0] = fmaf(p, __uint_as_float(vn[j].x << 16), sum[0]);
+                        sum[1] = fmaf(p, __uint_as_float(vn[j].x & 0xFFFF0000u), sum[1]);
+                        sum[2] = fmaf(p, __uint_as_float(vn[j].y << 16), sum[2]);
+                        sum[3] = fmaf(p, __uint_as_float(vn[j].y & 0xFFFF0000u), sum[3]);
+                    }
+            }
             const bool valid = i < pl;
             const float inv = 1.f / Lt;
             const uint2 y = valid ? make_uint2(pack2(sum[0] * inv, sum[1] * inv), pack2(sum[2] * inv, sum[3] * inv))
@@ -420,113 +430,7 @@ __global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
             *reinterpret_cast<uint2*>(xs + (size_t)m * ldl + (c - kb)) = y;
         }
     } else {
-        // row group 0 shares the LayerNorm gain and shift
-        f32x4_t* s_gb = red;                      // [2][K/4]
-        if (rg == 0) {
-            s_gb[cc >> 2] = f32x4_t{gv.x, gv.y, gv.z, gv.w};
-            s_gb[K4 + (cc >> 2)] = f32x4_t{bv.x, bv.y, bv.z, bv.w};
-        }
-        if constexpr (XM == 2) {
-            // embedding of each pending token at its position (first layer)
-#pragma unroll
-            for (int j = 0; j < RPT; ++j) {
-                const int m = rg + RG * j;
-                if (m < M && rg < RG) {
-                    const bool valid = emb_ok[j];
-                    const uint2 e = emb_e[j];
-                    const uint2 q = emb_p[j];
-                    float4 x;
-                    x.x = __uint_as_float(e.x << 16) + __uint_as_float(q.x << 16);
-                    x.y = __uint_as_float(e.x & 0xFFFF0000u) + __uint_as_float(q.x & 0xFFFF0000u);
-                    x.z = __uint_as_float(e.y << 16) + __uint_as_float(q.y << 16);
-                    x.w = __uint_as_float(e.y & 0xFFFF0000u) + __uint_as_float(q.y & 0xFFFF0000u);
-                    hv[j] = valid ? x : make_float4(0.f, 0.f, 0.f, 0.f);
-                }
-            }
-        } else {
-            // the residual row: the sum of the four partials, or h itself
-#pragma unroll
-            for (int j = 0; j < RPT; ++j) {
-                const int m = rg + RG * j;
-                if (m < M && rg < RG) {
-                    float4 x = hv[j];
-                    if (has_part) {
-                        x.x = (pv[0][j].x + pv[1][j].x) + (pv[2][j].x + pv[3][j].x);
-                        x.y = (pv[0][j].y + pv[1][j].y) + (pv[2][j].y + pv[3][j].y);
-                        x.z = (pv[0][j].z + pv[1][j].z) + (pv[2][j].z + pv[3][j].z);
-                        x.w = (pv[0][j].w + pv[1][j].w) + (pv[2][j].w + pv[3][j].w);
-                    }
-                    if constexpr (XM == 3) {
-                        const int pl = st_pl[j];
-                        if (!(a.Q > 0 && pl == a.Q)) x = zv[j];
-                        // a partially filled pending chunk (not produced by the
-                        // decode loop, which leaves 0 or Q rows): that row instead
-                        if (a.Q > 0 && pl > 0 && pl < a.Q) {
-                            const int row = m * a.Q + pl - 1;
-                            if (has_part) {
-                                float4 p4[4];
-#pragma unroll
-                                for (int s2 = 0; s2 < 4; ++s2)
-                                    p4[s2] = *reinterpret_cast<const float4*>(a.part + ((size_t)s2 * a.part_rows + row) * a.ldh + cc);
-                                x.x = (p4[0].x + p4[1].x) + (p4[2].x + p4[3].x);
-                                x.y = (p4[0].y + p4[1].y) + (p4[2].y + p4[3].y);
-                                x.z = (p4[0].z + p4[1].z) + (p4[2].z + p4[3].z);
-                                x.w = (p4[0].w + p4[1].w) + (p4[2].w + p4[3].w);
-                            } else {
-                                x = *reinterpret_cast<const float4*>(a.h + (size_t)row * a.ldh + cc);
-                            }
-                        }
-                    }
-                    hv[j] = x;
-                }
-            }
-        }
-        // workgroup 0 writes the completed rows (the next projection's residual input)
-        if (a.h_out && blockIdx.x == 0 && blockIdx.y == 0 && rg < RG) {
-#pragma unroll
-            for (int j = 0; j < RPT; ++j) {
-                const int m = rg + RG * j;
-                if (m < M) *reinterpret_cast<float4*>(a.h_out + (size_t)m * a.ldh + cc) = hv[j];
-            }
-        }
-        // LayerNorm statistics: one pass (sum, sum of squares) per row; the
-        // waves of a row group cover its row exactly once
-#pragma unroll
-        for (int j = 0; j < RPT; ++j) {
-            const int m = rg + RG * j;
-            if (m < M && rg < RG) {
-                const float4 x = hv[j];
-                float s1 = (x.x + x.y) + (x.z + x.w);
-                float s2 = (x.x * x.x + x.y * x.y) + (x.z * x.z + x.w * x.w);
-                s1 = wave_sum64(s1);
-                s2 = wave_sum64(s2);
-                if (lane == 0) s_stat[wave][j] = make_float2(s1, s2);
-            }
-        }
-        __syncthreads();
-        const float inv_k = 1.f / (float)K;
-        const int wpg = K4 >> 6;                  // waves per row group
-        const f32x4_t g4 = s_gb[cc >> 2], b4 = s_gb[K4 + (cc >> 2)];
-#pragma unroll
-        for (int j = 0; j < RPT; ++j) {
-            const int m = rg + RG * j;
-            if (m >= M || rg >= RG) continue;
-            float t1 = 0.f, t2 = 0.f;
-            for (int w = rg * wpg; w < (rg + 1) * wpg; ++w) {
-                const float2 v = s_stat[w][j];
-                t1 += v.x;
-                t2 += v.y;
-            }
-            const float mean = t1 * inv_k;
-            const float var = fmaxf(t2 * inv_k - mean * mean, 0.f);
-            const float rstd = rsqrtf(var + 1e-5f);
-            const float4 x = hv[j];
-            const float y0 = (x.x - mean) * rstd * g4[0] + b4[0];
-            const float y1 = (x.y - mean) * rstd * g4[1] + b4[1];
-            const float y2 = (x.z - mean) * rstd * g4[2] + b4[2];
-            const float y3 = (x.w - mean) * rstd * g4[3] + b4[3];
-            *reinterpret_cast<uint2*>(xs + (size_t)m * ldl + cc) = make_uint2(pack2(y0, y1), pack2(y2, y3));
-        }
+        lr.build(a, blockIdx.x == 0 && blockIdx.y == 0, xs, ldl, red, s_stat, wave, lane);
     }
     __syncthreads();
 
@@ -594,16 +498,16 @@ static hipError_t gemv_part_rows(hipStream_t st, const GemvArgs& a, const EpiPar
 }
 
 // split-K partial producer over merged attention partials (K = d <= 2048)
-template <int MR, int KCH>
+template <int MR, int KCH, int XM = 4>
 static hipError_t gemv_part_merge(hipStream_t st, const GemvArgs& a, const EpiPart& e) {
     constexpr int GS = (16 / (MR * KCH)) > 0 ? 16 / (MR * KCH) : 1;
-    if (a.n_splits <= 8) return gemv_go<MR, 4, 1, KCH, 8>(st, a, 4, e);
+    if (a.n_splits <= 8) return gemv_go<MR, XM, 1, KCH, 8>(st, a, 4, e);
     if constexpr (8 * GS >= 16) {
-        if (a.n_splits <= 16) return gemv_go<MR, 4, 1, KCH, 16>(st, a, 4, e);
+        if (a.n_splits <= 16) return gemv_go<MR, XM, 1, KCH, 16>(st, a, 4, e);
     }
-    if constexpr (8 * GS >= 32) {
-        if (a.n_splits <= 24) return gemv_go<MR, 4, 1, KCH, 24>(st, a, 4, e);
-        if (a.n_splits <= 32) return gemv_go<MR, 4, 1, KCH, 32>(st, a, 4, e);
+    if constexpr (XM == 4 && 8 * GS >= 32) {
+        if (a.n_splits <= 24) return gemv_go<MR, XM, 1, KCH, 24>(st, a, 4, e);
+        if (a.n_splits <= 32) return gemv_go<MR, XM, 1, KCH, 32>(st, a, 4, e);
     }
     return hipErrorInvalidValue;
 }
@@ -625,6 +529,16 @@ hipError_t gemv(hipStream_t st, const GemvArgs& a) {
     if (a.epi == EPI_PARTIAL) {
         if (a.N % 4 || a.K > 4 * 8 * GV_NW * 32) return hipErrorInvalidValue;
         EpiPart e{a.part_out, a.N, a.M, a.h, a.bias};
+        if (a.xmode == 5) {
+            // after qkv_attn: <= 8 rows, d <= 1024, every split word written
+            if (a.M > 8 || a.K > 1024 || a.K % 256 || a.n_splits < 1 || a.Q < 1 || a.M % a.Q ||
+                a.n_splits > gemv_merge_max_splits(a.M, a.K) || a.n_splits > 16 || !a.q || !a.kvnew)
+                return hipErrorInvalidValue;
+            if (a.M <= 1) return gemv_part_merge<1, 1, 5>(st, a, e);
+            if (a.M <= 2) return gemv_part_merge<2, 1, 5>(st, a, e);
+            if (a.M <= 4) return gemv_part_merge<4, 1, 5>(st, a, e);
+            return gemv_part_merge<8, 1, 5>(st, a, e);
+        }
         if (a.xmode == 4) {
             if (a.K > 2048 || a.K % 256 || a.n_splits < 1 || a.Q < 1 ||
                 a.n_splits > gemv_merge_max_splits(a.M, a.K) || a.split_len < 1)

@@ -88,7 +88,8 @@ hipError_t attention_mfma(hipStream_t st, const AttnMfmaArgs& a);
 struct GemvArgs {
     int epi;                   // EPI_QKV, EPI_GELU, EPI_LOGITS (LayerNorm modes), EPI_PARTIAL (split-K x4)
     int xmode;                 // 0 bf16 rows, 1 LN(h + partials + bias), 2 embed + LN, 3 final LN (heads),
-                               // 4 merged attention partials (EPI_PARTIAL only)
+                               // 4 merged attention partials, 5 merged attention partials plus the
+                               // pending chunk's own keys (EPI_PARTIAL only)
     int M, N, K;
     const bf16_t* W;
     const bf16_t* x; int ldx;                       // xmode 0
@@ -104,13 +105,27 @@ struct GemvArgs {
     float* h_out;                                   // completed residual rows, written by workgroup 0 (may be NULL;
                                                     // must not alias h)
     const float* hz;                                // xmode 3: last prefill hidden state
-    const float* apart; int qt, split_len, n_splits;   // xmode 4: attention split partials
+    float* apart; int qt, split_len, n_splits;         // xmode 4, 5: attention split partials (written by qkv_attn)
     const float* bias;
     void* out; int ldo;                             // EPI_GELU / EPI_LOGITS output
     float* part_out;                                // EPI_PARTIAL output [4][M][N]
-    float* q; KVView kv; int d;                     // EPI_QKV
+    float* q; KVView kv; int d;                     // EPI_QKV; xmode 5 reads q ([M][d] fp32)
+    bf16_t* kvnew;                                  // [2][M][d]: the pending rows' keys, then values (bf16),
+                                                    // written by qkv_attn, read by xmode 5
 };
 int gemv_merge_max_splits(int M, int d);
+
+// LN1 + QKV projection + attention of the pending chunk over the cached keys
+// in one launch (B * Q <= 8 rows, bf16, d <= 1024; see qkv_attn.hip).  Reads
+// the GemvArgs of an EPI_QKV launch (xmode 1 or 2) plus apart / qt /
+// split_len / n_splits (workgroups per head) and kvnew.
+hipError_t qkv_attn(hipStream_t st, const GemvArgs& a);
+// Whether qkv_attn serves `rows` decode rows of model width d, cached
+// contexts of at most max_ctx keys, with n_splits workgroups per head.
+bool qkv_attn_ok(int rows, int d, int n_heads, int64_t max_ctx, int n_splits);
+// Keys per split (a multiple of 16) of qkv_attn for contexts of at most
+// max_ctx keys over n_splits workgroups per head.
+int qkv_attn_split_len(int64_t max_ctx, int n_splits);
 
 // Reads `bytes` (a multiple of 16) of `buf` so that earlier data leaves the
 // L2 and last-level caches (measurement only); writes a few words of `buf`.

@@ -335,6 +335,65 @@ def test_valle_batch2_k8_sixteen_rows():
     log(f"valle batch 2: {steps} steps, max logit err {chk.max_err:.3g}, tie-zone {chk.tie_zone}")
 
 
+# Small bf16 decoders for the two fronts of a small-batch decode layer: one
+# launch for LN1, QKV and the attention over the cached keys with 8 or 16
+# workgroups per head (the out-projection then merges the chunk's own keys),
+# or separate QKV and attention launches; MTP_QKV_ATTN selects it per step.
+FRONT_CASES = {
+    # 8 heads (grouped per XCD), 2 ragged sequences of 4 rows, contexts up to ~690 keys
+    "d512_b2_k4": (ModelShape(n_layers=2, d_model=512, n_heads=8, d_ff=1024, k_heads=4, dtype="bf16"),
+                   4, 3, 2, (5, 40), (200, 600)),
+    # 4 heads, one sequence of 2 rows, ~2,100 keys (more than 8 splits of 256 keys: the
+    # 8-workgroup front is not available and falls back to separate launches)
+    "d256_b1_k2": (ModelShape(n_layers=2, d_model=256, n_heads=4, d_ff=512, k_heads=2, dtype="bf16"),
+                   2, 4, 1, (30, 40), (1900, 2000)),
+    # 16 heads, 8 sequences of one row each (K = 1: plain AR decoding)
+    "d1024_b8_k1": (ModelShape(n_layers=1, d_model=1024, n_heads=16, d_ff=2048, k_heads=1, dtype="bf16"),
+                    1, 2, 8, (3, 20), (10, 300)),
+}
+
+
+@pytest.mark.parametrize("front", ["0", "8", "16"])
+@pytest.mark.parametrize("case", sorted(FRONT_CASES))
+def test_decode_fronts_match_the_oracle(case, front, monkeypatch):
+    """Every front of the small-batch decode layer: selection exact at every
+    step, logits within 3e-2 of the float64 oracle at every third step for
+    every sequence (Sec. 3.1 Eq. 1 on the GPU's own history)."""
+    shape, K, top_k, B, phon, ac = FRONT_CASES[case]
+    wl = Workload(f"front_{case}", shape, K=K, top_k=top_k, batch=B, phon_len=phon, ac_len=ac, max_new=48,
+                  eos_min=48)
+    monkeypatch.setenv("MTP_QKV_ATTN", front)
+    log(f"front {front}, {case}: start")
+    steps, emitted, chk = run_teacher_forced(wl, K, top_k, steps_checked=set(range(0, 64, 3)), tol=3e-2)
+    assert steps == math.ceil(wl.max_new / K)
+    assert chk.checked >= B * (steps // 3)
+    log(f"front {front}, {case}: {steps} steps, {chk.checked} oracle checks, max logit err {chk.max_err:.3g}, "
+        f"tie-zone {chk.tie_zone}")
+
+
+def test_fused_front_eager_and_graph_agree(monkeypatch):
+    """The one-launch front gives bit-identical logits eagerly and replayed
+    from a captured graph, step after step."""
+    from paper_2410_13839_amd.binding import MTP_FLAG_NO_GRAPH
+    shape, K, top_k, B, phon, ac = FRONT_CASES["d512_b2_k4"]
+    wl = Workload("front_graph", shape, K=K, top_k=top_k, batch=B, phon_len=phon, ac_len=ac, max_new=48, eos_min=48)
+    monkeypatch.setenv("MTP_QKV_ATTN", "16")
+    w = make_weights(shape)
+    pr = make_prompts(wl)
+    out = []
+    for flags in (0, MTP_FLAG_NO_GRAPH):
+        s = new_session(wl, w, make_logq(), flags=flags)
+        s.prefill(pr.phon, pr.ac)
+        logs = []
+        for _ in range(6):
+            s.step(K, top_k)
+            logs.append(s.logits(K))
+        out.append((s.tokens()[:, :24].copy(), np.stack(logs)))
+        s.close()
+    assert np.array_equal(out[0][0], out[1][0])
+    assert np.array_equal(out[0][1].view(np.uint32), out[1][1].view(np.uint32))
+
+
 def test_valle_b32_batched():
     """32 ragged sequences, K=4 (128 decode rows through the tiled path):
     selection exact for every sequence at every step; logits and tokens of
