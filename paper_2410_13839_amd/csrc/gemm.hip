@@ -24,6 +24,37 @@
 namespace mtp {
 
 // ---------------------------------------------------------------- epilogues
+// An epilogue stores 4 consecutive n of one row m.  Its operands come in
+// three groups, so that a kernel storing many (m, n) issues their loads
+// ahead of its stores:
+//   RowKey  row_key(m)   one per output row (EpiQKV: its sequence and position)
+//   RowPre  row(key)     one per output row (EpiQKV: its cache page, a load
+//                        that depends on the key: all keys of a kernel's rows
+//                        are loaded before any of these)
+//   ColPre  col(n)       one per 4-column group (the biases)
+//   ElemPre elem(m, n)   one per 4 outputs (EpiResid: the residual values)
+//   store(rp, cp, ep, m, n, v, split, nvalid)
+// A load that follows a store it may alias cannot move above it, and vmcnt
+// counts stores as well as loads, so an epilogue that loads inside each
+// store4 waits one full memory round trip per store (32-64 per wave in the
+// large kernel).  The loads take clamped, valid m and n (the callers pass
+// m < M and n < N or the last valid ones); only the stores are guarded.
+// ok(rp) says whether a row is stored at all (EpiQKV: not a padding row);
+// store<true> may assume it is, so that a kernel whose wave holds only such
+// rows issues the same stores on every lane (a lane-dependent branch around
+// a store leaves the compiler unable to count the stores in flight, and it
+// then waits for all of them before the next one).
+struct EpiNoPre {};
+
+template <class Epi>
+__device__ __forceinline__ void epi_store4(const Epi& e, int m, int n, const float (&v)[4], int split, int nvalid) {
+    e.template store<false>(e.row(e.row_key(m)), e.col(n), e.elem(m, n), m, n, v, split, nvalid);
+}
+
+__device__ __forceinline__ uint32_t epi_pk2(float a, float b) {
+    return (uint32_t)f32_to_bf16(a) | ((uint32_t)f32_to_bf16(b) << 16);
+}
+
 template <typename KVT>
 struct EpiQKV {
     float* q;            // [M][d] queries (fp32)
@@ -31,36 +62,47 @@ struct EpiQKV {
     const RowInfo* rows;
     KVView kv;
     int d;
-    __device__ __forceinline__ void store4(int m, int n, const float (&v)[4], int, int) const {
-        const float4 bv = *reinterpret_cast<const float4*>(bias + n);
+    using RowKey = RowInfo;
+    struct RowPre { int page, pos; };        // pos < 0: a padding row (no cache write)
+    using ColPre = float4;
+    using ElemPre = EpiNoPre;
+    __device__ __forceinline__ RowKey row_key(int m) const { return rows[m]; }
+    // the page stays as loaded (nothing computed from it before the stores)
+    __device__ __forceinline__ RowPre row(const RowKey& ri) const {
+        const int pos = max(ri.pos, 0), seq = max(ri.seq, 0);
+        return RowPre{kv.block_table[(size_t)seq * kv.max_pages_per_seq + (pos >> kv.page_shift)], ri.pos};
+    }
+    __device__ __forceinline__ ColPre col(int n) const { return *reinterpret_cast<const float4*>(bias + n); }
+    __device__ __forceinline__ ElemPre elem(int, int) const { return {}; }
+    __device__ __forceinline__ bool ok(const RowPre& rp) const { return rp.pos >= 0; }
+    // every caller's wave holds 16 consecutive columns inside one section
+    // (d is a multiple of 64), so the section is wave-uniform
+    template <bool ROWS_OK>
+    __device__ __forceinline__ void store(const RowPre& rp, const ColPre& bv, const ElemPre&, int m, int n,
+                                          const float (&v)[4], int, int) const {
         const float r0 = v[0] + bv.x, r1 = v[1] + bv.y, r2 = v[2] + bv.z, r3 = v[3] + bv.w;
-        const int sec = (n >= d) + (n >= 2 * d);      // q, k or v (no integer division)
+        const int sec = __builtin_amdgcn_readfirstlane((n >= d) + (n >= 2 * d));   // q, k or v
         if (sec == 0) {
             *reinterpret_cast<float4*>(q + (size_t)m * d + n) = make_float4(r0, r1, r2, r3);
             return;
         }
-        RowInfo ri = rows[m];
-        if (ri.pos < 0) return;
-        int c = n - sec * d;
+        if (!ROWS_OK && rp.pos < 0) return;
+        const int c = n - sec * d;
+        const int slot = rp.pos & (kv.page_size - 1);
+        KVT* blk = reinterpret_cast<KVT*>(kv.pool) + kv_page_block(kv, rp.page, sec - 1, c >> 6);
         if constexpr (sizeof(KVT) == 2) {
-            if (sec == 2) {   // transposed V block
-                bf16_t* vt = reinterpret_cast<bf16_t*>(kv.pool) + kv.vt_offset(ri.seq, ri.pos, c >> 6);
-                const int dim = c & 63;
-                vt[(size_t)(dim + 0) * kv.page_size] = f32_to_bf16(r0);
-                vt[(size_t)(dim + 1) * kv.page_size] = f32_to_bf16(r1);
-                vt[(size_t)(dim + 2) * kv.page_size] = f32_to_bf16(r2);
-                vt[(size_t)(dim + 3) * kv.page_size] = f32_to_bf16(r3);
+            if (sec == 2) {   // transposed V block: [dim][slot]
+                bf16_t* vt = blk + (size_t)(c & 63) * kv.page_size + slot;
+                vt[0] = f32_to_bf16(r0);
+                vt[kv.page_size] = f32_to_bf16(r1);
+                vt[2 * kv.page_size] = f32_to_bf16(r2);
+                vt[3 * kv.page_size] = f32_to_bf16(r3);
                 return;
             }
-        }
-        KVT* dst = reinterpret_cast<KVT*>(kv.pool) + kv.offset(ri.seq, ri.pos, sec - 1, c >> 6) + (c & 63);
-        if constexpr (sizeof(KVT) == 2) {
-            uint2 pk;
-            pk.x = (uint32_t)f32_to_bf16(r0) | ((uint32_t)f32_to_bf16(r1) << 16);
-            pk.y = (uint32_t)f32_to_bf16(r2) | ((uint32_t)f32_to_bf16(r3) << 16);
-            *reinterpret_cast<uint2*>(dst) = pk;
+            *reinterpret_cast<uint2*>(blk + (size_t)slot * MTP_HEAD_DIM + (c & 63)) =
+                make_uint2(epi_pk2(r0, r1), epi_pk2(r2, r3));
         } else {
-            *reinterpret_cast<float4*>(dst) = make_float4(r0, r1, r2, r3);
+            *reinterpret_cast<float4*>(blk + (size_t)slot * MTP_HEAD_DIM + (c & 63)) = make_float4(r0, r1, r2, r3);
         }
     }
 };
@@ -71,15 +113,22 @@ struct EpiGelu {
     const float* bias;
     int ldo;
     int pk;               // bf16 output in fragment order (K = ldo)
-    __device__ __forceinline__ void store4(int m, int n, const float (&v)[4], int, int) const {
-        const float4 bv = *reinterpret_cast<const float4*>(bias + n);
+    using RowKey = EpiNoPre;
+    using RowPre = EpiNoPre;
+    using ColPre = float4;
+    using ElemPre = EpiNoPre;
+    __device__ __forceinline__ RowKey row_key(int) const { return {}; }
+    __device__ __forceinline__ RowPre row(const RowKey&) const { return {}; }
+    __device__ __forceinline__ ColPre col(int n) const { return *reinterpret_cast<const float4*>(bias + n); }
+    __device__ __forceinline__ ElemPre elem(int, int) const { return {}; }
+    __device__ __forceinline__ bool ok(const RowPre&) const { return true; }
+    template <bool ROWS_OK>
+    __device__ __forceinline__ void store(const RowPre&, const ColPre& bv, const ElemPre&, int m, int n,
+                                          const float (&v)[4], int, int) const {
         const float r[4] = {gelu_erf(v[0] + bv.x), gelu_erf(v[1] + bv.y), gelu_erf(v[2] + bv.z), gelu_erf(v[3] + bv.w)};
         OutT* p = out + (pk ? frag_off(m, n, ldo) : (size_t)m * ldo + n);
         if constexpr (sizeof(OutT) == 2) {
-            uint2 pk;
-            pk.x = (uint32_t)f32_to_bf16(r[0]) | ((uint32_t)f32_to_bf16(r[1]) << 16);
-            pk.y = (uint32_t)f32_to_bf16(r[2]) | ((uint32_t)f32_to_bf16(r[3]) << 16);
-            *reinterpret_cast<uint2*>(p) = pk;
+            *reinterpret_cast<uint2*>(p) = make_uint2(epi_pk2(r[0], r[1]), epi_pk2(r[2], r[3]));
         } else {
             *reinterpret_cast<float4*>(p) = make_float4(r[0], r[1], r[2], r[3]);
         }
@@ -90,7 +139,18 @@ struct EpiPartial {
     float* part;          // [split][M][ldo]
     int ldo;
     size_t split_stride;  // elements between splits
-    __device__ __forceinline__ void store4(int m, int n, const float (&v)[4], int split, int) const {
+    using RowKey = EpiNoPre;
+    using RowPre = EpiNoPre;
+    using ColPre = EpiNoPre;
+    using ElemPre = EpiNoPre;
+    __device__ __forceinline__ RowKey row_key(int) const { return {}; }
+    __device__ __forceinline__ RowPre row(const RowKey&) const { return {}; }
+    __device__ __forceinline__ ColPre col(int) const { return {}; }
+    __device__ __forceinline__ ElemPre elem(int, int) const { return {}; }
+    __device__ __forceinline__ bool ok(const RowPre&) const { return true; }
+    template <bool ROWS_OK>
+    __device__ __forceinline__ void store(const RowPre&, const ColPre&, const ElemPre&, int m, int n,
+                                          const float (&v)[4], int split, int) const {
         *reinterpret_cast<float4*>(part + split * split_stride + (size_t)m * ldo + n) =
             make_float4(v[0], v[1], v[2], v[3]);
     }
@@ -103,11 +163,22 @@ struct EpiResid {
     float* h;             // [M][ldh]
     const float* bias;    // [N]
     int ldh;
-    __device__ __forceinline__ void store4(int m, int n, const float (&v)[4], int, int) const {
-        const float4 bv = *reinterpret_cast<const float4*>(bias + n);
-        float4* p = reinterpret_cast<float4*>(h + (size_t)m * ldh + n);
-        const float4 x = *p;
-        *p = make_float4(x.x + (v[0] + bv.x), x.y + (v[1] + bv.y), x.z + (v[2] + bv.z), x.w + (v[3] + bv.w));
+    using RowKey = EpiNoPre;
+    using RowPre = EpiNoPre;
+    using ColPre = float4;
+    using ElemPre = float4;
+    __device__ __forceinline__ RowKey row_key(int) const { return {}; }
+    __device__ __forceinline__ RowPre row(const RowKey&) const { return {}; }
+    __device__ __forceinline__ ColPre col(int n) const { return *reinterpret_cast<const float4*>(bias + n); }
+    __device__ __forceinline__ ElemPre elem(int m, int n) const {
+        return *reinterpret_cast<const float4*>(h + (size_t)m * ldh + n);
+    }
+    __device__ __forceinline__ bool ok(const RowPre&) const { return true; }
+    template <bool ROWS_OK>
+    __device__ __forceinline__ void store(const RowPre&, const ColPre& bv, const ElemPre& x, int m, int n,
+                                          const float (&v)[4], int, int) const {
+        *reinterpret_cast<float4*>(h + (size_t)m * ldh + n) =
+            make_float4(x.x + (v[0] + bv.x), x.y + (v[1] + bv.y), x.z + (v[2] + bv.z), x.w + (v[3] + bv.w));
     }
 };
 
@@ -115,9 +186,24 @@ struct EpiLogits {
     float* out;           // [M][ldo]
     const float* bias;    // [N]
     int ldo;
-    __device__ __forceinline__ void store4(int m, int n, const float (&v)[4], int, int nvalid) const {
+    int N;
+    using RowKey = EpiNoPre;
+    using RowPre = EpiNoPre;
+    using ColPre = float4;
+    using ElemPre = EpiNoPre;
+    __device__ __forceinline__ RowKey row_key(int) const { return {}; }
+    __device__ __forceinline__ RowPre row(const RowKey&) const { return {}; }
+    __device__ __forceinline__ ColPre col(int n) const {
+        return make_float4(bias[min(n, N - 1)], bias[min(n + 1, N - 1)], bias[min(n + 2, N - 1)], bias[min(n + 3, N - 1)]);
+    }
+    __device__ __forceinline__ ElemPre elem(int, int) const { return {}; }
+    __device__ __forceinline__ bool ok(const RowPre&) const { return true; }
+    template <bool ROWS_OK>
+    __device__ __forceinline__ void store(const RowPre&, const ColPre& bv, const ElemPre&, int m, int n,
+                                          const float (&v)[4], int, int nvalid) const {
         float* p = out + (size_t)m * ldo + n;
-        for (int i = 0; i < nvalid; ++i) p[i] = v[i] + bias[n + i];
+        const float b[4] = {bv.x, bv.y, bv.z, bv.w};
+        for (int i = 0; i < nvalid; ++i) p[i] = v[i] + b[i];
     }
 };
 
@@ -197,23 +283,31 @@ __global__ __launch_bounds__(64 * GM_NW) void gemm_med_bf16(const bf16_t* __rest
         }
     }
 
+    // one output item (4 columns of one row) per thread: its epilogue
+    // operands load while the waves' sums go through LDS
+    static_assert(NT * MT * 64 <= 64 * GM_NW, "one epilogue item per thread");
+    const int t = threadIdx.x;
+    const int jm = min(t >> 6, NT * MT - 1), l = t & 63;
+    const int j = jm / MT, mt = jm - j * MT;
+    const int m = m0 + 16 * mt + (l & 15);
+    const int n = (nt0 + j) * 16 + 4 * (l >> 4);
+    const int mc = min(m, M - 1), nc = n < N ? n : ((N - 1) & ~3);
+    const typename Epi::RowPre rp = epi.row(epi.row_key(mc));
+    const typename Epi::ColPre cp = epi.col(nc);
+    const typename Epi::ElemPre ep = epi.elem(mc, nc);
     __shared__ f32x4_t red[GM_NW][NT * MT][64];
 #pragma unroll
-    for (int j = 0; j < NT; ++j)
+    for (int j2 = 0; j2 < NT; ++j2)
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) red[wave][j * MT + mt][lane] = acc[j][mt];
+        for (int mt2 = 0; mt2 < MT; ++mt2) red[wave][j2 * MT + mt2][lane] = acc[j2][mt2];
     __syncthreads();
-    for (int t = threadIdx.x; t < NT * MT * 64; t += 64 * GM_NW) {
-        const int jm = t >> 6, l = t & 63;
-        const int j = jm / MT, mt = jm - j * MT;
+    if (t < NT * MT * 64) {
         f32x4_t s = red[0][jm][l];
 #pragma unroll
         for (int w = 1; w < GM_NW; ++w) s += red[w][jm][l];
-        const int m = m0 + 16 * mt + (l & 15);
-        const int n = (nt0 + j) * 16 + 4 * (l >> 4);
         if (m < M && n < N) {
-            float v[4] = {s[0], s[1], s[2], s[3]};
-            epi.store4(m, n, v, split, min(4, N - n));
+            const float v[4] = {s[0], s[1], s[2], s[3]};
+            epi.template store<false>(rp, cp, ep, m, n, v, split, min(4, N - n));
         }
     }
 }
@@ -460,19 +554,68 @@ __global__ __launch_bounds__(64 * NWV) void gemm_big_bf16(const bf16_t* __restri
             if (2 < nst) issue(s2, 2);
         }
         // epilogue: lane (r, g) of tile (i, j) holds outputs n = 4 g .. 4 g + 3
-        // of weight fragment i, row m = r of activation fragment j
+        // of weight fragment i, row m = r of activation fragment j.  The
+        // rows' operands load once; each column fragment's operands load
+        // while the previous fragment's outputs are stored, so a wave waits
+        // about WFN + 1 memory round trips, not one per store.  A wave whose
+        // outputs all lie inside the product (and whose rows are all stored)
+        // stores without guards.
+        int em[WFM], emc[WFM];
+        typename Epi::RowKey rk[WFM];
+        typename Epi::RowPre rp[WFM];
+        bool rows_ok = true;
+#pragma unroll
+        for (int j = 0; j < WFM; ++j) {
+            em[j] = (em0 + wm * WFM + j) * 16 + r;
+            emc[j] = min(em[j], M - 1);
+            rk[j] = epi.row_key(emc[j]);
+        }
+#pragma unroll
+        for (int j = 0; j < WFM; ++j) rp[j] = epi.row(rk[j]);
+#pragma unroll
+        for (int j = 0; j < WFM; ++j) rows_ok = rows_ok && epi.ok(rp[j]);
+        const bool inside = (em0 + wm * WFM + WFM) * 16 <= M && (en0 + wn * WFN + WFN) * 16 <= N;   // uniform
+        const bool fast = inside && __all(rows_ok);
+        // column operands (biases) go out one fragment ahead; per-output
+        // operands (the residual values) one fragment at a time, after the
+        // previous fragment's stores, for want of registers (the 128 of the
+        // accumulators are still live)
+        typename Epi::ColPre cp[2];
+        typename Epi::ElemPre ep[WFM];
+        auto col_n = [&](int i) {
+            const int n = (en0 + wn * WFN + i) * 16 + 4 * g;
+            return n < N ? n : ((N - 1) & ~3);
+        };
+        auto store_all = [&](auto guarded) {
+            constexpr bool GUARD = decltype(guarded)::value;
+            cp[0] = epi.col(col_n(0));
+#pragma unroll
+            for (int j = 0; j < WFM; ++j) ep[j] = epi.elem(emc[j], col_n(0));
+#pragma unroll
+            for (int i = 0; i < WFN; ++i) {
+                if (i + 1 < WFN) cp[(i + 1) & 1] = epi.col(col_n(i + 1));
+                const int n = (en0 + wn * WFN + i) * 16 + 4 * g;
+#pragma unroll
+                for (int j = 0; j < WFM; ++j) {
+                    const float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+                    if (!GUARD) {
+                        epi.template store<true>(rp[j], cp[i & 1], ep[j], em[j], n, v, split, 4);
+                    } else if (em[j] < M && n < N) {
+                        epi.template store<false>(rp[j], cp[i & 1], ep[j], em[j], n, v, split, min(4, N - n));
+                    }
+                }
+                if (i + 1 < WFN) {
+#pragma unroll
+                    for (int j = 0; j < WFM; ++j) ep[j] = epi.elem(emc[j], col_n(i + 1));
+                }
+            }
+        };
+        if (fast) store_all(std::false_type{});
+        else store_all(std::true_type{});
 #pragma unroll
         for (int i = 0; i < WFN; ++i)
 #pragma unroll
-            for (int j = 0; j < WFM; ++j) {
-                const int n = (en0 + wn * WFN + i) * 16 + 4 * g;
-                const int m = (em0 + wm * WFM + j) * 16 + r;
-                if (m < M && n < N) {
-                    float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
-                    epi.store4(m, n, v, split, min(4, N - n));
-                }
-                acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-            }
+            for (int j = 0; j < WFM; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
         if (!more) break;
         t = t_next;
     }
@@ -539,7 +682,7 @@ __global__ __launch_bounds__(256) void gemm_f32(const float* __restrict__ X, int
         __syncthreads();
     }
     const int m = m0 + mi, n = n0 + n4 * 4;
-    if (m < M && n < N) epi.store4(m, n, acc, split, min(4, N - n));
+    if (m < M && n < N) epi_store4(epi, m, n, acc, split, min(4, N - n));
 }
 
 // ------------------------------------------------------------------ launchers
@@ -644,7 +787,7 @@ hipError_t gemm(hipStream_t st, const GemmArgs& a) {
         return launch_bf16(st, (const bf16_t*)a.X, a.ldx, a.M, (const bf16_t*)a.W, a.N, a.K, 1, a.xpk, e);
     }
     case EPI_LOGITS: {
-        EpiLogits e{(float*)a.out, a.bias, a.ldo};
+        EpiLogits e{(float*)a.out, a.bias, a.ldo, a.N};
         if (bf) return launch_bf16(st, (const bf16_t*)a.X, a.ldx, a.M, (const bf16_t*)a.W, a.N, a.K, 1, a.xpk, e);
         return launch_f32(st, (const float*)a.X, a.ldx, a.M, (const float*)a.W, a.N, a.K, 1, e);
     }
