@@ -50,6 +50,10 @@ def _parse():
                     help="only one workload's generation line (tiny, valle_k4, valle_k8, valle_b32, long_b8)")
     ap.add_argument("--batched-only", action="store_true",
                     help="only the batched decode kernel classes against their roofline ceilings")
+    ap.add_argument("--batched-workloads", default="valle_b32,long_b8",
+                    help="comma-separated workloads of --batched-only")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="--batched-only: decode steps launched eagerly instead of replayed graphs")
     ap.add_argument("--peaks-only", action="store_true", help="only the copy and library-GEMM figures")
     ap.add_argument("--qest-only", action="store_true",
                     help="only the transition-table estimation figures (one JSON line of them)")
@@ -380,7 +384,7 @@ BATCHED_CLASSES = {3: "QKV (gemm_med_bf16<EpiQKV>)", 4: "attention (attn_dec_ker
                    2: "FFN2 (gemm_med_bf16<EpiPartial>)", 8: "residual + LayerNorm (resid_ln_kernel)"}
 
 
-def bench_batched_kernels(torch, name, weights_cache, logq, passes):
+def bench_batched_kernels(torch, name, weights_cache, logq, passes, flags=0):
     """Per kernel class of a batched decode step (mid-generation): average
     launch time from cold replays (caches evicted before each pass), the
     achieved TFLOP/s and GB/s, and the fraction of the class's own roofline
@@ -393,7 +397,7 @@ def bench_batched_kernels(torch, name, weights_cache, logq, passes):
         weights_cache[wl.model] = make_weights(wl.model)
     pr = make_prompts(wl)
     s = Session(wl.model, weights_cache[wl.model], logq, max_batch=wl.batch, max_prompt=wl.max_prompt,
-                max_new=wl.max_new, eos_min=wl.eos_min, topk_max=max(8, wl.top_k))
+                max_new=wl.max_new, eos_min=wl.eos_min, topk_max=max(8, wl.top_k), flags=flags)
     mid = _steps_per_generation(wl) // 2
     s.prefill(pr.phon, pr.ac)
     for _ in range(mid):
@@ -597,9 +601,11 @@ def main():
         print(json.dumps(bench_config(torch, args.config_only, {}, make_logq())))
         return
     if args.batched_only:
+        from paper_2410_13839_amd.binding import MTP_FLAG_NO_GRAPH
         wc, lq = {}, make_logq()
-        print(json.dumps({n: bench_batched_kernels(torch, n, wc, lq, args.replay_passes)
-                          for n in ("valle_b32", "long_b8")}))
+        fl = MTP_FLAG_NO_GRAPH if args.no_graph else 0
+        print(json.dumps({n: bench_batched_kernels(torch, n, wc, lq, args.replay_passes, fl)
+                          for n in args.batched_workloads.split(",")}))
         return
     if args.peaks_only:
         print(json.dumps(bench_peaks(torch)))

@@ -68,7 +68,7 @@ struct EpiQKVDec {
         p.pl = s.pend_len;
         return p;
     }
-    __device__ __forceinline__ void store(const Pre& p, int m, int n, const float (&v)[4], int) const {
+    __device__ __forceinline__ void store(const Pre& p, int m, int n, const float (&v)[4], int, int) const {
         const float r0 = v[0] + p.b[0], r1 = v[1] + p.b[1], r2 = v[2] + p.b[2], r3 = v[3] + p.b[3];
         if (n < d) {
             *reinterpret_cast<float4*>(q + (size_t)m * d + n) = make_float4(r0, r1, r2, r3);
@@ -104,7 +104,7 @@ struct EpiGeluB {
         for (int i = 0; i < 4; ++i) p.b[i] = bias[n + i];
         return p;
     }
-    __device__ __forceinline__ void store(const Pre& p, int m, int n, const float (&v)[4], int) const {
+    __device__ __forceinline__ void store(const Pre& p, int m, int n, const float (&v)[4], int, int) const {
         float r[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) r[i] = gelu_erf(v[i] + p.b[i]);
@@ -129,15 +129,15 @@ struct EpiPart {
         p.x = *reinterpret_cast<const float4*>(h + (size_t)m * ldp + nn);
         return p;
     }
-    __device__ __forceinline__ void store(const Pre& p, int m, int n, const float (&v)[4], int) const {
+    __device__ __forceinline__ void store(const Pre& p, int m, int n, const float (&v)[4], int, int split) const {
         float4 o = make_float4(v[0], v[1], v[2], v[3]);
-        if (blockIdx.y == 0) {
+        if (split == 0) {
             o.x += p.b.x + p.x.x;
             o.y += p.b.y + p.x.y;
             o.z += p.b.z + p.x.z;
             o.w += p.b.w + p.x.w;
         }
-        *reinterpret_cast<float4*>(part + ((size_t)blockIdx.y * M + m) * ldp + n) = o;
+        *reinterpret_cast<float4*>(part + ((size_t)split * M + m) * ldp + n) = o;
     }
 };
 
@@ -153,7 +153,7 @@ struct EpiLogitsB {
         for (int i = 0; i < 4; ++i) p.b[i] = bias[min(n + i, N - 1)];
         return p;
     }
-    __device__ __forceinline__ void store(const Pre& p, int m, int n, const float (&v)[4], int nvalid) const {
+    __device__ __forceinline__ void store(const Pre& p, int m, int n, const float (&v)[4], int nvalid, int) const {
         float* o = out + (size_t)m * ldo + n;
 #pragma unroll
         for (int i = 0; i < 4; ++i)
@@ -204,8 +204,19 @@ __global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int r = lane & 15, g = lane >> 4;
-    const int n0 = blockIdx.x * 16;
-    const int S = gridDim.y, split = blockIdx.y;
+    // Split-K launches (four K ranges): workgroup j takes K range j % 4 and
+    // column tile j / 4, so that (the dispatcher dealing workgroups to the 8
+    // XCDs in turn) each K range's workgroups share two XCDs, whose L2s then
+    // hold only that range's activations (the out-projection's attention
+    // split words of its four heads, FFN2's hidden columns) instead of all.
+    const int S = gridDim.y;
+    int tile = blockIdx.x, split = blockIdx.y;
+    if (S == 4) {
+        const int j = blockIdx.x + gridDim.x * blockIdx.y;
+        tile = j >> 2;
+        split = j & 3;
+    }
+    const int n0 = tile * 16;
     const int K = a.K, M = a.M, N = a.N;
     const int ks = K / S;                         // this workgroup's K range
     const int kb = split * ks;
@@ -301,7 +312,7 @@ __global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
 
     // ---- B. weights of this workgroup's 16 columns, all in flight: in the
     //      packed fragment order one 1 KB fragment per wave load ----
-    const bf16_t* wp = a.W + ((size_t)blockIdx.x * (K >> 5) + (kb >> 5)) * 512 + lane * 8;
+    const bf16_t* wp = a.W + ((size_t)tile * (K >> 5) + (kb >> 5)) * 512 + lane * 8;
     uint4 wv[MAXF];
 #pragma unroll
     for (int i = 0; i < MAXF; ++i) {
@@ -430,7 +441,7 @@ __global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
             *reinterpret_cast<uint2*>(xs + (size_t)m * ldl + (c - kb)) = y;
         }
     } else {
-        lr.build(a, blockIdx.x == 0 && blockIdx.y == 0, xs, ldl, red, s_stat, wave, lane);
+        lr.build(a, tile == 0 && split == 0, xs, ldl, red, s_stat, wave, lane);
     }
     __syncthreads();
 
@@ -452,7 +463,7 @@ __global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
 #pragma unroll
         for (int w = 1; w < NW; ++w) sum += red[w * 64 + lane];
         const float v[4] = {sum[0], sum[1], sum[2], sum[3]};
-        epi.store(pre, em, en, v, envalid);
+        epi.store(pre, em, en, v, envalid, split);
     }
 }
 
