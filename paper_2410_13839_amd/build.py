@@ -9,6 +9,7 @@ from concurrent.futures import ThreadPoolExecutor
 PKG = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libmtp.so")
+PROBE_LIB = os.path.join(PKG, "libmtp_probe.so")
 SOURCES = ["api.hip", "gemm.hip", "gemv.hip", "attention.hip", "attn_mfma.hip", "rowops.hip", "select.hip", "qest.hip",
            "qkv_attn.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -40,8 +41,16 @@ def build(verbose: bool = True) -> str:
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stderr}")
     os.replace(tmp, LIB)
+    # measurement probes: a library of their own (the decode library never runs them)
+    pobj = _compile("probe.hip", obj_dir)
+    ptmp = PROBE_LIB + ".tmp"
+    r = subprocess.run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", pobj, "-o", ptmp], capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"probe link failed:\n{r.stderr}")
+    os.replace(ptmp, PROBE_LIB)
     if verbose:
         print(f"built {LIB}")
+        print(f"built {PROBE_LIB}")
     return LIB
 
 

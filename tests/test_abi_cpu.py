@@ -227,3 +227,13 @@ def test_q_estimation_validates_before_gpu_work():
         with pytest.raises(b.MTPError) as e:
             b.mtp_q_normalize(**args)
         assert e.value.code == b.MTP_EINVAL, (k, v)
+
+
+def test_probe_library_exports():
+    """The measurement-probe library is built beside libmtp.so and exports
+    its three entry points (no GPU call is made)."""
+    import ctypes
+    from paper_2410_13839_amd.probe import LIB_PATH
+    lib = ctypes.CDLL(LIB_PATH)
+    for name in ("mtp_probe_launch_floor", "mtp_probe_stream", "mtp_probe_flag_barrier"):
+        assert hasattr(lib, name), name
