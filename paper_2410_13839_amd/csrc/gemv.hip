@@ -49,6 +49,12 @@ __device__ __forceinline__ uint32_t pack2(float a, float b) {
 }
 
 // ---------------------------------------------------------------- epilogues
+// Epilogue operands load in two steps: early(m) with the activation loads
+// (phase A: it arrives before the weights), prefetch(early, m, n) after the
+// weight loads, so operands that depend on early ones (the cache page of a
+// key) arrive with the weights instead of one round trip after the product.
+struct EpiNoEarly {};
+
 // QKV of decode rows: row m = (seq m / Q, pending index m % Q).  K rows are
 // 4 consecutive dims of one key; V goes to the transposed block (4 dims of one
 // key, page_size elements apart).
@@ -58,14 +64,22 @@ struct EpiQKVDec {
     const SeqState* st;
     KVView kv;
     int d, Q;
-    struct Pre { float b[4]; int ctx, pl; };
-    __device__ __forceinline__ Pre prefetch(int m, int n, int) const {
+    using Early = int2;      // the row's sequence's (ctx_len, pend_len)
+    struct Pre { float b[4]; int page, slot; bool ok; };
+    __device__ __forceinline__ Early early(int m) const {
+        return *reinterpret_cast<const int2*>(&st[udiv_small(m, Q)]);
+    }
+    __device__ __forceinline__ Pre prefetch(const Early& e, int m, int n, int) const {
         Pre p;
 #pragma unroll
         for (int i = 0; i < 4; ++i) p.b[i] = bias[n + i];
-        const SeqState& s = st[udiv_small(m, Q)];
-        p.ctx = s.ctx_len;
-        p.pl = s.pend_len;
+        // the page of the row's key (K and V^T share it); the index is
+        // clamped to the block table for rows that store nothing
+        const int seq = udiv_small(m, Q), i = m - seq * Q;
+        const int pos = e.x + i;
+        p.ok = i < e.y;
+        p.slot = pos & (kv.page_size - 1);
+        p.page = kv.block_table[(size_t)seq * kv.max_pages_per_seq + min(pos >> kv.page_shift, kv.max_pages_per_seq - 1)];
         return p;
     }
     __device__ __forceinline__ void store(const Pre& p, int m, int n, const float (&v)[4], int, int) const {
@@ -74,16 +88,14 @@ struct EpiQKVDec {
             *reinterpret_cast<float4*>(q + (size_t)m * d + n) = make_float4(r0, r1, r2, r3);
             return;
         }
-        const int seq = udiv_small(m, Q), i = m - seq * Q;
-        if (i >= p.pl) return;
-        const int pos = p.ctx + i;
+        if (!p.ok) return;
         const int c = (n < 2 * d) ? n - d : n - 2 * d;
         bf16_t* pool = reinterpret_cast<bf16_t*>(kv.pool);
         if (n < 2 * d) {
-            bf16_t* dst = pool + kv.offset(seq, pos, 0, c >> 6) + (c & 63);
+            bf16_t* dst = pool + kv_page_block(kv, p.page, 0, c >> 6) + (size_t)p.slot * MTP_HEAD_DIM + (c & 63);
             *reinterpret_cast<uint2*>(dst) = make_uint2(pack2(r0, r1), pack2(r2, r3));
         } else {
-            bf16_t* dst = pool + kv.vt_offset(seq, pos, c >> 6) + (size_t)(c & 63) * kv.page_size;
+            bf16_t* dst = pool + kv_page_block(kv, p.page, 1, c >> 6) + (size_t)(c & 63) * kv.page_size + p.slot;
             const size_t P = kv.page_size;
             dst[0] = f32_to_bf16(r0);
             dst[P] = f32_to_bf16(r1);
@@ -97,8 +109,10 @@ struct EpiGeluB {
     bf16_t* out;
     const float* bias;
     int ldo;
+    using Early = EpiNoEarly;
     struct Pre { float b[4]; };
-    __device__ __forceinline__ Pre prefetch(int, int n, int) const {
+    __device__ __forceinline__ Early early(int) const { return {}; }
+    __device__ __forceinline__ Pre prefetch(const Early&, int, int n, int) const {
         Pre p;
 #pragma unroll
         for (int i = 0; i < 4; ++i) p.b[i] = bias[n + i];
@@ -121,8 +135,10 @@ struct EpiPart {
     int M;
     const float* h;      // residual rows [M][N] entering the projection
     const float* bias;   // [N]
+    using Early = EpiNoEarly;
     struct Pre { float4 b, x; };
-    __device__ __forceinline__ Pre prefetch(int m, int n, int) const {
+    __device__ __forceinline__ Early early(int) const { return {}; }
+    __device__ __forceinline__ Pre prefetch(const Early&, int m, int n, int) const {
         Pre p;
         const int nn = min(n, ldp - 4);
         p.b = *reinterpret_cast<const float4*>(bias + nn);
@@ -146,8 +162,10 @@ struct EpiLogitsB {
     const float* bias;
     int ldo;
     int N;
+    using Early = EpiNoEarly;
     struct Pre { float b[4]; };
-    __device__ __forceinline__ Pre prefetch(int, int n, int) const {
+    __device__ __forceinline__ Early early(int) const { return {}; }
+    __device__ __forceinline__ Pre prefetch(const Early&, int, int n, int) const {
         Pre p;
 #pragma unroll
         for (int i = 0; i < 4; ++i) p.b[i] = bias[min(n + i, N - 1)];
@@ -305,6 +323,9 @@ __global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
         lr.load(a);
     }
 
+    // the epilogue's early operands (the sequence state of the lane's row)
+    const typename Epi::Early early = epi.early(min(r, M - 1));
+
     // Every wave's activation loads go out before any weight load: a CU
     // returns load data in request order, so an activation load queued behind
     // another wave's weight loads (HBM misses) would wait for them.
@@ -323,7 +344,7 @@ __global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
     const int em = r;
     const int en = n0 + 4 * g;
     const int envalid = min(4, N - en);
-    const typename Epi::Pre pre = epi.prefetch(min(em, M - 1), min(en, N - 1), envalid);
+    const typename Epi::Pre pre = epi.prefetch(early, min(em, M - 1), min(en, N - 1), envalid);
     // every load above is issued before any of the prologue below may be
     // scheduled (the compiler otherwise sinks weight loads under the merge
     // arithmetic, serialising two memory round trips)
