@@ -107,6 +107,7 @@ def time_decode(sess, wl, prompts, steps, warmup, torch, top_k=None):
 
 
 KCLASSES = {  # kernel class -> (name, launches per decode step as a function of layers)
+    10: ("LN1 + QKV + decode attention, one launch (qkv_front_kernel)", lambda L: L),
     9: ("LN1 + QKV + attention over the cached keys (qkv_attn_kernel)", lambda L: L),
     4: ("attention (attn_dec_kernel)", lambda L: L),
     3: ("QKV projection (gemv_kernel<EpiQKVDec>)", lambda L: L),
@@ -133,7 +134,7 @@ def launch_bytes(wl, kclass, ctx):
         return B * (ctx + K) * 2 * d * 2 + M * d * 4 + M * d * 2
     if kclass == 3:
         return 3 * d * d * 2 + 3 * d * 4 + M * d * 4 + 2 * d * 4 + M * d * 4 + 2 * M * d * 2
-    if kclass == 9:   # the QKV projection, the cached K and V rows of every head, the attention output
+    if kclass in (9, 10):   # the QKV projection, the cached K and V rows of every head, the attention output
         return launch_bytes(wl, 3, ctx) + B * ctx * 2 * d * 2 + M * d * 2
     if kclass == 1:
         return f * d * 2 + f * 4 + 2 * M * d * 4 + 2 * d * 4 + M * f * 2
@@ -147,10 +148,10 @@ def launch_bytes(wl, kclass, ctx):
 
 
 KCLASS_SOURCES = {  # kernel class -> the sources its kernels are built from
-    4: ("attn_mfma.hip", "common.h", "launch.h"),
+    4: ("attn_mfma.hip", "attn_dec.h", "common.h", "launch.h", "wave.h"),
     9: ("qkv_attn.hip", "ln_rows.h", "common.h", "launch.h", "wave.h"),
 }
-GEMV_SOURCES = ("gemv.hip", "ln_rows.h", "common.h", "launch.h", "wave.h")
+GEMV_SOURCES = ("gemv.hip", "attn_dec.h", "ln_rows.h", "common.h", "launch.h", "wave.h")
 
 
 def kernel_source_digest(kclass):

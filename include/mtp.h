@@ -316,6 +316,9 @@ int mtp_get_tokens(mtp_ctx* ctx, int32_t* tokens);
 #define MTP_KCLASS_RESID_LN    8   /* residual + LayerNorm rows (batched path, two per layer) */
 #define MTP_KCLASS_QKV_ATTN    9   /* LN1 -> x W_qkv^T, K/V into the cache, attention over the
                                       cached keys, in one launch (B * K <= 8 rows, d <= 1024) */
+#define MTP_KCLASS_QKV_FRONT  10   /* LN1 -> x W_qkv^T, K/V into the cache, then the decode
+                                      attention, in one launch whose attention workgroups wait
+                                      for their head's QKV columns (B * K <= 16 rows) */
 int mtp_profile_replay(mtp_ctx* ctx, int kclass, int iters, void* flush_buf, uint64_t flush_bytes,
                        double* avg_us);
 

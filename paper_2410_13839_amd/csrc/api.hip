@@ -128,7 +128,8 @@ int validate(const mtp_config* c, std::string* why) {
 }
 
 struct WsLayout {
-    uint64_t rows, ids, tiles, last_row, state, btab, h, q, u, attn, ffn, part, apart, kvnew, hz, z, logits, cand, ehat,
+    uint64_t rows, ids, tiles, last_row, state, btab, h, q, qh, u, attn, ffn, part, apart, kvnew, fsync, hz, z, logits,
+        cand, ehat,
         u_states, u_m, u_ehat, u_delta, u_psi, smp_cfg, smp_u, codes, tgt_rows, nar_logits,
         delta, psi, slots, out_tok, out_cnt, hist, total;
     int64_t m_pre, m_dec, m_max, max_tiles, max_splits, maxp, num_pages;
@@ -171,6 +172,12 @@ WsLayout ws_layout(const mtp_config& c) {
     w.part = take(std::max(w.m_pre * 4, w.m_dec * (int64_t)MTP_SPLITK_MAX) * d * 4);
     w.apart = take(B * H * w.max_splits * MTP_ATTN_QT * 68 * 4);
     w.kvnew = take(front ? 2 * w.m_dec * d * 2 : 0);   // the pending rows' keys and values (bf16)
+    // the chained front (qkv_front): its bf16 queries, and its hand-off
+    // words (three sets of one flag per QKV column tile, a wait-overrun
+    // count and the dealing check)
+    const bool chain = c.dtype == MTP_DTYPE_BF16 && !is_nar(c);
+    w.qh = take(chain ? w.m_dec * d * 2 : 0);
+    w.fsync = take(chain ? (3 * (3 * d / 16) + 2) * 4 : 0);
     w.hz = take(B * d * 4);
     w.z = take((B + 15) / 16 * 16 * d * w.act_bytes);
     w.logits = take(B * KH * V * 4);
@@ -216,7 +223,10 @@ struct mtp_ctx {
     int q_pad = 0;               // pending rows per sequence for the next step
     int last_K = 0, last_topk = 0, last_lattice = 0, last_sample = 0;
     int split_len = 64, n_splits = 1;
-    bool front_fused = false;    // the step's layers start with one qkv_attn launch (small batches)
+    // how a small batch's layers start: 0 QKV and attention launches, 1 one
+    // qkv_attn launch (on request), 2 one qkv_front launch
+    int front = 0;
+    int xcd_deal = -1;           // workgroup j runs on XCD j % 8: -1 not yet checked, 0 no, 1 yes
     int lattice = MTP_LATTICE_OWN, anchored = 0;   // selection options (mtp_set_selection)
     int sample = 0;              // mtp_set_sampling: draw the path instead of the best one
     SampleCfg h_smp{0, 1.0f, 0}; // copied to the workspace before the next step when dirty
@@ -231,13 +241,13 @@ struct mtp_ctx {
     std::vector<int2> h_tiles;
     std::vector<SeqState> h_state;
     int n_pre_rows = 0, n_pre_tiles = 0;
-    // graphs keyed by (K, top_k, q_pad, batch, split_len, n_splits, lattice, anchored, sampling, fused front)
+    // graphs keyed by (K, top_k, q_pad, batch, split_len, n_splits, lattice, anchored, sampling, front)
     using StepKey = std::tuple<int, int, int, int, int, int, int, int, int, int>;
     std::map<StepKey, hipGraphExec_t> graphs;
     // every launch of each kernel class in the step of a key (arguments
     // captured by value), for replay timing
     using Launch = std::function<hipError_t(hipStream_t)>;
-    struct StepLaunches { std::vector<Launch> cls[MTP_KCLASS_QKV_ATTN + 1]; };
+    struct StepLaunches { std::vector<Launch> cls[MTP_KCLASS_QKV_FRONT + 1]; };
     std::map<StepKey, StepLaunches> step_launches;
     StepLaunches* recording = nullptr;
     StepKey last_key{};
@@ -289,7 +299,7 @@ int pick_splits(const mtp_ctx* c, int M, int N, int K) {
 // Launch through `f` and, while a step is being recorded, keep it under class `kclass`.
 hipError_t launch_rec(mtp_ctx* c, int kclass, std::function<hipError_t(hipStream_t)> f) {
     hipError_t e = f(c->stream);
-    if (kclass > 0 && kclass <= MTP_KCLASS_QKV_ATTN && c->recording) c->recording->cls[kclass].push_back(std::move(f));
+    if (kclass > 0 && kclass <= MTP_KCLASS_QKV_FRONT && c->recording) c->recording->cls[kclass].push_back(std::move(f));
     return e;
 }
 
@@ -350,13 +360,34 @@ int run_layer_fused(mtp_ctx* c, int l, int rows, int qt) {
     g.bias = (const float*)c->lt(l, MTP_T_B_QKV); g.q = c->ws_ptr<float>(c->ws.q); g.kv = c->kv(l); g.d = d;
     bf16_t* kvnew = c->ws_ptr<bf16_t>(c->ws.kvnew);
     bool pm;
-    if (c->front_fused) {
+    if (c->front == 1) {
         // LN1 + QKV + attention over the cached keys in one launch; the
         // out-projection merges the splits and the chunk's own keys
         g.apart = c->ws_ptr<float>(c->ws.apart); g.qt = qt; g.split_len = c->split_len; g.n_splits = c->n_splits;
         g.kvnew = kvnew;
         HIPCHK(c, launch_rec(c, MTP_KCLASS_QKV_ATTN, [g](hipStream_t s) { return qkv_attn(s, g); }), "qkv + attention");
         pm = true;
+    } else if (c->front == 2) {
+        // LN1 + QKV, then the decode attention of each head as soon as its
+        // columns are stored, in one launch
+        pm = prologue_merge(c, rows);
+        AttnDecArgs da = dec_attn_args(c, l, qt);
+        AttnMfmaArgs m{};
+        m.mode = 0; m.n_tiles = c->B; m.Q = c->q_pad; m.qt = qt; m.st = da.st;
+        m.q = da.q; m.ldq = da.ldq; m.kv = da.kv; m.split_len = da.split_len; m.n_splits = da.n_splits;
+        m.out = (bf16_t*)da.out; m.ldo = da.ldo; m.part = da.part; m.packed = 0;
+        m.qh = g.qh = c->ws_ptr<bf16_t>(c->ws.qh);
+        // flag sets: consecutive launches (layer order, then the next step's
+        // layer 0) alternate sets 0 and 1; with an odd layer count the last
+        // layer takes set 2
+        const int L = cf.n_layers, nf = 3 * (d / 16);
+        auto set_of = [L](int i) { return (L % 2 == 1 && i == L - 1) ? 2 : i % 2; };
+        FrontSync fs{};
+        unsigned* fw = c->ws_ptr<unsigned>(c->ws.fsync);
+        fs.flags = fw + set_of(l) * nf; fs.next_flags = fw + set_of((l + 1) % L) * nf; fs.err = fw + 3 * nf;
+        fs.tiles_per_mat = d / 16; fs.per_head = c->B * c->n_splits;
+        HIPCHK(c, launch_rec(c, MTP_KCLASS_QKV_FRONT, [g, m, fs](hipStream_t s) { return qkv_front(s, g, m, fs); }),
+               "qkv + attention front");
     } else {
         HIPCHK(c, launch_rec(c, MTP_KCLASS_GEMM_QKV, [g](hipStream_t s) { return gemv(s, g); }), "qkv gemv");
         pm = prologue_merge(c, rows);
@@ -364,7 +395,7 @@ int run_layer_fused(mtp_ctx* c, int l, int rows, int qt) {
     }
 
     g = GemvArgs{};
-    g.epi = EPI_PARTIAL; g.xmode = c->front_fused ? 5 : pm ? 4 : 0; g.M = rows; g.N = d; g.K = d;
+    g.epi = EPI_PARTIAL; g.xmode = c->front == 1 ? 5 : pm ? 4 : 0; g.M = rows; g.N = d; g.K = d;
     g.W = (const bf16_t*)c->lt(l, MTP_T_W_O); g.x = (const bf16_t*)(c->WS() + c->ws.attn); g.ldx = d;
     g.st = c->ws_ptr<SeqState>(c->ws.state); g.Q = c->q_pad;
     g.apart = c->ws_ptr<float>(c->ws.apart); g.qt = qt; g.split_len = c->split_len; g.n_splits = c->n_splits;
@@ -589,15 +620,66 @@ int plan_splits(mtp_ctx* c, int Q) {
     // so the launch takes about as long as the two it replaces (10.7 vs
     // 5.97 + 5.13 us at batch 1, K = 4) and the out-projection's merge of
     // the chunk's own keys adds ~1 us (323 vs 312 us per step)
-    c->front_fused = false;
+    c->front = 0;
     if (cf.dtype == MTP_DTYPE_BF16 && Q > 0 && !(cf.flags & MTP_FLAG_NAR)) {
         int G = 0;
         if (const char* env = getenv("MTP_QKV_ATTN")) G = atoi(env);
         if ((G == 8 || G == 16) && G <= c->ws.max_splits && G <= merge_max &&
             qkv_attn_ok((int)rows, cf.d_model, cf.n_heads, max_ctx, G)) {
-            c->front_fused = true;
+            c->front = 1;
             c->split_len = qkv_attn_split_len(max_ctx, G);
             c->n_splits = G;
+            return MTP_OK;
+        }
+    }
+    // small batches: QKV and the decode attention in one launch whose
+    // attention workgroups wait for their own head's columns (qkv_front).
+    // Keys per split: 256 (one 16-key group per wave of 16), or 512 when
+    // that keeps every workgroup of the launch resident at once (one per
+    // CU) or the splits within what the out-projection merges.  At least two
+    // layers: consecutive launches alternate their hand-off flag sets.
+    const char* fenv = getenv("MTP_FRONT");
+    if (cf.dtype == MTP_DTYPE_BF16 && Q > 0 && !(cf.flags & MTP_FLAG_NAR) && rows <= 16 && cf.n_layers >= 2 &&
+        !(fenv && atoi(fenv) == 0)) {
+        int n_cu = 0, dev = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+            n_cu = 0;
+        const int hpx = cf.n_heads / 8;
+        int pick = 0;
+        for (int sl2 : {256, 512}) {
+            const int64_t n = (max_ctx + sl2 - 1) / sl2;
+            if (n > c->ws.max_splits || (n > 1 && n > merge_max) ||
+                !qkv_front_ok((int)rows, cf.d_model, cf.n_heads, (int)B, sl2, (int)n))
+                continue;
+            if (!pick) pick = sl2;
+            if (8 * hpx * (12 + B * n) <= n_cu) { pick = sl2; break; }
+        }
+        if (fenv && (atoi(fenv) == 256 || atoi(fenv) == 512)) {
+            const int sl2 = atoi(fenv);
+            const int64_t n = (max_ctx + sl2 - 1) / sl2;
+            pick = (n <= c->ws.max_splits && (n == 1 || n <= merge_max) &&
+                    qkv_front_ok((int)rows, cf.d_model, cf.n_heads, (int)B, sl2, (int)n)) ? sl2 : 0;
+        }
+        if (pick && c->xcd_deal < 0) {
+            // once per context, outside any capture: the hand-off words
+            // start at zero, and the front needs workgroup j on XCD j % 8
+            unsigned* fw = c->ws_ptr<unsigned>(c->ws.fsync);
+            unsigned* bad = fw + 3 * (3 * cf.d_model / 16) + 1;
+            const size_t fbytes = (size_t)(3 * (3 * cf.d_model / 16) + 2) * 4;
+            unsigned h_bad = 1;
+            HIPCHK(c, hipMemsetAsync(fw, 0, fbytes, c->stream), "front hand-off words");
+            const int64_t n = (max_ctx + pick - 1) / pick;
+            HIPCHK(c, xcd_deal_check(c->stream, bad, (int)(8 * hpx * (12 + B * n))), "dealing check");
+            HIPCHK(c, hipMemcpyAsync(&h_bad, bad, 4, hipMemcpyDeviceToHost, c->stream), "dealing check");
+            HIPCHK(c, hipStreamSynchronize(c->stream), "dealing check");
+            HIPCHK(c, hipMemsetAsync(bad, 0, 4, c->stream), "dealing check");
+            c->xcd_deal = h_bad == 0 ? 1 : 0;
+        }
+        if (pick && c->xcd_deal == 1) {
+            c->front = 2;
+            c->split_len = pick;
+            c->n_splits = (int)((max_ctx + pick - 1) / pick);
             return MTP_OK;
         }
     }
@@ -643,7 +725,7 @@ int step_common(mtp_ctx* c, int K, int top_k) {
         c->smp_dirty = false;
     }
     const auto key = std::make_tuple(K, top_k, c->q_pad, c->B, c->split_len, c->n_splits, c->lattice, c->anchored,
-                                     c->sample, c->front_fused ? 1 : 0);
+                                     c->sample, c->front);
     auto record = [&]() {
         mtp_ctx::StepLaunches& sl = c->step_launches[key];
         for (auto& v : sl.cls) v.clear();
@@ -1199,7 +1281,7 @@ int mtp_profile_replay(mtp_ctx* c, int kclass, int iters, void* flush_buf, uint6
         return MTP_EINVAL;
     }
     const bool cold = flush_buf != nullptr;
-    if (kclass < MTP_KCLASS_GEMM_FFN1 || kclass > MTP_KCLASS_QKV_ATTN) { c->err = "unknown kernel class"; return MTP_EINVAL; }
+    if (kclass < MTP_KCLASS_GEMM_FFN1 || kclass > MTP_KCLASS_QKV_FRONT) { c->err = "unknown kernel class"; return MTP_EINVAL; }
     auto it = c->has_last ? c->step_launches.find(c->last_key) : c->step_launches.end();
     if (it == c->step_launches.end() || it->second.cls[kclass].empty()) {
         c->err = "the last decode step launched nothing of this kernel class";

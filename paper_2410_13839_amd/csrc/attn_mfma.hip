@@ -3,6 +3,7 @@
 // the matrix cores and the probabilities kept in registers.
 #include <math.h>
 
+#include "attn_dec.h"
 #include "common.h"
 #include "launch.h"
 #include "wave.h"
@@ -10,196 +11,21 @@
 namespace mtp {
 
 namespace {
-constexpr int PSTR = 68;     // floats per partial row: max, sum, 2 pad, 64 outputs
-
 __device__ __forceinline__ uint32_t pk2(float a, float b) {
     return (uint32_t)f32_to_bf16(a) | ((uint32_t)f32_to_bf16(b) << 16);
 }
 }  // namespace
 
-// Decode attention over a bf16 cache, NW waves per workgroup: one workgroup
-// per (sequence, head, key split); within a 16*NW-key chunk each wave owns 16
-// consecutive keys and keeps its own online-softmax state (running max, sum,
-// O^T accumulators) across the chunks of its split, so the chunk loop has no
-// barrier; the NW states are merged through LDS once at the end.
-//   S^T[key][q] = K[key][:] . Q[q][:] / 8    v_mfma_f32_16x16x32_bf16 (2 k-steps)
-//   O^T[dim][q] += V^T[dim][key] P^T[key][q] v_mfma_f32_16x16x16_bf16: the B
-//                                             operand (4 keys x query per lane)
-//                                             is exactly the lane's S^T result
-//                                             after exp, so P never leaves registers
-// A CU streams only ~25 GB/s from HBM, so short splits spread a small batch's
-// keys over many CUs (64-key splits, 4 waves, at batch 1); long splits use up
-// to 16 waves.  With long splits each wave keeps PD of its 16-key groups in
-// flight (a register ring, rotated by unrolling), so a CU's outstanding KV
-// reads grow with PD instead of stalling on one round trip per chunk.
-typedef short s16x4_t __attribute__((ext_vector_type(4)));
-
+// Decode attention (attn_dec.h): one workgroup per (sequence, head, key
+// split) of NW waves.
 template <int NW, int PD>
 __global__ __launch_bounds__(64 * NW) void attn_dec_kernel(AttnMfmaArgs p) {
-    const int b = blockIdx.x, head = blockIdx.y, split = blockIdx.z;
-    const int H = gridDim.y;
-    const int tid = threadIdx.x, lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int r = lane & 15, g = lane >> 4;
-    extern __shared__ float s_o[];               // [NW waves][64 dims][17]
-    __shared__ float s_m[NW][16], s_l[NW][16];
-    constexpr int CH = 16 * NW;                  // keys per chunk
-    const bf16_t* pool = reinterpret_cast<const bf16_t*>(p.kv.pool);
-    const int kb = split * p.split_len;
-    const int row0 = b * p.Q;
-
-    // Key groups start at multiples of 16 (splits and chunks are multiples of
-    // 16 keys), so each wave's 16-key group is exactly one cache page; group i
-    // of this wave is page (kb / 16) + wave + NW i of the sequence.  Lane j
-    // holds the page number of group j (64 groups at a time, reloaded every
-    // 64): a group's addresses then come from a register read, not from a
-    // page-table load that, completing in order with the vector loads before
-    // it, would hold each group's K / V loads behind the previous group's.
-    // Page indexes are clamped to the sequence's block table, whose unused
-    // entries name page 0, so loads past the context stay in the pool.
-    const int maxp = p.kv.max_pages_per_seq;
-    const int32_t* btab = p.kv.block_table + (size_t)b * maxp;
-    const int pg0 = (kb >> 4) + wave;
-    int pages = btab[min(pg0 + NW * lane, maxp - 1)];
-    uint4 kf[PD][2];
-    uint2 vf[PD][4];
-    auto load_keys = [&](int u, int gi) {        // gi: this wave's group index (uniform)
-        if ((gi & 63) == 0 && gi > 0) pages = btab[min(pg0 + NW * (gi + lane), maxp - 1)];
-        const int page = __builtin_amdgcn_readlane(pages, gi & 63);
-        const bf16_t* kp = pool + kv_page_block(p.kv, page, 0, head) + r * MTP_HEAD_DIM + g * 8;
-        kf[u][0] = *reinterpret_cast<const uint4*>(kp);
-        kf[u][1] = *reinterpret_cast<const uint4*>(kp + 32);
-        const bf16_t* vp = pool + kv_page_block(p.kv, page, 1, head) + 4 * g;
-#pragma unroll
-        for (int dt = 0; dt < 4; ++dt) vf[u][dt] = *reinterpret_cast<const uint2*>(vp + (16 * dt + r) * 16);
-    };
-#pragma unroll
-    for (int u = 0; u < PD; ++u) load_keys(u, u);
-    float4 qa[2], qb[2];
-    {
-        const float* qp = p.q + (size_t)(row0 + min(r, p.Q - 1)) * p.ldq + head * 64 + g * 8;
-        qa[0] = *reinterpret_cast<const float4*>(qp);
-        qb[0] = *reinterpret_cast<const float4*>(qp + 4);
-        qa[1] = *reinterpret_cast<const float4*>(qp + 32);
-        qb[1] = *reinterpret_cast<const float4*>(qp + 36);
-    }
-    const int nrows = p.st[b].pend_len;
-    const int pos0 = p.st[b].ctx_len;
-    const int kend = pos0 + nrows;
-    if (nrows <= 0 || kb >= kend) return;       // uniform over the workgroup
-    const int ke = min(kb + p.split_len, kend);
-
-    bf16x8_t qf[2];
-#pragma unroll
-    for (int h2 = 0; h2 < 2; ++h2)
-        qf[h2] = __builtin_bit_cast(bf16x8_t, make_uint4(pk2(qa[h2].x * 0.125f, qa[h2].y * 0.125f),
-                                                         pk2(qa[h2].z * 0.125f, qa[h2].w * 0.125f),
-                                                         pk2(qb[h2].x * 0.125f, qb[h2].y * 0.125f),
-                                                         pk2(qb[h2].z * 0.125f, qb[h2].w * 0.125f)));
-
-    float m_run = -INFINITY, l_run = 0.f;       // query r, this wave's keys
-    f32x4_t acc[4];                             // O^T rows 16 dt + 4 g + v, query r
-#pragma unroll
-    for (int dt = 0; dt < 4; ++dt) acc[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-
-    for (int cb = kb; cb < ke; cb += CH * PD) {
-#pragma unroll
-      for (int u = 0; u < PD; ++u) {
-        const int c0 = cb + u * CH;
-        if (c0 >= ke) break;                     // uniform over the workgroup
-        const uint4 k0 = kf[u][0], k1 = kf[u][1];
-        uint2 v[4];
-#pragma unroll
-        for (int dt = 0; dt < 4; ++dt) v[dt] = vf[u][dt];
-        if (c0 + PD * CH < ke) load_keys(u, (c0 - kb) / CH + PD);   // refill this ring slot (uniform branch)
-        const int wk = c0 + 16 * wave;
-        f32x4_t s = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, k0), qf[0], s, 0, 0, 0);
-        s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, k1), qf[1], s, 0, 0, 0);
-        float sc[4];
-        float mx = -INFINITY;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const int key = wk + 4 * g + e;
-            const bool ok = (key < ke) && (key <= pos0 + r) && (r < nrows);
-            sc[e] = ok ? s[e] : -INFINITY;
-            mx = fmaxf(mx, sc[e]);
-        }
-        mx = xor16_max(mx);
-        mx = xor32_max(mx);
-        const float m_new = fmaxf(m_run, mx);
-        const float scale = (m_run == -INFINITY) ? 0.f : __expf(m_run - m_new);
-        float pe[4], sum = 0.f;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            pe[e] = (sc[e] == -INFINITY) ? 0.f : __expf(sc[e] - m_new);
-            sum += pe[e];
-        }
-        sum = xor16_sum(sum);
-        sum = xor32_sum(sum);
-        l_run = l_run * scale + sum;
-        m_run = m_new;
-        const s16x4_t pf = __builtin_bit_cast(s16x4_t, make_uint2(pk2(pe[0], pe[1]), pk2(pe[2], pe[3])));
-        // V^T entries of keys past the context may hold anything: zero them
-        const int nvalid = ke - (wk + 4 * g);
-#pragma unroll
-        for (int dt = 0; dt < 4; ++dt) {
-            uint2 vv = v[dt];
-            if (nvalid < 4) {
-                uint32_t w0 = vv.x, w1 = vv.y;
-                if (nvalid <= 0) w0 = 0u;
-                else if (nvalid == 1) w0 &= 0x0000FFFFu;
-                if (nvalid <= 2) w1 = 0u;
-                else w1 &= 0x0000FFFFu;
-                vv = make_uint2(w0, w1);
-            }
-            acc[dt] *= scale;
-            acc[dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4_t, vv), pf, acc[dt], 0, 0, 0);
-        }
-      }
-    }
-
-    // merge the NW waves' states
-    if (g == 0) s_m[wave][r] = m_run;
-    __syncthreads();
-    float M = -INFINITY;
-#pragma unroll
-    for (int w = 0; w < NW; ++w) M = fmaxf(M, s_m[w][r]);
-    const float wsc = (m_run == -INFINITY) ? 0.f : __expf(m_run - M);
-#pragma unroll
-    for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) s_o[(wave * 64 + 16 * dt + 4 * g + e) * 17 + r] = acc[dt][e] * wsc;
-    if (g == 0) s_l[wave][r] = l_run * wsc;
-    __syncthreads();
-    // output: (dim, query) pairs over the workgroup's threads
-    for (int idx = tid; idx < 64 * 16; idx += 64 * NW) {
-        const int dim = idx >> 4, q = idx & 15;
-        if (q >= nrows) continue;
-        float o = 0.f, L = 0.f, Mq = -INFINITY;
-#pragma unroll
-        for (int w = 0; w < NW; ++w) {
-            o += s_o[(w * 64 + dim) * 17 + q];
-            L += s_l[w][q];
-            Mq = fmaxf(Mq, s_m[w][q]);
-        }
-        if (p.n_splits == 1) {
-            const int row = row0 + q, col = head * 64 + dim;
-            p.out[p.packed ? frag_off(row, col, p.ldo) : (size_t)row * p.ldo + col] = f32_to_bf16(o / L);
-        } else {
-            float* e = p.part + ((size_t)(b * H + head) * p.n_splits + split) * (p.qt * PSTR) + q * PSTR;
-            e[4 + dim] = o;
-            if (dim == 0) {
-                e[0] = Mq;
-                e[1] = L;
-            }
-        }
-    }
+    attn_dec_body<NW, PD, 16, false>(p, blockIdx.x, blockIdx.y, blockIdx.z, gridDim.y, FrontSync{});
 }
 
 template <int NW, int PD>
 static hipError_t attn_dec_go_pd(hipStream_t st, const AttnMfmaArgs& a) {
-    const size_t lds = (size_t)NW * 64 * 17 * sizeof(float);
+    const size_t lds = (size_t)NW * 16 * 64 * sizeof(float);    // attn_dec_body's s_acc at QN = 16
     static bool attr_set = false;
     if (!attr_set && lds > 48 * 1024) {
         hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_dec_kernel<NW, PD>),

@@ -33,6 +33,7 @@
 // output columns >= M, which are never stored.
 #include <algorithm>
 
+#include "attn_dec.h"
 #include "common.h"
 #include "launch.h"
 #include "ln_rows.h"
@@ -64,6 +65,7 @@ struct EpiQKVDec {
     const SeqState* st;
     KVView kv;
     int d, Q;
+    bf16_t* qh;              // non-null: the queries go here instead, as bf16 q / 8 ([M][d])
     using Early = int2;      // the row's sequence's (ctx_len, pend_len)
     struct Pre { float b[4]; int page, slot; bool ok; };
     __device__ __forceinline__ Early early(int m) const {
@@ -85,7 +87,11 @@ struct EpiQKVDec {
     __device__ __forceinline__ void store(const Pre& p, int m, int n, const float (&v)[4], int, int) const {
         const float r0 = v[0] + p.b[0], r1 = v[1] + p.b[1], r2 = v[2] + p.b[2], r3 = v[3] + p.b[3];
         if (n < d) {
-            *reinterpret_cast<float4*>(q + (size_t)m * d + n) = make_float4(r0, r1, r2, r3);
+            if (qh)
+                *reinterpret_cast<uint2*>(qh + (size_t)m * d + n) =
+                    make_uint2(pack2(r0 * 0.125f, r1 * 0.125f), pack2(r2 * 0.125f, r3 * 0.125f));
+            else
+                *reinterpret_cast<float4*>(q + (size_t)m * d + n) = make_float4(r0, r1, r2, r3);
             return;
         }
         if (!p.ok) return;
@@ -197,8 +203,11 @@ struct EpiLogitsB {
 // The LayerNorm modes' prologue is LnRows (ln_rows.h).
 constexpr int GV_NW = 16;
 
+// One workgroup's work: output columns [16 tile, 16 tile + 16) over K range
+// `split` of S.
 template <int MR, int XM, int MAXF, int KCH, int MAXS, int NW, class Epi>
-__global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
+__device__ __forceinline__ void gemv_body(const GemvArgs& a, const Epi& epi, const int tile, const int split,
+                                          const int S) {
     constexpr int T = 64 * NW;
     extern __shared__ __attribute__((aligned(16))) bf16_t xs[];   // [16][K / S + 8], this K range
     // wave partial sums of the MFMA phase; before it, the LayerNorm gain and
@@ -222,18 +231,6 @@ __global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int r = lane & 15, g = lane >> 4;
-    // Split-K launches (four K ranges): workgroup j takes K range j % 4 and
-    // column tile j / 4, so that (the dispatcher dealing workgroups to the 8
-    // XCDs in turn) each K range's workgroups share two XCDs, whose L2s then
-    // hold only that range's activations (the out-projection's attention
-    // split words of its four heads, FFN2's hidden columns) instead of all.
-    const int S = gridDim.y;
-    int tile = blockIdx.x, split = blockIdx.y;
-    if (S == 4) {
-        const int j = blockIdx.x + gridDim.x * blockIdx.y;
-        tile = j >> 2;
-        split = j & 3;
-    }
     const int n0 = tile * 16;
     const int K = a.K, M = a.M, N = a.N;
     const int ks = K / S;                         // this workgroup's K range
@@ -488,6 +485,74 @@ __global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
     }
 }
 
+template <int MR, int XM, int MAXF, int KCH, int MAXS, int NW, class Epi>
+__global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
+    // Split-K launches (four K ranges): workgroup j takes K range j % 4 and
+    // column tile j / 4, so that (the dispatcher dealing workgroups to the 8
+    // XCDs in turn) each K range's workgroups share two XCDs, whose L2s then
+    // hold only that range's activations (the out-projection's attention
+    // split words of its four heads, FFN2's hidden columns) instead of all.
+    const int S = gridDim.y;
+    int tile = blockIdx.x, split = blockIdx.y;
+    if (S == 4) {
+        const int j = blockIdx.x + gridDim.x * blockIdx.y;
+        tile = j >> 2;
+        split = j & 3;
+    }
+    gemv_body<MR, XM, MAXF, KCH, MAXS, NW, Epi>(a, epi, tile, split, S);
+}
+
+// ---------------------------------------------------------- the fused front
+// LN1 + QKV projection + decode attention of a small batch in one launch.
+// The attention workgroups start with the QKV workgroups, prefetch their
+// cached keys while the projection streams its weights, and then wait only
+// for the 12 QKV column tiles of their own head (a flag per tile: four
+// tiles each of the head's queries, keys and values), not for the whole
+// projection and a launch boundary.
+//
+// Workgroup j runs on XCD j % 8 (the dispatcher deals the workgroups of a
+// launch to the 8 XCDs in turn; the library checks this once per context
+// before it uses this kernel).  On XCD x the first 12 H / 8 workgroups are
+// the QKV tiles of heads x, x + 8, ..., the rest the attention workgroups of
+// those heads (batch x key splits each).  A head's producers and consumers
+// thus share one L2, which carries the hand-off: the producers' stores and
+// flags are plain stores, which reach it; the consumers read the flags, the
+// queries and the pending keys with loads that skip their CU's L1.  An XCD
+// dispatches its workgroups in order, producers first, so a consumer that
+// waits never holds a CU one of its producers still needs.
+template <int MR, int XM, int PD>
+__global__ __launch_bounds__(64 * GV_NW) void qkv_front_kernel(GemvArgs a, EpiQKVDec epi, AttnMfmaArgs p,
+                                                                FrontSync fs) {
+    const int j = blockIdx.x, x = j & 7, loc = j >> 3;
+    const int n_prod = 12 * (p.kv.n_heads >> 3);
+    if (loc < n_prod) {
+        const int hl = loc / 12, w = loc - 12 * hl;
+        const int tile = attn_dec_detail::front_tile(fs, x + 8 * hl, w);
+        gemv_body<MR, XM, 32 / GV_NW, 1, 1, GV_NW, EpiQKVDec>(a, epi, tile, 0, 1);
+        // only wave 0 stores (the epilogue): once its stores are complete,
+        // the tile is published
+        if (threadIdx.x < 64) {
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            if (threadIdx.x == 0) fs.flags[tile] = 1u;
+        }
+    } else {
+        const int cl = loc - n_prod, S = p.n_splits;
+        const int hl = cl / fs.per_head, rem = cl - hl * fs.per_head;
+        const int b = rem / S, split = rem - b * S;
+        attn_dec_body<GV_NW, PD, MR, true>(p, b, x + 8 * hl, split, p.kv.n_heads, fs);
+    }
+}
+
+// Reads the XCD of every workgroup of a launch of `grid` workgroups of 1024
+// threads and counts those not on XCD j % 8.
+__global__ __launch_bounds__(1024) void xcd_deal_check_kernel(unsigned* bad) {
+    if (threadIdx.x == 0) {
+        unsigned x;
+        asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(x));
+        if ((x & 0xFu) != (blockIdx.x & 7u)) atomicAdd(bad, 1u);
+    }
+}
+
 // --------------------------------------------------------------- launching
 template <int MR, int XM, int MAXF, int KCH, int MAXS, class Epi, int NW = GV_NW>
 static hipError_t gemv_go(hipStream_t st, const GemvArgs& a, int splits, const Epi& e) {
@@ -556,6 +621,59 @@ int gemv_merge_max_splits(int M, int d) {
     return std::min(32, 8 * gs);
 }
 
+bool qkv_front_ok(int rows, int d, int n_heads, int batch, int split_len, int n_splits) {
+    return rows >= 1 && rows <= 16 && d <= 1024 && d % 256 == 0 && n_heads % 8 == 0 && n_heads * 64 == d &&
+           batch >= 1 && rows % batch == 0 && (split_len == 256 || split_len == 512) && n_splits >= 1 &&
+           n_splits <= 64 && (int64_t)8 * (12 + batch * n_splits) * (n_heads / 8) <= 65535;
+}
+
+template <int MR, int XM, int PD>
+static hipError_t qkv_front_go(hipStream_t st, const GemvArgs& a, const EpiQKVDec& e, const AttnMfmaArgs& p,
+                               const FrontSync& fs) {
+    const size_t lds = std::max<size_t>((size_t)16 * (a.K + 8) * 2, (size_t)GV_NW * MR * 64 * sizeof(float));
+    static bool attr_set = false;
+    if (lds > 32 * 1024 && !attr_set) {
+        hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(&qkv_front_kernel<MR, XM, PD>),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, 128 * 1024);
+        if (err != hipSuccess) return err;
+        attr_set = true;
+    }
+    const int hpx = p.kv.n_heads / 8;
+    const int grid = 8 * hpx * (12 + fs.per_head);
+    hipLaunchKernelGGL((qkv_front_kernel<MR, XM, PD>), dim3(grid), dim3(64 * GV_NW), lds, st, a, e, p, fs);
+    return hipGetLastError();
+}
+
+template <int XM, int PD>
+static hipError_t qkv_front_mr(hipStream_t st, const GemvArgs& a, const EpiQKVDec& e, const AttnMfmaArgs& p,
+                               const FrontSync& fs) {
+    if (a.M <= 1) return qkv_front_go<1, XM, PD>(st, a, e, p, fs);
+    if (a.M <= 2) return qkv_front_go<2, XM, PD>(st, a, e, p, fs);
+    if (a.M <= 4) return qkv_front_go<4, XM, PD>(st, a, e, p, fs);
+    if (a.M <= 8) return qkv_front_go<8, XM, PD>(st, a, e, p, fs);
+    return qkv_front_go<16, XM, PD>(st, a, e, p, fs);
+}
+
+hipError_t qkv_front(hipStream_t st, const GemvArgs& a, const AttnMfmaArgs& p, const FrontSync& fs) {
+    const int H = p.kv.n_heads;
+    if (a.epi != EPI_QKV || (a.xmode != 1 && a.xmode != 2) || a.N != 3 * a.K || a.d != a.K || p.mode != 0 ||
+        p.kv.page_size != 16 || p.Q < 1 || p.Q > 16 || p.qt < p.Q || a.Q != p.Q || p.n_tiles * p.Q != a.M ||
+        p.ldq != a.K || !p.qh || p.qh != a.qh || !qkv_front_ok(a.M, a.K, H, p.n_tiles, p.split_len, p.n_splits) ||
+        fs.tiles_per_mat * 16 != a.K || fs.per_head != p.n_tiles * p.n_splits || !fs.flags || !fs.next_flags ||
+        fs.flags == fs.next_flags || !fs.err)
+        return hipErrorInvalidValue;
+    EpiQKVDec e{a.q, a.bias, a.st, a.kv, a.d, a.Q, a.qh};
+    const bool pd2 = p.split_len == 512;
+    if (a.xmode == 2) return pd2 ? qkv_front_mr<2, 2>(st, a, e, p, fs) : qkv_front_mr<2, 1>(st, a, e, p, fs);
+    return pd2 ? qkv_front_mr<1, 2>(st, a, e, p, fs) : qkv_front_mr<1, 1>(st, a, e, p, fs);
+}
+
+hipError_t xcd_deal_check(hipStream_t st, unsigned* bad, int grid) {
+    if (!bad || grid < 1) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(xcd_deal_check_kernel, dim3(grid), dim3(1024), 0, st, bad);
+    return hipGetLastError();
+}
+
 hipError_t gemv(hipStream_t st, const GemvArgs& a) {
     if (a.M < 1 || a.M > 16 || a.N < 4 || a.K % 128) return hipErrorInvalidValue;
     if (a.epi == EPI_PARTIAL) {
@@ -594,7 +712,7 @@ hipError_t gemv(hipStream_t st, const GemvArgs& a) {
     if (a.K > 2048 || a.K % 256 || (a.epi != EPI_LOGITS && a.N % 4)) return hipErrorInvalidValue;
     switch (a.epi) {
     case EPI_QKV: {
-        EpiQKVDec e{a.q, a.bias, a.st, a.kv, a.d, a.Q};
+        EpiQKVDec e{a.q, a.bias, a.st, a.kv, a.d, a.Q, nullptr};
         if (a.xmode == 2) return gemv_ln<2>(st, a, e);
         if (a.xmode == 1) return gemv_ln<1>(st, a, e);
         return hipErrorInvalidValue;

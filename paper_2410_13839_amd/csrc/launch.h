@@ -68,6 +68,18 @@ hipError_t attention_decode_merge(hipStream_t st, const AttnDecArgs& a);
 
 // MFMA attention for bf16 caches: mode 0 = decode (one tile per sequence, rows
 // from the sequence state), mode 1 = prefill (tiles of up to 16 rows).
+// Hand-off state of the fused decode front (qkv_front): one flag per QKV
+// column tile, set by the tile once its columns are stored.  Consecutive
+// launches use different flag sets: a launch clears the set of the next one
+// (next_flags), whose last user has finished.  Zero before the first launch.
+struct FrontSync {
+    unsigned* flags;      // [3 * tiles_per_mat]: this launch's set
+    unsigned* next_flags; // [3 * tiles_per_mat]: the next launch's set (cleared here)
+    unsigned* err;        // hand-off waits that ran out (a bounded wait; none expected)
+    int tiles_per_mat;    // d / 16
+    int per_head;         // attention workgroups per head (batch x key splits)
+};
+
 struct AttnMfmaArgs {
     int mode;
     int n_tiles;
@@ -75,6 +87,7 @@ struct AttnMfmaArgs {
     const SeqState* st;
     const int2* tiles; const RowInfo* rows;
     const float* q; int ldq;
+    const bf16_t* qh;          // decode inside the fused front: the queries as bf16 q / 8 ([rows][ldq])
     KVView kv;
     int split_len; int n_splits;
     bf16_t* out; int ldo;
@@ -110,6 +123,8 @@ struct GemvArgs {
     void* out; int ldo;                             // EPI_GELU / EPI_LOGITS output
     float* part_out;                                // EPI_PARTIAL output [4][M][N]
     float* q; KVView kv; int d;                     // EPI_QKV; xmode 5 reads q ([M][d] fp32)
+    bf16_t* qh;                                     // EPI_QKV in qkv_front: queries stored here as bf16 q / 8
+                                                    // instead of to q
     bf16_t* kvnew;                                  // [2][M][d]: the pending rows' keys, then values (bf16),
                                                     // written by qkv_attn, read by xmode 5
 };
@@ -126,6 +141,19 @@ bool qkv_attn_ok(int rows, int d, int n_heads, int64_t max_ctx, int n_splits);
 // Keys per split (a multiple of 16) of qkv_attn for contexts of at most
 // max_ctx keys over n_splits workgroups per head.
 int qkv_attn_split_len(int64_t max_ctx, int n_splits);
+
+// LN1 + QKV projection + decode attention in one launch (gemv.hip): the
+// GemvArgs of an EPI_QKV launch (xmode 1 or 2, rows = batch x Q <= 16) and
+// the AttnMfmaArgs of the decode attention over its q and cache (split_len
+// 256 or 512, whose partials the out-projection merges when n_splits > 1),
+// with the hand-off state fs (zero before the first launch; every launch
+// leaves it zero).  Needs n_heads a multiple of 8, head dim 64, d <= 1024,
+// and the dispatcher dealing workgroup j to XCD j % 8 (xcd_deal_check).
+hipError_t qkv_front(hipStream_t st, const GemvArgs& a, const AttnMfmaArgs& p, const FrontSync& fs);
+bool qkv_front_ok(int rows, int d, int n_heads, int batch, int split_len, int n_splits);
+// Adds to *bad the number of workgroups of a `grid`-workgroup launch that
+// do not run on XCD (workgroup index % 8).
+hipError_t xcd_deal_check(hipStream_t st, unsigned* bad, int grid);
 
 // Reads `bytes` (a multiple of 16) of `buf` so that earlier data leaves the
 // L2 and last-level caches (measurement only); writes a few words of `buf`.

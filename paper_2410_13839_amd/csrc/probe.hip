@@ -17,6 +17,16 @@
 //    also stores 256 bytes before its flag and checks a neighbour's after
 //    the barrier (stale reads are counted).
 //
+//  * mtp_probe_xcc_map: the XCD (the XCC_ID hardware register) that each
+//    workgroup of an ordinary launch runs on, to check the round-robin
+//    dealing of workgroups to the 8 XCDs that the decode kernels' tile
+//    mappings assume;
+//  * mtp_probe_handoff: the latency of one producer -> consumer hand-off
+//    between two co-resident workgroups (a ping-pong of data + flag), with
+//    the workgroups on one XCD or on two, for each combination of the
+//    stores' and the loads' cache bits (below): which of them make a store
+//    of one CU visible to the loads of another, and how soon.
+//
 // Each returns 0, or a negative value on a HIP error (its message on
 // stderr).  All memory is allocated and freed inside the call.
 #include <hip/hip_runtime.h>
@@ -112,6 +122,100 @@ __global__ __launch_bounds__(1024) void probe_flag_barrier_kernel(unsigned* flag
     }
 }
 
+__device__ __forceinline__ unsigned xcc_id() {
+    unsigned v;
+    asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(v));
+    return v & 0xFu;
+}
+
+__global__ void probe_xcc_kernel(unsigned* xcc, int spin) {
+    if (threadIdx.x == 0) xcc[blockIdx.x] = xcc_id();
+    // stay resident for a while, as a decode workgroup does
+    for (int i = 0; i < spin; ++i) __builtin_amdgcn_s_sleep(8);
+}
+
+// Cache bits of the hand-off's stores (ST) and loads (LD); every load waits
+// for its own data.
+//   ST 0: plain; 1: sc0; 2: sc1 (device scope); 3: nt
+//   LD 0: sc0; 1: plain after buffer_inv sc0 (the CU's L1 invalidated);
+//      2: sc1 (device scope); 3: plain after buffer_inv sc1; 4: nt
+template <int LD>
+__device__ __forceinline__ unsigned ld_bits(const unsigned* p) {
+    unsigned v;
+    if constexpr (LD == 0)
+        asm volatile("global_load_dword %0, %1, off sc0\n\ts_waitcnt vmcnt(0)" : "=v"(v) : "v"(p) : "memory");
+    else if constexpr (LD == 1)
+        asm volatile("buffer_inv sc0\n\tglobal_load_dword %0, %1, off\n\ts_waitcnt vmcnt(0)" : "=v"(v) : "v"(p) : "memory");
+    else if constexpr (LD == 2)
+        asm volatile("global_load_dword %0, %1, off sc1\n\ts_waitcnt vmcnt(0)" : "=v"(v) : "v"(p) : "memory");
+    else if constexpr (LD == 3)
+        asm volatile("buffer_inv sc1\n\tglobal_load_dword %0, %1, off\n\ts_waitcnt vmcnt(0)" : "=v"(v) : "v"(p) : "memory");
+    else
+        asm volatile("global_load_dword %0, %1, off nt\n\ts_waitcnt vmcnt(0)" : "=v"(v) : "v"(p) : "memory");
+    return v;
+}
+template <int ST>
+__device__ __forceinline__ void st_bits(unsigned* p, unsigned v) {
+    if constexpr (ST == 0)
+        asm volatile("global_store_dword %0, %1, off" : : "v"(p), "v"(v) : "memory");
+    else if constexpr (ST == 1)
+        asm volatile("global_store_dword %0, %1, off sc0" : : "v"(p), "v"(v) : "memory");
+    else if constexpr (ST == 2)
+        asm volatile("global_store_dword %0, %1, off sc1" : : "v"(p), "v"(v) : "memory");
+    else
+        asm volatile("global_store_dword %0, %1, off nt" : : "v"(p), "v"(v) : "memory");
+}
+
+// One wave per workgroup.  Workgroups b and b + stride form a pair (b with
+// (b / stride) even is the pinger).  Round r: the pinger stores 64 data
+// words and, once they are complete, its flag r; the ponger waits for the
+// flag, checks the data words and stores its own flag r, which the pinger
+// waits for.  err[0]: waits that ran out (the workgroup then stops, and its
+// partner's next wait runs out too); err[1]: stale data words; err[2]:
+// pairs on one XCD.
+template <int ST, int LD>
+__global__ __launch_bounds__(64) void probe_handoff_kernel(unsigned* flags, unsigned* data, unsigned* err, int stride,
+                                                           int rounds) {
+    const int b = blockIdx.x, lane = threadIdx.x;
+    const bool ping = ((b / stride) & 1) == 0;
+    const int pair = (b / (2 * stride)) * stride + b % stride;
+    unsigned* f_ab = flags + pair * 128;         // separate 256-byte blocks
+    unsigned* f_ba = f_ab + 64;
+    unsigned* dp = data + pair * 64 + lane;
+    if (ping && lane == 0) {
+        // the pair's XCDs, compared once
+        st_bits<2>(&flags[64 * 128 + b], xcc_id());
+    }
+    for (int r = 1; r <= rounds; ++r) {
+        if (ping) {
+            st_bits<ST>(dp, (unsigned)(r * 1000 + lane));
+            __builtin_amdgcn_s_waitcnt(0);
+            if (lane == 0) st_bits<ST>(f_ab, (unsigned)r);
+            int s = 0;
+            while (ld_bits<LD>(f_ba) < (unsigned)r && ++s < SPIN) __builtin_amdgcn_s_sleep(1);
+            if (s >= SPIN) {
+                if (lane == 0) atomicAdd(err, 1u);
+                return;
+            }
+        } else {
+            int s = 0;
+            while (ld_bits<LD>(f_ab) < (unsigned)r && ++s < SPIN) __builtin_amdgcn_s_sleep(1);
+            if (s >= SPIN) {
+                if (lane == 0) atomicAdd(err, 1u);
+                return;
+            }
+            if (ld_bits<LD>(dp) != (unsigned)(r * 1000 + lane)) atomicAdd(err + 1, 1u);
+            if (lane == 0) st_bits<ST>(f_ba, (unsigned)r);
+        }
+    }
+    if (!ping && lane == 0) {
+        const unsigned mine = xcc_id();
+        // the pinger stored its XCD before its first flag, which this
+        // workgroup has seen (or the round loop ended on a timeout)
+        if (ld_bits<2>(&flags[64 * 128 + b - stride]) == mine) atomicAdd(err + 2, 1u);
+    }
+}
+
 template <class F>
 int time_graph(hipStream_t st, int launches, F launch_one, double* us) {
     hipGraph_t g;
@@ -138,6 +242,19 @@ int time_graph(hipStream_t st, int launches, F launch_one, double* us) {
     PCK(hipGraphExecDestroy(ge));
     PCK(hipGraphDestroy(g));
     return 0;
+}
+
+template <int ST, int LD>
+const void* handoff_fn() { return (const void*)probe_handoff_kernel<ST, LD>; }
+template <int ST>
+const void* handoff_fn_ld(int ld) {
+    switch (ld) {
+    case 0: return handoff_fn<ST, 0>();
+    case 1: return handoff_fn<ST, 1>();
+    case 2: return handoff_fn<ST, 2>();
+    case 3: return handoff_fn<ST, 3>();
+    default: return handoff_fn<ST, 4>();
+    }
 }
 
 }  // namespace
@@ -224,6 +341,66 @@ int mtp_probe_flag_barrier(int mode, int data, int rounds, double* us_per_barrie
     PCK(hipFree(flags));
     PCK(hipFree(go));
     PCK(hipFree(buf));
+    PCK(hipFree(err));
+    return 0;
+}
+
+int mtp_probe_xcc_map(int grid, int block, uint32_t* xcc_out) {
+    if (grid < 1 || grid > 65536 || block < 1 || block > 1024 || !xcc_out) return -2;
+    unsigned* xcc = nullptr;
+    PCK(hipMalloc(&xcc, (size_t)grid * 4));
+    PCK(hipMemset(xcc, 0xFF, (size_t)grid * 4));
+    hipLaunchKernelGGL(probe_xcc_kernel, dim3(grid), dim3(block), 0, 0, xcc, 64);
+    PCK(hipGetLastError());
+    PCK(hipDeviceSynchronize());
+    PCK(hipMemcpy(xcc_out, xcc, (size_t)grid * 4, hipMemcpyDeviceToHost));
+    PCK(hipFree(xcc));
+    return 0;
+}
+
+int mtp_probe_handoff(int st_bits_sel, int ld_bits_sel, int stride, int rounds, double* us_per_handoff,
+                      uint32_t* timeouts, uint32_t* stale, uint32_t* pairs_same_xcd) {
+    if (st_bits_sel < 0 || st_bits_sel > 3 || ld_bits_sel < 0 || ld_bits_sel > 4 || (stride != 1 && stride != 8) ||
+        rounds < 1 || !us_per_handoff || !timeouts || !stale || !pairs_same_xcd)
+        return -2;
+    int dev = 0, coop = 0;
+    PCK(hipGetDevice(&dev));
+    PCK(hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev));
+    if (!coop) return -3;                            // both sides of a pair must be resident at once
+    const int nb = 16;                               // 8 pairs
+    unsigned *flags = nullptr, *data = nullptr, *err = nullptr;
+    const size_t fbytes = (size_t)(64 * 128 + nb) * 4;
+    PCK(hipMalloc(&flags, fbytes));
+    PCK(hipMalloc(&data, (size_t)8 * 64 * 4));
+    PCK(hipMalloc(&err, 16));
+    PCK(hipMemset(flags, 0, fbytes));
+    PCK(hipMemset(data, 0, (size_t)8 * 64 * 4));
+    PCK(hipMemset(err, 0, 16));
+    PCK(hipDeviceSynchronize());
+    void* args[] = {&flags, &data, &err, &stride, &rounds};
+    const void* fn = st_bits_sel == 0   ? handoff_fn_ld<0>(ld_bits_sel)
+                     : st_bits_sel == 1 ? handoff_fn_ld<1>(ld_bits_sel)
+                     : st_bits_sel == 2 ? handoff_fn_ld<2>(ld_bits_sel)
+                                        : handoff_fn_ld<3>(ld_bits_sel);
+    hipEvent_t a, b;
+    PCK(hipEventCreate(&a));
+    PCK(hipEventCreate(&b));
+    PCK(hipEventRecord(a, 0));
+    PCK(hipLaunchCooperativeKernel(fn, dim3(nb), dim3(64), args, 0, 0));
+    PCK(hipEventRecord(b, 0));
+    PCK(hipEventSynchronize(b));
+    float ms = 0.f;
+    PCK(hipEventElapsedTime(&ms, a, b));
+    unsigned h[4];
+    PCK(hipMemcpy(h, err, 16, hipMemcpyDeviceToHost));
+    *us_per_handoff = (double)ms * 1000.0 / (2.0 * rounds);
+    *timeouts = h[0];
+    *stale = h[1];
+    *pairs_same_xcd = h[2];
+    PCK(hipEventDestroy(a));
+    PCK(hipEventDestroy(b));
+    PCK(hipFree(flags));
+    PCK(hipFree(data));
     PCK(hipFree(err));
     return 0;
 }

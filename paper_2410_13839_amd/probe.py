@@ -1,5 +1,6 @@
 """Measurement probes behind the decode path's design (launch floor, a bare
-weight stream per launch, grid barriers), from libmtp_probe.so; see
+weight stream per launch, grid barriers, the dealing of workgroups to XCDs,
+workgroup-to-workgroup hand-off latency), from libmtp_probe.so; see
 csrc/probe.hip.  Prints one JSON object:
 
     python -m paper_2410_13839_amd.probe
@@ -24,6 +25,8 @@ def _lib():
     lib.mtp_probe_launch_floor.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, d]
     lib.mtp_probe_stream.argtypes = [ctypes.c_int, ctypes.c_uint64, ctypes.c_int, d]
     lib.mtp_probe_flag_barrier.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, d, u, u]
+    lib.mtp_probe_xcc_map.argtypes = [ctypes.c_int, ctypes.c_int, u]
+    lib.mtp_probe_handoff.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, d, u, u, u]
     return lib
 
 
@@ -51,9 +54,41 @@ def flag_barrier(lib, mode: int, data: bool, rounds: int = 2000):
     return us.value, to.value, st.value
 
 
+def xcc_map(lib, grid: int, block: int) -> list[int]:
+    buf = (ctypes.c_uint32 * grid)()
+    _check(lib.mtp_probe_xcc_map(grid, block, buf), "xcc map")
+    return list(buf)
+
+
+ST_BITS = ("plain", "sc0", "sc1", "nt")
+LD_BITS = ("sc0", "plain after buffer_inv sc0", "sc1", "plain after buffer_inv sc1", "nt")
+
+
+def handoff(lib, st: int, ld: int, stride: int, rounds: int = 2000):
+    us, to, sr, same = ctypes.c_double(), ctypes.c_uint32(), ctypes.c_uint32(), ctypes.c_uint32()
+    _check(lib.mtp_probe_handoff(st, ld, stride, rounds, ctypes.byref(us), ctypes.byref(to), ctypes.byref(sr),
+                                 ctypes.byref(same)), "handoff")
+    return us.value, to.value, sr.value, same.value
+
+
 def main() -> None:
     lib = _lib()
-    out = {"launch_floor_us": {}, "stream_us": {}, "flag_barrier": {}}
+    out = {"launch_floor_us": {}, "stream_us": {}, "flag_barrier": {}, "xcc_map": {}, "handoff": {}}
+    for grid, block in ((192, 1024), (384, 1024), (256, 512), (1024, 256)):
+        ids = xcc_map(lib, grid, block)
+        off = sum(1 for b, x in enumerate(ids) if x != b % 8)
+        out["xcc_map"][f"{grid}x{block}"] = {"workgroups_not_on_xcd_b_mod_8": off,
+                                             "per_xcd": [ids.count(x) for x in range(8)]}
+        print(f"[probe] xcc map {grid} x {block}: {off} off the b % 8 dealing", file=sys.stderr, flush=True)
+    for stride, where in ((8, "one XCD"), (1, "two XCDs")):
+        for st in range(len(ST_BITS)):
+            for ld in range(len(LD_BITS)):
+                us, to, sr, same = handoff(lib, st, ld, stride)
+                what = f"{where}: stores {ST_BITS[st]}, loads {LD_BITS[ld]}"
+                out["handoff"][what] = {"us_per_handoff": round(us, 3), "timeouts": to, "stale_reads": sr,
+                                        "pairs_on_one_xcd": same}
+                print(f"[probe] handoff {what}: {us:.3f} us (timeouts {to}, stale {sr}, same-XCD pairs {same} of 8)",
+                      file=sys.stderr, flush=True)
     for grid in (1, 64, 256, 1024):
         for block in (64, 256, 1024):
             out["launch_floor_us"][f"{grid}x{block}"] = round(launch_floor(lib, grid, block), 3)

@@ -231,9 +231,10 @@ def test_q_estimation_validates_before_gpu_work():
 
 def test_probe_library_exports():
     """The measurement-probe library is built beside libmtp.so and exports
-    its three entry points (no GPU call is made)."""
+    its entry points (no GPU call is made)."""
     import ctypes
     from paper_2410_13839_amd.probe import LIB_PATH
     lib = ctypes.CDLL(LIB_PATH)
-    for name in ("mtp_probe_launch_floor", "mtp_probe_stream", "mtp_probe_flag_barrier"):
+    for name in ("mtp_probe_launch_floor", "mtp_probe_stream", "mtp_probe_flag_barrier", "mtp_probe_xcc_map",
+                 "mtp_probe_handoff"):
         assert hasattr(lib, name), name

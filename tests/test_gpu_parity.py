@@ -335,10 +335,14 @@ def test_valle_batch2_k8_sixteen_rows():
     log(f"valle batch 2: {steps} steps, max logit err {chk.max_err:.3g}, tie-zone {chk.tie_zone}")
 
 
-# Small bf16 decoders for the two fronts of a small-batch decode layer: one
-# launch for LN1, QKV and the attention over the cached keys with 8 or 16
-# workgroups per head (the out-projection then merges the chunk's own keys),
-# or separate QKV and attention launches; MTP_QKV_ATTN selects it per step.
+# Small bf16 decoders for the fronts of a small-batch decode layer:
+#  * chain (the default where it applies: heads a multiple of 8): one launch
+#    whose attention workgroups wait for their head's QKV columns, with 256-
+#    or 512-key splits (MTP_FRONT=256 / 512 force one);
+#  * separate QKV and attention launches (MTP_FRONT=0);
+#  * one launch for LN1, QKV and the attention over the cached keys with 8 or
+#    16 workgroups per head (MTP_QKV_ATTN=8 / 16; the out-projection then
+#    merges the chunk's own keys).
 FRONT_CASES = {
     # 8 heads (grouped per XCD), 2 ragged sequences of 4 rows, contexts up to ~690 keys
     "d512_b2_k4": (ModelShape(n_layers=2, d_model=512, n_heads=8, d_ff=1024, k_heads=4, dtype="bf16"),
@@ -348,12 +352,23 @@ FRONT_CASES = {
     "d256_b1_k2": (ModelShape(n_layers=2, d_model=256, n_heads=4, d_ff=512, k_heads=2, dtype="bf16"),
                    2, 4, 1, (30, 40), (1900, 2000)),
     # 16 heads, 8 sequences of one row each (K = 1: plain AR decoding)
-    "d1024_b8_k1": (ModelShape(n_layers=1, d_model=1024, n_heads=16, d_ff=2048, k_heads=1, dtype="bf16"),
+    "d1024_b8_k1": (ModelShape(n_layers=2, d_model=1024, n_heads=16, d_ff=2048, k_heads=1, dtype="bf16"),
                     1, 2, 8, (3, 20), (10, 300)),
 }
 
 
-@pytest.mark.parametrize("front", ["0", "8", "16"])
+FRONT_ENV = {"separate": {"MTP_FRONT": "0"}, "chain": {}, "chain256": {"MTP_FRONT": "256"},
+             "chain512": {"MTP_FRONT": "512"}, "8": {"MTP_QKV_ATTN": "8"}, "16": {"MTP_QKV_ATTN": "16"}}
+
+
+def set_front(monkeypatch, front):
+    monkeypatch.delenv("MTP_FRONT", raising=False)
+    monkeypatch.delenv("MTP_QKV_ATTN", raising=False)
+    for k, v in FRONT_ENV[front].items():
+        monkeypatch.setenv(k, v)
+
+
+@pytest.mark.parametrize("front", sorted(FRONT_ENV))
 @pytest.mark.parametrize("case", sorted(FRONT_CASES))
 def test_decode_fronts_match_the_oracle(case, front, monkeypatch):
     """Every front of the small-batch decode layer: selection exact at every
@@ -362,7 +377,7 @@ def test_decode_fronts_match_the_oracle(case, front, monkeypatch):
     shape, K, top_k, B, phon, ac = FRONT_CASES[case]
     wl = Workload(f"front_{case}", shape, K=K, top_k=top_k, batch=B, phon_len=phon, ac_len=ac, max_new=48,
                   eos_min=48)
-    monkeypatch.setenv("MTP_QKV_ATTN", front)
+    set_front(monkeypatch, front)
     log(f"front {front}, {case}: start")
     steps, emitted, chk = run_teacher_forced(wl, K, top_k, steps_checked=set(range(0, 64, 3)), tol=3e-2)
     assert steps == math.ceil(wl.max_new / K)
@@ -371,13 +386,14 @@ def test_decode_fronts_match_the_oracle(case, front, monkeypatch):
         f"tie-zone {chk.tie_zone}")
 
 
-def test_fused_front_eager_and_graph_agree(monkeypatch):
-    """The one-launch front gives bit-identical logits eagerly and replayed
+@pytest.mark.parametrize("front", ["chain", "16"])
+def test_fused_front_eager_and_graph_agree(front, monkeypatch):
+    """The one-launch fronts give bit-identical logits eagerly and replayed
     from a captured graph, step after step."""
     from paper_2410_13839_amd.binding import MTP_FLAG_NO_GRAPH
     shape, K, top_k, B, phon, ac = FRONT_CASES["d512_b2_k4"]
     wl = Workload("front_graph", shape, K=K, top_k=top_k, batch=B, phon_len=phon, ac_len=ac, max_new=48, eos_min=48)
-    monkeypatch.setenv("MTP_QKV_ATTN", "16")
+    set_front(monkeypatch, front)
     w = make_weights(shape)
     pr = make_prompts(wl)
     out = []
