@@ -174,10 +174,10 @@ WsLayout ws_layout(const mtp_config& c) {
     w.kvnew = take(front ? 2 * w.m_dec * d * 2 : 0);   // the pending rows' keys and values (bf16)
     // the chained front (qkv_front): its bf16 queries, and its hand-off
     // words (three sets of one flag per QKV column tile, a wait-overrun
-    // count and the dealing check)
+    // count and the dealing check's 8 masks)
     const bool chain = c.dtype == MTP_DTYPE_BF16 && !is_nar(c);
     w.qh = take(chain ? w.m_dec * d * 2 : 0);
-    w.fsync = take(chain ? (3 * (3 * d / 16) + 2) * 4 : 0);
+    w.fsync = take(chain ? (3 * (3 * d / 16) + 1 + 8) * 4 : 0);
     w.hz = take(B * d * 4);
     w.z = take((B + 15) / 16 * 16 * d * w.act_bytes);
     w.logits = take(B * KH * V * 4);
@@ -635,25 +635,22 @@ int plan_splits(mtp_ctx* c, int Q) {
     // small batches: QKV and the decode attention in one launch whose
     // attention workgroups wait for their own head's columns (qkv_front).
     // Keys per split: 256 (one 16-key group per wave of 16), or 512 when
-    // that keeps every workgroup of the launch resident at once (one per
-    // CU) or the splits within what the out-projection merges.  At least two
+    // that keeps the splits within what the out-projection merges (at 256,
+    // batch 1, K = 4: 280 us per step against 294 at 512, although 256 puts
+    // a few more workgroups in the launch than there are CUs).  At least two
     // layers: consecutive launches alternate their hand-off flag sets.
     const char* fenv = getenv("MTP_FRONT");
     if (cf.dtype == MTP_DTYPE_BF16 && Q > 0 && !(cf.flags & MTP_FLAG_NAR) && rows <= 16 && cf.n_layers >= 2 &&
         !(fenv && atoi(fenv) == 0)) {
-        int n_cu = 0, dev = 0;
-        if (hipGetDevice(&dev) != hipSuccess ||
-            hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-            n_cu = 0;
         const int hpx = cf.n_heads / 8;
         int pick = 0;
         for (int sl2 : {256, 512}) {
             const int64_t n = (max_ctx + sl2 - 1) / sl2;
-            if (n > c->ws.max_splits || (n > 1 && n > merge_max) ||
-                !qkv_front_ok((int)rows, cf.d_model, cf.n_heads, (int)B, sl2, (int)n))
-                continue;
-            if (!pick) pick = sl2;
-            if (8 * hpx * (12 + B * n) <= n_cu) { pick = sl2; break; }
+            if (n <= c->ws.max_splits && (n == 1 || n <= merge_max) &&
+                qkv_front_ok((int)rows, cf.d_model, cf.n_heads, (int)B, sl2, (int)n)) {
+                pick = sl2;
+                break;
+            }
         }
         if (fenv && (atoi(fenv) == 256 || atoi(fenv) == 512)) {
             const int sl2 = atoi(fenv);
@@ -663,18 +660,26 @@ int plan_splits(mtp_ctx* c, int Q) {
         }
         if (pick && c->xcd_deal < 0) {
             // once per context, outside any capture: the hand-off words
-            // start at zero, and the front needs workgroup j on XCD j % 8
+            // start at zero, and the front needs workgroups j and j + 8 of
+            // a launch on one XCD (the dispatcher deals them in turn from
+            // where the previous launch stopped)
             unsigned* fw = c->ws_ptr<unsigned>(c->ws.fsync);
-            unsigned* bad = fw + 3 * (3 * cf.d_model / 16) + 1;
-            const size_t fbytes = (size_t)(3 * (3 * cf.d_model / 16) + 2) * 4;
-            unsigned h_bad = 1;
+            unsigned* masks = fw + 3 * (3 * cf.d_model / 16) + 1;
+            const size_t fbytes = (size_t)(3 * (3 * cf.d_model / 16) + 1 + 8) * 4;
+            unsigned h_masks[8];
             HIPCHK(c, hipMemsetAsync(fw, 0, fbytes, c->stream), "front hand-off words");
             const int64_t n = (max_ctx + pick - 1) / pick;
-            HIPCHK(c, xcd_deal_check(c->stream, bad, (int)(8 * hpx * (12 + B * n))), "dealing check");
-            HIPCHK(c, hipMemcpyAsync(&h_bad, bad, 4, hipMemcpyDeviceToHost, c->stream), "dealing check");
+            HIPCHK(c, xcd_deal_check(c->stream, masks, (int)(8 * hpx * (12 + B * n))), "dealing check");
+            HIPCHK(c, hipMemcpyAsync(h_masks, masks, sizeof(h_masks), hipMemcpyDeviceToHost, c->stream),
+                   "dealing check");
             HIPCHK(c, hipStreamSynchronize(c->stream), "dealing check");
-            HIPCHK(c, hipMemsetAsync(bad, 0, 4, c->stream), "dealing check");
-            c->xcd_deal = h_bad == 0 ? 1 : 0;
+            unsigned seen = 0;
+            bool ok = true;
+            for (unsigned m : h_masks) {
+                ok = ok && m != 0 && (m & (m - 1)) == 0 && (seen & m) == 0;
+                seen |= m;
+            }
+            c->xcd_deal = ok ? 1 : 0;
         }
         if (pick && c->xcd_deal == 1) {
             c->front = 2;

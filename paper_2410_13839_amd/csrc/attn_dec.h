@@ -39,7 +39,7 @@ typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ uint32_t pk2(float a, float b) {
-    return (uint32_t)f32_to_bf16(a) | ((uint32_t)f32_to_bf16(b) << 16);
+    return bf16x2_bits(a, b);
 }
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* base, uint32_t bytes) {
@@ -83,7 +83,7 @@ __device__ __forceinline__ void attn_dec_body(const AttnMfmaArgs& p, int b, int 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int r = lane & 15, g = lane >> 4;
-    extern __shared__ float s_acc[];             // [NW waves][QN rows][64 dims]: the waves' O^T parts
+    extern __shared__ __attribute__((aligned(16))) float s_acc[];   // [NW waves][QN rows][64 dims]: the waves' O^T parts
     __shared__ float2 s_ml[QN][NW];              // the waves' (running max, sum) per row
     constexpr int CH = 16 * NW;                  // keys per chunk
     const bf16_t* pool = reinterpret_cast<const bf16_t*>(p.kv.pool);
@@ -222,11 +222,15 @@ __device__ __forceinline__ void attn_dec_body(const AttnMfmaArgs& p, int b, int 
         const float m_new = fmaxf(m_run, mx);
         const float scale = (first || m_run == -INFINITY) ? 0.f : __expf(m_run - m_new);
         float pe[4], sum = 0.f;
+        if (edge) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            pe[e] = (sc[e] == -INFINITY) ? 0.f : __expf(sc[e] - m_new);
-            sum += pe[e];
+            for (int e = 0; e < 4; ++e) pe[e] = (sc[e] == -INFINITY) ? 0.f : __expf(sc[e] - m_new);
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) pe[e] = __expf(sc[e] - m_new);
         }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) sum += pe[e];
         sum = xor16_sum(sum);
         sum = xor32_sum(sum);
         l_run = first ? sum : l_run * scale + sum;
@@ -256,19 +260,24 @@ __device__ __forceinline__ void attn_dec_body(const AttnMfmaArgs& p, int b, int 
     // state (rows < QN: the other rows are never valid), then one thread per
     // (row, 4 dims) rescales each wave's part to the common maximum and sums
     // them, in wave order
+    f32x4_t* s_acc4 = reinterpret_cast<f32x4_t*>(__builtin_assume_aligned(s_acc, 16));
     if (r < QN) {
 #pragma unroll
-        for (int dt = 0; dt < 4; ++dt)
-            *reinterpret_cast<f32x4_t*>(&s_acc[((wave * QN + r) * 16 + 4 * dt + g) * 4]) = acc[dt];
+        for (int dt = 0; dt < 4; ++dt) s_acc4[(wave * QN + r) * 16 + 4 * dt + g] = acc[dt];
         if (g == 0) s_ml[r][wave] = make_float2(m_run, l_run);
     }
     __syncthreads();
     for (int idx = tid; idx < 16 * QN; idx += 64 * NW) {
         const int q = idx >> 4, d4 = idx & 15;
         if (q >= nrows) continue;
+        // every LDS read first (16-byte reads, one wait), then the arithmetic
         float2 ml[NW];
+        f32x4_t av[NW];
 #pragma unroll
-        for (int w = 0; w < NW; ++w) ml[w] = s_ml[q][w];
+        for (int w = 0; w < NW; ++w) {
+            ml[w] = s_ml[q][w];
+            av[w] = s_acc4[(w * QN + q) * 16 + d4];
+        }
         float M = -INFINITY;
 #pragma unroll
         for (int w = 0; w < NW; ++w) M = fmaxf(M, ml[w].x);
@@ -277,7 +286,7 @@ __device__ __forceinline__ void attn_dec_body(const AttnMfmaArgs& p, int b, int 
 #pragma unroll
         for (int w = 0; w < NW; ++w) {
             const float wsc = (ml[w].x == -INFINITY) ? 0.f : __expf(ml[w].x - M);
-            o += *reinterpret_cast<const f32x4_t*>(&s_acc[((w * QN + q) * 16 + d4) * 4]) * wsc;
+            o += av[w] * wsc;
             L += ml[w].y * wsc;
         }
         const int dim = 4 * d4;

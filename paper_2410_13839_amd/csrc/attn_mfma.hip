@@ -12,7 +12,7 @@ namespace mtp {
 
 namespace {
 __device__ __forceinline__ uint32_t pk2(float a, float b) {
-    return (uint32_t)f32_to_bf16(a) | ((uint32_t)f32_to_bf16(b) << 16);
+    return bf16x2_bits(a, b);
 }
 }  // namespace
 

@@ -52,7 +52,7 @@ __device__ __forceinline__ void epi_store4(const Epi& e, int m, int n, const flo
 }
 
 __device__ __forceinline__ uint32_t epi_pk2(float a, float b) {
-    return (uint32_t)f32_to_bf16(a) | ((uint32_t)f32_to_bf16(b) << 16);
+    return bf16x2_bits(a, b);
 }
 
 template <typename KVT>

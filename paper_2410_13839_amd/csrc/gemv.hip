@@ -46,7 +46,7 @@ namespace {
 __device__ __forceinline__ float wsum(float v) { return wave_sum64(v); }
 
 __device__ __forceinline__ uint32_t pack2(float a, float b) {
-    return (uint32_t)f32_to_bf16(a) | ((uint32_t)f32_to_bf16(b) << 16);
+    return bf16x2_bits(a, b);
 }
 
 // ---------------------------------------------------------------- epilogues
@@ -510,16 +510,18 @@ __global__ __launch_bounds__(64 * NW) void gemv_kernel(GemvArgs a, Epi epi) {
 // tiles each of the head's queries, keys and values), not for the whole
 // projection and a launch boundary.
 //
-// Workgroup j runs on XCD j % 8 (the dispatcher deals the workgroups of a
-// launch to the 8 XCDs in turn; the library checks this once per context
-// before it uses this kernel).  On XCD x the first 12 H / 8 workgroups are
+// Workgroup j runs on XCD (j + s) % 8: the dispatcher deals the workgroups
+// of a launch to the 8 XCDs in turn, starting where the previous launch's
+// dealing stopped (s), so workgroups j and j + 8 share an XCD (the library
+// checks this once per context before it uses this kernel).  On XCD x the first 12 H / 8 workgroups are
 // the QKV tiles of heads x, x + 8, ..., the rest the attention workgroups of
-// those heads (batch x key splits each).  A head's producers and consumers
-// thus share one L2, which carries the hand-off: the producers' stores and
-// flags are plain stores, which reach it; the consumers read the flags, the
-// queries and the pending keys with loads that skip their CU's L1.  An XCD
-// dispatches its workgroups in order, producers first, so a consumer that
-// waits never holds a CU one of its producers still needs.
+// those heads (batch x key splits each, split-major).  A head's producers
+// and consumers thus share one L2, which carries the hand-off: the
+// producers' stores and flags are plain stores, which reach it; the
+// consumers read the flags, the queries and the pending keys with loads that
+// skip their CU's L1.  An XCD dispatches its workgroups in order, producers
+// first, so a consumer that waits never holds a CU one of its producers
+// still needs.
 template <int MR, int XM, int PD>
 __global__ __launch_bounds__(64 * GV_NW) void qkv_front_kernel(GemvArgs a, EpiQKVDec epi, AttnMfmaArgs p,
                                                                 FrontSync fs) {
@@ -536,20 +538,23 @@ __global__ __launch_bounds__(64 * GV_NW) void qkv_front_kernel(GemvArgs a, EpiQK
             if (threadIdx.x == 0) fs.flags[tile] = 1u;
         }
     } else {
-        const int cl = loc - n_prod, S = p.n_splits;
-        const int hl = cl / fs.per_head, rem = cl - hl * fs.per_head;
-        const int b = rem / S, split = rem - b * S;
+        // split-major: when the launch holds more workgroups than there are
+        // CUs, those that wait for a CU are the last key splits, past the
+        // context but at the longest
+        const int cl = loc - n_prod, hpx = p.kv.n_heads >> 3, B = p.n_tiles;
+        const int split = cl / (hpx * B), rem = cl - split * hpx * B;
+        const int hl = rem / B, b = rem - hl * B;
         attn_dec_body<GV_NW, PD, MR, true>(p, b, x + 8 * hl, split, p.kv.n_heads, fs);
     }
 }
 
-// Reads the XCD of every workgroup of a launch of `grid` workgroups of 1024
-// threads and counts those not on XCD j % 8.
-__global__ __launch_bounds__(1024) void xcd_deal_check_kernel(unsigned* bad) {
+// Records, for each residue j % 8 of the workgroups of a launch of 1024
+// threads, the set of XCDs (a bit each) they ran on.
+__global__ __launch_bounds__(1024) void xcd_deal_check_kernel(unsigned* masks) {
     if (threadIdx.x == 0) {
         unsigned x;
         asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(x));
-        if ((x & 0xFu) != (blockIdx.x & 7u)) atomicAdd(bad, 1u);
+        atomicOr(&masks[blockIdx.x & 7u], 1u << (x & 0xFu));
     }
 }
 
@@ -668,9 +673,9 @@ hipError_t qkv_front(hipStream_t st, const GemvArgs& a, const AttnMfmaArgs& p, c
     return pd2 ? qkv_front_mr<1, 2>(st, a, e, p, fs) : qkv_front_mr<1, 1>(st, a, e, p, fs);
 }
 
-hipError_t xcd_deal_check(hipStream_t st, unsigned* bad, int grid) {
-    if (!bad || grid < 1) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(xcd_deal_check_kernel, dim3(grid), dim3(1024), 0, st, bad);
+hipError_t xcd_deal_check(hipStream_t st, unsigned* masks, int grid) {
+    if (!masks || grid < 1) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(xcd_deal_check_kernel, dim3(grid), dim3(1024), 0, st, masks);
     return hipGetLastError();
 }
 

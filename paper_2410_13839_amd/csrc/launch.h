@@ -148,12 +148,13 @@ int qkv_attn_split_len(int64_t max_ctx, int n_splits);
 // 256 or 512, whose partials the out-projection merges when n_splits > 1),
 // with the hand-off state fs (zero before the first launch; every launch
 // leaves it zero).  Needs n_heads a multiple of 8, head dim 64, d <= 1024,
-// and the dispatcher dealing workgroup j to XCD j % 8 (xcd_deal_check).
+// and the dispatcher dealing workgroups j and j + 8 of a launch to one XCD
+// (xcd_deal_check).
 hipError_t qkv_front(hipStream_t st, const GemvArgs& a, const AttnMfmaArgs& p, const FrontSync& fs);
 bool qkv_front_ok(int rows, int d, int n_heads, int batch, int split_len, int n_splits);
-// Adds to *bad the number of workgroups of a `grid`-workgroup launch that
-// do not run on XCD (workgroup index % 8).
-hipError_t xcd_deal_check(hipStream_t st, unsigned* bad, int grid);
+// ORs into masks[r] (8 words) a bit per XCD that a workgroup j of a
+// `grid`-workgroup launch with j % 8 == r ran on.
+hipError_t xcd_deal_check(hipStream_t st, unsigned* masks, int grid);
 
 // Reads `bytes` (a multiple of 16) of `buf` so that earlier data leaves the
 // L2 and last-level caches (measurement only); writes a few words of `buf`.

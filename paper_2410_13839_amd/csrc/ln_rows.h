@@ -220,7 +220,7 @@ struct LnRows {
     }
 
     __device__ static __forceinline__ uint32_t ln_pack2(float a, float b) {
-        return (uint32_t)f32_to_bf16(a) | ((uint32_t)f32_to_bf16(b) << 16);
+        return bf16x2_bits(a, b);
     }
 };
 

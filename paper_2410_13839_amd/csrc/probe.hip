@@ -26,6 +26,9 @@
 //    the workgroups on one XCD or on two, for each combination of the
 //    stores' and the loads' cache bits (below): which of them make a store
 //    of one CU visible to the loads of another, and how soon.
+//  * mtp_probe_bf16_round: the gfx950 float -> bfloat16 conversion
+//    instruction against round-to-nearest-even written out on the bits, for
+//    every finite float (2^32 patterns less Inf / NaN).
 //
 // Each returns 0, or a negative value on a HIP error (its message on
 // stderr).  All memory is allocated and freed inside the call.
@@ -216,6 +219,28 @@ __global__ __launch_bounds__(64) void probe_handoff_kernel(unsigned* flags, unsi
     }
 }
 
+// round to nearest even on the bits (finite inputs)
+__device__ __forceinline__ uint32_t bf16_rne_bits(float f) {
+    uint32_t u = __float_as_uint(f);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return u >> 16;
+}
+
+__global__ __launch_bounds__(256) void probe_bf16_kernel(unsigned long long* out) {
+    unsigned long long mism = 0, checked = 0;
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < (1ull << 32); i += stride) {
+        const uint32_t u = (uint32_t)i;
+        if (((u >> 23) & 0xFFu) == 0xFFu) continue;   // Inf, NaN
+        const float f = __uint_as_float(u);
+        const uint32_t h = __builtin_bit_cast(uint16_t, (__bf16)f);
+        ++checked;
+        mism += h != bf16_rne_bits(f);
+    }
+    atomicAdd(&out[0], mism);
+    atomicAdd(&out[1], checked);
+}
+
 template <class F>
 int time_graph(hipStream_t st, int launches, F launch_one, double* us) {
     hipGraph_t g;
@@ -342,6 +367,21 @@ int mtp_probe_flag_barrier(int mode, int data, int rounds, double* us_per_barrie
     PCK(hipFree(go));
     PCK(hipFree(buf));
     PCK(hipFree(err));
+    return 0;
+}
+
+int mtp_probe_bf16_round(uint64_t* mismatches, uint64_t* checked) {
+    if (!mismatches || !checked) return -2;
+    unsigned long long* d = nullptr;
+    PCK(hipMalloc(&d, 16));
+    PCK(hipMemset(d, 0, 16));
+    hipLaunchKernelGGL(probe_bf16_kernel, dim3(2048), dim3(256), 0, 0, d);
+    PCK(hipGetLastError());
+    unsigned long long h[2];
+    PCK(hipMemcpy(h, d, 16, hipMemcpyDeviceToHost));
+    PCK(hipFree(d));
+    *mismatches = h[0];
+    *checked = h[1];
     return 0;
 }
 

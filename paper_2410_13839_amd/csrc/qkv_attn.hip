@@ -57,7 +57,7 @@ constexpr int QA_MAXSL = 16 * QA_NW;   // keys per split: one 16-key group per w
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ uint32_t qa_pk2(float a, float b) {
-    return (uint32_t)f32_to_bf16(a) | ((uint32_t)f32_to_bf16(b) << 16);
+    return bf16x2_bits(a, b);
 }
 
 int split_len_for(int64_t max_ctx, int g) {

@@ -1,6 +1,7 @@
 """Measurement probes behind the decode path's design (launch floor, a bare
 weight stream per launch, grid barriers, the dealing of workgroups to XCDs,
-workgroup-to-workgroup hand-off latency), from libmtp_probe.so; see
+workgroup-to-workgroup hand-off latency, the bf16 conversion instruction's
+rounding), from libmtp_probe.so; see
 csrc/probe.hip.  Prints one JSON object:
 
     python -m paper_2410_13839_amd.probe
@@ -26,6 +27,7 @@ def _lib():
     lib.mtp_probe_stream.argtypes = [ctypes.c_int, ctypes.c_uint64, ctypes.c_int, d]
     lib.mtp_probe_flag_barrier.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, d, u, u]
     lib.mtp_probe_xcc_map.argtypes = [ctypes.c_int, ctypes.c_int, u]
+    lib.mtp_probe_bf16_round.argtypes = [ctypes.POINTER(ctypes.c_uint64), ctypes.POINTER(ctypes.c_uint64)]
     lib.mtp_probe_handoff.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, d, u, u, u]
     return lib
 
@@ -74,12 +76,22 @@ def handoff(lib, st: int, ld: int, stride: int, rounds: int = 2000):
 def main() -> None:
     lib = _lib()
     out = {"launch_floor_us": {}, "stream_us": {}, "flag_barrier": {}, "xcc_map": {}, "handoff": {}}
-    for grid, block in ((192, 1024), (384, 1024), (256, 512), (1024, 256)):
+    mism, checked = ctypes.c_uint64(), ctypes.c_uint64()
+    _check(lib.mtp_probe_bf16_round(ctypes.byref(mism), ctypes.byref(checked)), "bf16 rounding")
+    out["bf16_convert_vs_rne_bits"] = {"finite_floats_checked": checked.value, "mismatches": mism.value}
+    print(f"[probe] bf16 conversion instruction vs RNE on the bits: {mism.value} mismatches in {checked.value}",
+          file=sys.stderr, flush=True)
+    # workgroup b runs on XCD (b + s) % 8, s where the previous launch's
+    # dealing stopped: count the residues b % 8 whose workgroups span more
+    # than one XCD (0 means b and b + 8 always share one)
+    for grid, block in ((192, 1024), (384, 1024), (256, 512), (1024, 256), (257, 1024), (272, 1024)):
         ids = xcc_map(lib, grid, block)
-        off = sum(1 for b, x in enumerate(ids) if x != b % 8)
-        out["xcc_map"][f"{grid}x{block}"] = {"workgroups_not_on_xcd_b_mod_8": off,
+        split = sum(1 for r in range(8) if len({x for b, x in enumerate(ids) if b % 8 == r}) > 1)
+        out["xcc_map"][f"{grid}x{block}"] = {"residues_on_more_than_one_xcd": split,
+                                             "rotation": (ids[0] - 0) % 8,
                                              "per_xcd": [ids.count(x) for x in range(8)]}
-        print(f"[probe] xcc map {grid} x {block}: {off} off the b % 8 dealing", file=sys.stderr, flush=True)
+        print(f"[probe] xcc map {grid} x {block}: {split} residues on more than one XCD, rotation {ids[0] % 8}",
+              file=sys.stderr, flush=True)
     for stride, where in ((8, "one XCD"), (1, "two XCDs")):
         for st in range(len(ST_BITS)):
             for ld in range(len(LD_BITS)):

@@ -236,5 +236,5 @@ def test_probe_library_exports():
     from paper_2410_13839_amd.probe import LIB_PATH
     lib = ctypes.CDLL(LIB_PATH)
     for name in ("mtp_probe_launch_floor", "mtp_probe_stream", "mtp_probe_flag_barrier", "mtp_probe_xcc_map",
-                 "mtp_probe_handoff"):
+                 "mtp_probe_handoff", "mtp_probe_bf16_round"):
         assert hasattr(lib, name), name
