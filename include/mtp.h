@@ -48,6 +48,9 @@ extern "C" {
 #define MTP_ENOMEM  -2   /* KV page pool or workspace too small for the request */
 #define MTP_ESTATE  -3   /* call out of order (e.g. decode before prefill)      */
 #define MTP_EHIP    -4   /* a HIP runtime error; text in mtp_last_error         */
+#define MTP_ETIMEOUT -5  /* a bounded device-side wait ran out (decode front);
+                            the step's outputs and the sequence state are
+                            invalid: prefill again                            */
 
 /* ---- element types ------------------------------------------------------ */
 #define MTP_DTYPE_F32   0   /* fp32 weights, activations and KV cache          */
@@ -186,13 +189,29 @@ int mtp_prefill(mtp_ctx* ctx, int B, const int32_t* phon, const int32_t* phon_le
  * planned after it is set (raised where needed to keep at most 64 splits;
  * the library otherwise chooses it from the batch and the longest
  * context).  Results are the same up to floating-point rounding.
- * Second override: MTP_QKV_ATTN = 8 or 16 runs, for B * K <= 8 rows of a
- * bf16 model with d_model <= 1024 and contexts of at most 256 * that many
- * keys, the QKV projection and the attention over the cached keys as one
- * launch with that many workgroups (key splits) per head, the pending
- * chunk's attention to its own keys merged by the out-projection; unset or
- * 0, separate QKV and attention launches (the faster on MI355X).  Again the
- * same results up to rounding; read when a step is planned. */
+ * Default decode front for B * K <= 16 rows of a bf16 model with at least
+ * two layers: LayerNorm, the QKV projection and the decode attention in one
+ * launch, whose attention workgroups wait (bounded) for their own head's
+ * QKV columns, stored by workgroups of the same launch on the same XCD; it
+ * runs only if a check at the first such step finds that workgroups j and
+ * j + 8 of a launch share an XCD, with 256 or 512 keys per split (the first
+ * whose split count the out-projection can merge).  MTP_FRONT = 0 selects
+ * separate QKV and attention launches, 256 or 512 forces that split length
+ * (separate launches if it does not fit).  MTP_QKV_ATTN = 8 or 16 instead
+ * runs, for B * K <= 8 rows, d_model <= 1024 and contexts of at most 256 *
+ * that many keys, a front in which each of that many workgroups (key
+ * splits) per head computes its own head's queries, the pending chunk's
+ * attention to its own keys merged by the out-projection (slower on
+ * MI355X).  Every front gives the same results up to rounding; the
+ * variables are read when a step is planned.
+ * The one-launch front's waits are bounded (MTP_FRONT_SPIN polls, read by
+ * mtp_create; default 100000, tens of ms; 0 makes every wait give up at
+ * once, which the tests use to reach this error path).  A wait that ran
+ * out makes this call return MTP_ETIMEOUT: the tokens and the sequence
+ * state of the step are invalid, the context needs mtp_prefill again and
+ * uses separate QKV and attention launches from then on.  The count is
+ * read only here: mtp_decode_step_async does not report it, the next
+ * mtp_decode_step does. */
 int mtp_decode_step(mtp_ctx* ctx, int K, int top_k, int32_t* out_tokens, int32_t* out_count);
 
 /* Same step, outputs written to DEVICE buffers d_tokens[B*K] and d_count[B]

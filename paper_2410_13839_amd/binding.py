@@ -21,7 +21,7 @@ if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() (hipcc, gfx950)")
 _lib = ctypes.CDLL(LIB_PATH)
 
-MTP_OK, MTP_EINVAL, MTP_ENOMEM, MTP_ESTATE, MTP_EHIP = 0, -1, -2, -3, -4
+MTP_OK, MTP_EINVAL, MTP_ENOMEM, MTP_ESTATE, MTP_EHIP, MTP_ETIMEOUT = 0, -1, -2, -3, -4, -5
 MTP_DTYPE_F32, MTP_DTYPE_BF16 = 0, 1
 MTP_FLAG_NO_GRAPH, MTP_FLAG_NAR = 1, 2
 (MTP_T_EMB_PHONE, MTP_T_EMB_AC, MTP_T_POS, MTP_T_LN1_G, MTP_T_LN1_B, MTP_T_W_QKV, MTP_T_B_QKV, MTP_T_W_O,

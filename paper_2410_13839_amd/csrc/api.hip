@@ -226,7 +226,8 @@ struct mtp_ctx {
     // how a small batch's layers start: 0 QKV and attention launches, 1 one
     // qkv_attn launch (on request), 2 one qkv_front launch
     int front = 0;
-    int xcd_deal = -1;           // workgroup j runs on XCD j % 8: -1 not yet checked, 0 no, 1 yes
+    int xcd_deal = -1;           // workgroups j and j + 8 share an XCD: -1 not yet checked, 0 no, 1 yes
+    int front_spin = 100000;     // polls before a front hand-off wait gives up (MTP_FRONT_SPIN)
     int lattice = MTP_LATTICE_OWN, anchored = 0;   // selection options (mtp_set_selection)
     int sample = 0;              // mtp_set_sampling: draw the path instead of the best one
     SampleCfg h_smp{0, 1.0f, 0}; // copied to the workspace before the next step when dirty
@@ -385,7 +386,7 @@ int run_layer_fused(mtp_ctx* c, int l, int rows, int qt) {
         FrontSync fs{};
         unsigned* fw = c->ws_ptr<unsigned>(c->ws.fsync);
         fs.flags = fw + set_of(l) * nf; fs.next_flags = fw + set_of((l + 1) % L) * nf; fs.err = fw + 3 * nf;
-        fs.tiles_per_mat = d / 16; fs.per_head = c->B * c->n_splits;
+        fs.tiles_per_mat = d / 16; fs.per_head = c->B * c->n_splits; fs.spin = c->front_spin;
         HIPCHK(c, launch_rec(c, MTP_KCLASS_QKV_FRONT, [g, m, fs](hipStream_t s) { return qkv_front(s, g, m, fs); }),
                "qkv + attention front");
     } else {
@@ -784,6 +785,7 @@ const char* mtp_strerror(int code) {
     case MTP_ENOMEM: return "KV page pool or workspace too small";
     case MTP_ESTATE: return "call out of order";
     case MTP_EHIP: return "HIP runtime error";
+    case MTP_ETIMEOUT: return "a bounded device-side wait ran out";
     }
     return "unknown error";
 }
@@ -831,6 +833,7 @@ int mtp_create(const mtp_config* cfg, const mtp_buffers* bufs, void* hip_stream,
     if (!c) return MTP_ENOMEM;
     c->cfg = *cfg;
     c->buf = *bufs;
+    if (const char* env = getenv("MTP_FRONT_SPIN")) c->front_spin = std::max(0, atoi(env));
     c->stream = (hipStream_t)hip_stream;
     c->ws = ws_layout(*cfg);
     weight_layout(*cfg, &c->wglob, &c->wlay);
@@ -953,7 +956,24 @@ int mtp_decode_step(mtp_ctx* c, int K, int top_k, int32_t* out_tokens, int32_t* 
     if (rc) return rc;
     HIPCHK(c, hipMemcpyAsync(out_tokens, c->WS() + c->ws.out_tok, (size_t)c->B * K * 4, hipMemcpyDeviceToHost, c->stream), "tokens to host");
     HIPCHK(c, hipMemcpyAsync(out_count, c->WS() + c->ws.out_cnt, (size_t)c->B * 4, hipMemcpyDeviceToHost, c->stream), "counts to host");
+    unsigned waits_out = 0;
+    // (the word exists, zeroed, once a front has been planned)
+    unsigned* werr = c->xcd_deal == 1 ? c->ws_ptr<unsigned>(c->ws.fsync) + 3 * (3 * c->cfg.d_model / 16) : nullptr;
+    if (werr)
+        HIPCHK(c, hipMemcpyAsync(&waits_out, werr, 4, hipMemcpyDeviceToHost, c->stream), "front wait count");
     HIPCHK(c, hipStreamSynchronize(c->stream), "step sync");
+    if (waits_out) {
+        // a front's attention ran on data it could not see complete: the
+        // tokens and the sequences' state are not those of the model.  The
+        // context keeps separate QKV and attention launches from now on.
+        HIPCHK(c, hipMemsetAsync(werr, 0, 4, c->stream), "front wait count");
+        HIPCHK(c, hipStreamSynchronize(c->stream), "front wait count");
+        c->xcd_deal = 0;
+        c->prefilled = false;
+        c->err = "a decode front's hand-off wait ran out: this step's tokens and the sequence state are invalid; "
+                 "prefill again";
+        return MTP_ETIMEOUT;
+    }
     return MTP_OK;
 }
 

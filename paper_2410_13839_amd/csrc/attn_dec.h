@@ -32,7 +32,6 @@ namespace attn_dec_detail {
 
 constexpr int PSTR = 68;        // floats per partial row: max, sum, 2 pad, 64 outputs
 constexpr int CPOL_SC1 = 16;    // buffer-load cache policy: device scope (misses the CU's L1)
-constexpr int FRONT_SPIN = 100000;   // bounded hand-off wait (tens of ms at most)
 
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
@@ -56,16 +55,17 @@ __device__ __forceinline__ int front_tile(const FrontSync& fs, int head, int w) 
 // producers and this workgroup run on one XCD (the front's workgroup
 // mapping), so a plain store of theirs is visible in the XCD's L2, which a
 // device-scope load reads (a plain load could hit a stale line in this CU's
-// L1).  Every wave polls for itself; a wait that runs out is counted.
+// L1).  Every wave polls for itself, at most fs.spin times; a wait that
+// runs out is counted (and the body goes on with whatever it then reads).
 __device__ __forceinline__ void front_wait(const FrontSync& fs, int head, int lane) {
     const int t = front_tile(fs, head, min(lane, 11));
-    int s = 0;
-    while (true) {
+    bool ready = false;
+    for (int s = 0; s < fs.spin; ++s) {
         const unsigned f = __hip_atomic_load(&fs.flags[t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (__all(f != 0u) || ++s >= FRONT_SPIN) break;
+        if (__all(f != 0u)) { ready = true; break; }
         __builtin_amdgcn_s_sleep(2);
     }
-    if (s >= FRONT_SPIN && lane == 0) atomicAdd(fs.err, 1u);
+    if (!ready && lane == 0) atomicAdd(fs.err, 1u);
 }
 
 }  // namespace attn_dec_detail

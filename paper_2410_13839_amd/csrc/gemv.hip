@@ -665,7 +665,7 @@ hipError_t qkv_front(hipStream_t st, const GemvArgs& a, const AttnMfmaArgs& p, c
         p.kv.page_size != 16 || p.Q < 1 || p.Q > 16 || p.qt < p.Q || a.Q != p.Q || p.n_tiles * p.Q != a.M ||
         p.ldq != a.K || !p.qh || p.qh != a.qh || !qkv_front_ok(a.M, a.K, H, p.n_tiles, p.split_len, p.n_splits) ||
         fs.tiles_per_mat * 16 != a.K || fs.per_head != p.n_tiles * p.n_splits || !fs.flags || !fs.next_flags ||
-        fs.flags == fs.next_flags || !fs.err)
+        fs.flags == fs.next_flags || !fs.err || fs.spin < 0)
         return hipErrorInvalidValue;
     EpiQKVDec e{a.q, a.bias, a.st, a.kv, a.d, a.Q, a.qh};
     const bool pd2 = p.split_len == 512;

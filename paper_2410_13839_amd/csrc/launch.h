@@ -78,6 +78,7 @@ struct FrontSync {
     unsigned* err;        // hand-off waits that ran out (a bounded wait; none expected)
     int tiles_per_mat;    // d / 16
     int per_head;         // attention workgroups per head (batch x key splits)
+    int spin;             // polls before a hand-off wait gives up (0: at once)
 };
 
 struct AttnMfmaArgs {

@@ -410,6 +410,48 @@ def test_fused_front_eager_and_graph_agree(front, monkeypatch):
     assert np.array_equal(out[0][1].view(np.uint32), out[1][1].view(np.uint32))
 
 
+def test_front_wait_that_runs_out_is_reported(monkeypatch):
+    """The one-launch front's hand-off waits, set from the host to give up
+    at once (MTP_FRONT_SPIN=0: every kernel still runs to its end), make the
+    step return MTP_ETIMEOUT; the context then refuses to step until a new
+    prefill, after which it runs separate QKV and attention launches and
+    gives bit for bit the tokens and logits of a context that always did."""
+    from paper_2410_13839_amd.binding import MTP_ESTATE, MTP_ETIMEOUT, MTPError
+    shape, K, top_k, B, phon, ac = FRONT_CASES["d512_b2_k4"]
+    wl = Workload("front_timeout", shape, K=K, top_k=top_k, batch=B, phon_len=phon, ac_len=ac, max_new=48,
+                  eos_min=48)
+    w = make_weights(shape)
+    pr = make_prompts(wl)
+    logq = make_logq()
+    set_front(monkeypatch, "chain")
+    monkeypatch.setenv("MTP_FRONT_SPIN", "0")
+    s = new_session(wl, w, logq)
+    monkeypatch.delenv("MTP_FRONT_SPIN")
+    s.prefill(pr.phon, pr.ac)
+    s.step(K, top_k)            # the first step after a prefill runs no trunk layer
+    with pytest.raises(MTPError) as e:
+        s.step(K, top_k)
+    assert e.value.code == MTP_ETIMEOUT
+    with pytest.raises(MTPError) as e:
+        s.step(K, top_k)
+    assert e.value.code == MTP_ESTATE
+    runs = []
+    for sess in (s, None):
+        if sess is None:
+            set_front(monkeypatch, "separate")
+            sess = new_session(wl, w, logq)
+        sess.prefill(pr.phon, pr.ac)
+        logs = []
+        for _ in range(5):
+            sess.step(K, top_k)
+            logs.append(sess.logits(K))
+        runs.append((sess.tokens()[:, :20].copy(), np.stack(logs)))
+        sess.close()
+    assert np.array_equal(runs[0][0], runs[1][0])
+    assert np.array_equal(runs[0][1].view(np.uint32), runs[1][1].view(np.uint32))
+    log("front timeout: reported, then separate launches match")
+
+
 def test_valle_b32_batched():
     """32 ragged sequences, K=4 (128 decode rows through the tiled path):
     selection exact for every sequence at every step; logits and tokens of
