@@ -111,6 +111,7 @@ KCLASSES = {  # kernel class -> (name, launches per decode step as a function of
     9: ("LN1 + QKV + attention over the cached keys (qkv_attn_kernel)", lambda L: L),
     4: ("attention (attn_dec_kernel)", lambda L: L),
     3: ("QKV projection (gemv_kernel<EpiQKVDec>)", lambda L: L),
+    11: ("LN2 + FFN1 + FFN2, one launch (ffn_chain_kernel)", lambda L: L),
     1: ("FFN1 (gemv_kernel<EpiGeluB>)", lambda L: L),
     5: ("heads (gemv_kernel<EpiLogitsB>)", lambda L: 1),
     6: ("out-projection (gemv_kernel<EpiPart>, attention merge)", lambda L: L),
@@ -144,6 +145,8 @@ def launch_bytes(wl, kclass, ctx):
         return d * d * 2 + M * d * 2 + M * d * 4
     if kclass == 2:
         return d * f * 2 + M * f * 2 + M * d * 4
+    if kclass == 11:  # both FFN products; the GELU rows between them need not reach HBM
+        return launch_bytes(wl, 1, ctx) + launch_bytes(wl, 2, ctx) - 2 * M * f * 2
     raise ValueError(kclass)
 
 

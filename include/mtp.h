@@ -204,14 +204,18 @@ int mtp_prefill(mtp_ctx* ctx, int B, const int32_t* phon, const int32_t* phon_le
  * attention to its own keys merged by the out-projection (slower on
  * MI355X).  Every front gives the same results up to rounding; the
  * variables are read when a step is planned.
- * The one-launch front's waits are bounded (MTP_FRONT_SPIN polls, read by
- * mtp_create; default 100000, tens of ms; 0 makes every wait give up at
- * once, which the tests use to reach this error path).  A wait that ran
- * out makes this call return MTP_ETIMEOUT: the tokens and the sequence
- * state of the step are invalid, the context needs mtp_prefill again and
- * uses separate QKV and attention launches from then on.  The count is
- * read only here: mtp_decode_step_async does not report it, the next
- * mtp_decode_step does. */
+ * Likewise, for B * K <= 16 rows of a bf16 model with at least two layers,
+ * d_model <= 1024 and d_ff <= 4096 (multiples of 256 and 512), FFN1 and
+ * FFN2 run as one launch whose FFN2 workgroups wait (bounded) for their K
+ * range of the GELU rows; MTP_FFN_CHAIN = 0 selects two launches.
+ * The waits of both one-launch kinds are bounded (MTP_FRONT_SPIN polls,
+ * read by mtp_create; default 100000, tens of ms; 0 makes every wait give
+ * up at once, which the tests use to reach this error path).  A wait that
+ * ran out makes this call return MTP_ETIMEOUT: the tokens and the
+ * sequence state of the step are invalid, the context needs mtp_prefill
+ * again and uses separate launches for that kind from then on.  The counts
+ * are read only here: mtp_decode_step_async does not report them, the
+ * next mtp_decode_step does. */
 int mtp_decode_step(mtp_ctx* ctx, int K, int top_k, int32_t* out_tokens, int32_t* out_count);
 
 /* Same step, outputs written to DEVICE buffers d_tokens[B*K] and d_count[B]
@@ -338,6 +342,9 @@ int mtp_get_tokens(mtp_ctx* ctx, int32_t* tokens);
 #define MTP_KCLASS_QKV_FRONT  10   /* LN1 -> x W_qkv^T, K/V into the cache, then the decode
                                       attention, in one launch whose attention workgroups wait
                                       for their head's QKV columns (B * K <= 16 rows) */
+#define MTP_KCLASS_FFN_CHAIN  11   /* LN2 -> x W_1^T -> GELU, then x W_2^T (residual partials), in
+                                      one launch whose W_2 workgroups wait for their K range of
+                                      the GELU rows (B * K <= 16 rows) */
 int mtp_profile_replay(mtp_ctx* ctx, int kclass, int iters, void* flush_buf, uint64_t flush_bytes,
                        double* avg_us);
 

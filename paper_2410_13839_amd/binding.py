@@ -29,7 +29,7 @@ MTP_FLAG_NO_GRAPH, MTP_FLAG_NAR = 1, 2
  MTP_T_W_HEADS, MTP_T_B_HEADS, MTP_T_STAGE, MTP_T_COUNT) = range(21)
 (MTP_KCLASS_GEMM_FFN1, MTP_KCLASS_GEMM_FFN2, MTP_KCLASS_GEMM_QKV, MTP_KCLASS_ATTENTION, MTP_KCLASS_HEADS,
  MTP_KCLASS_GEMM_OPROJ, MTP_KCLASS_SELECT, MTP_KCLASS_RESID_LN, MTP_KCLASS_QKV_ATTN,
- MTP_KCLASS_QKV_FRONT) = 1, 2, 3, 4, 5, 6, 7, 8, 9, 10
+ MTP_KCLASS_QKV_FRONT, MTP_KCLASS_FFN_CHAIN) = 1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11
 
 EXPORTED = ["mtp_query_sizes", "mtp_weight_offset", "mtp_create", "mtp_prefill", "mtp_decode_step",
             "mtp_decode_step_async", "mtp_get_logits", "mtp_get_lattice", "mtp_force_tokens", "mtp_get_seq_state",

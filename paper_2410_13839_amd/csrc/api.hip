@@ -128,7 +128,7 @@ int validate(const mtp_config* c, std::string* why) {
 }
 
 struct WsLayout {
-    uint64_t rows, ids, tiles, last_row, state, btab, h, q, qh, u, attn, ffn, part, apart, kvnew, fsync, hz, z, logits,
+    uint64_t rows, ids, tiles, last_row, state, btab, h, q, qh, u, attn, ffn, part, apart, kvnew, fsync, ffs, hz, z, logits,
         cand, ehat,
         u_states, u_m, u_ehat, u_delta, u_psi, smp_cfg, smp_u, codes, tgt_rows, nar_logits,
         delta, psi, slots, out_tok, out_cnt, hist, total;
@@ -178,6 +178,9 @@ WsLayout ws_layout(const mtp_config& c) {
     const bool chain = c.dtype == MTP_DTYPE_BF16 && !is_nar(c);
     w.qh = take(chain ? w.m_dec * d * 2 : 0);
     w.fsync = take(chain ? (3 * (3 * d / 16) + 1 + 8) * 4 : 0);
+    // the chained FFN (ffn_chain): three sets of 16 hidden rows, then a
+    // wait-overrun count
+    w.ffs = take(chain ? 3 * 16 * F * 2 + 4 : 0);
     w.hz = take(B * d * 4);
     w.z = take((B + 15) / 16 * 16 * d * w.act_bytes);
     w.logits = take(B * KH * V * 4);
@@ -228,6 +231,10 @@ struct mtp_ctx {
     int front = 0;
     int xcd_deal = -1;           // workgroups j and j + 8 share an XCD: -1 not yet checked, 0 no, 1 yes
     int front_spin = 100000;     // polls before a front hand-off wait gives up (MTP_FRONT_SPIN)
+    // small batches: FFN1 and FFN2 in one launch (ffn_chain); -1 until the
+    // first step that can use it fills the row sets with the sentinel
+    int ffn_chain = 0;
+    int ffn_ready = -1;
     int lattice = MTP_LATTICE_OWN, anchored = 0;   // selection options (mtp_set_selection)
     int sample = 0;              // mtp_set_sampling: draw the path instead of the best one
     SampleCfg h_smp{0, 1.0f, 0}; // copied to the workspace before the next step when dirty
@@ -243,12 +250,12 @@ struct mtp_ctx {
     std::vector<SeqState> h_state;
     int n_pre_rows = 0, n_pre_tiles = 0;
     // graphs keyed by (K, top_k, q_pad, batch, split_len, n_splits, lattice, anchored, sampling, front)
-    using StepKey = std::tuple<int, int, int, int, int, int, int, int, int, int>;
+    using StepKey = std::tuple<int, int, int, int, int, int, int, int, int, int, int>;
     std::map<StepKey, hipGraphExec_t> graphs;
     // every launch of each kernel class in the step of a key (arguments
     // captured by value), for replay timing
     using Launch = std::function<hipError_t(hipStream_t)>;
-    struct StepLaunches { std::vector<Launch> cls[MTP_KCLASS_QKV_FRONT + 1]; };
+    struct StepLaunches { std::vector<Launch> cls[MTP_KCLASS_FFN_CHAIN + 1]; };
     std::map<StepKey, StepLaunches> step_launches;
     StepLaunches* recording = nullptr;
     StepKey last_key{};
@@ -300,7 +307,7 @@ int pick_splits(const mtp_ctx* c, int M, int N, int K) {
 // Launch through `f` and, while a step is being recorded, keep it under class `kclass`.
 hipError_t launch_rec(mtp_ctx* c, int kclass, std::function<hipError_t(hipStream_t)> f) {
     hipError_t e = f(c->stream);
-    if (kclass > 0 && kclass <= MTP_KCLASS_QKV_FRONT && c->recording) c->recording->cls[kclass].push_back(std::move(f));
+    if (kclass > 0 && kclass <= MTP_KCLASS_FFN_CHAIN && c->recording) c->recording->cls[kclass].push_back(std::move(f));
     return e;
 }
 
@@ -347,6 +354,9 @@ int run_layer_fused(mtp_ctx* c, int l, int rows, int qt) {
     const int d = cf.d_model, F = cf.d_ff;
     float* h = c->ws_ptr<float>(c->ws.h);
     float* part = c->ws_ptr<float>(c->ws.part);
+    // FFN2's partials: past the out-projection's when the two FFN products
+    // share a launch (the out-projection's are read in it)
+    float* part2 = c->ffn_chain ? part + (size_t)4 * rows * d : part;
     GemvArgs g{};
     g.epi = EPI_QKV; g.M = rows; g.N = 3 * d; g.K = d;
     g.W = (const bf16_t*)c->lt(l, MTP_T_W_QKV); g.ldh = d; g.h_out = h;
@@ -354,7 +364,7 @@ int run_layer_fused(mtp_ctx* c, int l, int rows, int qt) {
         g.xmode = 2;
         g.emb = (const bf16_t*)c->wt(MTP_T_EMB_AC); g.pos = (const bf16_t*)c->wt(MTP_T_POS);
     } else {
-        g.xmode = 1; g.part = part; g.part_rows = rows; g.part_on = 1;
+        g.xmode = 1; g.part = part2; g.part_rows = rows; g.part_on = 1;
     }
     g.g = (const float*)c->lt(l, MTP_T_LN1_G); g.beta = (const float*)c->lt(l, MTP_T_LN1_B);
     g.st = c->ws_ptr<SeqState>(c->ws.state); g.Q = c->q_pad;
@@ -409,13 +419,31 @@ int run_layer_fused(mtp_ctx* c, int l, int rows, int qt) {
     g.W = (const bf16_t*)c->lt(l, MTP_T_W_1); g.part = part; g.part_rows = rows; g.part_on = 1; g.h_out = h;
     g.g = (const float*)c->lt(l, MTP_T_LN2_G); g.beta = (const float*)c->lt(l, MTP_T_LN2_B);
     g.bias = (const float*)c->lt(l, MTP_T_B_1); g.out = c->WS() + c->ws.ffn; g.ldo = F;
+    GemvArgs g2{};
+    g2.epi = EPI_PARTIAL; g2.xmode = 0; g2.M = rows; g2.N = d; g2.K = F;
+    g2.W = (const bf16_t*)c->lt(l, MTP_T_W_2); g2.ldx = F;
+    g2.h = h; g2.ldh = d; g2.bias = (const float*)c->lt(l, MTP_T_B_2); g2.part_out = part2;
+    if (c->ffn_chain) {
+        // row sets: consecutive launches (layer order, then the next step's
+        // layer 0) alternate sets 0 and 1; with an odd layer count the last
+        // layer takes set 2
+        const int L = cf.n_layers;
+        auto set_of = [L](int i) { return (L % 2 == 1 && i == L - 1) ? 2 : i % 2; };
+        bf16_t* sets = c->ws_ptr<bf16_t>(c->ws.ffs);
+        const size_t per_set = (size_t)16 * F;
+        g.out = sets + set_of(l) * per_set;
+        g2.x = (const bf16_t*)g.out; g2.part = part; g2.part_rows = rows;
+        FfnSync fs{};
+        fs.next = sets + set_of((l + 1) % L) * per_set;
+        fs.err = reinterpret_cast<unsigned*>(sets + 3 * per_set);
+        fs.spin = c->front_spin;
+        HIPCHK(c, launch_rec(c, MTP_KCLASS_FFN_CHAIN, [g, g2, fs](hipStream_t s) { return ffn_chain(s, g, g2, fs); }),
+               "ffn chain");
+        return MTP_OK;
+    }
     HIPCHK(c, launch_rec(c, MTP_KCLASS_GEMM_FFN1, [g](hipStream_t s) { return gemv(s, g); }), "ffn1 gemv");
-
-    g = GemvArgs{};
-    g.epi = EPI_PARTIAL; g.xmode = 0; g.M = rows; g.N = d; g.K = F;
-    g.W = (const bf16_t*)c->lt(l, MTP_T_W_2); g.x = (const bf16_t*)(c->WS() + c->ws.ffn); g.ldx = F;
-    g.h = h; g.ldh = d; g.bias = (const float*)c->lt(l, MTP_T_B_2); g.part_out = part;
-    HIPCHK(c, launch_rec(c, MTP_KCLASS_GEMM_FFN2, [g](hipStream_t s) { return gemv(s, g); }), "ffn2 gemv");
+    g2.x = (const bf16_t*)(c->WS() + c->ws.ffn);
+    HIPCHK(c, launch_rec(c, MTP_KCLASS_GEMM_FFN2, [g2](hipStream_t s) { return gemv(s, g2); }), "ffn2 gemv");
     return MTP_OK;
 }
 
@@ -564,7 +592,8 @@ int enqueue_step(mtp_ctx* c, int K, int top_k) {
         GemvArgs g{};
         g.epi = EPI_LOGITS; g.xmode = 3; g.M = B; g.N = K * V; g.K = d;
         g.W = (const bf16_t*)c->wt(MTP_T_W_HEADS); g.h = c->ws_ptr<float>(c->ws.h); g.ldh = d;
-        g.part = c->ws_ptr<float>(c->ws.part); g.part_rows = B * Q; g.part_on = fin_part ? 1 : 0;
+        g.part = c->ws_ptr<float>(c->ws.part) + (c->ffn_chain ? (size_t)4 * B * Q * d : 0);
+        g.part_rows = B * Q; g.part_on = fin_part ? 1 : 0;
         g.hz = c->ws_ptr<float>(c->ws.hz); g.st = c->ws_ptr<SeqState>(c->ws.state); g.Q = Q;
         g.g = (const float*)c->wt(MTP_T_LNF_G); g.beta = (const float*)c->wt(MTP_T_LNF_B);
         g.bias = (const float*)c->wt(MTP_T_B_HEADS); g.out = c->WS() + c->ws.logits; g.ldo = K * V;
@@ -622,6 +651,26 @@ int plan_splits(mtp_ctx* c, int Q) {
     // 5.97 + 5.13 us at batch 1, K = 4) and the out-projection's merge of
     // the chunk's own keys adds ~1 us (323 vs 312 us per step)
     c->front = 0;
+    // small batches: FFN1 and FFN2 in one launch, whose FFN2 workgroups wait
+    // for their K range of the hidden rows (at least two layers: consecutive
+    // launches use different row sets)
+    c->ffn_chain = 0;
+    if (cf.dtype == MTP_DTYPE_BF16 && Q > 0 && !(cf.flags & MTP_FLAG_NAR) && rows <= 16 && cf.n_layers >= 2 &&
+        ffn_chain_ok((int)rows, cf.d_model, cf.d_ff)) {
+        const char* env = getenv("MTP_FFN_CHAIN");
+        if (!(env && atoi(env) == 0) && c->ffn_ready != 0) {
+            if (c->ffn_ready < 0) {
+                // once per context, outside any capture: every row set
+                // starts as the sentinel, the overrun count at zero
+                char* fb = c->WS() + c->ws.ffs;
+                const size_t sets = (size_t)3 * 16 * cf.d_ff * 2;
+                HIPCHK(c, hipMemsetAsync(fb, 0xFF, sets, c->stream), "ffn row sets");
+                HIPCHK(c, hipMemsetAsync(fb + sets, 0, 4, c->stream), "ffn row sets");
+                c->ffn_ready = 1;
+            }
+            c->ffn_chain = 1;
+        }
+    }
     if (cf.dtype == MTP_DTYPE_BF16 && Q > 0 && !(cf.flags & MTP_FLAG_NAR)) {
         int G = 0;
         if (const char* env = getenv("MTP_QKV_ATTN")) G = atoi(env);
@@ -731,7 +780,7 @@ int step_common(mtp_ctx* c, int K, int top_k) {
         c->smp_dirty = false;
     }
     const auto key = std::make_tuple(K, top_k, c->q_pad, c->B, c->split_len, c->n_splits, c->lattice, c->anchored,
-                                     c->sample, c->front);
+                                     c->sample, c->front, c->ffn_chain);
     auto record = [&]() {
         mtp_ctx::StepLaunches& sl = c->step_launches[key];
         for (auto& v : sl.cls) v.clear();
@@ -956,22 +1005,35 @@ int mtp_decode_step(mtp_ctx* c, int K, int top_k, int32_t* out_tokens, int32_t* 
     if (rc) return rc;
     HIPCHK(c, hipMemcpyAsync(out_tokens, c->WS() + c->ws.out_tok, (size_t)c->B * K * 4, hipMemcpyDeviceToHost, c->stream), "tokens to host");
     HIPCHK(c, hipMemcpyAsync(out_count, c->WS() + c->ws.out_cnt, (size_t)c->B * 4, hipMemcpyDeviceToHost, c->stream), "counts to host");
-    unsigned waits_out = 0;
-    // (the word exists, zeroed, once a front has been planned)
+    unsigned waits_out[2] = {0, 0};
+    // (each word exists, zeroed, once its launch has been planned)
     unsigned* werr = c->xcd_deal == 1 ? c->ws_ptr<unsigned>(c->ws.fsync) + 3 * (3 * c->cfg.d_model / 16) : nullptr;
+    unsigned* ferr = c->ffn_ready == 1
+                         ? reinterpret_cast<unsigned*>(c->ws_ptr<bf16_t>(c->ws.ffs) + (size_t)3 * 16 * c->cfg.d_ff)
+                         : nullptr;
     if (werr)
-        HIPCHK(c, hipMemcpyAsync(&waits_out, werr, 4, hipMemcpyDeviceToHost, c->stream), "front wait count");
+        HIPCHK(c, hipMemcpyAsync(&waits_out[0], werr, 4, hipMemcpyDeviceToHost, c->stream), "front wait count");
+    if (ferr)
+        HIPCHK(c, hipMemcpyAsync(&waits_out[1], ferr, 4, hipMemcpyDeviceToHost, c->stream), "ffn wait count");
     HIPCHK(c, hipStreamSynchronize(c->stream), "step sync");
-    if (waits_out) {
-        // a front's attention ran on data it could not see complete: the
-        // tokens and the sequences' state are not those of the model.  The
-        // context keeps separate QKV and attention launches from now on.
-        HIPCHK(c, hipMemsetAsync(werr, 0, 4, c->stream), "front wait count");
-        HIPCHK(c, hipStreamSynchronize(c->stream), "front wait count");
-        c->xcd_deal = 0;
+    if (waits_out[0] || waits_out[1]) {
+        // a one-launch front or FFN went on with data it could not see
+        // complete: the tokens and the sequences' state are not those of
+        // the model.  The context keeps separate launches from now on.
+        if (waits_out[0]) {
+            HIPCHK(c, hipMemsetAsync(werr, 0, 4, c->stream), "front wait count");
+            c->xcd_deal = 0;
+        }
+        if (waits_out[1]) {
+            HIPCHK(c, hipMemsetAsync(ferr, 0, 4, c->stream), "ffn wait count");
+            c->ffn_ready = 0;
+        }
+        HIPCHK(c, hipStreamSynchronize(c->stream), "wait counts");
         c->prefilled = false;
-        c->err = "a decode front's hand-off wait ran out: this step's tokens and the sequence state are invalid; "
-                 "prefill again";
+        c->err = waits_out[0] ? "a decode front's hand-off wait ran out: this step's tokens and the sequence state "
+                                "are invalid; prefill again"
+                              : "a chained FFN's wait ran out: this step's tokens and the sequence state are "
+                                "invalid; prefill again";
         return MTP_ETIMEOUT;
     }
     return MTP_OK;
@@ -1306,7 +1368,7 @@ int mtp_profile_replay(mtp_ctx* c, int kclass, int iters, void* flush_buf, uint6
         return MTP_EINVAL;
     }
     const bool cold = flush_buf != nullptr;
-    if (kclass < MTP_KCLASS_GEMM_FFN1 || kclass > MTP_KCLASS_QKV_FRONT) { c->err = "unknown kernel class"; return MTP_EINVAL; }
+    if (kclass < MTP_KCLASS_GEMM_FFN1 || kclass > MTP_KCLASS_FFN_CHAIN) { c->err = "unknown kernel class"; return MTP_EINVAL; }
     auto it = c->has_last ? c->step_launches.find(c->last_key) : c->step_launches.end();
     if (it == c->step_launches.end() || it->second.cls[kclass].empty()) {
         c->err = "the last decode step launched nothing of this kernel class";

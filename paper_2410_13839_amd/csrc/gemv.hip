@@ -132,6 +132,40 @@ struct EpiGeluB {
     }
 };
 
+// FFN1 of the chained FFN: bias + GELU into the rows that FFN2 workgroups
+// of the same launch poll, with device-scope stores (they reach memory, so
+// that loads of the same scope on any XCD see them).  The value 0xFFFF (a
+// NaN) marks a row element not yet stored, so it is never stored: a NaN
+// that would round to it is stored as the canonical quiet NaN 0x7FC0.
+__device__ __forceinline__ uint32_t ffn_unmark(uint32_t w) {
+    if ((w & 0xFFFFu) == 0xFFFFu) w = (w & 0xFFFF0000u) | 0x7FC0u;
+    if ((w >> 16) == 0xFFFFu) w = (w & 0xFFFFu) | 0x7FC00000u;
+    return w;
+}
+
+struct EpiGeluShared {
+    bf16_t* out;
+    const float* bias;
+    int ldo;
+    using Early = EpiNoEarly;
+    struct Pre { float b[4]; };
+    __device__ __forceinline__ Early early(int) const { return {}; }
+    __device__ __forceinline__ Pre prefetch(const Early&, int, int n, int) const {
+        Pre p;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) p.b[i] = bias[n + i];
+        return p;
+    }
+    __device__ __forceinline__ void store(const Pre& p, int m, int n, const float (&v)[4], int, int) const {
+        float r[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) r[i] = gelu_erf(v[i] + p.b[i]);
+        const uint64_t w = (uint64_t)ffn_unmark(pack2(r[0], r[1])) | ((uint64_t)ffn_unmark(pack2(r[2], r[3])) << 32);
+        __hip_atomic_store(reinterpret_cast<uint64_t*>(out + (size_t)m * ldo + n), w, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+    }
+};
+
 // split-K partial sums of the out-projection / FFN2: part[split][m][n]; the
 // first K range also carries the residual input row and the bias, so the
 // four partials sum to the complete new residual row
@@ -158,6 +192,45 @@ struct EpiPart {
             o.y += p.b.y + p.x.y;
             o.z += p.b.z + p.x.z;
             o.w += p.b.w + p.x.w;
+        }
+        *reinterpret_cast<float4*>(part + ((size_t)split * M + m) * ldp + n) = o;
+    }
+};
+
+// FFN2 of the chained FFN: as EpiPart, but the residual input of the first
+// K range is the sum of the previous projection's four partials (the rows
+// FFN1's LayerNorm completes in the same launch), added in the order the
+// LayerNorm prologue adds them
+struct EpiPartRes {
+    float* part;          // [4][M][ldp]
+    int ldp;              // N (= d)
+    int M;
+    const float* pin;     // [4][pin_rows][ldp]: the out-projection's partials
+    int pin_rows;
+    const float* bias;    // [N]
+    struct Pre { float4 b, p[4]; };
+    __device__ __forceinline__ Pre prefetch(int m, int n, int split) const {
+        Pre q;
+        const int nn = min(n, ldp - 4);
+        q.b = *reinterpret_cast<const float4*>(bias + nn);
+        if (split == 0) {
+#pragma unroll
+            for (int s2 = 0; s2 < 4; ++s2)
+                q.p[s2] = *reinterpret_cast<const float4*>(pin + ((size_t)s2 * pin_rows + m) * ldp + nn);
+        }
+        return q;
+    }
+    __device__ __forceinline__ void store(const Pre& q, int m, int n, const float (&v)[4], int split) const {
+        float4 o = make_float4(v[0], v[1], v[2], v[3]);
+        if (split == 0) {
+            const float x0 = (q.p[0].x + q.p[1].x) + (q.p[2].x + q.p[3].x);
+            const float x1 = (q.p[0].y + q.p[1].y) + (q.p[2].y + q.p[3].y);
+            const float x2 = (q.p[0].z + q.p[1].z) + (q.p[2].z + q.p[3].z);
+            const float x3 = (q.p[0].w + q.p[1].w) + (q.p[2].w + q.p[3].w);
+            o.x += q.b.x + x0;
+            o.y += q.b.y + x1;
+            o.z += q.b.z + x2;
+            o.w += q.b.w + x3;
         }
         *reinterpret_cast<float4*>(part + ((size_t)split * M + m) * ldp + n) = o;
     }
@@ -548,6 +621,125 @@ __global__ __launch_bounds__(64 * GV_NW) void qkv_front_kernel(GemvArgs a, EpiQK
     }
 }
 
+// ------------------------------------------------------ the chained FFN
+// FFN2 workgroup of the chained FFN: output columns [16 tile, 16 tile + 16)
+// over K range `split` of four.  Its weights and epilogue operands go out
+// first (they depend on nothing in this launch); then it polls its K range
+// of the hidden rows, written by FFN1 workgroups of the same launch, with
+// device-scope loads until none holds the sentinel, and finishes as the
+// plain GEMV does.
+__device__ __forceinline__ bool ffn_marked(uint64_t v) {
+    const uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
+    return (lo & 0xFFFFu) == 0xFFFFu || (lo >> 16) == 0xFFFFu || (hi & 0xFFFFu) == 0xFFFFu || (hi >> 16) == 0xFFFFu;
+}
+
+template <int MR, int MAXF, int NW>
+__device__ __forceinline__ void ffn2_chain_body(const GemvArgs& a, const EpiPartRes& epi, const int tile,
+                                                const int split, const FfnSync& fs) {
+    constexpr int T = 64 * NW;
+    constexpr int XI = (MR * MAXF + 15) / 16;     // 16-byte row chunks per thread
+    extern __shared__ __attribute__((aligned(16))) bf16_t xs[];   // [16][K / 4 + 8]
+    __shared__ f32x4_t red2[64 * NW];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int r = lane & 15, g = lane >> 4;
+    const int K = a.K, M = a.M, N = a.N;
+    const int ks = K >> 2, kb = split * ks;
+    const int nfrag = ks >> 5;
+    const int nf = (nfrag - wave + NW - 1) / NW;
+    const int ldl = ks + 8;
+    // weights of the 16 columns over this K range, one 1 KB fragment per wave load
+    const bf16_t* wp = a.W + ((size_t)tile * (K >> 5) + (kb >> 5)) * 512 + lane * 8;
+    uint4 wv[MAXF];
+#pragma unroll
+    for (int i = 0; i < MAXF; ++i) {
+        const int f = min(wave + NW * i, nfrag - 1);
+        wv[i] = *reinterpret_cast<const uint4*>(wp + (size_t)f * 512);
+    }
+    const int em = r, en = tile * 16 + 4 * g;
+    EpiPartRes::Pre pre{};
+    if (wave == 0) pre = epi.prefetch(min(em, M - 1), min(en, N - 1), split);
+    __builtin_amdgcn_sched_barrier(0);
+    // the hidden rows [0, M) x [kb, kb + ks), polled (bounded)
+    const int cpr = ks >> 3, total = M * cpr;
+    uint64_t xv[XI][2];
+#pragma unroll
+    for (int i = 0; i < XI; ++i) xv[i][0] = xv[i][1] = 0;
+    bool ready = false;
+    for (int s = 0; s < fs.spin; ++s) {
+        bool marked = false;
+#pragma unroll
+        for (int i = 0; i < XI; ++i) {
+            const int idx = min(tid + T * i, total - 1);
+            const int m = udiv_small(idx, cpr), c = (idx - m * cpr) * 8;
+            const uint64_t* p = reinterpret_cast<const uint64_t*>(a.x + (size_t)m * a.ldx + kb + c);
+            xv[i][0] = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            xv[i][1] = __hip_atomic_load(p + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            marked |= ffn_marked(xv[i][0]) || ffn_marked(xv[i][1]);
+        }
+        if (__all(!marked)) { ready = true; break; }
+        __builtin_amdgcn_s_sleep(2);
+    }
+    if (!ready && lane == 0) atomicAdd(fs.err, 1u);
+#pragma unroll
+    for (int i = 0; i < XI; ++i) {
+        const int idx = tid + T * i;
+        if (idx < total) {
+            const int m = udiv_small(idx, cpr), c = (idx - m * cpr) * 8;
+            *reinterpret_cast<uint4*>(xs + (size_t)m * ldl + c) =
+                make_uint4((uint32_t)xv[i][0], (uint32_t)(xv[i][0] >> 32), (uint32_t)xv[i][1],
+                           (uint32_t)(xv[i][1] >> 32));
+        }
+    }
+    __syncthreads();
+    f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < MAXF; ++i)
+        if (i < nf) {
+            const int f = wave + NW * i;
+            const bf16x8_t xf = *reinterpret_cast<const bf16x8_t*>(xs + (size_t)r * ldl + f * 32 + g * 8);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, wv[i]), xf, acc, 0, 0, 0);
+        }
+    red2[wave * 64 + lane] = acc;
+    __syncthreads();
+    if (wave == 0 && em < M && en < N) {
+        f32x4_t sum = red2[lane];
+#pragma unroll
+        for (int w = 1; w < NW; ++w) sum += red2[w * 64 + lane];
+        const float v[4] = {sum[0], sum[1], sum[2], sum[3]};
+        epi.store(pre, em, en, v, split);
+    }
+}
+
+// LN2 + FFN1 + GELU and FFN2 of a small batch in one launch.  Workgroups
+// j < d_ff / 16 are FFN1 column tiles (the plain GEMV with its LayerNorm
+// prologue); the rest are FFN2 workgroups (column tile c / 4, K range
+// c % 4), which start with FFN1, stream their weights meanwhile and wait
+// only for the FFN1 tiles of their K range.  Those tiles lie on every XCD,
+// so the hand-off goes through memory (device-scope stores and loads);
+// it needs no flag: the rows themselves start as the sentinel.  FFN1
+// workgroups precede every FFN2 workgroup in dispatch order and wait for
+// nothing, so a waiting FFN2 workgroup never holds a CU an FFN1 tile still
+// needs.  Each FFN1 tile also refills its columns of the next launch's
+// rows (all 16 rows) with the sentinel, after its own work.
+template <int MR, int MAXF2>
+__global__ __launch_bounds__(64 * GV_NW) void ffn_chain_kernel(GemvArgs a1, EpiGeluShared e1, GemvArgs a2,
+                                                                EpiPartRes e2, FfnSync fs) {
+    const int j = blockIdx.x;
+    const int n_prod = a1.N >> 4;
+    if (j < n_prod) {
+        gemv_body<MR, 1, 32 / GV_NW, 1, 1, GV_NW, EpiGeluShared>(a1, e1, j, 0, 1);
+        if (threadIdx.x >= 64 && threadIdx.x < 128) {
+            const int l = threadIdx.x - 64;
+            *reinterpret_cast<uint2*>(fs.next + (size_t)(l >> 2) * a1.ldo + j * 16 + (l & 3) * 4) =
+                make_uint2(0xFFFFFFFFu, 0xFFFFFFFFu);
+        }
+    } else {
+        const int c = j - n_prod;
+        ffn2_chain_body<MR, MAXF2, GV_NW>(a2, e2, c >> 2, c & 3, fs);
+    }
+}
+
 // Records, for each residue j % 8 of the workgroups of a launch of 1024
 // threads, the set of XCDs (a bit each) they ran on.
 __global__ __launch_bounds__(1024) void xcd_deal_check_kernel(unsigned* masks) {
@@ -671,6 +863,44 @@ hipError_t qkv_front(hipStream_t st, const GemvArgs& a, const AttnMfmaArgs& p, c
     const bool pd2 = p.split_len == 512;
     if (a.xmode == 2) return pd2 ? qkv_front_mr<2, 2>(st, a, e, p, fs) : qkv_front_mr<2, 1>(st, a, e, p, fs);
     return pd2 ? qkv_front_mr<1, 2>(st, a, e, p, fs) : qkv_front_mr<1, 1>(st, a, e, p, fs);
+}
+
+bool ffn_chain_ok(int rows, int d, int d_ff) {
+    return rows >= 1 && rows <= 16 && d >= 256 && d <= 1024 && d % 256 == 0 && d_ff >= 512 && d_ff % 512 == 0 &&
+           d_ff / 4 <= 2 * GV_NW * 32;
+}
+
+template <int MR>
+static hipError_t ffn_chain_go(hipStream_t st, const GemvArgs& a1, const EpiGeluShared& e1, const GemvArgs& a2,
+                               const EpiPartRes& e2, const FfnSync& fs) {
+    // the static LDS (two 16 KB reduction arrays) and this together stay
+    // within the CU's 160 KB: raise the dynamic limit only as far as needed
+    const size_t lds = (size_t)16 * (std::max(a1.K, a2.K / 4) + 8) * 2;
+    static size_t attr_set = 32 * 1024;
+    if (lds > attr_set) {
+        hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(&ffn_chain_kernel<MR, 2>),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (err != hipSuccess) return err;
+        attr_set = lds;
+    }
+    const int grid = a1.N / 16 + (a2.N / 16) * 4;
+    hipLaunchKernelGGL((ffn_chain_kernel<MR, 2>), dim3(grid), dim3(64 * GV_NW), lds, st, a1, e1, a2, e2, fs);
+    return hipGetLastError();
+}
+
+hipError_t ffn_chain(hipStream_t st, const GemvArgs& a1, const GemvArgs& a2, const FfnSync& fs) {
+    if (a1.epi != EPI_GELU || a1.xmode != 1 || a2.epi != EPI_PARTIAL || a2.xmode != 0 || a1.M != a2.M ||
+        !ffn_chain_ok(a1.M, a1.K, a1.N) || a2.K != a1.N || a2.N != a1.K || a1.ldo != a1.N || a2.ldx != a1.N ||
+        a2.x != a1.out || !a1.out || !a2.part || !a2.part_out || a2.part == a2.part_out || a2.part_rows < a2.M ||
+        !fs.next || fs.next == a1.out || !fs.err || fs.spin < 0)
+        return hipErrorInvalidValue;
+    EpiGeluShared e1{(bf16_t*)a1.out, a1.bias, a1.ldo};
+    EpiPartRes e2{a2.part_out, a2.N, a2.M, a2.part, a2.part_rows, a2.bias};
+    if (a1.M <= 1) return ffn_chain_go<1>(st, a1, e1, a2, e2, fs);
+    if (a1.M <= 2) return ffn_chain_go<2>(st, a1, e1, a2, e2, fs);
+    if (a1.M <= 4) return ffn_chain_go<4>(st, a1, e1, a2, e2, fs);
+    if (a1.M <= 8) return ffn_chain_go<8>(st, a1, e1, a2, e2, fs);
+    return ffn_chain_go<16>(st, a1, e1, a2, e2, fs);
 }
 
 hipError_t xcd_deal_check(hipStream_t st, unsigned* masks, int grid) {

@@ -81,6 +81,17 @@ struct FrontSync {
     int spin;             // polls before a hand-off wait gives up (0: at once)
 };
 
+// Hand-off state of the chained FFN (ffn_chain): the FFN1 workgroups store
+// the hidden rows of this launch's set (GemvArgs::out of FFN1, ::x of FFN2:
+// [16][d_ff] bf16, which held the sentinel 0xFFFF everywhere when the launch
+// began) and refill the next launch's set with the sentinel; the FFN2
+// workgroups poll their K range of the rows until no sentinel is left.
+struct FfnSync {
+    bf16_t* next;         // [16][d_ff]: the next launch's set
+    unsigned* err;        // polls that ran out (a bounded wait; none expected)
+    int spin;             // polls before a wait gives up (0: at once)
+};
+
 struct AttnMfmaArgs {
     int mode;
     int n_tiles;
@@ -153,6 +164,16 @@ int qkv_attn_split_len(int64_t max_ctx, int n_splits);
 // (xcd_deal_check).
 hipError_t qkv_front(hipStream_t st, const GemvArgs& a, const AttnMfmaArgs& p, const FrontSync& fs);
 bool qkv_front_ok(int rows, int d, int n_heads, int batch, int split_len, int n_splits);
+// LN2 + FFN1 + GELU, then FFN2 into four split-K partials, in one launch
+// (gemv.hip): a1 the GemvArgs of the EPI_GELU launch (xmode 1, rows <= 16,
+// d <= 1024) with a1.out the rows of this launch's set, a2 those of the
+// EPI_PARTIAL launch (xmode 0, x = a1.out, ldx = d_ff) whose split-K
+// partials go to a2.part_out, and whose first K range adds the bias and the
+// residual input, the sum of the four partials of a2.part (a2.part_rows
+// rows per split) that FFN1's LayerNorm also reads; a2.part_out must not be
+// a2.part.  Every set starts filled with the sentinel (see FfnSync).
+hipError_t ffn_chain(hipStream_t st, const GemvArgs& a1, const GemvArgs& a2, const FfnSync& fs);
+bool ffn_chain_ok(int rows, int d, int d_ff);
 // ORs into masks[r] (8 words) a bit per XCD that a workgroup j of a
 // `grid`-workgroup launch with j % 8 == r ran on.
 hipError_t xcd_deal_check(hipStream_t st, unsigned* masks, int grid);

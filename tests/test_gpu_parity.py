@@ -340,6 +340,9 @@ def test_valle_batch2_k8_sixteen_rows():
 #    whose attention workgroups wait for their head's QKV columns, with 256-
 #    or 512-key splits (MTP_FRONT=256 / 512 force one);
 #  * separate QKV and attention launches (MTP_FRONT=0);
+#  * every one of them with FFN1 and FFN2 in one launch whose FFN2
+#    workgroups wait for their K range (the default), and the chained front
+#    or separate launches with two FFN launches (MTP_FFN_CHAIN=0);
 #  * one launch for LN1, QKV and the attention over the cached keys with 8 or
 #    16 workgroups per head (MTP_QKV_ATTN=8 / 16; the out-projection then
 #    merges the chunk's own keys).
@@ -358,12 +361,14 @@ FRONT_CASES = {
 
 
 FRONT_ENV = {"separate": {"MTP_FRONT": "0"}, "chain": {}, "chain256": {"MTP_FRONT": "256"},
-             "chain512": {"MTP_FRONT": "512"}, "8": {"MTP_QKV_ATTN": "8"}, "16": {"MTP_QKV_ATTN": "16"}}
+             "chain512": {"MTP_FRONT": "512"}, "8": {"MTP_QKV_ATTN": "8"}, "16": {"MTP_QKV_ATTN": "16"},
+             "ffn2": {"MTP_FFN_CHAIN": "0"}, "unchained": {"MTP_FRONT": "0", "MTP_FFN_CHAIN": "0"}}
 
 
 def set_front(monkeypatch, front):
     monkeypatch.delenv("MTP_FRONT", raising=False)
     monkeypatch.delenv("MTP_QKV_ATTN", raising=False)
+    monkeypatch.delenv("MTP_FFN_CHAIN", raising=False)
     for k, v in FRONT_ENV[front].items():
         monkeypatch.setenv(k, v)
 
@@ -411,11 +416,11 @@ def test_fused_front_eager_and_graph_agree(front, monkeypatch):
 
 
 def test_front_wait_that_runs_out_is_reported(monkeypatch):
-    """The one-launch front's hand-off waits, set from the host to give up
-    at once (MTP_FRONT_SPIN=0: every kernel still runs to its end), make the
-    step return MTP_ETIMEOUT; the context then refuses to step until a new
-    prefill, after which it runs separate QKV and attention launches and
-    gives bit for bit the tokens and logits of a context that always did."""
+    """The one-launch front's and chained FFN's waits, set from the host to
+    give up at once (MTP_FRONT_SPIN=0: every kernel still runs to its end),
+    make the step return MTP_ETIMEOUT; the context then refuses to step
+    until a new prefill, after which it runs separate launches and gives bit
+    for bit the tokens and logits of a context that always did."""
     from paper_2410_13839_amd.binding import MTP_ESTATE, MTP_ETIMEOUT, MTPError
     shape, K, top_k, B, phon, ac = FRONT_CASES["d512_b2_k4"]
     wl = Workload("front_timeout", shape, K=K, top_k=top_k, batch=B, phon_len=phon, ac_len=ac, max_new=48,
@@ -429,6 +434,7 @@ def test_front_wait_that_runs_out_is_reported(monkeypatch):
     monkeypatch.delenv("MTP_FRONT_SPIN")
     s.prefill(pr.phon, pr.ac)
     s.step(K, top_k)            # the first step after a prefill runs no trunk layer
+    # (both one-launch kinds give up: the front and the chained FFN)
     with pytest.raises(MTPError) as e:
         s.step(K, top_k)
     assert e.value.code == MTP_ETIMEOUT
@@ -438,7 +444,7 @@ def test_front_wait_that_runs_out_is_reported(monkeypatch):
     runs = []
     for sess in (s, None):
         if sess is None:
-            set_front(monkeypatch, "separate")
+            set_front(monkeypatch, "unchained")
             sess = new_session(wl, w, logq)
         sess.prefill(pr.phon, pr.ac)
         logs = []
@@ -503,11 +509,12 @@ def test_replay_timing_then_prefill_again():
     s = new_session(wl, w, logq)
     ref = run(s, 6)
     # the classes the step launched: the front is one launch (class 10) or
-    # the QKV projection and the attention (3 and 4); the others raise
-    # MTP_ESTATE.  Replaying the one-launch front also runs its hand-off
-    # flags through many launches in a row, which the next generation checks.
+    # the QKV projection and the attention (3 and 4), the FFN one launch (11)
+    # or two (1 and 2); the others raise MTP_ESTATE.  Replaying the one-launch
+    # kinds also runs their hand-off state through many launches in a row,
+    # which the next generation checks.
     replayed = []
-    for kc in range(1, 11):
+    for kc in range(1, 12):
         for cold in (True, False):
             try:
                 us = s.replay(kc, 3, cold)
@@ -517,7 +524,7 @@ def test_replay_timing_then_prefill_again():
             assert 0.5 < us < 1000.0, (kc, cold, us)
             replayed.append(kc)
     replayed = sorted(set(replayed))
-    assert replayed in ([1, 2, 5, 6, 7, 10], [1, 2, 3, 4, 5, 6, 7]), replayed
+    assert replayed in ([5, 6, 7, 10, 11], [3, 4, 5, 6, 7, 11], [1, 2, 5, 6, 7, 10], [1, 2, 3, 4, 5, 6, 7]), replayed
     with pytest.raises(MTPError) as e:
         s.step(wl.K, wl.top_k)
     assert e.value.code == MTP_ESTATE
