@@ -660,25 +660,44 @@ __device__ __forceinline__ void ffn2_chain_body(const GemvArgs& a, const EpiPart
     EpiPartRes::Pre pre{};
     if (wave == 0) pre = epi.prefetch(min(em, M - 1), min(en, N - 1), split);
     __builtin_amdgcn_sched_barrier(0);
-    // the hidden rows [0, M) x [kb, kb + ks), polled (bounded)
+    // the hidden rows [0, M) x [kb, kb + ks): while FFN1 runs, wave 0 polls
+    // one word of each FFN1 tile of the range (a few hundred bytes a round,
+    // instead of every row chunk of every wave competing with FFN1's weight
+    // stream); then the waves that hold row chunks poll those until none
+    // holds the sentinel.  Both waits are bounded; one that runs out is
+    // counted.
     const int cpr = ks >> 3, total = M * cpr;
     uint64_t xv[XI][2];
 #pragma unroll
     for (int i = 0; i < XI; ++i) xv[i][0] = xv[i][1] = 0;
-    bool ready = false;
-    for (int s = 0; s < fs.spin; ++s) {
-        bool marked = false;
-#pragma unroll
-        for (int i = 0; i < XI; ++i) {
-            const int idx = min(tid + T * i, total - 1);
-            const int m = udiv_small(idx, cpr), c = (idx - m * cpr) * 8;
-            const uint64_t* p = reinterpret_cast<const uint64_t*>(a.x + (size_t)m * a.ldx + kb + c);
-            xv[i][0] = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            xv[i][1] = __hip_atomic_load(p + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            marked |= ffn_marked(xv[i][0]) || ffn_marked(xv[i][1]);
+    bool ready = true;
+    if (wave == 0) {
+        const uint64_t* probe = reinterpret_cast<const uint64_t*>(a.x + kb + 16 * min(lane, (ks >> 4) - 1));
+        ready = false;
+        for (int s = 0; s < fs.spin; ++s) {
+            const uint64_t v = __hip_atomic_load(probe, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (__all(!ffn_marked(v))) { ready = true; break; }
+            __builtin_amdgcn_s_sleep(2);
         }
-        if (__all(!marked)) { ready = true; break; }
-        __builtin_amdgcn_s_sleep(2);
+    }
+    __syncthreads();
+    if (wave * 64 < total) {              // uniform: the wave holds row chunks
+        bool done = false;
+        for (int s = 0; s < fs.spin; ++s) {
+            bool marked = false;
+#pragma unroll
+            for (int i = 0; i < XI; ++i) {
+                const int idx = min(tid + T * i, total - 1);
+                const int m = udiv_small(idx, cpr), c = (idx - m * cpr) * 8;
+                const uint64_t* p = reinterpret_cast<const uint64_t*>(a.x + (size_t)m * a.ldx + kb + c);
+                xv[i][0] = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                xv[i][1] = __hip_atomic_load(p + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                marked |= ffn_marked(xv[i][0]) || ffn_marked(xv[i][1]);
+            }
+            if (__all(!marked)) { done = true; break; }
+            __builtin_amdgcn_s_sleep(2);
+        }
+        ready = ready && done;
     }
     if (!ready && lane == 0) atomicAdd(fs.err, 1u);
 #pragma unroll
