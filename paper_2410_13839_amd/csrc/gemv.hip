@@ -651,6 +651,16 @@ __device__ __forceinline__ void ffn2_chain_body(const GemvArgs& a, const EpiPart
     // weights of the 16 columns over this K range, one 1 KB fragment per wave load
     const bf16_t* wp = a.W + ((size_t)tile * (K >> 5) + (kb >> 5)) * 512 + lane * 8;
     uint4 wv[MAXF];
+    // Up to 4 rows the kernel fits two workgroups per CU, so an FFN2
+    // workgroup shares its CU with an FFN1 tile: its weight loads wait ~1 us
+    // (2,560 clocks) so that the tile's LayerNorm rows and weights, the
+    // launch's critical path, go out first (a CU returns loads in request
+    // order).  Measured at batch 1, K = 4: 252.5 us per step with no delay,
+    // 243-244.5 us for 1,500-3,600 clocks, 254.5 us loading the weights
+    // only after the wait.  With one workgroup per CU (8 or 16 rows) the
+    // FFN2 workgroups start after FFN1 tiles end, and a delay only adds to
+    // the step (K = 8: 296.5 us without, 307.8 us with it).
+    if constexpr (MR <= 4) __builtin_amdgcn_s_sleep(40);
 #pragma unroll
     for (int i = 0; i < MAXF; ++i) {
         const int f = min(wave + NW * i, nfrag - 1);
