@@ -347,8 +347,9 @@ def test_valle_batch2_k8_sixteen_rows():
 #    16 workgroups per head (MTP_QKV_ATTN=8 / 16; the out-projection then
 #    merges the chunk's own keys).
 FRONT_CASES = {
-    # 8 heads (grouped per XCD), 2 ragged sequences of 4 rows, contexts up to ~690 keys
-    "d512_b2_k4": (ModelShape(n_layers=2, d_model=512, n_heads=8, d_ff=1024, k_heads=4, dtype="bf16"),
+    # 8 heads (grouped per XCD), 2 ragged sequences of 4 rows, contexts up to ~690 keys;
+    # three layers, so the one-launch kinds' last layer takes the third flag / row set
+    "d512_b2_k4": (ModelShape(n_layers=3, d_model=512, n_heads=8, d_ff=1024, k_heads=4, dtype="bf16"),
                    4, 3, 2, (5, 40), (200, 600)),
     # 4 heads, one sequence of 2 rows, ~2,100 keys (more than 8 splits of 256 keys: the
     # 8-workgroup front is not available and falls back to separate launches)
