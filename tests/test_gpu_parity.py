@@ -304,6 +304,38 @@ def test_changing_K_between_steps():
     s.close()
 
 
+def test_bf16_changing_K_between_steps():
+    """The same on a small bf16 decoder whose decode layers run the one-launch
+    front and chained FFN (8 heads, three layers, one sequence at ~350 keys:
+    two key splits): the pending chunk changes size every step (1 to 4 rows),
+    so each step runs another plan over the same hand-off words and row sets;
+    logits within 3e-2 of the oracle on the same history, selection exact."""
+    shape = ModelShape(n_layers=3, d_model=512, n_heads=8, d_ff=1024, k_heads=4, dtype="bf16")
+    wl = Workload("varK_bf16", shape, K=4, top_k=3, batch=1, phon_len=(20, 30), ac_len=(300, 330), max_new=40,
+                  eos_min=40)
+    w = make_weights(shape, seed=37)
+    logq = make_logq()
+    pr = make_prompts(wl)
+    s = new_session(wl, w, logq)
+    s.prefill(pr.phon, pr.ac)
+    model = ARDecoder(shape, w)
+    emitted = []
+    max_err = 0.0
+    for K in (4, 1, 2, 4, 3, 1, 4, 2):
+        gen = s.seq_state()["gen"].copy()
+        tok, cnt = s.step(K, 3)
+        lg = s.logits(K)
+        ref = oracle_logits_at(model, pr.phon[0], pr.ac[0], emitted, K)
+        err = float(np.abs(ref - lg[0]).max())
+        max_err = max(max_err, err)
+        assert err <= 3e-2, (K, err)
+        emitted.extend(int(x) for x in tok[0][:cnt[0]])
+        assert_selection_exact(lg, s.lattice(K, 3), logq, 3, gen, wl.eos_min, EOS_ID, np.ones(1, bool))
+    assert s.seq_state()["gen"][0] == 21
+    s.close()
+    log(f"bf16 changing K: max logit err {max_err:.3g}")
+
+
 def test_valle_k4_bf16_batch1():
     """12-layer d1024 bf16 decoder, K=4, top_k=4, batch 1, up to 750 tokens
     with EOS allowed from index 600: selection exact at every step, logits
