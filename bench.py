@@ -646,13 +646,13 @@ def main():
                          "bytes_per_launch": nbytes, "GB_s": round(nbytes / (us * 1e-6) / 1e9, 1),
                          "share_of_step": round(us * per_step(L) / (ms_step * 1000.0), 3),
                          "avg_launch_us_cache_warm": round(warm[kc], 3) if warm[kc] == warm[kc] else None}
-    # dominant kernel class: the largest time per step; classes within 5% of
-    # it are too close to rank by one measurement, and of those the one
-    # furthest below its roofline is reported (the conservative choice)
+    # dominant kernel class: the largest time per step (the rocprofv3
+    # summary's top kernel); the classes within 5% of it, too close to rank
+    # by one measurement, are listed beside it, and every class's fraction
     per_step = {kc: times[kc] * KCLASSES[kc][1](L) for kc in times}
     top = max(per_step.values())
     near = [kc for kc in per_step if per_step[kc] >= 0.95 * top]
-    dom = min(near, key=lambda kc: kernels[KCLASSES[kc][0]]["GB_s"])
+    dom = max(per_step, key=lambda kc: per_step[kc])
     dname = KCLASSES[dom][0]
     dk = kernels[dname]
     roof = {"kernel": dname, "bound": "hbm", "achieved": dk["GB_s"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -660,7 +660,7 @@ def main():
             "bytes_per_launch": dk["bytes_per_launch"], "avg_launch_us": dk["avg_launch_us"],
             "measured": f"{passes} passes over the {KCLASSES[dom][1](L)} launches of one step at step {mid} "
                         f"(context {ctx} tokens), caches evicted before each pass, HIP events on the library stream",
-            "selection": "largest time per step; among classes within 5% of it, the lowest fraction",
+            "selection": "largest time per step; near_dominant: the classes within 5% of it",
             "near_dominant": [KCLASSES[kc][0] for kc in near],
             "classes_frac": {KCLASSES[kc][0]: round(kernels[KCLASSES[kc][0]]["GB_s"] / HBM_PEAK_GBS, 4)
                              for kc in times}}
