@@ -686,9 +686,10 @@ int plan_splits(mtp_ctx* c, int Q) {
     // attention workgroups wait for their own head's columns (qkv_front).
     // Keys per split: 256 (one 16-key group per wave of 16), or 512 when
     // that keeps the splits within what the out-projection merges (at 256,
-    // batch 1, K = 4: 280 us per step against 294 at 512, although 256 puts
-    // a few more workgroups in the launch than there are CUs).  At least two
-    // layers: consecutive launches alternate their hand-off flag sets.
+    // batch 1, K = 4: 244.7 us per step against 263.8 at 512, K = 8: 296.4
+    // against 299.8, although 256 puts a few more workgroups in the launch
+    // than there are CUs at the longest contexts).  At least two layers:
+    // consecutive launches alternate their hand-off flag sets.
     const char* fenv = getenv("MTP_FRONT");
     if (cf.dtype == MTP_DTYPE_BF16 && Q > 0 && !(cf.flags & MTP_FLAG_NAR) && rows <= 16 && cf.n_layers >= 2 &&
         !(fenv && atoi(fenv) == 0)) {
