@@ -448,12 +448,14 @@ def test_fused_front_eager_and_graph_agree(front, monkeypatch):
     assert np.array_equal(out[0][1].view(np.uint32), out[1][1].view(np.uint32))
 
 
-def test_front_wait_that_runs_out_is_reported(monkeypatch):
-    """The one-launch front's and chained FFN's waits, set from the host to
-    give up at once (MTP_FRONT_SPIN=0: every kernel still runs to its end),
-    make the step return MTP_ETIMEOUT; the context then refuses to step
-    until a new prefill, after which it runs separate launches and gives bit
-    for bit the tokens and logits of a context that always did."""
+@pytest.mark.parametrize("front", ["chain", "separate"])
+def test_front_wait_that_runs_out_is_reported(front, monkeypatch):
+    """The one-launch front's and chained FFN's waits (with `separate`, the
+    chained FFN's alone), set from the host to give up at once
+    (MTP_FRONT_SPIN=0: every kernel still runs to its end), make the step
+    return MTP_ETIMEOUT; the context then refuses to step until a new
+    prefill, after which it runs separate launches and gives bit for bit the
+    tokens and logits of a context that always did."""
     from paper_2410_13839_amd.binding import MTP_ESTATE, MTP_ETIMEOUT, MTPError
     shape, K, top_k, B, phon, ac = FRONT_CASES["d512_b2_k4"]
     wl = Workload("front_timeout", shape, K=K, top_k=top_k, batch=B, phon_len=phon, ac_len=ac, max_new=48,
@@ -461,13 +463,12 @@ def test_front_wait_that_runs_out_is_reported(monkeypatch):
     w = make_weights(shape)
     pr = make_prompts(wl)
     logq = make_logq()
-    set_front(monkeypatch, "chain")
+    set_front(monkeypatch, front)
     monkeypatch.setenv("MTP_FRONT_SPIN", "0")
     s = new_session(wl, w, logq)
     monkeypatch.delenv("MTP_FRONT_SPIN")
     s.prefill(pr.phon, pr.ac)
     s.step(K, top_k)            # the first step after a prefill runs no trunk layer
-    # (both one-launch kinds give up: the front and the chained FFN)
     with pytest.raises(MTPError) as e:
         s.step(K, top_k)
     assert e.value.code == MTP_ETIMEOUT
