@@ -588,7 +588,7 @@ def bench_nar(torch, reps, cpu):
 def main():
     args = _parse()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported by this build "
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               f"(the decode path runs on a single MI355X).", file=sys.stderr)
         sys.exit(2)
     import torch
