@@ -66,6 +66,36 @@ __device__ __forceinline__ uint32_t bf16x2_bits(float lo, float hi) {
     return __builtin_bit_cast(uint32_t, __builtin_convertvector((f2_t){lo, hi}, b2_t));
 }
 
+// Split-K partial rows of the small-M projections (four K ranges, `rows`
+// rows of `ld` floats each): the first range, which carries the residual
+// input and the bias, in float32 at `part`; ranges 1..3 in bfloat16 after
+// it ([3][rows][ld]), half the bytes for the LayerNorm prologues that read
+// all four.
+__device__ __forceinline__ void store_partial4(float* part, int split, int rows, int ld, int m, int n,
+                                               float4 o) {
+    if (split == 0) {
+        *reinterpret_cast<float4*>(part + (size_t)m * ld + n) = o;
+    } else {
+        bf16_t* ph = reinterpret_cast<bf16_t*>(part + (size_t)rows * ld);
+        *reinterpret_cast<uint2*>(ph + ((size_t)(split - 1) * rows + m) * ld + n) =
+            make_uint2(bf16x2_bits(o.x, o.y), bf16x2_bits(o.z, o.w));
+    }
+}
+// Range 0 of row m, columns c .. c + 3, as float32
+__device__ __forceinline__ float4 load_partial0(const float* part, int ld, int m, int c) {
+    return *reinterpret_cast<const float4*>(part + (size_t)m * ld + c);
+}
+// Range s (1..3) of row m, columns c .. c + 3, as the raw bfloat16 bits
+// (converted where the values are used, so the load needs no wait)
+__device__ __forceinline__ uint2 load_partial_bits(const float* part, int s, int rows, int ld, int m, int c) {
+    const bf16_t* ph = reinterpret_cast<const bf16_t*>(part + (size_t)rows * ld);
+    return *reinterpret_cast<const uint2*>(ph + ((size_t)(s - 1) * rows + m) * ld + c);
+}
+__device__ __forceinline__ float4 bf16x4_to_f32(uint2 u) {
+    return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xFFFF0000u), __uint_as_float(u.y << 16),
+                       __uint_as_float(u.y & 0xFFFF0000u));
+}
+
 // Element (row, k) of a bf16 activation matrix with K columns (K a multiple
 // of 32) stored in MFMA fragment order, the order of the packed weights: 16 x
 // 32 blocks of 1 KB, block (row / 16, k / 32) at ((row / 16) * (K / 32) +

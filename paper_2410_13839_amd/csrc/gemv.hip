@@ -166,9 +166,10 @@ struct EpiGeluShared {
     }
 };
 
-// split-K partial sums of the out-projection / FFN2: part[split][m][n]; the
-// first K range also carries the residual input row and the bias, so the
-// four partials sum to the complete new residual row
+// split-K partial sums of the out-projection / FFN2 (store_partial4: range
+// 0 in float32, ranges 1..3 in bfloat16); the first K range also carries
+// the residual input row and the bias, so the four partials sum to the
+// complete new residual row
 struct EpiPart {
     float* part;
     int ldp;        // N (= d)
@@ -193,7 +194,7 @@ struct EpiPart {
             o.z += p.b.z + p.x.z;
             o.w += p.b.w + p.x.w;
         }
-        *reinterpret_cast<float4*>(part + ((size_t)split * M + m) * ldp + n) = o;
+        store_partial4(part, split, M, ldp, m, n, o);
     }
 };
 
@@ -208,31 +209,34 @@ struct EpiPartRes {
     const float* pin;     // [4][pin_rows][ldp]: the out-projection's partials
     int pin_rows;
     const float* bias;    // [N]
-    struct Pre { float4 b, p[4]; };
+    // the previous projection's range 0 and the raw bits of ranges 1..3
+    // (converted in store(), so the loads need no wait here)
+    struct Pre { float4 b, p0; uint2 ph[3]; };
     __device__ __forceinline__ Pre prefetch(int m, int n, int split) const {
         Pre q;
         const int nn = min(n, ldp - 4);
         q.b = *reinterpret_cast<const float4*>(bias + nn);
         if (split == 0) {
+            q.p0 = load_partial0(pin, ldp, m, nn);
 #pragma unroll
-            for (int s2 = 0; s2 < 4; ++s2)
-                q.p[s2] = *reinterpret_cast<const float4*>(pin + ((size_t)s2 * pin_rows + m) * ldp + nn);
+            for (int s2 = 1; s2 < 4; ++s2) q.ph[s2 - 1] = load_partial_bits(pin, s2, pin_rows, ldp, m, nn);
         }
         return q;
     }
     __device__ __forceinline__ void store(const Pre& q, int m, int n, const float (&v)[4], int split) const {
         float4 o = make_float4(v[0], v[1], v[2], v[3]);
         if (split == 0) {
-            const float x0 = (q.p[0].x + q.p[1].x) + (q.p[2].x + q.p[3].x);
-            const float x1 = (q.p[0].y + q.p[1].y) + (q.p[2].y + q.p[3].y);
-            const float x2 = (q.p[0].z + q.p[1].z) + (q.p[2].z + q.p[3].z);
-            const float x3 = (q.p[0].w + q.p[1].w) + (q.p[2].w + q.p[3].w);
+            const float4 p1 = bf16x4_to_f32(q.ph[0]), p2 = bf16x4_to_f32(q.ph[1]), p3 = bf16x4_to_f32(q.ph[2]);
+            const float x0 = (q.p0.x + p1.x) + (p2.x + p3.x);
+            const float x1 = (q.p0.y + p1.y) + (p2.y + p3.y);
+            const float x2 = (q.p0.z + p1.z) + (p2.z + p3.z);
+            const float x3 = (q.p0.w + p1.w) + (p2.w + p3.w);
             o.x += q.b.x + x0;
             o.y += q.b.y + x1;
             o.z += q.b.z + x2;
             o.w += q.b.w + x3;
         }
-        *reinterpret_cast<float4*>(part + ((size_t)split * M + m) * ldp + n) = o;
+        store_partial4(part, split, M, ldp, m, n, o);
     }
 };
 
@@ -314,11 +318,12 @@ __device__ __forceinline__ void gemv_body(const GemvArgs& a, const Epi& epi, con
     // ---- A. activation-side loads (compact, from clamped addresses; branches
     //      only on wave-uniform conditions, which cost no extra waits) ----
     // LayerNorm rows (XM 1..3): the register arrays are the kernel's own
-    float4 ln_hv[Rows::RPT], ln_pv[Rows::RES ? 4 : 1][Rows::RES ? Rows::RPT : 1], ln_zv[XM == 3 ? Rows::RPT : 1];
+    float4 ln_hv[Rows::RPT], ln_pv[Rows::RES ? Rows::RPT : 1], ln_zv[XM == 3 ? Rows::RPT : 1];
+    uint2 ln_ph[Rows::RES ? 3 : 1][Rows::RES ? Rows::RPT : 1];
     uint2 ln_ee[XM == 2 ? Rows::RPT : 1], ln_ep[XM == 2 ? Rows::RPT : 1];
     bool ln_eok[XM == 2 ? Rows::RPT : 1];
     int ln_pl[XM == 3 ? Rows::RPT : 1];
-    Rows lr{ln_hv, ln_pv, ln_zv, ln_ee, ln_ep, ln_eok, ln_pl};
+    Rows lr{ln_hv, ln_pv, ln_ph, ln_zv, ln_ee, ln_ep, ln_eok, ln_pl};
     // bf16 chunks (XM 0) as one vector value: an array of uint4 held across
     // the barrier below is demoted to scratch by the compiler
     typedef unsigned int xq_t __attribute__((ext_vector_type(4 * XI)));
@@ -651,16 +656,17 @@ __device__ __forceinline__ void ffn2_chain_body(const GemvArgs& a, const EpiPart
     // weights of the 16 columns over this K range, one 1 KB fragment per wave load
     const bf16_t* wp = a.W + ((size_t)tile * (K >> 5) + (kb >> 5)) * 512 + lane * 8;
     uint4 wv[MAXF];
-    // Up to 4 rows the kernel fits two workgroups per CU, so an FFN2
-    // workgroup shares its CU with an FFN1 tile: its weight loads wait ~1 us
-    // (2,560 clocks) so that the tile's LayerNorm rows and weights, the
-    // launch's critical path, go out first (a CU returns loads in request
-    // order).  Measured at batch 1, K = 4: 252.5 us per step with no delay,
-    // 243-244.5 us for 1,500-3,600 clocks, 254.5 us loading the weights
-    // only after the wait.  With one workgroup per CU (8 or 16 rows) the
-    // FFN2 workgroups start after FFN1 tiles end, and a delay only adds to
-    // the step (K = 8: 296.5 us without, 307.8 us with it).
-    if constexpr (MR <= 4) __builtin_amdgcn_s_sleep(40);
+    // Up to 8 rows the kernel fits two workgroups per CU (at most 60
+    // registers), so an FFN2 workgroup shares its CU with an FFN1 tile: its
+    // weight loads wait ~1 us (2,560 clocks) so that the tile's LayerNorm
+    // rows and weights, the launch's critical path, go out first (a CU
+    // returns loads in request order).  Measured at batch 1, K = 4: 252.5
+    // us per step with no delay, 243-244.5 us for 1,500-3,600 clocks,
+    // 254.5 us loading the weights only after the wait; K = 8: 296.4
+    // against 288.8 us.  With one workgroup per CU (16 rows) the FFN2
+    // workgroups start after FFN1 tiles end, and a delay only adds to the
+    // step.
+    if constexpr (MR <= 8) __builtin_amdgcn_s_sleep(40);
 #pragma unroll
     for (int i = 0; i < MAXF; ++i) {
         const int f = min(wave + NW * i, nfrag - 1);

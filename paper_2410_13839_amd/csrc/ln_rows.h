@@ -2,8 +2,8 @@
 // a LayerNorm input, normalised and rounded to bf16 into an LDS tile.
 //
 // Row sources (XM): 1 = the residual rows, completed here as the sum of the
-// producer's four split-K partials (the first of which carries the residual
-// input and the bias) or taken from h; 2 = token embedding + learned position
+// producer's four split-K partials (the first of which, in float32, carries
+// the residual input and the bias; the others are bfloat16) or taken from h; 2 = token embedding + learned position
 // of each pending token (first layer); 3 = the final LayerNorm input of each
 // sequence's last pending row (heads).
 //
@@ -32,7 +32,8 @@ struct LnRows {
     static constexpr bool RES = XM == 1 || XM == 3;                    // residual completed here
     static constexpr int RPT = (MR * KCH * 256 + T - 1) / T;           // rows per thread
     float4 (&hv)[RPT];                                                  // residual / embedding rows
-    float4 (&pv)[RES ? 4 : 1][RES ? RPT : 1];                           // split-K partials of the producer
+    float4 (&pv)[RES ? RPT : 1];                                        // the producer's split-K range 0 (float32)
+    uint2 (&ph)[RES ? 3 : 1][RES ? RPT : 1];                            //   and ranges 1..3 (bfloat16 bits)
     float4 (&zv)[XM == 3 ? RPT : 1];                                    // prefill hidden state (heads, first step)
     uint2 (&emb_e)[XM == 2 ? RPT : 1];                                  // first layer: embedding,
     uint2 (&emb_p)[XM == 2 ? RPT : 1];                                  //   position rows
@@ -91,9 +92,10 @@ struct LnRows {
                     const int row = (XM == 1) ? m : ((a.Q > 0) ? m * a.Q + a.Q - 1 : 0);
                     if constexpr (XM == 3) st_pl[j] = a.st[m].pend_len;
                     if (has_part) {
+                        pv[j] = load_partial0(a.part, a.ldh, row, cc);
 #pragma unroll
-                        for (int s2 = 0; s2 < 4; ++s2)
-                            pv[s2][j] = *reinterpret_cast<const float4*>(a.part + ((size_t)s2 * a.part_rows + row) * a.ldh + cc);
+                        for (int s2 = 1; s2 < 4; ++s2)
+                            ph[s2 - 1][j] = load_partial_bits(a.part, s2, a.part_rows, a.ldh, row, cc);
                     } else {
                         hv[j] = *reinterpret_cast<const float4*>(a.h + (size_t)row * a.ldh + cc);
                     }
@@ -140,10 +142,12 @@ struct LnRows {
                 if (m < M && rg < RG) {
                     float4 x = hv[j];
                     if (has_part) {
-                        x.x = (pv[0][j].x + pv[1][j].x) + (pv[2][j].x + pv[3][j].x);
-                        x.y = (pv[0][j].y + pv[1][j].y) + (pv[2][j].y + pv[3][j].y);
-                        x.z = (pv[0][j].z + pv[1][j].z) + (pv[2][j].z + pv[3][j].z);
-                        x.w = (pv[0][j].w + pv[1][j].w) + (pv[2][j].w + pv[3][j].w);
+                        const float4 p0 = pv[j], p1 = bf16x4_to_f32(ph[0][j]), p2 = bf16x4_to_f32(ph[1][j]),
+                                     p3 = bf16x4_to_f32(ph[2][j]);
+                        x.x = (p0.x + p1.x) + (p2.x + p3.x);
+                        x.y = (p0.y + p1.y) + (p2.y + p3.y);
+                        x.z = (p0.z + p1.z) + (p2.z + p3.z);
+                        x.w = (p0.w + p1.w) + (p2.w + p3.w);
                     }
                     if constexpr (XM == 3) {
                         const int pl = st_pl[j];
@@ -154,9 +158,10 @@ struct LnRows {
                             const int row = m * a.Q + pl - 1;
                             if (has_part) {
                                 float4 p4[4];
+                                p4[0] = load_partial0(a.part, a.ldh, row, cc);
 #pragma unroll
-                                for (int s2 = 0; s2 < 4; ++s2)
-                                    p4[s2] = *reinterpret_cast<const float4*>(a.part + ((size_t)s2 * a.part_rows + row) * a.ldh + cc);
+                                for (int s2 = 1; s2 < 4; ++s2)
+                                    p4[s2] = bf16x4_to_f32(load_partial_bits(a.part, s2, a.part_rows, a.ldh, row, cc));
                                 x.x = (p4[0].x + p4[1].x) + (p4[2].x + p4[3].x);
                                 x.y = (p4[0].y + p4[1].y) + (p4[2].y + p4[3].y);
                                 x.z = (p4[0].z + p4[1].z) + (p4[2].z + p4[3].z);

@@ -101,11 +101,12 @@ __global__ __launch_bounds__(QA_T) void qkv_attn_kernel(GemvArgs a) {
 
     // ---- A. activation-side loads, before any weight load (a CU returns
     //      load data in request order) ----
-    float4 ln_hv[Rows::RPT], ln_pv[Rows::RES ? 4 : 1][Rows::RES ? Rows::RPT : 1], ln_zv[1];
+    float4 ln_hv[Rows::RPT], ln_pv[Rows::RES ? Rows::RPT : 1], ln_zv[1];
+    uint2 ln_ph[Rows::RES ? 3 : 1][Rows::RES ? Rows::RPT : 1];
     uint2 ln_ee[XM == 2 ? Rows::RPT : 1], ln_ep[XM == 2 ? Rows::RPT : 1];
     bool ln_eok[XM == 2 ? Rows::RPT : 1];
     int ln_pl[1];
-    Rows lr{ln_hv, ln_pv, ln_zv, ln_ee, ln_ep, ln_eok, ln_pl};
+    Rows lr{ln_hv, ln_pv, ln_ph, ln_zv, ln_ee, ln_ep, ln_eok, ln_pl};
     lr.init(a, tid, wave);
     lr.load(a);
     // lane b: sequence b's (ctx_len, pend_len) and the page of this wave's
