@@ -67,26 +67,32 @@ __device__ __forceinline__ uint32_t bf16x2_bits(float lo, float hi) {
 }
 
 // Split-K partial rows of the small-M projections (four K ranges, `rows`
-// rows of `ld` floats each): the first range, which carries the residual
-// input and the bias, in float32 at `part`; ranges 1..3 in bfloat16 after
-// it ([3][rows][ld]), half the bytes for the LayerNorm prologues that read
-// all four.
+// rows of `ld` floats each): [4][rows][ld] float32; or, for more than 4
+// rows (partials_bf16), the first range, which carries the residual input
+// and the bias, in float32 at `part` and ranges 1..3 in bfloat16 after it
+// ([3][rows][ld]): the LayerNorm prologues that read all four then hold
+// fewer registers, so that at 8 rows the chained FFN fits two workgroups
+// per CU.  (At 4 rows and fewer the float32 form measured faster.)  The
+// kernels take the form as a template argument BF = partials_bf16(rows).
+__host__ __device__ __forceinline__ bool partials_bf16(int rows) { return rows > 4; }
+template <bool BF>
 __device__ __forceinline__ void store_partial4(float* part, int split, int rows, int ld, int m, int n,
                                                float4 o) {
-    if (split == 0) {
-        *reinterpret_cast<float4*>(part + (size_t)m * ld + n) = o;
+    if (!BF || split == 0) {
+        *reinterpret_cast<float4*>(part + ((size_t)split * rows + m) * ld + n) = o;
     } else {
         bf16_t* ph = reinterpret_cast<bf16_t*>(part + (size_t)rows * ld);
         *reinterpret_cast<uint2*>(ph + ((size_t)(split - 1) * rows + m) * ld + n) =
             make_uint2(bf16x2_bits(o.x, o.y), bf16x2_bits(o.z, o.w));
     }
 }
-// Range 0 of row m, columns c .. c + 3, as float32
-__device__ __forceinline__ float4 load_partial0(const float* part, int ld, int m, int c) {
-    return *reinterpret_cast<const float4*>(part + (size_t)m * ld + c);
+// Range s of row m, columns c .. c + 3, as float32: range 0, or any range
+// of the float32 form
+__device__ __forceinline__ float4 load_partial_f32(const float* part, int s, int rows, int ld, int m, int c) {
+    return *reinterpret_cast<const float4*>(part + ((size_t)s * rows + m) * ld + c);
 }
-// Range s (1..3) of row m, columns c .. c + 3, as the raw bfloat16 bits
-// (converted where the values are used, so the load needs no wait)
+// Range s (1..3) of row m of the bfloat16 form, columns c .. c + 3, as the
+// raw bits (converted where the values are used, so the load needs no wait)
 __device__ __forceinline__ uint2 load_partial_bits(const float* part, int s, int rows, int ld, int m, int c) {
     const bf16_t* ph = reinterpret_cast<const bf16_t*>(part + (size_t)rows * ld);
     return *reinterpret_cast<const uint2*>(ph + ((size_t)(s - 1) * rows + m) * ld + c);

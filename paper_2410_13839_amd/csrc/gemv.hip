@@ -32,6 +32,7 @@
 // Activation rows >= M are never written to LDS: their garbage only reaches
 // output columns >= M, which are never stored.
 #include <algorithm>
+#include <type_traits>
 
 #include "attn_dec.h"
 #include "common.h"
@@ -166,10 +167,10 @@ struct EpiGeluShared {
     }
 };
 
-// split-K partial sums of the out-projection / FFN2 (store_partial4: range
-// 0 in float32, ranges 1..3 in bfloat16); the first K range also carries
-// the residual input row and the bias, so the four partials sum to the
-// complete new residual row
+// split-K partial sums of the out-projection / FFN2 in the form BF
+// (store_partial4); the first K range also carries the residual input row
+// and the bias, so the four partials sum to the complete new residual row
+template <bool BF>
 struct EpiPart {
     float* part;
     int ldp;        // N (= d)
@@ -194,14 +195,16 @@ struct EpiPart {
             o.z += p.b.z + p.x.z;
             o.w += p.b.w + p.x.w;
         }
-        store_partial4(part, split, M, ldp, m, n, o);
+        store_partial4<BF>(part, split, M, ldp, m, n, o);
     }
 };
 
 // FFN2 of the chained FFN: as EpiPart, but the residual input of the first
 // K range is the sum of the previous projection's four partials (the rows
 // FFN1's LayerNorm completes in the same launch), added in the order the
-// LayerNorm prologue adds them
+// LayerNorm prologue adds them.  BF: the partials' form (bfloat16 ranges 1..3
+// with more than 4 rows), the same for pin and part, as both have M rows.
+template <bool BF>
 struct EpiPartRes {
     float* part;          // [4][M][ldp]
     int ldp;              // N (= d)
@@ -209,38 +212,62 @@ struct EpiPartRes {
     const float* pin;     // [4][pin_rows][ldp]: the out-projection's partials
     int pin_rows;
     const float* bias;    // [N]
-    // the previous projection's range 0 and the raw bits of ranges 1..3
-    // (converted in store(), so the loads need no wait here)
-    struct Pre { float4 b, p0; uint2 ph[3]; };
+    // the previous projection's partials: range 0 and ranges 1..3 as float32,
+    // or as raw bfloat16 bits (converted in store(), so the loads need no
+    // wait here)
+    struct Pre { float4 b, p[BF ? 1 : 4]; uint2 ph[BF ? 3 : 1]; };
     __device__ __forceinline__ Pre prefetch(int m, int n, int split) const {
         Pre q;
         const int nn = min(n, ldp - 4);
         q.b = *reinterpret_cast<const float4*>(bias + nn);
         if (split == 0) {
-            q.p0 = load_partial0(pin, ldp, m, nn);
+            q.p[0] = load_partial_f32(pin, 0, pin_rows, ldp, m, nn);
 #pragma unroll
-            for (int s2 = 1; s2 < 4; ++s2) q.ph[s2 - 1] = load_partial_bits(pin, s2, pin_rows, ldp, m, nn);
+            for (int s2 = 1; s2 < 4; ++s2) {
+                if constexpr (BF) q.ph[s2 - 1] = load_partial_bits(pin, s2, pin_rows, ldp, m, nn);
+                else q.p[s2 % (BF ? 1 : 4)] = load_partial_f32(pin, s2, pin_rows, ldp, m, nn);
+            }
         }
         return q;
     }
     __device__ __forceinline__ void store(const Pre& q, int m, int n, const float (&v)[4], int split) const {
         float4 o = make_float4(v[0], v[1], v[2], v[3]);
         if (split == 0) {
-            const float4 p1 = bf16x4_to_f32(q.ph[0]), p2 = bf16x4_to_f32(q.ph[1]), p3 = bf16x4_to_f32(q.ph[2]);
-            const float x0 = (q.p0.x + p1.x) + (p2.x + p3.x);
-            const float x1 = (q.p0.y + p1.y) + (p2.y + p3.y);
-            const float x2 = (q.p0.z + p1.z) + (p2.z + p3.z);
-            const float x3 = (q.p0.w + p1.w) + (p2.w + p3.w);
+            float4 p1, p2, p3;
+            if constexpr (BF) {
+                p1 = bf16x4_to_f32(q.ph[0]);
+                p2 = bf16x4_to_f32(q.ph[1]);
+                p3 = bf16x4_to_f32(q.ph[2 % (BF ? 3 : 1)]);
+            } else {
+                p1 = q.p[1 % (BF ? 1 : 4)];
+                p2 = q.p[2 % (BF ? 1 : 4)];
+                p3 = q.p[3 % (BF ? 1 : 4)];
+            }
+            const float4 p0 = q.p[0];
+            const float x0 = (p0.x + p1.x) + (p2.x + p3.x);
+            const float x1 = (p0.y + p1.y) + (p2.y + p3.y);
+            const float x2 = (p0.z + p1.z) + (p2.z + p3.z);
+            const float x3 = (p0.w + p1.w) + (p2.w + p3.w);
             o.x += q.b.x + x0;
             o.y += q.b.y + x1;
             o.z += q.b.z + x2;
             o.w += q.b.w + x3;
         }
-        store_partial4(part, split, M, ldp, m, n, o);
+        store_partial4<BF>(part, split, M, ldp, m, n, o);
     }
 };
 
+template <class E, class = void>
+struct HeadForm { static constexpr int v = 0; };
+template <class E>
+struct HeadForm<E, std::void_t<decltype(E::PF)>> { static constexpr int v = E::PF; };
+
+// logits of the heads.  PF: the form of the split-K partials their
+// LayerNorm rows complete (store_partial4); the heads' rows are not the
+// producer's, so the host picks it from the producer's row count.
+template <int PFv>
 struct EpiLogitsB {
+    static constexpr int PF = PFv;
     float* out;
     const float* bias;
     int ldo;
@@ -291,7 +318,9 @@ __device__ __forceinline__ void gemv_body(const GemvArgs& a, const Epi& epi, con
     // shift ([2][K/4] float4, K <= 2048)
     __shared__ f32x4_t red[1024];
     constexpr bool LN = XM >= 1 && XM <= 3;
-    using Rows = LnRows<MR, LN ? XM : 1, KCH, T>;
+    // the partials' form: the heads' epilogue names it (their rows are not
+    // the producer's); elsewhere it follows from MR (M > 4 iff MR > 4)
+    using Rows = LnRows<MR, LN ? XM : 1, KCH, T, XM == 3 ? HeadForm<Epi>::v : (MR > 4 ? 1 : 0)>;
     __shared__ float2 s_stat[NW][LN ? Rows::RPT : 1];
     constexpr int XI = (MR * MAXF + 15) / 16;                          // 16-byte chunks per thread (XM 0)
     // XM 4: the (row, float4 column chunk) items of this K range (at most
@@ -318,8 +347,8 @@ __device__ __forceinline__ void gemv_body(const GemvArgs& a, const Epi& epi, con
     // ---- A. activation-side loads (compact, from clamped addresses; branches
     //      only on wave-uniform conditions, which cost no extra waits) ----
     // LayerNorm rows (XM 1..3): the register arrays are the kernel's own
-    float4 ln_hv[Rows::RPT], ln_pv[Rows::RES ? Rows::RPT : 1], ln_zv[XM == 3 ? Rows::RPT : 1];
-    uint2 ln_ph[Rows::RES ? 3 : 1][Rows::RES ? Rows::RPT : 1];
+    float4 ln_hv[Rows::RPT], ln_pv[Rows::NPV][Rows::RES ? Rows::RPT : 1], ln_zv[XM == 3 ? Rows::RPT : 1];
+    uint2 ln_ph[Rows::NPH][Rows::RES ? Rows::RPT : 1];
     uint2 ln_ee[XM == 2 ? Rows::RPT : 1], ln_ep[XM == 2 ? Rows::RPT : 1];
     bool ln_eok[XM == 2 ? Rows::RPT : 1];
     int ln_pl[XM == 3 ? Rows::RPT : 1];
@@ -639,7 +668,7 @@ __device__ __forceinline__ bool ffn_marked(uint64_t v) {
 }
 
 template <int MR, int MAXF, int NW>
-__device__ __forceinline__ void ffn2_chain_body(const GemvArgs& a, const EpiPartRes& epi, const int tile,
+__device__ __forceinline__ void ffn2_chain_body(const GemvArgs& a, const EpiPartRes<(MR > 4)>& epi, const int tile,
                                                 const int split, const FfnSync& fs) {
     constexpr int T = 64 * NW;
     constexpr int XI = (MR * MAXF + 15) / 16;     // 16-byte row chunks per thread
@@ -673,7 +702,7 @@ __device__ __forceinline__ void ffn2_chain_body(const GemvArgs& a, const EpiPart
         wv[i] = *reinterpret_cast<const uint4*>(wp + (size_t)f * 512);
     }
     const int em = r, en = tile * 16 + 4 * g;
-    EpiPartRes::Pre pre{};
+    typename EpiPartRes<(MR > 4)>::Pre pre{};
     if (wave == 0) pre = epi.prefetch(min(em, M - 1), min(en, N - 1), split);
     __builtin_amdgcn_sched_barrier(0);
     // the hidden rows [0, M) x [kb, kb + ks): while FFN1 runs, wave 0 polls
@@ -759,7 +788,7 @@ __device__ __forceinline__ void ffn2_chain_body(const GemvArgs& a, const EpiPart
 // rows (all 16 rows) with the sentinel, after its own work.
 template <int MR, int MAXF2>
 __global__ __launch_bounds__(64 * GV_NW) void ffn_chain_kernel(GemvArgs a1, EpiGeluShared e1, GemvArgs a2,
-                                                                EpiPartRes e2, FfnSync fs) {
+                                                                EpiPartRes<(MR > 4)> e2, FfnSync fs) {
     const int j = blockIdx.x;
     const int n_prod = a1.N >> 4;
     if (j < n_prod) {
@@ -804,6 +833,8 @@ static hipError_t gemv_go(hipStream_t st, const GemvArgs& a, int splits, const E
 // LayerNorm modes: K = d_model <= 2048, one K range
 template <int XM, class Epi, int NW = GV_NW>
 static hipError_t gemv_ln(hipStream_t st, const GemvArgs& a, const Epi& e) {
+    // mode 1 reads the partials in the form its own row count implies
+    if (XM == 1 && a.part_on && partials_bf16(a.part_rows) != partials_bf16(a.M)) return hipErrorInvalidValue;
     const bool wide = a.K > 1024;
     constexpr int MF = 32 / NW;                   // fragments per wave at K = 1024
 #define MTP_GEMV_LN(MR) \
@@ -818,7 +849,8 @@ static hipError_t gemv_ln(hipStream_t st, const GemvArgs& a, const Epi& e) {
 
 // split-K partial producers (four K ranges) over bf16 rows
 template <int MR>
-static hipError_t gemv_part_rows(hipStream_t st, const GemvArgs& a, const EpiPart& e) {
+static hipError_t gemv_part_rows(hipStream_t st, const GemvArgs& a) {
+    const EpiPart<(MR > 4)> e{a.part_out, a.N, a.M, a.h, a.bias};   // M > 4 iff MR > 4
     const int per_wave = (a.K / 4 / 32 + GV_NW - 1) / GV_NW;
     if (per_wave <= 1) return gemv_go<MR, 0, 1, 1, 1>(st, a, 4, e);
     if (per_wave <= 2) return gemv_go<MR, 0, 2, 1, 1>(st, a, 4, e);
@@ -828,7 +860,8 @@ static hipError_t gemv_part_rows(hipStream_t st, const GemvArgs& a, const EpiPar
 
 // split-K partial producer over merged attention partials (K = d <= 2048)
 template <int MR, int KCH, int XM = 4>
-static hipError_t gemv_part_merge(hipStream_t st, const GemvArgs& a, const EpiPart& e) {
+static hipError_t gemv_part_merge(hipStream_t st, const GemvArgs& a) {
+    const EpiPart<(MR > 4)> e{a.part_out, a.N, a.M, a.h, a.bias};   // M > 4 iff MR > 4
     constexpr int GS = (16 / (MR * KCH)) > 0 ? 16 / (MR * KCH) : 1;
     if (a.n_splits <= 8) return gemv_go<MR, XM, 1, KCH, 8>(st, a, 4, e);
     if constexpr (8 * GS >= 16) {
@@ -907,7 +940,8 @@ bool ffn_chain_ok(int rows, int d, int d_ff) {
 
 template <int MR>
 static hipError_t ffn_chain_go(hipStream_t st, const GemvArgs& a1, const EpiGeluShared& e1, const GemvArgs& a2,
-                               const EpiPartRes& e2, const FfnSync& fs) {
+                               const FfnSync& fs) {
+    const EpiPartRes<(MR > 4)> e2{a2.part_out, a2.N, a2.M, a2.part, a2.part_rows, a2.bias};
     // the static LDS (two 16 KB reduction arrays) and this together stay
     // within the CU's 160 KB: raise the dynamic limit only as far as needed
     const size_t lds = (size_t)16 * (std::max(a1.K, a2.K / 4) + 8) * 2;
@@ -927,15 +961,15 @@ hipError_t ffn_chain(hipStream_t st, const GemvArgs& a1, const GemvArgs& a2, con
     if (a1.epi != EPI_GELU || a1.xmode != 1 || a2.epi != EPI_PARTIAL || a2.xmode != 0 || a1.M != a2.M ||
         !ffn_chain_ok(a1.M, a1.K, a1.N) || a2.K != a1.N || a2.N != a1.K || a1.ldo != a1.N || a2.ldx != a1.N ||
         a2.x != a1.out || !a1.out || !a2.part || !a2.part_out || a2.part == a2.part_out || a2.part_rows < a2.M ||
-        !fs.next || fs.next == a1.out || !fs.err || fs.spin < 0)
+        partials_bf16(a2.part_rows) != partials_bf16(a2.M) || !fs.next || fs.next == a1.out || !fs.err ||
+        fs.spin < 0)
         return hipErrorInvalidValue;
     EpiGeluShared e1{(bf16_t*)a1.out, a1.bias, a1.ldo};
-    EpiPartRes e2{a2.part_out, a2.N, a2.M, a2.part, a2.part_rows, a2.bias};
-    if (a1.M <= 1) return ffn_chain_go<1>(st, a1, e1, a2, e2, fs);
-    if (a1.M <= 2) return ffn_chain_go<2>(st, a1, e1, a2, e2, fs);
-    if (a1.M <= 4) return ffn_chain_go<4>(st, a1, e1, a2, e2, fs);
-    if (a1.M <= 8) return ffn_chain_go<8>(st, a1, e1, a2, e2, fs);
-    return ffn_chain_go<16>(st, a1, e1, a2, e2, fs);
+    if (a1.M <= 1) return ffn_chain_go<1>(st, a1, e1, a2, fs);
+    if (a1.M <= 2) return ffn_chain_go<2>(st, a1, e1, a2, fs);
+    if (a1.M <= 4) return ffn_chain_go<4>(st, a1, e1, a2, fs);
+    if (a1.M <= 8) return ffn_chain_go<8>(st, a1, e1, a2, fs);
+    return ffn_chain_go<16>(st, a1, e1, a2, fs);
 }
 
 hipError_t xcd_deal_check(hipStream_t st, unsigned* masks, int grid) {
@@ -948,23 +982,22 @@ hipError_t gemv(hipStream_t st, const GemvArgs& a) {
     if (a.M < 1 || a.M > 16 || a.N < 4 || a.K % 128) return hipErrorInvalidValue;
     if (a.epi == EPI_PARTIAL) {
         if (a.N % 4 || a.K > 4 * 8 * GV_NW * 32) return hipErrorInvalidValue;
-        EpiPart e{a.part_out, a.N, a.M, a.h, a.bias};
         if (a.xmode == 5) {
             // after qkv_attn: <= 8 rows, d <= 1024, every split word written
             if (a.M > 8 || a.K > 1024 || a.K % 256 || a.n_splits < 1 || a.Q < 1 || a.M % a.Q ||
                 a.n_splits > gemv_merge_max_splits(a.M, a.K) || a.n_splits > 16 || !a.q || !a.kvnew)
                 return hipErrorInvalidValue;
-            if (a.M <= 1) return gemv_part_merge<1, 1, 5>(st, a, e);
-            if (a.M <= 2) return gemv_part_merge<2, 1, 5>(st, a, e);
-            if (a.M <= 4) return gemv_part_merge<4, 1, 5>(st, a, e);
-            return gemv_part_merge<8, 1, 5>(st, a, e);
+            if (a.M <= 1) return gemv_part_merge<1, 1, 5>(st, a);
+            if (a.M <= 2) return gemv_part_merge<2, 1, 5>(st, a);
+            if (a.M <= 4) return gemv_part_merge<4, 1, 5>(st, a);
+            return gemv_part_merge<8, 1, 5>(st, a);
         }
         if (a.xmode == 4) {
             if (a.K > 2048 || a.K % 256 || a.n_splits < 1 || a.Q < 1 ||
                 a.n_splits > gemv_merge_max_splits(a.M, a.K) || a.split_len < 1)
                 return hipErrorInvalidValue;
             const bool wide = a.K > 1024;
-#define MTP_GEMV_MERGE(MR) return wide ? gemv_part_merge<MR, 2>(st, a, e) : gemv_part_merge<MR, 1>(st, a, e)
+#define MTP_GEMV_MERGE(MR) return wide ? gemv_part_merge<MR, 2>(st, a) : gemv_part_merge<MR, 1>(st, a)
             if (a.M <= 1) MTP_GEMV_MERGE(1);
             if (a.M <= 2) MTP_GEMV_MERGE(2);
             if (a.M <= 4) MTP_GEMV_MERGE(4);
@@ -973,11 +1006,11 @@ hipError_t gemv(hipStream_t st, const GemvArgs& a) {
 #undef MTP_GEMV_MERGE
         }
         if (a.xmode != 0) return hipErrorInvalidValue;
-        if (a.M <= 1) return gemv_part_rows<1>(st, a, e);
-        if (a.M <= 2) return gemv_part_rows<2>(st, a, e);
-        if (a.M <= 4) return gemv_part_rows<4>(st, a, e);
-        if (a.M <= 8) return gemv_part_rows<8>(st, a, e);
-        return gemv_part_rows<16>(st, a, e);
+        if (a.M <= 1) return gemv_part_rows<1>(st, a);
+        if (a.M <= 2) return gemv_part_rows<2>(st, a);
+        if (a.M <= 4) return gemv_part_rows<4>(st, a);
+        if (a.M <= 8) return gemv_part_rows<8>(st, a);
+        return gemv_part_rows<16>(st, a);
     }
     if (a.K > 2048 || a.K % 256 || (a.epi != EPI_LOGITS && a.N % 4)) return hipErrorInvalidValue;
     switch (a.epi) {
@@ -995,9 +1028,13 @@ hipError_t gemv(hipStream_t st, const GemvArgs& a) {
     case EPI_LOGITS: {
         // K x 1025 columns is a few tiles more than there are CUs: 8-wave
         // workgroups, two per CU, so the extra tiles do not form a second round
-        EpiLogitsB e{(float*)a.out, a.bias, a.ldo, a.N};
-        if (a.xmode == 3) return gemv_ln<3, EpiLogitsB, 8>(st, a, e);
-        return hipErrorInvalidValue;
+        if (a.xmode != 3) return hipErrorInvalidValue;
+        if (a.part_on && partials_bf16(a.part_rows)) {
+            EpiLogitsB<1> e{(float*)a.out, a.bias, a.ldo, a.N};
+            return gemv_ln<3, EpiLogitsB<1>, 8>(st, a, e);
+        }
+        EpiLogitsB<0> e{(float*)a.out, a.bias, a.ldo, a.N};
+        return gemv_ln<3, EpiLogitsB<0>, 8>(st, a, e);
     }
     }
     return hipErrorInvalidValue;

@@ -27,13 +27,18 @@
 
 namespace mtp {
 
-template <int MR, int XM, int KCH, int T>
+// PF: the form of the producer's split-K partials (store_partial4): 0 the
+// float32 form, 1 the bfloat16 one.
+template <int MR, int XM, int KCH, int T, int PF>
 struct LnRows {
     static constexpr bool RES = XM == 1 || XM == 3;                    // residual completed here
     static constexpr int RPT = (MR * KCH * 256 + T - 1) / T;           // rows per thread
+    static constexpr bool BFP = PF == 1;
+    static constexpr int NPV = RES ? (BFP ? 1 : 4) : 1;                // float32 ranges held
+    static constexpr int NPH = RES && BFP ? 3 : 1;                     // bfloat16 ranges held
     float4 (&hv)[RPT];                                                  // residual / embedding rows
-    float4 (&pv)[RES ? RPT : 1];                                        // the producer's split-K range 0 (float32)
-    uint2 (&ph)[RES ? 3 : 1][RES ? RPT : 1];                            //   and ranges 1..3 (bfloat16 bits)
+    float4 (&pv)[NPV][RES ? RPT : 1];                                   // the producer's partials: float32 ranges
+    uint2 (&ph)[NPH][RES ? RPT : 1];                                    //   and bfloat16 ranges 1..3 (raw bits)
     float4 (&zv)[XM == 3 ? RPT : 1];                                    // prefill hidden state (heads, first step)
     uint2 (&emb_e)[XM == 2 ? RPT : 1];                                  // first layer: embedding,
     uint2 (&emb_p)[XM == 2 ? RPT : 1];                                  //   position rows
@@ -92,10 +97,12 @@ struct LnRows {
                     const int row = (XM == 1) ? m : ((a.Q > 0) ? m * a.Q + a.Q - 1 : 0);
                     if constexpr (XM == 3) st_pl[j] = a.st[m].pend_len;
                     if (has_part) {
-                        pv[j] = load_partial0(a.part, a.ldh, row, cc);
+                        pv[0][j] = load_partial_f32(a.part, 0, a.part_rows, a.ldh, row, cc);
 #pragma unroll
-                        for (int s2 = 1; s2 < 4; ++s2)
-                            ph[s2 - 1][j] = load_partial_bits(a.part, s2, a.part_rows, a.ldh, row, cc);
+                        for (int s2 = 1; s2 < 4; ++s2) {
+                            if constexpr (BFP) ph[s2 - 1][j] = load_partial_bits(a.part, s2, a.part_rows, a.ldh, row, cc);
+                            else pv[s2 % NPV][j] = load_partial_f32(a.part, s2, a.part_rows, a.ldh, row, cc);
+                        }
                     } else {
                         hv[j] = *reinterpret_cast<const float4*>(a.h + (size_t)row * a.ldh + cc);
                     }
@@ -142,8 +149,17 @@ struct LnRows {
                 if (m < M && rg < RG) {
                     float4 x = hv[j];
                     if (has_part) {
-                        const float4 p0 = pv[j], p1 = bf16x4_to_f32(ph[0][j]), p2 = bf16x4_to_f32(ph[1][j]),
-                                     p3 = bf16x4_to_f32(ph[2][j]);
+                        const float4 p0 = pv[0][j];
+                        float4 p1, p2, p3;
+                        if constexpr (BFP) {
+                            p1 = bf16x4_to_f32(ph[0][j]);
+                            p2 = bf16x4_to_f32(ph[1][j]);
+                            p3 = bf16x4_to_f32(ph[NPH - 1][j]);
+                        } else {
+                            p1 = pv[1 % NPV][j];
+                            p2 = pv[2 % NPV][j];
+                            p3 = pv[3 % NPV][j];
+                        }
                         x.x = (p0.x + p1.x) + (p2.x + p3.x);
                         x.y = (p0.y + p1.y) + (p2.y + p3.y);
                         x.z = (p0.z + p1.z) + (p2.z + p3.z);
@@ -158,10 +174,11 @@ struct LnRows {
                             const int row = m * a.Q + pl - 1;
                             if (has_part) {
                                 float4 p4[4];
-                                p4[0] = load_partial0(a.part, a.ldh, row, cc);
+                                p4[0] = load_partial_f32(a.part, 0, a.part_rows, a.ldh, row, cc);
 #pragma unroll
                                 for (int s2 = 1; s2 < 4; ++s2)
-                                    p4[s2] = bf16x4_to_f32(load_partial_bits(a.part, s2, a.part_rows, a.ldh, row, cc));
+                                    p4[s2] = BFP ? bf16x4_to_f32(load_partial_bits(a.part, s2, a.part_rows, a.ldh, row, cc))
+                                                 : load_partial_f32(a.part, s2, a.part_rows, a.ldh, row, cc);
                                 x.x = (p4[0].x + p4[1].x) + (p4[2].x + p4[3].x);
                                 x.y = (p4[0].y + p4[1].y) + (p4[2].y + p4[3].y);
                                 x.z = (p4[0].z + p4[1].z) + (p4[2].z + p4[3].z);

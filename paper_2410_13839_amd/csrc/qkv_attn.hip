@@ -68,7 +68,7 @@ int split_len_for(int64_t max_ctx, int g) {
 
 template <int MR, int XM>
 __global__ __launch_bounds__(QA_T) void qkv_attn_kernel(GemvArgs a) {
-    using Rows = LnRows<MR, XM, 1, QA_T>;
+    using Rows = LnRows<MR, XM, 1, QA_T, (MR > 4 ? 1 : 0)>;          // M > 4 iff MR > 4
     // the first sequence's K / V group is loaded with the weights; at 8 rows
     // the LayerNorm registers leave no room for it (it is loaded in G)
     constexpr bool PRE = MR <= 4;
@@ -101,8 +101,8 @@ __global__ __launch_bounds__(QA_T) void qkv_attn_kernel(GemvArgs a) {
 
     // ---- A. activation-side loads, before any weight load (a CU returns
     //      load data in request order) ----
-    float4 ln_hv[Rows::RPT], ln_pv[Rows::RES ? Rows::RPT : 1], ln_zv[1];
-    uint2 ln_ph[Rows::RES ? 3 : 1][Rows::RES ? Rows::RPT : 1];
+    float4 ln_hv[Rows::RPT], ln_pv[Rows::NPV][Rows::RES ? Rows::RPT : 1], ln_zv[1];
+    uint2 ln_ph[Rows::NPH][Rows::RES ? Rows::RPT : 1];
     uint2 ln_ee[XM == 2 ? Rows::RPT : 1], ln_ep[XM == 2 ? Rows::RPT : 1];
     bool ln_eok[XM == 2 ? Rows::RPT : 1];
     int ln_pl[1];
@@ -375,6 +375,7 @@ hipError_t qkv_attn(hipStream_t st, const GemvArgs& a) {
     if (a.n_splits < QA_MING || a.n_splits > QA_MAXG || a.split_len < 16 || a.split_len > QA_MAXSL || a.split_len % 16)
         return hipErrorInvalidValue;
     if (!a.apart || !a.kvnew || !a.q || !a.st || a.kv.page_size != 16) return hipErrorInvalidValue;
+    if (a.xmode == 1 && a.part_on && partials_bf16(a.part_rows) != partials_bf16(a.M)) return hipErrorInvalidValue;
 #define MTP_QA(MR)                                                       \
     do {                                                                 \
         if (a.xmode == 1) return qa_go<MR, 1>(st, a);                    \
