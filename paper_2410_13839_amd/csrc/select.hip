@@ -167,23 +167,50 @@ __global__ __launch_bounds__(512) void select_fused_kernel(SelectArgs a) {
 #pragma unroll
         for (int j = 0; j < PER_LANE; ++j)
             if (lane + 64 * j == a.eos_id && mask_eos) v[j] = -INFINITY;
+        // Each lane keeps the best and the second best of its values not yet
+        // taken (order: value, then lower index); a round takes the wave's
+        // best of the lanes' bests, and the winning lane moves its second
+        // up.  A lane rescans its values only when it wins with no second
+        // held, so a round costs one wave reduction instead of a scan of
+        // every value.
         uint32_t taken = 0;
-        float top0 = 0.f;
-        int my_c = 0;
-        float my_e = 0.f;
-        for (int r = 0; r < k; ++r) {
-            float bv = -INFINITY;
-            int bi = INT_MAX;
+        float b1v, b2v;
+        int b1i, b2i;
+        bool have2;
+        auto rescan = [&]() {
+            b1v = b2v = -INFINITY;
+            b1i = b2i = INT_MAX;
 #pragma unroll
             for (int j = 0; j < PER_LANE; ++j) {
                 const int idx = lane + 64 * j;
                 const bool ok = (idx < V) & (((taken >> j) & 1u) == 0u);
-                const bool bt = ok & better(v[j], idx, bv, bi);
-                bv = bt ? v[j] : bv;
-                bi = bt ? idx : bi;
+                const bool n1 = ok & better(v[j], idx, b1v, b1i);
+                const bool n2 = ok & !n1 & better(v[j], idx, b2v, b2i);
+                b2v = n1 ? b1v : (n2 ? v[j] : b2v);
+                b2i = n1 ? b1i : (n2 ? idx : b2i);
+                b1v = n1 ? v[j] : b1v;
+                b1i = n1 ? idx : b1i;
             }
+            have2 = true;
+        };
+        rescan();
+        float top0 = 0.f;
+        int my_c = 0;
+        float my_e = 0.f;
+        for (int r = 0; r < k; ++r) {
+            float bv = b1v;
+            int bi = b1i;
             wave_argmax_uniform(bv, bi);
-            taken |= ((bi & 63) == lane) ? (1u << (bi >> 6)) : 0u;
+            if ((bi & 63) == lane) {
+                taken |= 1u << (bi >> 6);
+                if (have2) {
+                    b1v = b2v;
+                    b1i = b2i;
+                    have2 = false;
+                } else {
+                    rescan();
+                }
+            }
             if (r == 0) top0 = bv;
             const float e = bv - top0;
             my_c = (lane == r) ? bi : my_c;
